@@ -1,0 +1,331 @@
+"""CPU oracle for the Pici hot path -- TEST INFRASTRUCTURE ONLY.
+
+A thin ctypes wrapper over ``pici_oracle.c`` (plain single-threaded C, built
+with gcc).  Only ``tests/``, ``__graft_entry__.smoke()`` and the CPU-baseline
+leg of ``bench.py`` may import this package; the GPU library never does, and
+the two share no code.
+
+The C file cites the paper passage each function follows: Sec. III-B and
+Alg. 1 (format, compression), Sec. III-C (decompression), Sec. IV-B (where
+compression and reduction happen in the ring collectives), Sec. IV-C with
+Eq. 7 (the adaptive dense switch) and Sec. V-B (the 48-byte header).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+from dataclasses import dataclass
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "pici_oracle.c")
+_LIB = os.path.join(_HERE, "liboracle.so")
+
+F32, BF16 = 0, 1
+FMT_DENSE, FMT_PICI = 0, 1
+ARRAY, STREAM = 0, 1
+OK, ERR_INVALID_ARG, ERR_CAPACITY, ERR_UNSUPPORTED, ERR_CORRUPT_STREAM = 0, 1, 2, 3, 4
+NNZ_UNKNOWN = (1 << 64) - 1
+HEADER_BYTES = 48
+
+
+def build() -> str:
+    """Compile the oracle with gcc (-O2, IEEE arithmetic, no OpenMP)."""
+    tmp = _LIB + ".tmp"
+    subprocess.check_call(["gcc", "-O2", "-std=c99", "-Wall", "-Wextra", "-fPIC", "-shared",
+                           "-fno-fast-math", _SRC, "-o", tmp, "-lm"])
+    os.replace(tmp, _LIB)
+    return _LIB
+
+
+class _Policy(ctypes.Structure):
+    _fields_ = [("intra_thresh", ctypes.c_double), ("inter_thresh", ctypes.c_double),
+                ("ag_thresh", ctypes.c_double), ("ranks_per_node", ctypes.c_int),
+                ("adaptive", ctypes.c_int)]
+
+
+class _Trace(ctypes.Structure):
+    _fields_ = [("step", ctypes.c_int32), ("rank", ctypes.c_int32), ("fmt", ctypes.c_int32),
+                ("measured", ctypes.c_int32), ("bytes", ctypes.c_uint64), ("nnz", ctypes.c_uint64),
+                ("sigma", ctypes.c_double)]
+
+
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+            build()
+        L = ctypes.CDLL(_LIB)
+        u64, vp, i32 = ctypes.c_uint64, ctypes.c_void_p, ctypes.c_int
+        for name in ("orc_num_tiles", "orc_off_I", "orc_off_A"):
+            getattr(L, name).restype = u64
+            getattr(L, name).argtypes = [u64]
+        L.orc_pici_bytes.restype = u64
+        L.orc_pici_bytes.argtypes = [u64, i32, u64]
+        L.orc_dense_bytes.restype = u64
+        L.orc_dense_bytes.argtypes = [u64, i32]
+        L.orc_stream_bound.restype = u64
+        L.orc_stream_bound.argtypes = [u64, i32]
+        L.orc_compress.restype = i32
+        L.orc_compress.argtypes = [vp, u64, i32, vp, u64, ctypes.POINTER(u64)]
+        L.orc_encode_dense.restype = i32
+        L.orc_encode_dense.argtypes = [vp, u64, i32, vp, u64]
+        L.orc_validate.restype = i32
+        L.orc_validate.argtypes = [vp, u64, u64, i32]
+        L.orc_decompress.restype = i32
+        L.orc_decompress.argtypes = [vp, u64, vp, u64, i32]
+        L.orc_oplus.restype = ctypes.c_uint32
+        L.orc_oplus.argtypes = [ctypes.c_uint32, ctypes.c_uint32, i32]
+        L.orc_reduce.restype = i32
+        L.orc_reduce.argtypes = [i32, vp, u64, i32, vp, u64, i32, i32, vp, u64, u64, i32,
+                                 ctypes.POINTER(u64)]
+        L.orc_ring_reduce_scatter.restype = i32
+        L.orc_ring_reduce_scatter.argtypes = [ctypes.POINTER(vp), ctypes.POINTER(vp), i32, u64, i32,
+                                              ctypes.POINTER(_Policy), ctypes.POINTER(_Trace),
+                                              ctypes.POINTER(ctypes.c_double),
+                                              ctypes.POINTER(ctypes.c_double)]
+        L.orc_ring_all_gather.restype = i32
+        L.orc_ring_all_gather.argtypes = [ctypes.POINTER(vp), ctypes.POINTER(vp), i32, u64, i32,
+                                          ctypes.POINTER(_Trace)]
+        L.orc_ring_all_reduce.restype = i32
+        L.orc_ring_all_reduce.argtypes = [ctypes.POINTER(vp), ctypes.POINTER(vp), i32, u64, i32,
+                                          ctypes.POINTER(_Policy), ctypes.POINTER(_Trace)]
+        _lib = L
+    return _lib
+
+
+class OracleError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        super().__init__(f"{what}: oracle status {status}")
+        self.status = status
+
+
+def _check(st: int, what: str):
+    if st != OK:
+        raise OracleError(st, what)
+
+
+def dtype_code(arr: np.ndarray) -> int:
+    if arr.dtype == np.float32:
+        return F32
+    if arr.dtype == np.uint16:
+        return BF16
+    raise TypeError(f"unsupported dtype {arr.dtype}")
+
+
+def elem_size(dtype: int) -> int:
+    return 2 if dtype == BF16 else 4
+
+
+def _np_dtype(dtype: int):
+    return np.uint16 if dtype == BF16 else np.float32
+
+
+def _ptr(a: np.ndarray) -> int:
+    return a.ctypes.data
+
+
+# ---- sizes (Sec. III-B component sizes, Sec. V-B header) ----------------------
+
+def num_tiles(n: int) -> int:
+    return lib().orc_num_tiles(n)
+
+
+def off_I(n: int) -> int:
+    return lib().orc_off_I(n)
+
+
+def off_A(n: int) -> int:
+    return lib().orc_off_A(n)
+
+
+def pici_bytes(n: int, dtype: int, nnz: int) -> int:
+    return lib().orc_pici_bytes(n, dtype, nnz)
+
+
+def dense_bytes(n: int, dtype: int) -> int:
+    return lib().orc_dense_bytes(n, dtype)
+
+
+def stream_bound(n: int, dtype: int) -> int:
+    return lib().orc_stream_bound(n, dtype)
+
+
+# ---- codec ---------------------------------------------------------------------
+
+def compress(dense: np.ndarray) -> tuple[np.ndarray, int]:
+    """Pici message (uint8 array of exactly total_bytes) and nnz."""
+    dense = np.ascontiguousarray(dense)
+    dt = dtype_code(dense)
+    n = dense.size
+    cap = stream_bound(n, dt)
+    buf = np.zeros(max(cap, 1), dtype=np.uint8)
+    nnz = ctypes.c_uint64(0)
+    _check(lib().orc_compress(_ptr(dense), n, dt, _ptr(buf), cap, ctypes.byref(nnz)), "compress")
+    total = int(buf[40:48].view(np.uint64)[0])
+    return buf[:total].copy(), nnz.value
+
+
+def encode_dense(dense: np.ndarray) -> np.ndarray:
+    dense = np.ascontiguousarray(dense)
+    dt = dtype_code(dense)
+    cap = dense_bytes(dense.size, dt)
+    buf = np.zeros(cap, dtype=np.uint8)
+    _check(lib().orc_encode_dense(_ptr(dense), dense.size, dt, _ptr(buf), cap), "encode_dense")
+    return buf
+
+
+def validate(stream: np.ndarray, n: int, dtype: int) -> int:
+    stream = np.ascontiguousarray(stream, dtype=np.uint8)
+    return lib().orc_validate(_ptr(stream), stream.size, n, dtype)
+
+
+def decompress(stream: np.ndarray, n: int, dtype: int) -> np.ndarray:
+    stream = np.ascontiguousarray(stream, dtype=np.uint8)
+    out = np.empty(n, dtype=_np_dtype(dtype))
+    _check(lib().orc_decompress(_ptr(stream), stream.size, _ptr(out), n, dtype), "decompress")
+    return out
+
+
+def oplus(a_bits: int, b_bits: int, dtype: int) -> int:
+    """a (+) b on raw bit patterns (one element)."""
+    return lib().orc_oplus(a_bits, b_bits, dtype)
+
+
+@dataclass
+class Operand:
+    """A reduce operand: a dense array (kind ARRAY) or a message (kind STREAM)."""
+    kind: int
+    data: np.ndarray
+
+    @staticmethod
+    def array(a: np.ndarray) -> "Operand":
+        return Operand(ARRAY, np.ascontiguousarray(a))
+
+    @staticmethod
+    def stream(s: np.ndarray) -> "Operand":
+        return Operand(STREAM, np.ascontiguousarray(s, dtype=np.uint8))
+
+
+def reduce(a: Operand, b: Operand, n: int, dtype: int, out_kind: int = ARRAY,
+           out_fmt: int = FMT_DENSE):
+    """out = a (+) b.  Returns a dense array, or (message, nnz) for a message output."""
+    L = lib()
+    if out_kind == ARRAY:
+        out = np.empty(n, dtype=_np_dtype(dtype))
+        cap = 0
+    else:
+        cap = stream_bound(n, dtype)
+        out = np.zeros(cap, dtype=np.uint8)
+    nnz = ctypes.c_uint64(NNZ_UNKNOWN)
+    st = L.orc_reduce(a.kind, _ptr(a.data), a.data.nbytes, b.kind, _ptr(b.data), b.data.nbytes,
+                      out_kind, out_fmt, _ptr(out), cap, n, dtype, ctypes.byref(nnz))
+    _check(st, "reduce")
+    if out_kind == ARRAY:
+        return out
+    total = int(out[40:48].view(np.uint64)[0])
+    return out[:total].copy(), nnz.value
+
+
+# ---- ring collectives over virtual ranks (Sec. IV-A..C) --------------------------
+
+@dataclass
+class Policy:
+    intra_thresh: float = 0.6
+    inter_thresh: float = 0.5
+    ag_thresh: float = 0.1
+    ranks_per_node: int = 0      # 0: every link is intra-node
+    adaptive: int = 1            # 0 never dense, 1 threshold rule, 2 always dense
+
+    def c(self) -> _Policy:
+        return _Policy(self.intra_thresh, self.inter_thresh, self.ag_thresh,
+                       self.ranks_per_node, self.adaptive)
+
+
+@dataclass(frozen=True)
+class TraceEntry:
+    step: int
+    rank: int
+    fmt: int
+    measured: int
+    bytes: int
+    nnz: int
+    sigma: float
+
+
+def _trace_list(tr, count) -> list:
+    return [TraceEntry(tr[i].step, tr[i].rank, tr[i].fmt, tr[i].measured, tr[i].bytes, tr[i].nnz,
+                       tr[i].sigma) for i in range(count)]
+
+
+def _ptr_array(arrays):
+    return (ctypes.c_void_p * len(arrays))(*[a.ctypes.data for a in arrays])
+
+
+def ring_reduce_scatter(sends: list, policy: Policy | None = None):
+    """sends[r]: rank r's n-element input.  Returns (recv list of n/P arrays, trace)."""
+    policy = policy or Policy()
+    P = len(sends)
+    sends = [np.ascontiguousarray(s) for s in sends]
+    dt = dtype_code(sends[0])
+    n = sends[0].size
+    m = n // P
+    recvs = [np.empty(m, dtype=sends[0].dtype) for _ in range(P)]
+    ntr = P * (P - 1)
+    tr = (_Trace * max(ntr, 1))()
+    s0 = (ctypes.c_double * P)()
+    sp = (ctypes.c_double * P)()
+    pol = policy.c()
+    st = lib().orc_ring_reduce_scatter(_ptr_array(sends), _ptr_array(recvs), P, n, dt,
+                                       ctypes.byref(pol), tr, s0, sp)
+    _check(st, "ring_reduce_scatter")
+    return recvs, _trace_list(tr, ntr)
+
+
+def ring_all_gather(parts: list):
+    """parts[q]: rank q's n-element contribution.  Returns (P outputs of P*n, trace)."""
+    P = len(parts)
+    parts = [np.ascontiguousarray(p) for p in parts]
+    dt = dtype_code(parts[0])
+    n = parts[0].size
+    outs = [np.empty(P * n, dtype=parts[0].dtype) for _ in range(P)]
+    tr = (_Trace * P)()
+    _check(lib().orc_ring_all_gather(_ptr_array(parts), _ptr_array(outs), P, n, dt, tr),
+           "ring_all_gather")
+    return outs, _trace_list(tr, P)
+
+
+def ring_all_reduce(sends: list, policy: Policy | None = None):
+    """Returns (P outputs of n elements, trace of P*(P-1) + P entries)."""
+    policy = policy or Policy()
+    P = len(sends)
+    sends = [np.ascontiguousarray(s) for s in sends]
+    dt = dtype_code(sends[0])
+    n = sends[0].size
+    outs = [np.empty(n, dtype=sends[0].dtype) for _ in range(P)]
+    ntr = P * (P - 1) + P
+    tr = (_Trace * ntr)()
+    pol = policy.c()
+    _check(lib().orc_ring_all_reduce(_ptr_array(sends), _ptr_array(outs), P, n, dt,
+                                     ctypes.byref(pol), tr), "ring_all_reduce")
+    return outs, _trace_list(tr, ntr)
+
+
+def header(stream: np.ndarray) -> dict:
+    """The header fields of a message (little-endian, Sec. V-B layout)."""
+    s = np.ascontiguousarray(stream[:HEADER_BYTES], dtype=np.uint8)
+    return {
+        "magic": int(s[0:4].view(np.uint32)[0]),
+        "format": int(s[4:6].view(np.uint16)[0]),
+        "dtype": int(s[6:8].view(np.uint16)[0]),
+        "n": int(s[8:16].view(np.uint64)[0]),
+        "nnz": int(s[16:24].view(np.uint64)[0]),
+        "off_I": int(s[24:32].view(np.uint64)[0]),
+        "off_A": int(s[32:40].view(np.uint64)[0]),
+        "total_bytes": int(s[40:48].view(np.uint64)[0]),
+    }
