@@ -1,0 +1,294 @@
+"""Throughput of the Pici hot path on one MI355X.
+
+Workload: the codec sweep array -- 67,108,864 fp32 elements (256 MiB) with
+uniformly random nonzero positions and N(0,1) values -- at sparsity 99% (the
+headline), with 50 / 90 / 99.9% reported as a sweep.  Inputs are resident in
+HBM before timing; four copies of each operand rotate between steps so the
+256 MB Infinity Cache cannot serve a step's dense input.
+
+One step is one pass of the whole hot path over one batch:
+  compress(a)                     dense -> Pici, single pass (look-back scan)
+  send                            device-sized copy of the message
+  decompress(received)            Pici -> dense
+  reduce a (+) Pici(b) -> Pici    fused reduce-scatter step with fill-in
+  reduce Pici(a) (+) Pici(b) -> Pici
+  reduce a (+) Pici(b) -> dense   last reduce-scatter step
+  gather_expand of the two        all-gather receive side
+  adaptive switch                 read the nonzero count the fused step wrote,
+                                  Eq. 7 estimate vs the 0.6 threshold (one
+                                  stream synchronization per step)
+
+value = dense-equivalent bytes of the step (N*s per codec op, 2*N*s per
+reduce, P*N*s per gather) / step time.  Each kernel is also timed with HIP
+events on the stream it runs on; the roofline entry is the kernel with the
+largest time share, priced by its algorithmic bytes (dense bytes read or
+written plus message bytes read or written) against 8 TB/s.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+METRIC = "dense-equivalent GB/s (and % of HBM peak) for Pici compress/decompress/reduce"
+
+
+def _ensure_built():
+    lib = os.path.join(ROOT, "paper_2607_04676_amd", "libspccl.so")
+    if not os.path.exists(lib):
+        import __graft_entry__
+        __graft_entry__.build()
+
+
+def _log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+class Runner:
+    """Device buffers and the per-op launch closures for one sparsity."""
+
+    def __init__(self, S, torch, n, permille, copies):
+        import workloads as W
+        self.S, self.torch, self.n = S, torch, n
+        dt = S.SPCCL_F32
+        self.s = 4
+        t0 = time.time()
+        a = W.cfg2(permille, 0, n)
+        b = W.cfg2(permille, 1, n)
+        self.host_a, self.host_b = a, b
+        _log(f"generated sigma={permille / 1000} inputs in {time.time() - t0:.1f}s")
+        dev = "cuda"
+        ta, tb = torch.from_numpy(a).to(dev), torch.from_numpy(b).to(dev)
+        self.a = [ta] + [ta.clone() for _ in range(copies - 1)]
+        self.b = [tb] + [tb.clone() for _ in range(copies - 1)]
+        self.ws = S.alloc_workspace(n, dt, dev)
+        bound = S.spccl_stream_bound(n, dt)
+        mk = lambda: torch.empty(bound, dtype=torch.uint8, device=dev)
+        self.msg_b = [mk() for _ in range(copies)]
+        for k in range(copies):
+            S.spccl_compress(self.b[k], self.msg_b[k], self.ws)
+        self.msg_a, self.recv, self.red_p, self.red_pp = mk(), mk(), mk(), mk()
+        self.dense_out = torch.empty(n, dtype=torch.float32, device=dev)
+        self.red_d = torch.empty(n, dtype=torch.float32, device=dev)
+        self.gather_out = torch.empty(2 * n, dtype=torch.float32, device=dev)
+        torch.cuda.synchronize()
+        hb = S.spccl_read_header(self.msg_b[0])
+        self.nnz_b, self.bytes_b = hb["nnz"], hb["total_bytes"]
+        self.sigma0 = None
+
+    def ops(self, k):
+        """(name, launch, dense-equivalent bytes) of one step on copy k."""
+        S, n, s = self.S, self.n, self.s
+        a, b, mb, ws = self.a[k], self.b[k], self.msg_b[k], self.ws
+        F, P, D, A = S.SPCCL_F32, S.SPCCL_FMT_PICI, S.SPCCL_FMT_DENSE, S.SPCCL_STREAM
+        msg = lambda t, f=P: S.operand(t, A, f)
+        return [
+            ("compress", lambda: S.spccl_compress(a, self.msg_a, ws), n * s),
+            ("send", lambda: S.spccl_copy_message(self.msg_a, self.recv, ws), 0),
+            ("decompress", lambda: S.spccl_decompress(self.recv, self.dense_out, ws), n * s),
+            ("reduce_dense_pici_to_pici", lambda: S.spccl_reduce(S.operand(a), msg(mb), msg(self.red_p), n, F, ws),
+             2 * n * s),
+            ("reduce_pici_pici_to_pici", lambda: S.spccl_reduce(msg(self.msg_a), msg(mb), msg(self.red_pp), n, F, ws),
+             2 * n * s),
+            ("reduce_dense_pici_to_dense", lambda: S.spccl_reduce(S.operand(a), msg(mb), S.operand(self.red_d), n,
+                                                                  F, ws), 2 * n * s),
+            ("gather_expand", lambda: S.spccl_gather_expand([msg(self.recv), msg(self.red_p)], n, F,
+                                                            self.gather_out, ws), 2 * n * s),
+        ]
+
+    def decide(self):
+        """Adaptive switch for the next send (Sec. IV-C): measured sparsity of
+        the fused step's output against the extrapolation rule."""
+        h = self.S.spccl_read_header(self.red_p)
+        sigma = (self.n - h["nnz"]) / self.n
+        if self.sigma0 is None:
+            self.sigma0 = sigma
+        return sigma * self.sigma0 <= 0.6
+
+    def algorithmic_bytes(self):
+        """Bytes each kernel must move at minimum (reads + writes), per launch."""
+        S, n, s = self.S, self.n, self.s
+        torch = self.torch
+        torch.cuda.synchronize()
+        ba = S.spccl_read_header(self.msg_a)["total_bytes"]
+        bp = S.spccl_read_header(self.red_p)["total_bytes"]
+        bpp = S.spccl_read_header(self.red_pp)["total_bytes"]
+        bb = self.bytes_b
+        return {
+            "compress": n * s + ba,
+            "send": 2 * ba,
+            "decompress": ba + n * s,
+            "reduce_dense_pici_to_pici": n * s + bb + bp,
+            "reduce_pici_pici_to_pici": ba + bb + bpp,
+            "reduce_dense_pici_to_dense": n * s + bb + n * s,
+            "gather_expand": ba + bp + 2 * n * s,
+        }
+
+    def check_parity(self):
+        """Sampled parity against the oracle: the compressed message of a, whole."""
+        import oracle as O
+        exp, _ = O.compress(self.host_a)
+        got = self.msg_a[:exp.size].cpu().numpy()
+        return bool(np.array_equal(got, exp))
+
+
+def time_steps(R, steps, warmup, copies):
+    torch = R.torch
+    names = [op[0] for op in R.ops(0)]
+    for w in range(warmup):
+        for _, f, _ in R.ops(w % copies):
+            f()
+        R.decide()
+    torch.cuda.synchronize()
+    ev = {nm: [] for nm in names}
+    t0 = time.perf_counter()
+    start_all = torch.cuda.Event(enable_timing=True)
+    end_all = torch.cuda.Event(enable_timing=True)
+    start_all.record()
+    dense_eq = 0
+    for k in range(steps):
+        for nm, f, deq in R.ops(k % copies):
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record()
+            f()
+            e1.record()
+            ev[nm].append((e0, e1))
+            dense_eq += deq
+        R.decide()
+    end_all.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    total_ms = start_all.elapsed_time(end_all)
+    per = {nm: float(np.mean([a.elapsed_time(b) for a, b in ev[nm]])) for nm in names}
+    st = R.S.spccl_read_status(R.ws)
+    if st != 0:
+        raise RuntimeError(f"device status {st} after timing")
+    return total_ms, wall, per, dense_eq
+
+
+def cpu_baseline(permille, n_full, budget_s):
+    """The oracle (single thread, pinned to one core) on a bounded sample of
+    the same workload: the same op sequence on the first n_sample elements."""
+    import oracle as O
+    import workloads as W
+    try:
+        os.sched_setaffinity(0, {sorted(os.sched_getaffinity(0))[0]})
+    except (AttributeError, OSError):
+        pass
+    n = n_full // 16
+    a = W.cfg2(permille, 0, n_full)[:n].copy()
+    b = W.cfg2(permille, 1, n_full)[:n].copy()
+    s = 4
+    mb, _ = O.compress(b)
+    done_bytes, t_total, reps = 0, 0.0, 0
+    while t_total < budget_s and reps < 50:
+        t0 = time.perf_counter()
+        ma, _ = O.compress(a)
+        back = O.decompress(ma, n, O.F32)
+        O.reduce(O.Operand.array(a), O.Operand.stream(mb), n, O.F32, O.STREAM, O.FMT_PICI)
+        O.reduce(O.Operand.stream(ma), O.Operand.stream(mb), n, O.F32, O.STREAM, O.FMT_PICI)
+        O.reduce(O.Operand.array(a), O.Operand.stream(mb), n, O.F32)
+        O.decompress(ma, n, O.F32)
+        O.decompress(mb, n, O.F32)
+        t_total += time.perf_counter() - t0
+        done_bytes += (2 + 3 * 2 + 2) * n * s
+        reps += 1
+        assert np.array_equal(back.view(np.uint32), a.view(np.uint32))
+    cpu_model = "unknown"
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                cpu_model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    return {"value": done_bytes / t_total / 1e9, "unit": "GB/s", "cores": 1, "kind": "oracle",
+            "sample": f"first {n} of {n_full} elements (1/16) at sigma={permille / 1000}, the step's op sequence "
+                      f"x{reps} in {t_total:.1f} s, single thread pinned to one core; host cpu: {cpu_model}, "
+                      f"{os.cpu_count()} logical cpus"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=30)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--n", type=int, default=1 << 26)
+    ap.add_argument("--permille", type=int, default=990)
+    ap.add_argument("--sweep", default="500,900,999", help="other sparsities (permille) to report; '' for none")
+    ap.add_argument("--copies", type=int, default=4)
+    ap.add_argument("--cpu-budget", type=float, default=10.0)
+    ap.add_argument("--no-cpu", action="store_true")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (this build emulates P ranks on one device); "
+              f"--gpus {args.gpus} is not supported", file=sys.stderr)
+        sys.exit(2)
+
+    _ensure_built()
+    import torch
+    import paper_2607_04676_amd as S
+
+    torch.cuda.init()
+    _log(f"device: {torch.cuda.get_device_name(0)}")
+    R = Runner(S, torch, args.n, args.permille, args.copies)
+    total_ms, wall, per, dense_eq = time_steps(R, args.steps, args.warmup, args.copies)
+    alg = R.algorithmic_bytes()
+    parity = R.check_parity()
+    ms_per_step = total_ms / args.steps
+    value = dense_eq / (total_ms / 1e3) / 1e9
+    kernels = {}
+    for nm, ms in per.items():
+        gbs = alg[nm] / (ms / 1e3) / 1e9
+        kernels[nm] = {"ms": round(ms, 5), "algorithmic_bytes": alg[nm], "achieved_GBs": round(gbs, 1),
+                       "frac_of_hbm_peak": round(gbs / HBM_PEAK_GBS, 4)}
+    dom = max(per, key=lambda k: per[k])
+    dgbs = alg[dom] / (per[dom] / 1e3) / 1e9
+    roof = {"bound": "hbm", "kernel": dom, "achieved": round(dgbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": round(dgbs / HBM_PEAK_GBS, 4), "traffic": None,
+            "algorithmic_bytes_per_launch": alg[dom], "avg_launch_ms": round(per[dom], 5)}
+    sweep = {}
+    del R
+    torch.cuda.empty_cache()
+    for pm in [int(x) for x in args.sweep.split(",") if x.strip()]:
+        Rs = Runner(S, torch, args.n, pm, args.copies)
+        t_ms, _, p_s, deq = time_steps(Rs, max(5, args.steps // 3), 2, args.copies)
+        a_s = Rs.algorithmic_bytes()
+        sweep[str(pm / 1000)] = {
+            "dense_equiv_GBs": round(deq / (t_ms / 1e3) / 1e9, 1),
+            "kernels": {nm: {"ms": round(ms, 5), "frac_of_hbm_peak": round(a_s[nm] / (ms / 1e3) / 1e9 / HBM_PEAK_GBS,
+                                                                           4)} for nm, ms in p_s.items()},
+            "parity_compress": Rs.check_parity(),
+        }
+        del Rs
+        torch.cuda.empty_cache()
+    cpu = None
+    if not args.no_cpu:
+        _log("timing the CPU oracle")
+        cpu = cpu_baseline(args.permille, args.n, args.cpu_budget)
+    out = {
+        "metric": METRIC, "value": round(value, 1), "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": f"codec sweep array: {args.n:,} fp32 elements ({args.n * 4 >> 20} MiB), "
+                               f"sigma={args.permille / 1000}, uniform random nonzero positions, N(0,1) values; "
+                               "step = compress, send, decompress, 3 reduce variants, gather-expand, adaptive switch",
+                   "n": args.n, "sigma": args.permille / 1000, "parallelism": "1 GPU (virtual ranks)"},
+        "roofline": roof, "cpu_baseline": cpu, "kernels": kernels, "sweep": sweep,
+        "parity_compress_vs_oracle": parity, "wall_s_timed": round(wall, 3),
+    }
+    print(json.dumps(out))
+
+
+if __name__ == "__main__":
+    main()

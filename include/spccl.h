@@ -1,0 +1,243 @@
+/*
+ * spccl.h -- C ABI of the MI355X (gfx950) Pici hot path of SpCCL
+ * (arXiv 2607.04676): dense <-> Pici codec, elementwise reduction with
+ * fill-in, gather-expand, and ring collectives over P virtual ranks held in
+ * one GPU's memory.
+ *
+ * Conventions for every entry point:
+ *  - Pointers are device pointers unless marked "host".  Device pointers must
+ *    be 16-byte aligned.  The caller owns every buffer; the library allocates
+ *    and frees nothing.
+ *  - `stream` is a hipStream_t handle (NULL = the default stream).  Calls are
+ *    asynchronous on it, except spccl_read_header, spccl_read_status and the
+ *    spccl_vr_* collectives, which synchronize it.
+ *  - Errors found on the host (bad argument, capacity, size, dtype) are
+ *    returned before anything is launched.  Data errors found on the device
+ *    (a corrupt input message) set a sticky status word in the workspace `ws`
+ *    (read it with spccl_read_status).  A message whose header fails its
+ *    checks is not read and the call writes no output; a tile whose index
+ *    entries disagree with its bit vector is treated as empty.  After any
+ *    device error, re-initialise the workspace before reusing it.
+ *  - Element types: SPCCL_F32 (IEEE binary32) and SPCCL_BF16 (bfloat16),
+ *    handled as raw bit patterns.  n < 2^32 per message (I is 32-bit).
+ *  - An element is nonzero ("present") iff its bit pattern is not all zero,
+ *    so -0.0 is kept and decompress(compress(x)) == x bit for bit.
+ *  - NaN values are outside the contract of the reductions.
+ */
+#ifndef SPCCL_H
+#define SPCCL_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    SPCCL_OK = 0,
+    SPCCL_ERR_INVALID_ARG = 1,     /* null/unaligned pointer, bad enum, n % P != 0, ... */
+    SPCCL_ERR_CAPACITY = 2,        /* an output buffer is smaller than required */
+    SPCCL_ERR_UNSUPPORTED = 3,     /* dtype or size outside the supported range */
+    SPCCL_ERR_CORRUPT_STREAM = 4,  /* a message failed its header / index checks */
+    SPCCL_ERR_WORKSPACE = 5,       /* workspace too small or not initialised */
+    SPCCL_ERR_HIP = 6,             /* a HIP runtime call or kernel launch failed */
+    SPCCL_ERR_TIMEOUT = 7          /* a device-side wait exceeded its spin limit */
+} spccl_status_t;
+
+typedef enum { SPCCL_F32 = 0, SPCCL_BF16 = 1 } spccl_dtype_t;
+
+/* Message formats (Sec. V-B: each message carries its format in its header). */
+typedef enum { SPCCL_FMT_DENSE = 0, SPCCL_FMT_PICI = 1 } spccl_format_t;
+
+/* A reduce operand is either a raw dense array of n elements (ARRAY) or a
+ * header-prefixed message (STREAM). */
+typedef enum { SPCCL_ARRAY = 0, SPCCL_STREAM = 1 } spccl_kind_t;
+
+typedef struct {
+    int32_t kind;     /* spccl_kind_t */
+    int32_t fmt;      /* spccl_format_t of a STREAM: for an input, the format the
+                         caller expects (checked against the header on the device);
+                         for an output, the format to produce.  Ignored for ARRAY. */
+    void* ptr;        /* device pointer, 16-byte aligned */
+    uint64_t bytes;   /* capacity of the buffer in bytes */
+} spccl_operand_t;
+
+/* The 48-byte message header (Sec. V-B names its contents: format, size and
+ * component offsets; the layout is this library's).  Little-endian.
+ *   PICI:  B (u64[64*T]) at offset 48, I (u32[T+1]) at off_I = 48 + 512*T,
+ *          zero pad to 16 bytes, A (nnz values) at off_A,
+ *          total_bytes = off_A + nnz * elem_size.
+ *   DENSE: the n values at off_A = 48; off_I = 0; nnz = UINT64_MAX
+ *          ("not computed"); total_bytes = 48 + n * elem_size. */
+typedef struct {
+    uint32_t magic;        /* 0x49434950: the bytes "PICI" */
+    uint16_t format;       /* spccl_format_t */
+    uint16_t dtype;        /* spccl_dtype_t */
+    uint64_t n;            /* elements represented */
+    uint64_t nnz;          /* nonzeros (PICI) or UINT64_MAX (DENSE) */
+    uint64_t off_I;
+    uint64_t off_A;
+    uint64_t total_bytes;  /* bytes of the whole message, header included */
+} spccl_header_t;
+
+#define SPCCL_MAGIC 0x49434950u
+#define SPCCL_HEADER_BYTES 48u
+#define SPCCL_NNZ_UNKNOWN UINT64_MAX
+
+/* ---- sizes --------------------------------------------------------------- */
+
+/* T = ceil(n / 4096): the 64x64 virtual tiles covering n elements (Sec. III-B). */
+uint64_t spccl_num_tiles(uint64_t n);
+
+/* Exact byte size of a Pici message with nnz nonzeros: the paper's component
+ * sizes (B 512*T, I 4*(T+1), A nnz*s; Sec. III-B) plus header and pad. */
+uint64_t spccl_pici_bytes(uint64_t n, int32_t dtype, uint64_t nnz);
+
+/* Worst-case message size for n elements (every element present).  Every
+ * message output must have at least this capacity, because the size is only
+ * known once the kernel has counted (Sec. V-B enlarges FIFOs likewise).
+ * Returns 0 for an unsupported dtype. */
+uint64_t spccl_stream_bound(uint64_t n, int32_t dtype);
+
+/* Workspace for messages of up to n elements: control words (sticky status,
+ * partition ticket, epoch) and one look-back status word per partition of
+ * the single-pass scan.  Must be zero-filled once before first use (or
+ * cleared with spccl_workspace_init); the library keeps it consistent after
+ * that.  One workspace must not be used by two calls in flight at once. */
+uint64_t spccl_workspace_bytes(uint64_t n, int32_t dtype);
+
+/* Zero-fill a workspace with a fill kernel on `stream` (no memset nodes). */
+spccl_status_t spccl_workspace_init(void* ws, uint64_t ws_bytes, void* stream);
+
+/* ---- codec (Sec. III-B format, Alg. 1 compression, Sec. III-C) ----------- */
+
+/* Compress dense[0..n) into a Pici message at `out` (capacity out_bytes >=
+ * spccl_stream_bound(n, dtype)).  Single pass over the input: bit vector B,
+ * tile prefix sums I (decoupled look-back across partitions) and compacted
+ * values A, ordered tile -> column -> row.  nnz is in the written header. */
+spccl_status_t spccl_compress(const void* dense, uint64_t n, int32_t dtype,
+                              void* out, uint64_t out_bytes,
+                              void* ws, uint64_t ws_bytes, void* stream);
+
+/* Expand a message (PICI or DENSE, read from its header) of capacity
+ * in_bytes into all n elements of `dense` (absent elements become +0.0). */
+spccl_status_t spccl_decompress(const void* in, uint64_t in_bytes,
+                                void* dense, uint64_t n, int32_t dtype,
+                                void* ws, uint64_t ws_bytes, void* stream);
+
+/* Wrap dense[0..n) as a DENSE message (header + the n values) at `out`
+ * (capacity out_bytes >= 48 + n * elem_size).  Dense sends carry the same
+ * header as sparse ones (Sec. V-B); nnz is recorded as "not computed". */
+spccl_status_t spccl_encode_dense(const void* dense, uint64_t n, int32_t dtype,
+                                  void* out, uint64_t out_bytes, void* stream);
+
+/* ---- reduction with fill-in (Sec. IV-B) --------------------------------- */
+
+/* out = a (+) b elementwise over n elements.  An absent element (all-zero
+ * bits) is the identity; two present elements are added (fp32: IEEE add,
+ * nearest-even; bf16: fp32 add rounded once to bfloat16, nearest-even).  A
+ * result is present iff its bits are nonzero, so an exact cancellation drops
+ * the element from a Pici output.  In a ring step `a` is the received
+ * (earlier) contribution; the operation is commutative bit for bit.
+ * Supported operand kinds: a, b each ARRAY, STREAM/PICI or STREAM/DENSE;
+ * out ARRAY, STREAM/PICI or STREAM/DENSE.  out may alias a or b only when
+ * all three are ARRAYs (in-place accumulation).  A STREAM output needs
+ * capacity >= spccl_stream_bound(n, dtype). */
+spccl_status_t spccl_reduce(spccl_operand_t a, spccl_operand_t b, spccl_operand_t out,
+                            uint64_t n, int32_t dtype,
+                            void* ws, uint64_t ws_bytes, void* stream);
+
+/* ---- all-gather receive side (Sec. IV-B) --------------------------------- */
+
+/* dense_out[q*n_per_part .. (q+1)*n_per_part) = expand(parts[q]) for q < P.
+ * parts (host array of P operands) are ARRAYs or STREAMs of either format
+ * (a STREAM's format is read from its header; its fmt field is ignored). */
+spccl_status_t spccl_gather_expand(const spccl_operand_t* parts, int32_t P,
+                                   uint64_t n_per_part, int32_t dtype,
+                                   void* dense_out, uint64_t out_bytes,
+                                   void* ws, uint64_t ws_bytes, void* stream);
+
+/* ---- message transport and inspection ------------------------------------ */
+
+/* The virtual-rank "send": copy header.total_bytes bytes of the message at
+ * src (capacity src_bytes) to dst (capacity dst_bytes).  The size is read on
+ * the device, so no host synchronisation is needed.  A message that does not
+ * fit sets SPCCL_ERR_CORRUPT_STREAM in ws and copies nothing. */
+spccl_status_t spccl_copy_message(const void* src, uint64_t src_bytes, void* dst, uint64_t dst_bytes,
+                                  void* ws, uint64_t ws_bytes, void* stream);
+
+/* Copy the 48-byte header of a device message to host_out (synchronizes). */
+spccl_status_t spccl_read_header(const void* msg, spccl_header_t* host_out, void* stream);
+
+/* Synchronize `stream`, return the sticky device status in ws and, if clear
+ * != 0, reset it to SPCCL_OK. */
+spccl_status_t spccl_read_status(void* ws, int32_t clear, void* stream);
+
+const char* spccl_status_string(spccl_status_t s);
+
+/* ---- ring collectives over P virtual ranks on one GPU (Sec. IV) ----------- */
+
+/* Adaptive format policy (Sec. IV-C).  Defaults for Pici with fp32:
+ * intra 0.6, inter 0.5, ag 0.1. */
+typedef struct {
+    double intra_thresh;     /* dense iff sparsity <= this on an intra-node link */
+    double inter_thresh;     /* ... on an inter-node link */
+    double ag_thresh;        /* all-reduce: gather densely iff estimate <= this */
+    int32_t ranks_per_node;  /* link r -> r+1 is inter-node iff (r+1) % ranks_per_node == 0
+                                and ranks_per_node < P; 0 = all links intra-node */
+    int32_t adaptive;        /* 0: always Pici; 1: threshold rule; 2: always dense */
+} spccl_policy_t;
+
+/* One send decision of one rank (host array; see spccl_vr_*). */
+typedef struct {
+    int32_t step, rank;
+    int32_t fmt;             /* format of the message sent at this step */
+    int32_t measured;        /* 1 if this step counted the nonzeros */
+    uint64_t bytes;          /* message bytes, header included */
+    uint64_t nnz;            /* counted nonzeros, or SPCCL_NNZ_UNKNOWN */
+    double sigma;            /* tracked sparsity after this step (Eq. 7 estimate
+                                or measurement); for an all-gather entry of an
+                                all-reduce, the transition estimate */
+} spccl_trace_t;
+
+/* Scratch bytes the collectives need: P ranks exchanging messages of up to
+ * msg_elems elements (n / P for reduce-scatter and all-reduce, n for
+ * all-gather).  Holds one workspace and 3*P message buffers of
+ * spccl_stream_bound(msg_elems) bytes. */
+uint64_t spccl_vr_scratch_bytes(int32_t P, uint64_t msg_elems, int32_t dtype);
+
+/* Ring reduce-scatter (Sec. IV-B).  send: host array of P device pointers to
+ * n-element inputs; recv: host array of P device pointers, rank r receives
+ * the n/P-element chunk r: (((X_{r+1} (+) X_{r+2}) (+) ...) (+) X_{r-1}) (+) X_r.
+ * At step s rank r sends chunk (r-s-1) mod P to rank r+1; step 0 compresses
+ * and measures sigma0; later steps extrapolate sigma_prev * sigma0 (Eq. 7)
+ * and send dense iff the estimate <= the link's threshold.  trace (host,
+ * optional) gets P*(P-1) entries, step-major.  n % P == 0. */
+spccl_status_t spccl_vr_reduce_scatter(void* const* send, void* const* recv, int32_t P, uint64_t n,
+                                       int32_t dtype, const spccl_policy_t* policy,
+                                       void* scratch, uint64_t scratch_bytes,
+                                       spccl_trace_t* trace, void* stream);
+
+/* Ring all-gather (Sec. IV-B): each rank compresses its n-element part once,
+ * the message travels the ring unchanged, and every rank expands all P
+ * parts into recv[r] (P*n elements).  Never switches to dense.  trace gets P
+ * entries. */
+spccl_status_t spccl_vr_all_gather(void* const* send, void* const* recv, int32_t P, uint64_t n,
+                                   int32_t dtype, void* scratch, uint64_t scratch_bytes,
+                                   spccl_trace_t* trace, void* stream);
+
+/* Ring all-reduce = reduce-scatter, then all-gather of the reduced chunks;
+ * at the transition each rank gathers densely iff sigma_prev * sigma0 <=
+ * ag_thresh (phase-aware switch, Sec. IV-C).  recv[r] gets n elements.
+ * trace gets P*(P-1) + P entries. */
+spccl_status_t spccl_vr_all_reduce(void* const* send, void* const* recv, int32_t P, uint64_t n,
+                                   int32_t dtype, const spccl_policy_t* policy,
+                                   void* scratch, uint64_t scratch_bytes,
+                                   spccl_trace_t* trace, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SPCCL_H */

@@ -1,0 +1,280 @@
+// C ABI entry points: host-side argument checks, operand decoding and kernel
+// dispatch.  Nothing here allocates device memory or synchronizes, except
+// spccl_read_header / spccl_read_status.
+#include <hip/hip_runtime_api.h>
+#include <stdint.h>
+#include <string.h>
+
+#include "spccl_internal.h"
+#include "../../include/spccl.h"
+
+namespace spccl {
+spccl_status_t launch_to_pici_dt(int dtype, int sa, int sb, const PiciSinkArgs& g, hipStream_t st);
+spccl_status_t launch_to_dense_dt(int dtype, int sa, int sb, const DenseSinkArgs& g, hipStream_t st);
+spccl_status_t launch_gather_dt(int dtype, const GatherArgs& g, int P, hipStream_t st);
+spccl_status_t launch_dense_dense_dt(int dtype, const uint8_t* a_hdr, const uint8_t* a, uint64_t a_cap,
+                                     const uint8_t* b_hdr, const uint8_t* b, uint64_t b_cap, uint8_t* out_hdr,
+                                     uint8_t* out, uint64_t n, WsCtrl* ctrl, hipStream_t st);
+spccl_status_t launch_copy_message(const uint8_t* src, uint64_t src_cap, uint8_t* dst, uint64_t dst_cap,
+                                   WsCtrl* ctrl, hipStream_t st);
+spccl_status_t launch_fill_zero(void* p, uint64_t bytes, hipStream_t st);
+spccl_status_t launch_encode_dense_dt(int dtype, const uint8_t* src, uint8_t* out, uint64_t n, hipStream_t st);
+}  // namespace spccl
+
+using namespace spccl;
+
+namespace {
+
+inline bool dtype_ok(int32_t dt) { return dt == kF32 || dt == kBF16; }
+inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+inline hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s); }
+inline bool overlaps(const void* a, uint64_t an, const void* b, uint64_t bn) {
+    const uintptr_t x = reinterpret_cast<uintptr_t>(a), y = reinterpret_cast<uintptr_t>(b);
+    return an && bn && x < y + bn && y < x + an;
+}
+
+spccl_status_t check_ws(void* ws, uint64_t ws_bytes, uint64_t need) {
+    if (!ws || !aligned16(ws)) return SPCCL_ERR_INVALID_ARG;
+    if (ws_bytes < need) return SPCCL_ERR_WORKSPACE;
+    return SPCCL_OK;
+}
+
+// An input operand as a kernel source.
+struct Src {
+    int kind;          // SRC_DENSE or SRC_PICI
+    DevOperand dev;
+};
+
+spccl_status_t decode_input(const spccl_operand_t& o, uint64_t n, int32_t dt, Src* out) {
+    if (!o.ptr || !aligned16(o.ptr)) return (n == 0 && o.kind == SPCCL_ARRAY && !o.ptr) ? SPCCL_OK
+                                                                                       : SPCCL_ERR_INVALID_ARG;
+    const uint8_t* p = static_cast<const uint8_t*>(o.ptr);
+    if (o.kind == SPCCL_ARRAY) {
+        if (o.bytes < n * elem_bytes(dt)) return SPCCL_ERR_CAPACITY;
+        *out = Src{SRC_DENSE, DevOperand{nullptr, p, o.bytes}};
+        return SPCCL_OK;
+    }
+    if (o.kind != SPCCL_STREAM) return SPCCL_ERR_INVALID_ARG;
+    if (o.bytes < kHeaderBytes) return SPCCL_ERR_CAPACITY;
+    if (o.fmt == SPCCL_FMT_DENSE) *out = Src{SRC_DENSE, DevOperand{p, p + kHeaderBytes, o.bytes}};
+    else if (o.fmt == SPCCL_FMT_PICI) *out = Src{SRC_PICI, DevOperand{p, p, o.bytes}};
+    else return SPCCL_ERR_INVALID_ARG;
+    return SPCCL_OK;
+}
+
+uint64_t operand_extent(const spccl_operand_t& o) { return o.bytes; }
+
+}  // namespace
+
+extern "C" {
+
+uint64_t spccl_num_tiles(uint64_t n) { return num_tiles(n); }
+
+uint64_t spccl_pici_bytes(uint64_t n, int32_t dtype, uint64_t nnz) {
+    return dtype_ok(dtype) ? pici_bytes(n, dtype, nnz) : 0;
+}
+
+uint64_t spccl_stream_bound(uint64_t n, int32_t dtype) {
+    if (!dtype_ok(dtype)) return 0;
+    const uint64_t p = pici_bytes(n, dtype, n), d = dense_msg_bytes(n, dtype);
+    return p > d ? p : d;
+}
+
+uint64_t spccl_workspace_bytes(uint64_t n, int32_t dtype) {
+    (void)dtype;
+    return kWsFlagsOffset + 8ull * num_parts(n);
+}
+
+spccl_status_t spccl_workspace_init(void* ws, uint64_t ws_bytes, void* stream) {
+    if (!ws || !aligned16(ws) || ws_bytes < kWsFlagsOffset) return SPCCL_ERR_INVALID_ARG;
+    return launch_fill_zero(ws, ws_bytes, as_stream(stream));
+}
+
+spccl_status_t spccl_compress(const void* dense, uint64_t n, int32_t dtype, void* out, uint64_t out_bytes,
+                              void* ws, uint64_t ws_bytes, void* stream) {
+    if (!dtype_ok(dtype)) return SPCCL_ERR_UNSUPPORTED;
+    if (n >= (1ull << 32)) return SPCCL_ERR_UNSUPPORTED;
+    if ((n && (!dense || !aligned16(dense))) || !out || !aligned16(out)) return SPCCL_ERR_INVALID_ARG;
+    if (out_bytes < spccl_stream_bound(n, dtype)) return SPCCL_ERR_CAPACITY;
+    if (overlaps(dense, n * elem_bytes(dtype), out, out_bytes)) return SPCCL_ERR_INVALID_ARG;
+    spccl_status_t st = check_ws(ws, ws_bytes, spccl_workspace_bytes(n, dtype));
+    if (st != SPCCL_OK) return st;
+    PiciSinkArgs g{};
+    g.a = DevOperand{nullptr, static_cast<const uint8_t*>(dense), n * elem_bytes(dtype)};
+    g.out = static_cast<uint8_t*>(out);
+    g.n = n;
+    g.T = num_tiles(n);
+    g.nparts = (uint32_t)num_parts(n);
+    g.ctrl = static_cast<WsCtrl*>(ws);
+    g.flags = reinterpret_cast<uint64_t*>(static_cast<uint8_t*>(ws) + kWsFlagsOffset);
+    return launch_to_pici_dt(dtype, SRC_DENSE, SRC_NONE, g, as_stream(stream));
+}
+
+spccl_status_t spccl_encode_dense(const void* dense, uint64_t n, int32_t dtype, void* out, uint64_t out_bytes,
+                                  void* stream) {
+    if (!dtype_ok(dtype)) return SPCCL_ERR_UNSUPPORTED;
+    if (n >= (1ull << 32)) return SPCCL_ERR_UNSUPPORTED;
+    if ((n && (!dense || !aligned16(dense))) || !out || !aligned16(out)) return SPCCL_ERR_INVALID_ARG;
+    if (out_bytes < dense_msg_bytes(n, dtype)) return SPCCL_ERR_CAPACITY;
+    if (overlaps(dense, n * elem_bytes(dtype), out, out_bytes)) return SPCCL_ERR_INVALID_ARG;
+    return launch_encode_dense_dt(dtype, static_cast<const uint8_t*>(dense), static_cast<uint8_t*>(out), n,
+                                  as_stream(stream));
+}
+
+spccl_status_t spccl_gather_expand(const spccl_operand_t* parts, int32_t P, uint64_t n_per_part, int32_t dtype,
+                                   void* dense_out, uint64_t out_bytes, void* ws, uint64_t ws_bytes,
+                                   void* stream) {
+    if (!dtype_ok(dtype)) return SPCCL_ERR_UNSUPPORTED;
+    if (n_per_part >= (1ull << 32)) return SPCCL_ERR_UNSUPPORTED;
+    if (!parts || P < 0) return SPCCL_ERR_INVALID_ARG;
+    if (P == 0) return SPCCL_OK;
+    const uint64_t s = elem_bytes(dtype);
+    if (!dense_out || !aligned16(dense_out)) return SPCCL_ERR_INVALID_ARG;
+    if (out_bytes < (uint64_t)P * n_per_part * s) return SPCCL_ERR_CAPACITY;
+    spccl_status_t st = check_ws(ws, ws_bytes, kWsFlagsOffset);
+    if (st != SPCCL_OK) return st;
+    if (n_per_part == 0) return SPCCL_OK;
+    GatherArgs g{};
+    g.n = n_per_part;
+    g.T = num_tiles(n_per_part);
+    g.ctrl = static_cast<WsCtrl*>(ws);
+    for (int32_t q0 = 0; q0 < P; q0 += kMaxGatherParts) {
+        const int cnt = (P - q0) < kMaxGatherParts ? (P - q0) : kMaxGatherParts;
+        for (int k = 0; k < cnt; k++) {
+            const spccl_operand_t& o = parts[q0 + k];
+            if (!o.ptr || !aligned16(o.ptr)) return SPCCL_ERR_INVALID_ARG;
+            const uint8_t* p = static_cast<const uint8_t*>(o.ptr);
+            if (o.kind == SPCCL_ARRAY) {
+                if (o.bytes < n_per_part * s) return SPCCL_ERR_CAPACITY;
+                g.part[k] = DevOperand{nullptr, p, o.bytes};
+            } else if (o.kind == SPCCL_STREAM) {
+                if (o.bytes < kHeaderBytes) return SPCCL_ERR_CAPACITY;
+                g.part[k] = DevOperand{p, p, o.bytes};
+            } else {
+                return SPCCL_ERR_INVALID_ARG;
+            }
+            if (overlaps(o.ptr, o.bytes, dense_out, out_bytes)) return SPCCL_ERR_INVALID_ARG;
+        }
+        g.out = static_cast<uint8_t*>(dense_out) + (uint64_t)q0 * n_per_part * s;
+        st = launch_gather_dt(dtype, g, cnt, as_stream(stream));
+        if (st != SPCCL_OK) return st;
+    }
+    return SPCCL_OK;
+}
+
+spccl_status_t spccl_decompress(const void* in, uint64_t in_bytes, void* dense, uint64_t n, int32_t dtype,
+                                void* ws, uint64_t ws_bytes, void* stream) {
+    spccl_operand_t part{SPCCL_STREAM, SPCCL_FMT_PICI, const_cast<void*>(in), in_bytes};
+    return spccl_gather_expand(&part, 1, n, dtype, dense, n * (dtype == kBF16 ? 2u : 4u), ws, ws_bytes, stream);
+}
+
+spccl_status_t spccl_reduce(spccl_operand_t a, spccl_operand_t b, spccl_operand_t out, uint64_t n, int32_t dtype,
+                            void* ws, uint64_t ws_bytes, void* stream) {
+    if (!dtype_ok(dtype)) return SPCCL_ERR_UNSUPPORTED;
+    if (n >= (1ull << 32)) return SPCCL_ERR_UNSUPPORTED;
+    const uint64_t s = elem_bytes(dtype);
+    Src sa{}, sb{};
+    spccl_status_t st = decode_input(a, n, dtype, &sa);
+    if (st != SPCCL_OK) return st;
+    st = decode_input(b, n, dtype, &sb);
+    if (st != SPCCL_OK) return st;
+    if (!out.ptr || !aligned16(out.ptr)) return SPCCL_ERR_INVALID_ARG;
+    // aliasing: only ARRAY out == ARRAY input exactly (in-place accumulation)
+    for (const spccl_operand_t* in : {&a, &b}) {
+        if (!overlaps(out.ptr, operand_extent(out), in->ptr, operand_extent(*in))) continue;
+        const bool inplace = out.kind == SPCCL_ARRAY && in->kind == SPCCL_ARRAY && out.ptr == in->ptr;
+        if (!inplace) return SPCCL_ERR_INVALID_ARG;
+    }
+    hipStream_t hs = as_stream(stream);
+    WsCtrl* ctrl = static_cast<WsCtrl*>(ws);
+    if (out.kind == SPCCL_STREAM && out.fmt == SPCCL_FMT_PICI) {
+        if (out.bytes < spccl_stream_bound(n, dtype)) return SPCCL_ERR_CAPACITY;
+        st = check_ws(ws, ws_bytes, spccl_workspace_bytes(n, dtype));
+        if (st != SPCCL_OK) return st;
+        PiciSinkArgs g{};
+        g.a = sa.dev;
+        g.b = sb.dev;
+        g.out = static_cast<uint8_t*>(out.ptr);
+        g.n = n;
+        g.T = num_tiles(n);
+        g.nparts = (uint32_t)num_parts(n);
+        g.ctrl = ctrl;
+        g.flags = reinterpret_cast<uint64_t*>(static_cast<uint8_t*>(ws) + kWsFlagsOffset);
+        return launch_to_pici_dt(dtype, sa.kind, sb.kind, g, hs);
+    }
+    uint8_t* out_hdr = nullptr;
+    uint8_t* out_data = static_cast<uint8_t*>(out.ptr);
+    if (out.kind == SPCCL_STREAM) {
+        if (out.fmt != SPCCL_FMT_DENSE) return SPCCL_ERR_INVALID_ARG;
+        if (out.bytes < dense_msg_bytes(n, dtype)) return SPCCL_ERR_CAPACITY;
+        out_hdr = out_data;
+        out_data += kHeaderBytes;
+    } else if (out.kind == SPCCL_ARRAY) {
+        if (out.bytes < n * s) return SPCCL_ERR_CAPACITY;
+    } else {
+        return SPCCL_ERR_INVALID_ARG;
+    }
+    st = check_ws(ws, ws_bytes, kWsFlagsOffset);
+    if (st != SPCCL_OK) return st;
+    if (sa.kind == SRC_DENSE && sb.kind == SRC_DENSE)
+        return launch_dense_dense_dt(dtype, sa.dev.hdr, sa.dev.data, sa.dev.cap, sb.dev.hdr, sb.dev.data,
+                                     sb.dev.cap, out_hdr, out_data, n, ctrl, hs);
+    if (n == 0 && !out_hdr) return SPCCL_OK;
+    DenseSinkArgs g{};
+    g.a = sa.dev;
+    g.b = sb.dev;
+    g.out_hdr = out_hdr;
+    g.out = out_data;
+    g.n = n;
+    g.T = num_tiles(n);
+    g.ctrl = ctrl;
+    return launch_to_dense_dt(dtype, sa.kind, sb.kind, g, hs);
+}
+
+spccl_status_t spccl_copy_message(const void* src, uint64_t src_bytes, void* dst, uint64_t dst_bytes, void* ws,
+                                  uint64_t ws_bytes, void* stream) {
+    if (!src || !dst || !aligned16(src) || !aligned16(dst)) return SPCCL_ERR_INVALID_ARG;
+    if (src_bytes < kHeaderBytes) return SPCCL_ERR_CAPACITY;
+    if (overlaps(src, src_bytes, dst, dst_bytes)) return SPCCL_ERR_INVALID_ARG;
+    spccl_status_t st = check_ws(ws, ws_bytes, kWsFlagsOffset);
+    if (st != SPCCL_OK) return st;
+    return launch_copy_message(static_cast<const uint8_t*>(src), src_bytes, static_cast<uint8_t*>(dst), dst_bytes,
+                               static_cast<WsCtrl*>(ws), as_stream(stream));
+}
+
+spccl_status_t spccl_read_header(const void* msg, spccl_header_t* host_out, void* stream) {
+    if (!msg || !host_out) return SPCCL_ERR_INVALID_ARG;
+    hipStream_t hs = as_stream(stream);
+    if (hipMemcpyAsync(host_out, msg, sizeof(spccl_header_t), hipMemcpyDeviceToHost, hs) != hipSuccess)
+        return SPCCL_ERR_HIP;
+    return hipStreamSynchronize(hs) == hipSuccess ? SPCCL_OK : SPCCL_ERR_HIP;
+}
+
+spccl_status_t spccl_read_status(void* ws, int32_t clear, void* stream) {
+    if (!ws || !aligned16(ws)) return SPCCL_ERR_INVALID_ARG;
+    hipStream_t hs = as_stream(stream);
+    uint32_t v = 0;
+    if (hipMemcpyAsync(&v, ws, sizeof(v), hipMemcpyDeviceToHost, hs) != hipSuccess) return SPCCL_ERR_HIP;
+    if (hipStreamSynchronize(hs) != hipSuccess) return SPCCL_ERR_HIP;
+    if (clear && v != 0) {
+        if (launch_fill_zero(ws, sizeof(uint32_t), hs) != SPCCL_OK) return SPCCL_ERR_HIP;
+        if (hipStreamSynchronize(hs) != hipSuccess) return SPCCL_ERR_HIP;
+    }
+    return static_cast<spccl_status_t>(v);
+}
+
+const char* spccl_status_string(spccl_status_t s) {
+    switch (s) {
+        case SPCCL_OK: return "ok";
+        case SPCCL_ERR_INVALID_ARG: return "invalid argument";
+        case SPCCL_ERR_CAPACITY: return "buffer capacity too small";
+        case SPCCL_ERR_UNSUPPORTED: return "unsupported dtype or size";
+        case SPCCL_ERR_CORRUPT_STREAM: return "corrupt message";
+        case SPCCL_ERR_WORKSPACE: return "workspace too small";
+        case SPCCL_ERR_HIP: return "HIP runtime error";
+        case SPCCL_ERR_TIMEOUT: return "device wait exceeded its spin limit";
+    }
+    return "unknown status";
+}
+
+}  // extern "C"

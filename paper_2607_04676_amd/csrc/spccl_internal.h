@@ -1,0 +1,90 @@
+// Internal constants and layout helpers of the gfx950 Pici library.  Host and
+// device code of the library share this header; nothing outside the library
+// includes it.
+#pragma once
+#include <stdint.h>
+
+namespace spccl {
+
+constexpr uint32_t kMagic = 0x49434950u;        // "PICI"
+constexpr uint64_t kHeaderBytes = 48;
+constexpr uint64_t kNnzUnknown = ~0ull;
+constexpr uint32_t kTileElems = 4096;           // a 64 x 64 virtual tile
+constexpr uint32_t kWave = 64;                  // CDNA wavefront
+constexpr uint32_t kWavesPerBlock = 4;          // one tile per wave
+constexpr uint32_t kBlockThreads = kWave * kWavesPerBlock;
+constexpr uint32_t kTilesPerPart = kWavesPerBlock;   // look-back partition = one block
+constexpr uint32_t kStageBytes = 8192;          // LDS staging per wave
+
+constexpr int kFmtDense = 0, kFmtPici = 1;
+constexpr int kKindArray = 0, kKindStream = 1;
+constexpr int kF32 = 0, kBF16 = 1;
+
+// Workspace: a control block, then one 64-bit look-back word per partition.
+struct WsCtrl {
+    uint32_t status;     // sticky device status (first error wins)
+    uint32_t ticket;     // next partition to hand out (reset by the last block)
+    uint32_t done;       // partitions finished with their look-back
+    uint32_t epoch;      // call counter; tags look-back words of this call
+    uint32_t pad[60];
+};
+static_assert(sizeof(WsCtrl) == 256, "control block is 256 bytes");
+constexpr uint64_t kWsFlagsOffset = sizeof(WsCtrl);
+
+__host__ __device__ inline uint64_t elem_bytes(int dtype) { return dtype == kBF16 ? 2 : 4; }
+__host__ __device__ inline uint64_t num_tiles(uint64_t n) { return (n + kTileElems - 1) / kTileElems; }
+__host__ __device__ inline uint64_t off_I(uint64_t n) { return kHeaderBytes + 512ull * num_tiles(n); }
+__host__ __device__ inline uint64_t off_A(uint64_t n) {
+    return (off_I(n) + 4ull * (num_tiles(n) + 1) + 15ull) & ~15ull;
+}
+__host__ __device__ inline uint64_t pici_bytes(uint64_t n, int dtype, uint64_t nnz) {
+    return off_A(n) + nnz * elem_bytes(dtype);
+}
+__host__ __device__ inline uint64_t dense_msg_bytes(uint64_t n, int dtype) {
+    return kHeaderBytes + n * elem_bytes(dtype);
+}
+__host__ __device__ inline uint64_t num_parts(uint64_t n) {
+    uint64_t T = num_tiles(n);
+    uint64_t p = (T + kTilesPerPart - 1) / kTilesPerPart;
+    return p ? p : 1;
+}
+
+// Source kinds of the tile pipeline.
+enum SrcKind { SRC_NONE = 0, SRC_DENSE = 1, SRC_PICI = 2 };
+
+// A reduce / codec operand as the kernels see it.
+struct DevOperand {
+    const uint8_t* hdr;    // message header, or nullptr for a raw array
+    const uint8_t* data;   // raw array base, or the message base for Pici
+    uint64_t cap;          // capacity of the message buffer in bytes
+};
+
+struct PiciSinkArgs {
+    DevOperand a, b;
+    uint8_t* out;          // output message base
+    uint64_t n;
+    uint64_t T;
+    uint32_t nparts;
+    WsCtrl* ctrl;
+    uint64_t* flags;
+};
+
+struct DenseSinkArgs {
+    DevOperand a, b;
+    uint8_t* out_hdr;      // nullptr for an ARRAY output
+    uint8_t* out;          // output element base
+    uint64_t n;
+    uint64_t T;
+    WsCtrl* ctrl;
+};
+
+constexpr int kMaxGatherParts = 64;
+struct GatherArgs {
+    DevOperand part[kMaxGatherParts];
+    uint8_t* out;          // element base of part 0 of this launch
+    uint64_t n;            // elements per part
+    uint64_t T;
+    WsCtrl* ctrl;
+};
+
+}  // namespace spccl

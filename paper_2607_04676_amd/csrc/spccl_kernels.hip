@@ -1,0 +1,685 @@
+// gfx950 kernels of the Pici hot path (SpCCL, arXiv 2607.04676) and their
+// host launchers.
+//
+// Tile mapping.  The format views the input as 64x64 row-major tiles and
+// stores one 64-bit bit-vector word per tile column (Sec. III-B).  On a
+// 64-lane CDNA wavefront the natural mapping is one wave per tile and one
+// lane per column: lane c reads element 64r + c of row r, so each row load is
+// one fully coalesced 256-byte (fp32) access, the lane assembles its column
+// word on its own (no cross-lane traffic), and the per-column counts needed
+// for compaction are one wave prefix scan of 64 popcounts.  (The paper's
+// 32-lane warps give each thread two columns, Alg. 1; that split is not
+// needed here.)
+//
+// Single pass.  Compression and the Pici-producing reductions read their
+// input once: each block (four waves, four tiles = one look-back partition)
+// takes a partition ticket, builds B, counts, publishes its aggregate,
+// resolves its global offset by decoupled look-back over earlier partitions
+// (Merrill & Garland, "Single-pass Parallel Prefix Scan with Decoupled
+// Look-back", 2016), and writes I and A.  Values are compacted through an
+// 8 KiB per-wave LDS stage and written out contiguously.
+//
+// Numerics.  Elements are raw bit patterns; "present" = nonzero bits.  The
+// reduction adds in fp32 (bf16 operands widened exactly, the sum rounded once
+// to bf16, nearest-even); an absent operand is the identity.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "spccl_internal.h"
+#include "../../include/spccl.h"
+
+namespace spccl {
+
+// ---------------------------------------------------------------------------
+// element types
+struct F32 {
+    using raw = uint32_t;
+    static constexpr int dtype = kF32;
+    static constexpr uint32_t cap = kStageBytes / 4;   // staged values per wave
+};
+struct BF16 {
+    using raw = uint16_t;
+    static constexpr int dtype = kBF16;
+    static constexpr uint32_t cap = kStageBytes / 2;
+};
+
+// a (+) b on raw bits: absent (0) is the identity, otherwise add.
+__device__ __forceinline__ uint32_t oplus(F32, uint32_t a, uint32_t b) {
+    uint32_t s = __float_as_uint(__uint_as_float(a) + __uint_as_float(b));
+    s = (a == 0u) ? b : s;
+    return (b == 0u) ? a : s;
+}
+__device__ __forceinline__ uint32_t oplus(BF16, uint32_t a, uint32_t b) {
+    uint32_t u = __float_as_uint(__uint_as_float(a << 16) + __uint_as_float(b << 16));
+    uint32_t s = (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;     // nearest-even to bf16
+    s = (a == 0u) ? b : s;
+    return (b == 0u) ? a : s;
+}
+
+// ---------------------------------------------------------------------------
+// wave primitives
+__device__ __forceinline__ uint32_t lane_id() { return __lane_id(); }
+
+__device__ __forceinline__ uint32_t wave_sum(uint32_t x) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o, 64);
+    return x;
+}
+
+__device__ __forceinline__ uint32_t wave_excl_scan(uint32_t x) {
+    uint32_t inc = x;
+    const uint32_t l = lane_id();
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        uint32_t y = __shfl_up(inc, o, 64);
+        if (l >= (uint32_t)o) inc += y;
+    }
+    return inc - x;
+}
+
+// Order this wave's LDS accesses: a wave's LDS operations execute in order,
+// so waiting for its own outstanding ones (and stopping the compiler from
+// moving accesses across) is enough between lanes of one wave.
+__device__ __forceinline__ void wave_lds_sync() {
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    __builtin_amdgcn_wave_barrier();
+}
+
+__device__ __forceinline__ void set_status(WsCtrl* ctrl, uint32_t code) {
+    atomicCAS(&ctrl->status, 0u, code);
+}
+
+// ---------------------------------------------------------------------------
+// message headers
+
+struct HeaderView {
+    bool ok;
+    uint32_t fmt;
+    uint64_t nnz;
+};
+
+// Checks a message header against the expected n / dtype (and format if
+// want_fmt >= 0) and the buffer capacity; every offset must be the one the
+// layout implies, so a passing header bounds every later read.
+__device__ HeaderView read_header(const uint8_t* h, uint64_t cap, uint64_t n, int dtype, int want_fmt) {
+    HeaderView v{false, 0u, 0ull};
+    if (cap < kHeaderBytes) return v;
+    const uint64_t* w = reinterpret_cast<const uint64_t*>(h);
+    const uint64_t w0 = w[0], hn = w[1], nnz = w[2], oI = w[3], oA = w[4], total = w[5];
+    const uint32_t magic = (uint32_t)w0, fmt = (uint32_t)(w0 >> 32) & 0xFFFFu, dt = (uint32_t)(w0 >> 48);
+    bool ok = magic == kMagic && dt == (uint32_t)dtype && hn == n && total <= cap;
+    if (want_fmt >= 0) ok = ok && fmt == (uint32_t)want_fmt;
+    if (fmt == (uint32_t)kFmtPici)
+        ok = ok && oI == off_I(n) && oA == off_A(n) && nnz <= n && total == oA + nnz * elem_bytes(dtype);
+    else if (fmt == (uint32_t)kFmtDense)
+        ok = ok && oA == kHeaderBytes && total == dense_msg_bytes(n, dtype);
+    else
+        ok = false;
+    v.ok = ok;
+    v.fmt = fmt;
+    v.nnz = nnz;
+    return v;
+}
+
+__device__ __forceinline__ void write_header(uint8_t* out, int fmt, int dtype, uint64_t n, uint64_t nnz,
+                                             uint64_t oI, uint64_t oA, uint64_t total) {
+    uint64_t* w = reinterpret_cast<uint64_t*>(out);
+    w[0] = (uint64_t)kMagic | ((uint64_t)(uint32_t)fmt << 32) | ((uint64_t)(uint32_t)dtype << 48);
+    w[1] = n;
+    w[2] = nnz;
+    w[3] = oI;
+    w[4] = oA;
+    w[5] = total;
+}
+
+// ---------------------------------------------------------------------------
+// tile sources: fill v[r] = element (row r, column lane) of tile t
+
+// Dense source.  first: v = x; otherwise v = v (+) x.
+template <class E, bool First>
+__device__ __forceinline__ void fetch_dense(const uint8_t* base, uint64_t t, uint64_t n, uint32_t (&v)[64]) {
+    using raw = typename E::raw;
+    const uint32_t l = lane_id();
+    const raw* col = reinterpret_cast<const raw*>(base) + t * kTileElems + l;
+    const uint64_t rem = n - t * kTileElems;
+    uint32_t x[64];
+    if (rem >= kTileElems) {
+#pragma unroll
+        for (int r = 0; r < 64; r++) x[r] = col[64 * r];
+    } else {
+#pragma unroll
+        for (int r = 0; r < 64; r++) {
+            x[r] = 0u;
+            if ((uint64_t)(64 * r + l) < rem) x[r] = col[64 * r];
+        }
+    }
+#pragma unroll
+    for (int r = 0; r < 64; r++) v[r] = First ? x[r] : oplus(E{}, v[r], x[r]);
+}
+
+// Pici source: B words, I offsets and A values of tile t of a checked
+// message.  Values go through the wave's LDS stage (contiguous coalesced
+// reads of the tile's A range), then each lane walks its column word.  A
+// tile whose counts disagree with I (or overrun nnz) is treated as empty and
+// flagged.  first: v = x; otherwise v = v (+) x.
+template <class E, bool First>
+__device__ __forceinline__ void fetch_pici(const uint8_t* msg, uint64_t nnz, uint64_t t, uint64_t n,
+                                           typename E::raw* stage, WsCtrl* ctrl, uint32_t (&v)[64]) {
+    using raw = typename E::raw;
+    const uint32_t l = lane_id();
+    const uint64_t T = num_tiles(n);
+    const uint64_t* B = reinterpret_cast<const uint64_t*>(msg + kHeaderBytes);
+    const uint32_t* I = reinterpret_cast<const uint32_t*>(msg + off_I(n));
+    const raw* A = reinterpret_cast<const raw*>(msg + off_A(n));
+    uint64_t w = B[t * 64 + l];
+    const uint32_t base = I[t], next = I[t + 1];
+    uint32_t c = (uint32_t)__popcll(w);
+    uint32_t colpref = wave_excl_scan(c);
+    uint32_t cnt = __shfl(colpref + c, 63, 64);
+    if ((uint64_t)base + cnt > nnz || base + cnt != next || (t + 1 == T && (uint64_t)next != nnz)) {
+        if (l == 0) set_status(ctrl, SPCCL_ERR_CORRUPT_STREAM);
+        w = 0; c = 0; colpref = 0; cnt = 0;
+    }
+    const raw* src = A + base;
+    if (cnt <= E::cap) {
+        for (uint32_t i = l; i < cnt; i += 64) stage[i] = src[i];
+        wave_lds_sync();
+        uint32_t rank = colpref;
+#pragma unroll
+        for (int r = 0; r < 64; r++) {
+            uint32_t x = 0;
+            if ((w >> r) & 1ull) { x = stage[rank]; rank++; }
+            v[r] = First ? x : oplus(E{}, v[r], x);
+        }
+        wave_lds_sync();
+    } else {
+        // more values than the stage holds (fp32 tile more than half full):
+        // columns 0-31 first, then columns 32-63 (each at most 2048 values).
+#pragma unroll
+        for (int h = 0; h < 2; h++) {
+            const uint32_t lo = __shfl(colpref, 32 * h, 64);
+            const uint32_t hi = h == 0 ? __shfl(colpref, 32, 64) : cnt;
+            for (uint32_t i = l; i < hi - lo; i += 64) stage[i] = src[lo + i];
+            wave_lds_sync();
+            const bool mine = (l >> 5) == (uint32_t)h;
+            uint32_t rank = colpref - lo;
+#pragma unroll
+            for (int r = 0; r < 64; r++) {
+                uint32_t x = 0;
+                const bool bit = mine && ((w >> r) & 1ull);
+                if (bit) { x = stage[rank]; rank++; }
+                if (mine) v[r] = First ? x : oplus(E{}, v[r], x);
+            }
+            wave_lds_sync();
+        }
+    }
+}
+
+template <class E, int S, bool First>
+__device__ __forceinline__ void fetch(const DevOperand& op, uint64_t nnz, uint64_t t, uint64_t n,
+                                      typename E::raw* stage, WsCtrl* ctrl, uint32_t (&v)[64]) {
+    if constexpr (S == SRC_DENSE) fetch_dense<E, First>(op.data, t, n, v);
+    else if constexpr (S == SRC_PICI) fetch_pici<E, First>(op.data, nnz, t, n, stage, ctrl, v);
+}
+
+// ---------------------------------------------------------------------------
+// decoupled look-back
+
+constexpr uint32_t kFlagAggregate = 1, kFlagPrefix = 2;
+constexpr uint32_t kSpinLimit = 1u << 20;
+
+__device__ __forceinline__ void publish(uint64_t* flags, uint32_t p, uint32_t epoch30, uint32_t state, uint32_t val) {
+    const uint64_t f = ((uint64_t)epoch30 << 34) | ((uint64_t)state << 32) | (uint64_t)val;
+    __hip_atomic_store(&flags[p], f, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Exclusive prefix of partition p, computed by one whole wave: lane i looks
+// at partition (window start - i); the window slides back 64 partitions at a
+// time until it meets an inclusive prefix.  Words of another call carry
+// another epoch and count as not yet published.
+__device__ uint32_t lookback(const uint64_t* flags, uint32_t p, uint32_t epoch30, WsCtrl* ctrl) {
+    const uint32_t l = lane_id();
+    uint32_t excl = 0;
+    int64_t start = (int64_t)p - 1;
+    uint32_t spins = 0;
+    while (start >= 0) {
+        const int64_t q = start - (int64_t)l;
+        uint32_t state = kFlagPrefix, val = 0;
+        if (q >= 0) {
+            const uint64_t f = __hip_atomic_load(&flags[q], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            state = ((uint32_t)(f >> 34) == epoch30) ? (uint32_t)(f >> 32) & 3u : 0u;
+            val = (uint32_t)f;
+        }
+        const uint64_t mP = __ballot(state == kFlagPrefix);
+        const uint64_t mX = __ballot(state == 0u);
+        const uint64_t upto = mP ? (((mP & (~mP + 1ull)) << 1) - 1ull) : ~0ull;   // lanes 0..first prefix
+        if (mX & upto) {
+            if (++spins > kSpinLimit) {
+                if (l == 0) set_status(ctrl, SPCCL_ERR_TIMEOUT);
+                break;
+            }
+            __builtin_amdgcn_s_sleep(1);
+            continue;
+        }
+        excl += wave_sum(((upto >> l) & 1ull) ? val : 0u);
+        if (mP) break;
+        start -= 64;
+    }
+    return excl;
+}
+
+// ---------------------------------------------------------------------------
+// Pici sink: out = Pici(srcA (+) srcB), single pass.
+
+template <class E, int SA, int SB>
+__global__ void __launch_bounds__(kBlockThreads) k_to_pici(PiciSinkArgs g) {
+    using raw = typename E::raw;
+    __shared__ raw stage_all[kWavesPerBlock][E::cap];
+    __shared__ uint32_t s_cnt[kWavesPerBlock];
+    __shared__ uint32_t s_part, s_epoch, s_prefix, s_ok;
+    __shared__ uint64_t s_nnz_a, s_nnz_b;
+
+    const uint32_t wave = threadIdx.x >> 6, l = lane_id();
+    raw* stage = stage_all[wave];
+    if (threadIdx.x == 0) {
+        bool ok = true;
+        uint64_t na = 0, nb = 0;
+        if (g.a.hdr) {
+            HeaderView h = read_header(g.a.hdr, g.a.cap, g.n, E::dtype, SA == SRC_PICI ? kFmtPici : kFmtDense);
+            ok = ok && h.ok; na = h.nnz;
+        }
+        if (SB != SRC_NONE && g.b.hdr) {
+            HeaderView h = read_header(g.b.hdr, g.b.cap, g.n, E::dtype, SB == SRC_PICI ? kFmtPici : kFmtDense);
+            ok = ok && h.ok; nb = h.nnz;
+        }
+        s_ok = ok;
+        s_nnz_a = na;
+        s_nnz_b = nb;
+        if (ok) {
+            s_epoch = __hip_atomic_load(&g.ctrl->epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            s_part = atomicAdd(&g.ctrl->ticket, 1u);
+        } else if (blockIdx.x == 0) {
+            set_status(g.ctrl, SPCCL_ERR_CORRUPT_STREAM);
+        }
+    }
+    __syncthreads();
+    if (!s_ok) return;            // uniform over the grid: nobody took a ticket
+
+    const uint32_t p = s_part;
+    if (p >= g.nparts) {          // ticket counter not reset: workspace was not initialised
+        if (threadIdx.x == 0) set_status(g.ctrl, SPCCL_ERR_WORKSPACE);
+        return;
+    }
+    const uint32_t epoch30 = s_epoch & 0x3FFFFFFFu;
+    const uint64_t t = (uint64_t)p * kTilesPerPart + wave;
+    const bool has_tile = t < g.T;
+
+    uint32_t v[64];
+    uint64_t w = 0;
+    uint32_t c = 0;
+    if (has_tile) {
+        fetch<E, SA, true>(g.a, s_nnz_a, t, g.n, stage, g.ctrl, v);
+        if constexpr (SB != SRC_NONE) fetch<E, SB, false>(g.b, s_nnz_b, t, g.n, stage, g.ctrl, v);
+        const uint64_t rem = g.n - t * kTileElems;
+        if (rem < kTileElems) {
+#pragma unroll
+            for (int r = 0; r < 64; r++)
+                if ((uint64_t)(64 * r + l) >= rem) v[r] = 0;
+        }
+#pragma unroll
+        for (int r = 0; r < 64; r++) w |= (uint64_t)(v[r] != 0u) << r;
+        c = (uint32_t)__popcll(w);
+        reinterpret_cast<uint64_t*>(g.out + kHeaderBytes)[t * 64 + l] = w;
+    }
+    const uint32_t colpref = wave_excl_scan(c);
+    const uint32_t tilecnt = __shfl(colpref + c, 63, 64);
+    if (l == 0) s_cnt[wave] = tilecnt;
+    __syncthreads();
+
+    uint32_t tile_excl = 0, agg = 0;
+#pragma unroll
+    for (uint32_t k = 0; k < kWavesPerBlock; k++) {
+        const uint32_t ck = s_cnt[k];
+        tile_excl += k < wave ? ck : 0u;
+        agg += ck;
+    }
+    if (threadIdx.x == 0) publish(g.flags, p, epoch30, p == 0 ? kFlagPrefix : kFlagAggregate, agg);
+
+    const bool single = tilecnt <= E::cap;
+    if (has_tile && single) {
+        uint32_t rank = colpref;
+#pragma unroll
+        for (int r = 0; r < 64; r++)
+            if ((w >> r) & 1ull) { stage[rank] = (raw)v[r]; rank++; }
+    }
+    if (wave == 0) {
+        const uint32_t prefix = p == 0 ? 0u : lookback(g.flags, p, epoch30, g.ctrl);
+        if (l == 0) {
+            if (p != 0) publish(g.flags, p, epoch30, kFlagPrefix, prefix + agg);
+            s_prefix = prefix;
+            const uint32_t d = atomicAdd(&g.ctrl->done, 1u);
+            if (d == g.nparts - 1) {     // last partition through: reset for the next call
+                __hip_atomic_store(&g.ctrl->ticket, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                __hip_atomic_store(&g.ctrl->done, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                __hip_atomic_store(&g.ctrl->epoch, s_epoch + 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            }
+        }
+    }
+    __syncthreads();
+
+    const uint32_t prefix = s_prefix;
+    const uint64_t oI = off_I(g.n), oA = off_A(g.n);
+    raw* A = reinterpret_cast<raw*>(g.out + oA);
+    const uint32_t tbase = prefix + tile_excl;
+    if (has_tile) {
+        if (single) {
+            raw* dst = A + tbase;
+            for (uint32_t i = l; i < tilecnt; i += 64) dst[i] = stage[i];
+        } else {
+#pragma unroll
+            for (int h = 0; h < 2; h++) {
+                const uint32_t lo = __shfl(colpref, 32 * h, 64);
+                const uint32_t hi = h == 0 ? __shfl(colpref, 32, 64) : tilecnt;
+                const bool mine = (l >> 5) == (uint32_t)h;
+                uint32_t rank = colpref - lo;
+#pragma unroll
+                for (int r = 0; r < 64; r++)
+                    if (mine && ((w >> r) & 1ull)) { stage[rank] = (raw)v[r]; rank++; }
+                wave_lds_sync();
+                raw* dst = A + tbase + lo;
+                for (uint32_t i = l; i < hi - lo; i += 64) dst[i] = stage[i];
+                wave_lds_sync();
+            }
+        }
+        if (l == 0) reinterpret_cast<uint32_t*>(g.out + oI)[t] = tbase;
+    }
+    if (p == g.nparts - 1 && threadIdx.x == 0) {
+        const uint64_t nnz = (uint64_t)prefix + agg;
+        uint32_t* I = reinterpret_cast<uint32_t*>(g.out + oI);
+        I[g.T] = (uint32_t)nnz;
+        for (uint64_t b = oI + 4 * (g.T + 1); b < oA; b += 4) *reinterpret_cast<uint32_t*>(g.out + b) = 0u;
+        write_header(g.out, kFmtPici, E::dtype, g.n, nnz, oI, oA, oA + nnz * sizeof(raw));
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Dense sink: out[i] = (srcA (+) srcB)[i] for every i < n.
+
+template <class E>
+__device__ __forceinline__ void store_tile(uint8_t* out, uint64_t t, uint64_t n, const uint32_t (&v)[64]) {
+    using raw = typename E::raw;
+    const uint32_t l = lane_id();
+    raw* col = reinterpret_cast<raw*>(out) + t * kTileElems + l;
+    const uint64_t rem = n - t * kTileElems;
+    if (rem >= kTileElems) {
+#pragma unroll
+        for (int r = 0; r < 64; r++) col[64 * r] = (raw)v[r];
+    } else {
+#pragma unroll
+        for (int r = 0; r < 64; r++)
+            if ((uint64_t)(64 * r + l) < rem) col[64 * r] = (raw)v[r];
+    }
+}
+
+template <class E, int SA, int SB>
+__global__ void __launch_bounds__(kBlockThreads) k_to_dense(DenseSinkArgs g) {
+    using raw = typename E::raw;
+    __shared__ raw stage_all[kWavesPerBlock][E::cap];
+    __shared__ uint32_t s_ok;
+    __shared__ uint64_t s_nnz_a, s_nnz_b;
+    const uint32_t wave = threadIdx.x >> 6;
+    if (threadIdx.x == 0) {
+        bool ok = true;
+        uint64_t na = 0, nb = 0;
+        if (g.a.hdr) {
+            HeaderView h = read_header(g.a.hdr, g.a.cap, g.n, E::dtype, SA == SRC_PICI ? kFmtPici : kFmtDense);
+            ok = ok && h.ok; na = h.nnz;
+        }
+        if (SB != SRC_NONE && g.b.hdr) {
+            HeaderView h = read_header(g.b.hdr, g.b.cap, g.n, E::dtype, SB == SRC_PICI ? kFmtPici : kFmtDense);
+            ok = ok && h.ok; nb = h.nnz;
+        }
+        s_ok = ok;
+        s_nnz_a = na;
+        s_nnz_b = nb;
+        if (!ok && blockIdx.x == 0) set_status(g.ctrl, SPCCL_ERR_CORRUPT_STREAM);
+        if (ok && blockIdx.x == 0 && g.out_hdr)
+            write_header(g.out_hdr, kFmtDense, E::dtype, g.n, kNnzUnknown, 0, kHeaderBytes,
+                         dense_msg_bytes(g.n, E::dtype));
+    }
+    __syncthreads();
+    if (!s_ok) return;
+    const uint64_t t = (uint64_t)blockIdx.x * kWavesPerBlock + wave;
+    if (t >= g.T) return;
+    uint32_t v[64];
+    fetch<E, SA, true>(g.a, s_nnz_a, t, g.n, stage_all[wave], g.ctrl, v);
+    if constexpr (SB != SRC_NONE) fetch<E, SB, false>(g.b, s_nnz_b, t, g.n, stage_all[wave], g.ctrl, v);
+    store_tile<E>(g.out, t, g.n, v);
+}
+
+// Expansion of P parts (all-gather receive side and decompress): the format
+// of each message is read from its header on the device.
+template <class E>
+__global__ void __launch_bounds__(kBlockThreads) k_gather(GatherArgs g) {
+    using raw = typename E::raw;
+    __shared__ raw stage_all[kWavesPerBlock][E::cap];
+    __shared__ uint32_t s_ok, s_fmt;
+    __shared__ uint64_t s_nnz;
+    const uint32_t wave = threadIdx.x >> 6;
+    const DevOperand op = g.part[blockIdx.y];
+    if (threadIdx.x == 0) {
+        if (op.hdr) {
+            HeaderView h = read_header(op.hdr, op.cap, g.n, E::dtype, -1);
+            s_ok = h.ok; s_fmt = h.fmt; s_nnz = h.nnz;
+            if (!h.ok && blockIdx.x == 0) set_status(g.ctrl, SPCCL_ERR_CORRUPT_STREAM);
+        } else {
+            s_ok = 1; s_fmt = kFmtDense; s_nnz = 0;
+        }
+    }
+    __syncthreads();
+    if (!s_ok) return;
+    const uint64_t t = (uint64_t)blockIdx.x * kWavesPerBlock + wave;
+    if (t >= g.T) return;
+    uint32_t v[64];
+    if (s_fmt == (uint32_t)kFmtPici) {
+        fetch_pici<E, true>(op.data, s_nnz, t, g.n, stage_all[wave], g.ctrl, v);
+    } else {
+        const uint8_t* d = op.hdr ? op.hdr + kHeaderBytes : op.data;
+        fetch_dense<E, true>(d, t, g.n, v);
+    }
+    store_tile<E>(g.out + (uint64_t)blockIdx.y * g.n * sizeof(raw), t, g.n, v);
+}
+
+// ---------------------------------------------------------------------------
+// dense (+) dense -> dense, 16 bytes per lane per step (the dense ring step)
+
+template <class E>
+__global__ void __launch_bounds__(256) k_dense_dense(const uint8_t* a_hdr, const uint8_t* a, uint64_t a_cap,
+                                                     const uint8_t* b_hdr, const uint8_t* b, uint64_t b_cap,
+                                                     uint8_t* out_hdr, uint8_t* out, uint64_t n, WsCtrl* ctrl) {
+    using raw = typename E::raw;
+    __shared__ uint32_t s_ok;
+    if (threadIdx.x == 0) {
+        bool ok = true;
+        if (a_hdr) ok = ok && read_header(a_hdr, a_cap, n, E::dtype, kFmtDense).ok;
+        if (b_hdr) ok = ok && read_header(b_hdr, b_cap, n, E::dtype, kFmtDense).ok;
+        s_ok = ok;
+        if (!ok && blockIdx.x == 0) set_status(ctrl, SPCCL_ERR_CORRUPT_STREAM);
+        if (ok && blockIdx.x == 0 && out_hdr)
+            write_header(out_hdr, kFmtDense, E::dtype, n, kNnzUnknown, 0, kHeaderBytes, dense_msg_bytes(n, E::dtype));
+    }
+    __syncthreads();
+    if (!s_ok) return;
+    constexpr uint32_t per = 16 / sizeof(raw);
+    const uint64_t nvec = n / per;
+    const uint4* av = reinterpret_cast<const uint4*>(a);
+    const uint4* bv = reinterpret_cast<const uint4*>(b);
+    uint4* ov = reinterpret_cast<uint4*>(out);
+    const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
+    for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < nvec; i += stride) {
+        uint4 x = av[i], y = bv[i], z;
+        if constexpr (sizeof(raw) == 4) {
+            z.x = oplus(E{}, x.x, y.x); z.y = oplus(E{}, x.y, y.y);
+            z.z = oplus(E{}, x.z, y.z); z.w = oplus(E{}, x.w, y.w);
+        } else {
+            auto two = [](uint32_t p, uint32_t q) {
+                return oplus(E{}, p & 0xFFFFu, q & 0xFFFFu) | (oplus(E{}, p >> 16, q >> 16) << 16);
+            };
+            z.x = two(x.x, y.x); z.y = two(x.y, y.y); z.z = two(x.z, y.z); z.w = two(x.w, y.w);
+        }
+        ov[i] = z;
+    }
+    if (blockIdx.x == 0) {
+        const raw* ae = reinterpret_cast<const raw*>(a);
+        const raw* be = reinterpret_cast<const raw*>(b);
+        raw* oe = reinterpret_cast<raw*>(out);
+        for (uint64_t i = nvec * per + threadIdx.x; i < n; i += blockDim.x) oe[i] = (raw)oplus(E{}, ae[i], be[i]);
+    }
+}
+
+// ---------------------------------------------------------------------------
+// message copy sized on the device (the virtual-rank send)
+
+__global__ void __launch_bounds__(256) k_copy_message(const uint8_t* src, uint64_t src_cap, uint8_t* dst,
+                                                      uint64_t dst_cap, WsCtrl* ctrl) {
+    __shared__ uint64_t s_total;
+    if (threadIdx.x == 0) {
+        uint64_t total = 0;
+        if (src_cap >= kHeaderBytes) {
+            const uint64_t* w = reinterpret_cast<const uint64_t*>(src);
+            total = ((uint32_t)w[0] == kMagic) ? w[5] : 0;
+        }
+        if (total < kHeaderBytes || total > src_cap || total > dst_cap) {
+            if (blockIdx.x == 0) set_status(ctrl, SPCCL_ERR_CORRUPT_STREAM);
+            total = 0;
+        }
+        s_total = total;
+    }
+    __syncthreads();
+    const uint64_t total = s_total;
+    const uint64_t nvec = total / 16;
+    const uint4* s4 = reinterpret_cast<const uint4*>(src);
+    uint4* d4 = reinterpret_cast<uint4*>(dst);
+    const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
+    for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < nvec; i += stride) d4[i] = s4[i];
+    if (blockIdx.x == 0)
+        for (uint64_t b = nvec * 16 + threadIdx.x; b < total; b += blockDim.x) dst[b] = src[b];
+}
+
+template <class E>
+__global__ void __launch_bounds__(256) k_encode_dense(const uint8_t* src, uint8_t* out, uint64_t n) {
+    if (blockIdx.x == 0 && threadIdx.x == 0)
+        write_header(out, kFmtDense, E::dtype, n, kNnzUnknown, 0, kHeaderBytes, dense_msg_bytes(n, E::dtype));
+    const uint64_t bytes = n * sizeof(typename E::raw);
+    const uint64_t nvec = bytes / 16;
+    const uint4* s4 = reinterpret_cast<const uint4*>(src);
+    uint4* d4 = reinterpret_cast<uint4*>(out + kHeaderBytes);
+    const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
+    for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < nvec; i += stride) d4[i] = s4[i];
+    if (blockIdx.x == 0)
+        for (uint64_t b = nvec * 16 + threadIdx.x; b < bytes; b += blockDim.x) out[kHeaderBytes + b] = src[b];
+}
+
+__global__ void __launch_bounds__(256) k_fill_zero(uint4* p, uint64_t nvec, uint8_t* tail, uint64_t ntail) {
+    const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
+    for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < nvec; i += stride) p[i] = uint4{0, 0, 0, 0};
+    if (blockIdx.x == 0)
+        for (uint64_t b = threadIdx.x; b < ntail; b += blockDim.x) tail[b] = 0;
+}
+
+// ---------------------------------------------------------------------------
+// host launchers
+
+namespace {
+
+inline spccl_status_t launch_status() {
+    return hipGetLastError() == hipSuccess ? SPCCL_OK : SPCCL_ERR_HIP;
+}
+
+inline uint32_t stream_grid(uint64_t work_items, uint32_t per_block, uint32_t cap) {
+    uint64_t g = (work_items + per_block - 1) / per_block;
+    if (g < 1) g = 1;
+    if (g > cap) g = cap;
+    return (uint32_t)g;
+}
+
+template <class E>
+spccl_status_t launch_to_pici(int sa, int sb, const PiciSinkArgs& g, hipStream_t st) {
+    dim3 grid(g.nparts), block(kBlockThreads);
+#define SPCCL_TO_PICI(A, B) hipLaunchKernelGGL((k_to_pici<E, A, B>), grid, block, 0, st, g)
+    if (sa == SRC_DENSE && sb == SRC_NONE) SPCCL_TO_PICI(SRC_DENSE, SRC_NONE);
+    else if (sa == SRC_DENSE && sb == SRC_DENSE) SPCCL_TO_PICI(SRC_DENSE, SRC_DENSE);
+    else if (sa == SRC_DENSE && sb == SRC_PICI) SPCCL_TO_PICI(SRC_DENSE, SRC_PICI);
+    else if (sa == SRC_PICI && sb == SRC_DENSE) SPCCL_TO_PICI(SRC_PICI, SRC_DENSE);
+    else if (sa == SRC_PICI && sb == SRC_PICI) SPCCL_TO_PICI(SRC_PICI, SRC_PICI);
+    else return SPCCL_ERR_INVALID_ARG;
+#undef SPCCL_TO_PICI
+    return launch_status();
+}
+
+template <class E>
+spccl_status_t launch_to_dense(int sa, int sb, const DenseSinkArgs& g, hipStream_t st) {
+    dim3 grid(stream_grid(g.T, kWavesPerBlock, 0x7FFFFFFF)), block(kBlockThreads);
+#define SPCCL_TO_DENSE(A, B) hipLaunchKernelGGL((k_to_dense<E, A, B>), grid, block, 0, st, g)
+    if (sa == SRC_DENSE && sb == SRC_PICI) SPCCL_TO_DENSE(SRC_DENSE, SRC_PICI);
+    else if (sa == SRC_PICI && sb == SRC_DENSE) SPCCL_TO_DENSE(SRC_PICI, SRC_DENSE);
+    else if (sa == SRC_PICI && sb == SRC_PICI) SPCCL_TO_DENSE(SRC_PICI, SRC_PICI);
+    else if (sa == SRC_PICI && sb == SRC_NONE) SPCCL_TO_DENSE(SRC_PICI, SRC_NONE);
+    else return SPCCL_ERR_INVALID_ARG;
+#undef SPCCL_TO_DENSE
+    return launch_status();
+}
+
+}  // namespace
+
+spccl_status_t launch_to_pici_dt(int dtype, int sa, int sb, const PiciSinkArgs& g, hipStream_t st) {
+    return dtype == kBF16 ? launch_to_pici<BF16>(sa, sb, g, st) : launch_to_pici<F32>(sa, sb, g, st);
+}
+
+spccl_status_t launch_to_dense_dt(int dtype, int sa, int sb, const DenseSinkArgs& g, hipStream_t st) {
+    return dtype == kBF16 ? launch_to_dense<BF16>(sa, sb, g, st) : launch_to_dense<F32>(sa, sb, g, st);
+}
+
+spccl_status_t launch_gather_dt(int dtype, const GatherArgs& g, int P, hipStream_t st) {
+    dim3 grid(stream_grid(g.T, kWavesPerBlock, 0x7FFFFFFF), (unsigned)P), block(kBlockThreads);
+    if (dtype == kBF16) hipLaunchKernelGGL(k_gather<BF16>, grid, block, 0, st, g);
+    else hipLaunchKernelGGL(k_gather<F32>, grid, block, 0, st, g);
+    return launch_status();
+}
+
+spccl_status_t launch_dense_dense_dt(int dtype, const uint8_t* a_hdr, const uint8_t* a, uint64_t a_cap,
+                                     const uint8_t* b_hdr, const uint8_t* b, uint64_t b_cap, uint8_t* out_hdr,
+                                     uint8_t* out, uint64_t n, WsCtrl* ctrl, hipStream_t st) {
+    const uint64_t vec = n / (16 / elem_bytes(dtype));
+    dim3 grid(stream_grid(vec, 256 * 4, 8192)), block(256);
+    if (dtype == kBF16)
+        hipLaunchKernelGGL(k_dense_dense<BF16>, grid, block, 0, st, a_hdr, a, a_cap, b_hdr, b, b_cap, out_hdr, out, n, ctrl);
+    else
+        hipLaunchKernelGGL(k_dense_dense<F32>, grid, block, 0, st, a_hdr, a, a_cap, b_hdr, b, b_cap, out_hdr, out, n, ctrl);
+    return launch_status();
+}
+
+spccl_status_t launch_copy_message(const uint8_t* src, uint64_t src_cap, uint8_t* dst, uint64_t dst_cap,
+                                   WsCtrl* ctrl, hipStream_t st) {
+    const uint64_t cap = src_cap < dst_cap ? src_cap : dst_cap;
+    dim3 grid(stream_grid(cap / 16, 256 * 4, 4096)), block(256);
+    hipLaunchKernelGGL(k_copy_message, grid, block, 0, st, src, src_cap, dst, dst_cap, ctrl);
+    return launch_status();
+}
+
+spccl_status_t launch_encode_dense_dt(int dtype, const uint8_t* src, uint8_t* out, uint64_t n, hipStream_t st) {
+    dim3 grid(stream_grid(n * elem_bytes(dtype) / 16, 256 * 4, 4096)), block(256);
+    if (dtype == kBF16) hipLaunchKernelGGL(k_encode_dense<BF16>, grid, block, 0, st, src, out, n);
+    else hipLaunchKernelGGL(k_encode_dense<F32>, grid, block, 0, st, src, out, n);
+    return launch_status();
+}
+
+spccl_status_t launch_fill_zero(void* p, uint64_t bytes, hipStream_t st) {
+    const uint64_t nvec = bytes / 16;
+    dim3 grid(stream_grid(nvec, 256 * 4, 4096)), block(256);
+    hipLaunchKernelGGL(k_fill_zero, grid, block, 0, st, reinterpret_cast<uint4*>(p), nvec,
+                       reinterpret_cast<uint8_t*>(p) + nvec * 16, bytes - nvec * 16);
+    return launch_status();
+}
+
+}  // namespace spccl

@@ -1,0 +1,304 @@
+// Ring collectives over P virtual ranks held in one GPU's memory (Sec. IV).
+//
+// Each rank's send / receive buffers are regions of one scratch allocation;
+// a "send" is a device-side copy of the message (its size is read from the
+// header on the device).  Format decisions are made on the host, per sending
+// rank, from the nonzero counts the compressing kernels write into the
+// message headers: one stream synchronization per ring step reads all P
+// headers with a single strided copy.
+//
+// Decision rule (Sec. IV-C):
+//   step 0      compress the first chunk, sigma0 = sigma_prev = measured;
+//               send dense iff sigma0 <= tau(link)
+//   step s > 0  est = sigma_prev * sigma0 (Eq. 7); if est <= tau(link),
+//               reduce to a dense message and track est; otherwise reduce and
+//               compress in one pass and track the measured sparsity
+//   all-reduce  at the reduce-scatter -> all-gather transition each rank
+//               gathers densely iff sigma_prev * sigma0 <= ag_thresh
+// tau(link) is inter_thresh on a link r -> r+1 that leaves a node
+// ((r+1) % ranks_per_node == 0) and intra_thresh otherwise.
+#include <hip/hip_runtime_api.h>
+#include <stdint.h>
+#include <string.h>
+
+#include <vector>
+
+#include "spccl_internal.h"
+#include "../../include/spccl.h"
+
+using namespace spccl;
+
+namespace {
+
+constexpr uint64_t kAlign = 256;
+inline uint64_t round_up(uint64_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+inline hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s); }
+
+struct Layout {
+    uint8_t* ws;
+    uint64_t ws_bytes;
+    uint64_t slot_bytes;        // capacity of one message buffer
+    uint8_t* slots;             // 3 * P message buffers
+    uint8_t* slot(int which, int r, int P) const { return slots + ((uint64_t)which * P + r) * slot_bytes; }
+};
+
+uint64_t scratch_need(int32_t P, uint64_t msg_elems, int32_t dtype) {
+    return round_up(spccl_workspace_bytes(msg_elems, dtype)) + 3ull * (uint64_t)P * round_up(spccl_stream_bound(msg_elems, dtype));
+}
+
+Layout carve(void* scratch, int32_t P, uint64_t msg_elems, int32_t dtype) {
+    Layout L;
+    L.ws = static_cast<uint8_t*>(scratch);
+    L.ws_bytes = round_up(spccl_workspace_bytes(msg_elems, dtype));
+    L.slot_bytes = round_up(spccl_stream_bound(msg_elems, dtype));
+    L.slots = L.ws + L.ws_bytes;
+    return L;
+}
+
+double link_tau(const spccl_policy_t& pol, int r, int P) {
+    const int rpn = pol.ranks_per_node > 0 ? pol.ranks_per_node : P;
+    return ((r + 1) % rpn == 0 && rpn < P) ? pol.inter_thresh : pol.intra_thresh;
+}
+
+bool send_dense(const spccl_policy_t& pol, double sigma, double tau) {
+    if (pol.adaptive == 0) return false;
+    if (pol.adaptive == 2) return true;
+    return sigma <= tau;
+}
+
+double sparsity(uint64_t m, uint64_t nnz) { return m == 0 ? 1.0 : (double)(m - nnz) / (double)m; }
+
+// Read the headers of message slot `which` of all P ranks (one strided copy).
+spccl_status_t read_headers(const Layout& L, int which, int P, std::vector<spccl_header_t>& h, hipStream_t st) {
+    h.resize(P);
+    if (hipMemcpy2DAsync(h.data(), sizeof(spccl_header_t), L.slot(which, 0, P), L.slot_bytes, sizeof(spccl_header_t),
+                         P, hipMemcpyDeviceToHost, st) != hipSuccess)
+        return SPCCL_ERR_HIP;
+    return hipStreamSynchronize(st) == hipSuccess ? SPCCL_OK : SPCCL_ERR_HIP;
+}
+
+void put_trace(spccl_trace_t* tr, int idx, int step, int rank, int fmt, int measured, uint64_t bytes, uint64_t nnz,
+               double sigma) {
+    if (!tr) return;
+    tr[idx] = spccl_trace_t{step, rank, fmt, measured, bytes, nnz, sigma};
+}
+
+spccl_operand_t arr(const void* p, uint64_t bytes) {
+    return spccl_operand_t{SPCCL_ARRAY, 0, const_cast<void*>(p), bytes};
+}
+spccl_operand_t msg(void* p, int fmt, uint64_t bytes) { return spccl_operand_t{SPCCL_STREAM, fmt, p, bytes}; }
+
+#define SPCCL_TRY(x)                               \
+    do {                                           \
+        spccl_status_t st_ = (x);                  \
+        if (st_ != SPCCL_OK) return st_;           \
+    } while (0)
+
+// Reduce-scatter over the chunks; the reduced chunk r goes to out[r] (m
+// elements).  On return sig0 / sigp hold each rank's sigma0 and tracked
+// sparsity after its last send.
+spccl_status_t ring_rs(void* const* send, void* const* out, int P, uint64_t n, int dtype, const spccl_policy_t& pol,
+                       const Layout& L, spccl_trace_t* trace, std::vector<double>& sig0, std::vector<double>& sigp,
+                       hipStream_t st) {
+    const uint64_t m = n / (uint64_t)P, s = elem_bytes(dtype);
+    sig0.assign(P, 1.0);
+    sigp.assign(P, 1.0);
+    if (P == 1) {
+        if (m && hipMemcpyAsync(out[0], send[0], m * s, hipMemcpyDeviceToDevice, st) != hipSuccess) return SPCCL_ERR_HIP;
+        return SPCCL_OK;
+    }
+    std::vector<int> fmt(P);
+    std::vector<spccl_header_t> h;
+    // step 0: compress the first chunk of every rank into slot 0
+    for (int r = 0; r < P; r++) {
+        const int c = (r - 1 + P) % P;
+        const uint8_t* chunk = static_cast<const uint8_t*>(send[r]) + (uint64_t)c * m * s;
+        SPCCL_TRY(spccl_compress(chunk, m, dtype, L.slot(0, r, P), L.slot_bytes, L.ws, L.ws_bytes, st));
+    }
+    SPCCL_TRY(read_headers(L, 0, P, h, st));
+    for (int r = 0; r < P; r++) {
+        const uint64_t nnz = h[r].nnz;
+        sig0[r] = sigp[r] = sparsity(m, nnz);
+        fmt[r] = SPCCL_FMT_PICI;
+        if (send_dense(pol, sig0[r], link_tau(pol, r, P))) {
+            const int c = (r - 1 + P) % P;
+            const uint8_t* chunk = static_cast<const uint8_t*>(send[r]) + (uint64_t)c * m * s;
+            SPCCL_TRY(spccl_encode_dense(chunk, m, dtype, L.slot(0, r, P), L.slot_bytes, st));
+            fmt[r] = SPCCL_FMT_DENSE;
+        }
+        const uint64_t bytes = fmt[r] == SPCCL_FMT_PICI ? h[r].total_bytes : dense_msg_bytes(m, dtype);
+        put_trace(trace, r, 0, r, fmt[r], 1, bytes, nnz, sigp[r]);
+    }
+    for (int step = 1; step <= P - 1; step++) {
+        // every send of the previous step arrives: rank r receives rank r-1's message
+        for (int r = 0; r < P; r++)
+            SPCCL_TRY(spccl_copy_message(L.slot(0, (r - 1 + P) % P, P), L.slot_bytes, L.slot(1, r, P), L.slot_bytes,
+                                         L.ws, L.ws_bytes, st));
+        std::vector<int> in_fmt(P);
+        for (int r = 0; r < P; r++) in_fmt[r] = fmt[(r - 1 + P) % P];
+        bool any_measured = false;
+        for (int r = 0; r < P; r++) {
+            const int c = (r - step - 1 + 2 * P) % P;
+            const uint8_t* own = static_cast<const uint8_t*>(send[r]) + (uint64_t)c * m * s;
+            const spccl_operand_t in = msg(L.slot(1, r, P), in_fmt[r], L.slot_bytes);
+            if (step == P - 1) {   // the last receive completes chunk r
+                SPCCL_TRY(spccl_reduce(in, arr(own, m * s), arr(out[r], m * s), m, dtype, L.ws, L.ws_bytes, st));
+                continue;
+            }
+            const double est = sigp[r] * sig0[r];   // Eq. 7
+            if (send_dense(pol, est, link_tau(pol, r, P))) {
+                SPCCL_TRY(spccl_reduce(in, arr(own, m * s), msg(L.slot(0, r, P), SPCCL_FMT_DENSE, L.slot_bytes), m,
+                                       dtype, L.ws, L.ws_bytes, st));
+                fmt[r] = SPCCL_FMT_DENSE;
+                sigp[r] = est;
+                put_trace(trace, step * P + r, step, r, SPCCL_FMT_DENSE, 0, dense_msg_bytes(m, dtype),
+                          SPCCL_NNZ_UNKNOWN, est);
+            } else {
+                SPCCL_TRY(spccl_reduce(in, arr(own, m * s), msg(L.slot(0, r, P), SPCCL_FMT_PICI, L.slot_bytes), m,
+                                       dtype, L.ws, L.ws_bytes, st));
+                fmt[r] = SPCCL_FMT_PICI;
+                any_measured = true;
+            }
+        }
+        if (any_measured) {
+            SPCCL_TRY(read_headers(L, 0, P, h, st));
+            for (int r = 0; r < P; r++) {
+                if (fmt[r] != SPCCL_FMT_PICI) continue;
+                sigp[r] = sparsity(m, h[r].nnz);
+                put_trace(trace, step * P + r, step, r, SPCCL_FMT_PICI, 1, h[r].total_bytes, h[r].nnz, sigp[r]);
+            }
+        }
+    }
+    return SPCCL_OK;
+}
+
+// All-gather of P parts of `len` elements: part q is encoded once by rank q
+// (slot 0 holds those messages), travels the ring unchanged, and is expanded
+// into out[r] + q*len by every rank r != q; each rank's own part is copied
+// from `own[r]` unless it already sits in place.
+spccl_status_t ring_ag_forward(void* const* own, void* const* out, int P, uint64_t len, int dtype, const Layout& L,
+                               hipStream_t st) {
+    const uint64_t s = elem_bytes(dtype);
+    for (int r = 0; r < P; r++) {
+        uint8_t* dst = static_cast<uint8_t*>(out[r]) + (uint64_t)r * len * s;
+        if (len && dst != own[r] && hipMemcpyAsync(dst, own[r], len * s, hipMemcpyDeviceToDevice, st) != hipSuccess)
+            return SPCCL_ERR_HIP;
+    }
+    for (int k = 0; k < P - 1; k++) {
+        // step k: rank r receives from rank r-1 what r-1 received at step k-1
+        // (its own message at k = 0): the part of rank q = r-1-k.
+        const int in_slot = 1 + (k % 2), prev_slot = k == 0 ? 0 : 1 + ((k - 1) % 2);
+        for (int r = 0; r < P; r++)
+            SPCCL_TRY(spccl_copy_message(L.slot(prev_slot, (r - 1 + P) % P, P), L.slot_bytes, L.slot(in_slot, r, P),
+                                         L.slot_bytes, L.ws, L.ws_bytes, st));
+        for (int r = 0; r < P; r++) {
+            const int q = ((r - 1 - k) % P + P) % P;
+            const spccl_operand_t part = msg(L.slot(in_slot, r, P), SPCCL_FMT_PICI, L.slot_bytes);
+            uint8_t* dst = static_cast<uint8_t*>(out[r]) + (uint64_t)q * len * s;
+            SPCCL_TRY(spccl_gather_expand(&part, 1, len, dtype, dst, len * s, L.ws, L.ws_bytes, st));
+        }
+    }
+    return SPCCL_OK;
+}
+
+spccl_status_t check_common(void* const* send, void* const* recv, int32_t P, int32_t dtype, void* scratch,
+                            uint64_t scratch_bytes, uint64_t msg_elems) {
+    if (dtype != SPCCL_F32 && dtype != SPCCL_BF16) return SPCCL_ERR_UNSUPPORTED;
+    if (msg_elems >= (1ull << 32)) return SPCCL_ERR_UNSUPPORTED;
+    if (!send || !recv || P < 1 || !scratch || (reinterpret_cast<uintptr_t>(scratch) & 15u))
+        return SPCCL_ERR_INVALID_ARG;
+    for (int r = 0; r < P; r++)
+        if (!send[r] || !recv[r] || (reinterpret_cast<uintptr_t>(send[r]) & 15u) ||
+            (reinterpret_cast<uintptr_t>(recv[r]) & 15u))
+            return SPCCL_ERR_INVALID_ARG;
+    if (scratch_bytes < scratch_need(P, msg_elems, dtype)) return SPCCL_ERR_WORKSPACE;
+    return SPCCL_OK;
+}
+
+spccl_status_t finish(const Layout& L, hipStream_t st) {
+    return spccl_read_status(L.ws, 1, st);
+}
+
+}  // namespace
+
+extern "C" {
+
+uint64_t spccl_vr_scratch_bytes(int32_t P, uint64_t msg_elems, int32_t dtype) {
+    if (P < 1 || (dtype != SPCCL_F32 && dtype != SPCCL_BF16)) return 0;
+    return scratch_need(P, msg_elems, dtype);
+}
+
+spccl_status_t spccl_vr_reduce_scatter(void* const* send, void* const* recv, int32_t P, uint64_t n, int32_t dtype,
+                                       const spccl_policy_t* policy, void* scratch, uint64_t scratch_bytes,
+                                       spccl_trace_t* trace, void* stream) {
+    if (P < 1 || n % (uint64_t)P) return SPCCL_ERR_INVALID_ARG;
+    const uint64_t m = n / (uint64_t)P;
+    SPCCL_TRY(check_common(send, recv, P, dtype, scratch, scratch_bytes, m));
+    const spccl_policy_t pol = policy ? *policy : spccl_policy_t{0.6, 0.5, 0.1, 0, 1};
+    hipStream_t st = as_stream(stream);
+    const Layout L = carve(scratch, P, m, dtype);
+    SPCCL_TRY(spccl_workspace_init(L.ws, L.ws_bytes, stream));
+    std::vector<double> sig0, sigp;
+    SPCCL_TRY(ring_rs(send, recv, P, n, dtype, pol, L, trace, sig0, sigp, st));
+    return finish(L, st);
+}
+
+spccl_status_t spccl_vr_all_gather(void* const* send, void* const* recv, int32_t P, uint64_t n, int32_t dtype,
+                                   void* scratch, uint64_t scratch_bytes, spccl_trace_t* trace, void* stream) {
+    SPCCL_TRY(check_common(send, recv, P, dtype, scratch, scratch_bytes, n));
+    hipStream_t st = as_stream(stream);
+    const Layout L = carve(scratch, P, n, dtype);
+    SPCCL_TRY(spccl_workspace_init(L.ws, L.ws_bytes, stream));
+    for (int q = 0; q < P; q++)
+        SPCCL_TRY(spccl_compress(send[q], n, dtype, L.slot(0, q, P), L.slot_bytes, L.ws, L.ws_bytes, stream));
+    std::vector<spccl_header_t> h;
+    SPCCL_TRY(read_headers(L, 0, P, h, st));
+    for (int q = 0; q < P; q++)
+        put_trace(trace, q, 0, q, SPCCL_FMT_PICI, 1, h[q].total_bytes, h[q].nnz, sparsity(n, h[q].nnz));
+    SPCCL_TRY(ring_ag_forward(send, recv, P, n, dtype, L, st));
+    return finish(L, st);
+}
+
+spccl_status_t spccl_vr_all_reduce(void* const* send, void* const* recv, int32_t P, uint64_t n, int32_t dtype,
+                                   const spccl_policy_t* policy, void* scratch, uint64_t scratch_bytes,
+                                   spccl_trace_t* trace, void* stream) {
+    if (P < 1 || n % (uint64_t)P) return SPCCL_ERR_INVALID_ARG;
+    const uint64_t m = n / (uint64_t)P, s = elem_bytes(dtype);
+    SPCCL_TRY(check_common(send, recv, P, dtype, scratch, scratch_bytes, m));
+    for (int r = 0; r < P; r++)   // outputs must not overlap the inputs (chunks are reduced into them)
+        for (int q = 0; q < P; q++) {
+            const uintptr_t a = reinterpret_cast<uintptr_t>(recv[r]), b = reinterpret_cast<uintptr_t>(send[q]);
+            if (n && a < b + n * s && b < a + n * s) return SPCCL_ERR_INVALID_ARG;
+        }
+    const spccl_policy_t pol = policy ? *policy : spccl_policy_t{0.6, 0.5, 0.1, 0, 1};
+    hipStream_t st = as_stream(stream);
+    const Layout L = carve(scratch, P, m, dtype);
+    SPCCL_TRY(spccl_workspace_init(L.ws, L.ws_bytes, stream));
+    // reduce-scatter straight into each rank's own chunk of its output
+    std::vector<void*> chunk_out(P);
+    for (int r = 0; r < P; r++) chunk_out[r] = static_cast<uint8_t*>(recv[r]) + (uint64_t)r * m * s;
+    std::vector<double> sig0, sigp;
+    SPCCL_TRY(ring_rs(send, chunk_out.data(), P, n, dtype, pol, L, trace, sig0, sigp, st));
+    // phase-aware transition: one message per rank, encoded once
+    std::vector<int> fmt(P);
+    std::vector<double> est(P);
+    for (int r = 0; r < P; r++) {
+        est[r] = sigp[r] * sig0[r];
+        const bool dense = pol.adaptive == 2 ? true : (pol.adaptive == 0 ? false : est[r] <= pol.ag_thresh);
+        fmt[r] = dense ? SPCCL_FMT_DENSE : SPCCL_FMT_PICI;
+        if (dense) SPCCL_TRY(spccl_encode_dense(chunk_out[r], m, dtype, L.slot(0, r, P), L.slot_bytes, stream));
+        else SPCCL_TRY(spccl_compress(chunk_out[r], m, dtype, L.slot(0, r, P), L.slot_bytes, L.ws, L.ws_bytes, stream));
+    }
+    std::vector<spccl_header_t> h;
+    SPCCL_TRY(read_headers(L, 0, P, h, st));
+    spccl_trace_t* ag_tr = trace ? trace + (uint64_t)P * (uint64_t)(P - 1) : nullptr;
+    for (int r = 0; r < P; r++) {
+        const bool pici = fmt[r] == SPCCL_FMT_PICI;
+        put_trace(ag_tr, r, P - 1, r, fmt[r], pici ? 1 : 0, h[r].total_bytes, pici ? h[r].nnz : SPCCL_NNZ_UNKNOWN,
+                  est[r]);
+    }
+    SPCCL_TRY(ring_ag_forward(chunk_out.data(), recv, P, m, dtype, L, st));
+    return finish(L, st);
+}
+
+}  // extern "C"
