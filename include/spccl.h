@@ -5,9 +5,10 @@
  * one GPU's memory.
  *
  * Conventions for every entry point:
- *  - Pointers are device pointers unless marked "host".  Device pointers must
- *    be 16-byte aligned.  The caller owns every buffer; the library allocates
- *    and frees nothing.
+ *  - Pointers are device pointers unless marked "host".  Messages and
+ *    workspaces must be 16-byte aligned; dense arrays need only the alignment
+ *    of their element type.  The caller owns every buffer; the library
+ *    allocates and frees nothing.
  *  - `stream` is a hipStream_t handle (NULL = the default stream).  Calls are
  *    asynchronous on it, except spccl_read_header, spccl_read_status and the
  *    spccl_vr_* collectives, which synchronize it.
@@ -59,7 +60,7 @@ typedef struct {
     int32_t fmt;      /* spccl_format_t of a STREAM: for an input, the format the
                          caller expects (checked against the header on the device);
                          for an output, the format to produce.  Ignored for ARRAY. */
-    void* ptr;        /* device pointer, 16-byte aligned */
+    void* ptr;        /* device pointer (16-byte aligned for a STREAM) */
     uint64_t bytes;   /* capacity of the buffer in bytes */
 } spccl_operand_t;
 
@@ -100,11 +101,12 @@ uint64_t spccl_pici_bytes(uint64_t n, int32_t dtype, uint64_t nnz);
  * Returns 0 for an unsupported dtype. */
 uint64_t spccl_stream_bound(uint64_t n, int32_t dtype);
 
-/* Workspace for messages of up to n elements: control words (sticky status,
- * partition ticket, epoch) and one look-back status word per partition of
- * the single-pass scan.  Must be zero-filled once before first use (or
- * cleared with spccl_workspace_init); the library keeps it consistent after
- * that.  One workspace must not be used by two calls in flight at once. */
+/* Workspace for messages of up to n elements: a 256-byte control block
+ * (the sticky device status) and one 64-bit look-back word per partition of
+ * the single-pass scan.  Zero-fill it once before first use (or clear it with
+ * spccl_workspace_init); look-back words are tagged with a per-launch epoch,
+ * so it needs no clearing between calls.  One workspace must not be used by
+ * two calls in flight at once. */
 uint64_t spccl_workspace_bytes(uint64_t n, int32_t dtype);
 
 /* Zero-fill a workspace with a fill kernel on `stream` (no memset nodes). */

@@ -5,6 +5,8 @@
 #include <stdint.h>
 #include <string.h>
 
+#include <atomic>
+
 #include "spccl_internal.h"
 #include "../../include/spccl.h"
 
@@ -26,7 +28,18 @@ using namespace spccl;
 namespace {
 
 inline bool dtype_ok(int32_t dt) { return dt == kF32 || dt == kBF16; }
+
+// Every single-pass launch tags its look-back words with a fresh epoch, so a
+// workspace never needs clearing between calls: words left by earlier calls
+// carry other epochs (30 bits; a word would have to go unwritten for 2^30
+// launches to be mistaken).
+std::atomic<uint32_t> g_epoch{1};
+inline uint32_t next_epoch() { return g_epoch.fetch_add(1, std::memory_order_relaxed) & 0x3FFFFFFFu; }
 inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+// dense arrays need only element alignment (chunks of a rank's buffer start anywhere)
+inline bool aligned_elem(const void* p, int32_t dt) {
+    return (reinterpret_cast<uintptr_t>(p) & (elem_bytes(dt) - 1)) == 0;
+}
 inline hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s); }
 inline bool overlaps(const void* a, uint64_t an, const void* b, uint64_t bn) {
     const uintptr_t x = reinterpret_cast<uintptr_t>(a), y = reinterpret_cast<uintptr_t>(b);
@@ -46,8 +59,8 @@ struct Src {
 };
 
 spccl_status_t decode_input(const spccl_operand_t& o, uint64_t n, int32_t dt, Src* out) {
-    if (!o.ptr || !aligned16(o.ptr)) return (n == 0 && o.kind == SPCCL_ARRAY && !o.ptr) ? SPCCL_OK
-                                                                                       : SPCCL_ERR_INVALID_ARG;
+    if (!o.ptr) return SPCCL_ERR_INVALID_ARG;
+    if (o.kind == SPCCL_ARRAY ? !aligned_elem(o.ptr, dt) : !aligned16(o.ptr)) return SPCCL_ERR_INVALID_ARG;
     const uint8_t* p = static_cast<const uint8_t*>(o.ptr);
     if (o.kind == SPCCL_ARRAY) {
         if (o.bytes < n * elem_bytes(dt)) return SPCCL_ERR_CAPACITY;
@@ -94,7 +107,7 @@ spccl_status_t spccl_compress(const void* dense, uint64_t n, int32_t dtype, void
                               void* ws, uint64_t ws_bytes, void* stream) {
     if (!dtype_ok(dtype)) return SPCCL_ERR_UNSUPPORTED;
     if (n >= (1ull << 32)) return SPCCL_ERR_UNSUPPORTED;
-    if ((n && (!dense || !aligned16(dense))) || !out || !aligned16(out)) return SPCCL_ERR_INVALID_ARG;
+    if ((n && (!dense || !aligned_elem(dense, dtype))) || !out || !aligned16(out)) return SPCCL_ERR_INVALID_ARG;
     if (out_bytes < spccl_stream_bound(n, dtype)) return SPCCL_ERR_CAPACITY;
     if (overlaps(dense, n * elem_bytes(dtype), out, out_bytes)) return SPCCL_ERR_INVALID_ARG;
     spccl_status_t st = check_ws(ws, ws_bytes, spccl_workspace_bytes(n, dtype));
@@ -105,6 +118,7 @@ spccl_status_t spccl_compress(const void* dense, uint64_t n, int32_t dtype, void
     g.n = n;
     g.T = num_tiles(n);
     g.nparts = (uint32_t)num_parts(n);
+    g.epoch = next_epoch();
     g.ctrl = static_cast<WsCtrl*>(ws);
     g.flags = reinterpret_cast<uint64_t*>(static_cast<uint8_t*>(ws) + kWsFlagsOffset);
     return launch_to_pici_dt(dtype, SRC_DENSE, SRC_NONE, g, as_stream(stream));
@@ -114,7 +128,7 @@ spccl_status_t spccl_encode_dense(const void* dense, uint64_t n, int32_t dtype, 
                                   void* stream) {
     if (!dtype_ok(dtype)) return SPCCL_ERR_UNSUPPORTED;
     if (n >= (1ull << 32)) return SPCCL_ERR_UNSUPPORTED;
-    if ((n && (!dense || !aligned16(dense))) || !out || !aligned16(out)) return SPCCL_ERR_INVALID_ARG;
+    if ((n && (!dense || !aligned_elem(dense, dtype))) || !out || !aligned16(out)) return SPCCL_ERR_INVALID_ARG;
     if (out_bytes < dense_msg_bytes(n, dtype)) return SPCCL_ERR_CAPACITY;
     if (overlaps(dense, n * elem_bytes(dtype), out, out_bytes)) return SPCCL_ERR_INVALID_ARG;
     return launch_encode_dense_dt(dtype, static_cast<const uint8_t*>(dense), static_cast<uint8_t*>(out), n,
@@ -129,7 +143,7 @@ spccl_status_t spccl_gather_expand(const spccl_operand_t* parts, int32_t P, uint
     if (!parts || P < 0) return SPCCL_ERR_INVALID_ARG;
     if (P == 0) return SPCCL_OK;
     const uint64_t s = elem_bytes(dtype);
-    if (!dense_out || !aligned16(dense_out)) return SPCCL_ERR_INVALID_ARG;
+    if (!dense_out || !aligned_elem(dense_out, dtype)) return SPCCL_ERR_INVALID_ARG;
     if (out_bytes < (uint64_t)P * n_per_part * s) return SPCCL_ERR_CAPACITY;
     spccl_status_t st = check_ws(ws, ws_bytes, kWsFlagsOffset);
     if (st != SPCCL_OK) return st;
@@ -142,7 +156,8 @@ spccl_status_t spccl_gather_expand(const spccl_operand_t* parts, int32_t P, uint
         const int cnt = (P - q0) < kMaxGatherParts ? (P - q0) : kMaxGatherParts;
         for (int k = 0; k < cnt; k++) {
             const spccl_operand_t& o = parts[q0 + k];
-            if (!o.ptr || !aligned16(o.ptr)) return SPCCL_ERR_INVALID_ARG;
+            if (!o.ptr || (o.kind == SPCCL_ARRAY ? !aligned_elem(o.ptr, dtype) : !aligned16(o.ptr)))
+                return SPCCL_ERR_INVALID_ARG;
             const uint8_t* p = static_cast<const uint8_t*>(o.ptr);
             if (o.kind == SPCCL_ARRAY) {
                 if (o.bytes < n_per_part * s) return SPCCL_ERR_CAPACITY;
@@ -178,7 +193,8 @@ spccl_status_t spccl_reduce(spccl_operand_t a, spccl_operand_t b, spccl_operand_
     if (st != SPCCL_OK) return st;
     st = decode_input(b, n, dtype, &sb);
     if (st != SPCCL_OK) return st;
-    if (!out.ptr || !aligned16(out.ptr)) return SPCCL_ERR_INVALID_ARG;
+    if (!out.ptr || (out.kind == SPCCL_ARRAY ? !aligned_elem(out.ptr, dtype) : !aligned16(out.ptr)))
+        return SPCCL_ERR_INVALID_ARG;
     // aliasing: only ARRAY out == ARRAY input exactly (in-place accumulation)
     for (const spccl_operand_t* in : {&a, &b}) {
         if (!overlaps(out.ptr, operand_extent(out), in->ptr, operand_extent(*in))) continue;
@@ -198,6 +214,7 @@ spccl_status_t spccl_reduce(spccl_operand_t a, spccl_operand_t b, spccl_operand_
         g.n = n;
         g.T = num_tiles(n);
         g.nparts = (uint32_t)num_parts(n);
+        g.epoch = next_epoch();
         g.ctrl = ctrl;
         g.flags = reinterpret_cast<uint64_t*>(static_cast<uint8_t*>(ws) + kWsFlagsOffset);
         return launch_to_pici_dt(dtype, sa.kind, sb.kind, g, hs);

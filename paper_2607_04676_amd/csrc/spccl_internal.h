@@ -23,10 +23,7 @@ constexpr int kF32 = 0, kBF16 = 1;
 // Workspace: a control block, then one 64-bit look-back word per partition.
 struct WsCtrl {
     uint32_t status;     // sticky device status (first error wins)
-    uint32_t ticket;     // next partition to hand out (reset by the last block)
-    uint32_t done;       // partitions finished with their look-back
-    uint32_t epoch;      // call counter; tags look-back words of this call
-    uint32_t pad[60];
+    uint32_t pad[63];
 };
 static_assert(sizeof(WsCtrl) == 256, "control block is 256 bytes");
 constexpr uint64_t kWsFlagsOffset = sizeof(WsCtrl);
@@ -65,6 +62,7 @@ struct PiciSinkArgs {
     uint64_t n;
     uint64_t T;
     uint32_t nparts;
+    uint32_t epoch;        // tags this call's look-back words (unique per launch)
     WsCtrl* ctrl;
     uint64_t* flags;
 };

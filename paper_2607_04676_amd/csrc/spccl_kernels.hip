@@ -13,7 +13,7 @@
 //
 // Single pass.  Compression and the Pici-producing reductions read their
 // input once: each block (four waves, four tiles = one look-back partition)
-// takes a partition ticket, builds B, counts, publishes its aggregate,
+// builds B, counts, publishes its aggregate,
 // resolves its global offset by decoupled look-back over earlier partitions
 // (Merrill & Garland, "Single-pass Parallel Prefix Scan with Decoupled
 // Look-back", 2016), and writes I and A.  Values are compacted through an
@@ -233,27 +233,54 @@ __device__ __forceinline__ void publish(uint64_t* flags, uint32_t p, uint32_t ep
     __hip_atomic_store(&flags[p], f, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// Exclusive prefix of partition p, computed by one whole wave: lane i looks
-// at partition (window start - i); the window slides back 64 partitions at a
-// time until it meets an inclusive prefix.  Words of another call carry
-// another epoch and count as not yet published.
+// Exclusive prefix of partition p, computed by one whole wave.  Each round
+// inspects the 256 partitions before the window start: lane l reads the
+// words of partitions start-4l .. start-4l-3, so position k = 4l + j counts
+// back from the nearest predecessor (k = 0).  The round ends at the nearest
+// inclusive prefix; every position in front of it must have published (an
+// aggregate) or the round is retried.  Words of another call carry another
+// epoch and count as unpublished.  Partitions before 0 act as a prefix of 0.
 __device__ uint32_t lookback(const uint64_t* flags, uint32_t p, uint32_t epoch30, WsCtrl* ctrl) {
     const uint32_t l = lane_id();
     uint32_t excl = 0;
     int64_t start = (int64_t)p - 1;
     uint32_t spins = 0;
     while (start >= 0) {
-        const int64_t q = start - (int64_t)l;
-        uint32_t state = kFlagPrefix, val = 0;
-        if (q >= 0) {
-            const uint64_t f = __hip_atomic_load(&flags[q], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            state = ((uint32_t)(f >> 34) == epoch30) ? (uint32_t)(f >> 32) & 3u : 0u;
-            val = (uint32_t)f;
+        uint32_t state[4], val[4];
+#pragma unroll
+        for (int j = 0; j < 4; j++) {
+            const int64_t q = start - 4 * (int64_t)l - j;
+            state[j] = kFlagPrefix;
+            val[j] = 0;
+            if (q >= 0) {
+                const uint64_t f = __hip_atomic_load(&flags[q], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                state[j] = ((uint32_t)(f >> 34) == epoch30) ? (uint32_t)(f >> 32) & 3u : 0u;
+                val[j] = (uint32_t)f;
+            }
         }
-        const uint64_t mP = __ballot(state == kFlagPrefix);
-        const uint64_t mX = __ballot(state == 0u);
-        const uint64_t upto = mP ? (((mP & (~mP + 1ull)) << 1) - 1ull) : ~0ull;   // lanes 0..first prefix
-        if (mX & upto) {
+        // nearest inclusive prefix: smallest k = 4 * lane + j with state P
+        uint32_t kP = 256;
+        uint64_t mX[4];
+#pragma unroll
+        for (int j = 0; j < 4; j++) {
+            const uint64_t mP = __ballot(state[j] == kFlagPrefix);
+            mX[j] = __ballot(state[j] == 0u);
+            if (mP) {
+                const uint32_t k = 4u * (uint32_t)__builtin_ctzll(mP) + (uint32_t)j;
+                kP = k < kP ? k : kP;
+            }
+        }
+        // every position k < kP must have published
+        bool wait = false;
+#pragma unroll
+        for (int j = 0; j < 4; j++) {
+            if (kP > (uint32_t)j) {
+                const uint32_t lanes = (kP - (uint32_t)j + 3u) / 4u;        // lanes l with 4l + j < kP
+                const uint64_t below = lanes >= 64 ? ~0ull : ((1ull << lanes) - 1ull);
+                wait = wait || (mX[j] & below) != 0ull;
+            }
+        }
+        if (wait) {
             if (++spins > kSpinLimit) {
                 if (l == 0) set_status(ctrl, SPCCL_ERR_TIMEOUT);
                 break;
@@ -261,9 +288,12 @@ __device__ uint32_t lookback(const uint64_t* flags, uint32_t p, uint32_t epoch30
             __builtin_amdgcn_s_sleep(1);
             continue;
         }
-        excl += wave_sum(((upto >> l) & 1ull) ? val : 0u);
-        if (mP) break;
-        start -= 64;
+        uint32_t mine = 0;
+#pragma unroll
+        for (int j = 0; j < 4; j++) mine += (4u * l + (uint32_t)j <= kP) ? val[j] : 0u;
+        excl += wave_sum(mine);
+        if (kP < 256) break;
+        start -= 256;
     }
     return excl;
 }
@@ -276,7 +306,7 @@ __global__ void __launch_bounds__(kBlockThreads) k_to_pici(PiciSinkArgs g) {
     using raw = typename E::raw;
     __shared__ raw stage_all[kWavesPerBlock][E::cap];
     __shared__ uint32_t s_cnt[kWavesPerBlock];
-    __shared__ uint32_t s_part, s_epoch, s_prefix, s_ok;
+    __shared__ uint32_t s_prefix, s_ok;
     __shared__ uint64_t s_nnz_a, s_nnz_b;
 
     const uint32_t wave = threadIdx.x >> 6, l = lane_id();
@@ -295,22 +325,16 @@ __global__ void __launch_bounds__(kBlockThreads) k_to_pici(PiciSinkArgs g) {
         s_ok = ok;
         s_nnz_a = na;
         s_nnz_b = nb;
-        if (ok) {
-            s_epoch = __hip_atomic_load(&g.ctrl->epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            s_part = atomicAdd(&g.ctrl->ticket, 1u);
-        } else if (blockIdx.x == 0) {
-            set_status(g.ctrl, SPCCL_ERR_CORRUPT_STREAM);
-        }
+        if (!ok && blockIdx.x == 0) set_status(g.ctrl, SPCCL_ERR_CORRUPT_STREAM);
     }
     __syncthreads();
-    if (!s_ok) return;            // uniform over the grid: nobody took a ticket
+    if (!s_ok) return;            // uniform over the grid: no partition publishes
 
-    const uint32_t p = s_part;
-    if (p >= g.nparts) {          // ticket counter not reset: workspace was not initialised
-        if (threadIdx.x == 0) set_status(g.ctrl, SPCCL_ERR_WORKSPACE);
-        return;
-    }
-    const uint32_t epoch30 = s_epoch & 0x3FFFFFFFu;
+    // Partition = block index.  Work-groups start in index order on each XCD,
+    // so the lowest unfinished partition is always resident and every wait
+    // below ends (the spin limit bounds it regardless).
+    const uint32_t p = blockIdx.x;
+    const uint32_t epoch30 = g.epoch & 0x3FFFFFFFu;
     const uint64_t t = (uint64_t)p * kTilesPerPart + wave;
     const bool has_tile = t < g.T;
 
@@ -357,12 +381,6 @@ __global__ void __launch_bounds__(kBlockThreads) k_to_pici(PiciSinkArgs g) {
         if (l == 0) {
             if (p != 0) publish(g.flags, p, epoch30, kFlagPrefix, prefix + agg);
             s_prefix = prefix;
-            const uint32_t d = atomicAdd(&g.ctrl->done, 1u);
-            if (d == g.nparts - 1) {     // last partition through: reset for the next call
-                __hip_atomic_store(&g.ctrl->ticket, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                __hip_atomic_store(&g.ctrl->done, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                __hip_atomic_store(&g.ctrl->epoch, s_epoch + 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            }
         }
     }
     __syncthreads();
@@ -511,7 +529,9 @@ __global__ void __launch_bounds__(256) k_dense_dense(const uint8_t* a_hdr, const
     __syncthreads();
     if (!s_ok) return;
     constexpr uint32_t per = 16 / sizeof(raw);
-    const uint64_t nvec = n / per;
+    const bool vec_ok = ((reinterpret_cast<uintptr_t>(a) | reinterpret_cast<uintptr_t>(b) |
+                          reinterpret_cast<uintptr_t>(out)) & 15u) == 0;
+    const uint64_t nvec = vec_ok ? n / per : 0;
     const uint4* av = reinterpret_cast<const uint4*>(a);
     const uint4* bv = reinterpret_cast<const uint4*>(b);
     uint4* ov = reinterpret_cast<uint4*>(out);
@@ -529,12 +549,12 @@ __global__ void __launch_bounds__(256) k_dense_dense(const uint8_t* a_hdr, const
         }
         ov[i] = z;
     }
-    if (blockIdx.x == 0) {
-        const raw* ae = reinterpret_cast<const raw*>(a);
-        const raw* be = reinterpret_cast<const raw*>(b);
-        raw* oe = reinterpret_cast<raw*>(out);
-        for (uint64_t i = nvec * per + threadIdx.x; i < n; i += blockDim.x) oe[i] = (raw)oplus(E{}, ae[i], be[i]);
-    }
+    // the tail (or everything, for arrays that are not 16-byte aligned)
+    const raw* ae = reinterpret_cast<const raw*>(a);
+    const raw* be = reinterpret_cast<const raw*>(b);
+    raw* oe = reinterpret_cast<raw*>(out);
+    for (uint64_t i = nvec * per + (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride)
+        oe[i] = (raw)oplus(E{}, ae[i], be[i]);
 }
 
 // ---------------------------------------------------------------------------
@@ -570,14 +590,19 @@ template <class E>
 __global__ void __launch_bounds__(256) k_encode_dense(const uint8_t* src, uint8_t* out, uint64_t n) {
     if (blockIdx.x == 0 && threadIdx.x == 0)
         write_header(out, kFmtDense, E::dtype, n, kNnzUnknown, 0, kHeaderBytes, dense_msg_bytes(n, E::dtype));
-    const uint64_t bytes = n * sizeof(typename E::raw);
-    const uint64_t nvec = bytes / 16;
+    using raw = typename E::raw;
+    const uint64_t bytes = n * sizeof(raw);
+    const bool vec_ok = (reinterpret_cast<uintptr_t>(src) & 15u) == 0;
+    const uint64_t nvec = vec_ok ? bytes / 16 : 0;
     const uint4* s4 = reinterpret_cast<const uint4*>(src);
     uint4* d4 = reinterpret_cast<uint4*>(out + kHeaderBytes);
     const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
     for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < nvec; i += stride) d4[i] = s4[i];
-    if (blockIdx.x == 0)
-        for (uint64_t b = nvec * 16 + threadIdx.x; b < bytes; b += blockDim.x) out[kHeaderBytes + b] = src[b];
+    // the tail (or everything, for a source that is not 16-byte aligned), element by element
+    const raw* se = reinterpret_cast<const raw*>(src);
+    raw* de = reinterpret_cast<raw*>(out + kHeaderBytes);
+    for (uint64_t i = nvec * 16 / sizeof(raw) + (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride)
+        de[i] = se[i];
 }
 
 __global__ void __launch_bounds__(256) k_fill_zero(uint4* p, uint64_t nvec, uint8_t* tail, uint64_t ntail) {

@@ -207,9 +207,10 @@ spccl_status_t check_common(void* const* send, void* const* recv, int32_t P, int
     if (msg_elems >= (1ull << 32)) return SPCCL_ERR_UNSUPPORTED;
     if (!send || !recv || P < 1 || !scratch || (reinterpret_cast<uintptr_t>(scratch) & 15u))
         return SPCCL_ERR_INVALID_ARG;
+    const uintptr_t amask = (uintptr_t)elem_bytes(dtype) - 1;
     for (int r = 0; r < P; r++)
-        if (!send[r] || !recv[r] || (reinterpret_cast<uintptr_t>(send[r]) & 15u) ||
-            (reinterpret_cast<uintptr_t>(recv[r]) & 15u))
+        if (!send[r] || !recv[r] || (reinterpret_cast<uintptr_t>(send[r]) & amask) ||
+            (reinterpret_cast<uintptr_t>(recv[r]) & amask))
             return SPCCL_ERR_INVALID_ARG;
     if (scratch_bytes < scratch_need(P, msg_elems, dtype)) return SPCCL_ERR_WORKSPACE;
     return SPCCL_OK;

@@ -1,13 +1,24 @@
 """Shared helpers of the GPU tests: host <-> device transfer of the seeded
 inputs and byte-level comparison against the oracle."""
+import os
 import sys
+import time
 
 import numpy as np
 
 
+_PROGRESS = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "gpurun_out")
+
+
 def log(msg: str) -> None:
-    """Name the case before a GPU step (flushed, so it survives a crash)."""
-    print(f"[gpu-case] {msg}", file=sys.stderr, flush=True)
+    """Name the case before a GPU step (flushed, so it survives a crash); the
+    line also goes to gpurun_out/progress.log when that folder exists, so a
+    long test shows progress while pytest captures its output."""
+    line = f"[gpu-case] {time.strftime('%H:%M:%S')} {msg}"
+    print(line, file=sys.stderr, flush=True)
+    if os.path.isdir(_PROGRESS):
+        with open(os.path.join(_PROGRESS, "progress.log"), "a") as f:
+            f.write(line + "\n")
 
 
 def to_dev(arr: np.ndarray):

@@ -1,0 +1,191 @@
+"""Parity at the full sizes of the five workloads, in the launch configuration
+the benchmark uses, against the CPU oracle:
+
+1. 1,048,576 fp32 at 99%: compress, round trip, Pici (+) Pici, dense (+) Pici
+2. 67,108,864 fp32 (256 MiB) at 50 / 90 / 99 / 99.9%: compress, decompress,
+   and (at 90 / 99%) the three reduce variants the benchmark times
+3. reduce-scatter, P = 8 x 33,554,432 fp32 at 99%
+4. all-gather, P = 8 x 16,777,216 bf16 at 99.9%
+5. all-reduce, P = 8 x 268,435,456 fp32 in 64 segments of sparsity
+   U[0.5, 0.99] with 70% shared positions, adaptive switching
+
+Every comparison is of whole outputs (messages byte for byte, dense arrays
+bit for bit) plus the collectives' decision traces."""
+import threading
+
+import numpy as np
+import pytest
+
+import oracle as O
+import workloads as W
+from helpers import assert_bytes_equal, bits, first_diff, log, to_dev, to_host_bits
+
+pytestmark = [pytest.mark.gpu, pytest.mark.slow]
+torch = pytest.importorskip("torch")
+
+
+@pytest.fixture(scope="module")
+def S():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2607_04676_amd as S
+    return S
+
+
+def msg_op(S, t, fmt=1):
+    return S.operand(t, S.SPCCL_STREAM, fmt)
+
+
+def gpu_message(S, produce, n, dt):
+    out = S.alloc_stream(n, dt)
+    produce(out)
+    torch.cuda.synchronize()
+    total = S.spccl_read_header(out)["total_bytes"]
+    return out[:total].cpu().numpy()
+
+
+def test_config1(S):
+    a, b = W.cfg1()
+    n = a.size
+    ws = S.alloc_workspace(n, O.F32)
+    ta, tb = to_dev(a), to_dev(b)
+    log("cfg1 compress")
+    ma = gpu_message(S, lambda o: S.spccl_compress(ta, o, ws), n, O.F32)
+    ea, nnz = O.compress(a)
+    assert nnz == W.CFG1_NNZ
+    assert_bytes_equal(ma, ea, "cfg1 compress")
+    assert ma.size == 174104                      # closed-form size of the 10,486-nonzero message
+    tma = torch.from_numpy(ma).cuda()
+    back = torch.empty(n, dtype=torch.float32, device="cuda")
+    S.spccl_decompress(tma, back, ws)
+    assert np.array_equal(to_host_bits(back), bits(a))
+    tmb = torch.from_numpy(O.compress(b)[0]).cuda()
+    log("cfg1 reduce")
+    got = gpu_message(S, lambda o: S.spccl_reduce(msg_op(S, tma), msg_op(S, tmb), msg_op(S, o), n, O.F32, ws),
+                      n, O.F32)
+    exp, _ = O.reduce(O.Operand.stream(ea), O.Operand.stream(O.compress(b)[0]), n, O.F32, O.STREAM, O.FMT_PICI)
+    assert_bytes_equal(got, exp, "cfg1 pici+pici")
+    out = torch.empty(n, dtype=torch.float32, device="cuda")
+    S.spccl_reduce(S.operand(ta), msg_op(S, tmb), S.operand(out), n, O.F32, ws)
+    expd = O.reduce(O.Operand.array(a), O.Operand.stream(O.compress(b)[0]), n, O.F32)
+    assert np.array_equal(to_host_bits(out), bits(expd))
+    assert S.spccl_read_status(ws) == 0
+
+
+@pytest.mark.parametrize("permille", W.CFG2_PERMILLE)
+def test_config2_codec_and_reduce(S, permille):
+    n = W.CFG2_N
+    log(f"cfg2 sigma={permille / 1000} generate")
+    a = W.cfg2(permille, 0)
+    ws = S.alloc_workspace(n, O.F32)
+    ta = to_dev(a)
+    log(f"cfg2 sigma={permille / 1000} compress")
+    ma = gpu_message(S, lambda o: S.spccl_compress(ta, o, ws), n, O.F32)
+    ea, nnz = O.compress(a)
+    assert nnz == W.nnz_for(n, permille)
+    assert_bytes_equal(ma, ea, f"cfg2 compress {permille}")
+    tma = torch.from_numpy(ma).cuda()
+    back = torch.empty(n, dtype=torch.float32, device="cuda")
+    S.spccl_decompress(tma, back, ws)
+    assert np.array_equal(to_host_bits(back), bits(a)), "cfg2 round trip"
+    del back
+    if permille in (900, 990):
+        b = W.cfg2(permille, 1)
+        eb, _ = O.compress(b)
+        tmb = torch.from_numpy(eb).cuda()
+        log(f"cfg2 sigma={permille / 1000} reduce dense+pici->pici")
+        got = gpu_message(S, lambda o: S.spccl_reduce(S.operand(ta), msg_op(S, tmb), msg_op(S, o), n, O.F32, ws),
+                          n, O.F32)
+        exp, _ = O.reduce(O.Operand.array(a), O.Operand.stream(eb), n, O.F32, O.STREAM, O.FMT_PICI)
+        assert_bytes_equal(got, exp, "cfg2 dense+pici->pici")
+        log(f"cfg2 sigma={permille / 1000} reduce pici+pici->pici")
+        got = gpu_message(S, lambda o: S.spccl_reduce(msg_op(S, tma), msg_op(S, tmb), msg_op(S, o), n, O.F32, ws),
+                          n, O.F32)
+        assert_bytes_equal(got, exp, "cfg2 pici+pici->pici")      # same values, same message
+        log(f"cfg2 sigma={permille / 1000} reduce dense+pici->dense")
+        out = torch.empty(n, dtype=torch.float32, device="cuda")
+        S.spccl_reduce(S.operand(ta), msg_op(S, tmb), S.operand(out), n, O.F32, ws)
+        expd = O.decompress(exp, n, O.F32)
+        assert np.array_equal(to_host_bits(out), bits(expd))
+    assert S.spccl_read_status(ws) == 0
+
+
+def _trace_check(gtr, otr):
+    assert len(gtr) == len(otr)
+    for g, o in zip(gtr, otr):
+        assert g == (o.step, o.rank, o.fmt, o.measured, o.bytes, o.nnz, o.sigma), (g, o)
+
+
+def test_config3_reduce_scatter(S):
+    P, n = W.CFG3_P, W.CFG3_N
+    m = n // P
+    log("cfg3 generate")
+    sends = [W.cfg3_rank(r) for r in range(P)]
+    ts = [to_dev(x) for x in sends]
+    outs = [torch.empty(m, dtype=torch.float32, device="cuda") for _ in range(P)]
+    scratch = torch.empty(S.spccl_vr_scratch_bytes(P, m, O.F32), dtype=torch.uint8, device="cuda")
+    log("cfg3 gpu reduce-scatter")
+    gtr = S.spccl_vr_reduce_scatter(ts, outs, scratch)
+    log("cfg3 oracle reduce-scatter")
+    exp, otr = O.ring_reduce_scatter(sends)
+    _trace_check(gtr, otr)
+    assert all(g[2] == 1 for g in gtr)            # 0.99^8 > 0.6: never switches to dense
+    for r in range(P):
+        assert np.array_equal(to_host_bits(outs[r]), bits(exp[r])), f"rank {r}"
+
+
+def test_config4_all_gather(S):
+    P, n = W.CFG4_P, W.CFG4_N
+    log("cfg4 generate")
+    parts = [W.cfg4_rank(r) for r in range(P)]
+    ts = [to_dev(x) for x in parts]
+    outs = [torch.empty(P * n, dtype=torch.bfloat16, device="cuda") for _ in range(P)]
+    scratch = torch.empty(S.spccl_vr_scratch_bytes(P, n, O.BF16), dtype=torch.uint8, device="cuda")
+    log("cfg4 gpu all-gather")
+    gtr = S.spccl_vr_all_gather(ts, outs, scratch)
+    log("cfg4 oracle all-gather")
+    exp, otr = O.ring_all_gather(parts)
+    _trace_check(gtr, otr)
+    assert all(g[4] == O.pici_bytes(n, O.BF16, W.nnz_for(n, 999)) for g in gtr)
+    for r in range(P):
+        assert np.array_equal(to_host_bits(outs[r]), bits(exp[r])), f"rank {r}"
+
+
+@pytest.mark.timeout(900)
+def test_config5_all_reduce(S):
+    P = W.CFG5_P
+    log("cfg5 plan")
+    plan = W.cfg5_plan()
+    n = plan.n
+    m = n // P
+    sends = []
+    for r in range(P):
+        log(f"cfg5 generate rank {r}")
+        sends.append(W.cfg5_rank(plan, r))
+    result = {}
+
+    def run_oracle():
+        result["oracle"] = O.ring_all_reduce(sends)
+
+    th = threading.Thread(target=run_oracle)     # the C oracle releases the GIL
+    th.start()
+    ts = [to_dev(x) for x in sends]
+    outs = [torch.empty(n, dtype=torch.float32, device="cuda") for _ in range(P)]
+    scratch = torch.empty(S.spccl_vr_scratch_bytes(P, m, O.F32), dtype=torch.uint8, device="cuda")
+    log("cfg5 gpu all-reduce")
+    gtr = S.spccl_vr_all_reduce(ts, outs, scratch)
+    torch.cuda.synchronize()
+    del ts
+    log("cfg5 waiting for the oracle")
+    while th.is_alive():
+        th.join(timeout=20)
+        log("cfg5 oracle still running")
+    exp, otr = result["oracle"]
+    _trace_check(gtr, otr)
+    fmts_rs = {g[2] for g in gtr[:P * (P - 1)]}
+    fmts_ag = [g[2] for g in gtr[P * (P - 1):]]
+    log(f"cfg5 formats: reduce-scatter {sorted(fmts_rs)}, all-gather {fmts_ag}")
+    for r in range(P):
+        got = to_host_bits(outs[r])
+        assert np.array_equal(got, bits(exp[r])), f"rank {r}: {first_diff(got, bits(exp[r]))}"
+        outs[r] = None
