@@ -102,12 +102,19 @@ uint64_t spccl_pici_bytes(uint64_t n, int32_t dtype, uint64_t nnz);
 uint64_t spccl_stream_bound(uint64_t n, int32_t dtype);
 
 /* Workspace for messages of up to n elements: a 256-byte control block
- * (the sticky device status) and one 64-bit look-back word per partition of
- * the single-pass scan.  Zero-fill it once before first use (or clear it with
+ * (the sticky device status), one 64-bit look-back word per partition of
+ * 16384 elements, and one worst-case slot of compacted values per partition
+ * (n elements' worth).  With the slots, Pici-producing calls run as two
+ * passes that never wait while holding input data (count and park values,
+ * then resolve offsets by look-back and move); a workspace of only
+ * spccl_workspace_min_bytes selects the single-pass kernels, which resolve
+ * offsets by decoupled look-back while holding their tiles.  Outputs are
+ * identical.  Zero-fill a workspace once before first use (or clear it with
  * spccl_workspace_init); look-back words are tagged with a per-launch epoch,
  * so it needs no clearing between calls.  One workspace must not be used by
  * two calls in flight at once. */
 uint64_t spccl_workspace_bytes(uint64_t n, int32_t dtype);
+uint64_t spccl_workspace_min_bytes(uint64_t n, int32_t dtype);
 
 /* Zero-fill a workspace with a fill kernel on `stream` (no memset nodes). */
 spccl_status_t spccl_workspace_init(void* ws, uint64_t ws_bytes, void* stream);

@@ -33,6 +33,7 @@ NNZ_UNKNOWN = (1 << 64) - 1
 
 # every symbol the C header declares
 EXPORTS = ("spccl_num_tiles", "spccl_pici_bytes", "spccl_stream_bound", "spccl_workspace_bytes",
+           "spccl_workspace_min_bytes",
            "spccl_workspace_init", "spccl_compress", "spccl_decompress", "spccl_encode_dense",
            "spccl_reduce", "spccl_gather_expand", "spccl_copy_message", "spccl_read_header",
            "spccl_read_status", "spccl_status_string", "spccl_vr_scratch_bytes",
@@ -68,6 +69,7 @@ _sigs = {
     "spccl_pici_bytes": (_u64, [_u64, _i32, _u64]),
     "spccl_stream_bound": (_u64, [_u64, _i32]),
     "spccl_workspace_bytes": (_u64, [_u64, _i32]),
+    "spccl_workspace_min_bytes": (_u64, [_u64, _i32]),
     "spccl_workspace_init": (_i32, [_vp, _u64, _vp]),
     "spccl_compress": (_i32, [_vp, _u64, _i32, _vp, _u64, _vp, _u64, _vp]),
     "spccl_decompress": (_i32, [_vp, _u64, _vp, _u64, _i32, _vp, _u64, _vp]),
@@ -144,6 +146,10 @@ def spccl_stream_bound(n: int, dtype: int) -> int:
 
 def spccl_workspace_bytes(n: int, dtype: int) -> int:
     return _lib.spccl_workspace_bytes(n, dtype)
+
+
+def spccl_workspace_min_bytes(n: int, dtype: int) -> int:
+    return _lib.spccl_workspace_min_bytes(n, dtype)
 
 
 def spccl_vr_scratch_bytes(P: int, msg_elems: int, dtype: int) -> int:
@@ -257,7 +263,10 @@ def alloc_stream(n: int, dtype: int, device="cuda") -> torch.Tensor:
     return torch.empty(spccl_stream_bound(n, dtype), dtype=torch.uint8, device=device)
 
 
-def alloc_workspace(n: int, dtype: int, device="cuda", stream=None) -> torch.Tensor:
-    ws = torch.empty(max(spccl_workspace_bytes(n, dtype), 256), dtype=torch.uint8, device=device)
+def alloc_workspace(n: int, dtype: int, device="cuda", stream=None, minimal: bool = False) -> torch.Tensor:
+    """A zeroed workspace for messages of up to n elements.  minimal=True
+    sizes it for the single-pass kernels only (no per-partition slots)."""
+    need = spccl_workspace_min_bytes(n, dtype) if minimal else spccl_workspace_bytes(n, dtype)
+    ws = torch.empty(max(need, 256), dtype=torch.uint8, device=device)
     spccl_workspace_init(ws, stream)
     return ws

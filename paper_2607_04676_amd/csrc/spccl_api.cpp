@@ -28,6 +28,7 @@ using namespace spccl;
 namespace {
 
 inline bool dtype_ok(int32_t dt) { return dt == kF32 || dt == kBF16; }
+inline uint64_t slots_offset(uint64_t n) { return (kWsFlagsOffset + 8ull * num_parts(n) + 255ull) & ~255ull; }
 
 // Every single-pass launch tags its look-back words with a fresh epoch, so a
 // workspace never needs clearing between calls: words left by earlier calls
@@ -93,9 +94,13 @@ uint64_t spccl_stream_bound(uint64_t n, int32_t dtype) {
     return p > d ? p : d;
 }
 
-uint64_t spccl_workspace_bytes(uint64_t n, int32_t dtype) {
+uint64_t spccl_workspace_min_bytes(uint64_t n, int32_t dtype) {
     (void)dtype;
     return kWsFlagsOffset + 8ull * num_parts(n);
+}
+
+uint64_t spccl_workspace_bytes(uint64_t n, int32_t dtype) {
+    return slots_offset(n) + num_parts(n) * kPartElems * elem_bytes(dtype);
 }
 
 spccl_status_t spccl_workspace_init(void* ws, uint64_t ws_bytes, void* stream) {
@@ -110,9 +115,10 @@ spccl_status_t spccl_compress(const void* dense, uint64_t n, int32_t dtype, void
     if ((n && (!dense || !aligned_elem(dense, dtype))) || !out || !aligned16(out)) return SPCCL_ERR_INVALID_ARG;
     if (out_bytes < spccl_stream_bound(n, dtype)) return SPCCL_ERR_CAPACITY;
     if (overlaps(dense, n * elem_bytes(dtype), out, out_bytes)) return SPCCL_ERR_INVALID_ARG;
-    spccl_status_t st = check_ws(ws, ws_bytes, spccl_workspace_bytes(n, dtype));
+    spccl_status_t st = check_ws(ws, ws_bytes, spccl_workspace_min_bytes(n, dtype));
     if (st != SPCCL_OK) return st;
     PiciSinkArgs g{};
+    g.slots = ws_bytes >= spccl_workspace_bytes(n, dtype) ? static_cast<uint8_t*>(ws) + slots_offset(n) : nullptr;
     g.a = DevOperand{nullptr, static_cast<const uint8_t*>(dense), n * elem_bytes(dtype)};
     g.out = static_cast<uint8_t*>(out);
     g.n = n;
@@ -205,9 +211,10 @@ spccl_status_t spccl_reduce(spccl_operand_t a, spccl_operand_t b, spccl_operand_
     WsCtrl* ctrl = static_cast<WsCtrl*>(ws);
     if (out.kind == SPCCL_STREAM && out.fmt == SPCCL_FMT_PICI) {
         if (out.bytes < spccl_stream_bound(n, dtype)) return SPCCL_ERR_CAPACITY;
-        st = check_ws(ws, ws_bytes, spccl_workspace_bytes(n, dtype));
+        st = check_ws(ws, ws_bytes, spccl_workspace_min_bytes(n, dtype));
         if (st != SPCCL_OK) return st;
         PiciSinkArgs g{};
+        g.slots = ws_bytes >= spccl_workspace_bytes(n, dtype) ? static_cast<uint8_t*>(ws) + slots_offset(n) : nullptr;
         g.a = sa.dev;
         g.b = sb.dev;
         g.out = static_cast<uint8_t*>(out.ptr);

@@ -14,7 +14,7 @@ constexpr uint32_t kWave = 64;                  // CDNA wavefront
 constexpr uint32_t kWavesPerBlock = 4;          // one tile per wave
 constexpr uint32_t kBlockThreads = kWave * kWavesPerBlock;
 constexpr uint32_t kTilesPerPart = kWavesPerBlock;   // look-back partition = one block
-constexpr uint32_t kStageBytes = 8192;          // LDS staging per wave
+constexpr uint32_t kStageBytes = 4096;          // LDS staging per wave
 
 constexpr int kFmtDense = 0, kFmtPici = 1;
 constexpr int kKindArray = 0, kKindStream = 1;
@@ -40,6 +40,8 @@ __host__ __device__ inline uint64_t pici_bytes(uint64_t n, int dtype, uint64_t n
 __host__ __device__ inline uint64_t dense_msg_bytes(uint64_t n, int dtype) {
     return kHeaderBytes + n * elem_bytes(dtype);
 }
+constexpr uint64_t kPartElems = (uint64_t)kTilesPerPart * kTileElems;
+
 __host__ __device__ inline uint64_t num_parts(uint64_t n) {
     uint64_t T = num_tiles(n);
     uint64_t p = (T + kTilesPerPart - 1) / kTilesPerPart;
@@ -65,6 +67,7 @@ struct PiciSinkArgs {
     uint32_t epoch;        // tags this call's look-back words (unique per launch)
     WsCtrl* ctrl;
     uint64_t* flags;
+    uint8_t* slots;        // two-pass mode: one worst-case slot of compacted values per partition
 };
 
 struct DenseSinkArgs {

@@ -25,6 +25,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+
 #include "spccl_internal.h"
 #include "../../include/spccl.h"
 
@@ -32,15 +33,21 @@ namespace spccl {
 
 // ---------------------------------------------------------------------------
 // element types
+// cap: values one wave can stage in LDS.  A tile with more nonzeros is
+// staged in groups of group_cols columns (at most 64 values each).
 struct F32 {
     using raw = uint32_t;
     static constexpr int dtype = kF32;
-    static constexpr uint32_t cap = kStageBytes / 4;   // staged values per wave
+    static constexpr uint32_t cap = kStageBytes / 4;
+    static constexpr uint32_t group_cols = cap / 64;
+    static constexpr int groups = 64 / group_cols;
 };
 struct BF16 {
     using raw = uint16_t;
     static constexpr int dtype = kBF16;
     static constexpr uint32_t cap = kStageBytes / 2;
+    static constexpr uint32_t group_cols = cap / 64 < 64 ? cap / 64 : 64;
+    static constexpr int groups = 64 / group_cols;
 };
 
 // a (+) b on raw bits: absent (0) is the identity, otherwise add.
@@ -193,15 +200,14 @@ __device__ __forceinline__ void fetch_pici(const uint8_t* msg, uint64_t nnz, uin
         }
         wave_lds_sync();
     } else {
-        // more values than the stage holds (fp32 tile more than half full):
-        // columns 0-31 first, then columns 32-63 (each at most 2048 values).
+        // more values than the stage holds: one group of columns at a time
 #pragma unroll
-        for (int h = 0; h < 2; h++) {
-            const uint32_t lo = __shfl(colpref, 32 * h, 64);
-            const uint32_t hi = h == 0 ? __shfl(colpref, 32, 64) : cnt;
+        for (int h = 0; h < E::groups; h++) {
+            const uint32_t lo = __shfl(colpref, E::group_cols * h, 64);
+            const uint32_t hi = h == E::groups - 1 ? cnt : __shfl(colpref, E::group_cols * (h + 1), 64);
             for (uint32_t i = l; i < hi - lo; i += 64) stage[i] = src[lo + i];
             wave_lds_sync();
-            const bool mine = (l >> 5) == (uint32_t)h;
+            const bool mine = l / E::group_cols == (uint32_t)h;
             uint32_t rank = colpref - lo;
 #pragma unroll
             for (int r = 0; r < 64; r++) {
@@ -233,52 +239,64 @@ __device__ __forceinline__ void publish(uint64_t* flags, uint32_t p, uint32_t ep
     __hip_atomic_store(&flags[p], f, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// Exclusive prefix of partition p, computed by one whole wave.  Each round
-// inspects the 256 partitions before the window start: lane l reads the
-// words of partitions start-4l .. start-4l-3, so position k = 4l + j counts
-// back from the nearest predecessor (k = 0).  The round ends at the nearest
-// inclusive prefix; every position in front of it must have published (an
-// aggregate) or the round is retried.  Words of another call carry another
-// epoch and count as unpublished.  Partitions before 0 act as a prefix of 0.
-__device__ uint32_t lookback(const uint64_t* flags, uint32_t p, uint32_t epoch30, WsCtrl* ctrl) {
+// Look-back words of the 64*J partitions before `start`, position k = 64j + l
+// (counting back from the nearest predecessor) in word j of lane l, so each
+// of the J loads reads 64 consecutive words (512 contiguous bytes).
+// Partitions before 0 decode as an inclusive prefix of 0.
+template <int J>
+struct Window {
+    uint64_t f[J];
+};
+
+template <int J>
+__device__ __forceinline__ Window<J> load_window(const uint64_t* flags, int64_t start) {
+    const uint32_t l = lane_id();
+    Window<J> w;
+#pragma unroll
+    for (int j = 0; j < J; j++) {
+        const int64_t q = start - 64 * (int64_t)j - (int64_t)l;
+        w.f[j] = 0;
+        if (q >= 0) w.f[j] = __hip_atomic_load(&flags[q], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    return w;
+}
+
+// Exclusive prefix of partition p, computed by one whole wave, starting from
+// an already loaded first window.  Each round ends at the nearest inclusive
+// prefix; every position in front of it must have published (an aggregate)
+// or the round is retried.  Words of another call carry another epoch and
+// count as unpublished.
+template <int J>
+__device__ uint32_t lookback_from(const uint64_t* flags, uint32_t p, uint32_t epoch30, WsCtrl* ctrl, Window<J> win) {
+    constexpr int64_t span = 64 * J;
     const uint32_t l = lane_id();
     uint32_t excl = 0;
     int64_t start = (int64_t)p - 1;
     uint32_t spins = 0;
     while (start >= 0) {
-        uint32_t state[4], val[4];
+        uint32_t state[J], val[J];
 #pragma unroll
-        for (int j = 0; j < 4; j++) {
-            const int64_t q = start - 4 * (int64_t)l - j;
-            state[j] = kFlagPrefix;
-            val[j] = 0;
-            if (q >= 0) {
-                const uint64_t f = __hip_atomic_load(&flags[q], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                state[j] = ((uint32_t)(f >> 34) == epoch30) ? (uint32_t)(f >> 32) & 3u : 0u;
-                val[j] = (uint32_t)f;
-            }
+        for (int j = 0; j < J; j++) {
+            const int64_t q = start - 64 * (int64_t)j - (int64_t)l;
+            const uint64_t f = win.f[j];
+            state[j] = q < 0 ? kFlagPrefix : (((uint32_t)(f >> 34) == epoch30) ? (uint32_t)(f >> 32) & 3u : 0u);
+            val[j] = q < 0 ? 0u : (uint32_t)f;
         }
-        // nearest inclusive prefix: smallest k = 4 * lane + j with state P
-        uint32_t kP = 256;
-        uint64_t mX[4];
-#pragma unroll
-        for (int j = 0; j < 4; j++) {
-            const uint64_t mP = __ballot(state[j] == kFlagPrefix);
-            mX[j] = __ballot(state[j] == 0u);
-            if (mP) {
-                const uint32_t k = 4u * (uint32_t)__builtin_ctzll(mP) + (uint32_t)j;
-                kP = k < kP ? k : kP;
-            }
-        }
-        // every position k < kP must have published
+        // nearest inclusive prefix: the first word j holding one, then its lowest lane
+        int jP = J;
+        uint32_t lP = 64;
         bool wait = false;
 #pragma unroll
-        for (int j = 0; j < 4; j++) {
-            if (kP > (uint32_t)j) {
-                const uint32_t lanes = (kP - (uint32_t)j + 3u) / 4u;        // lanes l with 4l + j < kP
-                const uint64_t below = lanes >= 64 ? ~0ull : ((1ull << lanes) - 1ull);
-                wait = wait || (mX[j] & below) != 0ull;
-            }
+        for (int j = J - 1; j >= 0; j--) {
+            const uint64_t mP = __ballot(state[j] == kFlagPrefix);
+            if (mP) { jP = j; lP = (uint32_t)__builtin_ctzll(mP); }
+        }
+        // every position in front of it must have published
+#pragma unroll
+        for (int j = 0; j < J; j++) {
+            const uint64_t mX = __ballot(state[j] == 0u);
+            const uint64_t front = j < jP ? ~0ull : (j == jP ? ((1ull << lP) - 1ull) : 0ull);
+            wait = wait || (mX & front) != 0ull;
         }
         if (wait) {
             if (++spins > kSpinLimit) {
@@ -286,22 +304,34 @@ __device__ uint32_t lookback(const uint64_t* flags, uint32_t p, uint32_t epoch30
                 break;
             }
             __builtin_amdgcn_s_sleep(1);
+            win = load_window<J>(flags, start);
             continue;
         }
         uint32_t mine = 0;
 #pragma unroll
-        for (int j = 0; j < 4; j++) mine += (4u * l + (uint32_t)j <= kP) ? val[j] : 0u;
+        for (int j = 0; j < J; j++) mine += (j < jP || (j == jP && l <= lP)) ? val[j] : 0u;
         excl += wave_sum(mine);
-        if (kP < 256) break;
-        start -= 256;
+        if (jP < J) break;
+        start -= span;
+        if (start >= 0) win = load_window<J>(flags, start);
     }
     return excl;
+}
+
+__device__ __forceinline__ uint32_t lookback(const uint64_t* flags, uint32_t p, uint32_t epoch30, WsCtrl* ctrl) {
+    return lookback_from<4>(flags, p, epoch30, ctrl, load_window<4>(flags, (int64_t)p - 1));
 }
 
 // ---------------------------------------------------------------------------
 // Pici sink: out = Pici(srcA (+) srcB), single pass.
 
-template <class E, int SA, int SB>
+// Deferred = false: single pass; each partition resolves its global offset by
+// decoupled look-back and writes its values in place.
+// Deferred = true: first of two passes; each partition publishes its
+// aggregate, writes B and the tile offsets relative to the partition, and
+// parks its compacted values in its own worst-case slot of the workspace,
+// never waiting on another block; k_place then moves each slot into place.
+template <class E, int SA, int SB, bool Deferred>
 __global__ void __launch_bounds__(kBlockThreads) k_to_pici(PiciSinkArgs g) {
     using raw = typename E::raw;
     __shared__ raw stage_all[kWavesPerBlock][E::cap];
@@ -367,7 +397,8 @@ __global__ void __launch_bounds__(kBlockThreads) k_to_pici(PiciSinkArgs g) {
         tile_excl += k < wave ? ck : 0u;
         agg += ck;
     }
-    if (threadIdx.x == 0) publish(g.flags, p, epoch30, p == 0 ? kFlagPrefix : kFlagAggregate, agg);
+    if (threadIdx.x == 0)
+        publish(g.flags, p, epoch30, (p == 0 && !Deferred) ? kFlagPrefix : kFlagAggregate, agg);
 
     const bool single = tilecnt <= E::cap;
     if (has_tile && single) {
@@ -375,6 +406,30 @@ __global__ void __launch_bounds__(kBlockThreads) k_to_pici(PiciSinkArgs g) {
 #pragma unroll
         for (int r = 0; r < 64; r++)
             if ((w >> r) & 1ull) { stage[rank] = (raw)v[r]; rank++; }
+    }
+    if constexpr (Deferred) {
+        if (!has_tile) return;
+        raw* slot = reinterpret_cast<raw*>(g.slots) + (uint64_t)p * kPartElems + tile_excl;
+        if (single) {
+            wave_lds_sync();
+            for (uint32_t i = l; i < tilecnt; i += 64) slot[i] = stage[i];
+        } else {
+#pragma unroll
+            for (int h = 0; h < E::groups; h++) {
+                const uint32_t lo = __shfl(colpref, E::group_cols * h, 64);
+                const uint32_t hi = h == E::groups - 1 ? tilecnt : __shfl(colpref, E::group_cols * (h + 1), 64);
+                const bool mine = l / E::group_cols == (uint32_t)h;
+                uint32_t rank = colpref - lo;
+#pragma unroll
+                for (int r = 0; r < 64; r++)
+                    if (mine && ((w >> r) & 1ull)) { stage[rank] = (raw)v[r]; rank++; }
+                wave_lds_sync();
+                for (uint32_t i = l; i < hi - lo; i += 64) slot[lo + i] = stage[i];
+                wave_lds_sync();
+            }
+        }
+        if (l == 0) reinterpret_cast<uint32_t*>(g.out + off_I(g.n))[t] = tile_excl;   // k_place adds the prefix
+        return;
     }
     if (wave == 0) {
         const uint32_t prefix = p == 0 ? 0u : lookback(g.flags, p, epoch30, g.ctrl);
@@ -395,10 +450,10 @@ __global__ void __launch_bounds__(kBlockThreads) k_to_pici(PiciSinkArgs g) {
             for (uint32_t i = l; i < tilecnt; i += 64) dst[i] = stage[i];
         } else {
 #pragma unroll
-            for (int h = 0; h < 2; h++) {
-                const uint32_t lo = __shfl(colpref, 32 * h, 64);
-                const uint32_t hi = h == 0 ? __shfl(colpref, 32, 64) : tilecnt;
-                const bool mine = (l >> 5) == (uint32_t)h;
+            for (int h = 0; h < E::groups; h++) {
+                const uint32_t lo = __shfl(colpref, E::group_cols * h, 64);
+                const uint32_t hi = h == E::groups - 1 ? tilecnt : __shfl(colpref, E::group_cols * (h + 1), 64);
+                const bool mine = l / E::group_cols == (uint32_t)h;
                 uint32_t rank = colpref - lo;
 #pragma unroll
                 for (int r = 0; r < 64; r++)
@@ -417,6 +472,134 @@ __global__ void __launch_bounds__(kBlockThreads) k_to_pici(PiciSinkArgs g) {
         I[g.T] = (uint32_t)nnz;
         for (uint64_t b = oI + 4 * (g.T + 1); b < oA; b += 4) *reinterpret_cast<uint32_t*>(g.out + b) = 0u;
         write_header(g.out, kFmtPici, E::dtype, g.n, nnz, oI, oA, oA + nnz * sizeof(raw));
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Second pass of the two-pass Pici sink.  Every aggregate is final when this
+// kernel starts (the first pass has completed), so a block can add up its
+// predecessors' aggregates itself with ordinary cached loads -- no waiting on
+// other blocks.  That costs p loads for partition p, so past
+// kPlaceDirectMax partitions the blocks fall back to decoupled look-back
+// (which only waits for inclusive prefixes published by this pass).
+constexpr uint32_t kPlaceDirectMax = 16384;
+
+constexpr uint32_t kPlacePer = 8;          // partitions placed by one block (2 per wave)
+
+template <class E>
+__global__ void __launch_bounds__(kBlockThreads) k_place(PiciSinkArgs g) {
+    using raw = typename E::raw;
+    constexpr int J = 8;
+    constexpr uint32_t kEarly = 8;          // slot values per lane read before the offsets are known
+    __shared__ uint32_t s_base, s_part[kWavesPerBlock], s_agg[kPlacePer], s_prefix[kPlacePer];
+    const uint32_t wave = threadIdx.x >> 6, l = lane_id();
+    const uint32_t p0 = blockIdx.x * kPlacePer;
+    const uint32_t epoch30 = g.epoch & 0x3FFFFFFFu;
+    const uint64_t oI = off_I(g.n), oA = off_A(g.n);
+    uint32_t* I = reinterpret_cast<uint32_t*>(g.out + oI);
+    // independent of the offsets, so issued first: the first slot values of
+    // this wave's two partitions (a slot always has kPartElems of room) and
+    // their partition-relative tile offsets
+    raw early[2][kEarly];
+    uint32_t tile_rel[2] = {0u, 0u};
+#pragma unroll
+    for (uint32_t h = 0; h < 2; h++) {
+        const uint32_t p = p0 + wave + kWavesPerBlock * h;
+        const raw* slot = reinterpret_cast<const raw*>(g.slots) + (uint64_t)p * kPartElems;
+#pragma unroll
+        for (uint32_t u = 0; u < kEarly; u++) early[h][u] = p < g.nparts ? slot[l + 64 * u] : (raw)0;
+        const uint64_t t = (uint64_t)p * kTilesPerPart + l;
+        if (p < g.nparts && l < kTilesPerPart && t < g.T) tile_rel[h] = I[t];
+    }
+    if (threadIdx.x < kPlacePer) {
+        const uint32_t p = p0 + threadIdx.x;
+        uint32_t agg = 0;
+        if (p < g.nparts) {
+            const uint64_t f = g.flags[p];
+            agg = (uint32_t)f;
+            if ((uint32_t)(f >> 34) != epoch30 || agg > kPartElems) {   // the first pass did not run
+                set_status(g.ctrl, SPCCL_ERR_WORKSPACE);
+                agg = 0;
+            }
+        }
+        s_agg[threadIdx.x] = agg;
+    }
+    if (g.nparts <= kPlaceDirectMax) {
+        // sum of all earlier aggregates: two words per 16-byte load, eight
+        // independent loads in flight per thread
+        uint32_t part = 0;
+        const uint4* f2 = reinterpret_cast<const uint4*>(g.flags);
+        const uint32_t pairs = p0 / 2;                          // p0 is even
+        for (uint32_t q0 = threadIdx.x; q0 < pairs; q0 += 8 * kBlockThreads) {
+            uint4 x[8];
+#pragma unroll
+            for (int u = 0; u < 8; u++) {
+                const uint32_t q = q0 + u * kBlockThreads;
+                x[u] = q < pairs ? f2[q] : uint4{0, 0, 0, 0};
+            }
+#pragma unroll
+            for (int u = 0; u < 8; u++) part += x[u].x + x[u].z;    // low words hold the aggregates
+        }
+        part = wave_sum(part);
+        if (l == 0) s_part[wave] = part;
+        __syncthreads();
+        if (threadIdx.x == 0) {
+            uint32_t base = 0;
+            for (uint32_t k = 0; k < kWavesPerBlock; k++) base += s_part[k];
+            s_base = base;
+        }
+    } else if (wave == 0) {
+        Window<J> win{};
+        if (p0 != 0) win = load_window<J>(g.flags, (int64_t)p0 - 1);
+        const uint32_t base = p0 == 0 ? 0u : lookback_from<J>(g.flags, p0, epoch30, g.ctrl, win);
+        if (l == 0) {
+            uint32_t tot = 0;
+            for (uint32_t k = 0; k < kPlacePer; k++) tot += s_agg[k];
+            const uint32_t last = (g.nparts - p0 < kPlacePer ? g.nparts - p0 : kPlacePer) - 1;
+            publish(g.flags, p0 + last, epoch30, kFlagPrefix, base + tot);
+            s_base = base;
+        }
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        uint32_t run = s_base;
+        for (uint32_t k = 0; k < kPlacePer; k++) { s_prefix[k] = run; run += s_agg[k]; }
+    }
+    __syncthreads();
+#pragma unroll
+    for (uint32_t h = 0; h < 2; h++) {
+        const uint32_t k = wave + kWavesPerBlock * h;
+        const uint32_t p = p0 + k;
+        if (p >= g.nparts) continue;
+        const uint32_t prefix = s_prefix[k], agg = s_agg[k];
+        const raw* slot = reinterpret_cast<const raw*>(g.slots) + (uint64_t)p * kPartElems;
+        raw* dst = reinterpret_cast<raw*>(g.out + oA) + prefix;
+#pragma unroll
+        for (uint32_t u = 0; u < kEarly; u++) {
+            const uint32_t i = l + 64 * u;
+            if (i < agg) dst[i] = early[h][u];
+        }
+        for (uint32_t i0 = l + 64 * kEarly; i0 < agg; i0 += 64 * 8) {
+            raw x[8];
+#pragma unroll
+            for (int u = 0; u < 8; u++) {
+                const uint32_t i = i0 + 64 * u;
+                x[u] = i < agg ? slot[i] : (raw)0;
+            }
+#pragma unroll
+            for (int u = 0; u < 8; u++) {
+                const uint32_t i = i0 + 64 * u;
+                if (i < agg) dst[i] = x[u];
+            }
+        }
+        const uint64_t t = (uint64_t)p * kTilesPerPart + l;
+        if (l < kTilesPerPart && t < g.T) I[t] = tile_rel[h] + prefix;
+        if (p == g.nparts - 1 && l == 0) {
+            const uint64_t nnz = (uint64_t)prefix + agg;
+            I[g.T] = (uint32_t)nnz;
+            for (uint64_t b = oI + 4 * (g.T + 1); b < oA; b += 4) *reinterpret_cast<uint32_t*>(g.out + b) = 0u;
+            write_header(g.out, kFmtPici, E::dtype, g.n, nnz, oI, oA, oA + nnz * sizeof(raw));
+        }
     }
 }
 
@@ -631,7 +814,22 @@ inline uint32_t stream_grid(uint64_t work_items, uint32_t per_block, uint32_t ca
 template <class E>
 spccl_status_t launch_to_pici(int sa, int sb, const PiciSinkArgs& g, hipStream_t st) {
     dim3 grid(g.nparts), block(kBlockThreads);
-#define SPCCL_TO_PICI(A, B) hipLaunchKernelGGL((k_to_pici<E, A, B>), grid, block, 0, st, g)
+    if (g.slots) {
+#define SPCCL_TO_PICI2(A, B) hipLaunchKernelGGL((k_to_pici<E, A, B, true>), grid, block, 0, st, g)
+        if (sa == SRC_DENSE && sb == SRC_NONE) SPCCL_TO_PICI2(SRC_DENSE, SRC_NONE);
+        else if (sa == SRC_DENSE && sb == SRC_DENSE) SPCCL_TO_PICI2(SRC_DENSE, SRC_DENSE);
+        else if (sa == SRC_DENSE && sb == SRC_PICI) SPCCL_TO_PICI2(SRC_DENSE, SRC_PICI);
+        else if (sa == SRC_PICI && sb == SRC_DENSE) SPCCL_TO_PICI2(SRC_PICI, SRC_DENSE);
+        else if (sa == SRC_PICI && sb == SRC_PICI) SPCCL_TO_PICI2(SRC_PICI, SRC_PICI);
+        else return SPCCL_ERR_INVALID_ARG;
+#undef SPCCL_TO_PICI2
+        spccl_status_t st1 = launch_status();
+        if (st1 != SPCCL_OK) return st1;
+        dim3 pgrid((g.nparts + kPlacePer - 1) / kPlacePer);
+        hipLaunchKernelGGL(k_place<E>, pgrid, block, 0, st, g);
+        return launch_status();
+    }
+#define SPCCL_TO_PICI(A, B) hipLaunchKernelGGL((k_to_pici<E, A, B, false>), grid, block, 0, st, g)
     if (sa == SRC_DENSE && sb == SRC_NONE) SPCCL_TO_PICI(SRC_DENSE, SRC_NONE);
     else if (sa == SRC_DENSE && sb == SRC_DENSE) SPCCL_TO_PICI(SRC_DENSE, SRC_DENSE);
     else if (sa == SRC_DENSE && sb == SRC_PICI) SPCCL_TO_PICI(SRC_DENSE, SRC_PICI);

@@ -37,9 +37,15 @@ def make(n, nnz, seed, dtype, specials=False):
     return a
 
 
-def gpu_compress(S, a, ws=None):
+@pytest.fixture(params=["two_pass", "single_pass"])
+def ws_mode(request):
+    """Full workspace (count + place passes) or minimal (single-pass look-back)."""
+    return request.param
+
+
+def gpu_compress(S, a, ws=None, minimal=False):
     n, dt = a.size, dt_code(W.BF16 if a.dtype == np.uint16 else W.F32)
-    ws = S.alloc_workspace(max(n, 1), dt) if ws is None else ws
+    ws = S.alloc_workspace(max(n, 1), dt, minimal=minimal) if ws is None else ws
     out = S.alloc_stream(n, dt)
     out.fill_(0xA5)                  # junk: every byte up to total_bytes must be written
     S.spccl_compress(to_dev(a), out, ws)
@@ -54,25 +60,25 @@ FRACS = [0.0, 0.01, 0.1, 0.5, 0.7, 1.0]
 
 @pytest.mark.parametrize("dtype", [W.F32, W.BF16])
 @pytest.mark.parametrize("n", SIZES)
-def test_compress_matches_oracle(S, n, dtype):
+def test_compress_matches_oracle(S, n, dtype, ws_mode):
     for k, frac in enumerate(FRACS):
         nnz = int(round(frac * n))
-        log(f"compress n={n} dtype={dtype} nnz={nnz}")
+        log(f"compress n={n} dtype={dtype} nnz={nnz} {ws_mode}")
         a = make(n, nnz, [20, n, k], dtype, specials=frac > 0)
         exp, exp_nnz = O.compress(a)
-        out = gpu_compress(S, a)
+        out = gpu_compress(S, a, minimal=ws_mode == "single_pass")
         got = out[:exp.size].cpu().numpy()
         assert_bytes_equal(got, exp, f"compress n={n} frac={frac}")
         assert S.spccl_read_header(out)["total_bytes"] == exp.size
 
 
 @pytest.mark.parametrize("dtype", [W.F32, W.BF16])
-def test_compress_dense_tiles_two_pass(S, dtype):
+def test_compress_dense_tiles_two_pass(S, dtype, ws_mode):
     """Tiles with more than 2048 nonzeros (fp32) take the two-half staging path."""
     n = 9 * 4096 + 5
     a = make(n, n - 300, [21], dtype, specials=True)       # nearly all present
     exp, _ = O.compress(a)
-    got = gpu_compress(S, a)[:exp.size].cpu().numpy()
+    got = gpu_compress(S, a, minimal=ws_mode == "single_pass")[:exp.size].cpu().numpy()
     assert_bytes_equal(got, exp, "dense tiles")
 
 
@@ -138,13 +144,13 @@ def _gpu_operand(S, x, kind, keep):
 @pytest.mark.parametrize("n", [4097, 9 * 4096 + 333])
 @pytest.mark.parametrize("ka", KINDS)
 @pytest.mark.parametrize("kb", KINDS)
-def test_reduce_all_operand_kinds(S, n, dtype, ka, kb):
+def test_reduce_all_operand_kinds(S, n, dtype, ka, kb, ws_mode):
     dt = dt_code(dtype)
     for k, (fa, fb) in enumerate([(0.02, 0.03), (0.5, 0.4), (0.9, 0.95)]):
         a = make(n, int(fa * n), [23, n, k, 0], dtype, specials=True)
         b = make(n, int(fb * n), [23, n, k, 1], dtype)
         _cancel(a, b, 25, k)
-        ws = S.alloc_workspace(n, dt)
+        ws = S.alloc_workspace(n, dt, minimal=ws_mode == "single_pass")
         keep = []
         ga, gb = _gpu_operand(S, a, ka, keep), _gpu_operand(S, b, kb, keep)
         oa, ob = _oracle_operand(a, ka), _oracle_operand(b, kb)
@@ -217,10 +223,10 @@ def test_copy_message_device_sized(S):
     assert (got[msg.size:] == 0x77).all()          # nothing past total_bytes
 
 
-def test_workspace_reused_across_calls_and_sizes(S):
+def test_workspace_reused_across_calls_and_sizes(S, ws_mode):
     """The look-back words carry a per-call epoch: one workspace serves many
     consecutive calls of different sizes without being cleared."""
-    ws = S.alloc_workspace(64 * 4096, O.F32)
+    ws = S.alloc_workspace(64 * 4096, O.F32, minimal=ws_mode == "single_pass")
     for k, n in enumerate([64 * 4096, 4096, 13 * 4096 + 1, 64 * 4096, 0, 5, 40 * 4096 + 9, 64 * 4096]):
         log(f"ws reuse call {k} n={n}")
         a = make(n, n // 7, [27, k], W.F32)

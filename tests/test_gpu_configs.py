@@ -73,11 +73,12 @@ def test_config1(S):
 
 
 @pytest.mark.parametrize("permille", W.CFG2_PERMILLE)
-def test_config2_codec_and_reduce(S, permille):
+@pytest.mark.parametrize("minimal", [False, True], ids=["two_pass", "single_pass"])
+def test_config2_codec_and_reduce(S, permille, minimal):
     n = W.CFG2_N
-    log(f"cfg2 sigma={permille / 1000} generate")
+    log(f"cfg2 sigma={permille / 1000} generate (minimal workspace: {minimal})")
     a = W.cfg2(permille, 0)
-    ws = S.alloc_workspace(n, O.F32)
+    ws = S.alloc_workspace(n, O.F32, minimal=minimal)
     ta = to_dev(a)
     log(f"cfg2 sigma={permille / 1000} compress")
     ma = gpu_message(S, lambda o: S.spccl_compress(ta, o, ws), n, O.F32)
