@@ -52,19 +52,23 @@ SINGLE_KERNEL_OPS = {
 }
 
 
-def traffic_for(kernel: str):
-    """HBM bytes per launch measured with rocprofv3 FETCH_SIZE / WRITE_SIZE
-    counters (profiles/traffic.json), provided they were taken on the current
-    kernel source; otherwise null."""
+def kernel_source_digest() -> str:
     import hashlib
+    src = os.path.join(ROOT, "paper_2607_04676_amd", "csrc", "spccl_kernels.hip")
+    return hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
+
+
+def traffic_for(op: str):
+    """HBM bytes per launch of an op's kernel from rocprofv3 FETCH_SIZE and
+    WRITE_SIZE counters (profiles/traffic.json, already scaled by the plain
+    copy calibration), provided they were taken on the current kernel source;
+    otherwise null."""
     path = os.path.join(ROOT, "profiles", "traffic.json")
     if not os.path.exists(path):
         return None
     rec = json.load(open(path))
-    src = os.path.join(ROOT, "paper_2607_04676_amd", "csrc", "spccl_kernels.hip")
-    digest = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
-    ent = rec.get("kernels", {}).get(kernel)
-    if ent is None or rec.get("kernel_source_sha256_16") != digest:
+    ent = rec.get("ops", {}).get(op)
+    if ent is None or rec.get("kernel_source_sha256_16") != kernel_source_digest():
         return None
     return ent.get("hbm_bytes_per_launch")
 
@@ -301,7 +305,7 @@ def main():
     dgbs = alg[dom] / (per[dom] / 1e3) / 1e9
     roof = {"bound": "hbm", "kernel": SINGLE_KERNEL_OPS[dom], "op": dom, "achieved": round(dgbs, 1),
             "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(dgbs / HBM_PEAK_GBS, 4),
-            "traffic": traffic_for(SINGLE_KERNEL_OPS[dom]),
+            "traffic": traffic_for(dom),
             "algorithmic_bytes_per_launch": alg[dom], "avg_launch_ms": round(per[dom], 5)}
     sweep = {}
     del R

@@ -490,7 +490,7 @@ template <class E>
 __global__ void __launch_bounds__(kBlockThreads) k_place(PiciSinkArgs g) {
     using raw = typename E::raw;
     constexpr int J = 8;
-    constexpr uint32_t kEarly = 8;          // slot values per lane read before the offsets are known
+    constexpr uint32_t kEarly = 4;          // slot values per lane read before the offsets are known
     __shared__ uint32_t s_base, s_part[kWavesPerBlock], s_agg[kPlacePer], s_prefix[kPlacePer];
     const uint32_t wave = threadIdx.x >> 6, l = lane_id();
     const uint32_t p0 = blockIdx.x * kPlacePer;
