@@ -142,26 +142,36 @@ __device__ __forceinline__ void write_header(uint8_t* out, int fmt, int dtype, u
 // ---------------------------------------------------------------------------
 // tile sources: fill v[r] = element (row r, column lane) of tile t
 
-// Dense source.  first: v = x; otherwise v = v (+) x.
+// Dense source, column `lane` of tile t, read through a buffer resource that
+// covers only the tile's elements below n: the hardware range check returns 0
+// for the rest, so full and partial tiles take one branch-free path.  The tile
+// index is wave-uniform, so the resource sits in scalar registers and each row
+// is an immediate (plus scalar) offset from one lane offset.
+// first: v = x; otherwise v = v (+) x.
+constexpr int kBufferWord3 = 0x00020000;   // gfx9 raw buffer: 32-bit data format, no swizzle
+
 template <class E, bool First>
 __device__ __forceinline__ void fetch_dense(const uint8_t* base, uint64_t t, uint64_t n, uint32_t (&v)[64]) {
     using raw = typename E::raw;
-    const uint32_t l = lane_id();
-    const raw* col = reinterpret_cast<const raw*>(base) + t * kTileElems + l;
-    const uint64_t rem = n - t * kTileElems;
-    uint32_t x[64];
-    if (rem >= kTileElems) {
+    constexpr uint32_t rowb = 64 * sizeof(raw);             // bytes per tile row
+    constexpr int per = 4096 / rowb;                         // rows per 4 KiB immediate range
+    t = ((uint64_t)__builtin_amdgcn_readfirstlane((uint32_t)(t >> 32)) << 32) |
+        __builtin_amdgcn_readfirstlane((uint32_t)t);
+    const uint64_t start = t * kTileElems;
+    const uint64_t rem = start < n ? n - start : 0;
+    const uint32_t bytes = (uint32_t)((rem < kTileElems ? rem : kTileElems) * sizeof(raw));
+    const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint8_t*>(base) + (rem ? start : 0) * sizeof(raw), (short)0, (int)bytes, kBufferWord3);
+    const uint32_t lo = lane_id() * (uint32_t)sizeof(raw);
 #pragma unroll
-        for (int r = 0; r < 64; r++) x[r] = col[64 * r];
-    } else {
-#pragma unroll
-        for (int r = 0; r < 64; r++) {
-            x[r] = 0u;
-            if ((uint64_t)(64 * r + l) < rem) x[r] = col[64 * r];
-        }
+    for (int r = 0; r < 64; r++) {
+        uint32_t x;
+        if constexpr (sizeof(raw) == 4)
+            x = __builtin_amdgcn_raw_buffer_load_b32(rs, lo + rowb * (r % per), 4096 * (r / per), 0);
+        else
+            x = __builtin_amdgcn_raw_buffer_load_b16(rs, lo + rowb * (r % per), 4096 * (r / per), 0);
+        v[r] = First ? x : oplus(E{}, v[r], x);
     }
-#pragma unroll
-    for (int r = 0; r < 64; r++) v[r] = First ? x[r] : oplus(E{}, v[r], x[r]);
 }
 
 // Pici source: B words, I offsets and A values of tile t of a checked
@@ -169,25 +179,47 @@ __device__ __forceinline__ void fetch_dense(const uint8_t* base, uint64_t t, uin
 // reads of the tile's A range), then each lane walks its column word.  A
 // tile whose counts disagree with I (or overrun nnz) is treated as empty and
 // flagged.  first: v = x; otherwise v = v (+) x.
-template <class E, bool First>
-__device__ __forceinline__ void fetch_pici(const uint8_t* msg, uint64_t nnz, uint64_t t, uint64_t n,
-                                           typename E::raw* stage, WsCtrl* ctrl, uint32_t (&v)[64]) {
-    using raw = typename E::raw;
-    const uint32_t l = lane_id();
-    const uint64_t T = num_tiles(n);
+struct PiciMeta {
+    uint64_t w;        // this lane's column word (as loaded)
+    uint32_t base;     // I[t]
+    uint32_t next;     // I[t + 1]
+};
+
+template <class E>
+__device__ __forceinline__ PiciMeta load_pici_meta(const uint8_t* msg, uint64_t t, uint64_t n) {
     const uint64_t* B = reinterpret_cast<const uint64_t*>(msg + kHeaderBytes);
     const uint32_t* I = reinterpret_cast<const uint32_t*>(msg + off_I(n));
-    const raw* A = reinterpret_cast<const raw*>(msg + off_A(n));
-    uint64_t w = B[t * 64 + l];
-    const uint32_t base = I[t], next = I[t + 1];
+    return PiciMeta{B[t * 64 + lane_id()], I[t], I[t + 1]};
+}
+
+// Column counts and prefixes of a tile from its metadata, checked against
+// I and nnz; a tile that disagrees is flagged and reads as empty.
+struct PiciCols {
+    uint64_t w;
+    uint32_t colpref, cnt, base;
+};
+
+__device__ __forceinline__ PiciCols pici_columns(PiciMeta m, uint64_t nnz, uint64_t t, uint64_t n, WsCtrl* ctrl) {
+    const uint64_t T = num_tiles(n);
+    uint64_t w = m.w;
     uint32_t c = (uint32_t)__popcll(w);
     uint32_t colpref = wave_excl_scan(c);
     uint32_t cnt = __shfl(colpref + c, 63, 64);
-    if ((uint64_t)base + cnt > nnz || base + cnt != next || (t + 1 == T && (uint64_t)next != nnz)) {
-        if (l == 0) set_status(ctrl, SPCCL_ERR_CORRUPT_STREAM);
-        w = 0; c = 0; colpref = 0; cnt = 0;
+    if ((uint64_t)m.base + cnt > nnz || m.base + cnt != m.next || (t + 1 == T && (uint64_t)m.next != nnz)) {
+        if (lane_id() == 0) set_status(ctrl, SPCCL_ERR_CORRUPT_STREAM);
+        w = 0; colpref = 0; cnt = 0;
     }
-    const raw* src = A + base;
+    return PiciCols{w, colpref, cnt, m.base};
+}
+
+template <class E, bool First>
+__device__ __forceinline__ void expand_pici(PiciCols pc, const uint8_t* msg, uint64_t n, typename E::raw* stage,
+                                            uint32_t (&v)[64]) {
+    using raw = typename E::raw;
+    const uint32_t l = lane_id();
+    const uint64_t w = pc.w;
+    const uint32_t colpref = pc.colpref, cnt = pc.cnt;
+    const raw* src = reinterpret_cast<const raw*>(msg + off_A(n)) + pc.base;
     if (cnt <= E::cap) {
         for (uint32_t i = l; i < cnt; i += 64) stage[i] = src[i];
         wave_lds_sync();
@@ -219,6 +251,79 @@ __device__ __forceinline__ void fetch_pici(const uint8_t* msg, uint64_t nnz, uin
             wave_lds_sync();
         }
     }
+}
+
+template <class E, bool First>
+__device__ __forceinline__ void fetch_pici(const uint8_t* msg, uint64_t nnz, uint64_t t, uint64_t n,
+                                           typename E::raw* stage, WsCtrl* ctrl, uint32_t (&v)[64]) {
+    const PiciMeta m = load_pici_meta<E>(msg, t, n);
+    expand_pici<E, First>(pici_columns(m, nnz, t, n, ctrl), msg, n, stage, v);
+}
+
+// A dense operand and a Pici operand of the same tile, v = dense (+) pici
+// (the operation is symmetric bit for bit).  The Pici operand's metadata is
+// requested first and the dense tile right behind it, so its dependent value
+// read overlaps the dense tile's round trip instead of following it.
+template <class E>
+__device__ __forceinline__ void fetch_dense_and_pici(const uint8_t* dense, const uint8_t* msg, uint64_t nnz,
+                                                     uint64_t t, uint64_t n, typename E::raw* stage, WsCtrl* ctrl,
+                                                     uint32_t (&v)[64]) {
+    const PiciMeta m = load_pici_meta<E>(msg, t, n);
+    asm volatile("" ::: "memory");
+    fetch_dense<E, true>(dense, t, n, v);
+    expand_pici<E, false>(pici_columns(m, nnz, t, n, ctrl), msg, n, stage, v);
+}
+
+// Pici (+) Pici for one tile with work proportional to its nonzeros: both
+// operands' value ranges are staged in LDS (in[0..na) and in[na..na+nb)),
+// exact cancellations are found among the rows both hold, then each lane
+// merges its two column runs in row order into out[] at the output column
+// prefix.  Returns this lane's output column word.  Rows of a partial last
+// tile that lie past n are ignored.
+template <class E>
+__device__ __forceinline__ uint64_t merge_pici_pici(PiciCols ca, PiciCols cb, const uint8_t* amsg,
+                                                    const uint8_t* bmsg, uint64_t n, uint64_t rem,
+                                                    typename E::raw* in, typename E::raw* out) {
+    using raw = typename E::raw;
+    const uint32_t l = lane_id();
+    const raw* srca = reinterpret_cast<const raw*>(amsg + off_A(n)) + ca.base;
+    const raw* srcb = reinterpret_cast<const raw*>(bmsg + off_A(n)) + cb.base;
+    for (uint32_t i = l; i < ca.cnt; i += 64) in[i] = srca[i];
+    for (uint32_t i = l; i < cb.cnt; i += 64) in[ca.cnt + i] = srcb[i];
+    wave_lds_sync();
+    uint64_t valid = ~0ull;
+    if (rem < kTileElems) {
+        const uint64_t rows = l < rem ? (rem - l + 63) / 64 : 0;   // rows r with 64 r + l < rem
+        valid = rows >= 64 ? ~0ull : ((1ull << rows) - 1ull);
+    }
+    const uint64_t wa = ca.w, wb = cb.w, U = (wa | wb) & valid;
+    uint64_t ov = wa & wb & valid, cancel = 0;
+    while (__any(ov != 0ull)) {
+        if (ov) {
+            const uint32_t r = (uint32_t)__builtin_ctzll(ov);
+            ov &= ov - 1ull;
+            const uint64_t below = (1ull << r) - 1ull;
+            const uint32_t xa = in[ca.colpref + (uint32_t)__popcll(wa & below)];
+            const uint32_t xb = in[ca.cnt + cb.colpref + (uint32_t)__popcll(wb & below)];
+            if (oplus(E{}, xa, xb) == 0u) cancel |= 1ull << r;
+        }
+    }
+    const uint64_t wo = U & ~cancel;
+    uint32_t k = wave_excl_scan((uint32_t)__popcll(wo));
+    uint64_t todo = U;
+    uint32_t ia = ca.colpref, ib = ca.cnt + cb.colpref;
+    while (__any(todo != 0ull)) {
+        if (todo) {
+            const uint32_t r = (uint32_t)__builtin_ctzll(todo);
+            todo &= todo - 1ull;
+            uint32_t xa = 0, xb = 0;
+            if ((wa >> r) & 1ull) { xa = in[ia]; ia++; }
+            if ((wb >> r) & 1ull) { xb = in[ib]; ib++; }
+            if ((wo >> r) & 1ull) { out[k] = (raw)oplus(E{}, xa, xb); k++; }
+        }
+    }
+    wave_lds_sync();
+    return wo;
 }
 
 template <class E, int S, bool First>
@@ -334,13 +439,15 @@ __device__ __forceinline__ uint32_t lookback(const uint64_t* flags, uint32_t p, 
 template <class E, int SA, int SB, bool Deferred>
 __global__ void __launch_bounds__(kBlockThreads) k_to_pici(PiciSinkArgs g) {
     using raw = typename E::raw;
-    __shared__ raw stage_all[kWavesPerBlock][E::cap];
+    constexpr bool kPP = SA == SRC_PICI && SB == SRC_PICI;
+    __shared__ raw stage_all[kWavesPerBlock][kPP ? 2 * E::cap : E::cap];
     __shared__ uint32_t s_cnt[kWavesPerBlock];
     __shared__ uint32_t s_prefix, s_ok;
     __shared__ uint64_t s_nnz_a, s_nnz_b;
 
     const uint32_t wave = threadIdx.x >> 6, l = lane_id();
     raw* stage = stage_all[wave];
+    raw* ostage = stage;      // where the tile's compacted values end up
     if (threadIdx.x == 0) {
         bool ok = true;
         uint64_t na = 0, nb = 0;
@@ -371,17 +478,39 @@ __global__ void __launch_bounds__(kBlockThreads) k_to_pici(PiciSinkArgs g) {
     uint32_t v[64];
     uint64_t w = 0;
     uint32_t c = 0;
+    bool staged = false;      // values already compacted into ostage (sparse Pici (+) Pici)
     if (has_tile) {
-        fetch<E, SA, true>(g.a, s_nnz_a, t, g.n, stage, g.ctrl, v);
-        if constexpr (SB != SRC_NONE) fetch<E, SB, false>(g.b, s_nnz_b, t, g.n, stage, g.ctrl, v);
         const uint64_t rem = g.n - t * kTileElems;
-        if (rem < kTileElems) {
-#pragma unroll
-            for (int r = 0; r < 64; r++)
-                if ((uint64_t)(64 * r + l) >= rem) v[r] = 0;
+        if constexpr (kPP) {
+            const PiciMeta ma = load_pici_meta<E>(g.a.data, t, g.n);
+            const PiciMeta mb = load_pici_meta<E>(g.b.data, t, g.n);
+            const PiciCols ca = pici_columns(ma, s_nnz_a, t, g.n, g.ctrl);
+            const PiciCols cb = pici_columns(mb, s_nnz_b, t, g.n, g.ctrl);
+            if (ca.cnt + cb.cnt <= E::cap) {
+                w = merge_pici_pici<E>(ca, cb, g.a.data, g.b.data, g.n, rem, stage, stage + E::cap);
+                ostage = stage + E::cap;
+                staged = true;
+            } else {
+                expand_pici<E, true>(ca, g.a.data, g.n, stage, v);
+                expand_pici<E, false>(cb, g.b.data, g.n, stage, v);
+            }
+        } else if constexpr (SA == SRC_DENSE && SB == SRC_PICI) {
+            fetch_dense_and_pici<E>(g.a.data, g.b.data, s_nnz_b, t, g.n, stage, g.ctrl, v);
+        } else if constexpr (SA == SRC_PICI && SB == SRC_DENSE) {
+            fetch_dense_and_pici<E>(g.b.data, g.a.data, s_nnz_a, t, g.n, stage, g.ctrl, v);
+        } else {
+            fetch<E, SA, true>(g.a, s_nnz_a, t, g.n, stage, g.ctrl, v);
+            if constexpr (SB != SRC_NONE) fetch<E, SB, false>(g.b, s_nnz_b, t, g.n, stage, g.ctrl, v);
         }
+        if (!staged) {
+            if (rem < kTileElems) {
 #pragma unroll
-        for (int r = 0; r < 64; r++) w |= (uint64_t)(v[r] != 0u) << r;
+                for (int r = 0; r < 64; r++)
+                    if ((uint64_t)(64 * r + l) >= rem) v[r] = 0;
+            }
+#pragma unroll
+            for (int r = 0; r < 64; r++) w |= (uint64_t)(v[r] != 0u) << r;
+        }
         c = (uint32_t)__popcll(w);
         reinterpret_cast<uint64_t*>(g.out + kHeaderBytes)[t * 64 + l] = w;
     }
@@ -401,7 +530,7 @@ __global__ void __launch_bounds__(kBlockThreads) k_to_pici(PiciSinkArgs g) {
         publish(g.flags, p, epoch30, (p == 0 && !Deferred) ? kFlagPrefix : kFlagAggregate, agg);
 
     const bool single = tilecnt <= E::cap;
-    if (has_tile && single) {
+    if (has_tile && single && !staged) {
         uint32_t rank = colpref;
 #pragma unroll
         for (int r = 0; r < 64; r++)
@@ -412,7 +541,7 @@ __global__ void __launch_bounds__(kBlockThreads) k_to_pici(PiciSinkArgs g) {
         raw* slot = reinterpret_cast<raw*>(g.slots) + (uint64_t)p * kPartElems + tile_excl;
         if (single) {
             wave_lds_sync();
-            for (uint32_t i = l; i < tilecnt; i += 64) slot[i] = stage[i];
+            for (uint32_t i = l; i < tilecnt; i += 64) slot[i] = ostage[i];
         } else {
 #pragma unroll
             for (int h = 0; h < E::groups; h++) {
@@ -447,7 +576,7 @@ __global__ void __launch_bounds__(kBlockThreads) k_to_pici(PiciSinkArgs g) {
     if (has_tile) {
         if (single) {
             raw* dst = A + tbase;
-            for (uint32_t i = l; i < tilecnt; i += 64) dst[i] = stage[i];
+            for (uint32_t i = l; i < tilecnt; i += 64) dst[i] = ostage[i];
         } else {
 #pragma unroll
             for (int h = 0; h < E::groups; h++) {
@@ -653,8 +782,14 @@ __global__ void __launch_bounds__(kBlockThreads) k_to_dense(DenseSinkArgs g) {
     const uint64_t t = (uint64_t)blockIdx.x * kWavesPerBlock + wave;
     if (t >= g.T) return;
     uint32_t v[64];
-    fetch<E, SA, true>(g.a, s_nnz_a, t, g.n, stage_all[wave], g.ctrl, v);
-    if constexpr (SB != SRC_NONE) fetch<E, SB, false>(g.b, s_nnz_b, t, g.n, stage_all[wave], g.ctrl, v);
+    if constexpr (SA == SRC_DENSE && SB == SRC_PICI) {
+        fetch_dense_and_pici<E>(g.a.data, g.b.data, s_nnz_b, t, g.n, stage_all[wave], g.ctrl, v);
+    } else if constexpr (SA == SRC_PICI && SB == SRC_DENSE) {
+        fetch_dense_and_pici<E>(g.b.data, g.a.data, s_nnz_a, t, g.n, stage_all[wave], g.ctrl, v);
+    } else {
+        fetch<E, SA, true>(g.a, s_nnz_a, t, g.n, stage_all[wave], g.ctrl, v);
+        if constexpr (SB != SRC_NONE) fetch<E, SB, false>(g.b, s_nnz_b, t, g.n, stage_all[wave], g.ctrl, v);
+    }
     store_tile<E>(g.out, t, g.n, v);
 }
 
