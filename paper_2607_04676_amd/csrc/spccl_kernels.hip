@@ -274,58 +274,6 @@ __device__ __forceinline__ void fetch_dense_and_pici(const uint8_t* dense, const
     expand_pici<E, false>(pici_columns(m, nnz, t, n, ctrl), msg, n, stage, v);
 }
 
-// Pici (+) Pici for one tile with work proportional to its nonzeros: both
-// operands' value ranges are staged in LDS (in[0..na) and in[na..na+nb)),
-// exact cancellations are found among the rows both hold, then each lane
-// merges its two column runs in row order into out[] at the output column
-// prefix.  Returns this lane's output column word.  Rows of a partial last
-// tile that lie past n are ignored.
-template <class E>
-__device__ __forceinline__ uint64_t merge_pici_pici(PiciCols ca, PiciCols cb, const uint8_t* amsg,
-                                                    const uint8_t* bmsg, uint64_t n, uint64_t rem,
-                                                    typename E::raw* in, typename E::raw* out) {
-    using raw = typename E::raw;
-    const uint32_t l = lane_id();
-    const raw* srca = reinterpret_cast<const raw*>(amsg + off_A(n)) + ca.base;
-    const raw* srcb = reinterpret_cast<const raw*>(bmsg + off_A(n)) + cb.base;
-    for (uint32_t i = l; i < ca.cnt; i += 64) in[i] = srca[i];
-    for (uint32_t i = l; i < cb.cnt; i += 64) in[ca.cnt + i] = srcb[i];
-    wave_lds_sync();
-    uint64_t valid = ~0ull;
-    if (rem < kTileElems) {
-        const uint64_t rows = l < rem ? (rem - l + 63) / 64 : 0;   // rows r with 64 r + l < rem
-        valid = rows >= 64 ? ~0ull : ((1ull << rows) - 1ull);
-    }
-    const uint64_t wa = ca.w, wb = cb.w, U = (wa | wb) & valid;
-    uint64_t ov = wa & wb & valid, cancel = 0;
-    while (__any(ov != 0ull)) {
-        if (ov) {
-            const uint32_t r = (uint32_t)__builtin_ctzll(ov);
-            ov &= ov - 1ull;
-            const uint64_t below = (1ull << r) - 1ull;
-            const uint32_t xa = in[ca.colpref + (uint32_t)__popcll(wa & below)];
-            const uint32_t xb = in[ca.cnt + cb.colpref + (uint32_t)__popcll(wb & below)];
-            if (oplus(E{}, xa, xb) == 0u) cancel |= 1ull << r;
-        }
-    }
-    const uint64_t wo = U & ~cancel;
-    uint32_t k = wave_excl_scan((uint32_t)__popcll(wo));
-    uint64_t todo = U;
-    uint32_t ia = ca.colpref, ib = ca.cnt + cb.colpref;
-    while (__any(todo != 0ull)) {
-        if (todo) {
-            const uint32_t r = (uint32_t)__builtin_ctzll(todo);
-            todo &= todo - 1ull;
-            uint32_t xa = 0, xb = 0;
-            if ((wa >> r) & 1ull) { xa = in[ia]; ia++; }
-            if ((wb >> r) & 1ull) { xb = in[ib]; ib++; }
-            if ((wo >> r) & 1ull) { out[k] = (raw)oplus(E{}, xa, xb); k++; }
-        }
-    }
-    wave_lds_sync();
-    return wo;
-}
-
 template <class E, int S, bool First>
 __device__ __forceinline__ void fetch(const DevOperand& op, uint64_t nnz, uint64_t t, uint64_t n,
                                       typename E::raw* stage, WsCtrl* ctrl, uint32_t (&v)[64]) {
@@ -439,8 +387,7 @@ __device__ __forceinline__ uint32_t lookback(const uint64_t* flags, uint32_t p, 
 template <class E, int SA, int SB, bool Deferred>
 __global__ void __launch_bounds__(kBlockThreads) k_to_pici(PiciSinkArgs g) {
     using raw = typename E::raw;
-    constexpr bool kPP = SA == SRC_PICI && SB == SRC_PICI;
-    __shared__ raw stage_all[kWavesPerBlock][kPP ? 2 * E::cap : E::cap];
+    __shared__ raw stage_all[kWavesPerBlock][E::cap];
     __shared__ uint32_t s_cnt[kWavesPerBlock];
     __shared__ uint32_t s_prefix, s_ok;
     __shared__ uint64_t s_nnz_a, s_nnz_b;
@@ -478,23 +425,10 @@ __global__ void __launch_bounds__(kBlockThreads) k_to_pici(PiciSinkArgs g) {
     uint32_t v[64];
     uint64_t w = 0;
     uint32_t c = 0;
-    bool staged = false;      // values already compacted into ostage (sparse Pici (+) Pici)
+    const bool staged = false;
     if (has_tile) {
         const uint64_t rem = g.n - t * kTileElems;
-        if constexpr (kPP) {
-            const PiciMeta ma = load_pici_meta<E>(g.a.data, t, g.n);
-            const PiciMeta mb = load_pici_meta<E>(g.b.data, t, g.n);
-            const PiciCols ca = pici_columns(ma, s_nnz_a, t, g.n, g.ctrl);
-            const PiciCols cb = pici_columns(mb, s_nnz_b, t, g.n, g.ctrl);
-            if (ca.cnt + cb.cnt <= E::cap) {
-                w = merge_pici_pici<E>(ca, cb, g.a.data, g.b.data, g.n, rem, stage, stage + E::cap);
-                ostage = stage + E::cap;
-                staged = true;
-            } else {
-                expand_pici<E, true>(ca, g.a.data, g.n, stage, v);
-                expand_pici<E, false>(cb, g.b.data, g.n, stage, v);
-            }
-        } else if constexpr (SA == SRC_DENSE && SB == SRC_PICI) {
+        if constexpr (SA == SRC_DENSE && SB == SRC_PICI) {
             fetch_dense_and_pici<E>(g.a.data, g.b.data, s_nnz_b, t, g.n, stage, g.ctrl, v);
         } else if constexpr (SA == SRC_PICI && SB == SRC_DENSE) {
             fetch_dense_and_pici<E>(g.b.data, g.a.data, s_nnz_a, t, g.n, stage, g.ctrl, v);
@@ -605,6 +539,203 @@ __global__ void __launch_bounds__(kBlockThreads) k_to_pici(PiciSinkArgs g) {
 }
 
 // ---------------------------------------------------------------------------
+// ---------------------------------------------------------------------------
+// Pici (+) Pici -> Pici with work proportional to the nonzeros.
+//
+// Phase 1 finds each output column word: the operands' values for a group of
+// columns are staged in LDS (a's run, then b's run), and rows held by both
+// operands are added to find exact cancellations (every row of the group is
+// checked if a staged value is itself zero, which reads as absent).  Once the
+// tile's destination is known (its slot in the two-pass mode, the look-back
+// prefix in the single-pass mode), phase 2 merges each column's two runs in
+// row order into an LDS output stage and copies it out.  A tile whose values
+// fit the stage at once is one group of 64 columns, staged a single time;
+// denser tiles go through in groups of PPGroup::cols columns (at most cap
+// values per group), staged again in phase 2.
+
+template <class E>
+struct PPGroup {
+    static constexpr uint32_t cols = E::cap / 128;            // 2 operands x 64 rows per column
+    static constexpr int count = 64 / cols;
+};
+
+// The value ranges of columns [c0, c1) of both operands into in[]: a's at
+// [0, la), b's at [la, la + lb).  Returns la; zero = some staged value has
+// all-zero bits (uniform over the wave).
+template <class E>
+__device__ __forceinline__ uint32_t pp_stage(const PiciCols& ca, const PiciCols& cb, const typename E::raw* pa,
+                                             const typename E::raw* pb, uint32_t c0, uint32_t c1,
+                                             typename E::raw* in, bool& zero) {
+    const uint32_t l = lane_id();
+    const uint32_t a0 = __shfl(ca.colpref, c0, 64);
+    const uint32_t a1 = c1 == 64 ? ca.cnt : __shfl(ca.colpref, c1, 64);
+    const uint32_t b0 = __shfl(cb.colpref, c0, 64);
+    const uint32_t b1 = c1 == 64 ? cb.cnt : __shfl(cb.colpref, c1, 64);
+    const uint32_t la = a1 - a0, lb = b1 - b0;
+    bool z = false;
+    for (uint32_t i = l; i < la; i += 64) {
+        const typename E::raw x = pa[a0 + i];
+        z |= x == 0;
+        in[i] = x;
+    }
+    for (uint32_t i = l; i < lb; i += 64) {
+        const typename E::raw x = pb[b0 + i];
+        z |= x == 0;
+        in[la + i] = x;
+    }
+    zero = __any(z);
+    wave_lds_sync();
+    return la;
+}
+
+template <class E, bool Deferred>
+__global__ void __launch_bounds__(kBlockThreads) k_pp_to_pici(PiciSinkArgs g) {
+    using raw = typename E::raw;
+    __shared__ raw lds_in[kWavesPerBlock][E::cap];
+    __shared__ raw lds_out[kWavesPerBlock][E::cap];
+    __shared__ uint32_t s_cnt[kWavesPerBlock];
+    __shared__ uint32_t s_prefix, s_ok;
+    __shared__ uint64_t s_nnz_a, s_nnz_b;
+    const uint32_t wave = threadIdx.x >> 6, l = lane_id();
+    raw* in = lds_in[wave];
+    raw* out = lds_out[wave];
+    if (threadIdx.x == 0) {
+        const HeaderView ha = read_header(g.a.hdr, g.a.cap, g.n, E::dtype, kFmtPici);
+        const HeaderView hb = read_header(g.b.hdr, g.b.cap, g.n, E::dtype, kFmtPici);
+        s_ok = ha.ok && hb.ok;
+        s_nnz_a = ha.nnz;
+        s_nnz_b = hb.nnz;
+        if (!s_ok && blockIdx.x == 0) set_status(g.ctrl, SPCCL_ERR_CORRUPT_STREAM);
+    }
+    __syncthreads();
+    if (!s_ok) return;
+
+    const uint32_t p = blockIdx.x;
+    const uint32_t epoch30 = g.epoch & 0x3FFFFFFFu;
+    const uint64_t t = (uint64_t)p * kTilesPerPart + wave;
+    const bool has_tile = t < g.T;
+    const uint64_t oI = off_I(g.n), oA = off_A(g.n);
+    const raw* Aa = reinterpret_cast<const raw*>(g.a.data + oA);
+    const raw* Ab = reinterpret_cast<const raw*>(g.b.data + oA);
+
+    PiciCols ca{0, 0, 0, 0}, cb{0, 0, 0, 0};
+    const raw* pa = Aa;
+    const raw* pb = Ab;
+    uint64_t wa = 0, wb = 0, wo = 0;
+    bool one_group = true;
+    if (has_tile) {
+        const PiciMeta ma = load_pici_meta<E>(g.a.data, t, g.n);
+        const PiciMeta mb = load_pici_meta<E>(g.b.data, t, g.n);
+        ca = pici_columns(ma, s_nnz_a, t, g.n, g.ctrl);
+        cb = pici_columns(mb, s_nnz_b, t, g.n, g.ctrl);
+        const uint64_t rem = g.n - t * kTileElems;
+        uint64_t valid = ~0ull;                               // rows r with 64 r + l < n
+        if (rem < kTileElems) {
+            const uint64_t rows = l < rem ? (rem - l + 63) / 64 : 0;
+            valid = rows >= 64 ? ~0ull : ((1ull << rows) - 1ull);
+        }
+        wa = ca.w & valid;
+        wb = cb.w & valid;
+        one_group = ca.cnt + cb.cnt <= E::cap;
+        const int ngroups = one_group ? 1 : PPGroup<E>::count;
+        const uint32_t gcols = one_group ? 64u : PPGroup<E>::cols;
+        pa = Aa + ca.base;
+        pb = Ab + cb.base;
+        uint64_t cancel = 0;
+        for (int h = 0; h < ngroups; h++) {
+            const uint32_t c0 = gcols * h, c1 = c0 + gcols;
+            const bool mine = l >= c0 && l < c1;
+            bool zero;
+            const uint32_t la = pp_stage<E>(ca, cb, pa, pb, c0, c1, in, zero);
+            const uint32_t ra = ca.colpref - __shfl(ca.colpref, c0, 64);
+            const uint32_t rb = la + cb.colpref - __shfl(cb.colpref, c0, 64);
+            uint64_t chk = mine ? (zero ? (wa | wb) : (wa & wb)) : 0ull;
+            while (__any(chk != 0ull)) {
+                if (chk) {
+                    const uint32_t r = (uint32_t)__builtin_ctzll(chk);
+                    chk &= chk - 1ull;
+                    const uint64_t below = (1ull << r) - 1ull;
+                    const uint32_t xa = ((wa >> r) & 1ull) ? (uint32_t)in[ra + (uint32_t)__popcll(ca.w & below)] : 0u;
+                    const uint32_t xb = ((wb >> r) & 1ull) ? (uint32_t)in[rb + (uint32_t)__popcll(cb.w & below)] : 0u;
+                    if (oplus(E{}, xa, xb) == 0u) cancel |= 1ull << r;
+                }
+            }
+            if (!one_group) wave_lds_sync();                  // the stage is reused by the next group
+        }
+        wo = (wa | wb) & ~cancel;
+        reinterpret_cast<uint64_t*>(g.out + kHeaderBytes)[t * 64 + l] = wo;
+    }
+    const uint32_t colpref = wave_excl_scan((uint32_t)__popcll(wo));
+    const uint32_t tilecnt = __shfl(colpref + (uint32_t)__popcll(wo), 63, 64);
+    if (l == 0) s_cnt[wave] = tilecnt;
+    __syncthreads();
+    uint32_t tile_excl = 0, agg = 0;
+#pragma unroll
+    for (uint32_t k = 0; k < kWavesPerBlock; k++) {
+        const uint32_t ck = s_cnt[k];
+        tile_excl += k < wave ? ck : 0u;
+        agg += ck;
+    }
+    if (threadIdx.x == 0)
+        publish(g.flags, p, epoch30, (p == 0 && !Deferred) ? kFlagPrefix : kFlagAggregate, agg);
+    raw* dst;
+    uint32_t prefix = 0;
+    if constexpr (Deferred) {
+        dst = reinterpret_cast<raw*>(g.slots) + (uint64_t)p * kPartElems + tile_excl;
+    } else {
+        if (wave == 0) {
+            const uint32_t pr = p == 0 ? 0u : lookback(g.flags, p, epoch30, g.ctrl);
+            if (l == 0) {
+                if (p != 0) publish(g.flags, p, epoch30, kFlagPrefix, pr + agg);
+                s_prefix = pr;
+            }
+        }
+        __syncthreads();
+        prefix = s_prefix;
+        dst = reinterpret_cast<raw*>(g.out + oA) + prefix + tile_excl;
+    }
+    if (has_tile) {
+        // phase 2: merge the two runs of each column in row order
+        const int ngroups = one_group ? 1 : PPGroup<E>::count;
+        const uint32_t gcols = one_group ? 64u : PPGroup<E>::cols;
+        for (int h = 0; h < ngroups; h++) {
+            const uint32_t c0 = gcols * h, c1 = c0 + gcols;
+            const bool mine = l >= c0 && l < c1;
+            bool zero;
+            const uint32_t la = one_group ? ca.cnt : pp_stage<E>(ca, cb, pa, pb, c0, c1, in, zero);
+            uint32_t ia = ca.colpref - __shfl(ca.colpref, c0, 64);
+            uint32_t ib = la + cb.colpref - __shfl(cb.colpref, c0, 64);
+            const uint32_t o0 = __shfl(colpref, c0, 64);
+            const uint32_t o1 = c1 == 64 ? tilecnt : __shfl(colpref, c1, 64);
+            uint32_t k = colpref - o0;
+            uint64_t todo = mine ? (wa | wb) : 0ull;
+            while (__any(todo != 0ull)) {
+                if (todo) {
+                    const uint32_t r = (uint32_t)__builtin_ctzll(todo);
+                    todo &= todo - 1ull;
+                    uint32_t xa = 0, xb = 0;
+                    if ((ca.w >> r) & 1ull) { xa = in[ia]; ia++; }
+                    if ((cb.w >> r) & 1ull) { xb = in[ib]; ib++; }
+                    if ((wo >> r) & 1ull) { out[k] = (raw)oplus(E{}, xa, xb); k++; }
+                }
+            }
+            wave_lds_sync();
+            for (uint32_t i = l; i < o1 - o0; i += 64) dst[o0 + i] = out[i];
+            wave_lds_sync();
+        }
+        if (l == 0) reinterpret_cast<uint32_t*>(g.out + oI)[t] = Deferred ? tile_excl : prefix + tile_excl;
+    }
+    if constexpr (!Deferred) {
+        if (p == g.nparts - 1 && threadIdx.x == 0) {
+            const uint64_t nnz = (uint64_t)prefix + agg;
+            uint32_t* I = reinterpret_cast<uint32_t*>(g.out + oI);
+            I[g.T] = (uint32_t)nnz;
+            for (uint64_t b = oI + 4 * (g.T + 1); b < oA; b += 4) *reinterpret_cast<uint32_t*>(g.out + b) = 0u;
+            write_header(g.out, kFmtPici, E::dtype, g.n, nnz, oI, oA, oA + nnz * sizeof(raw));
+        }
+    }
+}
+
 // Second pass of the two-pass Pici sink.  Every aggregate is final when this
 // kernel starts (the first pass has completed), so a block can add up its
 // predecessors' aggregates itself with ordinary cached loads -- no waiting on
@@ -949,13 +1080,24 @@ inline uint32_t stream_grid(uint64_t work_items, uint32_t per_block, uint32_t ca
 template <class E>
 spccl_status_t launch_to_pici(int sa, int sb, const PiciSinkArgs& g, hipStream_t st) {
     dim3 grid(g.nparts), block(kBlockThreads);
+    if (sa == SRC_PICI && sb == SRC_PICI) {
+        if (g.slots) {
+            hipLaunchKernelGGL((k_pp_to_pici<E, true>), grid, block, 0, st, g);
+            spccl_status_t st1 = launch_status();
+            if (st1 != SPCCL_OK) return st1;
+            dim3 pgrid((g.nparts + kPlacePer - 1) / kPlacePer);
+            hipLaunchKernelGGL(k_place<E>, pgrid, block, 0, st, g);
+        } else {
+            hipLaunchKernelGGL((k_pp_to_pici<E, false>), grid, block, 0, st, g);
+        }
+        return launch_status();
+    }
     if (g.slots) {
 #define SPCCL_TO_PICI2(A, B) hipLaunchKernelGGL((k_to_pici<E, A, B, true>), grid, block, 0, st, g)
         if (sa == SRC_DENSE && sb == SRC_NONE) SPCCL_TO_PICI2(SRC_DENSE, SRC_NONE);
         else if (sa == SRC_DENSE && sb == SRC_DENSE) SPCCL_TO_PICI2(SRC_DENSE, SRC_DENSE);
         else if (sa == SRC_DENSE && sb == SRC_PICI) SPCCL_TO_PICI2(SRC_DENSE, SRC_PICI);
         else if (sa == SRC_PICI && sb == SRC_DENSE) SPCCL_TO_PICI2(SRC_PICI, SRC_DENSE);
-        else if (sa == SRC_PICI && sb == SRC_PICI) SPCCL_TO_PICI2(SRC_PICI, SRC_PICI);
         else return SPCCL_ERR_INVALID_ARG;
 #undef SPCCL_TO_PICI2
         spccl_status_t st1 = launch_status();
@@ -969,7 +1111,6 @@ spccl_status_t launch_to_pici(int sa, int sb, const PiciSinkArgs& g, hipStream_t
     else if (sa == SRC_DENSE && sb == SRC_DENSE) SPCCL_TO_PICI(SRC_DENSE, SRC_DENSE);
     else if (sa == SRC_DENSE && sb == SRC_PICI) SPCCL_TO_PICI(SRC_DENSE, SRC_PICI);
     else if (sa == SRC_PICI && sb == SRC_DENSE) SPCCL_TO_PICI(SRC_PICI, SRC_DENSE);
-    else if (sa == SRC_PICI && sb == SRC_PICI) SPCCL_TO_PICI(SRC_PICI, SRC_PICI);
     else return SPCCL_ERR_INVALID_ARG;
 #undef SPCCL_TO_PICI
     return launch_status();
