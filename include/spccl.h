@@ -17,7 +17,8 @@
  *    (a corrupt input message) set a sticky status word in the workspace `ws`
  *    (read it with spccl_read_status).  A message whose header fails its
  *    checks is not read and the call writes no output; a tile whose index
- *    entries disagree with its bit vector is treated as empty.  After any
+ *    entries disagree with its bit vector, or that sets a bit at a position
+ *    >= n, is treated as empty.  After any
  *    device error, re-initialise the workspace before reusing it.
  *  - Element types: SPCCL_F32 (IEEE binary32) and SPCCL_BF16 (bfloat16),
  *    handled as raw bit patterns.  n < 2^32 per message (I is 32-bit).
@@ -122,9 +123,11 @@ spccl_status_t spccl_workspace_init(void* ws, uint64_t ws_bytes, void* stream);
 /* ---- codec (Sec. III-B format, Alg. 1 compression, Sec. III-C) ----------- */
 
 /* Compress dense[0..n) into a Pici message at `out` (capacity out_bytes >=
- * spccl_stream_bound(n, dtype)).  Single pass over the input: bit vector B,
- * tile prefix sums I (decoupled look-back across partitions) and compacted
- * values A, ordered tile -> column -> row.  nnz is in the written header. */
+ * spccl_stream_bound(n, dtype)): bit vector B, tile prefix sums I and
+ * compacted values A, ordered tile -> column -> row.  The input is read
+ * once; partition offsets come from a count pass and a place pass (full
+ * workspace) or from decoupled look-back (minimal workspace).  nnz is in the
+ * written header. */
 spccl_status_t spccl_compress(const void* dense, uint64_t n, int32_t dtype,
                               void* out, uint64_t out_bytes,
                               void* ws, uint64_t ws_bytes, void* stream);

@@ -149,6 +149,11 @@ __device__ __forceinline__ void write_header(uint8_t* out, int fmt, int dtype, u
 // is an immediate (plus scalar) offset from one lane offset.
 // first: v = x; otherwise v = v (+) x.
 constexpr int kBufferWord3 = 0x00020000;   // gfx9 raw buffer: 32-bit data format, no swizzle
+// Cache policy of the dense stream loads: non-temporal.  The dense operand is
+// read once per launch; streaming it past the caches also spares the
+// dirty lines a preceding large write left behind (a normal load would
+// first have to write them back to make room).
+constexpr int kStreamLoad = 2;
 
 template <class E, bool First>
 __device__ __forceinline__ void fetch_dense(const uint8_t* base, uint64_t t, uint64_t n, uint32_t (&v)[64]) {
@@ -167,9 +172,9 @@ __device__ __forceinline__ void fetch_dense(const uint8_t* base, uint64_t t, uin
     for (int r = 0; r < 64; r++) {
         uint32_t x;
         if constexpr (sizeof(raw) == 4)
-            x = __builtin_amdgcn_raw_buffer_load_b32(rs, lo + rowb * (r % per), 4096 * (r / per), 0);
+            x = __builtin_amdgcn_raw_buffer_load_b32(rs, lo + rowb * (r % per), 4096 * (r / per), kStreamLoad);
         else
-            x = __builtin_amdgcn_raw_buffer_load_b16(rs, lo + rowb * (r % per), 4096 * (r / per), 0);
+            x = __builtin_amdgcn_raw_buffer_load_b16(rs, lo + rowb * (r % per), 4096 * (r / per), kStreamLoad);
         v[r] = First ? x : oplus(E{}, v[r], x);
     }
 }
@@ -193,7 +198,9 @@ __device__ __forceinline__ PiciMeta load_pici_meta(const uint8_t* msg, uint64_t 
 }
 
 // Column counts and prefixes of a tile from its metadata, checked against
-// I and nnz; a tile that disagrees is flagged and reads as empty.
+// I and nnz and against the array's end (a bit at a position >= n); a tile
+// that fails is flagged and reads as empty.  So no value beyond n ever leaves
+// a Pici source.
 struct PiciCols {
     uint64_t w;
     uint32_t colpref, cnt, base;
@@ -202,10 +209,18 @@ struct PiciCols {
 __device__ __forceinline__ PiciCols pici_columns(PiciMeta m, uint64_t nnz, uint64_t t, uint64_t n, WsCtrl* ctrl) {
     const uint64_t T = num_tiles(n);
     uint64_t w = m.w;
+    bool beyond = false;
+    const uint64_t rem = n - t * kTileElems;
+    if (rem < kTileElems) {                                   // last, partial tile: rows r with 64 r + l < n
+        const uint32_t l = lane_id();
+        const uint32_t rows = l < rem ? (uint32_t)((rem - l + 63) / 64) : 0u;
+        const uint64_t valid = rows >= 64 ? ~0ull : ((1ull << rows) - 1ull);
+        beyond = __any((w & ~valid) != 0ull);
+    }
     uint32_t c = (uint32_t)__popcll(w);
     uint32_t colpref = wave_excl_scan(c);
     uint32_t cnt = __shfl(colpref + c, 63, 64);
-    if ((uint64_t)m.base + cnt > nnz || m.base + cnt != m.next || (t + 1 == T && (uint64_t)m.next != nnz)) {
+    if (beyond || (uint64_t)m.base + cnt > nnz || m.base + cnt != m.next || (t + 1 == T && (uint64_t)m.next != nnz)) {
         if (lane_id() == 0) set_status(ctrl, SPCCL_ERR_CORRUPT_STREAM);
         w = 0; colpref = 0; cnt = 0;
     }
@@ -394,7 +409,6 @@ __global__ void __launch_bounds__(kBlockThreads) k_to_pici(PiciSinkArgs g) {
 
     const uint32_t wave = threadIdx.x >> 6, l = lane_id();
     raw* stage = stage_all[wave];
-    raw* ostage = stage;      // where the tile's compacted values end up
     if (threadIdx.x == 0) {
         bool ok = true;
         uint64_t na = 0, nb = 0;
@@ -425,9 +439,7 @@ __global__ void __launch_bounds__(kBlockThreads) k_to_pici(PiciSinkArgs g) {
     uint32_t v[64];
     uint64_t w = 0;
     uint32_t c = 0;
-    const bool staged = false;
     if (has_tile) {
-        const uint64_t rem = g.n - t * kTileElems;
         if constexpr (SA == SRC_DENSE && SB == SRC_PICI) {
             fetch_dense_and_pici<E>(g.a.data, g.b.data, s_nnz_b, t, g.n, stage, g.ctrl, v);
         } else if constexpr (SA == SRC_PICI && SB == SRC_DENSE) {
@@ -436,15 +448,10 @@ __global__ void __launch_bounds__(kBlockThreads) k_to_pici(PiciSinkArgs g) {
             fetch<E, SA, true>(g.a, s_nnz_a, t, g.n, stage, g.ctrl, v);
             if constexpr (SB != SRC_NONE) fetch<E, SB, false>(g.b, s_nnz_b, t, g.n, stage, g.ctrl, v);
         }
-        if (!staged) {
-            if (rem < kTileElems) {
+        // every source reads as zero at positions >= n (bounded buffer loads,
+        // Pici tiles checked against the array's end)
 #pragma unroll
-                for (int r = 0; r < 64; r++)
-                    if ((uint64_t)(64 * r + l) >= rem) v[r] = 0;
-            }
-#pragma unroll
-            for (int r = 0; r < 64; r++) w |= (uint64_t)(v[r] != 0u) << r;
-        }
+        for (int r = 0; r < 64; r++) w |= (uint64_t)(v[r] != 0u) << r;
         c = (uint32_t)__popcll(w);
         reinterpret_cast<uint64_t*>(g.out + kHeaderBytes)[t * 64 + l] = w;
     }
@@ -464,7 +471,7 @@ __global__ void __launch_bounds__(kBlockThreads) k_to_pici(PiciSinkArgs g) {
         publish(g.flags, p, epoch30, (p == 0 && !Deferred) ? kFlagPrefix : kFlagAggregate, agg);
 
     const bool single = tilecnt <= E::cap;
-    if (has_tile && single && !staged) {
+    if (has_tile && single) {
         uint32_t rank = colpref;
 #pragma unroll
         for (int r = 0; r < 64; r++)
@@ -475,7 +482,7 @@ __global__ void __launch_bounds__(kBlockThreads) k_to_pici(PiciSinkArgs g) {
         raw* slot = reinterpret_cast<raw*>(g.slots) + (uint64_t)p * kPartElems + tile_excl;
         if (single) {
             wave_lds_sync();
-            for (uint32_t i = l; i < tilecnt; i += 64) slot[i] = ostage[i];
+            for (uint32_t i = l; i < tilecnt; i += 64) slot[i] = stage[i];
         } else {
 #pragma unroll
             for (int h = 0; h < E::groups; h++) {
@@ -510,7 +517,7 @@ __global__ void __launch_bounds__(kBlockThreads) k_to_pici(PiciSinkArgs g) {
     if (has_tile) {
         if (single) {
             raw* dst = A + tbase;
-            for (uint32_t i = l; i < tilecnt; i += 64) dst[i] = ostage[i];
+            for (uint32_t i = l; i < tilecnt; i += 64) dst[i] = stage[i];
         } else {
 #pragma unroll
             for (int h = 0; h < E::groups; h++) {
@@ -628,14 +635,8 @@ __global__ void __launch_bounds__(kBlockThreads) k_pp_to_pici(PiciSinkArgs g) {
         const PiciMeta mb = load_pici_meta<E>(g.b.data, t, g.n);
         ca = pici_columns(ma, s_nnz_a, t, g.n, g.ctrl);
         cb = pici_columns(mb, s_nnz_b, t, g.n, g.ctrl);
-        const uint64_t rem = g.n - t * kTileElems;
-        uint64_t valid = ~0ull;                               // rows r with 64 r + l < n
-        if (rem < kTileElems) {
-            const uint64_t rows = l < rem ? (rem - l + 63) / 64 : 0;
-            valid = rows >= 64 ? ~0ull : ((1ull << rows) - 1ull);
-        }
-        wa = ca.w & valid;
-        wb = cb.w & valid;
+        wa = ca.w;                                            // no bits at positions >= n (checked)
+        wb = cb.w;
         one_group = ca.cnt + cb.cnt <= E::cap;
         const int ngroups = one_group ? 1 : PPGroup<E>::count;
         const uint32_t gcols = one_group ? 64u : PPGroup<E>::cols;

@@ -262,6 +262,43 @@ def test_corrupt_messages_flagged(S):
     assert_bytes_equal(got, msg, "after errors")
 
 
+def test_bit_beyond_n_flagged(S):
+    """A message whose counts agree with I but which sets a bit at a position
+    >= n is corrupt (the oracle's decoder rejects it): every kernel that reads
+    it flags the status and treats that tile as empty."""
+    n = 3 * 4096 - 100                       # last tile: row 63 of every column lies beyond n
+    a = make(n, 500, [31], W.F32)
+    msg = O.compress(a)[0]
+    t = 2
+    B = msg[48:48 + 8 * 64 * 3].view(np.uint64).copy()
+    col = next(c for c in range(64) if B[64 * t + c] != 0)
+    w = int(B[64 * t + col])
+    low = w & -w
+    w = (w & ~low) | (1 << 63)               # same count: one bit moved past the end
+    bad = msg.copy()
+    bad[48 + 8 * (64 * t + col):48 + 8 * (64 * t + col) + 8] = np.array([w], dtype=np.uint64).view(np.uint8)
+    with pytest.raises(O.OracleError):
+        O.decompress(bad, n, O.F32)
+    ws = S.alloc_workspace(n, O.F32)
+    tb = torch.from_numpy(bad).cuda()
+    out = torch.empty(n, dtype=torch.float32, device="cuda")
+    log("bit beyond n: decompress")
+    S.spccl_decompress(tb, out, ws)
+    assert S.spccl_read_status(ws, clear=True) == 4
+    log("bit beyond n: pici + pici")
+    so = S.alloc_stream(n, O.F32)
+    good = torch.from_numpy(msg).cuda()
+    S.spccl_reduce(S.operand(tb, S.SPCCL_STREAM, S.SPCCL_FMT_PICI), S.operand(good, S.SPCCL_STREAM, S.SPCCL_FMT_PICI),
+                   S.operand(so, S.SPCCL_STREAM, S.SPCCL_FMT_PICI), n, O.F32, ws)
+    assert S.spccl_read_status(ws, clear=True) == 4
+    log("bit beyond n: dense + pici")
+    S.spccl_reduce(S.operand(to_dev(a)), S.operand(tb, S.SPCCL_STREAM, S.SPCCL_FMT_PICI), S.operand(out), n, O.F32,
+                   ws)
+    assert S.spccl_read_status(ws, clear=True) == 4
+    got = gpu_compress(S, a, ws)[:msg.size].cpu().numpy()
+    assert_bytes_equal(got, msg, "after errors")
+
+
 def test_host_errors_launch_nothing(S):
     n = 4096
     ws = S.alloc_workspace(n, O.F32)
