@@ -204,6 +204,7 @@ __device__ __forceinline__ PiciMeta load_pici_meta(const uint8_t* msg, uint64_t 
 struct PiciCols {
     uint64_t w;
     uint32_t colpref, cnt, base;
+    bool ok;           // the tile passed its checks (else it reads as empty)
 };
 
 __device__ __forceinline__ PiciCols pici_columns(PiciMeta m, uint64_t nnz, uint64_t t, uint64_t n, WsCtrl* ctrl) {
@@ -220,11 +221,13 @@ __device__ __forceinline__ PiciCols pici_columns(PiciMeta m, uint64_t nnz, uint6
     uint32_t c = (uint32_t)__popcll(w);
     uint32_t colpref = wave_excl_scan(c);
     uint32_t cnt = __shfl(colpref + c, 63, 64);
-    if (beyond || (uint64_t)m.base + cnt > nnz || m.base + cnt != m.next || (t + 1 == T && (uint64_t)m.next != nnz)) {
+    const bool bad =
+        beyond || (uint64_t)m.base + cnt > nnz || m.base + cnt != m.next || (t + 1 == T && (uint64_t)m.next != nnz);
+    if (bad) {
         if (lane_id() == 0) set_status(ctrl, SPCCL_ERR_CORRUPT_STREAM);
         w = 0; colpref = 0; cnt = 0;
     }
-    return PiciCols{w, colpref, cnt, m.base};
+    return PiciCols{w, colpref, cnt, m.base, !bad};
 }
 
 template <class E, bool First>
@@ -625,7 +628,7 @@ __global__ void __launch_bounds__(kBlockThreads) k_pp_to_pici(PiciSinkArgs g) {
     const raw* Aa = reinterpret_cast<const raw*>(g.a.data + oA);
     const raw* Ab = reinterpret_cast<const raw*>(g.b.data + oA);
 
-    PiciCols ca{0, 0, 0, 0}, cb{0, 0, 0, 0};
+    PiciCols ca{0, 0, 0, 0, true}, cb{0, 0, 0, 0, true};
     const raw* pa = Aa;
     const raw* pb = Ab;
     uint64_t wa = 0, wb = 0, wo = 0;
@@ -927,13 +930,75 @@ __global__ void __launch_bounds__(kBlockThreads) k_to_dense(DenseSinkArgs g) {
 
 // Expansion of P parts (all-gather receive side and decompress): the format
 // of each message is read from its header on the device.
+//
+// Each wave expands K consecutive tiles of one part and issues its reads
+// before its first store: the K tiles' column words and offsets, then, in one
+// go, the values of as many leading tiles as fit kChunkVals (their value
+// ranges are contiguous), held in registers and staged in LDS; then it writes
+// the dense tiles.  On this architecture one counter tracks both loads and
+// stores, so a read that has to be waited for after a store also waits for
+// that store; with the reads in front the writes stream and the read latency
+// is paid once per K tiles.  Tiles that do not fit are expanded one at a
+// time (stage their values, then write), and a tile holding more than
+// kChunkVals values reads its column runs per lane, 16 rows at a time.
+constexpr uint32_t kChunkVals = 1024;
+constexpr int kChunkSlots = kChunkVals / 64;
+
+// Rows [r0, r0 + 16) of dense tile t (bounded buffer loads, zero past n).
 template <class E>
+__device__ __forceinline__ void fetch_dense_rows16(const uint8_t* base, uint64_t t, uint64_t n, int r0,
+                                                   uint32_t (&v)[16]) {
+    using raw = typename E::raw;
+    constexpr uint32_t rowb = 64 * sizeof(raw);
+    t = ((uint64_t)__builtin_amdgcn_readfirstlane((uint32_t)(t >> 32)) << 32) |
+        __builtin_amdgcn_readfirstlane((uint32_t)t);
+    const uint64_t start = t * kTileElems;
+    const uint64_t rem = start < n ? n - start : 0;
+    const uint32_t bytes = (uint32_t)((rem < kTileElems ? rem : kTileElems) * sizeof(raw));
+    const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint8_t*>(base) + (rem ? start : 0) * sizeof(raw), (short)0, (int)bytes, kBufferWord3);
+    const uint32_t lo = lane_id() * (uint32_t)sizeof(raw);
+    const int soff = (int)(rowb * (uint32_t)r0);
+#pragma unroll
+    for (int q = 0; q < 16; q++) {
+        if constexpr (sizeof(raw) == 4)
+            v[q] = __builtin_amdgcn_raw_buffer_load_b32(rs, lo + rowb * q, soff, kStreamLoad);
+        else
+            v[q] = __builtin_amdgcn_raw_buffer_load_b16(rs, lo + rowb * q, soff, kStreamLoad);
+    }
+}
+
+// One tile from the LDS stage: value of row r of this lane's column is
+// stage[rank] for its set bits, rank counting up from `rank`.
+template <class E>
+__device__ __forceinline__ void store_from_stage(typename E::raw* col, uint64_t rem, uint64_t w,
+                                                 const typename E::raw* stage, uint32_t rank) {
+    using raw = typename E::raw;
+    const uint32_t l = lane_id();
+    if (rem >= kTileElems) {
+#pragma unroll 8
+        for (int r = 0; r < 64; r++) {
+            raw v = 0;
+            if ((w >> r) & 1ull) { v = stage[rank]; rank++; }
+            col[64 * r] = v;
+        }
+    } else {
+#pragma unroll 8
+        for (int r = 0; r < 64; r++) {
+            raw v = 0;
+            if ((w >> r) & 1ull) { v = stage[rank]; rank++; }
+            if ((uint64_t)(64 * r + l) < rem) col[64 * r] = v;
+        }
+    }
+}
+
+template <class E, int K>
 __global__ void __launch_bounds__(kBlockThreads) k_gather(GatherArgs g) {
     using raw = typename E::raw;
-    __shared__ raw stage_all[kWavesPerBlock][E::cap];
+    __shared__ raw stage_all[kWavesPerBlock][kChunkVals];
     __shared__ uint32_t s_ok, s_fmt;
     __shared__ uint64_t s_nnz;
-    const uint32_t wave = threadIdx.x >> 6;
+    const uint32_t wave = threadIdx.x >> 6, l = lane_id();
     const DevOperand op = g.part[blockIdx.y];
     if (threadIdx.x == 0) {
         if (op.hdr) {
@@ -946,16 +1011,105 @@ __global__ void __launch_bounds__(kBlockThreads) k_gather(GatherArgs g) {
     }
     __syncthreads();
     if (!s_ok) return;
-    const uint64_t t = (uint64_t)blockIdx.x * kWavesPerBlock + wave;
-    if (t >= g.T) return;
-    uint32_t v[64];
-    if (s_fmt == (uint32_t)kFmtPici) {
-        fetch_pici<E, true>(op.data, s_nnz, t, g.n, stage_all[wave], g.ctrl, v);
-    } else {
+    const uint64_t t0 = ((uint64_t)blockIdx.x * kWavesPerBlock + wave) * K;
+    if (t0 >= g.T) return;
+    raw* out = reinterpret_cast<raw*>(g.out + (uint64_t)blockIdx.y * g.n * sizeof(raw));
+    if (s_fmt != (uint32_t)kFmtPici) {
+        // a dense part: copy its tiles, 16 rows at a time
         const uint8_t* d = op.hdr ? op.hdr + kHeaderBytes : op.data;
-        fetch_dense<E, true>(d, t, g.n, v);
+#pragma unroll 1
+        for (int k = 0; k < K; k++) {
+            const uint64_t t = t0 + k;
+            if (t >= g.T) break;
+            raw* col = out + t * kTileElems + l;
+            const uint64_t rem = g.n - t * kTileElems;
+#pragma unroll 1
+            for (int h = 0; h < 4; h++) {
+                uint32_t v[16];
+                fetch_dense_rows16<E>(d, t, g.n, 16 * h, v);
+#pragma unroll
+                for (int q = 0; q < 16; q++) {
+                    const int r = 16 * h + q;
+                    if ((uint64_t)(64 * r + l) < rem) col[64 * r] = (raw)v[q];
+                }
+            }
+        }
+        return;
     }
-    store_tile<E>(g.out + (uint64_t)blockIdx.y * g.n * sizeof(raw), t, g.n, v);
+    const raw* A = reinterpret_cast<const raw*>(op.data + off_A(g.n));
+    PiciMeta m[K];
+#pragma unroll
+    for (int k = 0; k < K; k++)
+        m[k] = t0 + k < g.T ? load_pici_meta<E>(op.data, t0 + k, g.n) : PiciMeta{0, 0, 0};
+    uint64_t cw[K];
+    uint32_t cpref[K], ccnt[K], cbase[K];
+    int kfit = 0;                       // leading tiles whose values are staged together
+#pragma unroll
+    for (int k = 0; k < K; k++) {
+        const bool have = t0 + k < g.T;
+        const PiciCols c = have ? pici_columns(m[k], s_nnz, t0 + k, g.n, g.ctrl) : PiciCols{0, 0, 0, 0, false};
+        cw[k] = c.w; cpref[k] = c.colpref; ccnt[k] = c.cnt; cbase[k] = c.base;
+        // valid tiles chain (base + cnt == next == the next tile's base)
+        if (kfit == k && c.ok && (c.base - cbase[0]) + c.cnt <= kChunkVals) kfit = k + 1;
+    }
+    const uint32_t chunk = kfit ? (cbase[kfit - 1] - cbase[0]) + ccnt[kfit - 1] : 0u;
+    raw* stage = stage_all[wave];
+    {
+        uint32_t x[kChunkSlots];
+#pragma unroll
+        for (int j = 0; j < kChunkSlots; j++) {
+            const uint32_t i = l + 64 * j;
+            x[j] = i < chunk ? (uint32_t)A[cbase[0] + i] : 0u;
+        }
+#pragma unroll
+        for (int j = 0; j < kChunkSlots; j++) {
+            const uint32_t i = l + 64 * j;
+            if (i < chunk) stage[i] = (raw)x[j];
+        }
+        wave_lds_sync();
+    }
+#pragma unroll
+    for (int k = 0; k < K; k++) {
+        if (k >= kfit) break;
+        store_from_stage<E>(out + (t0 + k) * kTileElems + l, g.n - (t0 + k) * kTileElems, cw[k], stage,
+                            (cbase[k] - cbase[0]) + cpref[k]);
+    }
+    // the rest one at a time
+#pragma unroll
+    for (int k = 0; k < K; k++) {
+        const uint64_t t = t0 + k;
+        if (k < kfit) continue;
+        if (t >= g.T) break;
+        raw* col = out + t * kTileElems + l;
+        const uint64_t rem = g.n - t * kTileElems;
+        const uint64_t w = cw[k];
+        const uint32_t cnt = ccnt[k];
+        if (cnt <= kChunkVals) {
+            wave_lds_sync();
+            for (uint32_t i = l; i < cnt; i += 64) stage[i] = A[cbase[k] + i];
+            wave_lds_sync();
+            store_from_stage<E>(col, rem, w, stage, cpref[k]);
+        } else {
+            // dense tile: each lane reads its own column run, 16 rows at a time
+            const raw* run = A + cbase[k] + cpref[k];
+            uint32_t rank = 0;
+#pragma unroll 1
+            for (int h = 0; h < 4; h++) {
+                raw y[16];
+#pragma unroll
+                for (int q = 0; q < 16; q++) {
+                    const bool bit = (w >> (16 * h + q)) & 1ull;
+                    y[q] = bit ? run[rank] : (raw)0;
+                    rank += bit ? 1u : 0u;
+                }
+#pragma unroll
+                for (int q = 0; q < 16; q++) {
+                    const int r = 16 * h + q;
+                    if ((uint64_t)(64 * r + l) < rem) col[64 * r] = y[q];
+                }
+            }
+        }
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -1140,10 +1294,22 @@ spccl_status_t launch_to_dense_dt(int dtype, int sa, int sb, const DenseSinkArgs
     return dtype == kBF16 ? launch_to_dense<BF16>(sa, sb, g, st) : launch_to_dense<F32>(sa, sb, g, st);
 }
 
+// Tiles per wave of the expansion: enough waves to fill the chip (about
+// 8192 resident), and as many tiles per wave as that leaves, up to 4.
+template <class E>
+void launch_gather_k(const GatherArgs& g, int P, hipStream_t st) {
+    const uint64_t tiles = g.T * (uint64_t)P;
+    const int K = tiles >= 4 * 8192 ? 4 : tiles >= 2 * 8192 ? 2 : 1;
+    dim3 block(kBlockThreads);
+    dim3 grid(stream_grid(g.T, kWavesPerBlock * K, 0x7FFFFFFF), (unsigned)P);
+    if (K == 4) hipLaunchKernelGGL((k_gather<E, 4>), grid, block, 0, st, g);
+    else if (K == 2) hipLaunchKernelGGL((k_gather<E, 2>), grid, block, 0, st, g);
+    else hipLaunchKernelGGL((k_gather<E, 1>), grid, block, 0, st, g);
+}
+
 spccl_status_t launch_gather_dt(int dtype, const GatherArgs& g, int P, hipStream_t st) {
-    dim3 grid(stream_grid(g.T, kWavesPerBlock, 0x7FFFFFFF), (unsigned)P), block(kBlockThreads);
-    if (dtype == kBF16) hipLaunchKernelGGL(k_gather<BF16>, grid, block, 0, st, g);
-    else hipLaunchKernelGGL(k_gather<F32>, grid, block, 0, st, g);
+    if (dtype == kBF16) launch_gather_k<BF16>(g, P, st);
+    else launch_gather_k<F32>(g, P, st);
     return launch_status();
 }
 
