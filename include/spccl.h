@@ -62,7 +62,10 @@ typedef struct {
                          caller expects (checked against the header on the device);
                          for an output, the format to produce.  Ignored for ARRAY. */
     void* ptr;        /* device pointer (16-byte aligned for a STREAM) */
-    uint64_t bytes;   /* capacity of the buffer in bytes */
+    uint64_t bytes;   /* capacity of the buffer in bytes; a STREAM input must hold
+                         at least the smallest valid message of its declared
+                         format (DENSE: 48 + n * elem_size; PICI: off_A, the
+                         header plus B and I), else SPCCL_ERR_CAPACITY */
 } spccl_operand_t;
 
 /* The 48-byte message header (Sec. V-B names its contents: format, size and

@@ -69,10 +69,18 @@ spccl_status_t decode_input(const spccl_operand_t& o, uint64_t n, int32_t dt, Sr
         return SPCCL_OK;
     }
     if (o.kind != SPCCL_STREAM) return SPCCL_ERR_INVALID_ARG;
-    if (o.bytes < kHeaderBytes) return SPCCL_ERR_CAPACITY;
-    if (o.fmt == SPCCL_FMT_DENSE) *out = Src{SRC_DENSE, DevOperand{p, p + kHeaderBytes, o.bytes}};
-    else if (o.fmt == SPCCL_FMT_PICI) *out = Src{SRC_PICI, DevOperand{p, p, o.bytes}};
-    else return SPCCL_ERR_INVALID_ARG;
+    // the smallest valid message of the declared format: kernels read a dense
+    // message's values, or a Pici message's index arrays, before its header
+    // has been checked
+    if (o.fmt == SPCCL_FMT_DENSE) {
+        if (o.bytes < dense_msg_bytes(n, dt)) return SPCCL_ERR_CAPACITY;
+        *out = Src{SRC_DENSE, DevOperand{p, p + kHeaderBytes, o.bytes}};
+    } else if (o.fmt == SPCCL_FMT_PICI) {
+        if (o.bytes < off_A(n)) return SPCCL_ERR_CAPACITY;
+        *out = Src{SRC_PICI, DevOperand{p, p, o.bytes}};
+    } else {
+        return SPCCL_ERR_INVALID_ARG;
+    }
     return SPCCL_OK;
 }
 

@@ -105,14 +105,25 @@ struct HeaderView {
     uint64_t nnz;
 };
 
+// The six 64-bit words of a header (messages are 16-byte aligned).
+struct HeaderWords {
+    uint64_t w[6];
+};
+
+__device__ __forceinline__ HeaderWords load_header_words(const uint8_t* h) {
+    const uint4* q = reinterpret_cast<const uint4*>(h);
+    const uint4 x = q[0], y = q[1], z = q[2];
+    return HeaderWords{{(uint64_t)x.x | ((uint64_t)x.y << 32), (uint64_t)x.z | ((uint64_t)x.w << 32),
+                        (uint64_t)y.x | ((uint64_t)y.y << 32), (uint64_t)y.z | ((uint64_t)y.w << 32),
+                        (uint64_t)z.x | ((uint64_t)z.y << 32), (uint64_t)z.z | ((uint64_t)z.w << 32)}};
+}
+
 // Checks a message header against the expected n / dtype (and format if
 // want_fmt >= 0) and the buffer capacity; every offset must be the one the
 // layout implies, so a passing header bounds every later read.
-__device__ HeaderView read_header(const uint8_t* h, uint64_t cap, uint64_t n, int dtype, int want_fmt) {
+__device__ HeaderView check_header(const HeaderWords& hw, uint64_t cap, uint64_t n, int dtype, int want_fmt) {
     HeaderView v{false, 0u, 0ull};
-    if (cap < kHeaderBytes) return v;
-    const uint64_t* w = reinterpret_cast<const uint64_t*>(h);
-    const uint64_t w0 = w[0], hn = w[1], nnz = w[2], oI = w[3], oA = w[4], total = w[5];
+    const uint64_t w0 = hw.w[0], hn = hw.w[1], nnz = hw.w[2], oI = hw.w[3], oA = hw.w[4], total = hw.w[5];
     const uint32_t magic = (uint32_t)w0, fmt = (uint32_t)(w0 >> 32) & 0xFFFFu, dt = (uint32_t)(w0 >> 48);
     bool ok = magic == kMagic && dt == (uint32_t)dtype && hn == n && total <= cap;
     if (want_fmt >= 0) ok = ok && fmt == (uint32_t)want_fmt;
@@ -126,6 +137,11 @@ __device__ HeaderView read_header(const uint8_t* h, uint64_t cap, uint64_t n, in
     v.fmt = fmt;
     v.nnz = nnz;
     return v;
+}
+
+__device__ HeaderView read_header(const uint8_t* h, uint64_t cap, uint64_t n, int dtype, int want_fmt) {
+    if (cap < kHeaderBytes) return HeaderView{false, 0u, 0ull};
+    return check_header(load_header_words(h), cap, n, dtype, want_fmt);
 }
 
 __device__ __forceinline__ void write_header(uint8_t* out, int fmt, int dtype, uint64_t n, uint64_t nnz,
@@ -230,6 +246,32 @@ __device__ __forceinline__ PiciCols pici_columns(PiciMeta m, uint64_t nnz, uint6
     return PiciCols{w, colpref, cnt, m.base, !bad};
 }
 
+// Values staged with all loads in flight at once: up to kChunkVals values,
+// kChunkSlots per lane.
+constexpr uint32_t kChunkVals = 1024;
+constexpr int kChunkSlots = kChunkVals / 64;
+
+// src[0 .. cnt) into stage[0 .. cnt), kChunkVals at a time with every load
+// of a chunk issued before the first is used.
+template <class E>
+__device__ __forceinline__ void stage_values(const typename E::raw* src, uint32_t cnt, typename E::raw* stage) {
+    using raw = typename E::raw;
+    const uint32_t l = lane_id();
+    for (uint32_t c0 = 0; c0 < cnt; c0 += kChunkVals) {
+        raw x[kChunkSlots];
+#pragma unroll
+        for (int j = 0; j < kChunkSlots; j++) {
+            const uint32_t i = c0 + l + 64 * j;
+            x[j] = i < cnt ? src[i] : (raw)0;
+        }
+#pragma unroll
+        for (int j = 0; j < kChunkSlots; j++) {
+            const uint32_t i = c0 + l + 64 * j;
+            if (i < cnt) stage[i] = x[j];
+        }
+    }
+}
+
 template <class E, bool First>
 __device__ __forceinline__ void expand_pici(PiciCols pc, const uint8_t* msg, uint64_t n, typename E::raw* stage,
                                             uint32_t (&v)[64]) {
@@ -238,65 +280,89 @@ __device__ __forceinline__ void expand_pici(PiciCols pc, const uint8_t* msg, uin
     const uint64_t w = pc.w;
     const uint32_t colpref = pc.colpref, cnt = pc.cnt;
     const raw* src = reinterpret_cast<const raw*>(msg + off_A(n)) + pc.base;
-    if (cnt <= E::cap) {
-        for (uint32_t i = l; i < cnt; i += 64) stage[i] = src[i];
+    if (First) {
+#pragma unroll
+        for (int r = 0; r < 64; r++) v[r] = 0;
+    }
+    // one pass over all 64 columns when the tile's values fit the stage,
+    // else one group of columns at a time
+    const bool one = cnt <= E::cap;
+    const int ngroups = one ? 1 : E::groups;
+    const uint32_t gcols = one ? 64u : E::group_cols;
+#pragma unroll 1
+    for (int h = 0; h < ngroups; h++) {
+        const uint32_t c0 = gcols * h, c1 = c0 + gcols;
+        const uint32_t lo = one ? 0u : __shfl(colpref, c0, 64);
+        const uint32_t hi = (one || c1 == 64) ? cnt : __shfl(colpref, c1, 64);
+        stage_values<E>(src + lo, hi - lo, stage);
         wave_lds_sync();
-        uint32_t rank = colpref;
+        const uint64_t wm = (l >= c0 && l < c1) ? w : 0ull;
+        uint32_t rank = colpref - lo;
 #pragma unroll
         for (int r = 0; r < 64; r++) {
-            uint32_t x = 0;
-            if ((w >> r) & 1ull) { x = stage[rank]; rank++; }
-            v[r] = First ? x : oplus(E{}, v[r], x);
+            const bool bit = (wm >> r) & 1ull;
+            if (__any(bit)) {                            // rows empty in every column cost one branch
+                if (bit) {
+                    const uint32_t x = stage[rank];
+                    rank++;
+                    v[r] = First ? x : oplus(E{}, v[r], x);
+                }
+            }
         }
         wave_lds_sync();
-    } else {
-        // more values than the stage holds: one group of columns at a time
-#pragma unroll
-        for (int h = 0; h < E::groups; h++) {
-            const uint32_t lo = __shfl(colpref, E::group_cols * h, 64);
-            const uint32_t hi = h == E::groups - 1 ? cnt : __shfl(colpref, E::group_cols * (h + 1), 64);
-            for (uint32_t i = l; i < hi - lo; i += 64) stage[i] = src[lo + i];
-            wave_lds_sync();
-            const bool mine = l / E::group_cols == (uint32_t)h;
-            uint32_t rank = colpref - lo;
-#pragma unroll
-            for (int r = 0; r < 64; r++) {
-                uint32_t x = 0;
-                const bool bit = mine && ((w >> r) & 1ull);
-                if (bit) { x = stage[rank]; rank++; }
-                if (mine) v[r] = First ? x : oplus(E{}, v[r], x);
-            }
-            wave_lds_sync();
-        }
     }
 }
 
-template <class E, bool First>
-__device__ __forceinline__ void fetch_pici(const uint8_t* msg, uint64_t nnz, uint64_t t, uint64_t n,
-                                           typename E::raw* stage, WsCtrl* ctrl, uint32_t (&v)[64]) {
-    const PiciMeta m = load_pici_meta<E>(msg, t, n);
-    expand_pici<E, First>(pici_columns(m, nnz, t, n, ctrl), msg, n, stage, v);
-}
-
-// A dense operand and a Pici operand of the same tile, v = dense (+) pici
-// (the operation is symmetric bit for bit).  The Pici operand's metadata is
-// requested first and the dense tile right behind it, so its dependent value
-// read overlaps the dense tile's round trip instead of following it.
-template <class E>
-__device__ __forceinline__ void fetch_dense_and_pici(const uint8_t* dense, const uint8_t* msg, uint64_t nnz,
-                                                     uint64_t t, uint64_t n, typename E::raw* stage, WsCtrl* ctrl,
-                                                     uint32_t (&v)[64]) {
-    const PiciMeta m = load_pici_meta<E>(msg, t, n);
-    asm volatile("" ::: "memory");
-    fetch_dense<E, true>(dense, t, n, v);
-    expand_pici<E, false>(pici_columns(m, nnz, t, n, ctrl), msg, n, stage, v);
-}
-
-template <class E, int S, bool First>
-__device__ __forceinline__ void fetch(const DevOperand& op, uint64_t nnz, uint64_t t, uint64_t n,
-                                      typename E::raw* stage, WsCtrl* ctrl, uint32_t (&v)[64]) {
-    if constexpr (S == SRC_DENSE) fetch_dense<E, First>(op.data, t, n, v);
-    else if constexpr (S == SRC_PICI) fetch_pici<E, First>(op.data, nnz, t, n, stage, ctrl, v);
+// Tile t of a (+) b into v[64] (sources: dense rows or Pici tiles; b may be
+// absent).  Every read that needs no header -- the headers themselves, dense
+// rows, Pici column words and offsets -- is issued first; the headers are
+// checked while those are in flight, and only then are Pici values read,
+// since their offsets come from the message.  The host guarantees that a
+// STREAM operand's capacity covers a dense message's values or a Pici
+// message's index arrays, so the early reads stay inside the caller's
+// buffers whatever the header says.  Returns false, the same in every wave
+// of the grid, when a header fails its check (and flags it once).
+template <class E, int SA, int SB>
+__device__ __forceinline__ bool load_tile_pair(const DevOperand& a, const DevOperand& b, uint64_t t, bool has_tile,
+                                               uint64_t n, typename E::raw* stage, WsCtrl* ctrl,
+                                               uint32_t (&v)[64]) {
+    const bool ha = a.hdr != nullptr;
+    const bool hb = SB != SRC_NONE && b.hdr != nullptr;
+    HeaderWords hwa{}, hwb{};
+    if (ha) hwa = load_header_words(a.hdr);
+    if (hb) hwb = load_header_words(b.hdr);
+    PiciMeta ma{0, 0, 0}, mb{0, 0, 0};
+    if (has_tile) {
+        if constexpr (SA == SRC_PICI) ma = load_pici_meta<E>(a.data, t, n);
+        if constexpr (SB == SRC_PICI) mb = load_pici_meta<E>(b.data, t, n);
+        asm volatile("" ::: "memory");
+        if constexpr (SA == SRC_DENSE) fetch_dense<E, true>(a.data, t, n, v);
+        if constexpr (SB == SRC_DENSE) fetch_dense<E, SA != SRC_DENSE>(b.data, t, n, v);
+    }
+    bool ok = true;
+    uint64_t nnza = 0, nnzb = 0;
+    if (ha) {
+        const HeaderView h = check_header(hwa, a.cap, n, E::dtype, SA == SRC_PICI ? kFmtPici : kFmtDense);
+        ok = ok && h.ok;
+        nnza = h.nnz;
+    }
+    if (hb) {
+        const HeaderView h = check_header(hwb, b.cap, n, E::dtype, SB == SRC_PICI ? kFmtPici : kFmtDense);
+        ok = ok && h.ok;
+        nnzb = h.nnz;
+    }
+    if (!ok) {
+        if (blockIdx.x == 0 && threadIdx.x == 0) set_status(ctrl, SPCCL_ERR_CORRUPT_STREAM);
+        return false;
+    }
+    if (has_tile) {
+        constexpr bool dense_first = SA == SRC_DENSE || SB == SRC_DENSE;
+        if constexpr (SA == SRC_PICI)
+            expand_pici<E, !dense_first>(pici_columns(ma, nnza, t, n, ctrl), a.data, n, stage, v);
+        if constexpr (SB == SRC_PICI)
+            expand_pici<E, !dense_first && SA != SRC_PICI>(pici_columns(mb, nnzb, t, n, ctrl), b.data, n, stage, v);
+    }
+    return true;
 }
 
 // ---------------------------------------------------------------------------
@@ -407,30 +473,10 @@ __global__ void __launch_bounds__(kBlockThreads) k_to_pici(PiciSinkArgs g) {
     using raw = typename E::raw;
     __shared__ raw stage_all[kWavesPerBlock][E::cap];
     __shared__ uint32_t s_cnt[kWavesPerBlock];
-    __shared__ uint32_t s_prefix, s_ok;
-    __shared__ uint64_t s_nnz_a, s_nnz_b;
+    __shared__ uint32_t s_prefix;
 
     const uint32_t wave = threadIdx.x >> 6, l = lane_id();
     raw* stage = stage_all[wave];
-    if (threadIdx.x == 0) {
-        bool ok = true;
-        uint64_t na = 0, nb = 0;
-        if (g.a.hdr) {
-            HeaderView h = read_header(g.a.hdr, g.a.cap, g.n, E::dtype, SA == SRC_PICI ? kFmtPici : kFmtDense);
-            ok = ok && h.ok; na = h.nnz;
-        }
-        if (SB != SRC_NONE && g.b.hdr) {
-            HeaderView h = read_header(g.b.hdr, g.b.cap, g.n, E::dtype, SB == SRC_PICI ? kFmtPici : kFmtDense);
-            ok = ok && h.ok; nb = h.nnz;
-        }
-        s_ok = ok;
-        s_nnz_a = na;
-        s_nnz_b = nb;
-        if (!ok && blockIdx.x == 0) set_status(g.ctrl, SPCCL_ERR_CORRUPT_STREAM);
-    }
-    __syncthreads();
-    if (!s_ok) return;            // uniform over the grid: no partition publishes
-
     // Partition = block index.  Work-groups start in index order on each XCD,
     // so the lowest unfinished partition is always resident and every wait
     // below ends (the spin limit bounds it regardless).
@@ -440,17 +486,11 @@ __global__ void __launch_bounds__(kBlockThreads) k_to_pici(PiciSinkArgs g) {
     const bool has_tile = t < g.T;
 
     uint32_t v[64];
+    if (!load_tile_pair<E, SA, SB>(g.a, g.b, t, has_tile, g.n, stage, g.ctrl, v))
+        return;                   // uniform over the grid: no partition publishes
     uint64_t w = 0;
     uint32_t c = 0;
     if (has_tile) {
-        if constexpr (SA == SRC_DENSE && SB == SRC_PICI) {
-            fetch_dense_and_pici<E>(g.a.data, g.b.data, s_nnz_b, t, g.n, stage, g.ctrl, v);
-        } else if constexpr (SA == SRC_PICI && SB == SRC_DENSE) {
-            fetch_dense_and_pici<E>(g.b.data, g.a.data, s_nnz_a, t, g.n, stage, g.ctrl, v);
-        } else {
-            fetch<E, SA, true>(g.a, s_nnz_a, t, g.n, stage, g.ctrl, v);
-            if constexpr (SB != SRC_NONE) fetch<E, SB, false>(g.b, s_nnz_b, t, g.n, stage, g.ctrl, v);
-        }
         // every source reads as zero at positions >= n (bounded buffer loads,
         // Pici tiles checked against the array's end)
 #pragma unroll
@@ -478,7 +518,9 @@ __global__ void __launch_bounds__(kBlockThreads) k_to_pici(PiciSinkArgs g) {
         uint32_t rank = colpref;
 #pragma unroll
         for (int r = 0; r < 64; r++)
-            if ((w >> r) & 1ull) { stage[rank] = (raw)v[r]; rank++; }
+            if (__any(v[r] != 0u)) {                     // rows empty in every column cost one branch
+                if (v[r] != 0u) { stage[rank] = (raw)v[r]; rank++; }
+            }
     }
     if constexpr (Deferred) {
         if (!has_tile) return;
@@ -495,7 +537,9 @@ __global__ void __launch_bounds__(kBlockThreads) k_to_pici(PiciSinkArgs g) {
                 uint32_t rank = colpref - lo;
 #pragma unroll
                 for (int r = 0; r < 64; r++)
-                    if (mine && ((w >> r) & 1ull)) { stage[rank] = (raw)v[r]; rank++; }
+                    if (__any(mine && v[r] != 0u)) {
+                        if (mine && v[r] != 0u) { stage[rank] = (raw)v[r]; rank++; }
+                    }
                 wave_lds_sync();
                 for (uint32_t i = l; i < hi - lo; i += 64) slot[lo + i] = stage[i];
                 wave_lds_sync();
@@ -530,7 +574,9 @@ __global__ void __launch_bounds__(kBlockThreads) k_to_pici(PiciSinkArgs g) {
                 uint32_t rank = colpref - lo;
 #pragma unroll
                 for (int r = 0; r < 64; r++)
-                    if (mine && ((w >> r) & 1ull)) { stage[rank] = (raw)v[r]; rank++; }
+                    if (__any(mine && v[r] != 0u)) {
+                        if (mine && v[r] != 0u) { stage[rank] = (raw)v[r]; rank++; }
+                    }
                 wave_lds_sync();
                 raw* dst = A + tbase + lo;
                 for (uint32_t i = l; i < hi - lo; i += 64) dst[i] = stage[i];
@@ -549,7 +595,6 @@ __global__ void __launch_bounds__(kBlockThreads) k_to_pici(PiciSinkArgs g) {
 }
 
 // ---------------------------------------------------------------------------
-// ---------------------------------------------------------------------------
 // Pici (+) Pici -> Pici with work proportional to the nonzeros.
 //
 // Phase 1 finds each output column word: the operands' values for a group of
@@ -558,179 +603,267 @@ __global__ void __launch_bounds__(kBlockThreads) k_to_pici(PiciSinkArgs g) {
 // checked if a staged value is itself zero, which reads as absent).  Once the
 // tile's destination is known (its slot in the two-pass mode, the look-back
 // prefix in the single-pass mode), phase 2 merges each column's two runs in
-// row order into an LDS output stage and copies it out.  A tile whose values
-// fit the stage at once is one group of 64 columns, staged a single time;
-// denser tiles go through in groups of PPGroup::cols columns (at most cap
-// values per group), staged again in phase 2.
-
-template <class E>
+// row order and each lane stores its column's results in place.  A tile
+// whose two value ranges fit kChunkVals together is one group of 64 columns,
+// read with all loads in flight at once and staged a single time; denser
+// tiles go through in groups of PPGroup::cols columns, staged again in
+// phase 2.
 struct PPGroup {
-    static constexpr uint32_t cols = E::cap / 128;            // 2 operands x 64 rows per column
+    static constexpr uint32_t cols = kChunkVals / 128;        // 2 operands x 64 rows per column
     static constexpr int count = 64 / cols;
 };
 
 // The value ranges of columns [c0, c1) of both operands into in[]: a's at
-// [0, la), b's at [la, la + lb).  Returns la; zero = some staged value has
+// [0, la), b's at [la, la + lb) (la + lb <= kChunkVals), every load issued
+// before the first is used.  Returns la; zero = some staged value has
 // all-zero bits (uniform over the wave).
 template <class E>
 __device__ __forceinline__ uint32_t pp_stage(const PiciCols& ca, const PiciCols& cb, const typename E::raw* pa,
                                              const typename E::raw* pb, uint32_t c0, uint32_t c1,
                                              typename E::raw* in, bool& zero) {
+    using raw = typename E::raw;
     const uint32_t l = lane_id();
     const uint32_t a0 = __shfl(ca.colpref, c0, 64);
     const uint32_t a1 = c1 == 64 ? ca.cnt : __shfl(ca.colpref, c1, 64);
     const uint32_t b0 = __shfl(cb.colpref, c0, 64);
     const uint32_t b1 = c1 == 64 ? cb.cnt : __shfl(cb.colpref, c1, 64);
     const uint32_t la = a1 - a0, lb = b1 - b0;
-    bool z = false;
-    for (uint32_t i = l; i < la; i += 64) {
-        const typename E::raw x = pa[a0 + i];
-        z |= x == 0;
-        in[i] = x;
+    raw x[kChunkSlots];
+#pragma unroll
+    for (int j = 0; j < kChunkSlots; j++) {
+        const uint32_t i = l + 64 * j;
+        x[j] = i < la ? pa[a0 + i] : (i < la + lb ? pb[b0 + (i - la)] : (raw)1);
     }
-    for (uint32_t i = l; i < lb; i += 64) {
-        const typename E::raw x = pb[b0 + i];
-        z |= x == 0;
-        in[la + i] = x;
+    bool z = false;
+#pragma unroll
+    for (int j = 0; j < kChunkSlots; j++) {
+        const uint32_t i = l + 64 * j;
+        z |= x[j] == 0;
+        if (i < la + lb) in[i] = x[j];
     }
     zero = __any(z);
     wave_lds_sync();
     return la;
 }
 
+// Cancellations (exact zero sums) among the rows of this lane's column held by
+// both operands -- or by either one when `zero` says a staged value is itself
+// zero -- with a's run at in[ra ...] and b's at in[rb ...].
+template <class E>
+__device__ __forceinline__ uint64_t pp_cancel(uint64_t wa, uint64_t wb, const typename E::raw* in, uint32_t ra,
+                                              uint32_t rb, bool zero, bool mine) {
+    uint64_t chk = mine ? (zero ? (wa | wb) : (wa & wb)) : 0ull;
+    uint64_t cancel = 0;
+    while (__any(chk != 0ull)) {
+        if (chk) {
+            const uint32_t r = (uint32_t)__builtin_ctzll(chk);
+            chk &= chk - 1ull;
+            const uint64_t below = (1ull << r) - 1ull;
+            const uint32_t xa = ((wa >> r) & 1ull) ? (uint32_t)in[ra + (uint32_t)__popcll(wa & below)] : 0u;
+            const uint32_t xb = ((wb >> r) & 1ull) ? (uint32_t)in[rb + (uint32_t)__popcll(wb & below)] : 0u;
+            if (oplus(E{}, xa, xb) == 0u) cancel |= 1ull << r;
+        }
+    }
+    return cancel;
+}
+
+// Row-order merge of this lane's two runs (a's at in[ia ...], b's at
+// in[ib ...]); results present in wo go to dst[k ...].
+template <class E>
+__device__ __forceinline__ void pp_merge(uint64_t wa, uint64_t wb, uint64_t wo, const typename E::raw* in,
+                                         uint32_t ia, uint32_t ib, typename E::raw* dst, uint32_t k, bool mine) {
+    uint64_t todo = mine ? (wa | wb) : 0ull;
+    while (__any(todo != 0ull)) {
+        if (todo) {
+            const uint32_t r = (uint32_t)__builtin_ctzll(todo);
+            todo &= todo - 1ull;
+            uint32_t xa = 0, xb = 0;
+            if ((wa >> r) & 1ull) { xa = in[ia]; ia++; }
+            if ((wb >> r) & 1ull) { xb = in[ib]; ib++; }
+            if ((wo >> r) & 1ull) { dst[k] = (typename E::raw)oplus(E{}, xa, xb); k++; }
+        }
+    }
+}
+
+// One wave per partition (kTilesPerPart consecutive tiles).  When every tile
+// checks out and the partition's two value ranges fit kChunkVals together,
+// both ranges are read at once (all loads in flight) and staged a single
+// time for both phases.  Otherwise the tiles go one at a time through
+// column groups (metadata read again per phase, the output column words read
+// back from the message).
 template <class E, bool Deferred>
 __global__ void __launch_bounds__(kBlockThreads) k_pp_to_pici(PiciSinkArgs g) {
     using raw = typename E::raw;
-    __shared__ raw lds_in[kWavesPerBlock][E::cap];
-    __shared__ raw lds_out[kWavesPerBlock][E::cap];
-    __shared__ uint32_t s_cnt[kWavesPerBlock];
-    __shared__ uint32_t s_prefix, s_ok;
-    __shared__ uint64_t s_nnz_a, s_nnz_b;
+    constexpr int K = kTilesPerPart;
+    __shared__ raw lds_in[kWavesPerBlock][kChunkVals];
+    __shared__ uint32_t s_tcnt[kWavesPerBlock][K];
     const uint32_t wave = threadIdx.x >> 6, l = lane_id();
     raw* in = lds_in[wave];
-    raw* out = lds_out[wave];
-    if (threadIdx.x == 0) {
-        const HeaderView ha = read_header(g.a.hdr, g.a.cap, g.n, E::dtype, kFmtPici);
-        const HeaderView hb = read_header(g.b.hdr, g.b.cap, g.n, E::dtype, kFmtPici);
-        s_ok = ha.ok && hb.ok;
-        s_nnz_a = ha.nnz;
-        s_nnz_b = hb.nnz;
-        if (!s_ok && blockIdx.x == 0) set_status(g.ctrl, SPCCL_ERR_CORRUPT_STREAM);
-    }
-    __syncthreads();
-    if (!s_ok) return;
-
-    const uint32_t p = blockIdx.x;
+    const uint32_t p = blockIdx.x * kWavesPerBlock + wave;
+    if (p >= g.nparts) return;
     const uint32_t epoch30 = g.epoch & 0x3FFFFFFFu;
-    const uint64_t t = (uint64_t)p * kTilesPerPart + wave;
-    const bool has_tile = t < g.T;
+    const uint64_t t0 = (uint64_t)p * K;
     const uint64_t oI = off_I(g.n), oA = off_A(g.n);
     const raw* Aa = reinterpret_cast<const raw*>(g.a.data + oA);
     const raw* Ab = reinterpret_cast<const raw*>(g.b.data + oA);
+    uint64_t* Bout = reinterpret_cast<uint64_t*>(g.out + kHeaderBytes);
 
-    PiciCols ca{0, 0, 0, 0, true}, cb{0, 0, 0, 0, true};
-    const raw* pa = Aa;
-    const raw* pb = Ab;
-    uint64_t wa = 0, wb = 0, wo = 0;
-    bool one_group = true;
-    if (has_tile) {
-        const PiciMeta ma = load_pici_meta<E>(g.a.data, t, g.n);
-        const PiciMeta mb = load_pici_meta<E>(g.b.data, t, g.n);
-        ca = pici_columns(ma, s_nnz_a, t, g.n, g.ctrl);
-        cb = pici_columns(mb, s_nnz_b, t, g.n, g.ctrl);
-        wa = ca.w;                                            // no bits at positions >= n (checked)
-        wb = cb.w;
-        one_group = ca.cnt + cb.cnt <= E::cap;
-        const int ngroups = one_group ? 1 : PPGroup<E>::count;
-        const uint32_t gcols = one_group ? 64u : PPGroup<E>::cols;
-        pa = Aa + ca.base;
-        pb = Ab + cb.base;
-        uint64_t cancel = 0;
-        for (int h = 0; h < ngroups; h++) {
-            const uint32_t c0 = gcols * h, c1 = c0 + gcols;
-            const bool mine = l >= c0 && l < c1;
-            bool zero;
-            const uint32_t la = pp_stage<E>(ca, cb, pa, pb, c0, c1, in, zero);
-            const uint32_t ra = ca.colpref - __shfl(ca.colpref, c0, 64);
-            const uint32_t rb = la + cb.colpref - __shfl(cb.colpref, c0, 64);
-            uint64_t chk = mine ? (zero ? (wa | wb) : (wa & wb)) : 0ull;
-            while (__any(chk != 0ull)) {
-                if (chk) {
-                    const uint32_t r = (uint32_t)__builtin_ctzll(chk);
-                    chk &= chk - 1ull;
-                    const uint64_t below = (1ull << r) - 1ull;
-                    const uint32_t xa = ((wa >> r) & 1ull) ? (uint32_t)in[ra + (uint32_t)__popcll(ca.w & below)] : 0u;
-                    const uint32_t xb = ((wb >> r) & 1ull) ? (uint32_t)in[rb + (uint32_t)__popcll(cb.w & below)] : 0u;
-                    if (oplus(E{}, xa, xb) == 0u) cancel |= 1ull << r;
-                }
-            }
-            if (!one_group) wave_lds_sync();                  // the stage is reused by the next group
-        }
-        wo = (wa | wb) & ~cancel;
-        reinterpret_cast<uint64_t*>(g.out + kHeaderBytes)[t * 64 + l] = wo;
-    }
-    const uint32_t colpref = wave_excl_scan((uint32_t)__popcll(wo));
-    const uint32_t tilecnt = __shfl(colpref + (uint32_t)__popcll(wo), 63, 64);
-    if (l == 0) s_cnt[wave] = tilecnt;
-    __syncthreads();
-    uint32_t tile_excl = 0, agg = 0;
+    // headers and column words / offsets first (the host guarantees both
+    // messages' capacities cover the index arrays), headers checked while
+    // the rest is in flight
+    const HeaderWords hwa = load_header_words(g.a.hdr);
+    const HeaderWords hwb = load_header_words(g.b.hdr);
+    PiciMeta ma[K], mb[K];
 #pragma unroll
-    for (uint32_t k = 0; k < kWavesPerBlock; k++) {
-        const uint32_t ck = s_cnt[k];
-        tile_excl += k < wave ? ck : 0u;
-        agg += ck;
+    for (int k = 0; k < K; k++) {
+        const bool have = t0 + k < g.T;
+        ma[k] = have ? load_pici_meta<E>(g.a.data, t0 + k, g.n) : PiciMeta{0, 0, 0};
+        mb[k] = have ? load_pici_meta<E>(g.b.data, t0 + k, g.n) : PiciMeta{0, 0, 0};
     }
-    if (threadIdx.x == 0)
-        publish(g.flags, p, epoch30, (p == 0 && !Deferred) ? kFlagPrefix : kFlagAggregate, agg);
+    const HeaderView ha = check_header(hwa, g.a.cap, g.n, E::dtype, kFmtPici);
+    const HeaderView hb = check_header(hwb, g.b.cap, g.n, E::dtype, kFmtPici);
+    if (!(ha.ok && hb.ok)) {          // the same in every wave: no partition publishes
+        if (blockIdx.x == 0 && threadIdx.x == 0) set_status(g.ctrl, SPCCL_ERR_CORRUPT_STREAM);
+        return;
+    }
+    const uint64_t nnz_a = ha.nnz, nnz_b = hb.nnz;
+
+    uint64_t wa[K], wb[K];
+    uint32_t pa[K], pb[K];                    // column prefixes
+    uint32_t na[K], nb[K], ba[K], bb[K];      // counts and bases (wave-uniform)
+    bool allok = true;
+#pragma unroll
+    for (int k = 0; k < K; k++) {
+        const bool have = t0 + k < g.T;
+        const PiciCols ca = have ? pici_columns(ma[k], nnz_a, t0 + k, g.n, g.ctrl) : PiciCols{0, 0, 0, 0, true};
+        const PiciCols cb = have ? pici_columns(mb[k], nnz_b, t0 + k, g.n, g.ctrl) : PiciCols{0, 0, 0, 0, true};
+        allok = allok && ca.ok && cb.ok;
+        wa[k] = ca.w; pa[k] = ca.colpref; na[k] = __builtin_amdgcn_readfirstlane(ca.cnt);
+        ba[k] = __builtin_amdgcn_readfirstlane(ca.base);
+        wb[k] = cb.w; pb[k] = cb.colpref; nb[k] = __builtin_amdgcn_readfirstlane(cb.cnt);
+        bb[k] = __builtin_amdgcn_readfirstlane(cb.base);
+    }
+    uint32_t La = 0, Lb = 0;
+#pragma unroll
+    for (int k = 0; k < K; k++) { La += na[k]; Lb += nb[k]; }
+    // valid tiles chain (base + cnt == next == the next tile's base), so the
+    // partition's values of each operand are one contiguous range
+    const bool staged = allok && La + Lb <= kChunkVals;
+
+    uint32_t agg = 0;
     raw* dst;
     uint32_t prefix = 0;
-    if constexpr (Deferred) {
-        dst = reinterpret_cast<raw*>(g.slots) + (uint64_t)p * kPartElems + tile_excl;
+    if (staged) {
+        bool zero;
+        {
+            raw x[kChunkSlots];
+#pragma unroll
+            for (int j = 0; j < kChunkSlots; j++) {
+                const uint32_t i = l + 64 * j;
+                x[j] = i < La ? Aa[ba[0] + i] : (i < La + Lb ? Ab[bb[0] + (i - La)] : (raw)1);
+            }
+            bool z = false;
+#pragma unroll
+            for (int j = 0; j < kChunkSlots; j++) {
+                const uint32_t i = l + 64 * j;
+                z |= x[j] == 0;
+                if (i < La + Lb) in[i] = x[j];
+            }
+            zero = __any(z);
+            wave_lds_sync();
+        }
+        uint64_t wo[K];
+        uint32_t cpo[K], texcl[K];
+#pragma unroll
+        for (int k = 0; k < K; k++) {
+            const uint64_t cancel = pp_cancel<E>(wa[k], wb[k], in, (ba[k] - ba[0]) + pa[k],
+                                                 La + (bb[k] - bb[0]) + pb[k], zero, true);
+            wo[k] = (wa[k] | wb[k]) & ~cancel;
+            if (t0 + k < g.T) Bout[(t0 + k) * 64 + l] = wo[k];
+            const uint32_t c = (uint32_t)__popcll(wo[k]);
+            cpo[k] = wave_excl_scan(c);
+            texcl[k] = agg;
+            agg += __builtin_amdgcn_readfirstlane(__shfl(cpo[k] + c, 63, 64));
+        }
+        if (l == 0) publish(g.flags, p, epoch30, (p == 0 && !Deferred) ? kFlagPrefix : kFlagAggregate, agg);
+        if constexpr (Deferred) {
+            dst = reinterpret_cast<raw*>(g.slots) + (uint64_t)p * kPartElems;
+        } else {
+            prefix = p == 0 ? 0u : lookback(g.flags, p, epoch30, g.ctrl);
+            if (l == 0 && p != 0) publish(g.flags, p, epoch30, kFlagPrefix, prefix + agg);
+            dst = reinterpret_cast<raw*>(g.out + oA) + prefix;
+        }
+#pragma unroll
+        for (int k = 0; k < K; k++) {
+            if (t0 + k >= g.T) break;
+            pp_merge<E>(wa[k], wb[k], wo[k], in, (ba[k] - ba[0]) + pa[k], La + (bb[k] - bb[0]) + pb[k],
+                        dst + texcl[k], cpo[k], true);
+            if (l == 0) reinterpret_cast<uint32_t*>(g.out + oI)[t0 + k] = prefix + texcl[k];
+        }
     } else {
-        if (wave == 0) {
-            const uint32_t pr = p == 0 ? 0u : lookback(g.flags, p, epoch30, g.ctrl);
-            if (l == 0) {
-                if (p != 0) publish(g.flags, p, epoch30, kFlagPrefix, pr + agg);
-                s_prefix = pr;
-            }
-        }
-        __syncthreads();
-        prefix = s_prefix;
-        dst = reinterpret_cast<raw*>(g.out + oA) + prefix + tile_excl;
-    }
-    if (has_tile) {
-        // phase 2: merge the two runs of each column in row order
-        const int ngroups = one_group ? 1 : PPGroup<E>::count;
-        const uint32_t gcols = one_group ? 64u : PPGroup<E>::cols;
-        for (int h = 0; h < ngroups; h++) {
-            const uint32_t c0 = gcols * h, c1 = c0 + gcols;
-            const bool mine = l >= c0 && l < c1;
-            bool zero;
-            const uint32_t la = one_group ? ca.cnt : pp_stage<E>(ca, cb, pa, pb, c0, c1, in, zero);
-            uint32_t ia = ca.colpref - __shfl(ca.colpref, c0, 64);
-            uint32_t ib = la + cb.colpref - __shfl(cb.colpref, c0, 64);
-            const uint32_t o0 = __shfl(colpref, c0, 64);
-            const uint32_t o1 = c1 == 64 ? tilecnt : __shfl(colpref, c1, 64);
-            uint32_t k = colpref - o0;
-            uint64_t todo = mine ? (wa | wb) : 0ull;
-            while (__any(todo != 0ull)) {
-                if (todo) {
-                    const uint32_t r = (uint32_t)__builtin_ctzll(todo);
-                    todo &= todo - 1ull;
-                    uint32_t xa = 0, xb = 0;
-                    if ((ca.w >> r) & 1ull) { xa = in[ia]; ia++; }
-                    if ((cb.w >> r) & 1ull) { xb = in[ib]; ib++; }
-                    if ((wo >> r) & 1ull) { out[k] = (raw)oplus(E{}, xa, xb); k++; }
+        // phase 1, one tile at a time
+#pragma unroll 1
+        for (int k = 0; k < K; k++) {
+            const uint64_t t = t0 + k;
+            uint32_t tc = 0;
+            if (t < g.T) {
+                const PiciCols ca = pici_columns(load_pici_meta<E>(g.a.data, t, g.n), nnz_a, t, g.n, g.ctrl);
+                const PiciCols cb = pici_columns(load_pici_meta<E>(g.b.data, t, g.n), nnz_b, t, g.n, g.ctrl);
+                const bool one = ca.cnt + cb.cnt <= kChunkVals;
+                const int ngroups = one ? 1 : PPGroup::count;
+                const uint32_t gcols = one ? 64u : PPGroup::cols;
+                uint64_t cancel = 0;
+                for (int h = 0; h < ngroups; h++) {
+                    const uint32_t c0 = gcols * h, c1 = c0 + gcols;
+                    bool zg;
+                    const uint32_t la = pp_stage<E>(ca, cb, Aa + ca.base, Ab + cb.base, c0, c1, in, zg);
+                    cancel |= pp_cancel<E>(ca.w, cb.w, in, ca.colpref - __shfl(ca.colpref, c0, 64),
+                                           la + cb.colpref - __shfl(cb.colpref, c0, 64), zg, l >= c0 && l < c1);
+                    wave_lds_sync();
                 }
+                const uint64_t wo = (ca.w | cb.w) & ~cancel;
+                Bout[t * 64 + l] = wo;
+                tc = (uint32_t)__popcll(wo);
+                tc = __shfl(wave_excl_scan(tc) + tc, 63, 64);
             }
-            wave_lds_sync();
-            for (uint32_t i = l; i < o1 - o0; i += 64) dst[o0 + i] = out[i];
-            wave_lds_sync();
+            if (l == 0) s_tcnt[wave][k] = tc;
+            agg += tc;
         }
-        if (l == 0) reinterpret_cast<uint32_t*>(g.out + oI)[t] = Deferred ? tile_excl : prefix + tile_excl;
+        if (l == 0) publish(g.flags, p, epoch30, (p == 0 && !Deferred) ? kFlagPrefix : kFlagAggregate, agg);
+        if constexpr (Deferred) {
+            dst = reinterpret_cast<raw*>(g.slots) + (uint64_t)p * kPartElems;
+        } else {
+            prefix = p == 0 ? 0u : lookback(g.flags, p, epoch30, g.ctrl);
+            if (l == 0 && p != 0) publish(g.flags, p, epoch30, kFlagPrefix, prefix + agg);
+            dst = reinterpret_cast<raw*>(g.out + oA) + prefix;
+        }
+        // phase 2, one tile at a time
+        uint32_t texcl = 0;
+#pragma unroll 1
+        for (int k = 0; k < K; k++) {
+            const uint64_t t = t0 + k;
+            if (t >= g.T) break;
+            const PiciCols ca = pici_columns(load_pici_meta<E>(g.a.data, t, g.n), nnz_a, t, g.n, g.ctrl);
+            const PiciCols cb = pici_columns(load_pici_meta<E>(g.b.data, t, g.n), nnz_b, t, g.n, g.ctrl);
+            const uint64_t wo = Bout[t * 64 + l];             // this wave's own phase-1 store
+            const uint32_t cpo = wave_excl_scan((uint32_t)__popcll(wo));
+            const bool one = ca.cnt + cb.cnt <= kChunkVals;
+            const int ngroups = one ? 1 : PPGroup::count;
+            const uint32_t gcols = one ? 64u : PPGroup::cols;
+            for (int h = 0; h < ngroups; h++) {
+                const uint32_t c0 = gcols * h, c1 = c0 + gcols;
+                bool zg;
+                const uint32_t la = pp_stage<E>(ca, cb, Aa + ca.base, Ab + cb.base, c0, c1, in, zg);
+                pp_merge<E>(ca.w, cb.w, wo, in, ca.colpref - __shfl(ca.colpref, c0, 64),
+                            la + cb.colpref - __shfl(cb.colpref, c0, 64), dst + texcl, cpo, l >= c0 && l < c1);
+                wave_lds_sync();
+            }
+            if (l == 0) reinterpret_cast<uint32_t*>(g.out + oI)[t] = prefix + texcl;
+            texcl += s_tcnt[wave][k];
+        }
     }
     if constexpr (!Deferred) {
-        if (p == g.nparts - 1 && threadIdx.x == 0) {
+        if (p == g.nparts - 1 && l == 0) {
             const uint64_t nnz = (uint64_t)prefix + agg;
             uint32_t* I = reinterpret_cast<uint32_t*>(g.out + oI);
             I[g.T] = (uint32_t)nnz;
@@ -748,50 +881,43 @@ __global__ void __launch_bounds__(kBlockThreads) k_pp_to_pici(PiciSinkArgs g) {
 // (which only waits for inclusive prefixes published by this pass).
 constexpr uint32_t kPlaceDirectMax = 16384;
 
-constexpr uint32_t kPlacePer = 8;          // partitions placed by one block (2 per wave)
+constexpr uint32_t kNoAggregate = 0xFFFFFFFFu;   // a partition the first pass did not publish
+constexpr uint32_t kPlacePer = kWavesPerBlock;   // partitions placed by one block (one per wave)
 
+// Each wave moves one partition.  Its own aggregate, the first kEarly slot
+// values per lane, its tiles' relative offsets and the block's share of the
+// predecessor sum are read at once; once the aggregate is known the rest of
+// the partition's values (up to kMore per lane) are read while the block
+// combines the predecessor sum; then every store.  Reads waited for after a
+// store would also wait for that store, hence all reads first.
 template <class E>
 __global__ void __launch_bounds__(kBlockThreads) k_place(PiciSinkArgs g) {
     using raw = typename E::raw;
     constexpr int J = 8;
-    constexpr uint32_t kEarly = 4;          // slot values per lane read before the offsets are known
-    __shared__ uint32_t s_base, s_part[kWavesPerBlock], s_agg[kPlacePer], s_prefix[kPlacePer];
+    constexpr uint32_t kEarly = 4;          // slot values per lane read before the aggregate is known
+    constexpr uint32_t kMore = 16;          // slot values per lane read once it is
+    __shared__ uint32_t s_base, s_part[kWavesPerBlock], s_agg[kPlacePer];
     const uint32_t wave = threadIdx.x >> 6, l = lane_id();
     const uint32_t p0 = blockIdx.x * kPlacePer;
+    const uint32_t p = p0 + wave;
+    const bool mine = p < g.nparts;
     const uint32_t epoch30 = g.epoch & 0x3FFFFFFFu;
     const uint64_t oI = off_I(g.n), oA = off_A(g.n);
     uint32_t* I = reinterpret_cast<uint32_t*>(g.out + oI);
-    // independent of the offsets, so issued first: the first slot values of
-    // this wave's two partitions (a slot always has kPartElems of room) and
-    // their partition-relative tile offsets
-    raw early[2][kEarly];
-    uint32_t tile_rel[2] = {0u, 0u};
+    const raw* slot = reinterpret_cast<const raw*>(g.slots) + (uint64_t)p * kPartElems;
+
+    // independent of every offset: own aggregate word, first slot values
+    // (a slot always has kPartElems of room), the tiles' relative offsets
+    const uint64_t f = mine ? g.flags[p] : 0ull;
+    raw early[kEarly];
 #pragma unroll
-    for (uint32_t h = 0; h < 2; h++) {
-        const uint32_t p = p0 + wave + kWavesPerBlock * h;
-        const raw* slot = reinterpret_cast<const raw*>(g.slots) + (uint64_t)p * kPartElems;
-#pragma unroll
-        for (uint32_t u = 0; u < kEarly; u++) early[h][u] = p < g.nparts ? slot[l + 64 * u] : (raw)0;
-        const uint64_t t = (uint64_t)p * kTilesPerPart + l;
-        if (p < g.nparts && l < kTilesPerPart && t < g.T) tile_rel[h] = I[t];
-    }
-    if (threadIdx.x < kPlacePer) {
-        const uint32_t p = p0 + threadIdx.x;
-        uint32_t agg = 0;
-        if (p < g.nparts) {
-            const uint64_t f = g.flags[p];
-            agg = (uint32_t)f;
-            if ((uint32_t)(f >> 34) != epoch30 || agg > kPartElems) {   // the first pass did not run
-                set_status(g.ctrl, SPCCL_ERR_WORKSPACE);
-                agg = 0;
-            }
-        }
-        s_agg[threadIdx.x] = agg;
-    }
+    for (uint32_t u = 0; u < kEarly; u++) early[u] = mine ? slot[l + 64 * u] : (raw)0;
+    const uint64_t t = (uint64_t)p * kTilesPerPart + l;
+    const uint32_t tile_rel = (mine && l < kTilesPerPart && t < g.T) ? I[t] : 0u;
+    // this block's share of the sum of all earlier aggregates: two words per
+    // 16-byte load, eight independent loads in flight per thread
+    uint32_t part = 0;
     if (g.nparts <= kPlaceDirectMax) {
-        // sum of all earlier aggregates: two words per 16-byte load, eight
-        // independent loads in flight per thread
-        uint32_t part = 0;
         const uint4* f2 = reinterpret_cast<const uint4*>(g.flags);
         const uint32_t pairs = p0 / 2;                          // p0 is even
         for (uint32_t q0 = threadIdx.x; q0 < pairs; q0 += 8 * kBlockThreads) {
@@ -804,66 +930,84 @@ __global__ void __launch_bounds__(kBlockThreads) k_place(PiciSinkArgs g) {
 #pragma unroll
             for (int u = 0; u < 8; u++) part += x[u].x + x[u].z;    // low words hold the aggregates
         }
-        part = wave_sum(part);
-        if (l == 0) s_part[wave] = part;
+    }
+    uint32_t agg = (uint32_t)f;
+    bool bad = mine && ((uint32_t)(f >> 34) != epoch30 || agg > kPartElems);   // the first pass did not run
+    if (bad) agg = 0;
+    if (!mine) agg = 0;
+    raw more[kMore];
+#pragma unroll
+    for (uint32_t u = 0; u < kMore; u++) {
+        const uint32_t i = l + 64 * (kEarly + u);
+        more[u] = i < agg ? slot[i] : (raw)0;
+    }
+    part = wave_sum(part);
+    if (l == 0) {
+        s_part[wave] = part;
+        s_agg[wave] = bad ? kNoAggregate : agg;
+        if (bad) set_status(g.ctrl, SPCCL_ERR_WORKSPACE);
+    }
+    __syncthreads();
+    bool any_bad = false;
+    uint32_t prefix = 0, tot = 0;
+#pragma unroll
+    for (uint32_t k = 0; k < kPlacePer; k++) {
+        const uint32_t ak = s_agg[k];
+        any_bad = any_bad || ak == kNoAggregate;
+        prefix += k < wave ? ak : 0u;
+        tot += ak;
+    }
+    if (any_bad) return;          // the first pass stopped at a bad header: write nothing
+    if (g.nparts <= kPlaceDirectMax) {
+        uint32_t base = 0;
+#pragma unroll
+        for (uint32_t k = 0; k < kWavesPerBlock; k++) base += s_part[k];
+        prefix += base;
+    } else {
+        if (wave == 0) {
+            Window<J> win{};
+            if (p0 != 0) win = load_window<J>(g.flags, (int64_t)p0 - 1);
+            const uint32_t base = p0 == 0 ? 0u : lookback_from<J>(g.flags, p0, epoch30, g.ctrl, win);
+            if (l == 0) {
+                const uint32_t last = (g.nparts - p0 < kPlacePer ? g.nparts - p0 : kPlacePer) - 1;
+                publish(g.flags, p0 + last, epoch30, kFlagPrefix, base + tot);
+                s_base = base;
+            }
+        }
         __syncthreads();
-        if (threadIdx.x == 0) {
-            uint32_t base = 0;
-            for (uint32_t k = 0; k < kWavesPerBlock; k++) base += s_part[k];
-            s_base = base;
+        prefix += s_base;
+    }
+    if (!mine) return;
+    raw* dst = reinterpret_cast<raw*>(g.out + oA) + prefix;
+#pragma unroll
+    for (uint32_t u = 0; u < kEarly; u++) {
+        const uint32_t i = l + 64 * u;
+        if (i < agg) dst[i] = early[u];
+    }
+#pragma unroll
+    for (uint32_t u = 0; u < kMore; u++) {
+        const uint32_t i = l + 64 * (kEarly + u);
+        if (i < agg) dst[i] = more[u];
+    }
+    for (uint32_t i0 = l + 64 * (kEarly + kMore); i0 < agg; i0 += 64 * 16) {
+        raw x[16];
+#pragma unroll
+        for (int u = 0; u < 16; u++) {
+            const uint32_t i = i0 + 64 * u;
+            x[u] = i < agg ? slot[i] : (raw)0;
         }
-    } else if (wave == 0) {
-        Window<J> win{};
-        if (p0 != 0) win = load_window<J>(g.flags, (int64_t)p0 - 1);
-        const uint32_t base = p0 == 0 ? 0u : lookback_from<J>(g.flags, p0, epoch30, g.ctrl, win);
-        if (l == 0) {
-            uint32_t tot = 0;
-            for (uint32_t k = 0; k < kPlacePer; k++) tot += s_agg[k];
-            const uint32_t last = (g.nparts - p0 < kPlacePer ? g.nparts - p0 : kPlacePer) - 1;
-            publish(g.flags, p0 + last, epoch30, kFlagPrefix, base + tot);
-            s_base = base;
+#pragma unroll
+        for (int u = 0; u < 16; u++) {
+            const uint32_t i = i0 + 64 * u;
+            if (i < agg) dst[i] = x[u];
         }
     }
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        uint32_t run = s_base;
-        for (uint32_t k = 0; k < kPlacePer; k++) { s_prefix[k] = run; run += s_agg[k]; }
-    }
-    __syncthreads();
-#pragma unroll
-    for (uint32_t h = 0; h < 2; h++) {
-        const uint32_t k = wave + kWavesPerBlock * h;
-        const uint32_t p = p0 + k;
-        if (p >= g.nparts) continue;
-        const uint32_t prefix = s_prefix[k], agg = s_agg[k];
-        const raw* slot = reinterpret_cast<const raw*>(g.slots) + (uint64_t)p * kPartElems;
-        raw* dst = reinterpret_cast<raw*>(g.out + oA) + prefix;
-#pragma unroll
-        for (uint32_t u = 0; u < kEarly; u++) {
-            const uint32_t i = l + 64 * u;
-            if (i < agg) dst[i] = early[h][u];
-        }
-        for (uint32_t i0 = l + 64 * kEarly; i0 < agg; i0 += 64 * 8) {
-            raw x[8];
-#pragma unroll
-            for (int u = 0; u < 8; u++) {
-                const uint32_t i = i0 + 64 * u;
-                x[u] = i < agg ? slot[i] : (raw)0;
-            }
-#pragma unroll
-            for (int u = 0; u < 8; u++) {
-                const uint32_t i = i0 + 64 * u;
-                if (i < agg) dst[i] = x[u];
-            }
-        }
-        const uint64_t t = (uint64_t)p * kTilesPerPart + l;
-        if (l < kTilesPerPart && t < g.T) I[t] = tile_rel[h] + prefix;
-        if (p == g.nparts - 1 && l == 0) {
-            const uint64_t nnz = (uint64_t)prefix + agg;
-            I[g.T] = (uint32_t)nnz;
-            for (uint64_t b = oI + 4 * (g.T + 1); b < oA; b += 4) *reinterpret_cast<uint32_t*>(g.out + b) = 0u;
-            write_header(g.out, kFmtPici, E::dtype, g.n, nnz, oI, oA, oA + nnz * sizeof(raw));
-        }
+    if (l < kTilesPerPart && t < g.T) I[t] = tile_rel + prefix;
+    if (p == g.nparts - 1 && l == 0) {
+        const uint64_t nnz = (uint64_t)prefix + agg;
+        I[g.T] = (uint32_t)nnz;
+        for (uint64_t b = oI + 4 * (g.T + 1); b < oA; b += 4) *reinterpret_cast<uint32_t*>(g.out + b) = 0u;
+        write_header(g.out, kFmtPici, E::dtype, g.n, nnz, oI, oA, oA + nnz * sizeof(raw));
     }
 }
 
@@ -890,41 +1034,14 @@ template <class E, int SA, int SB>
 __global__ void __launch_bounds__(kBlockThreads) k_to_dense(DenseSinkArgs g) {
     using raw = typename E::raw;
     __shared__ raw stage_all[kWavesPerBlock][E::cap];
-    __shared__ uint32_t s_ok;
-    __shared__ uint64_t s_nnz_a, s_nnz_b;
     const uint32_t wave = threadIdx.x >> 6;
-    if (threadIdx.x == 0) {
-        bool ok = true;
-        uint64_t na = 0, nb = 0;
-        if (g.a.hdr) {
-            HeaderView h = read_header(g.a.hdr, g.a.cap, g.n, E::dtype, SA == SRC_PICI ? kFmtPici : kFmtDense);
-            ok = ok && h.ok; na = h.nnz;
-        }
-        if (SB != SRC_NONE && g.b.hdr) {
-            HeaderView h = read_header(g.b.hdr, g.b.cap, g.n, E::dtype, SB == SRC_PICI ? kFmtPici : kFmtDense);
-            ok = ok && h.ok; nb = h.nnz;
-        }
-        s_ok = ok;
-        s_nnz_a = na;
-        s_nnz_b = nb;
-        if (!ok && blockIdx.x == 0) set_status(g.ctrl, SPCCL_ERR_CORRUPT_STREAM);
-        if (ok && blockIdx.x == 0 && g.out_hdr)
-            write_header(g.out_hdr, kFmtDense, E::dtype, g.n, kNnzUnknown, 0, kHeaderBytes,
-                         dense_msg_bytes(g.n, E::dtype));
-    }
-    __syncthreads();
-    if (!s_ok) return;
     const uint64_t t = (uint64_t)blockIdx.x * kWavesPerBlock + wave;
-    if (t >= g.T) return;
+    const bool has_tile = t < g.T;
     uint32_t v[64];
-    if constexpr (SA == SRC_DENSE && SB == SRC_PICI) {
-        fetch_dense_and_pici<E>(g.a.data, g.b.data, s_nnz_b, t, g.n, stage_all[wave], g.ctrl, v);
-    } else if constexpr (SA == SRC_PICI && SB == SRC_DENSE) {
-        fetch_dense_and_pici<E>(g.b.data, g.a.data, s_nnz_a, t, g.n, stage_all[wave], g.ctrl, v);
-    } else {
-        fetch<E, SA, true>(g.a, s_nnz_a, t, g.n, stage_all[wave], g.ctrl, v);
-        if constexpr (SB != SRC_NONE) fetch<E, SB, false>(g.b, s_nnz_b, t, g.n, stage_all[wave], g.ctrl, v);
-    }
+    if (!load_tile_pair<E, SA, SB>(g.a, g.b, t, has_tile, g.n, stage_all[wave], g.ctrl, v)) return;
+    if (blockIdx.x == 0 && threadIdx.x == 0 && g.out_hdr)
+        write_header(g.out_hdr, kFmtDense, E::dtype, g.n, kNnzUnknown, 0, kHeaderBytes, dense_msg_bytes(g.n, E::dtype));
+    if (!has_tile) return;
     store_tile<E>(g.out, t, g.n, v);
 }
 
@@ -941,9 +1058,6 @@ __global__ void __launch_bounds__(kBlockThreads) k_to_dense(DenseSinkArgs g) {
 // is paid once per K tiles.  Tiles that do not fit are expanded one at a
 // time (stage their values, then write), and a tile holding more than
 // kChunkVals values reads its column runs per lane, 16 rows at a time.
-constexpr uint32_t kChunkVals = 1024;
-constexpr int kChunkSlots = kChunkVals / 64;
-
 // Rows [r0, r0 + 16) of dense tile t (bounded buffer loads, zero past n).
 template <class E>
 __device__ __forceinline__ void fetch_dense_rows16(const uint8_t* base, uint64_t t, uint64_t n, int r0,
@@ -1236,14 +1350,15 @@ template <class E>
 spccl_status_t launch_to_pici(int sa, int sb, const PiciSinkArgs& g, hipStream_t st) {
     dim3 grid(g.nparts), block(kBlockThreads);
     if (sa == SRC_PICI && sb == SRC_PICI) {
+        const dim3 wgrid((g.nparts + kWavesPerBlock - 1) / kWavesPerBlock);   // one wave per partition
         if (g.slots) {
-            hipLaunchKernelGGL((k_pp_to_pici<E, true>), grid, block, 0, st, g);
+            hipLaunchKernelGGL((k_pp_to_pici<E, true>), wgrid, block, 0, st, g);
             spccl_status_t st1 = launch_status();
             if (st1 != SPCCL_OK) return st1;
             dim3 pgrid((g.nparts + kPlacePer - 1) / kPlacePer);
             hipLaunchKernelGGL(k_place<E>, pgrid, block, 0, st, g);
         } else {
-            hipLaunchKernelGGL((k_pp_to_pici<E, false>), grid, block, 0, st, g);
+            hipLaunchKernelGGL((k_pp_to_pici<E, false>), wgrid, block, 0, st, g);
         }
         return launch_status();
     }

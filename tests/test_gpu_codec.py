@@ -251,12 +251,24 @@ def test_corrupt_messages_flagged(S):
     # truncated capacity: the header claims more bytes than the buffer holds
     S.spccl_decompress(torch.from_numpy(msg).cuda(), out, ws, msg_bytes=msg.size - 4)
     assert S.spccl_read_status(ws, clear=True) == 4
-    # a Pici message passed where a dense one is declared
-    tm = torch.from_numpy(msg).cuda()
+    # a Pici message passed where a dense one is declared (in a buffer that
+    # could hold a dense message, so the host lets it through)
+    tm = S.alloc_stream(n, O.F32)
+    tm[:msg.size].copy_(torch.from_numpy(msg))
     so = S.alloc_stream(n, O.F32)
     S.spccl_reduce(S.operand(tm, S.SPCCL_STREAM, S.SPCCL_FMT_DENSE), S.operand(to_dev(a)),
                    S.operand(so, S.SPCCL_STREAM, S.SPCCL_FMT_PICI), n, O.F32, ws)
     assert S.spccl_read_status(ws, clear=True) == 4
+    # a buffer smaller than the smallest valid message of its declared format
+    # is refused on the host
+    with pytest.raises(S.SpcclError) as e:
+        S.spccl_reduce(S.operand(tm[:100], S.SPCCL_STREAM, S.SPCCL_FMT_DENSE), S.operand(to_dev(a)),
+                       S.operand(so, S.SPCCL_STREAM, S.SPCCL_FMT_PICI), n, O.F32, ws)
+    assert e.value.status == 2
+    with pytest.raises(S.SpcclError) as e:
+        S.spccl_reduce(S.operand(tm[:O.off_A(n) - 16], S.SPCCL_STREAM, S.SPCCL_FMT_PICI), S.operand(to_dev(a)),
+                       S.operand(so, S.SPCCL_STREAM, S.SPCCL_FMT_PICI), n, O.F32, ws)
+    assert e.value.status == 2
     # and the workspace still works afterwards
     got = gpu_compress(S, a, ws)[:msg.size].cpu().numpy()
     assert_bytes_equal(got, msg, "after errors")
