@@ -50,9 +50,9 @@ METRIC = "dense-equivalent GB/s (and % of HBM peak) for Pici compress/decompress
 
 # ops that launch exactly one kernel, and that kernel's name in profiles
 SINGLE_KERNEL_OPS = {
-    "decompress": "k_gather<F32>",
+    "decompress": "k_gather<F32, 2>",
     "reduce_dense_pici_to_dense": "k_to_dense<F32, 1, 2>",
-    "gather_expand": "k_gather<F32>",
+    "gather_expand": "k_gather<F32, 4>",
     "send": "k_copy_message",
 }
 
@@ -252,6 +252,28 @@ def time_steps(R, steps, warmup, copies):
     return total_ms, wall, per, dense_eq, dom, timed[dom]
 
 
+def copy_ceiling(torch, n, reps=20):
+    """Achievable HBM rate on this device for reference: back-to-back plain
+    device copies of n fp32 elements (n*4 bytes read and written each), so
+    each copy also pays for the previous one's write-back."""
+    src = torch.ones(n, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        dst.copy_(src)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    del src, dst
+    torch.cuda.empty_cache()
+    return {"GBs": round(2 * n * 4 / (ms / 1e3) / 1e9, 1), "bytes_per_copy": 2 * n * 4, "ms_per_copy": round(ms, 5),
+            "what": "torch device copy of 256 MiB fp32, back to back"}
+
+
 def cpu_baseline(permille, n_full, budget_s):
     """The oracle (single thread, pinned to one core) on a bounded sample of
     the same workload: the same op sequence on the first n_sample elements."""
@@ -343,6 +365,7 @@ def main():
     sweep = {}
     del R
     torch.cuda.empty_cache()
+    ceiling = copy_ceiling(torch, args.n)
     for pm in [int(x) for x in args.sweep.split(",") if x.strip()]:
         Rs = Runner(S, torch, args.n, pm, args.copies)
         t_ms, _, p_s, deq, _, _ = time_steps(Rs, max(5, args.steps // 3), 2, args.copies)
@@ -367,7 +390,7 @@ def main():
                                f"sigma={args.permille / 1000}, uniform random nonzero positions, N(0,1) values; "
                                "step = compress, send, decompress, 3 reduce variants, gather-expand, adaptive switch",
                    "n": args.n, "sigma": args.permille / 1000, "parallelism": "1 GPU (virtual ranks)"},
-        "roofline": roof, "cpu_baseline": cpu, "kernels": kernels, "sweep": sweep,
+        "roofline": roof, "cpu_baseline": cpu, "copy_ceiling": ceiling, "kernels": kernels, "sweep": sweep,
         "parity_compress_vs_oracle": parity, "wall_s_timed": round(wall, 3),
         "calibration_copy_bytes": calib,
     }
