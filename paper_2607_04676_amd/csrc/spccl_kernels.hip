@@ -67,22 +67,30 @@ __device__ __forceinline__ uint32_t oplus(BF16, uint32_t a, uint32_t b) {
 // wave primitives
 __device__ __forceinline__ uint32_t lane_id() { return __lane_id(); }
 
-__device__ __forceinline__ uint32_t wave_sum(uint32_t x) {
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o, 64);
-    return x;
+// Inclusive prefix sum over the wave's 64 lanes with DPP moves: shifts by
+// 1, 2, 4, 8 inside each row of 16 lanes (lanes shifted in from outside the
+// row read 0), then each row adds the total of the rows before it (row
+// broadcasts of lanes 15 and 31).  No LDS traffic and no address registers.
+__device__ __forceinline__ uint32_t wave_incl_scan(uint32_t x) {
+    constexpr int kRowShr = 0x110, kRowBcast15 = 0x142, kRowBcast31 = 0x143;
+    int v = (int)x;
+    v += __builtin_amdgcn_update_dpp(0, v, kRowShr + 1, 0xf, 0xf, false);
+    v += __builtin_amdgcn_update_dpp(0, v, kRowShr + 2, 0xf, 0xf, false);
+    v += __builtin_amdgcn_update_dpp(0, v, kRowShr + 4, 0xf, 0xf, false);
+    v += __builtin_amdgcn_update_dpp(0, v, kRowShr + 8, 0xf, 0xf, false);
+    v += __builtin_amdgcn_update_dpp(0, v, kRowBcast15, 0xa, 0xf, false);
+    v += __builtin_amdgcn_update_dpp(0, v, kRowBcast31, 0xc, 0xf, false);
+    return (uint32_t)v;
 }
 
-__device__ __forceinline__ uint32_t wave_excl_scan(uint32_t x) {
-    uint32_t inc = x;
-    const uint32_t l = lane_id();
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-        uint32_t y = __shfl_up(inc, o, 64);
-        if (l >= (uint32_t)o) inc += y;
-    }
-    return inc - x;
+__device__ __forceinline__ uint32_t wave_excl_scan(uint32_t x) { return wave_incl_scan(x) - x; }
+
+// x of lane `lane`, which must be the same in every lane (a scalar read).
+__device__ __forceinline__ uint32_t lane_bcast(uint32_t x, uint32_t lane) {
+    return (uint32_t)__builtin_amdgcn_readlane((int)x, (int)lane);
 }
+
+__device__ __forceinline__ uint32_t wave_sum(uint32_t x) { return lane_bcast(wave_incl_scan(x), 63); }
 
 // Order this wave's LDS accesses: a wave's LDS operations execute in order,
 // so waiting for its own outstanding ones (and stopping the compiler from
@@ -183,7 +191,10 @@ __device__ __forceinline__ void fetch_dense(const uint8_t* base, uint64_t t, uin
     const uint32_t bytes = (uint32_t)((rem < kTileElems ? rem : kTileElems) * sizeof(raw));
     const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
         const_cast<uint8_t*>(base) + (rem ? start : 0) * sizeof(raw), (short)0, (int)bytes, kBufferWord3);
-    const uint32_t lo = lane_id() * (uint32_t)sizeof(raw);
+    // an opaque lane offset: in a loop the compiler would otherwise hoist one
+    // offset register per row instead of using the immediate offsets
+    uint32_t lo = lane_id() * (uint32_t)sizeof(raw);
+    asm volatile("" : "+v"(lo));
 #pragma unroll
     for (int r = 0; r < 64; r++) {
         uint32_t x;
@@ -236,7 +247,7 @@ __device__ __forceinline__ PiciCols pici_columns(PiciMeta m, uint64_t nnz, uint6
     }
     uint32_t c = (uint32_t)__popcll(w);
     uint32_t colpref = wave_excl_scan(c);
-    uint32_t cnt = __shfl(colpref + c, 63, 64);
+    uint32_t cnt = lane_bcast(colpref + c, 63);
     const bool bad =
         beyond || (uint64_t)m.base + cnt > nnz || m.base + cnt != m.next || (t + 1 == T && (uint64_t)m.next != nnz);
     if (bad) {
@@ -292,8 +303,8 @@ __device__ __forceinline__ void expand_pici(PiciCols pc, const uint8_t* msg, uin
 #pragma unroll 1
     for (int h = 0; h < ngroups; h++) {
         const uint32_t c0 = gcols * h, c1 = c0 + gcols;
-        const uint32_t lo = one ? 0u : __shfl(colpref, c0, 64);
-        const uint32_t hi = (one || c1 == 64) ? cnt : __shfl(colpref, c1, 64);
+        const uint32_t lo = one ? 0u : lane_bcast(colpref, c0);
+        const uint32_t hi = (one || c1 == 64) ? cnt : lane_bcast(colpref, c1);
         stage_values<E>(src + lo, hi - lo, stage);
         wave_lds_sync();
         const uint64_t wm = (l >= c0 && l < c1) ? w : 0ull;
@@ -363,6 +374,22 @@ __device__ __forceinline__ bool load_tile_pair(const DevOperand& a, const DevOpe
             expand_pici<E, !dense_first && SA != SRC_PICI>(pici_columns(mb, nnzb, t, n, ctrl), b.data, n, stage, v);
     }
     return true;
+}
+
+// Bit r set iff v[r] is nonzero.  Each half is built as a doubling chain
+// from its top row down (one compare and one add-with-carry per row, written
+// out so that the compiler keeps no per-row constants live).
+__device__ __forceinline__ uint64_t nonzero_rows(const uint32_t (&v)[64]) {
+    uint32_t hi = 0, lo = 0;
+#pragma unroll
+    for (int r = 63; r >= 32; r--)
+        asm volatile("v_cmp_ne_u32_e32 vcc, 0, %1\n\tv_addc_co_u32_e32 %0, vcc, %0, %0, vcc"
+                     : "+v"(hi) : "v"(v[r]) : "vcc");
+#pragma unroll
+    for (int r = 31; r >= 0; r--)
+        asm volatile("v_cmp_ne_u32_e32 vcc, 0, %1\n\tv_addc_co_u32_e32 %0, vcc, %0, %0, vcc"
+                     : "+v"(lo) : "v"(v[r]) : "vcc");
+    return ((uint64_t)hi << 32) | lo;
 }
 
 // ---------------------------------------------------------------------------
@@ -493,13 +520,12 @@ __global__ void __launch_bounds__(kBlockThreads) k_to_pici(PiciSinkArgs g) {
     if (has_tile) {
         // every source reads as zero at positions >= n (bounded buffer loads,
         // Pici tiles checked against the array's end)
-#pragma unroll
-        for (int r = 0; r < 64; r++) w |= (uint64_t)(v[r] != 0u) << r;
+        w = nonzero_rows(v);
         c = (uint32_t)__popcll(w);
         reinterpret_cast<uint64_t*>(g.out + kHeaderBytes)[t * 64 + l] = w;
     }
     const uint32_t colpref = wave_excl_scan(c);
-    const uint32_t tilecnt = __shfl(colpref + c, 63, 64);
+    const uint32_t tilecnt = lane_bcast(colpref + c, 63);
     if (l == 0) s_cnt[wave] = tilecnt;
     __syncthreads();
 
@@ -531,8 +557,8 @@ __global__ void __launch_bounds__(kBlockThreads) k_to_pici(PiciSinkArgs g) {
         } else {
 #pragma unroll
             for (int h = 0; h < E::groups; h++) {
-                const uint32_t lo = __shfl(colpref, E::group_cols * h, 64);
-                const uint32_t hi = h == E::groups - 1 ? tilecnt : __shfl(colpref, E::group_cols * (h + 1), 64);
+                const uint32_t lo = lane_bcast(colpref, E::group_cols * h);
+                const uint32_t hi = h == E::groups - 1 ? tilecnt : lane_bcast(colpref, E::group_cols * (h + 1));
                 const bool mine = l / E::group_cols == (uint32_t)h;
                 uint32_t rank = colpref - lo;
 #pragma unroll
@@ -568,8 +594,8 @@ __global__ void __launch_bounds__(kBlockThreads) k_to_pici(PiciSinkArgs g) {
         } else {
 #pragma unroll
             for (int h = 0; h < E::groups; h++) {
-                const uint32_t lo = __shfl(colpref, E::group_cols * h, 64);
-                const uint32_t hi = h == E::groups - 1 ? tilecnt : __shfl(colpref, E::group_cols * (h + 1), 64);
+                const uint32_t lo = lane_bcast(colpref, E::group_cols * h);
+                const uint32_t hi = h == E::groups - 1 ? tilecnt : lane_bcast(colpref, E::group_cols * (h + 1));
                 const bool mine = l / E::group_cols == (uint32_t)h;
                 uint32_t rank = colpref - lo;
 #pragma unroll
@@ -593,6 +619,7 @@ __global__ void __launch_bounds__(kBlockThreads) k_to_pici(PiciSinkArgs g) {
         write_header(g.out, kFmtPici, E::dtype, g.n, nnz, oI, oA, oA + nnz * sizeof(raw));
     }
 }
+
 
 // ---------------------------------------------------------------------------
 // Pici (+) Pici -> Pici with work proportional to the nonzeros.
@@ -623,10 +650,10 @@ __device__ __forceinline__ uint32_t pp_stage(const PiciCols& ca, const PiciCols&
                                              typename E::raw* in, bool& zero) {
     using raw = typename E::raw;
     const uint32_t l = lane_id();
-    const uint32_t a0 = __shfl(ca.colpref, c0, 64);
-    const uint32_t a1 = c1 == 64 ? ca.cnt : __shfl(ca.colpref, c1, 64);
-    const uint32_t b0 = __shfl(cb.colpref, c0, 64);
-    const uint32_t b1 = c1 == 64 ? cb.cnt : __shfl(cb.colpref, c1, 64);
+    const uint32_t a0 = lane_bcast(ca.colpref, c0);
+    const uint32_t a1 = c1 == 64 ? ca.cnt : lane_bcast(ca.colpref, c1);
+    const uint32_t b0 = lane_bcast(cb.colpref, c0);
+    const uint32_t b1 = c1 == 64 ? cb.cnt : lane_bcast(cb.colpref, c1);
     const uint32_t la = a1 - a0, lb = b1 - b0;
     raw x[kChunkSlots];
 #pragma unroll
@@ -783,7 +810,7 @@ __global__ void __launch_bounds__(kBlockThreads) k_pp_to_pici(PiciSinkArgs g) {
             const uint32_t c = (uint32_t)__popcll(wo[k]);
             cpo[k] = wave_excl_scan(c);
             texcl[k] = agg;
-            agg += __builtin_amdgcn_readfirstlane(__shfl(cpo[k] + c, 63, 64));
+            agg += __builtin_amdgcn_readfirstlane(lane_bcast(cpo[k] + c, 63));
         }
         if (l == 0) publish(g.flags, p, epoch30, (p == 0 && !Deferred) ? kFlagPrefix : kFlagAggregate, agg);
         if constexpr (Deferred) {
@@ -817,14 +844,14 @@ __global__ void __launch_bounds__(kBlockThreads) k_pp_to_pici(PiciSinkArgs g) {
                     const uint32_t c0 = gcols * h, c1 = c0 + gcols;
                     bool zg;
                     const uint32_t la = pp_stage<E>(ca, cb, Aa + ca.base, Ab + cb.base, c0, c1, in, zg);
-                    cancel |= pp_cancel<E>(ca.w, cb.w, in, ca.colpref - __shfl(ca.colpref, c0, 64),
-                                           la + cb.colpref - __shfl(cb.colpref, c0, 64), zg, l >= c0 && l < c1);
+                    cancel |= pp_cancel<E>(ca.w, cb.w, in, ca.colpref - lane_bcast(ca.colpref, c0),
+                                           la + cb.colpref - lane_bcast(cb.colpref, c0), zg, l >= c0 && l < c1);
                     wave_lds_sync();
                 }
                 const uint64_t wo = (ca.w | cb.w) & ~cancel;
                 Bout[t * 64 + l] = wo;
                 tc = (uint32_t)__popcll(wo);
-                tc = __shfl(wave_excl_scan(tc) + tc, 63, 64);
+                tc = lane_bcast(wave_excl_scan(tc) + tc, 63);
             }
             if (l == 0) s_tcnt[wave][k] = tc;
             agg += tc;
@@ -854,8 +881,8 @@ __global__ void __launch_bounds__(kBlockThreads) k_pp_to_pici(PiciSinkArgs g) {
                 const uint32_t c0 = gcols * h, c1 = c0 + gcols;
                 bool zg;
                 const uint32_t la = pp_stage<E>(ca, cb, Aa + ca.base, Ab + cb.base, c0, c1, in, zg);
-                pp_merge<E>(ca.w, cb.w, wo, in, ca.colpref - __shfl(ca.colpref, c0, 64),
-                            la + cb.colpref - __shfl(cb.colpref, c0, 64), dst + texcl, cpo, l >= c0 && l < c1);
+                pp_merge<E>(ca.w, cb.w, wo, in, ca.colpref - lane_bcast(ca.colpref, c0),
+                            la + cb.colpref - lane_bcast(cb.colpref, c0), dst + texcl, cpo, l >= c0 && l < c1);
                 wave_lds_sync();
             }
             if (l == 0) reinterpret_cast<uint32_t*>(g.out + oI)[t] = prefix + texcl;
