@@ -92,6 +92,16 @@ def lib():
         L.orc_ring_all_gather.restype = i32
         L.orc_ring_all_gather.argtypes = [ctypes.POINTER(vp), ctypes.POINTER(vp), i32, u64, i32,
                                           ctypes.POINTER(_Trace)]
+        L.orc_slice_count.restype = u64
+        L.orc_slice_count.argtypes = [u64]
+        L.orc_slice_bytes.restype = u64
+        L.orc_slice_bytes.argtypes = [i32]
+        L.orc_encode_sliced.restype = i32
+        L.orc_encode_sliced.argtypes = [vp, u64, i32, ctypes.c_double, vp, u64]
+        L.orc_decode_sliced.restype = i32
+        L.orc_decode_sliced.argtypes = [vp, u64, vp, u64, i32]
+        L.orc_reduce_sliced.restype = i32
+        L.orc_reduce_sliced.argtypes = [vp, vp, u64, i32, ctypes.c_double, vp, u64, u64, i32]
         L.orc_ring_all_reduce.restype = i32
         L.orc_ring_all_reduce.argtypes = [ctypes.POINTER(vp), ctypes.POINTER(vp), i32, u64, i32,
                                           ctypes.POINTER(_Policy), ctypes.POINTER(_Trace)]
@@ -329,3 +339,66 @@ def header(stream: np.ndarray) -> dict:
         "off_A": int(s[32:40].view(np.uint64)[0]),
         "total_bytes": int(s[40:48].view(np.uint64)[0]),
     }
+
+
+# ---- sliced streams (Sec. III-B phase 2, Sec. V-B) --------------------------------
+
+SLICE_ELEMS = 16384
+
+
+def slice_count(n: int) -> int:
+    return lib().orc_slice_count(n)
+
+
+def slice_bytes(dtype: int) -> int:
+    """Bytes of one slot: the worst-case message of a full slice."""
+    return lib().orc_slice_bytes(dtype)
+
+
+def slice_len(n: int, q: int) -> int:
+    return min(SLICE_ELEMS, n - q * SLICE_ELEMS)
+
+
+def encode_sliced(dense: np.ndarray, dense_thresh: float = -1.0) -> np.ndarray:
+    """The sliced stream of a dense array: slot q holds slice q as a message,
+    dense iff that slice's sparsity is <= dense_thresh.  Bytes of a slot past
+    its message are zero here (the library leaves them unwritten)."""
+    dense = np.ascontiguousarray(dense)
+    n, dt = dense.size, dtype_code(dense)
+    cap = slice_count(n) * slice_bytes(dt)
+    out = np.zeros(max(cap, 1), dtype=np.uint8)
+    _check(lib().orc_encode_sliced(_ptr(dense), n, dt, float(dense_thresh), _ptr(out), cap), "encode_sliced")
+    return out[:cap]
+
+
+def decode_sliced(stream: np.ndarray, n: int, dtype: int) -> np.ndarray:
+    stream = np.ascontiguousarray(stream, dtype=np.uint8)
+    out = np.empty(n, dtype=_np_dtype(dtype))
+    _check(lib().orc_decode_sliced(_ptr(stream), stream.nbytes, _ptr(out), n, dtype), "decode_sliced")
+    return out
+
+
+def reduce_sliced(a: np.ndarray, b: np.ndarray, n: int, dtype: int, out_sliced: bool,
+                  dense_thresh: float = -1.0) -> np.ndarray:
+    """a (dense array) (+) b (sliced stream) -> dense array or sliced stream."""
+    a = np.ascontiguousarray(a)
+    b = np.ascontiguousarray(b, dtype=np.uint8)
+    if out_sliced:
+        cap = slice_count(n) * slice_bytes(dtype)
+        out = np.zeros(max(cap, 1), dtype=np.uint8)
+    else:
+        cap = 0
+        out = np.empty(n, dtype=_np_dtype(dtype))
+    _check(lib().orc_reduce_sliced(_ptr(a), _ptr(b), b.nbytes, 1 if out_sliced else 0, float(dense_thresh),
+                                   _ptr(out), cap, n, dtype), "reduce_sliced")
+    return out[:cap] if out_sliced else out
+
+
+def slot_messages(stream: np.ndarray, n: int, dtype: int) -> list:
+    """The message bytes of every slot (header.total_bytes of each)."""
+    slot = slice_bytes(dtype)
+    out = []
+    for q in range(slice_count(n)):
+        m = stream[q * slot:(q + 1) * slot]
+        out.append(m[:int(m[40:48].view(np.uint64)[0])])
+    return out

@@ -14,6 +14,8 @@
  *   - ring reduce-scatter / all-gather / all-reduce over P virtual ranks
  *                                             (Sec. II-A Eq. 2, Sec. IV-A/B)
  *   - the adaptive dense switch with Eq. 7    (Sec. IV-C)
+ *   - sliced streams: one message per slice, block-local prefix sums
+ *                                             (Sec. III-B phase 2, Sec. V-B)
  *
  * Pici is an exact encoding, so compression is written as its definition:
  * loops over tiles, columns and rows in the order the format fixes.  No
@@ -539,5 +541,83 @@ int orc_ring_all_reduce(const void* const* send, void* const* out, int P, uint64
 done:
     if (red) for (int r = 0; r < P; r++) free(red[r]);
     free(red); free(sig0); free(sigp); free(est); free(fmt);
+    return st;
+}
+
+/* ---- sliced streams (Sec. III-B phase 2 and Sec. V-B) -------------------
+ * Inside a collective the paper compresses independent segments, one per
+ * block, each with a block-local prefix sum, and sends each slice as its own
+ * message behind its own header, in FIFO reservations sized for the worst
+ * case.  A sliced stream is that layout for a whole array: slice q holds the
+ * ORC_SLICE_ELEMS consecutive elements starting at q * ORC_SLICE_ELEMS (the
+ * last slice may be shorter) as an ordinary message -- Pici, or dense -- in
+ * slot q of orc_slice_bytes(dtype) bytes.
+ * Format of each slice: dense iff its own sparsity (counted zeros / length,
+ * in double) is <= dense_thresh; a negative dense_thresh keeps every slice in
+ * Pici.  (Reading: per slice, the count is part of producing the slice, so
+ * the measured sparsity is used, not the Eq. 7 estimate.) */
+#define ORC_SLICE_ELEMS 16384u
+
+uint64_t orc_slice_count(uint64_t n) { return (n + ORC_SLICE_ELEMS - 1) / ORC_SLICE_ELEMS; }
+uint64_t orc_slice_bytes(int dtype) { return orc_stream_bound(ORC_SLICE_ELEMS, dtype); }
+
+static uint64_t slice_len(uint64_t n, uint64_t q) {
+    const uint64_t lo = q * ORC_SLICE_ELEMS;
+    return n - lo < ORC_SLICE_ELEMS ? n - lo : ORC_SLICE_ELEMS;
+}
+
+int orc_encode_sliced(const void* dense, uint64_t n, int dtype, double dense_thresh, uint8_t* out,
+                      uint64_t cap) {
+    if (dtype != ORC_F32 && dtype != ORC_BF16) return ORC_ERR_UNSUPPORTED;
+    const uint64_t S = orc_slice_count(n), slot = orc_slice_bytes(dtype), s = elem_size(dtype);
+    if (cap < S * slot) return ORC_ERR_CAPACITY;
+    for (uint64_t q = 0; q < S; q++) {
+        const uint64_t m = slice_len(n, q);
+        const uint8_t* src = (const uint8_t*)dense + q * ORC_SLICE_ELEMS * s;
+        uint64_t nnz = 0;
+        for (uint64_t i = 0; i < m; i++) nnz += present(load_bits(src, dtype, i)) ? 1u : 0u;
+        const double sigma = (double)(m - nnz) / (double)m;
+        int st;
+        if (sigma <= dense_thresh) {
+            st = orc_encode_dense(src, m, dtype, out + q * slot, slot);
+        } else {
+            uint64_t got = 0;
+            st = orc_compress(src, m, dtype, out + q * slot, slot, &got);
+        }
+        if (st != ORC_OK) return st;
+    }
+    return ORC_OK;
+}
+
+int orc_decode_sliced(const uint8_t* in, uint64_t cap, void* dense, uint64_t n, int dtype) {
+    if (dtype != ORC_F32 && dtype != ORC_BF16) return ORC_ERR_UNSUPPORTED;
+    const uint64_t S = orc_slice_count(n), slot = orc_slice_bytes(dtype), s = elem_size(dtype);
+    if (cap < S * slot) return ORC_ERR_CAPACITY;
+    for (uint64_t q = 0; q < S; q++) {
+        int st = orc_decompress(in + q * slot, slot, (uint8_t*)dense + q * ORC_SLICE_ELEMS * s,
+                                slice_len(n, q), dtype);
+        if (st != ORC_OK) return st;
+    }
+    return ORC_OK;
+}
+
+/* out = a (+) b with a a dense array and b a sliced stream; the result is a
+ * dense array (out_sliced = 0) or a sliced stream with the per-slice format
+ * rule above.  Accumulate densely, then encode -- the paper's reduce step. */
+int orc_reduce_sliced(const void* a, const uint8_t* b, uint64_t cap_b, int out_sliced, double dense_thresh,
+                      void* out, uint64_t cap_out, uint64_t n, int dtype) {
+    if (dtype != ORC_F32 && dtype != ORC_BF16) return ORC_ERR_UNSUPPORTED;
+    const uint64_t s = elem_size(dtype);
+    void* db = malloc(n * s + 1); void* dr = malloc(n * s + 1);
+    int st = ORC_ERR_INVALID_ARG;
+    if (!db || !dr) goto done;
+    st = orc_decode_sliced(b, cap_b, db, n, dtype);
+    if (st) goto done;
+    for (uint64_t i = 0; i < n; i++)
+        store_bits(dr, dtype, i, orc_oplus(load_bits(a, dtype, i), load_bits(db, dtype, i), dtype));
+    if (!out_sliced) { memcpy(out, dr, n * s); st = ORC_OK; }
+    else st = orc_encode_sliced(dr, n, dtype, dense_thresh, (uint8_t*)out, cap_out);
+done:
+    free(db); free(dr);
     return st;
 }

@@ -1,0 +1,103 @@
+"""Pins of the oracle's sliced streams (one message per slice of 16384
+elements, block-local prefix sums; Sec. III-B phase 2 and Sec. V-B) against
+what the format and numpy fix independently: round trips, per-slot headers
+and closed-form sizes, a hand-computed format decision at the threshold, and
+the reduction checked against numpy's IEEE add."""
+import numpy as np
+import pytest
+
+import oracle as O
+import workloads as W
+
+S = O.SLICE_ELEMS
+SIZES = [1, 4097, S, S + 1, 3 * S + 777]
+
+
+def _bits(x):
+    return x.view(np.uint32) if x.dtype == np.float32 else x.view(np.uint16)
+
+
+def _with_specials(x, seed):
+    raw = _bits(x).copy()
+    rng = np.random.default_rng(seed)
+    sp = [0x8000, 0x0001] if x.dtype == np.uint16 else [0x80000000, 0x00000001]
+    for v in sp:
+        raw[rng.integers(0, x.size)] = v
+    return raw.view(x.dtype)
+
+
+@pytest.mark.parametrize("n", SIZES)
+@pytest.mark.parametrize("dtype", [W.F32, W.BF16])
+@pytest.mark.parametrize("thresh", [-1.0, 0.6, 1.0])
+def test_round_trip_and_slot_headers(n, dtype, thresh):
+    dt = O.F32 if dtype == W.F32 else O.BF16
+    x = _with_specials(W.sparse_array(n, max(1, n // 50), [40, n], dtype), n)
+    stream = O.encode_sliced(x, thresh)
+    assert stream.size == O.slice_count(n) * O.slice_bytes(dt)
+    assert O.slice_count(n) == -(-n // S)
+    assert np.array_equal(_bits(O.decode_sliced(stream, n, dt)), _bits(x))
+    for q, msg in enumerate(O.slot_messages(stream, n, dt)):
+        part = _bits(x[q * S:(q + 1) * S])
+        m, nnz = part.size, int(np.count_nonzero(part))
+        h = O.header(msg)
+        assert h["n"] == m
+        dense = (m - nnz) / m <= thresh
+        if dense:
+            assert h["format"] == O.FMT_DENSE and msg.size == 48 + m * O.elem_size(dt)
+            assert np.array_equal(msg[48:].view(part.dtype), part)
+        else:
+            assert h["format"] == O.FMT_PICI and h["nnz"] == nnz
+            assert msg.size == O.pici_bytes(m, dt, nnz)              # closed-form size
+
+
+def test_threshold_decision_hand_computed():
+    """A full slice with 6554 nonzeros has sparsity 9830/16384 = 0.5999755859375,
+    <= 0.6, so it goes dense; with 6553 nonzeros, 9831/16384 = 0.60003662109375,
+    it stays Pici.  The test is inclusive."""
+    for nnz, fmt in ((6554, O.FMT_DENSE), (6553, O.FMT_PICI)):
+        x = W.sparse_array(S, nnz, [41, nnz], W.F32)
+        msg = O.slot_messages(O.encode_sliced(x, 0.6), S, O.F32)[0]
+        assert O.header(msg)["format"] == fmt
+    x = W.sparse_array(S, 6554, [41, 6554], W.F32)
+    assert O.header(O.slot_messages(O.encode_sliced(x, 0.5999755859375), S, O.F32)[0])["format"] == O.FMT_DENSE
+    assert O.header(O.slot_messages(O.encode_sliced(x, 0.5999755859374), S, O.F32)[0])["format"] == O.FMT_PICI
+
+
+def test_slots_are_independent_messages():
+    """Slice q is its own message: changing elements of one slice changes that
+    slot only, and a Pici slot decodes alone to its slice."""
+    n = 3 * S + 100
+    x = W.sparse_array(n, 800, [42], W.F32)
+    a = O.slot_messages(O.encode_sliced(x), n, O.F32)
+    y = x.copy()
+    y[S + 5] = np.float32(3.0)
+    b = O.slot_messages(O.encode_sliced(y), n, O.F32)
+    assert [np.array_equal(p, q) for p, q in zip(a, b)] == [True, False, True, True]
+    for q, msg in enumerate(a):
+        m = O.slice_len(n, q)
+        assert np.array_equal(O.decompress(msg, m, O.F32).view(np.uint32), x[q * S:q * S + m].view(np.uint32))
+
+
+def _np_oplus_f32(x, y):
+    with np.errstate(over="ignore"):
+        s = x + y
+    return np.where(y.view(np.uint32) == 0, x, np.where(x.view(np.uint32) == 0, y, s))
+
+
+@pytest.mark.parametrize("n", [4097, 2 * S + 333])
+@pytest.mark.parametrize("thresh", [-1.0, 0.6, 1.0])
+def test_reduce_sliced_matches_numpy(n, thresh):
+    a = W.sparse_array(n, n // 3, [43, 0], W.F32)
+    b = W.sparse_array(n, n // 40, [43, 1], W.F32)
+    hit = np.flatnonzero((a != 0) & (b != 0))
+    b[hit[:5]] = -a[hit[:5]]                                 # exact cancellations drop
+    sb = O.encode_sliced(b, thresh)
+    want = _np_oplus_f32(a, b)
+    got = O.reduce_sliced(a, sb, n, O.F32, out_sliced=False)
+    assert np.array_equal(got.view(np.uint32), want.view(np.uint32))
+    so = O.reduce_sliced(a, sb, n, O.F32, out_sliced=True, dense_thresh=thresh)
+    assert np.array_equal(O.decode_sliced(so, n, O.F32).view(np.uint32), want.view(np.uint32))
+    for q, msg in enumerate(O.slot_messages(so, n, O.F32)):
+        part = want[q * S:(q + 1) * S].view(np.uint32)
+        m, nnz = part.size, int(np.count_nonzero(part))
+        assert O.header(msg)["format"] == (O.FMT_DENSE if (m - nnz) / m <= thresh else O.FMT_PICI)
