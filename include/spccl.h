@@ -173,6 +173,49 @@ spccl_status_t spccl_gather_expand(const spccl_operand_t* parts, int32_t P,
                                    void* dense_out, uint64_t out_bytes,
                                    void* ws, uint64_t ws_bytes, void* stream);
 
+/* ---- sliced streams (Sec. III-B phase 2; Sec. V-B) -------------------------
+ * Inside its collectives the paper compresses independent segments, one per
+ * block, with block-local prefix sums, and sends every slice as its own
+ * message behind its own header, in FIFO reservations sized for the worst
+ * case.  A sliced stream is that layout for an n-element array: slot q, at
+ * byte q * spccl_slice_bytes(dtype) of the buffer, holds elements
+ * [SPCCL_SLICE_ELEMS q, min(n, SPCCL_SLICE_ELEMS (q + 1))) as an ordinary
+ * message (Pici or dense, the header layout above, n = the slice length).
+ * One device pass produces a slice, with no device-wide scan, and the
+ * format of every slice is decided on the device: a produced slice is dense
+ * iff its own sparsity (zeros / length, in double) is <= dense_thresh (give
+ * a negative threshold to keep every slice in Pici).  Bytes of a slot past
+ * its message are not written.  Sliced streams are 16-byte aligned and hold
+ * spccl_slice_count(n) slots; dense arrays are element-aligned.  ws needs
+ * only the control block (>= 256 bytes).  A slice of an input stream whose
+ * header fails its checks sets SPCCL_ERR_CORRUPT_STREAM and its output
+ * slice (or elements) is not written. */
+#define SPCCL_SLICE_ELEMS 16384
+
+uint64_t spccl_slice_count(uint64_t n);      /* ceil(n / SPCCL_SLICE_ELEMS) */
+uint64_t spccl_slice_bytes(int32_t dtype);   /* bytes of one slot: the worst-case message of a full slice; 0 for an unsupported dtype */
+
+/* dense[0..n) -> sliced stream at out (out_bytes >= slice_count * slice_bytes). */
+spccl_status_t spccl_compress_sliced(const void* dense, uint64_t n, int32_t dtype, double dense_thresh,
+                                     void* out, uint64_t out_bytes, void* ws, uint64_t ws_bytes, void* stream);
+
+/* sliced stream at in -> all n elements of dense (absent elements +0.0). */
+spccl_status_t spccl_decompress_sliced(const void* in, uint64_t in_bytes, void* dense, uint64_t n, int32_t dtype,
+                                       void* ws, uint64_t ws_bytes, void* stream);
+
+/* out = a (+) b (Sec. IV-B) with a a dense array and b a sliced stream; out
+ * is a sliced stream (out_sliced != 0, formats by dense_thresh) or a dense
+ * array, which may be a itself (in-place accumulation; no other overlap).
+ * The reduce-scatter step of the paper's in-collective mode. */
+spccl_status_t spccl_reduce_sliced(const void* a, const void* b, uint64_t b_bytes, void* out, uint64_t out_bytes,
+                                   int32_t out_sliced, double dense_thresh, uint64_t n, int32_t dtype,
+                                   void* ws, uint64_t ws_bytes, void* stream);
+
+/* The virtual-rank send of a sliced stream: every slot's header.total_bytes,
+ * read on the device (no host synchronisation). */
+spccl_status_t spccl_copy_sliced(const void* src, uint64_t src_bytes, void* dst, uint64_t dst_bytes, uint64_t n,
+                                 int32_t dtype, void* ws, uint64_t ws_bytes, void* stream);
+
 /* ---- message transport and inspection ------------------------------------ */
 
 /* The virtual-rank "send": copy header.total_bytes bytes of the message at

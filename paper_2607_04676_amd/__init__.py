@@ -37,7 +37,9 @@ EXPORTS = ("spccl_num_tiles", "spccl_pici_bytes", "spccl_stream_bound", "spccl_w
            "spccl_workspace_init", "spccl_compress", "spccl_decompress", "spccl_encode_dense",
            "spccl_reduce", "spccl_gather_expand", "spccl_copy_message", "spccl_read_header",
            "spccl_read_status", "spccl_status_string", "spccl_vr_scratch_bytes",
-           "spccl_vr_reduce_scatter", "spccl_vr_all_gather", "spccl_vr_all_reduce")
+           "spccl_vr_reduce_scatter", "spccl_vr_all_gather", "spccl_vr_all_reduce",
+           "spccl_slice_count", "spccl_slice_bytes", "spccl_compress_sliced", "spccl_decompress_sliced",
+           "spccl_reduce_sliced", "spccl_copy_sliced")
 
 
 class spccl_operand_t(ctypes.Structure):
@@ -90,6 +92,12 @@ _sigs = {
     "spccl_vr_all_reduce": (_i32, [ctypes.POINTER(_vp), ctypes.POINTER(_vp), _i32, _u64, _i32,
                                    ctypes.POINTER(spccl_policy_t), _vp, _u64, ctypes.POINTER(spccl_trace_t),
                                    _vp]),
+    "spccl_slice_count": (_u64, [_u64]),
+    "spccl_slice_bytes": (_u64, [_i32]),
+    "spccl_compress_sliced": (_i32, [_vp, _u64, _i32, ctypes.c_double, _vp, _u64, _vp, _u64, _vp]),
+    "spccl_decompress_sliced": (_i32, [_vp, _u64, _vp, _u64, _i32, _vp, _u64, _vp]),
+    "spccl_reduce_sliced": (_i32, [_vp, _vp, _u64, _vp, _u64, _i32, ctypes.c_double, _u64, _i32, _vp, _u64, _vp]),
+    "spccl_copy_sliced": (_i32, [_vp, _u64, _vp, _u64, _u64, _i32, _vp, _u64, _vp]),
 }
 for _name, (_res, _args) in _sigs.items():
     _f = getattr(_lib, _name)
@@ -254,6 +262,50 @@ def spccl_vr_all_reduce(send: list, recv: list, scratch: torch.Tensor, policy=No
                                     scratch.data_ptr(), _nbytes(scratch), tr, _stream(stream)),
            "spccl_vr_all_reduce")
     return _trace(tr, P * (P - 1) + P)
+
+
+# ---- sliced streams -----------------------------------------------------------------
+
+SPCCL_SLICE_ELEMS = 16384
+
+
+def spccl_slice_count(n: int) -> int:
+    return _lib.spccl_slice_count(n)
+
+
+def spccl_slice_bytes(dtype: int) -> int:
+    return _lib.spccl_slice_bytes(dtype)
+
+
+def spccl_compress_sliced(dense: torch.Tensor, out: torch.Tensor, ws: torch.Tensor, dense_thresh: float = -1.0,
+                          stream=None) -> None:
+    _check(_lib.spccl_compress_sliced(dense.data_ptr(), dense.numel(), _dt(dense), float(dense_thresh),
+                                      out.data_ptr(), _nbytes(out), ws.data_ptr(), _nbytes(ws), _stream(stream)),
+           "spccl_compress_sliced")
+
+
+def spccl_decompress_sliced(inp: torch.Tensor, dense: torch.Tensor, ws: torch.Tensor, stream=None) -> None:
+    _check(_lib.spccl_decompress_sliced(inp.data_ptr(), _nbytes(inp), dense.data_ptr(), dense.numel(), _dt(dense),
+                                        ws.data_ptr(), _nbytes(ws), _stream(stream)), "spccl_decompress_sliced")
+
+
+def spccl_reduce_sliced(a: torch.Tensor, b: torch.Tensor, out: torch.Tensor, ws: torch.Tensor, out_sliced: bool,
+                        dense_thresh: float = -1.0, stream=None) -> None:
+    """out = a (dense) (+) b (sliced stream); out is a sliced stream or a dense array."""
+    _check(_lib.spccl_reduce_sliced(a.data_ptr(), b.data_ptr(), _nbytes(b), out.data_ptr(), _nbytes(out),
+                                    1 if out_sliced else 0, float(dense_thresh), a.numel(), _dt(a), ws.data_ptr(),
+                                    _nbytes(ws), _stream(stream)), "spccl_reduce_sliced")
+
+
+def spccl_copy_sliced(src: torch.Tensor, dst: torch.Tensor, n: int, dtype: int, ws: torch.Tensor,
+                      stream=None) -> None:
+    _check(_lib.spccl_copy_sliced(src.data_ptr(), _nbytes(src), dst.data_ptr(), _nbytes(dst), n, dtype,
+                                  ws.data_ptr(), _nbytes(ws), _stream(stream)), "spccl_copy_sliced")
+
+
+def alloc_sliced(n: int, dtype: int, device="cuda") -> torch.Tensor:
+    """A uint8 buffer with every slot of an n-element sliced stream."""
+    return torch.empty(max(spccl_slice_count(n) * spccl_slice_bytes(dtype), 16), dtype=torch.uint8, device=device)
 
 
 # ---- tensor helpers (allocation stays with the caller; these only size buffers) -----

@@ -21,6 +21,8 @@ spccl_status_t launch_copy_message(const uint8_t* src, uint64_t src_cap, uint8_t
                                    WsCtrl* ctrl, hipStream_t st);
 spccl_status_t launch_fill_zero(void* p, uint64_t bytes, hipStream_t st);
 spccl_status_t launch_encode_dense_dt(int dtype, const uint8_t* src, uint8_t* out, uint64_t n, hipStream_t st);
+spccl_status_t launch_sliced_dt(int dtype, const SlicedArgs& g, int op, hipStream_t st);
+spccl_status_t launch_copy_sliced(const SlicedArgs& g, hipStream_t st);
 }  // namespace spccl
 
 using namespace spccl;
@@ -272,6 +274,93 @@ spccl_status_t spccl_copy_message(const void* src, uint64_t src_bytes, void* dst
     if (st != SPCCL_OK) return st;
     return launch_copy_message(static_cast<const uint8_t*>(src), src_bytes, static_cast<uint8_t*>(dst), dst_bytes,
                                static_cast<WsCtrl*>(ws), as_stream(stream));
+}
+
+/* ---- sliced streams ---------------------------------------------------------- */
+
+uint64_t spccl_slice_count(uint64_t n) { return num_slices(n); }
+
+uint64_t spccl_slice_bytes(int32_t dtype) { return dtype_ok(dtype) ? slice_slot_bytes(dtype) : 0; }
+
+namespace {
+
+// Common checks of the sliced entry points: a dense array (element-aligned,
+// n elements) and sliced streams (16-byte aligned, every slot present).
+spccl_status_t check_sliced_args(uint64_t n, int32_t dtype, void* ws, uint64_t ws_bytes) {
+    if (!dtype_ok(dtype)) return SPCCL_ERR_UNSUPPORTED;
+    if (n >= (1ull << 32)) return SPCCL_ERR_UNSUPPORTED;
+    return check_ws(ws, ws_bytes, kWsFlagsOffset);
+}
+
+spccl_status_t check_dense_arg(const void* p, uint64_t bytes, uint64_t n, int32_t dtype) {
+    if (!p || !aligned_elem(p, dtype)) return SPCCL_ERR_INVALID_ARG;
+    return bytes < n * elem_bytes(dtype) ? SPCCL_ERR_CAPACITY : SPCCL_OK;
+}
+
+spccl_status_t check_sliced_arg(const void* p, uint64_t bytes, uint64_t n, int32_t dtype) {
+    if (!p || !aligned16(p)) return SPCCL_ERR_INVALID_ARG;
+    return bytes < num_slices(n) * slice_slot_bytes(dtype) ? SPCCL_ERR_CAPACITY : SPCCL_OK;
+}
+
+}  // namespace
+
+spccl_status_t spccl_compress_sliced(const void* dense, uint64_t n, int32_t dtype, double dense_thresh, void* out,
+                                     uint64_t out_bytes, void* ws, uint64_t ws_bytes, void* stream) {
+    spccl_status_t st = check_sliced_args(n, dtype, ws, ws_bytes);
+    if (st == SPCCL_OK) st = check_dense_arg(dense, n * elem_bytes(dtype), n, dtype);
+    if (st == SPCCL_OK) st = check_sliced_arg(out, out_bytes, n, dtype);
+    if (st != SPCCL_OK) return st;
+    if (overlaps(dense, n * elem_bytes(dtype), out, out_bytes)) return SPCCL_ERR_INVALID_ARG;
+    if (n == 0) return SPCCL_OK;
+    SlicedArgs g{static_cast<const uint8_t*>(dense), nullptr, static_cast<uint8_t*>(out), n, slice_slot_bytes(dtype),
+                 dense_thresh, static_cast<WsCtrl*>(ws)};
+    return launch_sliced_dt(dtype, g, kSlicedCompress, as_stream(stream));
+}
+
+spccl_status_t spccl_decompress_sliced(const void* in, uint64_t in_bytes, void* dense, uint64_t n, int32_t dtype,
+                                       void* ws, uint64_t ws_bytes, void* stream) {
+    spccl_status_t st = check_sliced_args(n, dtype, ws, ws_bytes);
+    if (st == SPCCL_OK) st = check_sliced_arg(in, in_bytes, n, dtype);
+    if (st == SPCCL_OK) st = check_dense_arg(dense, n * elem_bytes(dtype), n, dtype);
+    if (st != SPCCL_OK) return st;
+    if (overlaps(in, in_bytes, dense, n * elem_bytes(dtype))) return SPCCL_ERR_INVALID_ARG;
+    if (n == 0) return SPCCL_OK;
+    SlicedArgs g{static_cast<const uint8_t*>(in), nullptr, static_cast<uint8_t*>(dense), n, slice_slot_bytes(dtype),
+                 0.0, static_cast<WsCtrl*>(ws)};
+    return launch_sliced_dt(dtype, g, kSlicedExpand, as_stream(stream));
+}
+
+spccl_status_t spccl_reduce_sliced(const void* a, const void* b, uint64_t b_bytes, void* out, uint64_t out_bytes,
+                                   int32_t out_sliced, double dense_thresh, uint64_t n, int32_t dtype, void* ws,
+                                   uint64_t ws_bytes, void* stream) {
+    spccl_status_t st = check_sliced_args(n, dtype, ws, ws_bytes);
+    if (st == SPCCL_OK) st = check_dense_arg(a, n * elem_bytes(dtype), n, dtype);
+    if (st == SPCCL_OK) st = check_sliced_arg(b, b_bytes, n, dtype);
+    if (st == SPCCL_OK)
+        st = out_sliced ? check_sliced_arg(out, out_bytes, n, dtype) : check_dense_arg(out, out_bytes, n, dtype);
+    if (st != SPCCL_OK) return st;
+    const uint64_t ab = n * elem_bytes(dtype);
+    // a dense output may overwrite a in place (each element is read before it is written, by the same lane)
+    if (overlaps(b, b_bytes, out, out_bytes) || overlaps(a, ab, b, b_bytes)) return SPCCL_ERR_INVALID_ARG;
+    if (out_sliced ? overlaps(a, ab, out, out_bytes) : (overlaps(a, ab, out, out_bytes) && a != out))
+        return SPCCL_ERR_INVALID_ARG;
+    if (n == 0) return SPCCL_OK;
+    SlicedArgs g{static_cast<const uint8_t*>(a), static_cast<const uint8_t*>(b), static_cast<uint8_t*>(out), n,
+                 slice_slot_bytes(dtype), dense_thresh, static_cast<WsCtrl*>(ws)};
+    return launch_sliced_dt(dtype, g, out_sliced ? kSlicedReduceToSliced : kSlicedReduceToDense, as_stream(stream));
+}
+
+spccl_status_t spccl_copy_sliced(const void* src, uint64_t src_bytes, void* dst, uint64_t dst_bytes, uint64_t n,
+                                 int32_t dtype, void* ws, uint64_t ws_bytes, void* stream) {
+    spccl_status_t st = check_sliced_args(n, dtype, ws, ws_bytes);
+    if (st == SPCCL_OK) st = check_sliced_arg(src, src_bytes, n, dtype);
+    if (st == SPCCL_OK) st = check_sliced_arg(dst, dst_bytes, n, dtype);
+    if (st != SPCCL_OK) return st;
+    if (overlaps(src, src_bytes, dst, dst_bytes)) return SPCCL_ERR_INVALID_ARG;
+    if (n == 0) return SPCCL_OK;
+    SlicedArgs g{static_cast<const uint8_t*>(src), nullptr, static_cast<uint8_t*>(dst), n, slice_slot_bytes(dtype),
+                 0.0, static_cast<WsCtrl*>(ws)};
+    return launch_copy_sliced(g, as_stream(stream));
 }
 
 spccl_status_t spccl_read_header(const void* msg, spccl_header_t* host_out, void* stream) {

@@ -88,4 +88,25 @@ struct GatherArgs {
     WsCtrl* ctrl;
 };
 
+// Sliced streams: slot q of a stream holds elements [kSliceElems q, ...) as
+// an ordinary message; one block (4 tiles) produces or consumes one slice.
+constexpr uint64_t kSliceElems = kPartElems;
+__host__ __device__ inline uint64_t num_slices(uint64_t n) { return (n + kSliceElems - 1) / kSliceElems; }
+__host__ __device__ inline uint64_t slice_slot_bytes(int dtype) {
+    const uint64_t p = pici_bytes(kSliceElems, dtype, kSliceElems), d = dense_msg_bytes(kSliceElems, dtype);
+    return p > d ? p : d;
+}
+
+enum SlicedOp { kSlicedCompress = 0, kSlicedReduceToSliced = 1, kSlicedReduceToDense = 2, kSlicedExpand = 3 };
+
+struct SlicedArgs {
+    const uint8_t* a;      // dense input array, or a sliced stream (expand, copy)
+    const uint8_t* b;      // sliced input stream, or nullptr
+    uint8_t* out;          // sliced output stream, or dense output array
+    uint64_t n;            // elements
+    uint64_t slot;         // bytes per slot
+    double thresh;         // a produced slice is dense iff its sparsity <= thresh
+    WsCtrl* ctrl;
+};
+
 }  // namespace spccl

@@ -1133,41 +1133,29 @@ __device__ __forceinline__ void store_from_stage(typename E::raw* col, uint64_t 
     }
 }
 
+// Tiles [t0, t0 + K) of one checked message (format fmt, nnz nonzeros, n
+// elements, T tiles; d = its dense values for a dense message, msg = the
+// message for a Pici one) expanded into out[0 .. n).  One wave; all reads
+// before the first store (see k_gather).
 template <class E, int K>
-__global__ void __launch_bounds__(kBlockThreads) k_gather(GatherArgs g) {
+__device__ __forceinline__ void expand_tiles(const uint8_t* msg, const uint8_t* d, uint32_t fmt, uint64_t nnz,
+                                             uint64_t n, uint64_t T, uint64_t t0, typename E::raw* out,
+                                             typename E::raw* stage, WsCtrl* ctrl) {
     using raw = typename E::raw;
-    __shared__ raw stage_all[kWavesPerBlock][kChunkVals];
-    __shared__ uint32_t s_ok, s_fmt;
-    __shared__ uint64_t s_nnz;
-    const uint32_t wave = threadIdx.x >> 6, l = lane_id();
-    const DevOperand op = g.part[blockIdx.y];
-    if (threadIdx.x == 0) {
-        if (op.hdr) {
-            HeaderView h = read_header(op.hdr, op.cap, g.n, E::dtype, -1);
-            s_ok = h.ok; s_fmt = h.fmt; s_nnz = h.nnz;
-            if (!h.ok && blockIdx.x == 0) set_status(g.ctrl, SPCCL_ERR_CORRUPT_STREAM);
-        } else {
-            s_ok = 1; s_fmt = kFmtDense; s_nnz = 0;
-        }
-    }
-    __syncthreads();
-    if (!s_ok) return;
-    const uint64_t t0 = ((uint64_t)blockIdx.x * kWavesPerBlock + wave) * K;
-    if (t0 >= g.T) return;
-    raw* out = reinterpret_cast<raw*>(g.out + (uint64_t)blockIdx.y * g.n * sizeof(raw));
-    if (s_fmt != (uint32_t)kFmtPici) {
-        // a dense part: copy its tiles, 16 rows at a time
-        const uint8_t* d = op.hdr ? op.hdr + kHeaderBytes : op.data;
+    const uint32_t l = lane_id();
+    const uint64_t g_n = n, g_T = T;
+    if (fmt != (uint32_t)kFmtPici) {
+        // a dense message: copy its tiles, 16 rows at a time
 #pragma unroll 1
         for (int k = 0; k < K; k++) {
             const uint64_t t = t0 + k;
-            if (t >= g.T) break;
+            if (t >= g_T) break;
             raw* col = out + t * kTileElems + l;
-            const uint64_t rem = g.n - t * kTileElems;
+            const uint64_t rem = g_n - t * kTileElems;
 #pragma unroll 1
             for (int h = 0; h < 4; h++) {
                 uint32_t v[16];
-                fetch_dense_rows16<E>(d, t, g.n, 16 * h, v);
+                fetch_dense_rows16<E>(d, t, g_n, 16 * h, v);
 #pragma unroll
                 for (int q = 0; q < 16; q++) {
                     const int r = 16 * h + q;
@@ -1177,24 +1165,23 @@ __global__ void __launch_bounds__(kBlockThreads) k_gather(GatherArgs g) {
         }
         return;
     }
-    const raw* A = reinterpret_cast<const raw*>(op.data + off_A(g.n));
+    const raw* A = reinterpret_cast<const raw*>(msg + off_A(g_n));
     PiciMeta m[K];
 #pragma unroll
     for (int k = 0; k < K; k++)
-        m[k] = t0 + k < g.T ? load_pici_meta<E>(op.data, t0 + k, g.n) : PiciMeta{0, 0, 0};
+        m[k] = t0 + k < g_T ? load_pici_meta<E>(msg, t0 + k, g_n) : PiciMeta{0, 0, 0};
     uint64_t cw[K];
     uint32_t cpref[K], ccnt[K], cbase[K];
     int kfit = 0;                       // leading tiles whose values are staged together
 #pragma unroll
     for (int k = 0; k < K; k++) {
-        const bool have = t0 + k < g.T;
-        const PiciCols c = have ? pici_columns(m[k], s_nnz, t0 + k, g.n, g.ctrl) : PiciCols{0, 0, 0, 0, false};
+        const bool have = t0 + k < g_T;
+        const PiciCols c = have ? pici_columns(m[k], nnz, t0 + k, g_n, ctrl) : PiciCols{0, 0, 0, 0, false};
         cw[k] = c.w; cpref[k] = c.colpref; ccnt[k] = c.cnt; cbase[k] = c.base;
         // valid tiles chain (base + cnt == next == the next tile's base)
         if (kfit == k && c.ok && (c.base - cbase[0]) + c.cnt <= kChunkVals) kfit = k + 1;
     }
     const uint32_t chunk = kfit ? (cbase[kfit - 1] - cbase[0]) + ccnt[kfit - 1] : 0u;
-    raw* stage = stage_all[wave];
     {
         uint32_t x[kChunkSlots];
 #pragma unroll
@@ -1212,7 +1199,7 @@ __global__ void __launch_bounds__(kBlockThreads) k_gather(GatherArgs g) {
 #pragma unroll
     for (int k = 0; k < K; k++) {
         if (k >= kfit) break;
-        store_from_stage<E>(out + (t0 + k) * kTileElems + l, g.n - (t0 + k) * kTileElems, cw[k], stage,
+        store_from_stage<E>(out + (t0 + k) * kTileElems + l, g_n - (t0 + k) * kTileElems, cw[k], stage,
                             (cbase[k] - cbase[0]) + cpref[k]);
     }
     // the rest one at a time
@@ -1220,9 +1207,9 @@ __global__ void __launch_bounds__(kBlockThreads) k_gather(GatherArgs g) {
     for (int k = 0; k < K; k++) {
         const uint64_t t = t0 + k;
         if (k < kfit) continue;
-        if (t >= g.T) break;
+        if (t >= g_T) break;
         raw* col = out + t * kTileElems + l;
-        const uint64_t rem = g.n - t * kTileElems;
+        const uint64_t rem = g_n - t * kTileElems;
         const uint64_t w = cw[k];
         const uint32_t cnt = ccnt[k];
         if (cnt <= kChunkVals) {
@@ -1251,6 +1238,202 @@ __global__ void __launch_bounds__(kBlockThreads) k_gather(GatherArgs g) {
             }
         }
     }
+}
+
+template <class E, int K>
+__global__ void __launch_bounds__(kBlockThreads) k_gather(GatherArgs g) {
+    using raw = typename E::raw;
+    __shared__ raw stage_all[kWavesPerBlock][kChunkVals];
+    __shared__ uint32_t s_ok, s_fmt;
+    __shared__ uint64_t s_nnz;
+    const uint32_t wave = threadIdx.x >> 6;
+    const DevOperand op = g.part[blockIdx.y];
+    if (threadIdx.x == 0) {
+        if (op.hdr) {
+            HeaderView h = read_header(op.hdr, op.cap, g.n, E::dtype, -1);
+            s_ok = h.ok; s_fmt = h.fmt; s_nnz = h.nnz;
+            if (!h.ok && blockIdx.x == 0) set_status(g.ctrl, SPCCL_ERR_CORRUPT_STREAM);
+        } else {
+            s_ok = 1; s_fmt = kFmtDense; s_nnz = 0;
+        }
+    }
+    __syncthreads();
+    if (!s_ok) return;
+    const uint64_t t0 = ((uint64_t)blockIdx.x * kWavesPerBlock + wave) * K;
+    if (t0 >= g.T) return;
+    raw* out = reinterpret_cast<raw*>(g.out + (uint64_t)blockIdx.y * g.n * sizeof(raw));
+    const uint8_t* d = op.hdr ? op.hdr + kHeaderBytes : op.data;
+    expand_tiles<E, K>(op.data, d, s_fmt, s_nnz, g.n, g.T, t0, out, stage_all[wave], g.ctrl);
+}
+
+// ---------------------------------------------------------------------------
+// Sliced streams (Sec. III-B phase 2, Sec. V-B): every slice of kSliceElems
+// elements is an independent message in its own slot.  One block of 4 waves
+// owns one slice (one tile per wave): its prefix sums are block-local, so a
+// single pass writes the finished message -- no look-back, no second pass --
+// and the format of the slice is decided on the device from its own count.
+
+// This wave's tile values (compacted, row order per column) to dst[0 ..
+// tilecnt): through the LDS stage, in column groups when they exceed it.
+template <class E>
+__device__ __forceinline__ void compact_tile(const uint32_t (&v)[64], uint64_t w, uint32_t colpref,
+                                             uint32_t tilecnt, typename E::raw* stage, typename E::raw* dst) {
+    using raw = typename E::raw;
+    const uint32_t l = lane_id();
+    const bool single = tilecnt <= E::cap;
+    const int ngroups = single ? 1 : E::groups;
+    const uint32_t gcols = single ? 64u : E::group_cols;
+#pragma unroll 1
+    for (int h = 0; h < ngroups; h++) {
+        const uint32_t c0 = gcols * h, c1 = c0 + gcols;
+        const uint32_t lo = single ? 0u : lane_bcast(colpref, c0);
+        const uint32_t hi = (single || c1 == 64) ? tilecnt : lane_bcast(colpref, c1);
+        const uint64_t wm = (l >= c0 && l < c1) ? w : 0ull;
+        uint32_t rank = colpref - lo;
+#pragma unroll
+        for (int r = 0; r < 64; r++) {
+            const bool bit = (wm >> r) & 1ull;
+            if (__any(bit)) {                            // rows empty in every column cost one branch
+                if (bit) { stage[rank] = (raw)v[r]; rank++; }
+            }
+        }
+        wave_lds_sync();
+        for (uint32_t i = l; i < hi - lo; i += 64) dst[lo + i] = stage[i];
+        wave_lds_sync();
+    }
+}
+
+// out = a (+) b per slice (HasB), or a alone (compress), into a sliced
+// stream (OutSliced) or a dense array.  b's slices may be Pici or dense; a
+// slice of b whose header fails its check is flagged and its output slice is
+// not written.
+template <class E, bool HasB, bool OutSliced>
+__global__ void __launch_bounds__(kBlockThreads) k_sliced(SlicedArgs g) {
+    using raw = typename E::raw;
+    __shared__ raw stage_all[kWavesPerBlock][E::cap];
+    __shared__ uint32_t s_cnt[kWavesPerBlock];
+    const uint32_t wave = threadIdx.x >> 6, l = lane_id();
+    raw* stage = stage_all[wave];
+    const uint64_t q = blockIdx.x;
+    const uint64_t base = q * kSliceElems;
+    const uint64_t ns = g.n - base < kSliceElems ? g.n - base : kSliceElems;
+    const uint64_t Ts = num_tiles(ns);
+    const uint64_t t = wave;
+    const bool has_tile = t < Ts;
+    const uint8_t* a = g.a + base * sizeof(raw);
+    uint32_t v[64];
+    if constexpr (HasB) {
+        // header and column words first (both lie inside the slot whatever
+        // the header says), then a's rows; the header is checked meanwhile
+        const uint8_t* bm = g.b + q * g.slot;
+        const HeaderWords hw = load_header_words(bm);
+        const PiciMeta m = has_tile ? load_pici_meta<E>(bm, t, ns) : PiciMeta{0, 0, 0};
+        asm volatile("" ::: "memory");
+        if (has_tile) fetch_dense<E, true>(a, t, ns, v);
+        const HeaderView h = check_header(hw, g.slot, ns, E::dtype, -1);
+        if (!h.ok) {                                     // the same in every wave of the block
+            if (threadIdx.x == 0) set_status(g.ctrl, SPCCL_ERR_CORRUPT_STREAM);
+            return;
+        }
+        if (has_tile) {
+            if (h.fmt == (uint32_t)kFmtPici)
+                expand_pici<E, false>(pici_columns(m, h.nnz, t, ns, g.ctrl), bm, ns, stage, v);
+            else
+                fetch_dense<E, false>(bm + kHeaderBytes, t, ns, v);
+        }
+    } else {
+        if (has_tile) fetch_dense<E, true>(a, t, ns, v);
+    }
+    if constexpr (!OutSliced) {
+        if (has_tile) store_tile<E>(g.out + base * sizeof(raw), t, ns, v);
+        return;
+    } else {
+        const uint64_t w = has_tile ? nonzero_rows(v) : 0ull;
+        const uint32_t c = (uint32_t)__popcll(w);
+        const uint32_t colpref = wave_excl_scan(c);
+        const uint32_t tilecnt = lane_bcast(colpref + c, 63);
+        if (l == 0) s_cnt[wave] = tilecnt;
+        __syncthreads();
+        uint32_t tile_excl = 0, agg = 0;
+#pragma unroll
+        for (uint32_t k = 0; k < kWavesPerBlock; k++) {
+            const uint32_t ck = s_cnt[k];
+            tile_excl += k < wave ? ck : 0u;
+            agg += ck;
+        }
+        uint8_t* om = g.out + q * g.slot;
+        if ((double)(ns - agg) / (double)ns <= g.thresh) {        // this slice goes dense
+            if (has_tile) store_tile<E>(om + kHeaderBytes, t, ns, v);
+            if (threadIdx.x == 0)
+                write_header(om, kFmtDense, E::dtype, ns, kNnzUnknown, 0, kHeaderBytes, dense_msg_bytes(ns, E::dtype));
+            return;
+        }
+        const uint64_t oI = off_I(ns), oA = off_A(ns);
+        uint32_t* I = reinterpret_cast<uint32_t*>(om + oI);
+        if (has_tile) {
+            reinterpret_cast<uint64_t*>(om + kHeaderBytes)[t * 64 + l] = w;
+            compact_tile<E>(v, w, colpref, tilecnt, stage, reinterpret_cast<raw*>(om + oA) + tile_excl);
+            if (l == 0) I[t] = tile_excl;
+        }
+        if (threadIdx.x == 0) {
+            I[Ts] = agg;
+            for (uint64_t b = oI + 4 * (Ts + 1); b < oA; b += 4) *reinterpret_cast<uint32_t*>(om + b) = 0u;
+            write_header(om, kFmtPici, E::dtype, ns, agg, oI, oA, oA + (uint64_t)agg * sizeof(raw));
+        }
+    }
+}
+
+// Expansion of a sliced stream: one wave per slice (its up to 4 tiles, all
+// reads before the first store).  A slice whose header fails its check is
+// flagged and not written.
+template <class E>
+__global__ void __launch_bounds__(kBlockThreads) k_expand_sliced(SlicedArgs g) {
+    using raw = typename E::raw;
+    __shared__ raw stage_all[kWavesPerBlock][kChunkVals];
+    const uint32_t wave = threadIdx.x >> 6;
+    const uint64_t q = (uint64_t)blockIdx.x * kWavesPerBlock + wave;
+    if (q >= num_slices(g.n)) return;
+    const uint64_t base = q * kSliceElems;
+    const uint64_t ns = g.n - base < kSliceElems ? g.n - base : kSliceElems;
+    const uint8_t* bm = g.a + q * g.slot;
+    const HeaderView h = check_header(load_header_words(bm), g.slot, ns, E::dtype, -1);
+    if (!h.ok) {
+        if (lane_id() == 0) set_status(g.ctrl, SPCCL_ERR_CORRUPT_STREAM);
+        return;
+    }
+    expand_tiles<E, kTilesPerPart>(bm, bm + kHeaderBytes, h.fmt, h.nnz, ns, num_tiles(ns), 0,
+                                   reinterpret_cast<raw*>(g.out) + base, stage_all[wave], g.ctrl);
+}
+
+// The virtual-rank send of a sliced stream: each slot's header.total_bytes,
+// read on the device; one wave per slot, eight 16-byte loads per lane in
+// flight before their stores, the last partial 16 bytes bytewise.  A slot whose header is not a message that
+// fits is flagged and not copied.
+__global__ void __launch_bounds__(kBlockThreads) k_copy_sliced(SlicedArgs g, uint64_t nslices) {
+    const uint32_t wave = threadIdx.x >> 6, l = lane_id();
+    const uint64_t q = (uint64_t)blockIdx.x * kWavesPerBlock + wave;
+    if (q >= nslices) return;
+    const uint8_t* src = g.a + q * g.slot;
+    uint8_t* dst = g.out + q * g.slot;
+    const HeaderWords hw = load_header_words(src);
+    const uint64_t total = hw.w[5];
+    if ((uint32_t)hw.w[0] != kMagic || total < kHeaderBytes || total > g.slot) {
+        if (l == 0) set_status(g.ctrl, SPCCL_ERR_CORRUPT_STREAM);
+        return;
+    }
+    const uint4* s4 = reinterpret_cast<const uint4*>(src);
+    uint4* d4 = reinterpret_cast<uint4*>(dst);
+    const uint32_t nvec = (uint32_t)(total / 16);
+    for (uint32_t i0 = l; i0 < nvec; i0 += 64 * 8) {
+        uint4 x[8];
+#pragma unroll
+        for (int u = 0; u < 8; u++) x[u] = i0 + 64 * u < nvec ? s4[i0 + 64 * u] : uint4{0, 0, 0, 0};
+#pragma unroll
+        for (int u = 0; u < 8; u++)
+            if (i0 + 64 * u < nvec) d4[i0 + 64 * u] = x[u];
+    }
+    const uint32_t tail = (uint32_t)(total & 15u);      // a Pici message ends on an element boundary
+    if (l < tail) dst[16ull * nvec + l] = src[16ull * nvec + l];
 }
 
 // ---------------------------------------------------------------------------
@@ -1479,6 +1662,29 @@ spccl_status_t launch_encode_dense_dt(int dtype, const uint8_t* src, uint8_t* ou
     dim3 grid(stream_grid(n * elem_bytes(dtype) / 16, 256 * 4, 4096)), block(256);
     if (dtype == kBF16) hipLaunchKernelGGL(k_encode_dense<BF16>, grid, block, 0, st, src, out, n);
     else hipLaunchKernelGGL(k_encode_dense<F32>, grid, block, 0, st, src, out, n);
+    return launch_status();
+}
+
+template <class E>
+void launch_sliced_t(const SlicedArgs& g, int op, hipStream_t st) {
+    const uint64_t S = num_slices(g.n);
+    dim3 block(kBlockThreads);
+    if (op == kSlicedCompress) hipLaunchKernelGGL((k_sliced<E, false, true>), dim3(S), block, 0, st, g);
+    else if (op == kSlicedReduceToSliced) hipLaunchKernelGGL((k_sliced<E, true, true>), dim3(S), block, 0, st, g);
+    else if (op == kSlicedReduceToDense) hipLaunchKernelGGL((k_sliced<E, true, false>), dim3(S), block, 0, st, g);
+    else hipLaunchKernelGGL(k_expand_sliced<E>, dim3((S + kWavesPerBlock - 1) / kWavesPerBlock), block, 0, st, g);
+}
+
+spccl_status_t launch_sliced_dt(int dtype, const SlicedArgs& g, int op, hipStream_t st) {
+    if (dtype == kBF16) launch_sliced_t<BF16>(g, op, st);
+    else launch_sliced_t<F32>(g, op, st);
+    return launch_status();
+}
+
+spccl_status_t launch_copy_sliced(const SlicedArgs& g, hipStream_t st) {
+    const uint64_t S = num_slices(g.n);
+    hipLaunchKernelGGL(k_copy_sliced, dim3((S + kWavesPerBlock - 1) / kWavesPerBlock), dim3(kBlockThreads), 0, st,
+                       g, S);
     return launch_status();
 }
 

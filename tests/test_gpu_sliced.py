@@ -1,0 +1,175 @@
+"""Sliced streams on the GPU (one message per 16384-element slice, block-local
+prefix sums, per-slice dense switch on the device) against the oracle: every
+slot's message byte for byte, dense outputs bit for bit."""
+import numpy as np
+import pytest
+
+import oracle as O
+import workloads as W
+from helpers import assert_bytes_equal, bits, log, to_dev, to_host_bits
+
+pytestmark = pytest.mark.gpu
+torch = pytest.importorskip("torch")
+
+S = O.SLICE_ELEMS
+
+
+@pytest.fixture(scope="module")
+def S_():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2607_04676_amd as lib
+    return lib
+
+
+def dt_code(dtype):
+    return O.F32 if dtype == W.F32 else O.BF16
+
+
+def gpu_slots(lib, t, n, dt):
+    """Per-slot message bytes of a device sliced stream."""
+    torch.cuda.synchronize()
+    return O.slot_messages(t.cpu().numpy(), n, dt)
+
+
+def assert_slots_equal(got, exp, what):
+    assert len(got) == len(exp), what
+    for q, (g, e) in enumerate(zip(got, exp)):
+        assert_bytes_equal(g, e, f"{what}: slot {q}")
+
+
+def make(n, frac, seed, dtype):
+    x = W.sparse_array(n, int(round(frac * n)), seed, dtype)
+    raw = bits(x).copy()
+    if n > 10:                                           # -0.0 and a subnormal, kept as present
+        raw[3] = 0x8000 if dtype == W.BF16 else 0x80000000
+        raw[n // 2] = 1
+    return raw.view(x.dtype)
+
+
+SIZES = [1, 4097, S, S + 1, 3 * S + 777, 37 * 4096 + 123]
+
+
+@pytest.mark.parametrize("n", SIZES)
+@pytest.mark.parametrize("dtype", [W.F32, W.BF16])
+@pytest.mark.parametrize("frac,thresh", [(0.01, -1.0), (0.01, 0.6), (0.5, 0.6), (0.5, -1.0), (0.3, 1.0)])
+def test_compress_and_decompress_sliced(S_, n, dtype, frac, thresh):
+    lib, dt = S_, dt_code(dtype)
+    log(f"sliced compress n={n} {dtype} frac={frac} thresh={thresh}")
+    x = make(n, frac, [50, n, int(frac * 100)], dtype)
+    ws = lib.alloc_workspace(1, dt, minimal=True)
+    out = lib.alloc_sliced(n, dt)
+    out.fill_(0xA5)
+    lib.spccl_compress_sliced(to_dev(x), out, ws, thresh)
+    got = gpu_slots(lib, out, n, dt)
+    assert_slots_equal(got, O.slot_messages(O.encode_sliced(x, thresh), n, dt), "compress_sliced")
+    back = torch.empty(n, dtype=torch.float32 if dt == O.F32 else torch.bfloat16, device="cuda")
+    lib.spccl_decompress_sliced(out, back, ws)
+    assert np.array_equal(to_host_bits(back), bits(x))
+    assert lib.spccl_read_status(ws) == 0
+
+
+@pytest.mark.parametrize("n", [4097, 3 * S + 777])
+@pytest.mark.parametrize("dtype", [W.F32, W.BF16])
+@pytest.mark.parametrize("thresh", [-1.0, 0.6, 1.0])
+def test_reduce_sliced(S_, n, dtype, thresh):
+    lib, dt = S_, dt_code(dtype)
+    log(f"sliced reduce n={n} {dtype} thresh={thresh}")
+    a = make(n, 0.2, [51, n, 0], dtype)
+    # b: slices of alternating density, so the stream mixes Pici and dense slices
+    b = make(n, 0.02, [51, n, 1], dtype)
+    dense_part = make(n, 0.7, [51, n, 2], dtype)
+    for q in range(0, O.slice_count(n), 2):
+        b[q * S:(q + 1) * S] = dense_part[q * S:(q + 1) * S]
+    hit = np.flatnonzero((bits(a) != 0) & (bits(b) != 0))
+    braw = bits(b).copy()
+    braw[hit[:4]] = bits(a)[hit[:4]] ^ (0x8000 if dt == O.BF16 else 0x80000000)    # exact cancellations
+    b = braw.view(b.dtype)
+    sb = O.encode_sliced(b, 0.6)
+    if n > S:
+        assert {O.header(m)["format"] for m in O.slot_messages(sb, n, dt)} == {O.FMT_PICI, O.FMT_DENSE}
+    ws = lib.alloc_workspace(1, dt, minimal=True)
+    ta, tb = to_dev(a), torch.from_numpy(sb.copy()).cuda()
+    tb_full = lib.alloc_sliced(n, dt)
+    tb_full[:tb.numel()].copy_(tb)
+    out = lib.alloc_sliced(n, dt)
+    lib.spccl_reduce_sliced(ta, tb_full, out, ws, out_sliced=True, dense_thresh=thresh)
+    exp = O.reduce_sliced(a, sb, n, dt, out_sliced=True, dense_thresh=thresh)
+    assert_slots_equal(gpu_slots(lib, out, n, dt), O.slot_messages(exp, n, dt), "reduce_sliced -> sliced")
+    dense = torch.empty_like(ta)
+    lib.spccl_reduce_sliced(ta, tb_full, dense, ws, out_sliced=False)
+    expd = O.reduce_sliced(a, sb, n, dt, out_sliced=False)
+    assert np.array_equal(to_host_bits(dense), bits(expd))
+    lib.spccl_reduce_sliced(ta, tb_full, ta, ws, out_sliced=False)         # in place
+    assert np.array_equal(to_host_bits(ta), bits(expd))
+    assert lib.spccl_read_status(ws) == 0
+
+
+def test_copy_sliced_copies_each_message(S_):
+    lib, n, dt = S_, 5 * S + 99, O.F32
+    x = make(n, 0.05, [52], W.F32)
+    ws = lib.alloc_workspace(1, dt, minimal=True)
+    src, dst = lib.alloc_sliced(n, dt), lib.alloc_sliced(n, dt)
+    lib.spccl_compress_sliced(to_dev(x), src, ws, 0.6)
+    dst.fill_(0)
+    lib.spccl_copy_sliced(src, dst, n, dt, ws)
+    assert_slots_equal(gpu_slots(lib, dst, n, dt), gpu_slots(lib, src, n, dt), "copy_sliced")
+    assert lib.spccl_read_status(ws) == 0
+
+
+def test_corrupt_slice_is_flagged_and_skipped(S_):
+    lib, n, dt = S_, 3 * S, O.F32
+    x = make(n, 0.05, [53], W.F32)
+    sb = O.encode_sliced(x)
+    bad = sb.copy()
+    bad[O.slice_bytes(dt) + 0] ^= 0xFF                   # magic of slot 1
+    ws = lib.alloc_workspace(1, dt, minimal=True)
+    out = torch.full((n,), 7.0, dtype=torch.float32, device="cuda")
+    lib.spccl_decompress_sliced(torch.from_numpy(bad).cuda(), out, ws)
+    assert lib.spccl_read_status(ws, clear=True) == 4
+    got = to_host_bits(out)
+    assert np.array_equal(got[:S], bits(x)[:S]) and np.array_equal(got[2 * S:], bits(x)[2 * S:])
+    assert np.all(got[S:2 * S] == np.float32(7.0).view(np.uint32))     # the bad slice is not written
+    lib.spccl_copy_sliced(torch.from_numpy(bad).cuda(), lib.alloc_sliced(n, dt), n, dt, ws)
+    assert lib.spccl_read_status(ws, clear=True) == 4
+
+
+def test_sliced_host_errors(S_):
+    lib, n, dt = S_, 2 * S, O.F32
+    ws = lib.alloc_workspace(1, dt, minimal=True)
+    a = torch.zeros(n, dtype=torch.float32, device="cuda")
+    out = lib.alloc_sliced(n, dt)
+    with pytest.raises(lib.SpcclError) as e:
+        lib.spccl_compress_sliced(a, out[:100], ws)
+    assert e.value.status == 2
+    with pytest.raises(lib.SpcclError) as e:
+        lib.spccl_compress_sliced(a, out[8:], ws)               # not 16-byte aligned
+    assert e.value.status in (1, 2)
+    with pytest.raises(lib.SpcclError) as e:
+        lib.spccl_reduce_sliced(a, out, out, ws, out_sliced=True)    # output aliases an input
+    assert e.value.status == 1
+
+
+def test_full_size_sliced_reduce_scatter_step(S_):
+    """The codec sweep array (67,108,864 fp32 at 99%): compress, the fused
+    reduce-scatter step into a sliced stream, its dense form, and decompress."""
+    lib, n, dt = S_, W.CFG2_N, O.F32
+    log("sliced full size: generate")
+    a, b = W.cfg2(990, 0), W.cfg2(990, 1)
+    ws = lib.alloc_workspace(1, dt, minimal=True)
+    ta, tb = to_dev(a), to_dev(b)
+    sa, sb = lib.alloc_sliced(n, dt), lib.alloc_sliced(n, dt)
+    log("sliced full size: compress")
+    lib.spccl_compress_sliced(ta, sa, ws, 0.6)
+    lib.spccl_compress_sliced(tb, sb, ws, 0.6)
+    exp_b = O.encode_sliced(b, 0.6)
+    assert_slots_equal(gpu_slots(lib, sb, n, dt), O.slot_messages(exp_b, n, dt), "full compress")
+    log("sliced full size: reduce")
+    out = lib.alloc_sliced(n, dt)
+    lib.spccl_reduce_sliced(ta, sb, out, ws, out_sliced=True, dense_thresh=0.6)
+    exp = O.reduce_sliced(a, exp_b, n, dt, out_sliced=True, dense_thresh=0.6)
+    assert_slots_equal(gpu_slots(lib, out, n, dt), O.slot_messages(exp, n, dt), "full reduce")
+    back = torch.empty(n, dtype=torch.float32, device="cuda")
+    lib.spccl_decompress_sliced(out, back, ws)
+    assert np.array_equal(to_host_bits(back), bits(O.decode_sliced(exp, n, dt)))
+    assert lib.spccl_read_status(ws) == 0
