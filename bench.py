@@ -200,6 +200,69 @@ class Runner:
         return bool(np.array_equal(got, exp))
 
 
+class SlicedRunner:
+    """The in-collective form of the same ops (Sec. III-B phase 2, Sec. V-B):
+    sliced streams, one message per 16384-element slice with its own
+    block-local prefix sums and its own format decision, on the arrays of R."""
+
+    def __init__(self, R, dense_thresh=0.6):
+        S, torch = R.S, R.torch
+        self.R, self.S, self.torch, self.n, self.ws = R, S, torch, R.n, R.ws
+        self.thresh = dense_thresh
+        self.slot = S.spccl_slice_bytes(S.SPCCL_F32)
+        self.nslices = S.spccl_slice_count(R.n)
+        mk = lambda: S.alloc_sliced(R.n, S.SPCCL_F32)
+        self.sb = [mk() for _ in R.b]
+        for k, b in enumerate(R.b):
+            S.spccl_compress_sliced(b, self.sb[k], R.ws, self.thresh)
+        self.sa, self.recv, self.red = mk(), mk(), mk()
+        torch.cuda.synchronize()
+
+    def ops(self, k):
+        S, R, n, s = self.S, self.R, self.n, self.R.s
+        a, sb, ws, th = R.a[k], self.sb[k], R.ws, self.thresh
+        return [
+            ("compress_sliced", lambda: S.spccl_compress_sliced(a, self.sa, ws, th), n * s),
+            ("send_sliced", lambda: S.spccl_copy_sliced(self.sa, self.recv, n, S.SPCCL_F32, ws), 0),
+            ("decompress_sliced", lambda: S.spccl_decompress_sliced(self.recv, R.dense_out, ws), n * s),
+            ("reduce_dense_sliced_to_sliced", lambda: S.spccl_reduce_sliced(a, sb, self.red, ws, True, th), 2 * n * s),
+            ("reduce_dense_sliced_to_dense", lambda: S.spccl_reduce_sliced(a, sb, R.red_d, ws, False, th), 2 * n * s),
+        ]
+
+    def decide(self):
+        pass
+
+    def stream_bytes(self, buf):
+        """Sum of the slots' message sizes (header.total_bytes of each slot)."""
+        h = buf[: self.nslices * self.slot].view(self.nslices, self.slot)[:, :48].cpu().numpy()
+        return int(h[:, 40:48].copy().view(np.uint64).sum())
+
+    def algorithmic_bytes(self):
+        n, s = self.n, self.R.s
+        self.torch.cuda.synchronize()
+        ba, bb, bo = self.stream_bytes(self.sa), self.stream_bytes(self.sb[0]), self.stream_bytes(self.red)
+        return {
+            "compress_sliced": n * s + ba,
+            "send_sliced": 2 * ba,
+            "decompress_sliced": ba + n * s,
+            "reduce_dense_sliced_to_sliced": n * s + bb + bo,
+            "reduce_dense_sliced_to_dense": 2 * n * s + bb,
+        }
+
+    def check_parity(self):
+        """Sampled parity against the oracle: the first and last slices of the
+        compressed stream of a, each message whole."""
+        import oracle as O
+        ok = True
+        for q in (0, self.nslices - 1):
+            lo = q * O.SLICE_ELEMS
+            x = self.R.host_a[lo: lo + O.SLICE_ELEMS]
+            exp = O.slot_messages(O.encode_sliced(x, self.thresh), x.size, O.F32)[0]
+            got = self.sa[q * self.slot: q * self.slot + exp.size].cpu().numpy()
+            ok = ok and bool(np.array_equal(got, exp))
+        return ok
+
+
 def run_steps(R, steps, copies, bracket):
     """steps steps of the op sequence; ops named in bracket are each wrapped in
     a pair of HIP events on the current stream.  Returns (total ms, wall s,
@@ -362,6 +425,20 @@ def main():
             "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(dgbs / HBM_PEAK_GBS, 4),
             "traffic": traffic_for(dom),
             "algorithmic_bytes_per_launch": alg[dom], "avg_launch_ms": round(dom_ms, 5)}
+    # the in-collective (sliced) form of the codec and reduce ops, per op
+    SR = SlicedRunner(R)
+    for w in range(2):
+        for _, f, _ in SR.ops(w % args.copies):
+            f()
+    _, _, per_s, _ = run_steps(SR, max(5, args.steps // 3), args.copies, [op[0] for op in SR.ops(0)])
+    alg_s = SR.algorithmic_bytes()
+    sliced = {"slice_elems": 16384, "dense_thresh": SR.thresh, "parity_compress_vs_oracle": SR.check_parity(),
+              "kernels": {}}
+    for nm, ms in per_s.items():
+        gbs = alg_s[nm] / (ms / 1e3) / 1e9
+        sliced["kernels"][nm] = {"ms": round(ms, 5), "algorithmic_bytes": alg_s[nm], "achieved_GBs": round(gbs, 1),
+                                 "frac_of_hbm_peak": round(gbs / HBM_PEAK_GBS, 4)}
+    del SR
     sweep = {}
     del R
     torch.cuda.empty_cache()
@@ -390,7 +467,8 @@ def main():
                                f"sigma={args.permille / 1000}, uniform random nonzero positions, N(0,1) values; "
                                "step = compress, send, decompress, 3 reduce variants, gather-expand, adaptive switch",
                    "n": args.n, "sigma": args.permille / 1000, "parallelism": "1 GPU (virtual ranks)"},
-        "roofline": roof, "cpu_baseline": cpu, "copy_ceiling": ceiling, "kernels": kernels, "sweep": sweep,
+        "roofline": roof, "cpu_baseline": cpu, "copy_ceiling": ceiling, "kernels": kernels, "sliced": sliced,
+        "sweep": sweep,
         "parity_compress_vs_oracle": parity, "wall_s_timed": round(wall, 3),
         "calibration_copy_bytes": calib,
     }
