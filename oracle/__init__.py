@@ -8,7 +8,8 @@ the two share no code.
 The C file cites the paper passage each function follows: Sec. III-B and
 Alg. 1 (format, compression), Sec. III-C (decompression), Sec. IV-B (where
 compression and reduction happen in the ring collectives), Sec. IV-C with
-Eq. 7 (the adaptive dense switch) and Sec. V-B (the 48-byte header).
+Eq. 7 (the adaptive dense switch), Sec. V-B (the 48-byte header), and
+Sec. II-B with Sec. IV-D (the flat COO format and its collectives).
 """
 from __future__ import annotations
 
@@ -24,7 +25,7 @@ _SRC = os.path.join(_HERE, "pici_oracle.c")
 _LIB = os.path.join(_HERE, "liboracle.so")
 
 F32, BF16 = 0, 1
-FMT_DENSE, FMT_PICI = 0, 1
+FMT_DENSE, FMT_PICI, FMT_COO = 0, 1, 2
 ARRAY, STREAM = 0, 1
 OK, ERR_INVALID_ARG, ERR_CAPACITY, ERR_UNSUPPORTED, ERR_CORRUPT_STREAM = 0, 1, 2, 3, 4
 NNZ_UNKNOWN = (1 << 64) - 1
@@ -43,7 +44,7 @@ def build() -> str:
 class _Policy(ctypes.Structure):
     _fields_ = [("intra_thresh", ctypes.c_double), ("inter_thresh", ctypes.c_double),
                 ("ag_thresh", ctypes.c_double), ("ranks_per_node", ctypes.c_int),
-                ("adaptive", ctypes.c_int)]
+                ("adaptive", ctypes.c_int), ("sparse_fmt", ctypes.c_int)]
 
 
 class _Trace(ctypes.Structure):
@@ -71,6 +72,14 @@ def lib():
         L.orc_dense_bytes.argtypes = [u64, i32]
         L.orc_stream_bound.restype = u64
         L.orc_stream_bound.argtypes = [u64, i32]
+        L.orc_coo_off_V.restype = u64
+        L.orc_coo_off_V.argtypes = [u64]
+        L.orc_coo_bytes.restype = u64
+        L.orc_coo_bytes.argtypes = [i32, u64]
+        L.orc_message_bound.restype = u64
+        L.orc_message_bound.argtypes = [u64, i32, i32]
+        L.orc_compress_coo.restype = i32
+        L.orc_compress_coo.argtypes = [vp, u64, i32, vp, u64, ctypes.POINTER(u64)]
         L.orc_compress.restype = i32
         L.orc_compress.argtypes = [vp, u64, i32, vp, u64, ctypes.POINTER(u64)]
         L.orc_encode_dense.restype = i32
@@ -90,7 +99,7 @@ def lib():
                                               ctypes.POINTER(ctypes.c_double),
                                               ctypes.POINTER(ctypes.c_double)]
         L.orc_ring_all_gather.restype = i32
-        L.orc_ring_all_gather.argtypes = [ctypes.POINTER(vp), ctypes.POINTER(vp), i32, u64, i32,
+        L.orc_ring_all_gather.argtypes = [ctypes.POINTER(vp), ctypes.POINTER(vp), i32, u64, i32, i32,
                                           ctypes.POINTER(_Trace)]
         L.orc_slice_count.restype = u64
         L.orc_slice_count.argtypes = [u64]
@@ -166,6 +175,20 @@ def stream_bound(n: int, dtype: int) -> int:
     return lib().orc_stream_bound(n, dtype)
 
 
+def coo_off_V(nnz: int) -> int:
+    return lib().orc_coo_off_V(nnz)
+
+
+def coo_bytes(dtype: int, nnz: int) -> int:
+    """Exact size of a COO message with nnz nonzeros (header, J, pad, V)."""
+    return lib().orc_coo_bytes(dtype, nnz)
+
+
+def message_bound(n: int, dtype: int, fmt: int) -> int:
+    """Worst-case size of an n-element message in format fmt (or dense)."""
+    return lib().orc_message_bound(n, dtype, fmt)
+
+
 # ---- codec ---------------------------------------------------------------------
 
 def compress(dense: np.ndarray) -> tuple[np.ndarray, int]:
@@ -177,6 +200,19 @@ def compress(dense: np.ndarray) -> tuple[np.ndarray, int]:
     buf = np.zeros(max(cap, 1), dtype=np.uint8)
     nnz = ctypes.c_uint64(0)
     _check(lib().orc_compress(_ptr(dense), n, dt, _ptr(buf), cap, ctypes.byref(nnz)), "compress")
+    total = int(buf[40:48].view(np.uint64)[0])
+    return buf[:total].copy(), nnz.value
+
+
+def compress_coo(dense: np.ndarray) -> tuple[np.ndarray, int]:
+    """COO message (uint8 array of exactly total_bytes) and nnz."""
+    dense = np.ascontiguousarray(dense)
+    dt = dtype_code(dense)
+    n = dense.size
+    cap = message_bound(n, dt, FMT_COO)
+    buf = np.zeros(max(cap, 1), dtype=np.uint8)
+    nnz = ctypes.c_uint64(0)
+    _check(lib().orc_compress_coo(_ptr(dense), n, dt, _ptr(buf), cap, ctypes.byref(nnz)), "compress_coo")
     total = int(buf[40:48].view(np.uint64)[0])
     return buf[:total].copy(), nnz.value
 
@@ -230,7 +266,7 @@ def reduce(a: Operand, b: Operand, n: int, dtype: int, out_kind: int = ARRAY,
         out = np.empty(n, dtype=_np_dtype(dtype))
         cap = 0
     else:
-        cap = stream_bound(n, dtype)
+        cap = message_bound(n, dtype, out_fmt)
         out = np.zeros(cap, dtype=np.uint8)
     nnz = ctypes.c_uint64(NNZ_UNKNOWN)
     st = L.orc_reduce(a.kind, _ptr(a.data), a.data.nbytes, b.kind, _ptr(b.data), b.data.nbytes,
@@ -251,10 +287,17 @@ class Policy:
     ag_thresh: float = 0.1
     ranks_per_node: int = 0      # 0: every link is intra-node
     adaptive: int = 1            # 0 never dense, 1 threshold rule, 2 always dense
+    sparse_fmt: int = FMT_PICI   # format of sparse sends: Pici or COO
+
+    @staticmethod
+    def coo(**kw) -> "Policy":
+        """COO sends with the paper's COO thresholds (Sec. IV-D): intra 0.8,
+        inter 0.7, ag 0.5."""
+        return Policy(**{"intra_thresh": 0.8, "inter_thresh": 0.7, "ag_thresh": 0.5, "sparse_fmt": FMT_COO, **kw})
 
     def c(self) -> _Policy:
         return _Policy(self.intra_thresh, self.inter_thresh, self.ag_thresh,
-                       self.ranks_per_node, self.adaptive)
+                       self.ranks_per_node, self.adaptive, self.sparse_fmt)
 
 
 @dataclass(frozen=True)
@@ -297,7 +340,7 @@ def ring_reduce_scatter(sends: list, policy: Policy | None = None):
     return recvs, _trace_list(tr, ntr)
 
 
-def ring_all_gather(parts: list):
+def ring_all_gather(parts: list, sparse_fmt: int = FMT_PICI):
     """parts[q]: rank q's n-element contribution.  Returns (P outputs of P*n, trace)."""
     P = len(parts)
     parts = [np.ascontiguousarray(p) for p in parts]
@@ -305,7 +348,7 @@ def ring_all_gather(parts: list):
     n = parts[0].size
     outs = [np.empty(P * n, dtype=parts[0].dtype) for _ in range(P)]
     tr = (_Trace * P)()
-    _check(lib().orc_ring_all_gather(_ptr_array(parts), _ptr_array(outs), P, n, dt, tr),
+    _check(lib().orc_ring_all_gather(_ptr_array(parts), _ptr_array(outs), P, n, dt, sparse_fmt, tr),
            "ring_all_gather")
     return outs, _trace_list(tr, P)
 

@@ -16,6 +16,8 @@
  *   - the adaptive dense switch with Eq. 7    (Sec. IV-C)
  *   - sliced streams: one message per slice, block-local prefix sums
  *                                             (Sec. III-B phase 2, Sec. V-B)
+ *   - the flat COO format (one 32-bit index and one value per nonzero) and
+ *     its use in the same collectives            (Sec. II-B, Sec. IV-D)
  *
  * Pici is an exact encoding, so compression is written as its definition:
  * loops over tiles, columns and rows in the order the format fixes.  No
@@ -41,7 +43,7 @@
 
 /* dtype codes and format / kind codes of the library interface */
 enum { ORC_F32 = 0, ORC_BF16 = 1 };
-enum { ORC_FMT_DENSE = 0, ORC_FMT_PICI = 1 };
+enum { ORC_FMT_DENSE = 0, ORC_FMT_PICI = 1, ORC_FMT_COO = 2 };
 enum { ORC_ARRAY = 0, ORC_STREAM = 1 };
 /* status codes of the library interface */
 enum { ORC_OK = 0, ORC_ERR_INVALID_ARG = 1, ORC_ERR_CAPACITY = 2,
@@ -69,6 +71,22 @@ uint64_t orc_dense_bytes(uint64_t n, int dtype) { return ORC_HEADER_BYTES + n * 
 uint64_t orc_stream_bound(uint64_t n, int dtype) {
     uint64_t p = orc_pici_bytes(n, dtype, n), d = orc_dense_bytes(n, dtype);
     return p > d ? p : d;
+}
+
+/* A COO message (Sec. II-B: the one-dimensional variant, a single flat
+ * 32-bit index per nonzero, and its value): the header, then J (nnz unsigned
+ * 32-bit indices, strictly increasing), zero pad to a 16-byte boundary, then
+ * V (the nnz values, in index order).  The paper sizes COO as 32-bit indices
+ * plus 32-bit values; the layout (indices apart from values) is this
+ * library's. */
+uint64_t orc_coo_off_V(uint64_t nnz) { return align16(ORC_HEADER_BYTES + 4u * nnz); }
+uint64_t orc_coo_bytes(int dtype, uint64_t nnz) { return orc_coo_off_V(nnz) + nnz * elem_size(dtype); }
+/* worst case of any message of n elements in format fmt (the dense message
+ * included: a sender may always fall back to it) */
+uint64_t orc_message_bound(uint64_t n, int dtype, int fmt) {
+    uint64_t d = orc_dense_bytes(n, dtype);
+    uint64_t w = fmt == ORC_FMT_COO ? orc_coo_bytes(dtype, n) : orc_stream_bound(n, dtype);
+    return w > d ? w : d;
 }
 
 /* ---- little-endian field access, byte by byte ------------------------- */
@@ -190,6 +208,31 @@ int orc_encode_dense(const void* dense, uint64_t n, int dtype, uint8_t* stream, 
     return ORC_OK;
 }
 
+/* ---- COO compression (Sec. II-B; used as in Sec. IV-D) ---------------- */
+/* Encodes dense[0..n) as a COO message: every present element, in index
+ * order, contributes its flat index to J and its value to V. */
+int orc_compress_coo(const void* dense, uint64_t n, int dtype, uint8_t* stream, uint64_t cap,
+                     uint64_t* nnz_out) {
+    if (dtype != ORC_F32 && dtype != ORC_BF16) return ORC_ERR_UNSUPPORTED;
+    if (n >= ((uint64_t)1 << 32)) return ORC_ERR_UNSUPPORTED;   /* 32-bit indices */
+    uint64_t nnz = 0;
+    for (uint64_t i = 0; i < n; i++) nnz += present(load_bits(dense, dtype, i)) ? 1u : 0u;
+    const uint64_t offV = orc_coo_off_V(nnz), total = orc_coo_bytes(dtype, nnz);
+    if (cap < total) return ORC_ERR_CAPACITY;
+    memset(stream, 0, offV);
+    write_header(stream, ORC_FMT_COO, dtype, n, nnz, ORC_HEADER_BYTES, offV, total);
+    uint64_t k = 0;
+    for (uint64_t i = 0; i < n; i++) {
+        uint32_t v = load_bits(dense, dtype, i);
+        if (!present(v)) continue;
+        put_u32(stream + ORC_HEADER_BYTES + 4 * k, (uint32_t)i);
+        store_bits(stream + offV, dtype, k, v);
+        k++;
+    }
+    if (nnz_out) *nnz_out = nnz;
+    return ORC_OK;
+}
+
 /* Header and index checks of a message of capacity cap that should hold n
  * elements of dtype.  Returns ORC_OK or ORC_ERR_CORRUPT_STREAM. */
 int orc_validate(const uint8_t* s, uint64_t cap, uint64_t n, int dtype) {
@@ -201,6 +244,18 @@ int orc_validate(const uint8_t* s, uint64_t cap, uint64_t n, int dtype) {
     if (dt != dtype || hn != n || total > cap) return ORC_ERR_CORRUPT_STREAM;
     if (fmt == ORC_FMT_DENSE) {
         if (offA != ORC_HEADER_BYTES || total != orc_dense_bytes(n, dtype)) return ORC_ERR_CORRUPT_STREAM;
+        return ORC_OK;
+    }
+    if (fmt == ORC_FMT_COO) {
+        if (nnz > n || offI != ORC_HEADER_BYTES || offA != orc_coo_off_V(nnz) ||
+            total != orc_coo_bytes(dtype, nnz))
+            return ORC_ERR_CORRUPT_STREAM;
+        /* indices strictly increasing and inside the array */
+        for (uint64_t k = 0; k < nnz; k++) {
+            uint64_t j = get_u32(s + offI + 4 * k);
+            if (j >= n) return ORC_ERR_CORRUPT_STREAM;
+            if (k > 0 && j <= (uint64_t)get_u32(s + offI + 4 * (k - 1))) return ORC_ERR_CORRUPT_STREAM;
+        }
         return ORC_OK;
     }
     if (fmt != ORC_FMT_PICI) return ORC_ERR_CORRUPT_STREAM;
@@ -222,13 +277,20 @@ int orc_validate(const uint8_t* s, uint64_t cap, uint64_t n, int dtype) {
 
 /* ---- decompression (Sec. III-C: the compaction phase run backwards) --- */
 /* Writes all n elements of dense: absent elements become +0.0, present ones
- * take their value from A in tile -> column -> row order.  Accepts a Pici or
- * a dense message. */
+ * take their value from A in tile -> column -> row order.  Accepts a Pici, a
+ * COO or a dense message. */
 int orc_decompress(const uint8_t* s, uint64_t cap, void* dense, uint64_t n, int dtype) {
     int st = orc_validate(s, cap, n, dtype);
     if (st != ORC_OK) return st;
     if (get_u16(s + 4) == ORC_FMT_DENSE) {
         memcpy(dense, s + ORC_HEADER_BYTES, n * elem_size(dtype));
+        return ORC_OK;
+    }
+    if (get_u16(s + 4) == ORC_FMT_COO) {   /* read the index-value pairs back (Sec. IV-D) */
+        const uint64_t nnz = get_u64(s + 16), offV = get_u64(s + 32);
+        memset(dense, 0, n * elem_size(dtype));
+        for (uint64_t k = 0; k < nnz; k++)
+            store_bits(dense, dtype, get_u32(s + ORC_HEADER_BYTES + 4 * k), load_bits(s + offV, dtype, k));
         return ORC_OK;
     }
     const uint64_t T = orc_num_tiles(n);
@@ -297,7 +359,7 @@ static int decode_operand(int kind, const void* p, uint64_t cap, uint64_t n, int
 }
 
 /* out = a (+) b over n elements.  Operands are dense arrays or messages of
- * either format; the output is a dense array, or a message in format
+ * any format; the output is a dense array, or a message in format
  * out_fmt.  Follows the paper's reduce step literally: accumulate densely,
  * then (for a Pici output) compress the dense result again. */
 int orc_reduce(int kind_a, const void* a, uint64_t cap_a, int kind_b, const void* b, uint64_t cap_b,
@@ -314,6 +376,7 @@ int orc_reduce(int kind_a, const void* a, uint64_t cap_a, int kind_b, const void
         store_bits(dr, dtype, i, orc_oplus(load_bits(da, dtype, i), load_bits(db, dtype, i), dtype));
     if (kind_out == ORC_ARRAY) { memcpy(out, dr, n * s); st = ORC_OK; }
     else if (out_fmt == ORC_FMT_PICI) st = orc_compress(dr, n, dtype, (uint8_t*)out, cap_out, nnz_out);
+    else if (out_fmt == ORC_FMT_COO) st = orc_compress_coo(dr, n, dtype, (uint8_t*)out, cap_out, nnz_out);
     else if (out_fmt == ORC_FMT_DENSE) st = orc_encode_dense(dr, n, dtype, (uint8_t*)out, cap_out);
     else st = ORC_ERR_INVALID_ARG;
 done:
@@ -328,6 +391,7 @@ typedef struct {
     double ag_thresh;      /* 0.1, at the RS -> AG transition of all-reduce */
     int ranks_per_node;    /* link r -> r+1 is inter-node iff (r+1) % ranks_per_node == 0 */
     int adaptive;          /* 0: never switch to dense; 1: threshold rule; 2: always dense */
+    int sparse_fmt;        /* format of the sparse sends: ORC_FMT_PICI, or ORC_FMT_COO (Sec. IV-D) */
 } orc_policy_t;
 
 typedef struct {
@@ -365,6 +429,14 @@ static void put_trace(orc_trace_t* tr, int idx, int step, int rank, int fmt, int
 
 static uint64_t msg_bytes(const uint8_t* s) { return get_u64(s + 40); }
 
+/* the sparse encoding of a collective: Pici, or COO (Sec. IV-D) */
+static int compress_fmt(int fmt, const void* dense, uint64_t n, int dtype, uint8_t* out, uint64_t cap,
+                        uint64_t* nnz) {
+    if (fmt == ORC_FMT_COO) return orc_compress_coo(dense, n, dtype, out, cap, nnz);
+    if (fmt == ORC_FMT_PICI) return orc_compress(dense, n, dtype, out, cap, nnz);
+    return ORC_ERR_INVALID_ARG;
+}
+
 /* Ring reduce-scatter.  send[r] holds rank r's n elements; recv[r] gets the
  * reduced chunk r (m = n / P elements).  At step s (0 <= s <= P-2) rank r
  * sends chunk (r - s - 1) mod P to rank r+1; the receiver folds in its own
@@ -383,7 +455,9 @@ int orc_ring_reduce_scatter(const void* const* send, void* const* recv, int P, u
     if (P < 1 || n % (uint64_t)P) return ORC_ERR_INVALID_ARG;
     if (dtype != ORC_F32 && dtype != ORC_BF16) return ORC_ERR_UNSUPPORTED;
     const uint64_t m = n / (uint64_t)P, s = elem_size(dtype);
-    const uint64_t cap = orc_stream_bound(m, dtype);
+    const int sfmt = pol->sparse_fmt;
+    if (sfmt != ORC_FMT_PICI && sfmt != ORC_FMT_COO) return ORC_ERR_INVALID_ARG;
+    const uint64_t cap = orc_message_bound(m, dtype, sfmt);
     int st = ORC_OK;
     if (P == 1) {
         memcpy(recv[0], send[0], m * s);
@@ -406,7 +480,7 @@ int orc_ring_reduce_scatter(const void* const* send, void* const* recv, int P, u
         int c = (r - 1 + P) % P;
         const uint8_t* chunk = (const uint8_t*)send[r] + (uint64_t)c * m * s;
         uint64_t nnz = 0;
-        st = orc_compress(chunk, m, dtype, tmp, cap, &nnz); if (st) goto done;
+        st = compress_fmt(sfmt, chunk, m, dtype, tmp, cap, &nnz); if (st) goto done;
         sig0[r] = sigp[r] = sparsity(m, nnz);
         if (go_dense(pol, sig0[r], tau_link(pol, r, P))) {
             st = orc_encode_dense(chunk, m, dtype, out_msg[r], cap); if (st) goto done;
@@ -440,11 +514,11 @@ int orc_ring_reduce_scatter(const void* const* send, void* const* recv, int P, u
                 put_trace(trace, idx, step, r, ORC_FMT_DENSE, 0, msg_bytes(out_msg[r]), ORC_NNZ_UNKNOWN, sigp[r]);
             } else {
                 uint64_t nnz = 0;
-                st = orc_reduce(ORC_STREAM, in_msg[r], cap, ORC_ARRAY, own, 0, ORC_STREAM, ORC_FMT_PICI,
+                st = orc_reduce(ORC_STREAM, in_msg[r], cap, ORC_ARRAY, own, 0, ORC_STREAM, sfmt,
                                 out_msg[r], cap, m, dtype, &nnz);
                 if (st) goto done;
                 sigp[r] = sparsity(m, nnz);
-                put_trace(trace, idx, step, r, ORC_FMT_PICI, 1, msg_bytes(out_msg[r]), nnz, sigp[r]);
+                put_trace(trace, idx, step, r, sfmt, 1, msg_bytes(out_msg[r]), nnz, sigp[r]);
             }
         }
     }
@@ -467,7 +541,7 @@ done:
  * entries (step = trace_step). */
 static int ring_all_gather_fmt(const void* const* part, const int* fmt, void* const* out, int P, uint64_t n,
                                int dtype, orc_trace_t* trace, int trace_step, const double* sig_track) {
-    const uint64_t s = elem_size(dtype), cap = orc_stream_bound(n, dtype);
+    const uint64_t s = elem_size(dtype), cap = orc_message_bound(n, dtype, ORC_FMT_COO);
     int st = ORC_OK;
     uint8_t** msg = (uint8_t**)calloc((size_t)P, sizeof(uint8_t*));
     uint8_t* hop = (uint8_t*)malloc(cap);
@@ -476,11 +550,11 @@ static int ring_all_gather_fmt(const void* const* part, const int* fmt, void* co
         msg[q] = (uint8_t*)malloc(cap);
         if (!msg[q]) { st = ORC_ERR_INVALID_ARG; goto done; }
         uint64_t nnz = ORC_NNZ_UNKNOWN;
-        if (fmt[q] == ORC_FMT_PICI) st = orc_compress(part[q], n, dtype, msg[q], cap, &nnz);
-        else st = orc_encode_dense(part[q], n, dtype, msg[q], cap);
+        if (fmt[q] == ORC_FMT_DENSE) st = orc_encode_dense(part[q], n, dtype, msg[q], cap);
+        else st = compress_fmt(fmt[q], part[q], n, dtype, msg[q], cap, &nnz);
         if (st) goto done;
         double sig = sig_track ? sig_track[q] : sparsity(n, nnz);
-        put_trace(trace, q, trace_step, q, fmt[q], fmt[q] == ORC_FMT_PICI, msg_bytes(msg[q]), nnz, sig);
+        put_trace(trace, q, trace_step, q, fmt[q], fmt[q] != ORC_FMT_DENSE, msg_bytes(msg[q]), nnz, sig);
     }
     for (int r = 0; r < P; r++) {
         memcpy((uint8_t*)out[r] + (uint64_t)r * n * s, part[r], n * s);
@@ -498,14 +572,16 @@ done:
     return st;
 }
 
-/* Standalone all-gather: never switches to dense (it does not densify). */
+/* Standalone all-gather in sparse format sparse_fmt (Pici or COO): never
+ * switches to dense (it does not densify). */
 int orc_ring_all_gather(const void* const* part, void* const* out, int P, uint64_t n, int dtype,
-                        orc_trace_t* trace) {
+                        int sparse_fmt, orc_trace_t* trace) {
     if (P < 1) return ORC_ERR_INVALID_ARG;
     if (dtype != ORC_F32 && dtype != ORC_BF16) return ORC_ERR_UNSUPPORTED;
+    if (sparse_fmt != ORC_FMT_PICI && sparse_fmt != ORC_FMT_COO) return ORC_ERR_INVALID_ARG;
     int* fmt = (int*)malloc(sizeof(int) * (size_t)P);
     if (!fmt) return ORC_ERR_INVALID_ARG;
-    for (int q = 0; q < P; q++) fmt[q] = ORC_FMT_PICI;
+    for (int q = 0; q < P; q++) fmt[q] = sparse_fmt;
     int st = ring_all_gather_fmt(part, fmt, out, P, n, dtype, trace, 0, NULL);
     free(fmt);
     return st;
@@ -534,7 +610,7 @@ int orc_ring_all_reduce(const void* const* send, void* const* out, int P, uint64
     for (int r = 0; r < P; r++) {
         est[r] = sigp[r] * sig0[r];
         int dense = pol->adaptive == 2 ? 1 : (pol->adaptive == 0 ? 0 : est[r] <= pol->ag_thresh);
-        fmt[r] = dense ? ORC_FMT_DENSE : ORC_FMT_PICI;
+        fmt[r] = dense ? ORC_FMT_DENSE : pol->sparse_fmt;
     }
     st = ring_all_gather_fmt((const void* const*)red, fmt, out, P, m, dtype,
                              trace ? trace + (size_t)P * (size_t)(P - 1) : NULL, P - 1, est);
