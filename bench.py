@@ -263,6 +263,61 @@ class SlicedRunner:
         return ok
 
 
+class CooRunner:
+    """The same ops with COO messages (Sec. II-B format; Sec. IV-D runs it
+    beside Pici): compress, send, decompress, the reduce-scatter step
+    dense (+) COO -> COO, and dense (+) COO -> dense, on the arrays of R."""
+
+    def __init__(self, R):
+        S, torch = R.S, R.torch
+        self.R, self.S, self.torch, self.n, self.ws = R, S, torch, R.n, R.ws
+        F = S.SPCCL_F32
+        mk = lambda: S.alloc_stream(R.n, F, fmt=S.SPCCL_FMT_COO)
+        self.cb = [mk() for _ in R.b]
+        for k, b in enumerate(R.b):
+            S.spccl_compress_coo(b, self.cb[k], R.ws)
+        self.ca, self.recv, self.red = mk(), mk(), mk()
+        torch.cuda.synchronize()
+
+    def ops(self, k):
+        S, R, n, s = self.S, self.R, self.n, self.R.s
+        a, cb, ws = R.a[k], self.cb[k], R.ws
+        F, C = S.SPCCL_F32, S.SPCCL_FMT_COO
+        msg = lambda t: S.operand(t, S.SPCCL_STREAM, C)
+        return [
+            ("compress_coo", lambda: S.spccl_compress_coo(a, self.ca, ws), n * s),
+            ("send_coo", lambda: S.spccl_copy_message(self.ca, self.recv, ws), 0),
+            ("decompress_coo", lambda: S.spccl_decompress(self.recv, R.dense_out, ws), n * s),
+            ("reduce_dense_coo_to_coo", lambda: S.spccl_reduce(S.operand(a), msg(cb), msg(self.red), n, F, ws),
+             2 * n * s),
+            ("reduce_dense_coo_to_dense", lambda: S.spccl_reduce(S.operand(a), msg(cb), S.operand(R.red_d), n, F, ws),
+             2 * n * s),
+        ]
+
+    def decide(self):
+        pass
+
+    def algorithmic_bytes(self):
+        S, n, s = self.S, self.n, self.R.s
+        self.torch.cuda.synchronize()
+        ba = S.spccl_read_header(self.ca)["total_bytes"]
+        bb = S.spccl_read_header(self.cb[0])["total_bytes"]
+        bo = S.spccl_read_header(self.red)["total_bytes"]
+        return {
+            "compress_coo": n * s + ba,
+            "send_coo": 2 * ba,
+            "decompress_coo": ba + n * s,
+            "reduce_dense_coo_to_coo": n * s + bb + bo,
+            "reduce_dense_coo_to_dense": 2 * n * s + bb,
+        }
+
+    def check_parity(self):
+        """Sampled parity against the oracle: the COO message of a, whole."""
+        import oracle as O
+        exp, _ = O.compress_coo(self.R.host_a)
+        return bool(np.array_equal(self.ca[:exp.size].cpu().numpy(), exp))
+
+
 def run_steps(R, steps, copies, bracket):
     """steps steps of the op sequence; ops named in bracket are each wrapped in
     a pair of HIP events on the current stream.  Returns (total ms, wall s,
@@ -439,6 +494,19 @@ def main():
         sliced["kernels"][nm] = {"ms": round(ms, 5), "algorithmic_bytes": alg_s[nm], "achieved_GBs": round(gbs, 1),
                                  "frac_of_hbm_peak": round(gbs / HBM_PEAK_GBS, 4)}
     del SR
+    # the COO form of the codec and reduce ops
+    CR = CooRunner(R)
+    for w in range(2):
+        for _, f, _ in CR.ops(w % args.copies):
+            f()
+    _, _, per_c, _ = run_steps(CR, max(5, args.steps // 3), args.copies, [op[0] for op in CR.ops(0)])
+    alg_c = CR.algorithmic_bytes()
+    coo = {"parity_compress_vs_oracle": CR.check_parity(), "kernels": {}}
+    for nm, ms in per_c.items():
+        gbs = alg_c[nm] / (ms / 1e3) / 1e9
+        coo["kernels"][nm] = {"ms": round(ms, 5), "algorithmic_bytes": alg_c[nm], "achieved_GBs": round(gbs, 1),
+                              "frac_of_hbm_peak": round(gbs / HBM_PEAK_GBS, 4)}
+    del CR
     sweep = {}
     del R
     torch.cuda.empty_cache()
@@ -468,7 +536,7 @@ def main():
                                "step = compress, send, decompress, 3 reduce variants, gather-expand, adaptive switch",
                    "n": args.n, "sigma": args.permille / 1000, "parallelism": "1 GPU (virtual ranks)"},
         "roofline": roof, "cpu_baseline": cpu, "copy_ceiling": ceiling, "kernels": kernels, "sliced": sliced,
-        "sweep": sweep,
+        "coo": coo, "sweep": sweep,
         "parity_compress_vs_oracle": parity, "wall_s_timed": round(wall, 3),
         "calibration_copy_bytes": calib,
     }

@@ -49,8 +49,10 @@ typedef enum {
 
 typedef enum { SPCCL_F32 = 0, SPCCL_BF16 = 1 } spccl_dtype_t;
 
-/* Message formats (Sec. V-B: each message carries its format in its header). */
-typedef enum { SPCCL_FMT_DENSE = 0, SPCCL_FMT_PICI = 1 } spccl_format_t;
+/* Message formats (Sec. V-B: each message carries its format in its header).
+ * COO is the flat variant of Sec. II-B that the paper runs beside Pici
+ * (Sec. IV-D): one 32-bit index and one value per nonzero. */
+typedef enum { SPCCL_FMT_DENSE = 0, SPCCL_FMT_PICI = 1, SPCCL_FMT_COO = 2 } spccl_format_t;
 
 /* A reduce operand is either a raw dense array of n elements (ARRAY) or a
  * header-prefixed message (STREAM). */
@@ -65,13 +67,18 @@ typedef struct {
     uint64_t bytes;   /* capacity of the buffer in bytes; a STREAM input must hold
                          at least the smallest valid message of its declared
                          format (DENSE: 48 + n * elem_size; PICI: off_A, the
-                         header plus B and I), else SPCCL_ERR_CAPACITY */
+                         header plus B and I; COO: the 48-byte header), else
+                         SPCCL_ERR_CAPACITY */
 } spccl_operand_t;
 
 /* The 48-byte message header (Sec. V-B names its contents: format, size and
  * component offsets; the layout is this library's).  Little-endian.
  *   PICI:  B (u64[64*T]) at offset 48, I (u32[T+1]) at off_I = 48 + 512*T,
  *          zero pad to 16 bytes, A (nnz values) at off_A,
+ *          total_bytes = off_A + nnz * elem_size.
+ *   COO:   J (u32[nnz], the flat indices of the nonzeros, strictly
+ *          increasing) at off_I = 48, zero pad to 16 bytes, V (nnz values in
+ *          index order) at off_A = align16(48 + 4*nnz),
  *          total_bytes = off_A + nnz * elem_size.
  *   DENSE: the n values at off_A = 48; off_I = 0; nnz = UINT64_MAX
  *          ("not computed"); total_bytes = 48 + n * elem_size. */
@@ -107,13 +114,14 @@ uint64_t spccl_stream_bound(uint64_t n, int32_t dtype);
 
 /* Workspace for messages of up to n elements: a 256-byte control block
  * (the sticky device status), one 64-bit look-back word per partition of
- * 16384 elements, and one worst-case slot of compacted values per partition
- * (n elements' worth).  With the slots, Pici-producing calls run as two
- * passes that never wait while holding input data (count and park values,
- * then resolve offsets by look-back and move); a workspace of only
- * spccl_workspace_min_bytes selects the single-pass kernels, which resolve
- * offsets by decoupled look-back while holding their tiles.  Outputs are
- * identical.  Zero-fill a workspace once before first use (or clear it with
+ * 16384 elements, one worst-case slot of compacted values per partition
+ * (n elements' worth) and one of 32-bit indices (COO outputs).  With the
+ * value slots, Pici-producing calls run as two passes that never wait while
+ * holding input data (count and park values, then resolve offsets by
+ * look-back and move); a workspace of only spccl_workspace_min_bytes selects
+ * the single-pass kernels, which resolve offsets by decoupled look-back
+ * while holding their tiles.  Outputs are identical.  COO outputs always
+ * take three passes and need the full workspace.  Zero-fill a workspace once before first use (or clear it with
  * spccl_workspace_init); look-back words are tagged with a per-launch epoch,
  * so it needs no clearing between calls.  One workspace must not be used by
  * two calls in flight at once. */
@@ -122,6 +130,17 @@ uint64_t spccl_workspace_min_bytes(uint64_t n, int32_t dtype);
 
 /* Zero-fill a workspace with a fill kernel on `stream` (no memset nodes). */
 spccl_status_t spccl_workspace_init(void* ws, uint64_t ws_bytes, void* stream);
+
+/* Exact byte size of a COO message with nnz nonzeros (Sec. II-B sizes: a
+ * 32-bit index and a value per nonzero; plus header and pad).  0 for an
+ * unsupported dtype. */
+uint64_t spccl_coo_bytes(int32_t dtype, uint64_t nnz);
+
+/* Worst-case size of an n-element message in format fmt, or of the dense
+ * message if that is larger (a sender may always fall back to dense).  A
+ * COO output needs this capacity (every element present: 48 + pad + n *
+ * (4 + elem_size)).  0 for an unsupported dtype or format. */
+uint64_t spccl_message_bound(uint64_t n, int32_t dtype, int32_t fmt);
 
 /* ---- codec (Sec. III-B format, Alg. 1 compression, Sec. III-C) ----------- */
 
@@ -135,11 +154,25 @@ spccl_status_t spccl_compress(const void* dense, uint64_t n, int32_t dtype,
                               void* out, uint64_t out_bytes,
                               void* ws, uint64_t ws_bytes, void* stream);
 
-/* Expand a message (PICI or DENSE, read from its header) of capacity
- * in_bytes into all n elements of `dense` (absent elements become +0.0). */
+/* Expand a message (PICI, COO or DENSE, read from its header) of capacity
+ * in_bytes into all n elements of `dense` (absent elements become +0.0).  A
+ * COO tile's entries are found by searching J; entries outside their tile,
+ * at or past n, or not strictly increasing flag SPCCL_ERR_CORRUPT_STREAM and
+ * their tile reads as empty. */
 spccl_status_t spccl_decompress(const void* in, uint64_t in_bytes,
                                 void* dense, uint64_t n, int32_t dtype,
                                 void* ws, uint64_t ws_bytes, void* stream);
+
+/* Compress dense[0..n) into a COO message at `out` (capacity out_bytes >=
+ * spccl_message_bound(n, dtype, SPCCL_FMT_COO)): the flat index and the
+ * value of every present element, by increasing index (Sec. II-B; the
+ * paper's collectives use it beside Pici, Sec. IV-D).  Three passes (count
+ * and park entries per 16384-element partition, scan the partition counts,
+ * place); needs ws_bytes >= spccl_workspace_bytes(n, dtype), else
+ * SPCCL_ERR_WORKSPACE. */
+spccl_status_t spccl_compress_coo(const void* dense, uint64_t n, int32_t dtype,
+                                  void* out, uint64_t out_bytes,
+                                  void* ws, uint64_t ws_bytes, void* stream);
 
 /* Wrap dense[0..n) as a DENSE message (header + the n values) at `out`
  * (capacity out_bytes >= 48 + n * elem_size).  Dense sends carry the same
@@ -153,12 +186,16 @@ spccl_status_t spccl_encode_dense(const void* dense, uint64_t n, int32_t dtype,
  * bits) is the identity; two present elements are added (fp32: IEEE add,
  * nearest-even; bf16: fp32 add rounded once to bfloat16, nearest-even).  A
  * result is present iff its bits are nonzero, so an exact cancellation drops
- * the element from a Pici output.  In a ring step `a` is the received
+ * the element from a Pici or COO output.  In a ring step `a` is the received
  * (earlier) contribution; the operation is commutative bit for bit.
- * Supported operand kinds: a, b each ARRAY, STREAM/PICI or STREAM/DENSE;
- * out ARRAY, STREAM/PICI or STREAM/DENSE.  out may alias a or b only when
- * all three are ARRAYs (in-place accumulation).  A STREAM output needs
- * capacity >= spccl_stream_bound(n, dtype). */
+ * Supported operand kinds: a, b each ARRAY, STREAM/PICI, STREAM/COO or
+ * STREAM/DENSE; out ARRAY, STREAM/PICI, STREAM/COO or STREAM/DENSE.  Pici
+ * and COO do not meet in one call (a COO operand with a Pici operand or a
+ * Pici output, or a Pici operand with a COO output: SPCCL_ERR_UNSUPPORTED).
+ * out may alias a or b only when all three are ARRAYs (in-place
+ * accumulation).  A PICI or DENSE STREAM output needs capacity >=
+ * spccl_stream_bound(n, dtype), a COO one spccl_message_bound(n, dtype,
+ * SPCCL_FMT_COO) and the full workspace. */
 spccl_status_t spccl_reduce(spccl_operand_t a, spccl_operand_t b, spccl_operand_t out,
                             uint64_t n, int32_t dtype,
                             void* ws, uint64_t ws_bytes, void* stream);
@@ -166,7 +203,7 @@ spccl_status_t spccl_reduce(spccl_operand_t a, spccl_operand_t b, spccl_operand_
 /* ---- all-gather receive side (Sec. IV-B) --------------------------------- */
 
 /* dense_out[q*n_per_part .. (q+1)*n_per_part) = expand(parts[q]) for q < P.
- * parts (host array of P operands) are ARRAYs or STREAMs of either format
+ * parts (host array of P operands) are ARRAYs or STREAMs of any format
  * (a STREAM's format is read from its header; its fmt field is ignored). */
 spccl_status_t spccl_gather_expand(const spccl_operand_t* parts, int32_t P,
                                    uint64_t n_per_part, int32_t dtype,
@@ -180,7 +217,8 @@ spccl_status_t spccl_gather_expand(const spccl_operand_t* parts, int32_t P,
  * case.  A sliced stream is that layout for an n-element array: slot q, at
  * byte q * spccl_slice_bytes(dtype) of the buffer, holds elements
  * [SPCCL_SLICE_ELEMS q, min(n, SPCCL_SLICE_ELEMS (q + 1))) as an ordinary
- * message (Pici or dense, the header layout above, n = the slice length).
+ * message (Pici or dense only; the header layout above, n = the slice
+ * length).
  * One device pass produces a slice, with no device-wide scan, and the
  * format of every slice is decided on the device: a produced slice is dense
  * iff its own sparsity (zeros / length, in double) is <= dense_thresh (give
@@ -237,14 +275,16 @@ const char* spccl_status_string(spccl_status_t s);
 /* ---- ring collectives over P virtual ranks on one GPU (Sec. IV) ----------- */
 
 /* Adaptive format policy (Sec. IV-C).  Defaults for Pici with fp32:
- * intra 0.6, inter 0.5, ag 0.1. */
+ * intra 0.6, inter 0.5, ag 0.1; the paper's COO values (Sec. IV-D) are
+ * intra 0.8, inter 0.7, ag 0.5. */
 typedef struct {
     double intra_thresh;     /* dense iff sparsity <= this on an intra-node link */
     double inter_thresh;     /* ... on an inter-node link */
     double ag_thresh;        /* all-reduce: gather densely iff estimate <= this */
     int32_t ranks_per_node;  /* link r -> r+1 is inter-node iff (r+1) % ranks_per_node == 0
                                 and ranks_per_node < P; 0 = all links intra-node */
-    int32_t adaptive;        /* 0: always Pici; 1: threshold rule; 2: always dense */
+    int32_t adaptive;        /* 0: always sparse; 1: threshold rule; 2: always dense */
+    int32_t sparse_fmt;      /* format of the sparse sends: SPCCL_FMT_PICI or SPCCL_FMT_COO */
 } spccl_policy_t;
 
 /* One send decision of one rank (host array; see spccl_vr_*). */
@@ -262,7 +302,8 @@ typedef struct {
 /* Scratch bytes the collectives need: P ranks exchanging messages of up to
  * msg_elems elements (n / P for reduce-scatter and all-reduce, n for
  * all-gather).  Holds one workspace and 3*P message buffers of
- * spccl_stream_bound(msg_elems) bytes. */
+ * spccl_message_bound(msg_elems, dtype, SPCCL_FMT_COO) bytes (any format
+ * fits). */
 uint64_t spccl_vr_scratch_bytes(int32_t P, uint64_t msg_elems, int32_t dtype);
 
 /* Ring reduce-scatter (Sec. IV-B).  send: host array of P device pointers to
@@ -277,12 +318,13 @@ spccl_status_t spccl_vr_reduce_scatter(void* const* send, void* const* recv, int
                                        void* scratch, uint64_t scratch_bytes,
                                        spccl_trace_t* trace, void* stream);
 
-/* Ring all-gather (Sec. IV-B): each rank compresses its n-element part once,
- * the message travels the ring unchanged, and every rank expands all P
- * parts into recv[r] (P*n elements).  Never switches to dense.  trace gets P
- * entries. */
+/* Ring all-gather (Sec. IV-B): each rank compresses its n-element part once
+ * (in policy->sparse_fmt; NULL policy = Pici), the message travels the ring
+ * unchanged, and every rank expands all P parts into recv[r] (P*n
+ * elements).  Never switches to dense.  trace gets P entries. */
 spccl_status_t spccl_vr_all_gather(void* const* send, void* const* recv, int32_t P, uint64_t n,
-                                   int32_t dtype, void* scratch, uint64_t scratch_bytes,
+                                   int32_t dtype, const spccl_policy_t* policy,
+                                   void* scratch, uint64_t scratch_bytes,
                                    spccl_trace_t* trace, void* stream);
 
 /* Ring all-reduce = reduce-scatter, then all-gather of the reduced chunks;

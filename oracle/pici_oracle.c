@@ -85,7 +85,7 @@ uint64_t orc_coo_bytes(int dtype, uint64_t nnz) { return orc_coo_off_V(nnz) + nn
  * included: a sender may always fall back to it) */
 uint64_t orc_message_bound(uint64_t n, int dtype, int fmt) {
     uint64_t d = orc_dense_bytes(n, dtype);
-    uint64_t w = fmt == ORC_FMT_COO ? orc_coo_bytes(dtype, n) : orc_stream_bound(n, dtype);
+    uint64_t w = fmt == ORC_FMT_COO ? orc_coo_bytes(dtype, n) : (fmt == ORC_FMT_PICI ? orc_pici_bytes(n, dtype, n) : d);
     return w > d ? w : d;
 }
 
@@ -670,6 +670,8 @@ int orc_decode_sliced(const uint8_t* in, uint64_t cap, void* dense, uint64_t n, 
     const uint64_t S = orc_slice_count(n), slot = orc_slice_bytes(dtype), s = elem_size(dtype);
     if (cap < S * slot) return ORC_ERR_CAPACITY;
     for (uint64_t q = 0; q < S; q++) {
+        /* a slot holds a Pici or a dense message; any other format is corrupt */
+        if (get_u16(in + q * slot + 4) == ORC_FMT_COO) return ORC_ERR_CORRUPT_STREAM;
         int st = orc_decompress(in + q * slot, slot, (uint8_t*)dense + q * ORC_SLICE_ELEMS * s,
                                 slice_len(n, q), dtype);
         if (st != ORC_OK) return st;

@@ -26,7 +26,7 @@ SPCCL_OK = 0
 STATUS_NAMES = {0: "OK", 1: "ERR_INVALID_ARG", 2: "ERR_CAPACITY", 3: "ERR_UNSUPPORTED",
                 4: "ERR_CORRUPT_STREAM", 5: "ERR_WORKSPACE", 6: "ERR_HIP", 7: "ERR_TIMEOUT"}
 SPCCL_F32, SPCCL_BF16 = 0, 1
-SPCCL_FMT_DENSE, SPCCL_FMT_PICI = 0, 1
+SPCCL_FMT_DENSE, SPCCL_FMT_PICI, SPCCL_FMT_COO = 0, 1, 2
 SPCCL_ARRAY, SPCCL_STREAM = 0, 1
 HEADER_BYTES = 48
 NNZ_UNKNOWN = (1 << 64) - 1
@@ -39,7 +39,8 @@ EXPORTS = ("spccl_num_tiles", "spccl_pici_bytes", "spccl_stream_bound", "spccl_w
            "spccl_read_status", "spccl_status_string", "spccl_vr_scratch_bytes",
            "spccl_vr_reduce_scatter", "spccl_vr_all_gather", "spccl_vr_all_reduce",
            "spccl_slice_count", "spccl_slice_bytes", "spccl_compress_sliced", "spccl_decompress_sliced",
-           "spccl_reduce_sliced", "spccl_copy_sliced")
+           "spccl_reduce_sliced", "spccl_copy_sliced", "spccl_coo_bytes", "spccl_message_bound",
+           "spccl_compress_coo")
 
 
 class spccl_operand_t(ctypes.Structure):
@@ -56,7 +57,7 @@ class spccl_header_t(ctypes.Structure):
 class spccl_policy_t(ctypes.Structure):
     _fields_ = [("intra_thresh", ctypes.c_double), ("inter_thresh", ctypes.c_double),
                 ("ag_thresh", ctypes.c_double), ("ranks_per_node", ctypes.c_int32),
-                ("adaptive", ctypes.c_int32)]
+                ("adaptive", ctypes.c_int32), ("sparse_fmt", ctypes.c_int32)]
 
 
 class spccl_trace_t(ctypes.Structure):
@@ -74,6 +75,9 @@ _sigs = {
     "spccl_workspace_min_bytes": (_u64, [_u64, _i32]),
     "spccl_workspace_init": (_i32, [_vp, _u64, _vp]),
     "spccl_compress": (_i32, [_vp, _u64, _i32, _vp, _u64, _vp, _u64, _vp]),
+    "spccl_compress_coo": (_i32, [_vp, _u64, _i32, _vp, _u64, _vp, _u64, _vp]),
+    "spccl_coo_bytes": (_u64, [_i32, _u64]),
+    "spccl_message_bound": (_u64, [_u64, _i32, _i32]),
     "spccl_decompress": (_i32, [_vp, _u64, _vp, _u64, _i32, _vp, _u64, _vp]),
     "spccl_encode_dense": (_i32, [_vp, _u64, _i32, _vp, _u64, _vp]),
     "spccl_reduce": (_i32, [spccl_operand_t, spccl_operand_t, spccl_operand_t, _u64, _i32, _vp, _u64, _vp]),
@@ -87,8 +91,8 @@ _sigs = {
     "spccl_vr_reduce_scatter": (_i32, [ctypes.POINTER(_vp), ctypes.POINTER(_vp), _i32, _u64, _i32,
                                        ctypes.POINTER(spccl_policy_t), _vp, _u64, ctypes.POINTER(spccl_trace_t),
                                        _vp]),
-    "spccl_vr_all_gather": (_i32, [ctypes.POINTER(_vp), ctypes.POINTER(_vp), _i32, _u64, _i32, _vp, _u64,
-                                   ctypes.POINTER(spccl_trace_t), _vp]),
+    "spccl_vr_all_gather": (_i32, [ctypes.POINTER(_vp), ctypes.POINTER(_vp), _i32, _u64, _i32,
+                                   ctypes.POINTER(spccl_policy_t), _vp, _u64, ctypes.POINTER(spccl_trace_t), _vp]),
     "spccl_vr_all_reduce": (_i32, [ctypes.POINTER(_vp), ctypes.POINTER(_vp), _i32, _u64, _i32,
                                    ctypes.POINTER(spccl_policy_t), _vp, _u64, ctypes.POINTER(spccl_trace_t),
                                    _vp]),
@@ -160,6 +164,14 @@ def spccl_workspace_min_bytes(n: int, dtype: int) -> int:
     return _lib.spccl_workspace_min_bytes(n, dtype)
 
 
+def spccl_coo_bytes(dtype: int, nnz: int) -> int:
+    return _lib.spccl_coo_bytes(dtype, nnz)
+
+
+def spccl_message_bound(n: int, dtype: int, fmt: int) -> int:
+    return _lib.spccl_message_bound(n, dtype, fmt)
+
+
 def spccl_vr_scratch_bytes(P: int, msg_elems: int, dtype: int) -> int:
     return _lib.spccl_vr_scratch_bytes(P, msg_elems, dtype)
 
@@ -173,6 +185,11 @@ def spccl_workspace_init(ws: torch.Tensor, stream=None) -> None:
 def spccl_compress(dense: torch.Tensor, out: torch.Tensor, ws: torch.Tensor, stream=None) -> None:
     _check(_lib.spccl_compress(dense.data_ptr(), dense.numel(), _dt(dense), out.data_ptr(), _nbytes(out),
                                ws.data_ptr(), _nbytes(ws), _stream(stream)), "spccl_compress")
+
+
+def spccl_compress_coo(dense: torch.Tensor, out: torch.Tensor, ws: torch.Tensor, stream=None) -> None:
+    _check(_lib.spccl_compress_coo(dense.data_ptr(), dense.numel(), _dt(dense), out.data_ptr(), _nbytes(out),
+                                   ws.data_ptr(), _nbytes(ws), _stream(stream)), "spccl_compress_coo")
 
 
 def spccl_decompress(msg: torch.Tensor, dense: torch.Tensor, ws: torch.Tensor, stream=None,
@@ -220,11 +237,11 @@ def spccl_status_string(status: int) -> str:
 
 def _policy(policy) -> spccl_policy_t:
     if policy is None:
-        return spccl_policy_t(0.6, 0.5, 0.1, 0, 1)
+        return spccl_policy_t(0.6, 0.5, 0.1, 0, 1, SPCCL_FMT_PICI)
     if isinstance(policy, spccl_policy_t):
         return policy
     return spccl_policy_t(policy.intra_thresh, policy.inter_thresh, policy.ag_thresh, policy.ranks_per_node,
-                          policy.adaptive)
+                          policy.adaptive, getattr(policy, "sparse_fmt", SPCCL_FMT_PICI))
 
 
 def _ptrs(ts) -> ctypes.Array:
@@ -246,11 +263,12 @@ def spccl_vr_reduce_scatter(send: list, recv: list, scratch: torch.Tensor, polic
     return _trace(tr, P * (P - 1))
 
 
-def spccl_vr_all_gather(send: list, recv: list, scratch: torch.Tensor, stream=None) -> list:
+def spccl_vr_all_gather(send: list, recv: list, scratch: torch.Tensor, policy=None, stream=None) -> list:
     P, n = len(send), send[0].numel()
     tr = (spccl_trace_t * P)()
-    _check(_lib.spccl_vr_all_gather(_ptrs(send), _ptrs(recv), P, n, _dt(send[0]), scratch.data_ptr(),
-                                    _nbytes(scratch), tr, _stream(stream)), "spccl_vr_all_gather")
+    pol = _policy(policy)
+    _check(_lib.spccl_vr_all_gather(_ptrs(send), _ptrs(recv), P, n, _dt(send[0]), ctypes.byref(pol),
+                                    scratch.data_ptr(), _nbytes(scratch), tr, _stream(stream)), "spccl_vr_all_gather")
     return _trace(tr, P)
 
 
@@ -310,9 +328,9 @@ def alloc_sliced(n: int, dtype: int, device="cuda") -> torch.Tensor:
 
 # ---- tensor helpers (allocation stays with the caller; these only size buffers) -----
 
-def alloc_stream(n: int, dtype: int, device="cuda") -> torch.Tensor:
-    """A uint8 buffer able to hold any message of n elements."""
-    return torch.empty(spccl_stream_bound(n, dtype), dtype=torch.uint8, device=device)
+def alloc_stream(n: int, dtype: int, device="cuda", fmt: int = SPCCL_FMT_PICI) -> torch.Tensor:
+    """A uint8 buffer able to hold any n-element message of format fmt (or dense)."""
+    return torch.empty(spccl_message_bound(n, dtype, fmt), dtype=torch.uint8, device=device)
 
 
 def alloc_workspace(n: int, dtype: int, device="cuda", stream=None, minimal: bool = False) -> torch.Tensor:

@@ -13,6 +13,7 @@
 namespace spccl {
 spccl_status_t launch_to_pici_dt(int dtype, int sa, int sb, const PiciSinkArgs& g, hipStream_t st);
 spccl_status_t launch_to_dense_dt(int dtype, int sa, int sb, const DenseSinkArgs& g, hipStream_t st);
+spccl_status_t launch_to_coo_dt(int dtype, int sa, int sb, const PiciSinkArgs& g, hipStream_t st);
 spccl_status_t launch_gather_dt(int dtype, const GatherArgs& g, int P, hipStream_t st);
 spccl_status_t launch_dense_dense_dt(int dtype, const uint8_t* a_hdr, const uint8_t* a, uint64_t a_cap,
                                      const uint8_t* b_hdr, const uint8_t* b, uint64_t b_cap, uint8_t* out_hdr,
@@ -31,6 +32,11 @@ namespace {
 
 inline bool dtype_ok(int32_t dt) { return dt == kF32 || dt == kBF16; }
 inline uint64_t slots_offset(uint64_t n) { return (kWsFlagsOffset + 8ull * num_parts(n) + 255ull) & ~255ull; }
+// Workspace regions: control block, look-back words, value slots (the
+// two-pass Pici sink and the COO sink), index slots (the COO sink).
+inline uint64_t value_slots_end(uint64_t n, int32_t dt) {
+    return slots_offset(n) + num_parts(n) * kPartElems * elem_bytes(dt);
+}
 
 // Every single-pass launch tags its look-back words with a fresh epoch, so a
 // workspace never needs clearing between calls: words left by earlier calls
@@ -80,6 +86,10 @@ spccl_status_t decode_input(const spccl_operand_t& o, uint64_t n, int32_t dt, Sr
     } else if (o.fmt == SPCCL_FMT_PICI) {
         if (o.bytes < off_A(n)) return SPCCL_ERR_CAPACITY;
         *out = Src{SRC_PICI, DevOperand{p, p, o.bytes}};
+    } else if (o.fmt == SPCCL_FMT_COO) {
+        // nothing of a COO message is read before its header is checked
+        if (o.bytes < kHeaderBytes) return SPCCL_ERR_CAPACITY;
+        *out = Src{SRC_COO, DevOperand{p, p, o.bytes}};
     } else {
         return SPCCL_ERR_INVALID_ARG;
     }
@@ -110,7 +120,20 @@ uint64_t spccl_workspace_min_bytes(uint64_t n, int32_t dtype) {
 }
 
 uint64_t spccl_workspace_bytes(uint64_t n, int32_t dtype) {
-    return slots_offset(n) + num_parts(n) * kPartElems * elem_bytes(dtype);
+    return value_slots_end(n, dtype) + num_parts(n) * kPartElems * 4ull;
+}
+
+uint64_t spccl_coo_bytes(int32_t dtype, uint64_t nnz) { return dtype_ok(dtype) ? coo_bytes(dtype, nnz) : 0; }
+
+uint64_t spccl_message_bound(uint64_t n, int32_t dtype, int32_t fmt) {
+    if (!dtype_ok(dtype)) return 0;
+    const uint64_t d = dense_msg_bytes(n, dtype);
+    uint64_t w;
+    if (fmt == SPCCL_FMT_DENSE) w = d;
+    else if (fmt == SPCCL_FMT_PICI) w = pici_bytes(n, dtype, n);
+    else if (fmt == SPCCL_FMT_COO) w = coo_bytes(dtype, n);
+    else return 0;
+    return w > d ? w : d;
 }
 
 spccl_status_t spccl_workspace_init(void* ws, uint64_t ws_bytes, void* stream) {
@@ -128,7 +151,7 @@ spccl_status_t spccl_compress(const void* dense, uint64_t n, int32_t dtype, void
     spccl_status_t st = check_ws(ws, ws_bytes, spccl_workspace_min_bytes(n, dtype));
     if (st != SPCCL_OK) return st;
     PiciSinkArgs g{};
-    g.slots = ws_bytes >= spccl_workspace_bytes(n, dtype) ? static_cast<uint8_t*>(ws) + slots_offset(n) : nullptr;
+    g.slots = ws_bytes >= value_slots_end(n, dtype) ? static_cast<uint8_t*>(ws) + slots_offset(n) : nullptr;
     g.a = DevOperand{nullptr, static_cast<const uint8_t*>(dense), n * elem_bytes(dtype)};
     g.out = static_cast<uint8_t*>(out);
     g.n = n;
@@ -138,6 +161,40 @@ spccl_status_t spccl_compress(const void* dense, uint64_t n, int32_t dtype, void
     g.ctrl = static_cast<WsCtrl*>(ws);
     g.flags = reinterpret_cast<uint64_t*>(static_cast<uint8_t*>(ws) + kWsFlagsOffset);
     return launch_to_pici_dt(dtype, SRC_DENSE, SRC_NONE, g, as_stream(stream));
+}
+
+namespace {
+// The COO sink (three passes; needs the full workspace with its slots).
+spccl_status_t run_coo_sink(const Src& sa, const Src& sb, uint8_t* out, uint64_t n, int32_t dtype, void* ws,
+                            uint64_t ws_bytes, hipStream_t hs) {
+    spccl_status_t st = check_ws(ws, ws_bytes, spccl_workspace_bytes(n, dtype));
+    if (st != SPCCL_OK) return st;
+    PiciSinkArgs g{};
+    g.slots = static_cast<uint8_t*>(ws) + slots_offset(n);
+    g.idx_slots = reinterpret_cast<uint32_t*>(static_cast<uint8_t*>(ws) + value_slots_end(n, dtype));
+    g.a = sa.dev;
+    g.b = sb.dev;
+    g.out = out;
+    g.n = n;
+    g.T = num_tiles(n);
+    g.nparts = (uint32_t)num_parts(n);
+    g.epoch = next_epoch();
+    g.ctrl = static_cast<WsCtrl*>(ws);
+    g.flags = reinterpret_cast<uint64_t*>(static_cast<uint8_t*>(ws) + kWsFlagsOffset);
+    return launch_to_coo_dt(dtype, sa.kind, sb.kind, g, hs);
+}
+}  // namespace
+
+spccl_status_t spccl_compress_coo(const void* dense, uint64_t n, int32_t dtype, void* out, uint64_t out_bytes,
+                                  void* ws, uint64_t ws_bytes, void* stream) {
+    if (!dtype_ok(dtype)) return SPCCL_ERR_UNSUPPORTED;
+    if (n >= (1ull << 32)) return SPCCL_ERR_UNSUPPORTED;
+    if ((n && (!dense || !aligned_elem(dense, dtype))) || !out || !aligned16(out)) return SPCCL_ERR_INVALID_ARG;
+    if (out_bytes < spccl_message_bound(n, dtype, SPCCL_FMT_COO)) return SPCCL_ERR_CAPACITY;
+    if (overlaps(dense, n * elem_bytes(dtype), out, out_bytes)) return SPCCL_ERR_INVALID_ARG;
+    const Src sa{SRC_DENSE, DevOperand{nullptr, static_cast<const uint8_t*>(dense), n * elem_bytes(dtype)}};
+    const Src sb{SRC_NONE, DevOperand{nullptr, nullptr, 0}};
+    return run_coo_sink(sa, sb, static_cast<uint8_t*>(out), n, dtype, ws, ws_bytes, as_stream(stream));
 }
 
 spccl_status_t spccl_encode_dense(const void* dense, uint64_t n, int32_t dtype, void* out, uint64_t out_bytes,
@@ -219,12 +276,23 @@ spccl_status_t spccl_reduce(spccl_operand_t a, spccl_operand_t b, spccl_operand_
     }
     hipStream_t hs = as_stream(stream);
     WsCtrl* ctrl = static_cast<WsCtrl*>(ws);
+    // Pici and COO do not meet in one call: a COO operand combines with dense
+    // operands or another COO operand, into a dense or COO result
+    const bool any_coo = sa.kind == SRC_COO || sb.kind == SRC_COO;
+    const bool any_pici = sa.kind == SRC_PICI || sb.kind == SRC_PICI;
+    const bool out_pici = out.kind == SPCCL_STREAM && out.fmt == SPCCL_FMT_PICI;
+    const bool out_coo = out.kind == SPCCL_STREAM && out.fmt == SPCCL_FMT_COO;
+    if ((any_coo && (any_pici || out_pici)) || (out_coo && any_pici)) return SPCCL_ERR_UNSUPPORTED;
+    if (out_coo) {
+        if (out.bytes < spccl_message_bound(n, dtype, SPCCL_FMT_COO)) return SPCCL_ERR_CAPACITY;
+        return run_coo_sink(sa, sb, static_cast<uint8_t*>(out.ptr), n, dtype, ws, ws_bytes, hs);
+    }
     if (out.kind == SPCCL_STREAM && out.fmt == SPCCL_FMT_PICI) {
         if (out.bytes < spccl_stream_bound(n, dtype)) return SPCCL_ERR_CAPACITY;
         st = check_ws(ws, ws_bytes, spccl_workspace_min_bytes(n, dtype));
         if (st != SPCCL_OK) return st;
         PiciSinkArgs g{};
-        g.slots = ws_bytes >= spccl_workspace_bytes(n, dtype) ? static_cast<uint8_t*>(ws) + slots_offset(n) : nullptr;
+        g.slots = ws_bytes >= value_slots_end(n, dtype) ? static_cast<uint8_t*>(ws) + slots_offset(n) : nullptr;
         g.a = sa.dev;
         g.b = sb.dev;
         g.out = static_cast<uint8_t*>(out.ptr);

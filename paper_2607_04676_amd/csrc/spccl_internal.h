@@ -16,7 +16,7 @@ constexpr uint32_t kBlockThreads = kWave * kWavesPerBlock;
 constexpr uint32_t kTilesPerPart = kWavesPerBlock;   // look-back partition = one block
 constexpr uint32_t kStageBytes = 4096;          // LDS staging per wave
 
-constexpr int kFmtDense = 0, kFmtPici = 1;
+constexpr int kFmtDense = 0, kFmtPici = 1, kFmtCoo = 2;
 constexpr int kKindArray = 0, kKindStream = 1;
 constexpr int kF32 = 0, kBF16 = 1;
 
@@ -40,6 +40,12 @@ __host__ __device__ inline uint64_t pici_bytes(uint64_t n, int dtype, uint64_t n
 __host__ __device__ inline uint64_t dense_msg_bytes(uint64_t n, int dtype) {
     return kHeaderBytes + n * elem_bytes(dtype);
 }
+// COO message: header, J (nnz 32-bit flat indices, increasing) at 48, zero
+// pad to 16 bytes, V (nnz values) at coo_off_V(nnz).
+__host__ __device__ inline uint64_t coo_off_V(uint64_t nnz) { return (kHeaderBytes + 4ull * nnz + 15ull) & ~15ull; }
+__host__ __device__ inline uint64_t coo_bytes(int dtype, uint64_t nnz) {
+    return coo_off_V(nnz) + nnz * elem_bytes(dtype);
+}
 constexpr uint64_t kPartElems = (uint64_t)kTilesPerPart * kTileElems;
 
 __host__ __device__ inline uint64_t num_parts(uint64_t n) {
@@ -49,12 +55,12 @@ __host__ __device__ inline uint64_t num_parts(uint64_t n) {
 }
 
 // Source kinds of the tile pipeline.
-enum SrcKind { SRC_NONE = 0, SRC_DENSE = 1, SRC_PICI = 2 };
+enum SrcKind { SRC_NONE = 0, SRC_DENSE = 1, SRC_PICI = 2, SRC_COO = 3 };
 
 // A reduce / codec operand as the kernels see it.
 struct DevOperand {
     const uint8_t* hdr;    // message header, or nullptr for a raw array
-    const uint8_t* data;   // raw array base, or the message base for Pici
+    const uint8_t* data;   // raw array base, or the message base for Pici / COO
     uint64_t cap;          // capacity of the message buffer in bytes
 };
 
@@ -68,6 +74,7 @@ struct PiciSinkArgs {
     WsCtrl* ctrl;
     uint64_t* flags;
     uint8_t* slots;        // two-pass mode: one worst-case slot of compacted values per partition
+    uint32_t* idx_slots;   // COO output: one worst-case slot of flat indices per partition
 };
 
 struct DenseSinkArgs {

@@ -139,6 +139,8 @@ __device__ HeaderView check_header(const HeaderWords& hw, uint64_t cap, uint64_t
         ok = ok && oI == off_I(n) && oA == off_A(n) && nnz <= n && total == oA + nnz * elem_bytes(dtype);
     else if (fmt == (uint32_t)kFmtDense)
         ok = ok && oA == kHeaderBytes && total == dense_msg_bytes(n, dtype);
+    else if (fmt == (uint32_t)kFmtCoo)
+        ok = ok && oI == kHeaderBytes && nnz <= n && oA == coo_off_V(nnz) && total == coo_bytes(dtype, nnz);
     else
         ok = false;
     v.ok = ok;
@@ -324,6 +326,162 @@ __device__ __forceinline__ void expand_pici(PiciCols pc, const uint8_t* msg, uin
     }
 }
 
+// ---------------------------------------------------------------------------
+// COO sources (Sec. II-B format: J = flat 32-bit indices, increasing; V =
+// values in index order).  A tile's entries are a contiguous range of J,
+// found by searching J for the tile's first element; inside the tile they
+// are row-major, so row r's entries are contiguous and sorted by column.
+
+// Lower bound of `key` in J[lo, hi) -- the first position whose index is
+// >= key, hi if none -- searched by G groups of 64/G consecutive lanes, each
+// group with its own key and range: every round each lane of a group probes
+// one position and the group keeps the one interval between probes that
+// holds the answer, so a range of length L takes about log_{64/G}(L)
+// rounds of dependent loads.  J is read only inside [lo, hi).  The result
+// depends only on (J, lo, hi, key), so two waves that search the same key
+// over the same range agree and neighbouring tiles' ranges meet exactly
+// even when J is corrupt.
+template <int G>
+__device__ uint32_t coo_lower_bound(const uint32_t* J, uint32_t lo, uint32_t hi, uint64_t key) {
+    constexpr uint32_t W = 64 / G;
+    const uint32_t l = lane_id(), j = l % W, sh = (l / W) * W;
+    const uint64_t gmask = W == 64 ? ~0ull : (((1ull << W) - 1ull) << sh);
+    while (__any(hi > lo)) {
+        const uint32_t len = hi - lo;
+        const uint32_t step = len ? (len + W - 1) / W : 1u;
+        const uint32_t p = lo + j * step;
+        const bool valid = len != 0 && p < hi;
+        const bool ge = valid && (uint64_t)J[p] >= key;
+        const uint64_t mg = __ballot(ge) & gmask, mv = __ballot(valid) & gmask;
+        if (len) {
+            const uint32_t nv = (uint32_t)__popcll(mv);
+            const uint32_t f = mg ? (uint32_t)__builtin_ctzll(mg) - sh : nv;
+            const uint32_t nlo = f == 0 ? lo : lo + (f - 1) * step + 1;
+            const uint32_t nhi = f < nv ? lo + f * step : hi;
+            lo = nlo;
+            hi = nhi;
+        }
+    }
+    return lo;
+}
+
+// Per-wave LDS of a COO tile expansion: row r's staged entries as a column
+// mask and the stage position of the first of them.
+struct CooLds {
+    uint64_t rw[64];
+    uint32_t rf[64];
+};
+
+constexpr uint32_t kCooChunk = 512;            // entries staged at a time (8 per lane)
+constexpr int kCooSlots = kCooChunk / 64;
+
+// popcount of the bits of w below this lane
+__device__ __forceinline__ uint32_t bits_below_lane(uint64_t w) {
+    return __builtin_amdgcn_mbcnt_hi((uint32_t)(w >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)w, 0u));
+}
+
+// Entries [lo, hi) of a checked COO message, claimed by tile t, checked:
+// every index inside the tile and below n, strictly increasing.  Uniform.
+__device__ bool coo_range_ok(const uint32_t* J, uint32_t lo, uint32_t hi, uint64_t t, uint64_t n) {
+    const uint32_t l = lane_id();
+    const uint64_t t0 = t * kTileElems, tend = t0 + kTileElems < n ? t0 + kTileElems : n;
+    bool bad = hi < lo || hi - lo > kTileElems;
+    if (!__any(bad)) {
+        for (uint32_t i0 = 0; i0 < hi - lo; i0 += kCooChunk) {
+            uint32_t x[kCooSlots], y[kCooSlots];
+#pragma unroll
+            for (int q = 0; q < kCooSlots; q++) {
+                const uint32_t i = i0 + l + 64 * q;
+                x[q] = i < hi - lo ? J[lo + i] : 0u;
+                y[q] = (i > 0 && i < hi - lo) ? J[lo + i - 1] : 0u;
+            }
+#pragma unroll
+            for (int q = 0; q < kCooSlots; q++) {
+                const uint32_t i = i0 + l + 64 * q;
+                if (i < hi - lo) bad = bad || x[q] < t0 || x[q] >= tend || (i > 0 && x[q] <= y[q]);
+            }
+        }
+    }
+    return !__any(bad);
+}
+
+// Adds tile t's COO entries [lo, hi) (already checked) into v (First: v =
+// the entries, zero elsewhere).  kCooChunk entries at a time: each lane takes
+// entries l, l+64, ..., stages their values in LDS, sets bit c of row word r
+// and, for the first entry of a row in the chunk, records the row's stage
+// position; then lane c reads row r's value at rf[r] + (set bits of rw[r]
+// below c).
+template <class E, bool First>
+__device__ void coo_expand_tile(const uint32_t* J, const typename E::raw* V, uint32_t lo, uint32_t hi, uint64_t t,
+                                typename E::raw* stage, CooLds* cl, uint32_t (&v)[64]) {
+    using raw = typename E::raw;
+    const uint32_t l = lane_id();
+    const uint64_t t0 = t * kTileElems;
+    if (First) {
+#pragma unroll
+        for (int r = 0; r < 64; r++) v[r] = 0;
+    }
+    const uint32_t cnt = hi - lo;
+#pragma unroll 1
+    for (uint32_t i0 = 0; i0 < cnt; i0 += kCooChunk) {
+        const uint32_t m = cnt - i0 < kCooChunk ? cnt - i0 : kCooChunk;
+        uint32_t x[kCooSlots], y[kCooSlots];
+        raw val[kCooSlots];
+#pragma unroll
+        for (int q = 0; q < kCooSlots; q++) {
+            const uint32_t i = l + 64 * q;
+            x[q] = i < m ? J[lo + i0 + i] : 0u;
+            y[q] = (i > 0 && i < m) ? J[lo + i0 + i - 1] : 0u;
+            val[q] = i < m ? V[lo + i0 + i] : (raw)0;
+        }
+        cl->rw[l] = 0ull;
+        wave_lds_sync();
+#pragma unroll
+        for (int q = 0; q < kCooSlots; q++) {
+            const uint32_t i = l + 64 * q;
+            if (i < m) {
+                const uint32_t loc = (uint32_t)(x[q] - t0), r = loc >> 6;
+                stage[i] = val[q];
+                atomicOr((unsigned long long*)&cl->rw[r], 1ull << (loc & 63u));
+                if (i == 0 || (y[q] >> 6) != (x[q] >> 6)) cl->rf[r] = i;
+            }
+        }
+        wave_lds_sync();
+        const uint64_t myrw = cl->rw[l];
+        const uint32_t myrf = cl->rf[l];
+        wave_lds_sync();
+#pragma unroll
+        for (int r = 0; r < 64; r++) {
+            const uint64_t w = ((uint64_t)lane_bcast((uint32_t)(myrw >> 32), r) << 32) | lane_bcast((uint32_t)myrw, r);
+            if (w != 0ull) {
+                if ((w >> l) & 1ull) {
+                    const uint32_t xv = stage[lane_bcast(myrf, r) + bits_below_lane(w)];
+                    v[r] = First ? xv : oplus(E{}, v[r], xv);
+                }
+            }
+        }
+        wave_lds_sync();
+    }
+}
+
+// Tile t of a checked COO message (nnz entries) into v: its entry range is
+// searched for, checked, and expanded; a tile that fails the checks is
+// flagged and reads as empty.
+template <class E, bool First>
+__device__ void coo_tile(const uint8_t* msg, uint64_t nnz, uint64_t t, uint64_t n, typename E::raw* stage,
+                         CooLds* cl, WsCtrl* ctrl, uint32_t (&v)[64]) {
+    using raw = typename E::raw;
+    const uint32_t* J = reinterpret_cast<const uint32_t*>(msg + kHeaderBytes);
+    const raw* V = reinterpret_cast<const raw*>(msg + coo_off_V(nnz));
+    const uint64_t T = num_tiles(n);
+    const uint64_t key = (lane_id() < 32 ? t : t + 1) * kTileElems;
+    const uint32_t b = coo_lower_bound<2>(J, 0u, (uint32_t)nnz, key);
+    const uint32_t lo = lane_bcast(b, 0), hi = lane_bcast(b, 32);
+    const bool ok = (t + 1 < T || hi == nnz) && coo_range_ok(J, lo, hi, t, n);
+    if (!ok && lane_id() == 0) set_status(ctrl, SPCCL_ERR_CORRUPT_STREAM);
+    coo_expand_tile<E, First>(J, V, lo, ok ? hi : lo, t, stage, cl, v);
+}
+
 // Tile t of a (+) b into v[64] (sources: dense rows or Pici tiles; b may be
 // absent).  Every read that needs no header -- the headers themselves, dense
 // rows, Pici column words and offsets -- is issued first; the headers are
@@ -335,7 +493,7 @@ __device__ __forceinline__ void expand_pici(PiciCols pc, const uint8_t* msg, uin
 // of the grid, when a header fails its check (and flags it once).
 template <class E, int SA, int SB>
 __device__ __forceinline__ bool load_tile_pair(const DevOperand& a, const DevOperand& b, uint64_t t, bool has_tile,
-                                               uint64_t n, typename E::raw* stage, WsCtrl* ctrl,
+                                               uint64_t n, typename E::raw* stage, CooLds* cl, WsCtrl* ctrl,
                                                uint32_t (&v)[64]) {
     const bool ha = a.hdr != nullptr;
     const bool hb = SB != SRC_NONE && b.hdr != nullptr;
@@ -352,13 +510,15 @@ __device__ __forceinline__ bool load_tile_pair(const DevOperand& a, const DevOpe
     }
     bool ok = true;
     uint64_t nnza = 0, nnzb = 0;
+    constexpr int fa = SA == SRC_PICI ? kFmtPici : (SA == SRC_COO ? kFmtCoo : kFmtDense);
+    constexpr int fb = SB == SRC_PICI ? kFmtPici : (SB == SRC_COO ? kFmtCoo : kFmtDense);
     if (ha) {
-        const HeaderView h = check_header(hwa, a.cap, n, E::dtype, SA == SRC_PICI ? kFmtPici : kFmtDense);
+        const HeaderView h = check_header(hwa, a.cap, n, E::dtype, fa);
         ok = ok && h.ok;
         nnza = h.nnz;
     }
     if (hb) {
-        const HeaderView h = check_header(hwb, b.cap, n, E::dtype, SB == SRC_PICI ? kFmtPici : kFmtDense);
+        const HeaderView h = check_header(hwb, b.cap, n, E::dtype, fb);
         ok = ok && h.ok;
         nnzb = h.nnz;
     }
@@ -368,10 +528,15 @@ __device__ __forceinline__ bool load_tile_pair(const DevOperand& a, const DevOpe
     }
     if (has_tile) {
         constexpr bool dense_first = SA == SRC_DENSE || SB == SRC_DENSE;
+        constexpr bool a_sparse = SA == SRC_PICI || SA == SRC_COO;
         if constexpr (SA == SRC_PICI)
             expand_pici<E, !dense_first>(pici_columns(ma, nnza, t, n, ctrl), a.data, n, stage, v);
+        if constexpr (SA == SRC_COO)
+            coo_tile<E, !dense_first>(a.data, nnza, t, n, stage, cl, ctrl, v);
         if constexpr (SB == SRC_PICI)
-            expand_pici<E, !dense_first && SA != SRC_PICI>(pici_columns(mb, nnzb, t, n, ctrl), b.data, n, stage, v);
+            expand_pici<E, !dense_first && !a_sparse>(pici_columns(mb, nnzb, t, n, ctrl), b.data, n, stage, v);
+        if constexpr (SB == SRC_COO)
+            coo_tile<E, !dense_first && !a_sparse>(b.data, nnzb, t, n, stage, cl, ctrl, v);
     }
     return true;
 }
@@ -513,7 +678,7 @@ __global__ void __launch_bounds__(kBlockThreads) k_to_pici(PiciSinkArgs g) {
     const bool has_tile = t < g.T;
 
     uint32_t v[64];
-    if (!load_tile_pair<E, SA, SB>(g.a, g.b, t, has_tile, g.n, stage, g.ctrl, v))
+    if (!load_tile_pair<E, SA, SB>(g.a, g.b, t, has_tile, g.n, stage, nullptr, g.ctrl, v))
         return;                   // uniform over the grid: no partition publishes
     uint64_t w = 0;
     uint32_t c = 0;
@@ -1039,6 +1204,175 @@ __global__ void __launch_bounds__(kBlockThreads) k_place(PiciSinkArgs g) {
 }
 
 // ---------------------------------------------------------------------------
+// COO sink: out = COO(srcA (+) srcB) (Sec. II-B format), in three passes.
+// The value array of a COO message starts after all nnz indices, so no entry
+// can be placed before the total is known:
+//   k_to_coo       each partition (one block, one tile per wave) computes its
+//                  tiles, counts, publishes its aggregate and parks its
+//                  (index, value) entries in its own worst-case slots; never
+//                  waits on another block;
+//   k_coo_total    one block turns the aggregates into exclusive prefixes
+//                  (written back into the look-back words) and writes the
+//                  header and the pad;
+//   k_place_coo    one wave per partition moves its entries into place.
+// Entries leave a tile in row-major order, i.e. by increasing flat index:
+// row r's present lanes are a ballot mask, and each takes the position of
+// the set bits below it.
+
+constexpr uint32_t kCooOut = 1024;             // entries staged per wave before a flush
+
+template <class E, int SA, int SB>
+__global__ void __launch_bounds__(kBlockThreads) k_to_coo(PiciSinkArgs g) {
+    using raw = typename E::raw;
+    constexpr bool coo_in = SA == SRC_COO || SB == SRC_COO;
+    __shared__ raw stage_all[kWavesPerBlock][E::cap];
+    __shared__ uint32_t sidx_all[kWavesPerBlock][kCooOut];
+    __shared__ CooLds coo_all[coo_in ? kWavesPerBlock : 1];
+    __shared__ uint32_t s_cnt[kWavesPerBlock];
+    const uint32_t wave = threadIdx.x >> 6, l = lane_id();
+    raw* stage = stage_all[wave];
+    uint32_t* sidx = sidx_all[wave];
+    const uint32_t p = blockIdx.x;
+    const uint32_t epoch30 = g.epoch & 0x3FFFFFFFu;
+    const uint64_t t = (uint64_t)p * kTilesPerPart + wave;
+    const bool has_tile = t < g.T;
+    uint32_t v[64];
+    if (!load_tile_pair<E, SA, SB>(g.a, g.b, t, has_tile, g.n, stage, &coo_all[coo_in ? wave : 0], g.ctrl, v))
+        return;                   // uniform over the grid: no partition publishes
+    uint32_t tilecnt = 0;
+    if (has_tile) {
+#pragma unroll
+        for (int r = 0; r < 64; r++) tilecnt += (uint32_t)__popcll(__ballot(v[r] != 0u));
+    }
+    if (l == 0) s_cnt[wave] = tilecnt;
+    __syncthreads();
+    uint32_t tile_excl = 0, agg = 0;
+#pragma unroll
+    for (uint32_t k = 0; k < kWavesPerBlock; k++) {
+        const uint32_t ck = s_cnt[k];
+        tile_excl += k < wave ? ck : 0u;
+        agg += ck;
+    }
+    if (threadIdx.x == 0) publish(g.flags, p, epoch30, kFlagAggregate, agg);
+    if (!has_tile) return;
+    uint32_t* islot = g.idx_slots + (uint64_t)p * kPartElems + tile_excl;
+    raw* vslot = reinterpret_cast<raw*>(g.slots) + (uint64_t)p * kPartElems + tile_excl;
+    const uint32_t base_idx = (uint32_t)(t * kTileElems) + l;
+    uint32_t done = 0, rank = 0;                 // entries flushed, entries staged
+    wave_lds_sync();                             // the COO source's stage reads are over
+#pragma unroll
+    for (int r = 0; r < 64; r++) {
+        const uint64_t m = __ballot(v[r] != 0u);
+        if (m) {
+            const uint32_t c = (uint32_t)__popcll(m);
+            if (rank + c > kCooOut) {
+                wave_lds_sync();
+                for (uint32_t i = l; i < rank; i += 64) { islot[done + i] = sidx[i]; vslot[done + i] = stage[i]; }
+                wave_lds_sync();
+                done += rank;
+                rank = 0;
+            }
+            if (v[r] != 0u) {
+                const uint32_t pos = rank + bits_below_lane(m);
+                sidx[pos] = base_idx + 64u * (uint32_t)r;
+                stage[pos] = (raw)v[r];
+            }
+            rank += c;
+        }
+    }
+    wave_lds_sync();
+    for (uint32_t i = l; i < rank; i += 64) { islot[done + i] = sidx[i]; vslot[done + i] = stage[i]; }
+}
+
+// One block: exclusive prefixes of the partitions' aggregates (each thread
+// sums a contiguous run of partitions, the block scans the run totals), the
+// header and the pad between J and V.  A partition that did not publish
+// (an input failed its header check) stops the call: nothing is written.
+constexpr uint32_t kTotalThreads = 1024;
+
+template <class E>
+__global__ void __launch_bounds__(kTotalThreads) k_coo_total(PiciSinkArgs g) {
+    __shared__ uint32_t s_wsum[kTotalThreads / 64];
+    __shared__ uint32_t s_bad;
+    const uint32_t tid = threadIdx.x, l = lane_id(), wave = tid >> 6;
+    const uint32_t epoch30 = g.epoch & 0x3FFFFFFFu;
+    const uint32_t per = (g.nparts + kTotalThreads - 1) / kTotalThreads;
+    const uint32_t p0 = tid * per, p1 = p0 + per < g.nparts ? p0 + per : g.nparts;
+    if (tid == 0) s_bad = 0;
+    __syncthreads();
+    uint32_t run = 0;
+    bool bad = false;
+    for (uint32_t q = p0; q < p1; q++) {
+        const uint64_t f = __hip_atomic_load(&g.flags[q], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        bad = bad || (uint32_t)(f >> 34) != epoch30 || (uint32_t)f > kPartElems;
+        run += (uint32_t)f;
+    }
+    if (bad) s_bad = 1;
+    const uint32_t incl = wave_incl_scan(run);
+    if (l == 63) s_wsum[wave] = incl;
+    __syncthreads();
+    if (s_bad) {
+        if (tid == 0) set_status(g.ctrl, SPCCL_ERR_WORKSPACE);
+        return;
+    }
+    uint32_t wbase = 0, total = 0;
+    for (uint32_t k = 0; k < kTotalThreads / 64; k++) {
+        const uint32_t x = s_wsum[k];
+        wbase += k < wave ? x : 0u;
+        total += x;
+    }
+    uint32_t excl = wbase + incl - run;
+    for (uint32_t q = p0; q < p1; q++) {
+        const uint64_t f = g.flags[q];
+        publish(g.flags, q, epoch30, kFlagPrefix, excl);
+        excl += (uint32_t)f;
+    }
+    const uint64_t nnz = total, oV = coo_off_V(nnz);
+    if (tid == 0) write_header(g.out, kFmtCoo, E::dtype, g.n, nnz, kHeaderBytes, oV, coo_bytes(E::dtype, nnz));
+    for (uint64_t b = kHeaderBytes + 4 * nnz + tid; b < oV; b += kTotalThreads) g.out[b] = 0;
+}
+
+// One wave per partition: its prefix and count from the scanned words, all
+// its slot reads before its stores.
+template <class E>
+__global__ void __launch_bounds__(kBlockThreads) k_place_coo(PiciSinkArgs g) {
+    using raw = typename E::raw;
+    constexpr int U = 8;
+    const uint32_t wave = threadIdx.x >> 6, l = lane_id();
+    const uint32_t p = blockIdx.x * kWavesPerBlock + wave;
+    if (p >= g.nparts) return;
+    const uint32_t epoch30 = g.epoch & 0x3FFFFFFFu;
+    const uint64_t f = g.flags[p];
+    const uint64_t fn = p + 1 < g.nparts ? g.flags[p + 1] : 0ull;
+    const HeaderWords hw = load_header_words(g.out);
+    const uint64_t nnz = hw.w[2];
+    if ((uint32_t)hw.w[0] != kMagic || (uint32_t)(f >> 34) != epoch30 || ((uint32_t)(f >> 32) & 3u) != kFlagPrefix)
+        return;                   // k_coo_total stopped the call
+    const uint32_t prefix = (uint32_t)f;
+    const uint32_t next = p + 1 < g.nparts ? (uint32_t)fn : (uint32_t)nnz;
+    const uint32_t cnt = next - prefix;
+    const uint32_t* islot = g.idx_slots + (uint64_t)p * kPartElems;
+    const raw* vslot = reinterpret_cast<const raw*>(g.slots) + (uint64_t)p * kPartElems;
+    uint32_t* J = reinterpret_cast<uint32_t*>(g.out + kHeaderBytes) + prefix;
+    raw* V = reinterpret_cast<raw*>(g.out + coo_off_V(nnz)) + prefix;
+    for (uint32_t i0 = l; i0 < cnt; i0 += 64 * U) {
+        uint32_t x[U];
+        raw y[U];
+#pragma unroll
+        for (int u = 0; u < U; u++) {
+            const uint32_t i = i0 + 64 * u;
+            x[u] = i < cnt ? islot[i] : 0u;
+            y[u] = i < cnt ? vslot[i] : (raw)0;
+        }
+#pragma unroll
+        for (int u = 0; u < U; u++) {
+            const uint32_t i = i0 + 64 * u;
+            if (i < cnt) { J[i] = x[u]; V[i] = y[u]; }
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
 // Dense sink: out[i] = (srcA (+) srcB)[i] for every i < n.
 
 template <class E>
@@ -1060,12 +1394,15 @@ __device__ __forceinline__ void store_tile(uint8_t* out, uint64_t t, uint64_t n,
 template <class E, int SA, int SB>
 __global__ void __launch_bounds__(kBlockThreads) k_to_dense(DenseSinkArgs g) {
     using raw = typename E::raw;
+    constexpr bool coo = SA == SRC_COO || SB == SRC_COO;
     __shared__ raw stage_all[kWavesPerBlock][E::cap];
+    __shared__ CooLds coo_all[coo ? kWavesPerBlock : 1];
     const uint32_t wave = threadIdx.x >> 6;
     const uint64_t t = (uint64_t)blockIdx.x * kWavesPerBlock + wave;
     const bool has_tile = t < g.T;
     uint32_t v[64];
-    if (!load_tile_pair<E, SA, SB>(g.a, g.b, t, has_tile, g.n, stage_all[wave], g.ctrl, v)) return;
+    if (!load_tile_pair<E, SA, SB>(g.a, g.b, t, has_tile, g.n, stage_all[wave], &coo_all[coo ? wave : 0], g.ctrl, v))
+        return;
     if (blockIdx.x == 0 && threadIdx.x == 0 && g.out_hdr)
         write_header(g.out_hdr, kFmtDense, E::dtype, g.n, kNnzUnknown, 0, kHeaderBytes, dense_msg_bytes(g.n, E::dtype));
     if (!has_tile) return;
@@ -1140,10 +1477,52 @@ __device__ __forceinline__ void store_from_stage(typename E::raw* col, uint64_t 
 template <class E, int K>
 __device__ __forceinline__ void expand_tiles(const uint8_t* msg, const uint8_t* d, uint32_t fmt, uint64_t nnz,
                                              uint64_t n, uint64_t T, uint64_t t0, typename E::raw* out,
-                                             typename E::raw* stage, WsCtrl* ctrl) {
+                                             typename E::raw* stage, CooLds* cl, WsCtrl* ctrl) {
     using raw = typename E::raw;
     const uint32_t l = lane_id();
     const uint64_t g_n = n, g_T = T;
+    if (fmt == (uint32_t)kFmtCoo) {
+        // the wave's entry range (searched over the whole index array, so
+        // neighbouring waves meet exactly), then its tiles' boundaries
+        // inside it; every tile's entries are checked before use
+        const uint32_t* J = reinterpret_cast<const uint32_t*>(msg + kHeaderBytes);
+        const raw* V = reinterpret_cast<const raw*>(msg + coo_off_V(nnz));
+        const uint64_t tend = t0 + K < g_T ? t0 + K : g_T;
+        const uint32_t nt = (uint32_t)(tend - t0);
+        const uint32_t b = coo_lower_bound<2>(J, 0u, (uint32_t)nnz, (l < 32 ? t0 : tend) * kTileElems);
+        const uint32_t lo = lane_bcast(b, 0), hi = lane_bcast(b, 32);
+        bool ok = hi >= lo && (tend < g_T || hi == nnz);
+        uint32_t bnd[K + 1];
+        bnd[0] = lo;
+#pragma unroll
+        for (int k = 1; k <= K; k++) bnd[k] = hi;
+        if (K > 1 && nt > 1 && ok) {
+            const uint32_t gi = l / 16;
+            const uint64_t key = (t0 + 1 + (gi < nt - 1 ? gi : nt - 2)) * kTileElems;
+            const uint32_t c = coo_lower_bound<4>(J, lo, hi, key);
+#pragma unroll
+            for (int k = 1; k < K; k++)
+                if ((uint32_t)k < nt) bnd[k] = lane_bcast(c, 16 * (k - 1));
+#pragma unroll
+            for (int k = 0; k < K; k++)
+                if ((uint32_t)k < nt) ok = ok && bnd[k + 1] >= bnd[k];
+        }
+        if (!ok && l == 0) set_status(ctrl, SPCCL_ERR_CORRUPT_STREAM);
+#pragma unroll 1
+        for (uint32_t k = 0; k < nt; k++) {
+            const uint64_t t = t0 + k;
+            uint32_t lo_k = bnd[0], hi_k = bnd[0];
+#pragma unroll
+            for (int q = 0; q < K; q++)
+                if ((uint32_t)q == k) { lo_k = bnd[q]; hi_k = bnd[q + 1]; }
+            bool tok = ok && coo_range_ok(J, lo_k, hi_k, t, g_n);
+            if (ok && !tok && l == 0) set_status(ctrl, SPCCL_ERR_CORRUPT_STREAM);
+            uint32_t v[64];
+            coo_expand_tile<E, true>(J, V, lo_k, tok ? hi_k : lo_k, t, stage, cl, v);
+            store_tile<E>(reinterpret_cast<uint8_t*>(out), t, g_n, v);
+        }
+        return;
+    }
     if (fmt != (uint32_t)kFmtPici) {
         // a dense message: copy its tiles, 16 rows at a time
 #pragma unroll 1
@@ -1244,6 +1623,7 @@ template <class E, int K>
 __global__ void __launch_bounds__(kBlockThreads) k_gather(GatherArgs g) {
     using raw = typename E::raw;
     __shared__ raw stage_all[kWavesPerBlock][kChunkVals];
+    __shared__ CooLds coo_all[kWavesPerBlock];
     __shared__ uint32_t s_ok, s_fmt;
     __shared__ uint64_t s_nnz;
     const uint32_t wave = threadIdx.x >> 6;
@@ -1263,7 +1643,7 @@ __global__ void __launch_bounds__(kBlockThreads) k_gather(GatherArgs g) {
     if (t0 >= g.T) return;
     raw* out = reinterpret_cast<raw*>(g.out + (uint64_t)blockIdx.y * g.n * sizeof(raw));
     const uint8_t* d = op.hdr ? op.hdr + kHeaderBytes : op.data;
-    expand_tiles<E, K>(op.data, d, s_fmt, s_nnz, g.n, g.T, t0, out, stage_all[wave], g.ctrl);
+    expand_tiles<E, K>(op.data, d, s_fmt, s_nnz, g.n, g.T, t0, out, stage_all[wave], &coo_all[wave], g.ctrl);
 }
 
 // ---------------------------------------------------------------------------
@@ -1331,7 +1711,7 @@ __global__ void __launch_bounds__(kBlockThreads) k_sliced(SlicedArgs g) {
         asm volatile("" ::: "memory");
         if (has_tile) fetch_dense<E, true>(a, t, ns, v);
         const HeaderView h = check_header(hw, g.slot, ns, E::dtype, -1);
-        if (!h.ok) {                                     // the same in every wave of the block
+        if (!h.ok || h.fmt == (uint32_t)kFmtCoo) {       // the same in every wave of the block
             if (threadIdx.x == 0) set_status(g.ctrl, SPCCL_ERR_CORRUPT_STREAM);
             return;
         }
@@ -1397,12 +1777,12 @@ __global__ void __launch_bounds__(kBlockThreads) k_expand_sliced(SlicedArgs g) {
     const uint64_t ns = g.n - base < kSliceElems ? g.n - base : kSliceElems;
     const uint8_t* bm = g.a + q * g.slot;
     const HeaderView h = check_header(load_header_words(bm), g.slot, ns, E::dtype, -1);
-    if (!h.ok) {
+    if (!h.ok || h.fmt == (uint32_t)kFmtCoo) {           // slices are Pici or dense
         if (lane_id() == 0) set_status(g.ctrl, SPCCL_ERR_CORRUPT_STREAM);
         return;
     }
     expand_tiles<E, kTilesPerPart>(bm, bm + kHeaderBytes, h.fmt, h.nnz, ns, num_tiles(ns), 0,
-                                   reinterpret_cast<raw*>(g.out) + base, stage_all[wave], g.ctrl);
+                                   reinterpret_cast<raw*>(g.out) + base, stage_all[wave], nullptr, g.ctrl);
 }
 
 // The virtual-rank send of a sliced stream: each slot's header.total_bytes,
@@ -1578,7 +1958,7 @@ spccl_status_t launch_to_pici(int sa, int sb, const PiciSinkArgs& g, hipStream_t
         else if (sa == SRC_DENSE && sb == SRC_DENSE) SPCCL_TO_PICI2(SRC_DENSE, SRC_DENSE);
         else if (sa == SRC_DENSE && sb == SRC_PICI) SPCCL_TO_PICI2(SRC_DENSE, SRC_PICI);
         else if (sa == SRC_PICI && sb == SRC_DENSE) SPCCL_TO_PICI2(SRC_PICI, SRC_DENSE);
-        else return SPCCL_ERR_INVALID_ARG;
+        else return SPCCL_ERR_UNSUPPORTED;
 #undef SPCCL_TO_PICI2
         spccl_status_t st1 = launch_status();
         if (st1 != SPCCL_OK) return st1;
@@ -1591,8 +1971,29 @@ spccl_status_t launch_to_pici(int sa, int sb, const PiciSinkArgs& g, hipStream_t
     else if (sa == SRC_DENSE && sb == SRC_DENSE) SPCCL_TO_PICI(SRC_DENSE, SRC_DENSE);
     else if (sa == SRC_DENSE && sb == SRC_PICI) SPCCL_TO_PICI(SRC_DENSE, SRC_PICI);
     else if (sa == SRC_PICI && sb == SRC_DENSE) SPCCL_TO_PICI(SRC_PICI, SRC_DENSE);
-    else return SPCCL_ERR_INVALID_ARG;
+    else return SPCCL_ERR_UNSUPPORTED;
 #undef SPCCL_TO_PICI
+    return launch_status();
+}
+
+// COO sink: count pass, one-block scan of the partition totals, place pass.
+template <class E>
+spccl_status_t launch_to_coo(int sa, int sb, const PiciSinkArgs& g, hipStream_t st) {
+    dim3 grid(g.nparts), block(kBlockThreads);
+#define SPCCL_TO_COO(A, B) hipLaunchKernelGGL((k_to_coo<E, A, B>), grid, block, 0, st, g)
+    if (sa == SRC_DENSE && sb == SRC_NONE) SPCCL_TO_COO(SRC_DENSE, SRC_NONE);
+    else if (sa == SRC_DENSE && sb == SRC_DENSE) SPCCL_TO_COO(SRC_DENSE, SRC_DENSE);
+    else if (sa == SRC_DENSE && sb == SRC_COO) SPCCL_TO_COO(SRC_DENSE, SRC_COO);
+    else if (sa == SRC_COO && sb == SRC_DENSE) SPCCL_TO_COO(SRC_COO, SRC_DENSE);
+    else if (sa == SRC_COO && sb == SRC_COO) SPCCL_TO_COO(SRC_COO, SRC_COO);
+    else return SPCCL_ERR_UNSUPPORTED;
+#undef SPCCL_TO_COO
+    spccl_status_t st1 = launch_status();
+    if (st1 != SPCCL_OK) return st1;
+    hipLaunchKernelGGL(k_coo_total<E>, dim3(1), dim3(kTotalThreads), 0, st, g);
+    st1 = launch_status();
+    if (st1 != SPCCL_OK) return st1;
+    hipLaunchKernelGGL(k_place_coo<E>, dim3((g.nparts + kWavesPerBlock - 1) / kWavesPerBlock), block, 0, st, g);
     return launch_status();
 }
 
@@ -1604,7 +2005,11 @@ spccl_status_t launch_to_dense(int sa, int sb, const DenseSinkArgs& g, hipStream
     else if (sa == SRC_PICI && sb == SRC_DENSE) SPCCL_TO_DENSE(SRC_PICI, SRC_DENSE);
     else if (sa == SRC_PICI && sb == SRC_PICI) SPCCL_TO_DENSE(SRC_PICI, SRC_PICI);
     else if (sa == SRC_PICI && sb == SRC_NONE) SPCCL_TO_DENSE(SRC_PICI, SRC_NONE);
-    else return SPCCL_ERR_INVALID_ARG;
+    else if (sa == SRC_DENSE && sb == SRC_COO) SPCCL_TO_DENSE(SRC_DENSE, SRC_COO);
+    else if (sa == SRC_COO && sb == SRC_DENSE) SPCCL_TO_DENSE(SRC_COO, SRC_DENSE);
+    else if (sa == SRC_COO && sb == SRC_COO) SPCCL_TO_DENSE(SRC_COO, SRC_COO);
+    else if (sa == SRC_COO && sb == SRC_NONE) SPCCL_TO_DENSE(SRC_COO, SRC_NONE);
+    else return SPCCL_ERR_UNSUPPORTED;
 #undef SPCCL_TO_DENSE
     return launch_status();
 }
@@ -1617,6 +2022,10 @@ spccl_status_t launch_to_pici_dt(int dtype, int sa, int sb, const PiciSinkArgs& 
 
 spccl_status_t launch_to_dense_dt(int dtype, int sa, int sb, const DenseSinkArgs& g, hipStream_t st) {
     return dtype == kBF16 ? launch_to_dense<BF16>(sa, sb, g, st) : launch_to_dense<F32>(sa, sb, g, st);
+}
+
+spccl_status_t launch_to_coo_dt(int dtype, int sa, int sb, const PiciSinkArgs& g, hipStream_t st) {
+    return dtype == kBF16 ? launch_to_coo<BF16>(sa, sb, g, st) : launch_to_coo<F32>(sa, sb, g, st);
 }
 
 // Tiles per wave of the expansion: enough waves to fill the chip (about

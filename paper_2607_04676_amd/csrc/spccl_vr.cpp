@@ -1,6 +1,8 @@
 // Ring collectives over P virtual ranks held in one GPU's memory (Sec. IV).
 //
-// Each rank's send / receive buffers are regions of one scratch allocation;
+// Sparse sends are Pici messages or, with policy.sparse_fmt = COO, COO
+// messages (the paper runs both, Sec. IV-D).  Each rank's send / receive
+// buffers are regions of one scratch allocation;
 // a "send" is a device-side copy of the message (its size is read from the
 // header on the device).  Format decisions are made on the host, per sending
 // rank, from the nonzero counts the compressing kernels write into the
@@ -42,15 +44,20 @@ struct Layout {
     uint8_t* slot(int which, int r, int P) const { return slots + ((uint64_t)which * P + r) * slot_bytes; }
 };
 
+// every message buffer holds the worst case of any format (COO's is the largest)
+uint64_t slot_need(uint64_t msg_elems, int32_t dtype) {
+    return round_up(spccl_message_bound(msg_elems, dtype, SPCCL_FMT_COO));
+}
+
 uint64_t scratch_need(int32_t P, uint64_t msg_elems, int32_t dtype) {
-    return round_up(spccl_workspace_bytes(msg_elems, dtype)) + 3ull * (uint64_t)P * round_up(spccl_stream_bound(msg_elems, dtype));
+    return round_up(spccl_workspace_bytes(msg_elems, dtype)) + 3ull * (uint64_t)P * slot_need(msg_elems, dtype);
 }
 
 Layout carve(void* scratch, int32_t P, uint64_t msg_elems, int32_t dtype) {
     Layout L;
     L.ws = static_cast<uint8_t*>(scratch);
     L.ws_bytes = round_up(spccl_workspace_bytes(msg_elems, dtype));
-    L.slot_bytes = round_up(spccl_stream_bound(msg_elems, dtype));
+    L.slot_bytes = slot_need(msg_elems, dtype);
     L.slots = L.ws + L.ws_bytes;
     return L;
 }
@@ -88,6 +95,20 @@ spccl_operand_t arr(const void* p, uint64_t bytes) {
 }
 spccl_operand_t msg(void* p, int fmt, uint64_t bytes) { return spccl_operand_t{SPCCL_STREAM, fmt, p, bytes}; }
 
+// the sparse encoding of the collective (Pici, or COO as in Sec. IV-D)
+spccl_status_t compress_fmt(int fmt, const void* dense, uint64_t m, int dtype, const Layout& L, uint8_t* out,
+                            hipStream_t st) {
+    if (fmt == SPCCL_FMT_COO) return spccl_compress_coo(dense, m, dtype, out, L.slot_bytes, L.ws, L.ws_bytes, st);
+    return spccl_compress(dense, m, dtype, out, L.slot_bytes, L.ws, L.ws_bytes, st);
+}
+
+const spccl_policy_t kDefaultPolicy{0.6, 0.5, 0.1, 0, 1, SPCCL_FMT_PICI};
+
+bool policy_ok(const spccl_policy_t& pol) {
+    return (pol.sparse_fmt == SPCCL_FMT_PICI || pol.sparse_fmt == SPCCL_FMT_COO) && pol.adaptive >= 0 &&
+           pol.adaptive <= 2;
+}
+
 #define SPCCL_TRY(x)                               \
     do {                                           \
         spccl_status_t st_ = (x);                  \
@@ -107,26 +128,27 @@ spccl_status_t ring_rs(void* const* send, void* const* out, int P, uint64_t n, i
         if (m && hipMemcpyAsync(out[0], send[0], m * s, hipMemcpyDeviceToDevice, st) != hipSuccess) return SPCCL_ERR_HIP;
         return SPCCL_OK;
     }
+    const int sfmt = pol.sparse_fmt;
     std::vector<int> fmt(P);
     std::vector<spccl_header_t> h;
     // step 0: compress the first chunk of every rank into slot 0
     for (int r = 0; r < P; r++) {
         const int c = (r - 1 + P) % P;
         const uint8_t* chunk = static_cast<const uint8_t*>(send[r]) + (uint64_t)c * m * s;
-        SPCCL_TRY(spccl_compress(chunk, m, dtype, L.slot(0, r, P), L.slot_bytes, L.ws, L.ws_bytes, st));
+        SPCCL_TRY(compress_fmt(sfmt, chunk, m, dtype, L, L.slot(0, r, P), st));
     }
     SPCCL_TRY(read_headers(L, 0, P, h, st));
     for (int r = 0; r < P; r++) {
         const uint64_t nnz = h[r].nnz;
         sig0[r] = sigp[r] = sparsity(m, nnz);
-        fmt[r] = SPCCL_FMT_PICI;
+        fmt[r] = sfmt;
         if (send_dense(pol, sig0[r], link_tau(pol, r, P))) {
             const int c = (r - 1 + P) % P;
             const uint8_t* chunk = static_cast<const uint8_t*>(send[r]) + (uint64_t)c * m * s;
             SPCCL_TRY(spccl_encode_dense(chunk, m, dtype, L.slot(0, r, P), L.slot_bytes, st));
             fmt[r] = SPCCL_FMT_DENSE;
         }
-        const uint64_t bytes = fmt[r] == SPCCL_FMT_PICI ? h[r].total_bytes : dense_msg_bytes(m, dtype);
+        const uint64_t bytes = fmt[r] == sfmt ? h[r].total_bytes : dense_msg_bytes(m, dtype);
         put_trace(trace, r, 0, r, fmt[r], 1, bytes, nnz, sigp[r]);
     }
     for (int step = 1; step <= P - 1; step++) {
@@ -154,18 +176,18 @@ spccl_status_t ring_rs(void* const* send, void* const* out, int P, uint64_t n, i
                 put_trace(trace, step * P + r, step, r, SPCCL_FMT_DENSE, 0, dense_msg_bytes(m, dtype),
                           SPCCL_NNZ_UNKNOWN, est);
             } else {
-                SPCCL_TRY(spccl_reduce(in, arr(own, m * s), msg(L.slot(0, r, P), SPCCL_FMT_PICI, L.slot_bytes), m,
-                                       dtype, L.ws, L.ws_bytes, st));
-                fmt[r] = SPCCL_FMT_PICI;
+                SPCCL_TRY(spccl_reduce(in, arr(own, m * s), msg(L.slot(0, r, P), sfmt, L.slot_bytes), m, dtype,
+                                       L.ws, L.ws_bytes, st));
+                fmt[r] = sfmt;
                 any_measured = true;
             }
         }
         if (any_measured) {
             SPCCL_TRY(read_headers(L, 0, P, h, st));
             for (int r = 0; r < P; r++) {
-                if (fmt[r] != SPCCL_FMT_PICI) continue;
+                if (fmt[r] != sfmt) continue;
                 sigp[r] = sparsity(m, h[r].nnz);
-                put_trace(trace, step * P + r, step, r, SPCCL_FMT_PICI, 1, h[r].total_bytes, h[r].nnz, sigp[r]);
+                put_trace(trace, step * P + r, step, r, sfmt, 1, h[r].total_bytes, h[r].nnz, sigp[r]);
             }
         }
     }
@@ -235,7 +257,8 @@ spccl_status_t spccl_vr_reduce_scatter(void* const* send, void* const* recv, int
     if (P < 1 || n % (uint64_t)P) return SPCCL_ERR_INVALID_ARG;
     const uint64_t m = n / (uint64_t)P;
     SPCCL_TRY(check_common(send, recv, P, dtype, scratch, scratch_bytes, m));
-    const spccl_policy_t pol = policy ? *policy : spccl_policy_t{0.6, 0.5, 0.1, 0, 1};
+    const spccl_policy_t pol = policy ? *policy : kDefaultPolicy;
+    if (!policy_ok(pol)) return SPCCL_ERR_INVALID_ARG;
     hipStream_t st = as_stream(stream);
     const Layout L = carve(scratch, P, m, dtype);
     SPCCL_TRY(spccl_workspace_init(L.ws, L.ws_bytes, stream));
@@ -245,17 +268,19 @@ spccl_status_t spccl_vr_reduce_scatter(void* const* send, void* const* recv, int
 }
 
 spccl_status_t spccl_vr_all_gather(void* const* send, void* const* recv, int32_t P, uint64_t n, int32_t dtype,
-                                   void* scratch, uint64_t scratch_bytes, spccl_trace_t* trace, void* stream) {
+                                   const spccl_policy_t* policy, void* scratch, uint64_t scratch_bytes,
+                                   spccl_trace_t* trace, void* stream) {
     SPCCL_TRY(check_common(send, recv, P, dtype, scratch, scratch_bytes, n));
+    const spccl_policy_t pol = policy ? *policy : kDefaultPolicy;
+    if (!policy_ok(pol)) return SPCCL_ERR_INVALID_ARG;
     hipStream_t st = as_stream(stream);
     const Layout L = carve(scratch, P, n, dtype);
     SPCCL_TRY(spccl_workspace_init(L.ws, L.ws_bytes, stream));
-    for (int q = 0; q < P; q++)
-        SPCCL_TRY(spccl_compress(send[q], n, dtype, L.slot(0, q, P), L.slot_bytes, L.ws, L.ws_bytes, stream));
+    for (int q = 0; q < P; q++) SPCCL_TRY(compress_fmt(pol.sparse_fmt, send[q], n, dtype, L, L.slot(0, q, P), st));
     std::vector<spccl_header_t> h;
     SPCCL_TRY(read_headers(L, 0, P, h, st));
     for (int q = 0; q < P; q++)
-        put_trace(trace, q, 0, q, SPCCL_FMT_PICI, 1, h[q].total_bytes, h[q].nnz, sparsity(n, h[q].nnz));
+        put_trace(trace, q, 0, q, pol.sparse_fmt, 1, h[q].total_bytes, h[q].nnz, sparsity(n, h[q].nnz));
     SPCCL_TRY(ring_ag_forward(send, recv, P, n, dtype, L, st));
     return finish(L, st);
 }
@@ -271,7 +296,8 @@ spccl_status_t spccl_vr_all_reduce(void* const* send, void* const* recv, int32_t
             const uintptr_t a = reinterpret_cast<uintptr_t>(recv[r]), b = reinterpret_cast<uintptr_t>(send[q]);
             if (n && a < b + n * s && b < a + n * s) return SPCCL_ERR_INVALID_ARG;
         }
-    const spccl_policy_t pol = policy ? *policy : spccl_policy_t{0.6, 0.5, 0.1, 0, 1};
+    const spccl_policy_t pol = policy ? *policy : kDefaultPolicy;
+    if (!policy_ok(pol)) return SPCCL_ERR_INVALID_ARG;
     hipStream_t st = as_stream(stream);
     const Layout L = carve(scratch, P, m, dtype);
     SPCCL_TRY(spccl_workspace_init(L.ws, L.ws_bytes, stream));
@@ -286,17 +312,17 @@ spccl_status_t spccl_vr_all_reduce(void* const* send, void* const* recv, int32_t
     for (int r = 0; r < P; r++) {
         est[r] = sigp[r] * sig0[r];
         const bool dense = pol.adaptive == 2 ? true : (pol.adaptive == 0 ? false : est[r] <= pol.ag_thresh);
-        fmt[r] = dense ? SPCCL_FMT_DENSE : SPCCL_FMT_PICI;
+        fmt[r] = dense ? SPCCL_FMT_DENSE : pol.sparse_fmt;
         if (dense) SPCCL_TRY(spccl_encode_dense(chunk_out[r], m, dtype, L.slot(0, r, P), L.slot_bytes, stream));
-        else SPCCL_TRY(spccl_compress(chunk_out[r], m, dtype, L.slot(0, r, P), L.slot_bytes, L.ws, L.ws_bytes, stream));
+        else SPCCL_TRY(compress_fmt(pol.sparse_fmt, chunk_out[r], m, dtype, L, L.slot(0, r, P), st));
     }
     std::vector<spccl_header_t> h;
     SPCCL_TRY(read_headers(L, 0, P, h, st));
     spccl_trace_t* ag_tr = trace ? trace + (uint64_t)P * (uint64_t)(P - 1) : nullptr;
     for (int r = 0; r < P; r++) {
-        const bool pici = fmt[r] == SPCCL_FMT_PICI;
-        put_trace(ag_tr, r, P - 1, r, fmt[r], pici ? 1 : 0, h[r].total_bytes, pici ? h[r].nnz : SPCCL_NNZ_UNKNOWN,
-                  est[r]);
+        const bool sparse = fmt[r] != SPCCL_FMT_DENSE;
+        put_trace(ag_tr, r, P - 1, r, fmt[r], sparse ? 1 : 0, h[r].total_bytes,
+                  sparse ? h[r].nnz : SPCCL_NNZ_UNKNOWN, est[r]);
     }
     SPCCL_TRY(ring_ag_forward(chunk_out.data(), recv, P, m, dtype, L, st));
     return finish(L, st);
