@@ -380,6 +380,122 @@ __device__ __forceinline__ uint32_t bits_below_lane(uint64_t w) {
     return __builtin_amdgcn_mbcnt_hi((uint32_t)(w >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)w, 0u));
 }
 
+// Entries [lo, lo + m) of J and V (m <= kCooChunk) into registers with
+// every load in flight at once -- index x, its predecessor y (0 for the
+// first) -- and the values into the stage.  With check, every index must
+// lie in [first, limit) and the indices must increase strictly; returns
+// false (the same in every lane) otherwise.
+template <class E>
+__device__ __forceinline__ bool coo_load(const uint32_t* J, const typename E::raw* V, uint32_t lo, uint32_t m,
+                                         bool check, uint64_t first, uint64_t limit, typename E::raw* stage,
+                                         uint32_t (&x)[kCooSlots], uint32_t (&y)[kCooSlots]) {
+    using raw = typename E::raw;
+    const uint32_t l = lane_id();
+    raw val[kCooSlots];
+#pragma unroll
+    for (int q = 0; q < kCooSlots; q++) {
+        const uint32_t i = l + 64 * q;
+        x[q] = i < m ? J[lo + i] : 0u;
+        y[q] = (i > 0 && i < m) ? J[lo + i - 1] : 0u;
+        val[q] = i < m ? V[lo + i] : (raw)0;
+    }
+    bool bad = false;
+#pragma unroll
+    for (int q = 0; q < kCooSlots; q++) {
+        const uint32_t i = l + 64 * q;
+        if (i < m) {
+            stage[i] = val[q];
+            bad = bad || (check && (x[q] < first || x[q] >= limit || (i > 0 && x[q] <= y[q])));
+        }
+    }
+    return !__any(bad);
+}
+
+// Adds the loaded entries that fall in tile t (positions i < m of the
+// stage; indices checked) into v: each such lane sets bit c of row word r
+// and, for the first entry of a row among the loaded ones, records the row's
+// stage position; then lane c reads row r's value at rf[r] + (set bits of
+// rw[r] below c).  (An all-zero v takes the entries exactly: zero is the
+// identity of the reduction.)
+template <class E>
+__device__ __forceinline__ void coo_apply(const uint32_t (&x)[kCooSlots], const uint32_t (&y)[kCooSlots],
+                                          uint32_t m, uint64_t t, const typename E::raw* stage, CooLds* cl,
+                                          uint32_t (&v)[64]) {
+    const uint32_t l = lane_id();
+    const uint64_t t0 = t * kTileElems;
+    cl->rw[l] = 0ull;
+    wave_lds_sync();
+#pragma unroll
+    for (int q = 0; q < kCooSlots; q++) {
+        const uint32_t i = l + 64 * q;
+        if (i < m && x[q] >= t0 && x[q] < t0 + kTileElems) {
+            const uint32_t loc = (uint32_t)(x[q] - t0), r = loc >> 6;
+            atomicOr((unsigned long long*)&cl->rw[r], 1ull << (loc & 63u));
+            if (i == 0 || (y[q] >> 6) != (x[q] >> 6)) cl->rf[r] = i;
+        }
+    }
+    wave_lds_sync();
+    const uint64_t myrw = cl->rw[l];
+    const uint32_t myrf = cl->rf[l];
+    wave_lds_sync();
+#pragma unroll
+    for (int r = 0; r < 64; r++) {
+        const uint64_t w = ((uint64_t)lane_bcast((uint32_t)(myrw >> 32), r) << 32) | lane_bcast((uint32_t)myrw, r);
+        if (w != 0ull) {
+            if ((w >> l) & 1ull) v[r] = oplus(E{}, v[r], (uint32_t)stage[lane_bcast(myrf, r) + bits_below_lane(w)]);
+        }
+    }
+    wave_lds_sync();
+}
+
+// Entries [lo, hi) of J checked: every index in [first, limit), strictly
+// increasing.  Uniform.
+__device__ bool coo_span_ok(const uint32_t* J, uint32_t lo, uint32_t hi, uint64_t first, uint64_t limit) {
+    const uint32_t l = lane_id();
+    bool bad = hi < lo;
+    if (!__any(bad)) {
+        for (uint32_t i0 = 0; i0 < hi - lo; i0 += kCooChunk) {
+            uint32_t x[kCooSlots], y[kCooSlots];
+#pragma unroll
+            for (int q = 0; q < kCooSlots; q++) {
+                const uint32_t i = i0 + l + 64 * q;
+                x[q] = i < hi - lo ? J[lo + i] : 0u;
+                y[q] = (i > 0 && i < hi - lo) ? J[lo + i - 1] : 0u;
+            }
+#pragma unroll
+            for (int q = 0; q < kCooSlots; q++) {
+                const uint32_t i = i0 + l + 64 * q;
+                if (i < hi - lo) bad = bad || x[q] < first || x[q] >= limit || (i > 0 && x[q] <= y[q]);
+            }
+        }
+    }
+    return !__any(bad);
+}
+
+// Entries [lo, lo + m) (m <= kCooChunk) of J and V into registers, every
+// load in flight at once; with check, verified as coo_span_ok does.
+template <class E>
+__device__ __forceinline__ bool coo_load_pairs(const uint32_t* J, const typename E::raw* V, uint32_t lo, uint32_t m,
+                                               bool check, uint64_t first, uint64_t limit,
+                                               uint32_t (&x)[kCooSlots], typename E::raw (&val)[kCooSlots]) {
+    const uint32_t l = lane_id();
+    uint32_t y[kCooSlots];
+#pragma unroll
+    for (int q = 0; q < kCooSlots; q++) {
+        const uint32_t i = l + 64 * q;
+        x[q] = i < m ? J[lo + i] : 0u;
+        y[q] = (check && i > 0 && i < m) ? J[lo + i - 1] : 0u;
+        val[q] = i < m ? V[lo + i] : (typename E::raw)0;
+    }
+    bool bad = false;
+#pragma unroll
+    for (int q = 0; q < kCooSlots; q++) {
+        const uint32_t i = l + 64 * q;
+        if (check && i < m) bad = bad || x[q] < first || x[q] >= limit || (i > 0 && x[q] <= y[q]);
+    }
+    return !__any(bad);
+}
+
 // Entries [lo, hi) of a checked COO message, claimed by tile t, checked:
 // every index inside the tile and below n, strictly increasing.  Uniform.
 __device__ bool coo_range_ok(const uint32_t* J, uint32_t lo, uint32_t hi, uint64_t t, uint64_t n) {
@@ -405,81 +521,38 @@ __device__ bool coo_range_ok(const uint32_t* J, uint32_t lo, uint32_t hi, uint64
     return !__any(bad);
 }
 
-// Adds tile t's COO entries [lo, hi) (already checked) into v (First: v =
-// the entries, zero elsewhere).  kCooChunk entries at a time: each lane takes
-// entries l, l+64, ..., stages their values in LDS, sets bit c of row word r
-// and, for the first entry of a row in the chunk, records the row's stage
-// position; then lane c reads row r's value at rf[r] + (set bits of rw[r]
-// below c).
-template <class E, bool First>
-__device__ void coo_expand_tile(const uint32_t* J, const typename E::raw* V, uint32_t lo, uint32_t hi, uint64_t t,
-                                typename E::raw* stage, CooLds* cl, uint32_t (&v)[64]) {
-    using raw = typename E::raw;
-    const uint32_t l = lane_id();
-    const uint64_t t0 = t * kTileElems;
-    if (First) {
-#pragma unroll
-        for (int r = 0; r < 64; r++) v[r] = 0;
-    }
-    const uint32_t cnt = hi - lo;
-#pragma unroll 1
-    for (uint32_t i0 = 0; i0 < cnt; i0 += kCooChunk) {
-        const uint32_t m = cnt - i0 < kCooChunk ? cnt - i0 : kCooChunk;
-        uint32_t x[kCooSlots], y[kCooSlots];
-        raw val[kCooSlots];
-#pragma unroll
-        for (int q = 0; q < kCooSlots; q++) {
-            const uint32_t i = l + 64 * q;
-            x[q] = i < m ? J[lo + i0 + i] : 0u;
-            y[q] = (i > 0 && i < m) ? J[lo + i0 + i - 1] : 0u;
-            val[q] = i < m ? V[lo + i0 + i] : (raw)0;
-        }
-        cl->rw[l] = 0ull;
-        wave_lds_sync();
-#pragma unroll
-        for (int q = 0; q < kCooSlots; q++) {
-            const uint32_t i = l + 64 * q;
-            if (i < m) {
-                const uint32_t loc = (uint32_t)(x[q] - t0), r = loc >> 6;
-                stage[i] = val[q];
-                atomicOr((unsigned long long*)&cl->rw[r], 1ull << (loc & 63u));
-                if (i == 0 || (y[q] >> 6) != (x[q] >> 6)) cl->rf[r] = i;
-            }
-        }
-        wave_lds_sync();
-        const uint64_t myrw = cl->rw[l];
-        const uint32_t myrf = cl->rf[l];
-        wave_lds_sync();
-#pragma unroll
-        for (int r = 0; r < 64; r++) {
-            const uint64_t w = ((uint64_t)lane_bcast((uint32_t)(myrw >> 32), r) << 32) | lane_bcast((uint32_t)myrw, r);
-            if (w != 0ull) {
-                if ((w >> l) & 1ull) {
-                    const uint32_t xv = stage[lane_bcast(myrf, r) + bits_below_lane(w)];
-                    v[r] = First ? xv : oplus(E{}, v[r], xv);
-                }
-            }
-        }
-        wave_lds_sync();
-    }
-}
-
-// Tile t of a checked COO message (nnz entries) into v: its entry range is
-// searched for, checked, and expanded; a tile that fails the checks is
-// flagged and reads as empty.
-template <class E, bool First>
+// Tile t of a checked COO message (nnz entries) added into v.  Its entry
+// range is searched for; a range that fits one chunk is checked as it is
+// loaded, a larger one is checked in a pass of its own before any entry is
+// used; then the entries are applied a chunk at a time (a row split
+// between chunks gets its columns from both).  A tile that fails the checks
+// is flagged and adds nothing.
+template <class E>
 __device__ void coo_tile(const uint8_t* msg, uint64_t nnz, uint64_t t, uint64_t n, typename E::raw* stage,
                          CooLds* cl, WsCtrl* ctrl, uint32_t (&v)[64]) {
     using raw = typename E::raw;
     const uint32_t* J = reinterpret_cast<const uint32_t*>(msg + kHeaderBytes);
     const raw* V = reinterpret_cast<const raw*>(msg + coo_off_V(nnz));
     const uint64_t T = num_tiles(n);
+    const uint64_t t0 = t * kTileElems, tlim = t0 + kTileElems < n ? t0 + kTileElems : n;
     const uint64_t key = (lane_id() < 32 ? t : t + 1) * kTileElems;
     const uint32_t b = coo_lower_bound<2>(J, 0u, (uint32_t)nnz, key);
     const uint32_t lo = lane_bcast(b, 0), hi = lane_bcast(b, 32);
-    const bool ok = (t + 1 < T || hi == nnz) && coo_range_ok(J, lo, hi, t, n);
+    bool ok = hi >= lo && hi - lo <= kTileElems && (t + 1 < T || hi == nnz);
+    const bool one = ok && hi - lo <= kCooChunk;
+    if (ok && !one) ok = coo_range_ok(J, lo, hi, t, n);
+    const uint32_t cnt = ok ? hi - lo : 0u;
+    uint32_t x[kCooSlots], y[kCooSlots];
+#pragma unroll 1
+    for (uint32_t i0 = 0; i0 < cnt; i0 += kCooChunk) {
+        const uint32_t m = cnt - i0 < kCooChunk ? cnt - i0 : kCooChunk;
+        if (!coo_load<E>(J, V, lo + i0, m, one, t0, tlim, stage, x, y)) {
+            ok = false;                    // only a single-chunk range is checked here: nothing applied yet
+            break;
+        }
+        coo_apply<E>(x, y, m, t, stage, cl, v);
+    }
     if (!ok && lane_id() == 0) set_status(ctrl, SPCCL_ERR_CORRUPT_STREAM);
-    coo_expand_tile<E, First>(J, V, lo, ok ? hi : lo, t, stage, cl, v);
 }
 
 // Tile t of a (+) b into v[64] (sources: dense rows or Pici tiles; b may be
@@ -531,12 +604,22 @@ __device__ __forceinline__ bool load_tile_pair(const DevOperand& a, const DevOpe
         constexpr bool a_sparse = SA == SRC_PICI || SA == SRC_COO;
         if constexpr (SA == SRC_PICI)
             expand_pici<E, !dense_first>(pici_columns(ma, nnza, t, n, ctrl), a.data, n, stage, v);
-        if constexpr (SA == SRC_COO)
-            coo_tile<E, !dense_first>(a.data, nnza, t, n, stage, cl, ctrl, v);
+        if constexpr (SA == SRC_COO) {
+            if (!dense_first) {
+#pragma unroll
+                for (int r = 0; r < 64; r++) v[r] = 0;
+            }
+            coo_tile<E>(a.data, nnza, t, n, stage, cl, ctrl, v);
+        }
         if constexpr (SB == SRC_PICI)
             expand_pici<E, !dense_first && !a_sparse>(pici_columns(mb, nnzb, t, n, ctrl), b.data, n, stage, v);
-        if constexpr (SB == SRC_COO)
-            coo_tile<E, !dense_first && !a_sparse>(b.data, nnzb, t, n, stage, cl, ctrl, v);
+        if constexpr (SB == SRC_COO) {
+            if (!dense_first && !a_sparse) {
+#pragma unroll
+                for (int r = 0; r < 64; r++) v[r] = 0;
+            }
+            coo_tile<E>(b.data, nnzb, t, n, stage, cl, ctrl, v);
+        }
     }
     return true;
 }
@@ -1288,7 +1371,12 @@ __global__ void __launch_bounds__(kBlockThreads) k_to_coo(PiciSinkArgs g) {
 // sums a contiguous run of partitions, the block scans the run totals), the
 // header and the pad between J and V.  A partition that did not publish
 // (an input failed its header check) stops the call: nothing is written.
+// The words are read with device-scope loads (they were published by
+// device-scope stores from every XCD; this block's own XCD may still cache
+// the lines it wrote in an earlier call), kTotalRun at a time with every
+// load in flight.
 constexpr uint32_t kTotalThreads = 1024;
+constexpr uint32_t kTotalRun = 8;
 
 template <class E>
 __global__ void __launch_bounds__(kTotalThreads) k_coo_total(PiciSinkArgs g) {
@@ -1302,10 +1390,18 @@ __global__ void __launch_bounds__(kTotalThreads) k_coo_total(PiciSinkArgs g) {
     __syncthreads();
     uint32_t run = 0;
     bool bad = false;
-    for (uint32_t q = p0; q < p1; q++) {
-        const uint64_t f = __hip_atomic_load(&g.flags[q], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        bad = bad || (uint32_t)(f >> 34) != epoch30 || (uint32_t)f > kPartElems;
-        run += (uint32_t)f;
+    for (uint32_t q0 = p0; q0 < p1; q0 += kTotalRun) {
+        uint64_t f[kTotalRun];
+#pragma unroll
+        for (uint32_t u = 0; u < kTotalRun; u++)
+            f[u] = q0 + u < p1 ? __hip_atomic_load(&g.flags[q0 + u], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0ull;
+#pragma unroll
+        for (uint32_t u = 0; u < kTotalRun; u++) {
+            if (q0 + u < p1) {
+                bad = bad || (uint32_t)(f[u] >> 34) != epoch30 || (uint32_t)f[u] > kPartElems;
+                run += (uint32_t)f[u];
+            }
+        }
     }
     if (bad) s_bad = 1;
     const uint32_t incl = wave_incl_scan(run);
@@ -1322,10 +1418,18 @@ __global__ void __launch_bounds__(kTotalThreads) k_coo_total(PiciSinkArgs g) {
         total += x;
     }
     uint32_t excl = wbase + incl - run;
-    for (uint32_t q = p0; q < p1; q++) {
-        const uint64_t f = g.flags[q];
-        publish(g.flags, q, epoch30, kFlagPrefix, excl);
-        excl += (uint32_t)f;
+    for (uint32_t q0 = p0; q0 < p1; q0 += kTotalRun) {
+        uint64_t f[kTotalRun];
+#pragma unroll
+        for (uint32_t u = 0; u < kTotalRun; u++)
+            f[u] = q0 + u < p1 ? __hip_atomic_load(&g.flags[q0 + u], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0ull;
+#pragma unroll
+        for (uint32_t u = 0; u < kTotalRun; u++) {
+            if (q0 + u < p1) {
+                publish(g.flags, q0 + u, epoch30, kFlagPrefix, excl);
+                excl += (uint32_t)f[u];
+            }
+        }
     }
     const uint64_t nnz = total, oV = coo_off_V(nnz);
     if (tid == 0) write_header(g.out, kFmtCoo, E::dtype, g.n, nnz, kHeaderBytes, oV, coo_bytes(E::dtype, nnz));
@@ -1342,8 +1446,9 @@ __global__ void __launch_bounds__(kBlockThreads) k_place_coo(PiciSinkArgs g) {
     const uint32_t p = blockIdx.x * kWavesPerBlock + wave;
     if (p >= g.nparts) return;
     const uint32_t epoch30 = g.epoch & 0x3FFFFFFFu;
-    const uint64_t f = g.flags[p];
-    const uint64_t fn = p + 1 < g.nparts ? g.flags[p + 1] : 0ull;
+    const uint64_t f = __hip_atomic_load(&g.flags[p], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const uint64_t fn = p + 1 < g.nparts ? __hip_atomic_load(&g.flags[p + 1], __ATOMIC_RELAXED,
+                                                             __HIP_MEMORY_SCOPE_AGENT) : 0ull;
     const HeaderWords hw = load_header_words(g.out);
     const uint64_t nnz = hw.w[2];
     if ((uint32_t)hw.w[0] != kMagic || (uint32_t)(f >> 34) != epoch30 || ((uint32_t)(f >> 32) & 3u) != kFlagPrefix)
@@ -1410,7 +1515,8 @@ __global__ void __launch_bounds__(kBlockThreads) k_to_dense(DenseSinkArgs g) {
 }
 
 // Expansion of P parts (all-gather receive side and decompress): the format
-// of each message is read from its header on the device.
+// of each message (dense, Pici or COO) is read from its header on the
+// device.
 //
 // Each wave expands K consecutive tiles of one part and issues its reads
 // before its first store: the K tiles' column words and offsets, then, in one
@@ -1477,49 +1583,49 @@ __device__ __forceinline__ void store_from_stage(typename E::raw* col, uint64_t 
 template <class E, int K>
 __device__ __forceinline__ void expand_tiles(const uint8_t* msg, const uint8_t* d, uint32_t fmt, uint64_t nnz,
                                              uint64_t n, uint64_t T, uint64_t t0, typename E::raw* out,
-                                             typename E::raw* stage, CooLds* cl, WsCtrl* ctrl) {
+                                             typename E::raw* stage, WsCtrl* ctrl) {
     using raw = typename E::raw;
     const uint32_t l = lane_id();
     const uint64_t g_n = n, g_T = T;
     if (fmt == (uint32_t)kFmtCoo) {
-        // the wave's entry range (searched over the whole index array, so
-        // neighbouring waves meet exactly), then its tiles' boundaries
-        // inside it; every tile's entries are checked before use
+        // The wave's entry range, searched over the whole index array (so
+        // neighbouring waves meet exactly).  Its entries are read (checked:
+        // inside the wave's tiles, below n, strictly increasing), the tiles
+        // are written with zeros, and after those stores have completed each
+        // lane stores its entries' values at their indices.  A range larger
+        // than one chunk is checked in a pass of its own first.
         const uint32_t* J = reinterpret_cast<const uint32_t*>(msg + kHeaderBytes);
         const raw* V = reinterpret_cast<const raw*>(msg + coo_off_V(nnz));
         const uint64_t tend = t0 + K < g_T ? t0 + K : g_T;
-        const uint32_t nt = (uint32_t)(tend - t0);
+        const uint64_t first = t0 * kTileElems, limit = tend * kTileElems < g_n ? tend * kTileElems : g_n;
         const uint32_t b = coo_lower_bound<2>(J, 0u, (uint32_t)nnz, (l < 32 ? t0 : tend) * kTileElems);
         const uint32_t lo = lane_bcast(b, 0), hi = lane_bcast(b, 32);
-        bool ok = hi >= lo && (tend < g_T || hi == nnz);
-        uint32_t bnd[K + 1];
-        bnd[0] = lo;
-#pragma unroll
-        for (int k = 1; k <= K; k++) bnd[k] = hi;
-        if (K > 1 && nt > 1 && ok) {
-            const uint32_t gi = l / 16;
-            const uint64_t key = (t0 + 1 + (gi < nt - 1 ? gi : nt - 2)) * kTileElems;
-            const uint32_t c = coo_lower_bound<4>(J, lo, hi, key);
-#pragma unroll
-            for (int k = 1; k < K; k++)
-                if ((uint32_t)k < nt) bnd[k] = lane_bcast(c, 16 * (k - 1));
-#pragma unroll
-            for (int k = 0; k < K; k++)
-                if ((uint32_t)k < nt) ok = ok && bnd[k + 1] >= bnd[k];
+        bool ok = hi >= lo && hi - lo <= (uint32_t)(tend - t0) * kTileElems && (tend < g_T || hi == nnz);
+        const bool one = ok && hi - lo <= kCooChunk;
+        if (ok && !one) ok = coo_span_ok(J, lo, hi, first, limit);
+        uint32_t cnt = ok ? hi - lo : 0u;
+        uint32_t x[kCooSlots];
+        raw val[kCooSlots];
+        if (cnt) ok = coo_load_pairs<E>(J, V, lo, cnt < kCooChunk ? cnt : kCooChunk, one, first, limit, x, val);
+        if (!ok) {
+            cnt = 0;
+            if (l == 0) set_status(ctrl, SPCCL_ERR_CORRUPT_STREAM);
         }
-        if (!ok && l == 0) set_status(ctrl, SPCCL_ERR_CORRUPT_STREAM);
+        for (uint64_t t = t0; t < tend; t++) {
+            raw* col = out + t * kTileElems + l;
+            const uint64_t rem = g_n - t * kTileElems;
+#pragma unroll 8
+            for (int r = 0; r < 64; r++)
+                if ((uint64_t)(64 * r + l) < rem) col[64 * r] = (raw)0;
+        }
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");      // the zeros are written before any value
 #pragma unroll 1
-        for (uint32_t k = 0; k < nt; k++) {
-            const uint64_t t = t0 + k;
-            uint32_t lo_k = bnd[0], hi_k = bnd[0];
+        for (uint32_t i0 = 0; i0 < cnt; i0 += kCooChunk) {
+            const uint32_t m = cnt - i0 < kCooChunk ? cnt - i0 : kCooChunk;
+            if (i0) coo_load_pairs<E>(J, V, lo + i0, m, false, 0, 0, x, val);
 #pragma unroll
-            for (int q = 0; q < K; q++)
-                if ((uint32_t)q == k) { lo_k = bnd[q]; hi_k = bnd[q + 1]; }
-            bool tok = ok && coo_range_ok(J, lo_k, hi_k, t, g_n);
-            if (ok && !tok && l == 0) set_status(ctrl, SPCCL_ERR_CORRUPT_STREAM);
-            uint32_t v[64];
-            coo_expand_tile<E, true>(J, V, lo_k, tok ? hi_k : lo_k, t, stage, cl, v);
-            store_tile<E>(reinterpret_cast<uint8_t*>(out), t, g_n, v);
+            for (int q = 0; q < kCooSlots; q++)
+                if (l + 64u * q < m) out[x[q]] = val[q];
         }
         return;
     }
@@ -1623,7 +1729,6 @@ template <class E, int K>
 __global__ void __launch_bounds__(kBlockThreads) k_gather(GatherArgs g) {
     using raw = typename E::raw;
     __shared__ raw stage_all[kWavesPerBlock][kChunkVals];
-    __shared__ CooLds coo_all[kWavesPerBlock];
     __shared__ uint32_t s_ok, s_fmt;
     __shared__ uint64_t s_nnz;
     const uint32_t wave = threadIdx.x >> 6;
@@ -1643,7 +1748,7 @@ __global__ void __launch_bounds__(kBlockThreads) k_gather(GatherArgs g) {
     if (t0 >= g.T) return;
     raw* out = reinterpret_cast<raw*>(g.out + (uint64_t)blockIdx.y * g.n * sizeof(raw));
     const uint8_t* d = op.hdr ? op.hdr + kHeaderBytes : op.data;
-    expand_tiles<E, K>(op.data, d, s_fmt, s_nnz, g.n, g.T, t0, out, stage_all[wave], &coo_all[wave], g.ctrl);
+    expand_tiles<E, K>(op.data, d, s_fmt, s_nnz, g.n, g.T, t0, out, stage_all[wave], g.ctrl);
 }
 
 // ---------------------------------------------------------------------------
@@ -1782,7 +1887,7 @@ __global__ void __launch_bounds__(kBlockThreads) k_expand_sliced(SlicedArgs g) {
         return;
     }
     expand_tiles<E, kTilesPerPart>(bm, bm + kHeaderBytes, h.fmt, h.nnz, ns, num_tiles(ns), 0,
-                                   reinterpret_cast<raw*>(g.out) + base, stage_all[wave], nullptr, g.ctrl);
+                                   reinterpret_cast<raw*>(g.out) + base, stage_all[wave], g.ctrl);
 }
 
 // The virtual-rank send of a sliced stream: each slot's header.total_bytes,
