@@ -370,6 +370,36 @@ def time_steps(R, steps, warmup, copies):
     return total_ms, wall, per, dense_eq, dom, timed[dom]
 
 
+def time_dense_ops(S, torch, n, reps=10):
+    """The dense ops of the ring's dense steps (for the threshold model):
+    dense (+) dense -> dense array, and wrapping an array as a dense message
+    (a plain copy), each priced by its algorithmic bytes."""
+    F = S.SPCCL_F32
+    x = torch.ones(n, dtype=torch.float32, device="cuda")
+    y = torch.ones(n, dtype=torch.float32, device="cuda")
+    z = torch.empty(n, dtype=torch.float32, device="cuda")
+    msg = torch.empty(S.spccl_stream_bound(n, F), dtype=torch.uint8, device="cuda")
+    ws = S.alloc_workspace(16, F)
+    ops = {"dense_dense": (lambda: S.spccl_reduce(S.operand(x), S.operand(y), S.operand(z), n, F, ws), 3 * n * 4),
+           "copy": (lambda: S.spccl_encode_dense(x, msg), 2 * n * 4 + 48)}
+    res = {}
+    for nm, (f, nbytes) in ops.items():
+        for _ in range(3):
+            f()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(reps):
+            f()
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / reps
+        res[nm] = {"ms": round(ms, 5), "algorithmic_bytes": nbytes, "achieved_GBs": round(nbytes / (ms / 1e3) / 1e9, 1)}
+    del x, y, z, msg
+    torch.cuda.empty_cache()
+    return res
+
+
 def copy_ceiling(torch, n, reps=20):
     """Achievable HBM rate on this device for reference: back-to-back plain
     device copies of n fp32 elements (n*4 bytes read and written each), so
@@ -517,12 +547,14 @@ def main():
         a_s = Rs.algorithmic_bytes()
         sweep[str(pm / 1000)] = {
             "dense_equiv_GBs": round(deq / (t_ms / 1e3) / 1e9, 1),
-            "kernels": {nm: {"ms": round(ms, 5), "frac_of_hbm_peak": round(a_s[nm] / (ms / 1e3) / 1e9 / HBM_PEAK_GBS,
-                                                                           4)} for nm, ms in p_s.items()},
+            "kernels": {nm: {"ms": round(ms, 5), "algorithmic_bytes": a_s[nm],
+                             "frac_of_hbm_peak": round(a_s[nm] / (ms / 1e3) / 1e9 / HBM_PEAK_GBS, 4)}
+                        for nm, ms in p_s.items()},
             "parity_compress": Rs.check_parity(),
         }
         del Rs
         torch.cuda.empty_cache()
+    dense_ops = time_dense_ops(S, torch, args.n)
     cpu = None
     if not args.no_cpu:
         _log("timing the CPU oracle")
@@ -536,10 +568,17 @@ def main():
                                "step = compress, send, decompress, 3 reduce variants, gather-expand, adaptive switch",
                    "n": args.n, "sigma": args.permille / 1000, "parallelism": "1 GPU (virtual ranks)"},
         "roofline": roof, "cpu_baseline": cpu, "copy_ceiling": ceiling, "kernels": kernels, "sliced": sliced,
-        "coo": coo, "sweep": sweep,
+        "coo": coo, "sweep": sweep, "dense_ops": dense_ops,
         "parity_compress_vs_oracle": parity, "wall_s_timed": round(wall, 3),
         "calibration_copy_bytes": calib,
     }
+    if sweep:
+        # thresholds for this machine from the modelled sweep (Sec. IV-C),
+        # with the kernel costs just measured
+        from paper_2607_04676_amd import tuner
+        rec = tuner.recommend(tuner.KernelModel.from_bench(out))
+        out["thresholds"] = {k: rec[k] for k in ("intra_thresh", "inter_thresh", "ag_thresh",
+                                                  "geomean_slowdown_vs_best", "paper_pair_geomean_slowdown")}
     print(json.dumps(out))
 
 

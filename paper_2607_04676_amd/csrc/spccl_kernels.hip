@@ -1148,6 +1148,127 @@ __global__ void __launch_bounds__(kBlockThreads) k_pp_to_pici(PiciSinkArgs g) {
     }
 }
 
+// Pici (+) Pici -> Pici, one tile per wave and one partition per block (the
+// partition's four tile counts meet in LDS, as in k_to_pici).  Each wave
+// reads its tile's column words and offsets from both messages, stages both
+// value ranges in its LDS buffer (one load round when together they fit
+// kChunkVals, else per column group), finds exact cancellations among the
+// rows both operands hold, and merges each column's two runs in row order
+// into the destination: its slot (two-pass mode) or its place once the
+// partition's offset is known by look-back (single pass).
+template <class E, bool Deferred>
+__global__ void __launch_bounds__(kBlockThreads) k_pp_tile(PiciSinkArgs g) {
+    using raw = typename E::raw;
+    __shared__ raw lds_in[kWavesPerBlock][kChunkVals];
+    __shared__ uint32_t s_cnt[kWavesPerBlock];
+    __shared__ uint32_t s_prefix;
+    const uint32_t wave = threadIdx.x >> 6, l = lane_id();
+    raw* in = lds_in[wave];
+    const uint32_t p = blockIdx.x;
+    const uint32_t epoch30 = g.epoch & 0x3FFFFFFFu;
+    const uint64_t t = (uint64_t)p * kTilesPerPart + wave;
+    const bool has_tile = t < g.T;
+    const uint64_t oI = off_I(g.n), oA = off_A(g.n);
+    const raw* Aa = reinterpret_cast<const raw*>(g.a.data + oA);
+    const raw* Ab = reinterpret_cast<const raw*>(g.b.data + oA);
+
+    // headers and this tile's column words / offsets first (the host
+    // guarantees both capacities cover the index arrays); headers checked
+    // while those are in flight
+    const HeaderWords hwa = load_header_words(g.a.hdr);
+    const HeaderWords hwb = load_header_words(g.b.hdr);
+    const PiciMeta ma = has_tile ? load_pici_meta<E>(g.a.data, t, g.n) : PiciMeta{0, 0, 0};
+    const PiciMeta mb = has_tile ? load_pici_meta<E>(g.b.data, t, g.n) : PiciMeta{0, 0, 0};
+    const HeaderView ha = check_header(hwa, g.a.cap, g.n, E::dtype, kFmtPici);
+    const HeaderView hb = check_header(hwb, g.b.cap, g.n, E::dtype, kFmtPici);
+    if (!(ha.ok && hb.ok)) {          // the same in every wave: no partition publishes
+        if (blockIdx.x == 0 && threadIdx.x == 0) set_status(g.ctrl, SPCCL_ERR_CORRUPT_STREAM);
+        return;
+    }
+    PiciCols ca{0, 0, 0, 0, true}, cb{0, 0, 0, 0, true};
+    uint64_t wo = 0;
+    uint32_t cpo = 0, tilecnt = 0, la = 0;
+    bool one = true;
+    if (has_tile) {
+        ca = pici_columns(ma, ha.nnz, t, g.n, g.ctrl);
+        cb = pici_columns(mb, hb.nnz, t, g.n, g.ctrl);
+        one = ca.cnt + cb.cnt <= kChunkVals;
+        uint64_t cancel = 0;
+        if (one) {
+            bool zero;
+            la = pp_stage<E>(ca, cb, Aa + ca.base, Ab + cb.base, 0, 64, in, zero);
+            cancel = pp_cancel<E>(ca.w, cb.w, in, ca.colpref, la + cb.colpref, zero, true);
+        } else {
+#pragma unroll 1
+            for (int h = 0; h < PPGroup::count; h++) {
+                const uint32_t c0 = PPGroup::cols * h, c1 = c0 + PPGroup::cols;
+                bool zg;
+                const uint32_t lg = pp_stage<E>(ca, cb, Aa + ca.base, Ab + cb.base, c0, c1, in, zg);
+                cancel |= pp_cancel<E>(ca.w, cb.w, in, ca.colpref - lane_bcast(ca.colpref, c0),
+                                       lg + cb.colpref - lane_bcast(cb.colpref, c0), zg, l >= c0 && l < c1);
+                wave_lds_sync();
+            }
+        }
+        wo = (ca.w | cb.w) & ~cancel;
+        reinterpret_cast<uint64_t*>(g.out + kHeaderBytes)[t * 64 + l] = wo;
+        const uint32_t c = (uint32_t)__popcll(wo);
+        cpo = wave_excl_scan(c);
+        tilecnt = lane_bcast(cpo + c, 63);
+    }
+    if (l == 0) s_cnt[wave] = tilecnt;
+    __syncthreads();
+    uint32_t tile_excl = 0, agg = 0;
+#pragma unroll
+    for (uint32_t k = 0; k < kWavesPerBlock; k++) {
+        const uint32_t ck = s_cnt[k];
+        tile_excl += k < wave ? ck : 0u;
+        agg += ck;
+    }
+    if (threadIdx.x == 0)
+        publish(g.flags, p, epoch30, (p == 0 && !Deferred) ? kFlagPrefix : kFlagAggregate, agg);
+    raw* dst;
+    uint32_t prefix = 0;
+    if constexpr (Deferred) {
+        dst = reinterpret_cast<raw*>(g.slots) + (uint64_t)p * kPartElems + tile_excl;
+    } else {
+        if (wave == 0) {
+            const uint32_t pre = p == 0 ? 0u : lookback(g.flags, p, epoch30, g.ctrl);
+            if (l == 0) {
+                if (p != 0) publish(g.flags, p, epoch30, kFlagPrefix, pre + agg);
+                s_prefix = pre;
+            }
+        }
+        __syncthreads();
+        prefix = s_prefix;
+        dst = reinterpret_cast<raw*>(g.out + oA) + prefix + tile_excl;
+    }
+    if (has_tile) {
+        if (one) {
+            pp_merge<E>(ca.w, cb.w, wo, in, ca.colpref, la + cb.colpref, dst, cpo, true);
+        } else {
+#pragma unroll 1
+            for (int h = 0; h < PPGroup::count; h++) {
+                const uint32_t c0 = PPGroup::cols * h, c1 = c0 + PPGroup::cols;
+                bool zg;
+                const uint32_t lg = pp_stage<E>(ca, cb, Aa + ca.base, Ab + cb.base, c0, c1, in, zg);
+                pp_merge<E>(ca.w, cb.w, wo, in, ca.colpref - lane_bcast(ca.colpref, c0),
+                            lg + cb.colpref - lane_bcast(cb.colpref, c0), dst, cpo, l >= c0 && l < c1);
+                wave_lds_sync();
+            }
+        }
+        if (l == 0) reinterpret_cast<uint32_t*>(g.out + oI)[t] = Deferred ? tile_excl : prefix + tile_excl;
+    }
+    if constexpr (!Deferred) {
+        if (p == g.nparts - 1 && threadIdx.x == 0) {
+            const uint64_t nnz = (uint64_t)prefix + agg;
+            uint32_t* I = reinterpret_cast<uint32_t*>(g.out + oI);
+            I[g.T] = (uint32_t)nnz;
+            for (uint64_t b = oI + 4 * (g.T + 1); b < oA; b += 4) *reinterpret_cast<uint32_t*>(g.out + b) = 0u;
+            write_header(g.out, kFmtPici, E::dtype, g.n, nnz, oI, oA, oA + nnz * sizeof(raw));
+        }
+    }
+}
+
 // Second pass of the two-pass Pici sink.  Every aggregate is final when this
 // kernel starts (the first pass has completed), so a block can add up its
 // predecessors' aggregates itself with ordinary cached loads -- no waiting on
@@ -2045,15 +2166,14 @@ template <class E>
 spccl_status_t launch_to_pici(int sa, int sb, const PiciSinkArgs& g, hipStream_t st) {
     dim3 grid(g.nparts), block(kBlockThreads);
     if (sa == SRC_PICI && sb == SRC_PICI) {
-        const dim3 wgrid((g.nparts + kWavesPerBlock - 1) / kWavesPerBlock);   // one wave per partition
         if (g.slots) {
-            hipLaunchKernelGGL((k_pp_to_pici<E, true>), wgrid, block, 0, st, g);
+            hipLaunchKernelGGL((k_pp_tile<E, true>), grid, block, 0, st, g);
             spccl_status_t st1 = launch_status();
             if (st1 != SPCCL_OK) return st1;
             dim3 pgrid((g.nparts + kPlacePer - 1) / kPlacePer);
             hipLaunchKernelGGL(k_place<E>, pgrid, block, 0, st, g);
         } else {
-            hipLaunchKernelGGL((k_pp_to_pici<E, false>), wgrid, block, 0, st, g);
+            hipLaunchKernelGGL((k_pp_tile<E, false>), grid, block, 0, st, g);
         }
         return launch_status();
     }
