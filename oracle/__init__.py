@@ -111,6 +111,9 @@ def lib():
         L.orc_decode_sliced.argtypes = [vp, u64, vp, u64, i32]
         L.orc_reduce_sliced.restype = i32
         L.orc_reduce_sliced.argtypes = [vp, vp, u64, i32, ctypes.c_double, vp, u64, u64, i32]
+        L.orc_ring_reduce_scatter_sliced.restype = i32
+        L.orc_ring_reduce_scatter_sliced.argtypes = [ctypes.POINTER(vp), ctypes.POINTER(vp), i32, u64, i32,
+                                                     ctypes.POINTER(_Policy), vp]
         L.orc_ring_all_reduce.restype = i32
         L.orc_ring_all_reduce.argtypes = [ctypes.POINTER(vp), ctypes.POINTER(vp), i32, u64, i32,
                                           ctypes.POINTER(_Policy), ctypes.POINTER(_Trace)]
@@ -445,3 +448,23 @@ def slot_messages(stream: np.ndarray, n: int, dtype: int) -> list:
         m = stream[q * slot:(q + 1) * slot]
         out.append(m[:int(m[40:48].view(np.uint64)[0])])
     return out
+
+
+def ring_reduce_scatter_sliced(sends: list, policy: Policy | None = None):
+    """Ring reduce-scatter over sliced streams with per-slice decisions.
+    Returns (recv list of n/P arrays, formats uint8[P-1, P, S]: the format of
+    every slice sent at every step by every rank)."""
+    policy = policy or Policy()
+    P = len(sends)
+    sends = [np.ascontiguousarray(s) for s in sends]
+    dt = dtype_code(sends[0])
+    n = sends[0].size
+    m = n // P
+    S = slice_count(m)
+    recvs = [np.empty(m, dtype=sends[0].dtype) for _ in range(P)]
+    fm = np.zeros(max(1, (P - 1) * P * S), dtype=np.uint8)
+    pol = policy.c()
+    _check(lib().orc_ring_reduce_scatter_sliced(_ptr_array(sends), _ptr_array(recvs), P, n, dt,
+                                                ctypes.byref(pol), _ptr(fm)), "ring_reduce_scatter_sliced")
+    return recvs, fm[:(P - 1) * P * S].reshape(max(P - 1, 0), P, S)
+

@@ -699,3 +699,81 @@ done:
     free(db); free(dr);
     return st;
 }
+
+/* ---- sliced ring reduce-scatter with per-slice decisions ---------------
+ * The paper decides formats inside NCCLX per slice (Sec. V-B) with the
+ * Sec. IV-C rule.  Reading: every slice q of the chunk a rank sends keeps its
+ * own sigma0 (measured when the slice is first compressed, at step 0) and
+ * its own tracked sparsity; at a later step the slice is sent dense iff
+ * sigma_prev * sigma0 <= tau(link) (Eq. 7; the estimate is then tracked),
+ * otherwise it is reduced and compressed and its measured sparsity is
+ * tracked.  Step 0 sends a slice dense iff its sigma0 <= tau(link).  The last
+ * receive reduces into the dense output.  Values are those of the plain ring
+ * (formats never change values).  fmt_out (optional) gets the format of
+ * every sent slice, indexed [(step * P + rank) * S + q], S = slices of a
+ * chunk. */
+int orc_ring_reduce_scatter_sliced(const void* const* send, void* const* recv, int P, uint64_t n, int dtype,
+                                   const orc_policy_t* pol, uint8_t* fmt_out) {
+    if (P < 1 || n % (uint64_t)P) return ORC_ERR_INVALID_ARG;
+    if (dtype != ORC_F32 && dtype != ORC_BF16) return ORC_ERR_UNSUPPORTED;
+    const uint64_t m = n / (uint64_t)P, s = elem_size(dtype);
+    const uint64_t S = orc_slice_count(m), slot = orc_slice_bytes(dtype), cap = S * slot;
+    int st = ORC_OK;
+    if (P == 1) { memcpy(recv[0], send[0], m * s); return ORC_OK; }
+    uint8_t** out_msg = (uint8_t**)calloc((size_t)P, sizeof(uint8_t*));
+    uint8_t** in_msg = (uint8_t**)calloc((size_t)P, sizeof(uint8_t*));
+    double* sig0 = (double*)calloc((size_t)(P * S + 1), sizeof(double));
+    double* sigp = (double*)calloc((size_t)(P * S + 1), sizeof(double));
+    uint8_t* acc = (uint8_t*)malloc(m * s + 1);
+    uint8_t* tmp = (uint8_t*)malloc(slot + 1);
+    if (!out_msg || !in_msg || !sig0 || !sigp || !acc || !tmp) { st = ORC_ERR_INVALID_ARG; goto done; }
+    for (int r = 0; r < P; r++) {
+        out_msg[r] = (uint8_t*)calloc(cap + 1, 1); in_msg[r] = (uint8_t*)calloc(cap + 1, 1);
+        if (!out_msg[r] || !in_msg[r]) { st = ORC_ERR_INVALID_ARG; goto done; }
+    }
+    for (int step = 0; step <= P - 1; step++) {
+        if (step > 0)   /* the sends of the previous step arrive: rank r gets rank r-1's stream */
+            for (int r = 0; r < P; r++) memcpy(in_msg[r], out_msg[(r - 1 + P) % P], cap);
+        for (int r = 0; r < P; r++) {
+            int c = (r - step - 1 + 2 * P) % P;
+            const uint8_t* own = (const uint8_t*)send[r] + (uint64_t)c * m * s;
+            if (step == 0) {
+                memcpy(acc, own, m * s);
+            } else {
+                st = orc_decode_sliced(in_msg[r], cap, acc, m, dtype); if (st) goto done;
+                for (uint64_t i = 0; i < m; i++)
+                    store_bits(acc, dtype, i, orc_oplus(load_bits(acc, dtype, i), load_bits(own, dtype, i), dtype));
+            }
+            if (step == P - 1) { memcpy(recv[r], acc, m * s); continue; }
+            const double tau = tau_link(pol, r, P);
+            for (uint64_t q = 0; q < S; q++) {
+                const uint64_t len = slice_len(m, q);
+                const uint8_t* src = acc + q * ORC_SLICE_ELEMS * s;
+                uint64_t nnz = 0;
+                for (uint64_t i = 0; i < len; i++) nnz += present(load_bits(src, dtype, i)) ? 1u : 0u;
+                const double meas = (double)(len - nnz) / (double)len;
+                double* s0 = &sig0[r * S + q]; double* sp = &sigp[r * S + q];
+                int dense;
+                if (step == 0) {
+                    *s0 = *sp = meas;
+                    dense = go_dense(pol, meas, tau);
+                } else {
+                    const double est = *sp * *s0;   /* Eq. 7 */
+                    dense = go_dense(pol, est, tau);
+                    *sp = dense ? est : meas;
+                }
+                uint8_t* dst = out_msg[r] + q * slot;
+                if (dense) st = orc_encode_dense(src, len, dtype, dst, slot);
+                else st = orc_compress(src, len, dtype, dst, slot, &nnz);
+                if (st) goto done;
+                if (fmt_out) fmt_out[((uint64_t)step * P + r) * S + q] = (uint8_t)(dense ? ORC_FMT_DENSE : ORC_FMT_PICI);
+            }
+        }
+    }
+done:
+    if (out_msg) for (int r = 0; r < P; r++) free(out_msg[r]);
+    if (in_msg) for (int r = 0; r < P; r++) free(in_msg[r]);
+    free(out_msg); free(in_msg); free(sig0); free(sigp); free(acc); free(tmp);
+    return st;
+}
+

@@ -101,3 +101,46 @@ def test_reduce_sliced_matches_numpy(n, thresh):
         part = want[q * S:(q + 1) * S].view(np.uint32)
         m, nnz = part.size, int(np.count_nonzero(part))
         assert O.header(msg)["format"] == (O.FMT_DENSE if (m - nnz) / m <= thresh else O.FMT_PICI)
+
+
+# ---- ring reduce-scatter over sliced streams, per-slice decisions --------------------------------
+
+@pytest.mark.parametrize("P", [1, 2, 3, 8])
+@pytest.mark.parametrize("adaptive", [0, 1, 2])
+def test_sliced_ring_values_equal_the_plain_ring(P, adaptive):
+    m = 2 * O.SLICE_ELEMS + 777
+    sends = [W.sparse_array(P * m, P * m // 8, [80, P, r], W.BF16) for r in range(P)]
+    got, fm = O.ring_reduce_scatter_sliced(sends, O.Policy(adaptive=adaptive))
+    exp, _ = O.ring_reduce_scatter(sends, O.Policy(adaptive=adaptive))
+    for r in range(P):
+        assert np.array_equal(got[r], exp[r])
+    if P > 1 and adaptive != 1:
+        assert (fm == (O.FMT_DENSE if adaptive == 2 else O.FMT_PICI)).all()
+
+
+def test_sliced_ring_decides_per_slice():
+    """Chunk = one full slice + one slice of 10,000 elements.  Slice 0: rank
+    j-th in the fold order holds the residue j-1 mod 100 (disjoint), so its
+    sparsity after k contributions is 1 - k/100 and never reaches 0.6.  Slice
+    1: the digit supports of the canonical pin (sparsity 0.9^k exactly), so
+    with tau = 0.6 it is sent as Pici at steps 0-3 and dense at steps 4-6
+    (0.59049 after extrapolation).  Each slice follows its own tracker."""
+    P, L0, L1 = 8, O.SLICE_ELEMS, 10000
+    m = L0 + L1
+    idx0, idx1 = np.arange(L0), np.arange(L1)
+    sends = []
+    for r in range(P):
+        x = np.zeros(P * m, dtype=np.float32)
+        for c in range(P):
+            j = (r - c) % P or P
+            base = c * m
+            x[base:base + L0][idx0 % 100 == (j - 1)] = 1.0
+            x[base + L0:base + m][(idx1 // 10 ** ((j - 1) % 4)) % 10 == 0] = 1.0
+        sends.append(x)
+    got, fm = O.ring_reduce_scatter_sliced(sends, O.Policy())
+    assert (fm[:, :, 0] == O.FMT_PICI).all()
+    for r in range(P):
+        assert fm[:, r, 1].tolist() == [1, 1, 1, 1, 0, 0, 0]
+    exp, _ = O.ring_reduce_scatter(sends, O.Policy(adaptive=0))
+    for r in range(P):
+        assert np.array_equal(got[r], exp[r])
