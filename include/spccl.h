@@ -254,6 +254,32 @@ spccl_status_t spccl_reduce_sliced(const void* a, const void* b, uint64_t b_byte
 spccl_status_t spccl_copy_sliced(const void* src, uint64_t src_bytes, void* dst, uint64_t dst_bytes, uint64_t n,
                                  int32_t dtype, void* ws, uint64_t ws_bytes, void* stream);
 
+/* Per-slice format tracking (Sec. IV-C applied per slice, as the paper's
+ * in-collective decisions are made per slice, Sec. V-B): a tracker holds,
+ * for each slice of an n-element array, sigma0 and the tracked sparsity
+ * sigma_prev as two doubles (16 bytes per slice, 8-byte aligned device
+ * memory, caller-owned).  The decisions are made on the device, so a ring
+ * of tracked calls needs no host synchronisation between steps. */
+uint64_t spccl_slice_tracker_bytes(uint64_t n);   /* 16 * spccl_slice_count(n) */
+
+/* First send of a ring: compress dense[0..n) into a sliced stream; each
+ * slice's measured sparsity becomes its sigma0 and sigma_prev, and the slice
+ * is dense iff that sparsity <= tau.  fmt_out (device, optional) gets one
+ * byte per slice: the format produced. */
+spccl_status_t spccl_compress_sliced_tracked(const void* dense, uint64_t n, int32_t dtype, double tau,
+                                             void* out, uint64_t out_bytes, double* tracker,
+                                             uint64_t tracker_bytes, uint8_t* fmt_out,
+                                             void* ws, uint64_t ws_bytes, void* stream);
+
+/* A later send: out = a (+) b (dense array, sliced stream) as a sliced
+ * stream; per slice, est = sigma_prev * sigma0 (Eq. 7): the slice is dense
+ * iff est <= tau (sigma_prev := est), otherwise Pici (sigma_prev := its
+ * measured sparsity).  No operand may overlap another. */
+spccl_status_t spccl_reduce_sliced_tracked(const void* a, const void* b, uint64_t b_bytes, void* out,
+                                           uint64_t out_bytes, double tau, double* tracker,
+                                           uint64_t tracker_bytes, uint8_t* fmt_out, uint64_t n,
+                                           int32_t dtype, void* ws, uint64_t ws_bytes, void* stream);
+
 /* ---- message transport and inspection ------------------------------------ */
 
 /* The virtual-rank "send": copy header.total_bytes bytes of the message at
@@ -335,6 +361,22 @@ spccl_status_t spccl_vr_all_reduce(void* const* send, void* const* recv, int32_t
                                    int32_t dtype, const spccl_policy_t* policy,
                                    void* scratch, uint64_t scratch_bytes,
                                    spccl_trace_t* trace, void* stream);
+
+/* Ring reduce-scatter over sliced streams with the decisions on the device
+ * (the paper's in-collective mode, Sec. V-B, with Sec. IV-C per slice):
+ * step 0 compresses with spccl_compress_sliced_tracked, later steps send
+ * through spccl_copy_sliced and reduce with spccl_reduce_sliced_tracked, the
+ * last receive reduces into recv[r] (n/P elements, the same values as
+ * spccl_vr_reduce_scatter).  tau per link as in spccl_policy_t (adaptive 0:
+ * never dense, 2: always); sparse_fmt must be SPCCL_FMT_PICI.  The stream is
+ * synchronised once, at the end.  fmt_trace (host, optional) gets the
+ * format of every slice sent: (P-1) * P * S bytes, index
+ * (step * P + rank) * S + slice, S = spccl_slice_count(n / P). */
+uint64_t spccl_vr_sliced_scratch_bytes(int32_t P, uint64_t msg_elems, int32_t dtype);
+spccl_status_t spccl_vr_reduce_scatter_sliced(void* const* send, void* const* recv, int32_t P, uint64_t n,
+                                              int32_t dtype, const spccl_policy_t* policy,
+                                              void* scratch, uint64_t scratch_bytes,
+                                              uint8_t* fmt_trace, void* stream);
 
 #ifdef __cplusplus
 }

@@ -40,7 +40,8 @@ EXPORTS = ("spccl_num_tiles", "spccl_pici_bytes", "spccl_stream_bound", "spccl_w
            "spccl_vr_reduce_scatter", "spccl_vr_all_gather", "spccl_vr_all_reduce",
            "spccl_slice_count", "spccl_slice_bytes", "spccl_compress_sliced", "spccl_decompress_sliced",
            "spccl_reduce_sliced", "spccl_copy_sliced", "spccl_coo_bytes", "spccl_message_bound",
-           "spccl_compress_coo")
+           "spccl_compress_coo", "spccl_slice_tracker_bytes", "spccl_compress_sliced_tracked",
+           "spccl_reduce_sliced_tracked", "spccl_vr_sliced_scratch_bytes", "spccl_vr_reduce_scatter_sliced")
 
 
 class spccl_operand_t(ctypes.Structure):
@@ -102,6 +103,14 @@ _sigs = {
     "spccl_decompress_sliced": (_i32, [_vp, _u64, _vp, _u64, _i32, _vp, _u64, _vp]),
     "spccl_reduce_sliced": (_i32, [_vp, _vp, _u64, _vp, _u64, _i32, ctypes.c_double, _u64, _i32, _vp, _u64, _vp]),
     "spccl_copy_sliced": (_i32, [_vp, _u64, _vp, _u64, _u64, _i32, _vp, _u64, _vp]),
+    "spccl_slice_tracker_bytes": (_u64, [_u64]),
+    "spccl_compress_sliced_tracked": (_i32, [_vp, _u64, _i32, ctypes.c_double, _vp, _u64, _vp, _u64, _vp, _vp,
+                                             _u64, _vp]),
+    "spccl_reduce_sliced_tracked": (_i32, [_vp, _vp, _u64, _vp, _u64, ctypes.c_double, _vp, _u64, _vp, _u64, _i32,
+                                           _vp, _u64, _vp]),
+    "spccl_vr_sliced_scratch_bytes": (_u64, [_i32, _u64, _i32]),
+    "spccl_vr_reduce_scatter_sliced": (_i32, [ctypes.POINTER(_vp), ctypes.POINTER(_vp), _i32, _u64, _i32,
+                                              ctypes.POINTER(spccl_policy_t), _vp, _u64, _vp, _vp]),
 }
 for _name, (_res, _args) in _sigs.items():
     _f = getattr(_lib, _name)
@@ -319,6 +328,48 @@ def spccl_copy_sliced(src: torch.Tensor, dst: torch.Tensor, n: int, dtype: int, 
                       stream=None) -> None:
     _check(_lib.spccl_copy_sliced(src.data_ptr(), _nbytes(src), dst.data_ptr(), _nbytes(dst), n, dtype,
                                   ws.data_ptr(), _nbytes(ws), _stream(stream)), "spccl_copy_sliced")
+
+
+def spccl_slice_tracker_bytes(n: int) -> int:
+    return _lib.spccl_slice_tracker_bytes(n)
+
+
+def _ptr_or_null(t) -> int | None:
+    return None if t is None else t.data_ptr()
+
+
+def spccl_compress_sliced_tracked(dense: torch.Tensor, out: torch.Tensor, tracker: torch.Tensor, ws: torch.Tensor,
+                                  tau: float, fmt_out: torch.Tensor | None = None, stream=None) -> None:
+    _check(_lib.spccl_compress_sliced_tracked(dense.data_ptr(), dense.numel(), _dt(dense), float(tau),
+                                              out.data_ptr(), _nbytes(out), tracker.data_ptr(), _nbytes(tracker),
+                                              _ptr_or_null(fmt_out), ws.data_ptr(), _nbytes(ws), _stream(stream)),
+           "spccl_compress_sliced_tracked")
+
+
+def spccl_reduce_sliced_tracked(a: torch.Tensor, b: torch.Tensor, out: torch.Tensor, tracker: torch.Tensor,
+                                ws: torch.Tensor, tau: float, fmt_out: torch.Tensor | None = None,
+                                stream=None) -> None:
+    _check(_lib.spccl_reduce_sliced_tracked(a.data_ptr(), b.data_ptr(), _nbytes(b), out.data_ptr(), _nbytes(out),
+                                            float(tau), tracker.data_ptr(), _nbytes(tracker), _ptr_or_null(fmt_out),
+                                            a.numel(), _dt(a), ws.data_ptr(), _nbytes(ws), _stream(stream)),
+           "spccl_reduce_sliced_tracked")
+
+
+def spccl_vr_sliced_scratch_bytes(P: int, msg_elems: int, dtype: int) -> int:
+    return _lib.spccl_vr_sliced_scratch_bytes(P, msg_elems, dtype)
+
+
+def spccl_vr_reduce_scatter_sliced(send: list, recv: list, scratch: torch.Tensor, policy=None, stream=None):
+    """Returns the per-slice formats sent, shape (P-1, P, S)."""
+    import numpy as np
+    P, n = len(send), send[0].numel()
+    S = spccl_slice_count(n // P)
+    fm = np.zeros(max(1, (P - 1) * P * S), dtype=np.uint8)
+    pol = _policy(policy)
+    _check(_lib.spccl_vr_reduce_scatter_sliced(_ptrs(send), _ptrs(recv), P, n, _dt(send[0]), ctypes.byref(pol),
+                                               scratch.data_ptr(), _nbytes(scratch), fm.ctypes.data,
+                                               _stream(stream)), "spccl_vr_reduce_scatter_sliced")
+    return fm[:(P - 1) * P * S].reshape(max(P - 1, 0), P, S)
 
 
 def alloc_sliced(n: int, dtype: int, device="cuda") -> torch.Tensor:

@@ -418,6 +418,51 @@ spccl_status_t spccl_reduce_sliced(const void* a, const void* b, uint64_t b_byte
     return launch_sliced_dt(dtype, g, out_sliced ? kSlicedReduceToSliced : kSlicedReduceToDense, as_stream(stream));
 }
 
+uint64_t spccl_slice_tracker_bytes(uint64_t n) { return 16ull * num_slices(n); }
+
+namespace {
+spccl_status_t check_tracker(const double* track, uint64_t track_bytes, uint64_t n) {
+    if (!track || (reinterpret_cast<uintptr_t>(track) & 7u)) return SPCCL_ERR_INVALID_ARG;
+    return track_bytes < 16ull * num_slices(n) ? SPCCL_ERR_CAPACITY : SPCCL_OK;
+}
+}  // namespace
+
+spccl_status_t spccl_compress_sliced_tracked(const void* dense, uint64_t n, int32_t dtype, double tau, void* out,
+                                             uint64_t out_bytes, double* tracker, uint64_t tracker_bytes,
+                                             uint8_t* fmt_out, void* ws, uint64_t ws_bytes, void* stream) {
+    spccl_status_t st = check_sliced_args(n, dtype, ws, ws_bytes);
+    if (st == SPCCL_OK) st = check_dense_arg(dense, n * elem_bytes(dtype), n, dtype);
+    if (st == SPCCL_OK) st = check_sliced_arg(out, out_bytes, n, dtype);
+    if (st == SPCCL_OK) st = check_tracker(tracker, tracker_bytes, n);
+    if (st != SPCCL_OK) return st;
+    if (overlaps(dense, n * elem_bytes(dtype), out, out_bytes) || overlaps(tracker, tracker_bytes, out, out_bytes))
+        return SPCCL_ERR_INVALID_ARG;
+    if (n == 0) return SPCCL_OK;
+    SlicedArgs g{static_cast<const uint8_t*>(dense), nullptr, static_cast<uint8_t*>(out), n, slice_slot_bytes(dtype),
+                 tau, static_cast<WsCtrl*>(ws), tracker, 0, fmt_out};
+    return launch_sliced_dt(dtype, g, kSlicedCompress, as_stream(stream));
+}
+
+spccl_status_t spccl_reduce_sliced_tracked(const void* a, const void* b, uint64_t b_bytes, void* out,
+                                           uint64_t out_bytes, double tau, double* tracker, uint64_t tracker_bytes,
+                                           uint8_t* fmt_out, uint64_t n, int32_t dtype, void* ws, uint64_t ws_bytes,
+                                           void* stream) {
+    spccl_status_t st = check_sliced_args(n, dtype, ws, ws_bytes);
+    if (st == SPCCL_OK) st = check_dense_arg(a, n * elem_bytes(dtype), n, dtype);
+    if (st == SPCCL_OK) st = check_sliced_arg(b, b_bytes, n, dtype);
+    if (st == SPCCL_OK) st = check_sliced_arg(out, out_bytes, n, dtype);
+    if (st == SPCCL_OK) st = check_tracker(tracker, tracker_bytes, n);
+    if (st != SPCCL_OK) return st;
+    const uint64_t ab = n * elem_bytes(dtype);
+    if (overlaps(b, b_bytes, out, out_bytes) || overlaps(a, ab, b, b_bytes) || overlaps(a, ab, out, out_bytes) ||
+        overlaps(tracker, tracker_bytes, out, out_bytes))
+        return SPCCL_ERR_INVALID_ARG;
+    if (n == 0) return SPCCL_OK;
+    SlicedArgs g{static_cast<const uint8_t*>(a), static_cast<const uint8_t*>(b), static_cast<uint8_t*>(out), n,
+                 slice_slot_bytes(dtype), tau, static_cast<WsCtrl*>(ws), tracker, 1, fmt_out};
+    return launch_sliced_dt(dtype, g, kSlicedReduceToSliced, as_stream(stream));
+}
+
 spccl_status_t spccl_copy_sliced(const void* src, uint64_t src_bytes, void* dst, uint64_t dst_bytes, uint64_t n,
                                  int32_t dtype, void* ws, uint64_t ws_bytes, void* stream) {
     spccl_status_t st = check_sliced_args(n, dtype, ws, ws_bytes);

@@ -112,8 +112,12 @@ struct SlicedArgs {
     uint8_t* out;          // sliced output stream, or dense output array
     uint64_t n;            // elements
     uint64_t slot;         // bytes per slot
-    double thresh;         // a produced slice is dense iff its sparsity <= thresh
+    double thresh;         // a produced slice is dense iff its sparsity <= thresh (tracked: iff the
+                           // tracker's estimate <= thresh)
     WsCtrl* ctrl;
+    double* track;         // per slice: sigma0, sigma_prev (nullptr: decide on the measured sparsity)
+    int32_t track_step;    // 0: the first send (sigma0 := measured); 1: a later one (Eq. 7 estimate)
+    uint8_t* fmt_out;      // per slice: the format produced (nullptr: not recorded)
 };
 
 }  // namespace spccl

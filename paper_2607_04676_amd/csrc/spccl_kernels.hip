@@ -1958,6 +1958,10 @@ __global__ void __launch_bounds__(kBlockThreads) k_sliced(SlicedArgs g) {
         const uint32_t c = (uint32_t)__popcll(w);
         const uint32_t colpref = wave_excl_scan(c);
         const uint32_t tilecnt = lane_bcast(colpref + c, 63);
+        // the slice's tracker (Sec. IV-C, per slice): read by every thread
+        // before the barrier, updated by one thread after it
+        double s0 = 0.0, sp = 0.0;
+        if (g.track && g.track_step) { s0 = g.track[2 * q]; sp = g.track[2 * q + 1]; }
         if (l == 0) s_cnt[wave] = tilecnt;
         __syncthreads();
         uint32_t tile_excl = 0, agg = 0;
@@ -1967,8 +1971,19 @@ __global__ void __launch_bounds__(kBlockThreads) k_sliced(SlicedArgs g) {
             tile_excl += k < wave ? ck : 0u;
             agg += ck;
         }
+        const double meas = (double)(ns - agg) / (double)ns;
+        bool dense;
+        if (g.track && g.track_step) {
+            const double est = sp * s0;                               // Eq. 7
+            dense = est <= g.thresh;
+            if (threadIdx.x == 0) g.track[2 * q + 1] = dense ? est : meas;
+        } else {
+            dense = meas <= g.thresh;
+            if (g.track && threadIdx.x == 0) { g.track[2 * q] = meas; g.track[2 * q + 1] = meas; }
+        }
+        if (g.fmt_out && threadIdx.x == 0) g.fmt_out[q] = (uint8_t)(dense ? kFmtDense : kFmtPici);
         uint8_t* om = g.out + q * g.slot;
-        if ((double)(ns - agg) / (double)ns <= g.thresh) {        // this slice goes dense
+        if (dense) {                                               // this slice goes dense
             if (has_tile) store_tile<E>(om + kHeaderBytes, t, ns, v);
             if (threadIdx.x == 0)
                 write_header(om, kFmtDense, E::dtype, ns, kNnzUnknown, 0, kHeaderBytes, dense_msg_bytes(ns, E::dtype));

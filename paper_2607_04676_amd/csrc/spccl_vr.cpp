@@ -328,4 +328,104 @@ spccl_status_t spccl_vr_all_reduce(void* const* send, void* const* recv, int32_t
     return finish(L, st);
 }
 
+/* ---- sliced ring reduce-scatter: decisions on the device -------------------- */
+
+namespace {
+struct SlicedLayout {
+    uint8_t* ws;           // control block
+    double* track;         // P trackers of S slices
+    uint8_t* fmt;          // (P-1) * P * S formats
+    uint8_t* streams;      // 2 * P sliced streams (sent, received)
+    uint64_t S, sbytes, track_bytes;
+    uint8_t* stream(int which, int r, int P) const { return streams + ((uint64_t)which * P + r) * sbytes; }
+};
+
+uint64_t sliced_need(int32_t P, uint64_t m, int32_t dtype, SlicedLayout* L, void* base) {
+    const uint64_t S = spccl_slice_count(m);
+    const uint64_t sbytes = round_up(S * spccl_slice_bytes(dtype));
+    const uint64_t wsb = round_up(kWsFlagsOffset), trb = round_up(16ull * S * (uint64_t)P),
+                   fmb = round_up((uint64_t)(P > 1 ? P - 1 : 1) * (uint64_t)P * S);
+    if (L) {
+        uint8_t* b = static_cast<uint8_t*>(base);
+        L->ws = b;
+        L->track = reinterpret_cast<double*>(b + wsb);
+        L->fmt = b + wsb + trb;
+        L->streams = b + wsb + trb + fmb;
+        L->S = S;
+        L->sbytes = sbytes;
+        L->track_bytes = 16ull * S;
+    }
+    return wsb + trb + fmb + 2ull * (uint64_t)P * sbytes;
+}
+
+// The policy as one threshold per link: adaptive 0 never goes dense (no
+// sparsity is below -1), adaptive 2 always does (none is above 2).
+double sliced_tau(const spccl_policy_t& pol, int r, int P) {
+    if (pol.adaptive == 0) return -1.0;
+    if (pol.adaptive == 2) return 2.0;
+    return link_tau(pol, r, P);
+}
+}  // namespace
+
+uint64_t spccl_vr_sliced_scratch_bytes(int32_t P, uint64_t msg_elems, int32_t dtype) {
+    if (P < 1 || (dtype != SPCCL_F32 && dtype != SPCCL_BF16)) return 0;
+    return sliced_need(P, msg_elems, dtype, nullptr, nullptr);
+}
+
+spccl_status_t spccl_vr_reduce_scatter_sliced(void* const* send, void* const* recv, int32_t P, uint64_t n,
+                                              int32_t dtype, const spccl_policy_t* policy, void* scratch,
+                                              uint64_t scratch_bytes, uint8_t* fmt_trace, void* stream) {
+    if (P < 1 || n % (uint64_t)P) return SPCCL_ERR_INVALID_ARG;
+    const uint64_t m = n / (uint64_t)P, s = elem_bytes(dtype);
+    if (dtype != SPCCL_F32 && dtype != SPCCL_BF16) return SPCCL_ERR_UNSUPPORTED;
+    if (m >= (1ull << 32)) return SPCCL_ERR_UNSUPPORTED;
+    if (!send || !recv || !scratch || (reinterpret_cast<uintptr_t>(scratch) & 15u)) return SPCCL_ERR_INVALID_ARG;
+    const uintptr_t amask = (uintptr_t)s - 1;
+    for (int r = 0; r < P; r++)
+        if (!send[r] || !recv[r] || (reinterpret_cast<uintptr_t>(send[r]) & amask) ||
+            (reinterpret_cast<uintptr_t>(recv[r]) & amask))
+            return SPCCL_ERR_INVALID_ARG;
+    const spccl_policy_t pol = policy ? *policy : kDefaultPolicy;
+    if (!policy_ok(pol)) return SPCCL_ERR_INVALID_ARG;
+    if (pol.sparse_fmt != SPCCL_FMT_PICI) return SPCCL_ERR_UNSUPPORTED;      // slices are Pici or dense
+    if (scratch_bytes < sliced_need(P, m, dtype, nullptr, nullptr)) return SPCCL_ERR_WORKSPACE;
+    hipStream_t st = as_stream(stream);
+    if (P == 1) {
+        if (m && hipMemcpyAsync(recv[0], send[0], m * s, hipMemcpyDeviceToDevice, st) != hipSuccess) return SPCCL_ERR_HIP;
+        return hipStreamSynchronize(st) == hipSuccess ? SPCCL_OK : SPCCL_ERR_HIP;
+    }
+    SlicedLayout L;
+    sliced_need(P, m, dtype, &L, scratch);
+    SPCCL_TRY(spccl_workspace_init(L.ws, kWsFlagsOffset, stream));
+    const uint64_t slen = L.S * spccl_slice_bytes(dtype);   // bytes of one sliced stream
+    auto chunk = [&](int r, int c) { return static_cast<const uint8_t*>(send[r]) + (uint64_t)c * m * s; };
+    auto fmt_at = [&](int step, int r) { return L.fmt + ((uint64_t)step * P + r) * L.S; };
+    // step 0: every rank compresses its first chunk and initialises the
+    // trackers of its slices; nothing returns to the host until the end
+    for (int r = 0; r < P; r++)
+        SPCCL_TRY(spccl_compress_sliced_tracked(chunk(r, (r - 1 + P) % P), m, dtype, sliced_tau(pol, r, P),
+                                                L.stream(0, r, P), slen, L.track + 2 * L.S * r, L.track_bytes,
+                                                fmt_at(0, r), L.ws, kWsFlagsOffset, st));
+    for (int step = 1; step <= P - 1; step++) {
+        for (int r = 0; r < P; r++)
+            SPCCL_TRY(spccl_copy_sliced(L.stream(0, (r - 1 + P) % P, P), slen, L.stream(1, r, P), slen, m, dtype,
+                                        L.ws, kWsFlagsOffset, st));
+        for (int r = 0; r < P; r++) {
+            const uint8_t* own = chunk(r, (r - step - 1 + 2 * P) % P);
+            if (step == P - 1)
+                SPCCL_TRY(spccl_reduce_sliced(own, L.stream(1, r, P), slen, recv[r], m * s, 0, 0.0, m, dtype, L.ws,
+                                              kWsFlagsOffset, st));
+            else
+                SPCCL_TRY(spccl_reduce_sliced_tracked(own, L.stream(1, r, P), slen, L.stream(0, r, P), slen,
+                                                      sliced_tau(pol, r, P), L.track + 2 * L.S * r, L.track_bytes,
+                                                      fmt_at(step, r), m, dtype, L.ws, kWsFlagsOffset, st));
+        }
+    }
+    if (fmt_trace && hipMemcpyAsync(fmt_trace, L.fmt, (uint64_t)(P - 1) * P * L.S, hipMemcpyDeviceToHost, st) !=
+                         hipSuccess)
+        return SPCCL_ERR_HIP;
+    return spccl_read_status(L.ws, 1, st);
+}
+
 }  // extern "C"
+

@@ -173,3 +173,74 @@ def test_full_size_sliced_reduce_scatter_step(S_):
     lib.spccl_decompress_sliced(out, back, ws)
     assert np.array_equal(to_host_bits(back), bits(O.decode_sliced(exp, n, dt)))
     assert lib.spccl_read_status(ws) == 0
+
+
+# ---- ring reduce-scatter over sliced streams, decisions on the device ----------------------------
+
+POLICIES = {"default": O.Policy(), "never_dense": O.Policy(adaptive=0), "always_dense": O.Policy(adaptive=2),
+            "two_nodes": O.Policy(ranks_per_node=2, inter_thresh=0.7)}
+
+
+def run_sliced_rs(lib, sends, policy):
+    P, n = len(sends), sends[0].size
+    m = n // P
+    dt = O.dtype_code(sends[0])
+    ts = [to_dev(x) for x in sends]
+    outs = [torch.empty(m, dtype=torch.bfloat16 if dt else torch.float32, device="cuda") for _ in range(P)]
+    scratch = torch.empty(lib.spccl_vr_sliced_scratch_bytes(P, m, dt), dtype=torch.uint8, device="cuda")
+    fm = lib.spccl_vr_reduce_scatter_sliced(ts, outs, scratch, policy)
+    return [to_host_bits(o) for o in outs], fm
+
+
+@pytest.mark.parametrize("dtype", [W.F32, W.BF16])
+@pytest.mark.parametrize("P", [1, 2, 3, 8])
+@pytest.mark.parametrize("pol", list(POLICIES))
+def test_vr_reduce_scatter_sliced_matches_oracle(S_, dtype, P, pol):
+    m = 2 * S + 777
+    frac = [0.5, 0.02, 0.15][P % 3]
+    sends = [W.sparse_array(P * m, int(frac * P * m), [81, P, r], dtype) for r in range(P)]
+    log(f"sliced rs P={P} dtype={dtype} policy={pol}")
+    got, gfm = run_sliced_rs(S_, sends, POLICIES[pol])
+    exp, efm = O.ring_reduce_scatter_sliced(sends, POLICIES[pol])
+    for r in range(P):
+        assert np.array_equal(got[r], bits(exp[r])), f"rank {r}"
+    assert np.array_equal(gfm, efm)
+
+
+def test_vr_reduce_scatter_sliced_per_slice_trace(S_):
+    """The two-slice construction of the oracle pin: slice 0 stays Pici,
+    slice 1 goes dense at step 4 (Sec. IV-C, per slice)."""
+    P, L0, L1 = 8, S, 10000
+    m = L0 + L1
+    idx0, idx1 = np.arange(L0), np.arange(L1)
+    sends = []
+    for r in range(P):
+        x = np.zeros(P * m, dtype=np.float32)
+        for c in range(P):
+            j = (r - c) % P or P
+            x[c * m:c * m + L0][idx0 % 100 == (j - 1)] = 1.0
+            x[c * m + L0:(c + 1) * m][(idx1 // 10 ** ((j - 1) % 4)) % 10 == 0] = 1.0
+        sends.append(x)
+    got, gfm = run_sliced_rs(S_, sends, O.Policy())
+    assert (gfm[:, :, 0] == O.FMT_PICI).all()
+    for r in range(P):
+        assert gfm[:, r, 1].tolist() == [1, 1, 1, 1, 0, 0, 0]
+    exp, _ = O.ring_reduce_scatter_sliced(sends, O.Policy())
+    for r in range(P):
+        assert np.array_equal(got[r], bits(exp[r]))
+
+
+@pytest.mark.slow
+def test_vr_reduce_scatter_sliced_config3(S_):
+    """The reduce-scatter workload (P = 8 x 33,554,432 fp32 at 99%) with the
+    per-slice decisions on the device: outputs and every slice's format."""
+    P = W.CFG3_P
+    log("sliced rs config 3: generate")
+    sends = [W.cfg3_rank(r) for r in range(P)]
+    log("sliced rs config 3: run")
+    got, gfm = run_sliced_rs(S_, sends, O.Policy())
+    log("sliced rs config 3: oracle")
+    exp, efm = O.ring_reduce_scatter_sliced(sends, O.Policy())
+    for r in range(P):
+        assert np.array_equal(got[r], bits(exp[r])), f"rank {r}"
+    assert np.array_equal(gfm, efm)
