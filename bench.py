@@ -30,6 +30,13 @@ plus message bytes read or written) against 8 TB/s.  With a full workspace
 the Pici-producing ops launch two kernels (count pass, place pass); the
 roofline entry is the single-kernel op with the largest time share, so its
 event time is one kernel's duration and matches the rocprofv3 summary.
+
+Reported beside the step (not part of value): the same ops in the
+in-collective sliced form ("sliced") and in COO ("coo"), per op; the dense
+ops of dense ring steps ("dense_ops"); the emulated reduce-scatter of the
+P = 8 x 33,554,432 workload in its canonical and device-decided sliced forms
+("collectives"); and the thresholds the modelled sweep picks for this GPU
+from the kernel costs just measured ("thresholds").
 """
 from __future__ import annotations
 
@@ -400,6 +407,38 @@ def time_dense_ops(S, torch, n, reps=10):
     return res
 
 
+def time_collectives(S, torch, reps=3):
+    """The emulated reduce-scatter of the P = 8 x 33,554,432 fp32 workload at
+    99%: the canonical ring (one global message per step, the host reads the
+    step's headers to decide) and the sliced ring (per-slice decisions on
+    the device, one synchronisation at the end).  Wall time per collective,
+    each call synchronizing the stream itself."""
+    import workloads as W
+    P, m = W.CFG3_P, W.CFG3_N // W.CFG3_P
+    F = S.SPCCL_F32
+    sends = [torch.from_numpy(W.cfg3_rank(r)).cuda() for r in range(P)]
+    outs = [torch.empty(m, dtype=torch.float32, device="cuda") for _ in range(P)]
+    res = {"workload": f"reduce-scatter, P = {P} x {W.CFG3_N:,} fp32, sigma = 0.99"}
+    runs = {
+        "canonical_ring_ms": (torch.empty(S.spccl_vr_scratch_bytes(P, m, F), dtype=torch.uint8, device="cuda"),
+                              S.spccl_vr_reduce_scatter),
+        "sliced_ring_device_decisions_ms": (torch.empty(S.spccl_vr_sliced_scratch_bytes(P, m, F), dtype=torch.uint8,
+                                                        device="cuda"), S.spccl_vr_reduce_scatter_sliced),
+    }
+    for nm, (scratch, f) in runs.items():
+        f(sends, outs, scratch)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(reps):
+            f(sends, outs, scratch)
+        torch.cuda.synchronize()
+        res[nm] = round((time.perf_counter() - t0) / reps * 1e3, 3)
+        del scratch
+    del sends, outs
+    torch.cuda.empty_cache()
+    return res
+
+
 def copy_ceiling(torch, n, reps=20):
     """Achievable HBM rate on this device for reference: back-to-back plain
     device copies of n fp32 elements (n*4 bytes read and written each), so
@@ -476,6 +515,8 @@ def main():
     ap.add_argument("--cpu-budget", type=float, default=10.0)
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--calib", action="store_true", help="also run one large plain copy (counter calibration)")
+    ap.add_argument("--no-collectives", dest="collectives", action="store_false",
+                    help="skip timing the emulated reduce-scatter collectives")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -555,6 +596,7 @@ def main():
         del Rs
         torch.cuda.empty_cache()
     dense_ops = time_dense_ops(S, torch, args.n)
+    collectives = time_collectives(S, torch) if args.collectives else None
     cpu = None
     if not args.no_cpu:
         _log("timing the CPU oracle")
@@ -568,7 +610,7 @@ def main():
                                "step = compress, send, decompress, 3 reduce variants, gather-expand, adaptive switch",
                    "n": args.n, "sigma": args.permille / 1000, "parallelism": "1 GPU (virtual ranks)"},
         "roofline": roof, "cpu_baseline": cpu, "copy_ceiling": ceiling, "kernels": kernels, "sliced": sliced,
-        "coo": coo, "sweep": sweep, "dense_ops": dense_ops,
+        "coo": coo, "sweep": sweep, "dense_ops": dense_ops, "collectives": collectives,
         "parity_compress_vs_oracle": parity, "wall_s_timed": round(wall, 3),
         "calibration_copy_bytes": calib,
     }
