@@ -1429,7 +1429,7 @@ template <class E, int SA, int SB>
 __global__ void __launch_bounds__(kBlockThreads) k_to_coo(PiciSinkArgs g) {
     using raw = typename E::raw;
     constexpr bool coo_in = SA == SRC_COO || SB == SRC_COO;
-    __shared__ raw stage_all[kWavesPerBlock][E::cap];
+    __shared__ raw stage_all[kWavesPerBlock][kCooOut * 4 / sizeof(raw)];   // input chunks, then output values
     __shared__ uint32_t sidx_all[kWavesPerBlock][kCooOut];
     __shared__ CooLds coo_all[coo_in ? kWavesPerBlock : 1];
     __shared__ uint32_t s_cnt[kWavesPerBlock];
@@ -1824,23 +1824,19 @@ __device__ __forceinline__ void expand_tiles(const uint8_t* msg, const uint8_t* 
             wave_lds_sync();
             store_from_stage<E>(col, rem, w, stage, cpref[k]);
         } else {
-            // dense tile: each lane reads its own column run, 16 rows at a time
-            const raw* run = A + cbase[k] + cpref[k];
-            uint32_t rank = 0;
+            // dense tile: 16 columns at a time; their values (contiguous in A,
+            // at most 1024) are staged with coalesced loads, then the group's
+            // lanes write their columns
+            const uint32_t myp = cpref[k];
 #pragma unroll 1
             for (int h = 0; h < 4; h++) {
-                raw y[16];
-#pragma unroll
-                for (int q = 0; q < 16; q++) {
-                    const bool bit = (w >> (16 * h + q)) & 1ull;
-                    y[q] = bit ? run[rank] : (raw)0;
-                    rank += bit ? 1u : 0u;
-                }
-#pragma unroll
-                for (int q = 0; q < 16; q++) {
-                    const int r = 16 * h + q;
-                    if ((uint64_t)(64 * r + l) < rem) col[64 * r] = y[q];
-                }
+                const uint32_t c0 = 16u * h;
+                const uint32_t lo = lane_bcast(myp, c0);
+                const uint32_t hi = h == 3 ? cnt : lane_bcast(myp, c0 + 16);
+                wave_lds_sync();
+                stage_values<E>(A + cbase[k] + lo, hi - lo, stage);
+                wave_lds_sync();
+                if (l >= c0 && l < c0 + 16) store_from_stage<E>(col, rem, w, stage, myp - lo);
             }
         }
     }
