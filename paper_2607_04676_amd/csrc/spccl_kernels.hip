@@ -85,6 +85,19 @@ __device__ __forceinline__ uint32_t wave_incl_scan(uint32_t x) {
 
 __device__ __forceinline__ uint32_t wave_excl_scan(uint32_t x) { return wave_incl_scan(x) - x; }
 
+// OR of x over the wave's 64 lanes (same DPP pattern), as a scalar.
+__device__ __forceinline__ uint32_t wave_or(uint32_t x) {
+    constexpr int kRowShr = 0x110, kRowBcast15 = 0x142, kRowBcast31 = 0x143;
+    int v = (int)x;
+    v |= __builtin_amdgcn_update_dpp(0, v, kRowShr + 1, 0xf, 0xf, false);
+    v |= __builtin_amdgcn_update_dpp(0, v, kRowShr + 2, 0xf, 0xf, false);
+    v |= __builtin_amdgcn_update_dpp(0, v, kRowShr + 4, 0xf, 0xf, false);
+    v |= __builtin_amdgcn_update_dpp(0, v, kRowShr + 8, 0xf, 0xf, false);
+    v |= __builtin_amdgcn_update_dpp(0, v, kRowBcast15, 0xa, 0xf, false);
+    v |= __builtin_amdgcn_update_dpp(0, v, kRowBcast31, 0xc, 0xf, false);
+    return (uint32_t)__builtin_amdgcn_readlane(v, 63);
+}
+
 // x of lane `lane`, which must be the same in every lane (a scalar read).
 __device__ __forceinline__ uint32_t lane_bcast(uint32_t x, uint32_t lane) {
     return (uint32_t)__builtin_amdgcn_readlane((int)x, (int)lane);
@@ -181,7 +194,8 @@ constexpr int kBufferWord3 = 0x00020000;   // gfx9 raw buffer: 32-bit data forma
 // first have to write them back to make room).
 constexpr int kStreamLoad = 2;
 
-template <class E, bool First>
+// Rows [R0, R1) of the tile.
+template <class E, bool First, int R0 = 0, int R1 = 64>
 __device__ __forceinline__ void fetch_dense(const uint8_t* base, uint64_t t, uint64_t n, uint32_t (&v)[64]) {
     using raw = typename E::raw;
     constexpr uint32_t rowb = 64 * sizeof(raw);             // bytes per tile row
@@ -198,7 +212,7 @@ __device__ __forceinline__ void fetch_dense(const uint8_t* base, uint64_t t, uin
     uint32_t lo = lane_id() * (uint32_t)sizeof(raw);
     asm volatile("" : "+v"(lo));
 #pragma unroll
-    for (int r = 0; r < 64; r++) {
+    for (int r = R0; r < R1; r++) {
         uint32_t x;
         if constexpr (sizeof(raw) == 4)
             x = __builtin_amdgcn_raw_buffer_load_b32(rs, lo + rowb * (r % per), 4096 * (r / per), kStreamLoad);
@@ -212,7 +226,9 @@ __device__ __forceinline__ void fetch_dense(const uint8_t* base, uint64_t t, uin
 // message.  Values go through the wave's LDS stage (contiguous coalesced
 // reads of the tile's A range), then each lane walks its column word.  A
 // tile whose counts disagree with I (or overrun nnz) is treated as empty and
-// flagged.  first: v = x; otherwise v = v (+) x.
+// flagged.  first: v = x; otherwise v = v (+) x.  The column words and
+// offsets are read non-temporally, like the dense rows they travel with (a
+// cached read measured 2-3 us slower per 256 MiB reduce).
 struct PiciMeta {
     uint64_t w;        // this lane's column word (as loaded)
     uint32_t base;     // I[t]
@@ -223,7 +239,8 @@ template <class E>
 __device__ __forceinline__ PiciMeta load_pici_meta(const uint8_t* msg, uint64_t t, uint64_t n) {
     const uint64_t* B = reinterpret_cast<const uint64_t*>(msg + kHeaderBytes);
     const uint32_t* I = reinterpret_cast<const uint32_t*>(msg + off_I(n));
-    return PiciMeta{B[t * 64 + lane_id()], I[t], I[t + 1]};
+    return PiciMeta{__builtin_nontemporal_load(&B[t * 64 + lane_id()]), __builtin_nontemporal_load(&I[t]),
+                    __builtin_nontemporal_load(&I[t + 1])};
 }
 
 // Column counts and prefixes of a tile from its metadata, checked against
@@ -285,6 +302,29 @@ __device__ __forceinline__ void stage_values(const typename E::raw* src, uint32_
     }
 }
 
+// v (+)= the staged values of the columns whose words are in wm (zero for
+// the other lanes), this lane's first value at stage[rank].  Rows set in no
+// lane's word are skipped by a scalar test of the wave's OR of the words.
+// With col (this lane's column of a full output tile), each row is also
+// stored as soon as it is final, so the stores overlap the rest of the walk.
+template <class E, bool First>
+__device__ __forceinline__ void apply_staged(uint64_t wm, uint32_t rank, const typename E::raw* stage,
+                                             uint32_t (&v)[64], typename E::raw* col = nullptr) {
+    const uint32_t ulo = wave_or((uint32_t)wm), uhi = wave_or((uint32_t)(wm >> 32));
+#pragma unroll
+    for (int r = 0; r < 64; r++) {
+        const bool bit = (wm >> r) & 1ull;
+        if (((r < 32 ? ulo : uhi) >> (r & 31)) & 1u) {   // rows empty in every column cost one scalar branch
+            if (bit) {
+                const uint32_t x = stage[rank];
+                rank++;
+                v[r] = First ? x : oplus(E{}, v[r], x);
+            }
+        }
+        if (col) col[64 * r] = (typename E::raw)v[r];
+    }
+}
+
 template <class E, bool First>
 __device__ __forceinline__ void expand_pici(PiciCols pc, const uint8_t* msg, uint64_t n, typename E::raw* stage,
                                             uint32_t (&v)[64]) {
@@ -309,21 +349,81 @@ __device__ __forceinline__ void expand_pici(PiciCols pc, const uint8_t* msg, uin
         const uint32_t hi = (one || c1 == 64) ? cnt : lane_bcast(colpref, c1);
         stage_values<E>(src + lo, hi - lo, stage);
         wave_lds_sync();
-        const uint64_t wm = (l >= c0 && l < c1) ? w : 0ull;
-        uint32_t rank = colpref - lo;
-#pragma unroll
-        for (int r = 0; r < 64; r++) {
-            const bool bit = (wm >> r) & 1ull;
-            if (__any(bit)) {                            // rows empty in every column cost one branch
-                if (bit) {
-                    const uint32_t x = stage[rank];
-                    rank++;
-                    v[r] = First ? x : oplus(E{}, v[r], x);
-                }
-            }
-        }
+        apply_staged<E, First>((l >= c0 && l < c1) ? w : 0ull, colpref - lo, stage, v);
         wave_lds_sync();
     }
+}
+
+// Early values of a Pici tile.  The tile's value range [I[t], I[t+1]) is
+// known as soon as its offsets arrive, so when it holds at most kEarlyVals
+// values they are read into registers right then, while the rest of a dense
+// operand's rows are still in flight, instead of in a second round trip after
+// all of them.  The range comes from the message and is not yet checked, so
+// the loads go through a buffer resource that ends at the message's capacity
+// (past it the hardware returns zeros); the values are used only once
+// pici_columns has confirmed the range against the column words.  Like the
+// column words, they are read non-temporally.
+constexpr int kEarlySlots = 8;
+constexpr int kEarlySplit = 32;          // dense rows issued before the early values
+constexpr uint32_t kEarlyVals = 64 * kEarlySlots;
+constexpr uint32_t kNotEarly = 0xFFFFFFFFu;
+
+struct EarlyVals {
+    uint32_t x[kEarlySlots];   // value l + 64 j of the range in x[j]
+    uint32_t cnt;              // the range's length, or kNotEarly: not read early
+};
+
+template <class E>
+__device__ __forceinline__ EarlyVals fetch_early(const uint8_t* msg, uint64_t cap, uint64_t n, const PiciMeta& m) {
+    using raw = typename E::raw;
+    EarlyVals e;
+    const uint32_t base = __builtin_amdgcn_readfirstlane(m.base);
+    const uint32_t next = __builtin_amdgcn_readfirstlane(m.next);
+    e.cnt = (next >= base && next - base <= kEarlyVals) ? next - base : kNotEarly;
+    const uint64_t start = off_A(n) + (uint64_t)base * sizeof(raw);
+    const uint64_t avail = cap > start ? cap - start : 0ull;
+    const uint64_t want = e.cnt == kNotEarly ? 0ull : (uint64_t)e.cnt * sizeof(raw);
+    const uint32_t bytes = (uint32_t)(want < avail ? want : avail);
+    const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint8_t*>(msg) + (bytes ? start : 0ull), (short)0, (int)bytes, kBufferWord3);
+    uint32_t lo = lane_id() * (uint32_t)sizeof(raw);
+    asm volatile("" : "+v"(lo));
+#pragma unroll
+    for (int j = 0; j < kEarlySlots; j++) {
+        if constexpr (sizeof(raw) == 4)
+            e.x[j] = __builtin_amdgcn_raw_buffer_load_b32(rs, lo + 64 * sizeof(raw) * j, 0, kStreamLoad);
+        else
+            e.x[j] = __builtin_amdgcn_raw_buffer_load_b16(rs, lo + 64 * sizeof(raw) * j, 0, kStreamLoad);
+    }
+    return e;
+}
+
+// v (+)= the tile from its early values when they cover it (the checked
+// count equals the early range), else from the message as expand_pici does.
+// With col (see apply_staged) the rows of an early tile are also stored;
+// returns whether they were.
+template <class E, bool First>
+__device__ __forceinline__ bool expand_pici_early(PiciCols pc, const EarlyVals& e, const uint8_t* msg, uint64_t n,
+                                                  typename E::raw* stage, uint32_t (&v)[64],
+                                                  typename E::raw* col = nullptr) {
+    using raw = typename E::raw;
+    static_assert(kEarlyVals <= E::cap, "early values fit the stage");
+    if (e.cnt != pc.cnt) {
+        expand_pici<E, First>(pc, msg, n, stage, v);
+        return false;
+    }
+    const uint32_t l = lane_id();
+    if (First) {
+#pragma unroll
+        for (int r = 0; r < 64; r++) v[r] = 0;
+    }
+#pragma unroll
+    for (int j = 0; j < kEarlySlots; j++)
+        if (l + 64u * j < pc.cnt) stage[l + 64 * j] = (raw)e.x[j];
+    wave_lds_sync();
+    apply_staged<E, First>(pc.w, pc.colpref, stage, v, col);
+    wave_lds_sync();
+    return col != nullptr;
 }
 
 // ---------------------------------------------------------------------------
@@ -564,22 +664,40 @@ __device__ void coo_tile(const uint8_t* msg, uint64_t nnz, uint64_t t, uint64_t 
 // message's index arrays, so the early reads stay inside the caller's
 // buffers whatever the header says.  Returns false, the same in every wave
 // of the grid, when a header fails its check (and flags it once).
+// A dense sink passes col (this lane's column of the output tile when the
+// tile is full): a Pici operand read early then stores the rows as they are
+// finished, and *stored says so.
 template <class E, int SA, int SB>
 __device__ __forceinline__ bool load_tile_pair(const DevOperand& a, const DevOperand& b, uint64_t t, bool has_tile,
                                                uint64_t n, typename E::raw* stage, CooLds* cl, WsCtrl* ctrl,
-                                               uint32_t (&v)[64]) {
+                                               uint32_t (&v)[64], typename E::raw* col = nullptr,
+                                               bool* stored = nullptr) {
     const bool ha = a.hdr != nullptr;
     const bool hb = SB != SRC_NONE && b.hdr != nullptr;
     HeaderWords hwa{}, hwb{};
     if (ha) hwa = load_header_words(a.hdr);
     if (hb) hwb = load_header_words(b.hdr);
     PiciMeta ma{0, 0, 0}, mb{0, 0, 0};
+    // one dense and one Pici operand: the Pici tile's values are read early,
+    // between the two halves of the dense rows
+    constexpr bool early_a = SA == SRC_PICI && SB == SRC_DENSE;
+    constexpr bool early_b = SA == SRC_DENSE && SB == SRC_PICI;
+    EarlyVals ev{{0u}, kNotEarly};
     if (has_tile) {
         if constexpr (SA == SRC_PICI) ma = load_pici_meta<E>(a.data, t, n);
         if constexpr (SB == SRC_PICI) mb = load_pici_meta<E>(b.data, t, n);
         asm volatile("" ::: "memory");
-        if constexpr (SA == SRC_DENSE) fetch_dense<E, true>(a.data, t, n, v);
-        if constexpr (SB == SRC_DENSE) fetch_dense<E, SA != SRC_DENSE>(b.data, t, n, v);
+        if constexpr (early_a || early_b) {
+            const uint8_t* d = early_b ? a.data : b.data;
+            fetch_dense<E, true, 0, kEarlySplit>(d, t, n, v);
+            asm volatile("" ::: "memory");
+            ev = early_b ? fetch_early<E>(b.data, b.cap, n, mb) : fetch_early<E>(a.data, a.cap, n, ma);
+            asm volatile("" ::: "memory");
+            fetch_dense<E, true, kEarlySplit, 64>(d, t, n, v);
+        } else {
+            if constexpr (SA == SRC_DENSE) fetch_dense<E, true>(a.data, t, n, v);
+            if constexpr (SB == SRC_DENSE) fetch_dense<E, SA != SRC_DENSE>(b.data, t, n, v);
+        }
     }
     bool ok = true;
     uint64_t nnza = 0, nnzb = 0;
@@ -602,7 +720,12 @@ __device__ __forceinline__ bool load_tile_pair(const DevOperand& a, const DevOpe
     if (has_tile) {
         constexpr bool dense_first = SA == SRC_DENSE || SB == SRC_DENSE;
         constexpr bool a_sparse = SA == SRC_PICI || SA == SRC_COO;
-        if constexpr (SA == SRC_PICI)
+        if constexpr (early_a) {
+            const bool st = expand_pici_early<E, false>(pici_columns(ma, nnza, t, n, ctrl), ev, a.data, n, stage, v,
+                                                        col);
+            if (stored) *stored = st;
+        }
+        else if constexpr (SA == SRC_PICI)
             expand_pici<E, !dense_first>(pici_columns(ma, nnza, t, n, ctrl), a.data, n, stage, v);
         if constexpr (SA == SRC_COO) {
             if (!dense_first) {
@@ -611,7 +734,12 @@ __device__ __forceinline__ bool load_tile_pair(const DevOperand& a, const DevOpe
             }
             coo_tile<E>(a.data, nnza, t, n, stage, cl, ctrl, v);
         }
-        if constexpr (SB == SRC_PICI)
+        if constexpr (early_b) {
+            const bool st = expand_pici_early<E, false>(pici_columns(mb, nnzb, t, n, ctrl), ev, b.data, n, stage, v,
+                                                        col);
+            if (stored) *stored = st;
+        }
+        else if constexpr (SB == SRC_PICI)
             expand_pici<E, !dense_first && !a_sparse>(pici_columns(mb, nnzb, t, n, ctrl), b.data, n, stage, v);
         if constexpr (SB == SRC_COO) {
             if (!dense_first && !a_sparse) {
@@ -1627,11 +1755,15 @@ __global__ void __launch_bounds__(kBlockThreads) k_to_dense(DenseSinkArgs g) {
     const uint64_t t = (uint64_t)blockIdx.x * kWavesPerBlock + wave;
     const bool has_tile = t < g.T;
     uint32_t v[64];
-    if (!load_tile_pair<E, SA, SB>(g.a, g.b, t, has_tile, g.n, stage_all[wave], &coo_all[coo ? wave : 0], g.ctrl, v))
+    raw* col = (has_tile && g.n - t * kTileElems >= kTileElems)
+                   ? reinterpret_cast<raw*>(g.out) + t * kTileElems + lane_id() : nullptr;
+    bool stored = false;
+    if (!load_tile_pair<E, SA, SB>(g.a, g.b, t, has_tile, g.n, stage_all[wave], &coo_all[coo ? wave : 0], g.ctrl, v,
+                                   col, &stored))
         return;
     if (blockIdx.x == 0 && threadIdx.x == 0 && g.out_hdr)
         write_header(g.out_hdr, kFmtDense, E::dtype, g.n, kNnzUnknown, 0, kHeaderBytes, dense_msg_bytes(g.n, E::dtype));
-    if (!has_tile) return;
+    if (!has_tile || stored) return;
     store_tile<E>(g.out, t, g.n, v);
 }
 
@@ -1926,22 +2058,37 @@ __global__ void __launch_bounds__(kBlockThreads) k_sliced(SlicedArgs g) {
     uint32_t v[64];
     if constexpr (HasB) {
         // header and column words first (both lie inside the slot whatever
-        // the header says), then a's rows; the header is checked meanwhile
+        // the header says), then half of a's rows; by then the header is in,
+        // and a Pici slice's values are read early, before the other half
+        // These reads stay inside the slot (sized for a full slice) or the
+        // slice's rows (a buffer resource that ends there) whether or not the
+        // wave has a tile, so no branch guards them: one would make the wave
+        // wait for the first reads before issuing the rest.
         const uint8_t* bm = g.b + q * g.slot;
         const HeaderWords hw = load_header_words(bm);
-        const PiciMeta m = has_tile ? load_pici_meta<E>(bm, t, ns) : PiciMeta{0, 0, 0};
+        const PiciMeta m = load_pici_meta<E>(bm, t, ns);
         asm volatile("" ::: "memory");
-        if (has_tile) fetch_dense<E, true>(a, t, ns, v);
+        fetch_dense<E, true, 0, kEarlySplit>(a, t, ns, v);
+        asm volatile("" ::: "memory");
         const HeaderView h = check_header(hw, g.slot, ns, E::dtype, -1);
+        const bool pici = h.ok && h.fmt == (uint32_t)kFmtPici;
+        EarlyVals ev = fetch_early<E>(bm, pici ? g.slot : 0ull, ns, m);
+        asm volatile("" ::: "memory");
+        fetch_dense<E, true, kEarlySplit, 64>(a, t, ns, v);
         if (!h.ok || h.fmt == (uint32_t)kFmtCoo) {       // the same in every wave of the block
             if (threadIdx.x == 0) set_status(g.ctrl, SPCCL_ERR_CORRUPT_STREAM);
             return;
         }
         if (has_tile) {
-            if (h.fmt == (uint32_t)kFmtPici)
-                expand_pici<E, false>(pici_columns(m, h.nnz, t, ns, g.ctrl), bm, ns, stage, v);
-            else
+            if (h.fmt == (uint32_t)kFmtPici) {
+                // a dense output tile that is full takes its rows as they are finished
+                raw* col = (!OutSliced && ns - t * kTileElems >= kTileElems)
+                               ? reinterpret_cast<raw*>(g.out) + base + t * kTileElems + l : nullptr;
+                if (expand_pici_early<E, false>(pici_columns(m, h.nnz, t, ns, g.ctrl), ev, bm, ns, stage, v, col))
+                    return;
+            } else {
                 fetch_dense<E, false>(bm + kHeaderBytes, t, ns, v);
+            }
         }
     } else {
         if (has_tile) fetch_dense<E, true>(a, t, ns, v);
