@@ -16,9 +16,10 @@ One step is one pass of the whole hot path over one batch:
   gather_expand of the two        all-gather receive side
   adaptive switch                 the fused step's header (nonzero count) is
                                   copied to pinned host memory as soon as that
-                                  reduce ends; the host waits for that copy
-                                  only, then applies Eq. 7 against the 0.6
-                                  threshold while the GPU runs the rest
+                                  reduce ends (op "switch_header"); the host
+                                  waits for that copy only, then applies Eq. 7
+                                  against the 0.6 threshold while the GPU runs
+                                  the rest
 
 value = dense-equivalent bytes of the step (N*s per codec op, 2*N*s per
 reduce, P*N*s per gather) / step time over K timed steps.  Inside the timed
@@ -140,8 +141,9 @@ class Runner:
             ("compress", lambda: S.spccl_compress(a, self.msg_a, ws), n * s),
             ("send", lambda: S.spccl_copy_message(self.msg_a, self.recv, ws), 0),
             ("decompress", lambda: S.spccl_decompress(self.recv, self.dense_out, ws), n * s),
-            ("reduce_dense_pici_to_pici", lambda: (S.spccl_reduce(S.operand(a), msg(mb), msg(self.red_p), n, F, ws),
-                                                   self.fetch_header()), 2 * n * s),
+            ("reduce_dense_pici_to_pici", lambda: S.spccl_reduce(S.operand(a), msg(mb), msg(self.red_p), n, F, ws),
+             2 * n * s),
+            ("switch_header", self.fetch_header, 0),
             ("reduce_pici_pici_to_pici", lambda: S.spccl_reduce(msg(self.msg_a), msg(mb), msg(self.red_pp), n, F, ws),
              2 * n * s),
             ("reduce_dense_pici_to_dense", lambda: S.spccl_reduce(S.operand(a), msg(mb), S.operand(self.red_d), n,
@@ -186,6 +188,7 @@ class Runner:
             "reduce_pici_pici_to_pici": ba + bb + bpp,
             "reduce_dense_pici_to_dense": n * s + bb + n * s,
             "gather_expand": ba + bp + 2 * n * s,
+            "switch_header": 48,
         }
 
     def calibration_copy(self):

@@ -243,6 +243,24 @@ __device__ __forceinline__ PiciMeta load_pici_meta(const uint8_t* msg, uint64_t 
                     __builtin_nontemporal_load(&I[t + 1])};
 }
 
+// The same through a buffer resource that ends at the message's index
+// arrays (or its capacity, if smaller): any tile index reads inside the
+// buffer (past the end the hardware returns zeros), so a wave without a tile
+// issues the loads too and no branch makes it wait for them early.
+template <class E>
+__device__ __forceinline__ PiciMeta load_pici_meta_any(const uint8_t* msg, uint64_t cap, uint64_t t, uint64_t n) {
+    const uint64_t end = off_A(n) < cap ? off_A(n) : cap;
+    const __amdgpu_buffer_rsrc_t rs =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(msg), (short)0, (int)(uint32_t)end, kBufferWord3);
+    t = ((uint64_t)__builtin_amdgcn_readfirstlane((uint32_t)(t >> 32)) << 32) |
+        __builtin_amdgcn_readfirstlane((uint32_t)t);
+    const uint32_t ob = (uint32_t)(kHeaderBytes + 512ull * t), oi = (uint32_t)(off_I(n) + 4ull * t);
+    // every offset in the per-lane part, which the range check always covers
+    const auto w = __builtin_amdgcn_raw_buffer_load_b64(rs, ob + lane_id() * 8u, 0, kStreamLoad);
+    const auto i2 = __builtin_amdgcn_raw_buffer_load_b64(rs, oi, 0, kStreamLoad);
+    return PiciMeta{(uint64_t)w[0] | ((uint64_t)w[1] << 32), i2[0], i2[1]};
+}
+
 // Column counts and prefixes of a tile from its metadata, checked against
 // I and nnz and against the array's end (a bit at a position >= n); a tile
 // that fails is flagged and reads as empty.  So no value beyond n ever leaves
@@ -1305,8 +1323,8 @@ __global__ void __launch_bounds__(kBlockThreads) k_pp_tile(PiciSinkArgs g) {
     // while those are in flight
     const HeaderWords hwa = load_header_words(g.a.hdr);
     const HeaderWords hwb = load_header_words(g.b.hdr);
-    const PiciMeta ma = has_tile ? load_pici_meta<E>(g.a.data, t, g.n) : PiciMeta{0, 0, 0};
-    const PiciMeta mb = has_tile ? load_pici_meta<E>(g.b.data, t, g.n) : PiciMeta{0, 0, 0};
+    const PiciMeta ma = load_pici_meta_any<E>(g.a.data, g.a.cap, t, g.n);
+    const PiciMeta mb = load_pici_meta_any<E>(g.b.data, g.b.cap, t, g.n);
     const HeaderView ha = check_header(hwa, g.a.cap, g.n, E::dtype, kFmtPici);
     const HeaderView hb = check_header(hwb, g.b.cap, g.n, E::dtype, kFmtPici);
     if (!(ha.ok && hb.ok)) {          // the same in every wave: no partition publishes
