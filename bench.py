@@ -60,7 +60,7 @@ METRIC = "dense-equivalent GB/s (and % of HBM peak) for Pici compress/decompress
 SINGLE_KERNEL_OPS = {
     "decompress": "k_gather<F32, 2>",
     "reduce_dense_pici_to_dense": "k_to_dense<F32, 1, 2>",
-    "gather_expand": "k_gather<F32, 4>",
+    "gather_expand": "k_gather<F32, 2>",
     "send": "k_copy_message",
 }
 

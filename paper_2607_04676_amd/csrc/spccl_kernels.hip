@@ -2429,16 +2429,17 @@ spccl_status_t launch_to_coo_dt(int dtype, int sa, int sb, const PiciSinkArgs& g
     return dtype == kBF16 ? launch_to_coo<BF16>(sa, sb, g, st) : launch_to_coo<F32>(sa, sb, g, st);
 }
 
-// Tiles per wave of the expansion: enough waves to fill the chip (about
-// 8192 resident), and as many tiles per wave as that leaves, up to 4.
+// Tiles per wave of the expansion: two once that still leaves enough waves
+// to fill the chip (about 8192 resident), else one.  Four tiles per wave
+// measured the same at 99% sparsity and 10% slower at 90% (their values no
+// longer fit one staged chunk), one tile per wave 5-10% slower at 99%.
 template <class E>
 void launch_gather_k(const GatherArgs& g, int P, hipStream_t st) {
     const uint64_t tiles = g.T * (uint64_t)P;
-    const int K = tiles >= 4 * 8192 ? 4 : tiles >= 2 * 8192 ? 2 : 1;
+    const int K = tiles >= 2 * 8192 ? 2 : 1;
     dim3 block(kBlockThreads);
     dim3 grid(stream_grid(g.T, kWavesPerBlock * K, 0x7FFFFFFF), (unsigned)P);
-    if (K == 4) hipLaunchKernelGGL((k_gather<E, 4>), grid, block, 0, st, g);
-    else if (K == 2) hipLaunchKernelGGL((k_gather<E, 2>), grid, block, 0, st, g);
+    if (K == 2) hipLaunchKernelGGL((k_gather<E, 2>), grid, block, 0, st, g);
     else hipLaunchKernelGGL((k_gather<E, 1>), grid, block, 0, st, g);
 }
 
