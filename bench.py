@@ -32,6 +32,10 @@ the Pici-producing ops launch two kernels (count pass, place pass); the
 roofline entry is the single-kernel op with the largest time share, so its
 event time is one kernel's duration and matches the rocprofv3 summary.
 
+Each op is also timed on its own ("isolated": median, min and max over 50
+repetitions, each after 512 MiB of scratch writes), at the headline sparsity,
+in the sliced form and at each swept sparsity.
+
 Reported beside the step (not part of value): the same ops in the
 in-collective sliced form ("sliced") and in COO ("coo"), per op; the dense
 ops of dense ring steps ("dense_ops"); the emulated reduce-scatter of the
@@ -380,6 +384,38 @@ def time_steps(R, steps, warmup, copies):
     return total_ms, wall, per, dense_eq, dom, timed[dom]
 
 
+def time_isolated(R, reps=50, warm=5):
+    """Each op of a runner on its own: before every repetition 512 MiB of
+    scratch is written (untimed), so neither the Infinity Cache nor the L2
+    holds the op's operands and the op pays for that write-back as a cold
+    launch would; the op is bracketed by HIP events.  Median, min and max
+    over reps, in microseconds, and the median's fraction of 8 TB/s by
+    algorithmic bytes."""
+    torch = R.torch
+    junk = torch.empty(1 << 27, dtype=torch.float32, device="cuda")
+    alg = R.algorithmic_bytes()
+    res = {}
+    for nm, f, _ in R.ops(0):
+        if nm == "switch_header":
+            continue
+        ts = []
+        for r in range(warm + reps):
+            junk.fill_(float(r))
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            f()
+            e1.record()
+            e1.synchronize()
+            if r >= warm:
+                ts.append(e0.elapsed_time(e1) * 1e3)
+        med = float(np.median(ts))
+        res[nm] = {"median_us": round(med, 2), "min_us": round(min(ts), 2), "max_us": round(max(ts), 2),
+                   "reps": reps, "algorithmic_bytes": alg[nm],
+                   "frac_of_hbm_peak": round(alg[nm] / (med * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)}
+    del junk
+    return res
+
+
 def time_dense_ops(S, torch, n, reps=10):
     """The dense ops of the ring's dense steps (for the threshold model):
     dense (+) dense -> dense array, and wrapping an array as a dense message
@@ -554,6 +590,7 @@ def main():
             "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(dgbs / HBM_PEAK_GBS, 4),
             "traffic": traffic_for(dom),
             "algorithmic_bytes_per_launch": alg[dom], "avg_launch_ms": round(dom_ms, 5)}
+    isolated = time_isolated(R)
     # the in-collective (sliced) form of the codec and reduce ops, per op
     SR = SlicedRunner(R)
     for w in range(2):
@@ -562,7 +599,7 @@ def main():
     _, _, per_s, _ = run_steps(SR, max(5, args.steps // 3), args.copies, [op[0] for op in SR.ops(0)])
     alg_s = SR.algorithmic_bytes()
     sliced = {"slice_elems": 16384, "dense_thresh": SR.thresh, "parity_compress_vs_oracle": SR.check_parity(),
-              "kernels": {}}
+              "kernels": {}, "isolated": time_isolated(SR)}
     for nm, ms in per_s.items():
         gbs = alg_s[nm] / (ms / 1e3) / 1e9
         sliced["kernels"][nm] = {"ms": round(ms, 5), "algorithmic_bytes": alg_s[nm], "achieved_GBs": round(gbs, 1),
@@ -595,6 +632,7 @@ def main():
                              "frac_of_hbm_peak": round(a_s[nm] / (ms / 1e3) / 1e9 / HBM_PEAK_GBS, 4)}
                         for nm, ms in p_s.items()},
             "parity_compress": Rs.check_parity(),
+            "isolated": time_isolated(Rs),
         }
         del Rs
         torch.cuda.empty_cache()
@@ -612,7 +650,8 @@ def main():
                                f"sigma={args.permille / 1000}, uniform random nonzero positions, N(0,1) values; "
                                "step = compress, send, decompress, 3 reduce variants, gather-expand, adaptive switch",
                    "n": args.n, "sigma": args.permille / 1000, "parallelism": "1 GPU (virtual ranks)"},
-        "roofline": roof, "cpu_baseline": cpu, "copy_ceiling": ceiling, "kernels": kernels, "sliced": sliced,
+        "roofline": roof, "cpu_baseline": cpu, "copy_ceiling": ceiling, "kernels": kernels, "isolated": isolated,
+        "sliced": sliced,
         "coo": coo, "sweep": sweep, "dense_ops": dense_ops, "collectives": collectives,
         "parity_compress_vs_oracle": parity, "wall_s_timed": round(wall, 3),
         "calibration_copy_bytes": calib,

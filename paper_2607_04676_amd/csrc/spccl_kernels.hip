@@ -1106,194 +1106,6 @@ __device__ __forceinline__ void pp_merge(uint64_t wa, uint64_t wb, uint64_t wo, 
     }
 }
 
-// One wave per partition (kTilesPerPart consecutive tiles).  When every tile
-// checks out and the partition's two value ranges fit kChunkVals together,
-// both ranges are read at once (all loads in flight) and staged a single
-// time for both phases.  Otherwise the tiles go one at a time through
-// column groups (metadata read again per phase, the output column words read
-// back from the message).
-template <class E, bool Deferred>
-__global__ void __launch_bounds__(kBlockThreads) k_pp_to_pici(PiciSinkArgs g) {
-    using raw = typename E::raw;
-    constexpr int K = kTilesPerPart;
-    __shared__ raw lds_in[kWavesPerBlock][kChunkVals];
-    __shared__ uint32_t s_tcnt[kWavesPerBlock][K];
-    const uint32_t wave = threadIdx.x >> 6, l = lane_id();
-    raw* in = lds_in[wave];
-    const uint32_t p = blockIdx.x * kWavesPerBlock + wave;
-    if (p >= g.nparts) return;
-    const uint32_t epoch30 = g.epoch & 0x3FFFFFFFu;
-    const uint64_t t0 = (uint64_t)p * K;
-    const uint64_t oI = off_I(g.n), oA = off_A(g.n);
-    const raw* Aa = reinterpret_cast<const raw*>(g.a.data + oA);
-    const raw* Ab = reinterpret_cast<const raw*>(g.b.data + oA);
-    uint64_t* Bout = reinterpret_cast<uint64_t*>(g.out + kHeaderBytes);
-
-    // headers and column words / offsets first (the host guarantees both
-    // messages' capacities cover the index arrays), headers checked while
-    // the rest is in flight
-    const HeaderWords hwa = load_header_words(g.a.hdr);
-    const HeaderWords hwb = load_header_words(g.b.hdr);
-    PiciMeta ma[K], mb[K];
-#pragma unroll
-    for (int k = 0; k < K; k++) {
-        const bool have = t0 + k < g.T;
-        ma[k] = have ? load_pici_meta<E>(g.a.data, t0 + k, g.n) : PiciMeta{0, 0, 0};
-        mb[k] = have ? load_pici_meta<E>(g.b.data, t0 + k, g.n) : PiciMeta{0, 0, 0};
-    }
-    const HeaderView ha = check_header(hwa, g.a.cap, g.n, E::dtype, kFmtPici);
-    const HeaderView hb = check_header(hwb, g.b.cap, g.n, E::dtype, kFmtPici);
-    if (!(ha.ok && hb.ok)) {          // the same in every wave: no partition publishes
-        if (blockIdx.x == 0 && threadIdx.x == 0) set_status(g.ctrl, SPCCL_ERR_CORRUPT_STREAM);
-        return;
-    }
-    const uint64_t nnz_a = ha.nnz, nnz_b = hb.nnz;
-
-    uint64_t wa[K], wb[K];
-    uint32_t pa[K], pb[K];                    // column prefixes
-    uint32_t na[K], nb[K], ba[K], bb[K];      // counts and bases (wave-uniform)
-    bool allok = true;
-#pragma unroll
-    for (int k = 0; k < K; k++) {
-        const bool have = t0 + k < g.T;
-        const PiciCols ca = have ? pici_columns(ma[k], nnz_a, t0 + k, g.n, g.ctrl) : PiciCols{0, 0, 0, 0, true};
-        const PiciCols cb = have ? pici_columns(mb[k], nnz_b, t0 + k, g.n, g.ctrl) : PiciCols{0, 0, 0, 0, true};
-        allok = allok && ca.ok && cb.ok;
-        wa[k] = ca.w; pa[k] = ca.colpref; na[k] = __builtin_amdgcn_readfirstlane(ca.cnt);
-        ba[k] = __builtin_amdgcn_readfirstlane(ca.base);
-        wb[k] = cb.w; pb[k] = cb.colpref; nb[k] = __builtin_amdgcn_readfirstlane(cb.cnt);
-        bb[k] = __builtin_amdgcn_readfirstlane(cb.base);
-    }
-    uint32_t La = 0, Lb = 0;
-#pragma unroll
-    for (int k = 0; k < K; k++) { La += na[k]; Lb += nb[k]; }
-    // valid tiles chain (base + cnt == next == the next tile's base), so the
-    // partition's values of each operand are one contiguous range
-    const bool staged = allok && La + Lb <= kChunkVals;
-
-    uint32_t agg = 0;
-    raw* dst;
-    uint32_t prefix = 0;
-    if (staged) {
-        bool zero;
-        {
-            raw x[kChunkSlots];
-#pragma unroll
-            for (int j = 0; j < kChunkSlots; j++) {
-                const uint32_t i = l + 64 * j;
-                x[j] = i < La ? Aa[ba[0] + i] : (i < La + Lb ? Ab[bb[0] + (i - La)] : (raw)1);
-            }
-            bool z = false;
-#pragma unroll
-            for (int j = 0; j < kChunkSlots; j++) {
-                const uint32_t i = l + 64 * j;
-                z |= x[j] == 0;
-                if (i < La + Lb) in[i] = x[j];
-            }
-            zero = __any(z);
-            wave_lds_sync();
-        }
-        uint64_t wo[K];
-        uint32_t cpo[K], texcl[K];
-#pragma unroll
-        for (int k = 0; k < K; k++) {
-            const uint64_t cancel = pp_cancel<E>(wa[k], wb[k], in, (ba[k] - ba[0]) + pa[k],
-                                                 La + (bb[k] - bb[0]) + pb[k], zero, true);
-            wo[k] = (wa[k] | wb[k]) & ~cancel;
-            if (t0 + k < g.T) Bout[(t0 + k) * 64 + l] = wo[k];
-            const uint32_t c = (uint32_t)__popcll(wo[k]);
-            cpo[k] = wave_excl_scan(c);
-            texcl[k] = agg;
-            agg += __builtin_amdgcn_readfirstlane(lane_bcast(cpo[k] + c, 63));
-        }
-        if (l == 0) publish(g.flags, p, epoch30, (p == 0 && !Deferred) ? kFlagPrefix : kFlagAggregate, agg);
-        if constexpr (Deferred) {
-            dst = reinterpret_cast<raw*>(g.slots) + (uint64_t)p * kPartElems;
-        } else {
-            prefix = p == 0 ? 0u : lookback(g.flags, p, epoch30, g.ctrl);
-            if (l == 0 && p != 0) publish(g.flags, p, epoch30, kFlagPrefix, prefix + agg);
-            dst = reinterpret_cast<raw*>(g.out + oA) + prefix;
-        }
-#pragma unroll
-        for (int k = 0; k < K; k++) {
-            if (t0 + k >= g.T) break;
-            pp_merge<E>(wa[k], wb[k], wo[k], in, (ba[k] - ba[0]) + pa[k], La + (bb[k] - bb[0]) + pb[k],
-                        dst + texcl[k], cpo[k], true);
-            if (l == 0) reinterpret_cast<uint32_t*>(g.out + oI)[t0 + k] = prefix + texcl[k];
-        }
-    } else {
-        // phase 1, one tile at a time
-#pragma unroll 1
-        for (int k = 0; k < K; k++) {
-            const uint64_t t = t0 + k;
-            uint32_t tc = 0;
-            if (t < g.T) {
-                const PiciCols ca = pici_columns(load_pici_meta<E>(g.a.data, t, g.n), nnz_a, t, g.n, g.ctrl);
-                const PiciCols cb = pici_columns(load_pici_meta<E>(g.b.data, t, g.n), nnz_b, t, g.n, g.ctrl);
-                const bool one = ca.cnt + cb.cnt <= kChunkVals;
-                const int ngroups = one ? 1 : PPGroup::count;
-                const uint32_t gcols = one ? 64u : PPGroup::cols;
-                uint64_t cancel = 0;
-                for (int h = 0; h < ngroups; h++) {
-                    const uint32_t c0 = gcols * h, c1 = c0 + gcols;
-                    bool zg;
-                    const uint32_t la = pp_stage<E>(ca, cb, Aa + ca.base, Ab + cb.base, c0, c1, in, zg);
-                    cancel |= pp_cancel<E>(ca.w, cb.w, in, ca.colpref - lane_bcast(ca.colpref, c0),
-                                           la + cb.colpref - lane_bcast(cb.colpref, c0), zg, l >= c0 && l < c1);
-                    wave_lds_sync();
-                }
-                const uint64_t wo = (ca.w | cb.w) & ~cancel;
-                Bout[t * 64 + l] = wo;
-                tc = (uint32_t)__popcll(wo);
-                tc = lane_bcast(wave_excl_scan(tc) + tc, 63);
-            }
-            if (l == 0) s_tcnt[wave][k] = tc;
-            agg += tc;
-        }
-        if (l == 0) publish(g.flags, p, epoch30, (p == 0 && !Deferred) ? kFlagPrefix : kFlagAggregate, agg);
-        if constexpr (Deferred) {
-            dst = reinterpret_cast<raw*>(g.slots) + (uint64_t)p * kPartElems;
-        } else {
-            prefix = p == 0 ? 0u : lookback(g.flags, p, epoch30, g.ctrl);
-            if (l == 0 && p != 0) publish(g.flags, p, epoch30, kFlagPrefix, prefix + agg);
-            dst = reinterpret_cast<raw*>(g.out + oA) + prefix;
-        }
-        // phase 2, one tile at a time
-        uint32_t texcl = 0;
-#pragma unroll 1
-        for (int k = 0; k < K; k++) {
-            const uint64_t t = t0 + k;
-            if (t >= g.T) break;
-            const PiciCols ca = pici_columns(load_pici_meta<E>(g.a.data, t, g.n), nnz_a, t, g.n, g.ctrl);
-            const PiciCols cb = pici_columns(load_pici_meta<E>(g.b.data, t, g.n), nnz_b, t, g.n, g.ctrl);
-            const uint64_t wo = Bout[t * 64 + l];             // this wave's own phase-1 store
-            const uint32_t cpo = wave_excl_scan((uint32_t)__popcll(wo));
-            const bool one = ca.cnt + cb.cnt <= kChunkVals;
-            const int ngroups = one ? 1 : PPGroup::count;
-            const uint32_t gcols = one ? 64u : PPGroup::cols;
-            for (int h = 0; h < ngroups; h++) {
-                const uint32_t c0 = gcols * h, c1 = c0 + gcols;
-                bool zg;
-                const uint32_t la = pp_stage<E>(ca, cb, Aa + ca.base, Ab + cb.base, c0, c1, in, zg);
-                pp_merge<E>(ca.w, cb.w, wo, in, ca.colpref - lane_bcast(ca.colpref, c0),
-                            la + cb.colpref - lane_bcast(cb.colpref, c0), dst + texcl, cpo, l >= c0 && l < c1);
-                wave_lds_sync();
-            }
-            if (l == 0) reinterpret_cast<uint32_t*>(g.out + oI)[t] = prefix + texcl;
-            texcl += s_tcnt[wave][k];
-        }
-    }
-    if constexpr (!Deferred) {
-        if (p == g.nparts - 1 && l == 0) {
-            const uint64_t nnz = (uint64_t)prefix + agg;
-            uint32_t* I = reinterpret_cast<uint32_t*>(g.out + oI);
-            I[g.T] = (uint32_t)nnz;
-            for (uint64_t b = oI + 4 * (g.T + 1); b < oA; b += 4) *reinterpret_cast<uint32_t*>(g.out + b) = 0u;
-            write_header(g.out, kFmtPici, E::dtype, g.n, nnz, oI, oA, oA + nnz * sizeof(raw));
-        }
-    }
-}
-
 // Pici (+) Pici -> Pici, one tile per wave and one partition per block (the
 // partition's four tile counts meet in LDS, as in k_to_pici).  Each wave
 // reads its tile's column words and offsets from both messages, stages both
