@@ -364,14 +364,16 @@ spccl_status_t spccl_vr_all_reduce(void* const* send, void* const* recv, int32_t
 
 /* Ring reduce-scatter over sliced streams with the decisions on the device
  * (the paper's in-collective mode, Sec. V-B, with Sec. IV-C per slice):
- * step 0 compresses with spccl_compress_sliced_tracked, later steps send
- * through spccl_copy_sliced and reduce with spccl_reduce_sliced_tracked, the
- * last receive reduces into recv[r] (n/P elements, the same values as
- * spccl_vr_reduce_scatter).  tau per link as in spccl_policy_t (adaptive 0:
- * never dense, 2: always); sparse_fmt must be SPCCL_FMT_PICI.  The stream is
- * synchronised once, at the end.  fmt_trace (host, optional) gets the
- * format of every slice sent: (P-1) * P * S bytes, index
- * (step * P + rank) * S + slice, S = spccl_slice_count(n / P). */
+ * step 0 compresses as spccl_compress_sliced_tracked does, later steps send
+ * as spccl_copy_sliced and reduce as spccl_reduce_sliced_tracked, the last
+ * receive reduces into recv[r] (n/P elements, the same values as
+ * spccl_vr_reduce_scatter).  The P ranks' kernels of one ring step are one
+ * launch (up to 32 ranks each), so no recv[r] may overlap another rank's
+ * recv or any send buffer (SPCCL_ERR_INVALID_ARG).  tau per link as in
+ * spccl_policy_t (adaptive 0: never dense, 2: always); sparse_fmt must be
+ * SPCCL_FMT_PICI.  The stream is synchronised once, at the end.  fmt_trace
+ * (host, optional) gets the format of every slice sent: (P-1) * P * S bytes,
+ * index (step * P + rank) * S + slice, S = spccl_slice_count(n / P). */
 uint64_t spccl_vr_sliced_scratch_bytes(int32_t P, uint64_t msg_elems, int32_t dtype);
 spccl_status_t spccl_vr_reduce_scatter_sliced(void* const* send, void* const* recv, int32_t P, uint64_t n,
                                               int32_t dtype, const spccl_policy_t* policy,

@@ -120,4 +120,31 @@ struct SlicedArgs {
     uint8_t* fmt_out;      // per slice: the format produced (nullptr: not recorded)
 };
 
+// One sliced ring step for up to kMaxBatchRanks virtual ranks in a single
+// launch (grid y = rank): rank r's arguments are base with its own dense or
+// source pointer a[r], its own dense output (out_dense[r], else the strided
+// stream base.out + r out_stride), its threshold, and strided received
+// streams, trackers and format records.
+constexpr int kMaxBatchRanks = 32;
+struct SlicedBatch {
+    SlicedArgs base;
+    const uint8_t* a[kMaxBatchRanks];
+    uint8_t* out_dense[kMaxBatchRanks];
+    double thresh[kMaxBatchRanks];
+    uint64_t b_stride, out_stride;   // bytes between ranks
+    uint64_t track_stride;           // doubles between ranks
+    uint64_t fmt_stride;             // bytes between ranks
+};
+
+__host__ __device__ inline SlicedArgs batch_rank(const SlicedBatch& b, uint32_t r) {
+    SlicedArgs g = b.base;
+    g.a = b.a[r];
+    if (g.b) g.b = b.base.b + r * b.b_stride;
+    g.out = b.out_dense[r] ? b.out_dense[r] : b.base.out + r * b.out_stride;
+    g.thresh = b.thresh[r];
+    if (g.track) g.track = b.base.track + r * b.track_stride;
+    if (g.fmt_out) g.fmt_out = b.base.fmt_out + r * b.fmt_stride;
+    return g;
+}
+
 }  // namespace spccl

@@ -1871,14 +1871,15 @@ __device__ __forceinline__ void compact_tile(const uint32_t (&v)[64], uint64_t w
 // stream (OutSliced) or a dense array.  b's slices may be Pici or dense; a
 // slice of b whose header fails its check is flagged and its output slice is
 // not written.
+// The body works on slice q of one call's arguments, so that one launch can
+// also cover the same step of several virtual ranks (k_sliced_batch).
 template <class E, bool HasB, bool OutSliced>
-__global__ void __launch_bounds__(kBlockThreads) k_sliced(SlicedArgs g) {
+__device__ __forceinline__ void sliced_slice(const SlicedArgs& g, uint64_t q) {
     using raw = typename E::raw;
     __shared__ raw stage_all[kWavesPerBlock][E::cap];
     __shared__ uint32_t s_cnt[kWavesPerBlock];
     const uint32_t wave = threadIdx.x >> 6, l = lane_id();
     raw* stage = stage_all[wave];
-    const uint64_t q = blockIdx.x;
     const uint64_t base = q * kSliceElems;
     const uint64_t ns = g.n - base < kSliceElems ? g.n - base : kSliceElems;
     const uint64_t Ts = num_tiles(ns);
@@ -1977,6 +1978,19 @@ __global__ void __launch_bounds__(kBlockThreads) k_sliced(SlicedArgs g) {
     }
 }
 
+template <class E, bool HasB, bool OutSliced>
+__global__ void __launch_bounds__(kBlockThreads) k_sliced(SlicedArgs g) {
+    sliced_slice<E, HasB, OutSliced>(g, blockIdx.x);
+}
+
+// One step of the sliced ring for a batch of virtual ranks: blockIdx.y is
+// the rank, whose arguments are the batch's base arguments with its own dense
+// pointers, threshold and strided streams, trackers and format records.
+template <class E, bool HasB, bool OutSliced>
+__global__ void __launch_bounds__(kBlockThreads) k_sliced_batch(SlicedBatch b) {
+    sliced_slice<E, HasB, OutSliced>(batch_rank(b, blockIdx.y), blockIdx.x);
+}
+
 // Expansion of a sliced stream: one wave per slice (its up to 4 tiles, all
 // reads before the first store).  A slice whose header fails its check is
 // flagged and not written.
@@ -2003,7 +2017,7 @@ __global__ void __launch_bounds__(kBlockThreads) k_expand_sliced(SlicedArgs g) {
 // read on the device; one wave per slot, eight 16-byte loads per lane in
 // flight before their stores, the last partial 16 bytes bytewise.  A slot whose header is not a message that
 // fits is flagged and not copied.
-__global__ void __launch_bounds__(kBlockThreads) k_copy_sliced(SlicedArgs g, uint64_t nslices) {
+__device__ __forceinline__ void copy_slice(const SlicedArgs& g, uint64_t nslices) {
     const uint32_t wave = threadIdx.x >> 6, l = lane_id();
     const uint64_t q = (uint64_t)blockIdx.x * kWavesPerBlock + wave;
     if (q >= nslices) return;
@@ -2028,6 +2042,15 @@ __global__ void __launch_bounds__(kBlockThreads) k_copy_sliced(SlicedArgs g, uin
     }
     const uint32_t tail = (uint32_t)(total & 15u);      // a Pici message ends on an element boundary
     if (l < tail) dst[16ull * nvec + l] = src[16ull * nvec + l];
+}
+
+__global__ void __launch_bounds__(kBlockThreads) k_copy_sliced(SlicedArgs g, uint64_t nslices) {
+    copy_slice(g, nslices);
+}
+
+// The sends of one ring step for a batch of virtual ranks (blockIdx.y).
+__global__ void __launch_bounds__(kBlockThreads) k_copy_sliced_batch(SlicedBatch b, uint64_t nslices) {
+    copy_slice(batch_rank(b, blockIdx.y), nslices);
 }
 
 // ---------------------------------------------------------------------------
@@ -2301,6 +2324,29 @@ void launch_sliced_t(const SlicedArgs& g, int op, hipStream_t st) {
 spccl_status_t launch_sliced_dt(int dtype, const SlicedArgs& g, int op, hipStream_t st) {
     if (dtype == kBF16) launch_sliced_t<BF16>(g, op, st);
     else launch_sliced_t<F32>(g, op, st);
+    return launch_status();
+}
+
+template <class E>
+void launch_sliced_batch_t(const SlicedBatch& b, uint32_t ranks, int op, hipStream_t st) {
+    const dim3 grid((unsigned)num_slices(b.base.n), ranks), block(kBlockThreads);
+    if (op == kSlicedCompress) hipLaunchKernelGGL((k_sliced_batch<E, false, true>), grid, block, 0, st, b);
+    else if (op == kSlicedReduceToSliced) hipLaunchKernelGGL((k_sliced_batch<E, true, true>), grid, block, 0, st, b);
+    else hipLaunchKernelGGL((k_sliced_batch<E, true, false>), grid, block, 0, st, b);
+}
+
+spccl_status_t launch_sliced_batch_dt(int dtype, const SlicedBatch& b, uint32_t ranks, int op, hipStream_t st) {
+    if (ranks == 0 || ranks > (uint32_t)kMaxBatchRanks || op == kSlicedExpand) return SPCCL_ERR_INVALID_ARG;
+    if (dtype == kBF16) launch_sliced_batch_t<BF16>(b, ranks, op, st);
+    else launch_sliced_batch_t<F32>(b, ranks, op, st);
+    return launch_status();
+}
+
+spccl_status_t launch_copy_sliced_batch(const SlicedBatch& b, uint32_t ranks, hipStream_t st) {
+    if (ranks == 0 || ranks > (uint32_t)kMaxBatchRanks) return SPCCL_ERR_INVALID_ARG;
+    const uint64_t S = num_slices(b.base.n);
+    hipLaunchKernelGGL(k_copy_sliced_batch, dim3((unsigned)((S + kWavesPerBlock - 1) / kWavesPerBlock), ranks),
+                       dim3(kBlockThreads), 0, st, b, S);
     return launch_status();
 }
 

@@ -30,10 +30,19 @@
 
 using namespace spccl;
 
+namespace spccl {
+spccl_status_t launch_sliced_batch_dt(int dtype, const SlicedBatch& b, uint32_t ranks, int op, hipStream_t st);
+spccl_status_t launch_copy_sliced_batch(const SlicedBatch& b, uint32_t ranks, hipStream_t st);
+}  // namespace spccl
+
 namespace {
 
 constexpr uint64_t kAlign = 256;
 inline uint64_t round_up(uint64_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+inline bool overlaps(const void* a, uint64_t an, const void* b, uint64_t bn) {
+    const uintptr_t x = reinterpret_cast<uintptr_t>(a), y = reinterpret_cast<uintptr_t>(b);
+    return an && bn && x < y + bn && y < x + an;
+}
 inline hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s); }
 
 struct Layout {
@@ -394,31 +403,65 @@ spccl_status_t spccl_vr_reduce_scatter_sliced(void* const* send, void* const* re
         if (m && hipMemcpyAsync(recv[0], send[0], m * s, hipMemcpyDeviceToDevice, st) != hipSuccess) return SPCCL_ERR_HIP;
         return hipStreamSynchronize(st) == hipSuccess ? SPCCL_OK : SPCCL_ERR_HIP;
     }
+    // the ranks' buffers are read and written by the same launches: no
+    // receive buffer may overlap another receive buffer or any send buffer
+    for (int r = 0; r < P; r++)
+        for (int q = 0; q < P; q++)
+            if (overlaps(recv[r], m * s, send[q], n * s) || (q != r && overlaps(recv[r], m * s, recv[q], m * s)))
+                return SPCCL_ERR_INVALID_ARG;
     SlicedLayout L;
     sliced_need(P, m, dtype, &L, scratch);
     SPCCL_TRY(spccl_workspace_init(L.ws, kWsFlagsOffset, stream));
-    const uint64_t slen = L.S * spccl_slice_bytes(dtype);   // bytes of one sliced stream
+    if (m == 0) return spccl_read_status(L.ws, 1, st);
     auto chunk = [&](int r, int c) { return static_cast<const uint8_t*>(send[r]) + (uint64_t)c * m * s; };
     auto fmt_at = [&](int step, int r) { return L.fmt + ((uint64_t)step * P + r) * L.S; };
-    // step 0: every rank compresses its first chunk and initialises the
-    // trackers of its slices; nothing returns to the host until the end
-    for (int r = 0; r < P; r++)
-        SPCCL_TRY(spccl_compress_sliced_tracked(chunk(r, (r - 1 + P) % P), m, dtype, sliced_tau(pol, r, P),
-                                                L.stream(0, r, P), slen, L.track + 2 * L.S * r, L.track_bytes,
-                                                fmt_at(0, r), L.ws, kWsFlagsOffset, st));
-    for (int step = 1; step <= P - 1; step++) {
-        for (int r = 0; r < P; r++)
-            SPCCL_TRY(spccl_copy_sliced(L.stream(0, (r - 1 + P) % P, P), slen, L.stream(1, r, P), slen, m, dtype,
-                                        L.ws, kWsFlagsOffset, st));
-        for (int r = 0; r < P; r++) {
-            const uint8_t* own = chunk(r, (r - step - 1 + 2 * P) % P);
-            if (step == P - 1)
-                SPCCL_TRY(spccl_reduce_sliced(own, L.stream(1, r, P), slen, recv[r], m * s, 0, 0.0, m, dtype, L.ws,
-                                              kWsFlagsOffset, st));
-            else
-                SPCCL_TRY(spccl_reduce_sliced_tracked(own, L.stream(1, r, P), slen, L.stream(0, r, P), slen,
-                                                      sliced_tau(pol, r, P), L.track + 2 * L.S * r, L.track_bytes,
-                                                      fmt_at(step, r), m, dtype, L.ws, kWsFlagsOffset, st));
+    // Every step runs all ranks in one launch per kernel (up to
+    // kMaxBatchRanks ranks each, grid y = rank): the P reductions of a ring
+    // step are independent, and nothing returns to the host until the end.
+    auto batch = [&](int r0, uint8_t* out0, const uint8_t* b0, double* track0, int32_t track_step, uint8_t* fmt0) {
+        SlicedBatch b{};
+        b.base = SlicedArgs{nullptr, b0, out0, m, slice_slot_bytes(dtype), 0.0, reinterpret_cast<WsCtrl*>(L.ws),
+                            track0, track_step, fmt0};
+        b.b_stride = L.sbytes;
+        b.out_stride = L.sbytes;
+        b.track_stride = 2 * L.S;
+        b.fmt_stride = L.S;
+        (void)r0;
+        return b;
+    };
+    for (int step = 0; step <= P - 1; step++) {
+        for (int r0 = 0; r0 < P; r0 += kMaxBatchRanks) {
+            const int cnt = P - r0 < kMaxBatchRanks ? P - r0 : kMaxBatchRanks;
+            if (step == 0) {
+                // every rank compresses its first chunk and initialises its slices' trackers
+                SlicedBatch b = batch(r0, L.stream(0, r0, P), nullptr, L.track + 2 * L.S * r0, 0, fmt_at(0, r0));
+                for (int j = 0; j < cnt; j++) {
+                    b.a[j] = chunk(r0 + j, (r0 + j - 1 + P) % P);
+                    b.thresh[j] = sliced_tau(pol, r0 + j, P);
+                }
+                SPCCL_TRY(launch_sliced_batch_dt(dtype, b, (uint32_t)cnt, kSlicedCompress, st));
+                continue;
+            }
+            // the sends: rank r receives rank r-1's stream
+            SlicedBatch c = batch(r0, L.stream(1, r0, P), nullptr, nullptr, 0, nullptr);
+            for (int j = 0; j < cnt; j++) c.a[j] = L.stream(0, (r0 + j - 1 + P) % P, P);
+            SPCCL_TRY(launch_copy_sliced_batch(c, (uint32_t)cnt, st));
+        }
+        if (step == 0) continue;
+        for (int r0 = 0; r0 < P; r0 += kMaxBatchRanks) {
+            const int cnt = P - r0 < kMaxBatchRanks ? P - r0 : kMaxBatchRanks;
+            const bool last = step == P - 1;
+            SlicedBatch b = last ? batch(r0, nullptr, L.stream(1, r0, P), nullptr, 0, nullptr)
+                                 : batch(r0, L.stream(0, r0, P), L.stream(1, r0, P), L.track + 2 * L.S * r0, 1,
+                                         fmt_at(step, r0));
+            for (int j = 0; j < cnt; j++) {
+                const int r = r0 + j;
+                b.a[j] = chunk(r, (r - step - 1 + 2 * P) % P);
+                b.thresh[j] = last ? 0.0 : sliced_tau(pol, r, P);
+                if (last) b.out_dense[j] = static_cast<uint8_t*>(recv[r]);
+            }
+            SPCCL_TRY(launch_sliced_batch_dt(dtype, b, (uint32_t)cnt, last ? kSlicedReduceToDense : kSlicedReduceToSliced,
+                                             st));
         }
     }
     if (fmt_trace && hipMemcpyAsync(fmt_trace, L.fmt, (uint64_t)(P - 1) * P * L.S, hipMemcpyDeviceToHost, st) !=

@@ -244,3 +244,29 @@ def test_vr_reduce_scatter_sliced_config3(S_):
     for r in range(P):
         assert np.array_equal(got[r], bits(exp[r])), f"rank {r}"
     assert np.array_equal(gfm, efm)
+
+
+def test_vr_reduce_scatter_sliced_more_ranks_than_one_launch(S_):
+    """P = 40: a ring step's kernels cover 32 ranks per launch, so the step
+    runs as two launches per kernel; values and formats as the oracle's."""
+    P, m = 40, S + 123
+    sends = [W.sparse_array(P * m, int(0.03 * P * m), [82, P, r], W.F32) for r in range(P)]
+    log(f"sliced rs P={P}")
+    got, gfm = run_sliced_rs(S_, sends, O.Policy())
+    exp, efm = O.ring_reduce_scatter_sliced(sends, O.Policy())
+    for r in range(P):
+        assert np.array_equal(got[r], bits(exp[r])), f"rank {r}"
+    assert np.array_equal(gfm, efm)
+
+
+def test_vr_reduce_scatter_sliced_rejects_overlapping_buffers(S_):
+    """The ranks of a step share one launch: a receive buffer inside a send
+    buffer, or two receive buffers that overlap, are argument errors."""
+    P, m = 3, 1000
+    ts = [torch.zeros(P * m, dtype=torch.float32, device="cuda") for _ in range(P)]
+    scratch = torch.empty(S_.spccl_vr_sliced_scratch_bytes(P, m, S_.SPCCL_F32), dtype=torch.uint8, device="cuda")
+    outs = [torch.empty(m, dtype=torch.float32, device="cuda") for _ in range(P)]
+    for bad in ([outs[0], ts[1][:m], outs[2]], [outs[0], outs[0], outs[2]]):
+        with pytest.raises(S_.SpcclError) as e:
+            S_.spccl_vr_reduce_scatter_sliced(ts, bad, scratch)
+        assert S_.STATUS_NAMES[e.value.status] == "ERR_INVALID_ARG"
