@@ -117,6 +117,11 @@ def lib():
         L.orc_ring_all_reduce.restype = i32
         L.orc_ring_all_reduce.argtypes = [ctypes.POINTER(vp), ctypes.POINTER(vp), i32, u64, i32,
                                           ctypes.POINTER(_Policy), ctypes.POINTER(_Trace)]
+        L.orc_ring_all_gather_sliced.restype = i32
+        L.orc_ring_all_gather_sliced.argtypes = [ctypes.POINTER(vp), ctypes.POINTER(vp), i32, u64, i32, vp]
+        L.orc_ring_all_reduce_sliced.restype = i32
+        L.orc_ring_all_reduce_sliced.argtypes = [ctypes.POINTER(vp), ctypes.POINTER(vp), i32, u64, i32,
+                                                 ctypes.POINTER(_Policy), vp, vp]
         _lib = L
     return _lib
 
@@ -448,6 +453,41 @@ def slot_messages(stream: np.ndarray, n: int, dtype: int) -> list:
         m = stream[q * slot:(q + 1) * slot]
         out.append(m[:int(m[40:48].view(np.uint64)[0])])
     return out
+
+
+def ring_all_gather_sliced(parts: list):
+    """All-gather over sliced streams (every slice Pici).  Returns (P outputs
+    of P*n, formats uint8[P, S])."""
+    P = len(parts)
+    parts = [np.ascontiguousarray(p) for p in parts]
+    dt = dtype_code(parts[0])
+    n = parts[0].size
+    S = slice_count(n)
+    outs = [np.empty(P * n, dtype=parts[0].dtype) for _ in range(P)]
+    fm = np.zeros(max(1, P * S), dtype=np.uint8)
+    _check(lib().orc_ring_all_gather_sliced(_ptr_array(parts), _ptr_array(outs), P, n, dt, _ptr(fm)),
+           "ring_all_gather_sliced")
+    return outs, fm[:P * S].reshape(P, S)
+
+
+def ring_all_reduce_sliced(sends: list, policy: Policy | None = None):
+    """All-reduce over sliced streams: the sliced reduce-scatter, then the
+    all-gather with a per-slice dense switch.  Returns (P outputs of n,
+    reduce-scatter formats uint8[P-1, P, S], all-gather formats uint8[P, S]),
+    S = slices of a chunk."""
+    policy = policy or Policy()
+    P = len(sends)
+    sends = [np.ascontiguousarray(s) for s in sends]
+    dt = dtype_code(sends[0])
+    n = sends[0].size
+    S = slice_count(n // P)
+    outs = [np.empty(n, dtype=sends[0].dtype) for _ in range(P)]
+    frs = np.zeros(max(1, (P - 1) * P * S), dtype=np.uint8)
+    fag = np.zeros(max(1, P * S), dtype=np.uint8)
+    pol = policy.c()
+    _check(lib().orc_ring_all_reduce_sliced(_ptr_array(sends), _ptr_array(outs), P, n, dt, ctypes.byref(pol),
+                                            _ptr(frs), _ptr(fag)), "ring_all_reduce_sliced")
+    return outs, frs[:(P - 1) * P * S].reshape(max(P - 1, 0), P, S), fag[:P * S].reshape(P, S)
 
 
 def ring_reduce_scatter_sliced(sends: list, policy: Policy | None = None):

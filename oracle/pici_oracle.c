@@ -712,8 +712,19 @@ done:
  * (formats never change values).  fmt_out (optional) gets the format of
  * every sent slice, indexed [(step * P + rank) * S + q], S = slices of a
  * chunk. */
+static int rs_sliced(const void* const* send, void* const* recv, int P, uint64_t n, int dtype,
+                     const orc_policy_t* pol, uint8_t* fmt_out, double* sig0_out, double* sigp_out);
+
 int orc_ring_reduce_scatter_sliced(const void* const* send, void* const* recv, int P, uint64_t n, int dtype,
                                    const orc_policy_t* pol, uint8_t* fmt_out) {
+    return rs_sliced(send, recv, P, n, dtype, pol, fmt_out, NULL, NULL);
+}
+
+/* The sliced ring reduce-scatter; sig0_out / sigp_out (optional, P * S
+ * doubles each) get every rank's slice trackers as they stand after its last
+ * tracked send (step P - 2). */
+static int rs_sliced(const void* const* send, void* const* recv, int P, uint64_t n, int dtype,
+                     const orc_policy_t* pol, uint8_t* fmt_out, double* sig0_out, double* sigp_out) {
     if (P < 1 || n % (uint64_t)P) return ORC_ERR_INVALID_ARG;
     if (dtype != ORC_F32 && dtype != ORC_BF16) return ORC_ERR_UNSUPPORTED;
     const uint64_t m = n / (uint64_t)P, s = elem_size(dtype);
@@ -770,10 +781,106 @@ int orc_ring_reduce_scatter_sliced(const void* const* send, void* const* recv, i
             }
         }
     }
+    if (sig0_out) memcpy(sig0_out, sig0, sizeof(double) * (size_t)P * (size_t)S);
+    if (sigp_out) memcpy(sigp_out, sigp, sizeof(double) * (size_t)P * (size_t)S);
 done:
     if (out_msg) for (int r = 0; r < P; r++) free(out_msg[r]);
     if (in_msg) for (int r = 0; r < P; r++) free(in_msg[r]);
     free(out_msg); free(in_msg); free(sig0); free(sigp); free(acc); free(tmp);
+    return st;
+}
+
+/* ---- sliced all-gather and all-reduce (Sec. IV-B over the Sec. V-B slice
+ * layout) --------------------------------------------------------------
+ * All-gather: every rank encodes its n-element part once as a sliced stream,
+ * slice q of rank r in format fmt[r * S + q] (dense or Pici), the stream
+ * travels the ring unchanged, and every rank decodes all P parts: out[r]
+ * holds part q at q * n.  Decoding ignores the format, so the values are
+ * those of the plain all-gather. */
+static int ring_all_gather_sliced_fmt(const void* const* part, const uint8_t* fmt, void* const* out, int P,
+                                      uint64_t n, int dtype) {
+    const uint64_t s = elem_size(dtype), S = orc_slice_count(n), slot = orc_slice_bytes(dtype), cap = S * slot;
+    int st = ORC_OK;
+    uint8_t** msg = (uint8_t**)calloc((size_t)P, sizeof(uint8_t*));
+    uint8_t* hop = (uint8_t*)malloc(cap + 1);
+    if (!msg || !hop) { st = ORC_ERR_INVALID_ARG; goto done; }
+    for (int q = 0; q < P; q++) {
+        msg[q] = (uint8_t*)calloc(cap + 1, 1);
+        if (!msg[q]) { st = ORC_ERR_INVALID_ARG; goto done; }
+        for (uint64_t j = 0; j < S; j++) {
+            const uint64_t len = slice_len(n, j);
+            const uint8_t* src = (const uint8_t*)part[q] + j * ORC_SLICE_ELEMS * s;
+            uint64_t nnz = 0;
+            if (fmt[(uint64_t)q * S + j] == ORC_FMT_DENSE) st = orc_encode_dense(src, len, dtype, msg[q] + j * slot, slot);
+            else st = orc_compress(src, len, dtype, msg[q] + j * slot, slot, &nnz);
+            if (st) goto done;
+        }
+    }
+    for (int r = 0; r < P; r++) {
+        memcpy((uint8_t*)out[r] + (uint64_t)r * n * s, part[r], n * s);
+        /* hop k brings rank r the stream of rank r-1-k */
+        for (int k = 0; k < P - 1; k++) {
+            const int q = ((r - 1 - k) % P + P) % P;
+            memcpy(hop, msg[q], cap);
+            st = orc_decode_sliced(hop, cap, (uint8_t*)out[r] + (uint64_t)q * n * s, n, dtype);
+            if (st) goto done;
+        }
+    }
+done:
+    if (msg) for (int q = 0; q < P; q++) free(msg[q]);
+    free(msg); free(hop);
+    return st;
+}
+
+/* Standalone: every slice Pici (the all-gather never densifies).  fmt_out
+ * (optional) gets the P * S slice formats. */
+int orc_ring_all_gather_sliced(const void* const* part, void* const* out, int P, uint64_t n, int dtype,
+                               uint8_t* fmt_out) {
+    if (P < 1) return ORC_ERR_INVALID_ARG;
+    if (dtype != ORC_F32 && dtype != ORC_BF16) return ORC_ERR_UNSUPPORTED;
+    const uint64_t S = orc_slice_count(n);
+    uint8_t* fmt = (uint8_t*)malloc((size_t)(P * S) + 1);
+    if (!fmt) return ORC_ERR_INVALID_ARG;
+    memset(fmt, ORC_FMT_PICI, (size_t)(P * S));
+    int st = ring_all_gather_sliced_fmt(part, fmt, out, P, n, dtype);
+    if (st == ORC_OK && fmt_out) memcpy(fmt_out, fmt, (size_t)(P * S));
+    free(fmt);
+    return st;
+}
+
+/* All-reduce: the sliced reduce-scatter, then the sliced all-gather of the
+ * reduced chunks.  At the transition every slice of a rank's reduced chunk
+ * extrapolates once more from that rank's slice tracker, est = sigma_prev *
+ * sigma0, and goes dense iff est <= ag_thresh (Sec. IV-C per slice; adaptive
+ * 0 / 2 as everywhere).  out[r] gets n elements.  fmt_rs (optional) as
+ * orc_ring_reduce_scatter_sliced; fmt_ag (optional) gets the P * S slice
+ * formats of the all-gather.  P = 1 sends nothing: out[0] = send[0] and the
+ * formats are not written. */
+int orc_ring_all_reduce_sliced(const void* const* send, void* const* out, int P, uint64_t n, int dtype,
+                               const orc_policy_t* pol, uint8_t* fmt_rs, uint8_t* fmt_ag) {
+    if (P < 1 || n % (uint64_t)P) return ORC_ERR_INVALID_ARG;
+    if (dtype != ORC_F32 && dtype != ORC_BF16) return ORC_ERR_UNSUPPORTED;
+    const uint64_t m = n / (uint64_t)P, s = elem_size(dtype), S = orc_slice_count(m);
+    if (P == 1) { memcpy(out[0], send[0], n * s); return ORC_OK; }
+    int st = ORC_ERR_INVALID_ARG;
+    void** red = (void**)calloc((size_t)P, sizeof(void*));
+    double* sig0 = (double*)calloc((size_t)(P * S + 1), sizeof(double));
+    double* sigp = (double*)calloc((size_t)(P * S + 1), sizeof(double));
+    uint8_t* fmt = (uint8_t*)malloc((size_t)(P * S) + 1);
+    if (!red || !sig0 || !sigp || !fmt) goto done;
+    for (int r = 0; r < P; r++) if (!(red[r] = malloc(m * s + 1))) goto done;
+    st = rs_sliced(send, red, P, n, dtype, pol, fmt_rs, sig0, sigp);
+    if (st) goto done;
+    for (int r = 0; r < P; r++)
+        for (uint64_t q = 0; q < S; q++) {
+            const double est = sigp[r * S + q] * sig0[r * S + q];
+            fmt[r * S + q] = (uint8_t)(go_dense(pol, est, pol->ag_thresh) ? ORC_FMT_DENSE : ORC_FMT_PICI);
+        }
+    st = ring_all_gather_sliced_fmt((const void* const*)red, fmt, out, P, m, dtype);
+    if (st == ORC_OK && fmt_ag) memcpy(fmt_ag, fmt, (size_t)(P * S));
+done:
+    if (red) for (int r = 0; r < P; r++) free(red[r]);
+    free(red); free(sig0); free(sigp); free(fmt);
     return st;
 }
 

@@ -144,3 +144,72 @@ def test_sliced_ring_decides_per_slice():
     exp, _ = O.ring_reduce_scatter(sends, O.Policy(adaptive=0))
     for r in range(P):
         assert np.array_equal(got[r], exp[r])
+
+
+@pytest.mark.parametrize("P", [1, 2, 3, 8])
+@pytest.mark.parametrize("dtype", [W.F32, W.BF16])
+def test_sliced_all_gather_equals_the_plain_all_gather(P, dtype):
+    """Formats never change values: the sliced all-gather delivers every
+    part exactly as the plain ring all-gather does, and every slice is Pici
+    (a standalone all-gather does not densify, Sec. IV-C)."""
+    n = 2 * S + 555
+    parts = [W.sparse_array(n, [40, 3000, n // 3][r % 3], [91, P, r], dtype) for r in range(P)]
+    got, fm = O.ring_all_gather_sliced(parts)
+    exp, _ = O.ring_all_gather(parts)
+    for r in range(P):
+        assert np.array_equal(_bits(got[r]), _bits(exp[r])), r
+        for q in range(P):
+            assert np.array_equal(_bits(got[r][q * n:(q + 1) * n]), _bits(parts[q])), (r, q)
+    assert fm.shape == (P, O.slice_count(n)) and (fm == O.FMT_PICI).all()
+
+
+@pytest.mark.parametrize("P", [1, 2, 3, 8])
+@pytest.mark.parametrize("adaptive", [0, 1, 2])
+def test_sliced_all_reduce_values_equal_the_plain_ring(P, adaptive):
+    """Every rank ends with the full left-fold (Sec. IV-B): the plain ring
+    all-reduce's values on every rank, whatever the formats."""
+    m = S + 4097
+    sends = [W.sparse_array(P * m, int(0.05 * P * m), [92, P, r]) for r in range(P)]
+    pol = O.Policy(adaptive=adaptive)
+    got, frs, fag = O.ring_all_reduce_sliced(sends, pol)
+    exp, _ = O.ring_all_reduce(sends, pol)
+    for r in range(P):
+        assert np.array_equal(_bits(got[r]), _bits(exp[r])), r
+        assert np.array_equal(_bits(got[r]), _bits(got[0])), r
+    if P > 1:
+        assert frs.shape == (P - 1, P, O.slice_count(m)) and fag.shape == (P, O.slice_count(m))
+        if adaptive == 0:
+            assert (frs == O.FMT_PICI).all() and (fag == O.FMT_PICI).all()
+        if adaptive == 2:
+            assert (frs == O.FMT_DENSE).all() and (fag == O.FMT_DENSE).all()
+
+
+def test_sliced_all_reduce_transition_per_slice():
+    """Hand-computed decisions (Sec. IV-C, per slice).  Each chunk has two
+    slices.  Slice 0: every rank holds 1 in 100 of it at its own residue, so
+    its sparsity stays near 0.99 - 0.93 and it is Pici everywhere; at the
+    transition est = sigma_prev * sigma0 ~ 0.92 > 0.1: Pici.  Slice 1: 30%
+    nonzeros (sigma0 = 0.7 > 0.6: Pici at step 0), then est = 0.7^(k+1) <=
+    0.6: dense at steps 1-6 (tracking the estimate), and at the transition
+    est = 0.7^7 * 0.7 = 0.0576 <= 0.1: dense."""
+    P, L0, L1 = 8, O.SLICE_ELEMS, 10000
+    m = L0 + L1
+    idx0, idx1 = np.arange(L0), np.arange(L1)
+    sends = []
+    for r in range(P):
+        x = np.zeros(P * m, dtype=np.float32)
+        for c in range(P):
+            j = (r - c) % P or P
+            base = c * m
+            x[base:base + L0][idx0 % 100 == (j - 1)] = 1.0
+            x[base + L0:base + m][(idx1 + 7 * j) % 10 < 3] = 1.0
+        sends.append(x)
+    got, frs, fag = O.ring_all_reduce_sliced(sends, O.Policy())
+    assert (frs[:, :, 0] == O.FMT_PICI).all()
+    for r in range(P):
+        assert frs[:, r, 1].tolist() == [1, 0, 0, 0, 0, 0, 0]
+    assert fag[:, 0].tolist() == [O.FMT_PICI] * P
+    assert fag[:, 1].tolist() == [O.FMT_DENSE] * P
+    exp, _ = O.ring_all_reduce(sends, O.Policy(adaptive=0))
+    for r in range(P):
+        assert np.array_equal(got[r], exp[r])
