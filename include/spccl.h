@@ -374,11 +374,44 @@ spccl_status_t spccl_vr_all_reduce(void* const* send, void* const* recv, int32_t
  * SPCCL_FMT_PICI.  The stream is synchronised once, at the end.  fmt_trace
  * (host, optional) gets the format of every slice sent: (P-1) * P * S bytes,
  * index (step * P + rank) * S + slice, S = spccl_slice_count(n / P). */
+/* Scratch of the sliced collectives (device, 16-byte aligned): msg_elems is
+ * the elements of one rank's message -- n / P for the reduce-scatter and the
+ * all-reduce, n for the all-gather.  0 for an invalid P or dtype. */
 uint64_t spccl_vr_sliced_scratch_bytes(int32_t P, uint64_t msg_elems, int32_t dtype);
 spccl_status_t spccl_vr_reduce_scatter_sliced(void* const* send, void* const* recv, int32_t P, uint64_t n,
                                               int32_t dtype, const spccl_policy_t* policy,
                                               void* scratch, uint64_t scratch_bytes,
                                               uint8_t* fmt_trace, void* stream);
+
+/* Ring all-gather over sliced streams (Sec. IV-B with the Sec. V-B slice
+ * layout): every rank encodes its n-element part send[r] once, every slice
+ * Pici (a standalone all-gather never densifies), and the stream travels the
+ * ring unchanged; recv[r] (P*n elements) gets part q at q*n on every rank,
+ * the same values as spccl_vr_all_gather.  One launch per kernel and hop
+ * for up to 32 ranks; no recv[r] may overlap another rank's recv or any send
+ * (SPCCL_ERR_INVALID_ARG).  Scratch: spccl_vr_sliced_scratch_bytes(P, n,
+ * dtype).  fmt_trace (host, optional) gets the P * S slice formats, index
+ * rank * S + slice, S = spccl_slice_count(n).  Synchronises the stream once,
+ * at the end; P = 1 copies. */
+spccl_status_t spccl_vr_all_gather_sliced(void* const* send, void* const* recv, int32_t P, uint64_t n,
+                                          int32_t dtype, void* scratch, uint64_t scratch_bytes,
+                                          uint8_t* fmt_trace, void* stream);
+
+/* Ring all-reduce over sliced streams: the sliced reduce-scatter (rank r's
+ * reduced chunk lands at r*n/P of recv[r]), then the sliced all-gather of
+ * the reduced chunks.  At the transition every slice extrapolates once more
+ * from its tracker, est = sigma_prev * sigma0, and is gathered densely iff
+ * est <= policy->ag_thresh (Sec. IV-C per slice; adaptive 0: never, 2:
+ * always).  recv[r] gets n elements, the same values as spccl_vr_all_reduce.
+ * Buffer rules as spccl_vr_reduce_scatter_sliced; scratch:
+ * spccl_vr_sliced_scratch_bytes(P, n / P, dtype).  fmt_rs (host, optional):
+ * the reduce-scatter's (P-1) * P * S slice formats as there; fmt_ag (host,
+ * optional): the all-gather's P * S, index rank * S + slice, S =
+ * spccl_slice_count(n / P).  P = 1 copies and writes no formats. */
+spccl_status_t spccl_vr_all_reduce_sliced(void* const* send, void* const* recv, int32_t P, uint64_t n,
+                                          int32_t dtype, const spccl_policy_t* policy,
+                                          void* scratch, uint64_t scratch_bytes,
+                                          uint8_t* fmt_rs, uint8_t* fmt_ag, void* stream);
 
 #ifdef __cplusplus
 }

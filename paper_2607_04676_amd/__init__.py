@@ -41,7 +41,8 @@ EXPORTS = ("spccl_num_tiles", "spccl_pici_bytes", "spccl_stream_bound", "spccl_w
            "spccl_slice_count", "spccl_slice_bytes", "spccl_compress_sliced", "spccl_decompress_sliced",
            "spccl_reduce_sliced", "spccl_copy_sliced", "spccl_coo_bytes", "spccl_message_bound",
            "spccl_compress_coo", "spccl_slice_tracker_bytes", "spccl_compress_sliced_tracked",
-           "spccl_reduce_sliced_tracked", "spccl_vr_sliced_scratch_bytes", "spccl_vr_reduce_scatter_sliced")
+           "spccl_reduce_sliced_tracked", "spccl_vr_sliced_scratch_bytes", "spccl_vr_reduce_scatter_sliced",
+           "spccl_vr_all_gather_sliced", "spccl_vr_all_reduce_sliced")
 
 
 class spccl_operand_t(ctypes.Structure):
@@ -111,6 +112,10 @@ _sigs = {
     "spccl_vr_sliced_scratch_bytes": (_u64, [_i32, _u64, _i32]),
     "spccl_vr_reduce_scatter_sliced": (_i32, [ctypes.POINTER(_vp), ctypes.POINTER(_vp), _i32, _u64, _i32,
                                               ctypes.POINTER(spccl_policy_t), _vp, _u64, _vp, _vp]),
+    "spccl_vr_all_gather_sliced": (_i32, [ctypes.POINTER(_vp), ctypes.POINTER(_vp), _i32, _u64, _i32, _vp, _u64,
+                                          _vp, _vp]),
+    "spccl_vr_all_reduce_sliced": (_i32, [ctypes.POINTER(_vp), ctypes.POINTER(_vp), _i32, _u64, _i32,
+                                          ctypes.POINTER(spccl_policy_t), _vp, _u64, _vp, _vp, _vp]),
 }
 for _name, (_res, _args) in _sigs.items():
     _f = getattr(_lib, _name)
@@ -370,6 +375,32 @@ def spccl_vr_reduce_scatter_sliced(send: list, recv: list, scratch: torch.Tensor
                                                scratch.data_ptr(), _nbytes(scratch), fm.ctypes.data,
                                                _stream(stream)), "spccl_vr_reduce_scatter_sliced")
     return fm[:(P - 1) * P * S].reshape(max(P - 1, 0), P, S)
+
+
+def spccl_vr_all_gather_sliced(send: list, recv: list, scratch: torch.Tensor, stream=None):
+    """Returns the per-slice formats sent, shape (P, S)."""
+    import numpy as np
+    P, n = len(send), send[0].numel()
+    S = spccl_slice_count(n)
+    fm = np.zeros(max(1, P * S), dtype=np.uint8)
+    _check(_lib.spccl_vr_all_gather_sliced(_ptrs(send), _ptrs(recv), P, n, _dt(send[0]), scratch.data_ptr(),
+                                           _nbytes(scratch), fm.ctypes.data, _stream(stream)),
+           "spccl_vr_all_gather_sliced")
+    return fm[:P * S].reshape(P, S)
+
+
+def spccl_vr_all_reduce_sliced(send: list, recv: list, scratch: torch.Tensor, policy=None, stream=None):
+    """Returns the per-slice formats (reduce-scatter (P-1, P, S), all-gather (P, S))."""
+    import numpy as np
+    P, n = len(send), send[0].numel()
+    S = spccl_slice_count(n // P)
+    frs = np.zeros(max(1, (P - 1) * P * S), dtype=np.uint8)
+    fag = np.zeros(max(1, P * S), dtype=np.uint8)
+    pol = _policy(policy)
+    _check(_lib.spccl_vr_all_reduce_sliced(_ptrs(send), _ptrs(recv), P, n, _dt(send[0]), ctypes.byref(pol),
+                                           scratch.data_ptr(), _nbytes(scratch), frs.ctypes.data, fag.ctypes.data,
+                                           _stream(stream)), "spccl_vr_all_reduce_sliced")
+    return frs[:(P - 1) * P * S].reshape(max(P - 1, 0), P, S), fag[:P * S].reshape(P, S)
 
 
 def alloc_sliced(n: int, dtype: int, device="cuda") -> torch.Tensor:

@@ -1995,7 +1995,7 @@ __global__ void __launch_bounds__(kBlockThreads) k_sliced_batch(SlicedBatch b) {
 // reads before the first store).  A slice whose header fails its check is
 // flagged and not written.
 template <class E>
-__global__ void __launch_bounds__(kBlockThreads) k_expand_sliced(SlicedArgs g) {
+__device__ __forceinline__ void expand_slice(const SlicedArgs& g) {
     using raw = typename E::raw;
     __shared__ raw stage_all[kWavesPerBlock][kChunkVals];
     const uint32_t wave = threadIdx.x >> 6;
@@ -2011,6 +2011,17 @@ __global__ void __launch_bounds__(kBlockThreads) k_expand_sliced(SlicedArgs g) {
     }
     expand_tiles<E, kTilesPerPart>(bm, bm + kHeaderBytes, h.fmt, h.nnz, ns, num_tiles(ns), 0,
                                    reinterpret_cast<raw*>(g.out) + base, stage_all[wave], g.ctrl);
+}
+
+template <class E>
+__global__ void __launch_bounds__(kBlockThreads) k_expand_sliced(SlicedArgs g) {
+    expand_slice<E>(g);
+}
+
+// One all-gather hop's expansions for a batch of virtual ranks (blockIdx.y).
+template <class E>
+__global__ void __launch_bounds__(kBlockThreads) k_expand_sliced_batch(SlicedBatch b) {
+    expand_slice<E>(batch_rank(b, blockIdx.y));
 }
 
 // The virtual-rank send of a sliced stream: each slot's header.total_bytes,
@@ -2329,14 +2340,18 @@ spccl_status_t launch_sliced_dt(int dtype, const SlicedArgs& g, int op, hipStrea
 
 template <class E>
 void launch_sliced_batch_t(const SlicedBatch& b, uint32_t ranks, int op, hipStream_t st) {
-    const dim3 grid((unsigned)num_slices(b.base.n), ranks), block(kBlockThreads);
-    if (op == kSlicedCompress) hipLaunchKernelGGL((k_sliced_batch<E, false, true>), grid, block, 0, st, b);
+    const uint64_t S = num_slices(b.base.n);
+    const dim3 grid((unsigned)S, ranks), block(kBlockThreads);
+    if (op == kSlicedExpand)
+        hipLaunchKernelGGL(k_expand_sliced_batch<E>, dim3((unsigned)((S + kWavesPerBlock - 1) / kWavesPerBlock), ranks),
+                           block, 0, st, b);
+    else if (op == kSlicedCompress) hipLaunchKernelGGL((k_sliced_batch<E, false, true>), grid, block, 0, st, b);
     else if (op == kSlicedReduceToSliced) hipLaunchKernelGGL((k_sliced_batch<E, true, true>), grid, block, 0, st, b);
     else hipLaunchKernelGGL((k_sliced_batch<E, true, false>), grid, block, 0, st, b);
 }
 
 spccl_status_t launch_sliced_batch_dt(int dtype, const SlicedBatch& b, uint32_t ranks, int op, hipStream_t st) {
-    if (ranks == 0 || ranks > (uint32_t)kMaxBatchRanks || op == kSlicedExpand) return SPCCL_ERR_INVALID_ARG;
+    if (ranks == 0 || ranks > (uint32_t)kMaxBatchRanks) return SPCCL_ERR_INVALID_ARG;
     if (dtype == kBF16) launch_sliced_batch_t<BF16>(b, ranks, op, st);
     else launch_sliced_batch_t<F32>(b, ranks, op, st);
     return launch_status();

@@ -337,13 +337,13 @@ spccl_status_t spccl_vr_all_reduce(void* const* send, void* const* recv, int32_t
     return finish(L, st);
 }
 
-/* ---- sliced ring reduce-scatter: decisions on the device -------------------- */
+/* ---- sliced ring collectives: decisions on the device ------------------------ */
 
 namespace {
 struct SlicedLayout {
     uint8_t* ws;           // control block
     double* track;         // P trackers of S slices
-    uint8_t* fmt;          // (P-1) * P * S formats
+    uint8_t* fmt;          // (P-1) * P * S reduce-scatter formats, then P * S all-gather formats
     uint8_t* streams;      // 2 * P sliced streams (sent, received)
     uint64_t S, sbytes, track_bytes;
     uint8_t* stream(int which, int r, int P) const { return streams + ((uint64_t)which * P + r) * sbytes; }
@@ -353,7 +353,7 @@ uint64_t sliced_need(int32_t P, uint64_t m, int32_t dtype, SlicedLayout* L, void
     const uint64_t S = spccl_slice_count(m);
     const uint64_t sbytes = round_up(S * spccl_slice_bytes(dtype));
     const uint64_t wsb = round_up(kWsFlagsOffset), trb = round_up(16ull * S * (uint64_t)P),
-                   fmb = round_up((uint64_t)(P > 1 ? P - 1 : 1) * (uint64_t)P * S);
+                   fmb = round_up((uint64_t)P * (uint64_t)P * S);    // reduce-scatter steps, then an all-gather
     if (L) {
         uint8_t* b = static_cast<uint8_t*>(base);
         L->ws = b;
@@ -381,6 +381,118 @@ uint64_t spccl_vr_sliced_scratch_bytes(int32_t P, uint64_t msg_elems, int32_t dt
     return sliced_need(P, msg_elems, dtype, nullptr, nullptr);
 }
 
+namespace {
+
+// Buffers of the sliced collectives: P send buffers of send_elems and P
+// receive buffers of recv_elems elements, element-aligned; no receive
+// buffer may overlap another or any send buffer, because the ranks of a step
+// share one launch.
+spccl_status_t check_sliced_ranks(void* const* send, uint64_t send_elems, void* const* recv, uint64_t recv_elems,
+                                  int32_t P, int32_t dtype, const void* scratch) {
+    const uint64_t s = elem_bytes(dtype);
+    if (!send || !recv || !scratch || (reinterpret_cast<uintptr_t>(scratch) & 15u)) return SPCCL_ERR_INVALID_ARG;
+    const uintptr_t amask = (uintptr_t)s - 1;
+    for (int r = 0; r < P; r++)
+        if (!send[r] || !recv[r] || (reinterpret_cast<uintptr_t>(send[r]) & amask) ||
+            (reinterpret_cast<uintptr_t>(recv[r]) & amask))
+            return SPCCL_ERR_INVALID_ARG;
+    for (int r = 0; r < P; r++)
+        for (int q = 0; q < P; q++)
+            if (overlaps(recv[r], recv_elems * s, send[q], send_elems * s) ||
+                (q != r && overlaps(recv[r], recv_elems * s, recv[q], recv_elems * s)))
+                return SPCCL_ERR_INVALID_ARG;
+    return SPCCL_OK;
+}
+
+SlicedBatch make_batch(const SlicedLayout& L, uint64_t m, int32_t dtype, uint8_t* out0, const uint8_t* b0,
+                       double* track0, int32_t track_step, uint8_t* fmt0) {
+    SlicedBatch b{};
+    b.base = SlicedArgs{nullptr, b0, out0, m, slice_slot_bytes(dtype), 0.0, reinterpret_cast<WsCtrl*>(L.ws), track0,
+                        track_step, fmt0};
+    b.b_stride = L.sbytes;
+    b.out_stride = L.sbytes;
+    b.track_stride = 2 * L.S;
+    b.fmt_stride = L.S;
+    return b;
+}
+
+inline int batch_count(int P, int r0) { return P - r0 < kMaxBatchRanks ? P - r0 : kMaxBatchRanks; }
+
+// The sliced reduce-scatter's steps (m > 0, P > 1): every step is one launch
+// per kernel for up to kMaxBatchRanks ranks (grid y = rank), the P
+// reductions of a ring step being independent; rank r's reduced chunk lands
+// at out[r].  Formats go to L.fmt, step-major.
+spccl_status_t sliced_rs_steps(void* const* send, uint8_t* const* out, int32_t P, uint64_t m, int32_t dtype,
+                               const spccl_policy_t& pol, const SlicedLayout& L, hipStream_t st) {
+    const uint64_t s = elem_bytes(dtype);
+    auto chunk = [&](int r, int c) { return static_cast<const uint8_t*>(send[r]) + (uint64_t)c * m * s; };
+    auto fmt_at = [&](int step, int r) { return L.fmt + ((uint64_t)step * P + r) * L.S; };
+    for (int step = 0; step <= P - 1; step++) {
+        if (step > 0)   // the sends: rank r receives rank r-1's stream
+            for (int r0 = 0; r0 < P; r0 += kMaxBatchRanks) {
+                SlicedBatch c = make_batch(L, m, dtype, L.stream(1, r0, P), nullptr, nullptr, 0, nullptr);
+                for (int j = 0; j < batch_count(P, r0); j++) c.a[j] = L.stream(0, (r0 + j - 1 + P) % P, P);
+                SPCCL_TRY(launch_copy_sliced_batch(c, (uint32_t)batch_count(P, r0), st));
+            }
+        for (int r0 = 0; r0 < P; r0 += kMaxBatchRanks) {
+            const int cnt = batch_count(P, r0);
+            const bool first = step == 0, last = step == P - 1;
+            // step 0 compresses each rank's first chunk and starts its slices'
+            // trackers; later steps reduce the received stream into the own
+            // chunk (Eq. 7 per slice); the last one into the dense output
+            SlicedBatch b = last ? make_batch(L, m, dtype, nullptr, L.stream(1, r0, P), nullptr, 0, nullptr)
+                                 : make_batch(L, m, dtype, L.stream(0, r0, P), first ? nullptr : L.stream(1, r0, P),
+                                              L.track + 2 * L.S * r0, first ? 0 : 1, fmt_at(step, r0));
+            for (int j = 0; j < cnt; j++) {
+                const int r = r0 + j;
+                b.a[j] = chunk(r, (r - step - 1 + 2 * P) % P);
+                b.thresh[j] = last ? 0.0 : sliced_tau(pol, r, P);
+                if (last) b.out_dense[j] = out[r];
+            }
+            SPCCL_TRY(launch_sliced_batch_dt(dtype, b, (uint32_t)cnt,
+                                             first ? kSlicedCompress : (last ? kSlicedReduceToDense : kSlicedReduceToSliced),
+                                             st));
+        }
+    }
+    return SPCCL_OK;
+}
+
+// The sliced all-gather's hops (n_part > 0): stream(0, r) holds rank r's
+// encoded part; rank r expands it into its own place (unless own_in_place:
+// the part is already there), then at hop k receives rank r-k's stream into
+// stream(1, r) and expands it into part r-k of recv[r].  One launch per
+// kernel and hop for up to kMaxBatchRanks ranks.
+spccl_status_t sliced_ag_hops(void* const* recv, int32_t P, uint64_t n_part, int32_t dtype, const SlicedLayout& L,
+                              bool own_in_place, hipStream_t st) {
+    const uint64_t s = elem_bytes(dtype);
+    auto place = [&](int r, int q) { return static_cast<uint8_t*>(recv[r]) + (uint64_t)q * n_part * s; };
+    for (int k = own_in_place ? 1 : 0; k <= P - 1; k++) {
+        for (int r0 = 0; r0 < P; r0 += kMaxBatchRanks) {
+            const int cnt = batch_count(P, r0);
+            if (k > 0) {
+                SlicedBatch c = make_batch(L, n_part, dtype, L.stream(1, r0, P), nullptr, nullptr, 0, nullptr);
+                for (int j = 0; j < cnt; j++) c.a[j] = L.stream(0, (r0 + j - k + P) % P, P);
+                SPCCL_TRY(launch_copy_sliced_batch(c, (uint32_t)cnt, st));
+            }
+            SlicedBatch e = make_batch(L, n_part, dtype, nullptr, nullptr, nullptr, 0, nullptr);
+            for (int j = 0; j < cnt; j++) {
+                const int r = r0 + j;
+                e.a[j] = k == 0 ? L.stream(0, r, P) : L.stream(1, r, P);
+                e.out_dense[j] = place(r, (r - k + P) % P);
+            }
+            SPCCL_TRY(launch_sliced_batch_dt(dtype, e, (uint32_t)cnt, kSlicedExpand, st));
+        }
+    }
+    return SPCCL_OK;
+}
+
+spccl_status_t copy_to_host(void* dst, const void* src, uint64_t bytes, hipStream_t st) {
+    if (!dst || !bytes) return SPCCL_OK;
+    return hipMemcpyAsync(dst, src, bytes, hipMemcpyDeviceToHost, st) == hipSuccess ? SPCCL_OK : SPCCL_ERR_HIP;
+}
+
+}  // namespace
+
 spccl_status_t spccl_vr_reduce_scatter_sliced(void* const* send, void* const* recv, int32_t P, uint64_t n,
                                               int32_t dtype, const spccl_policy_t* policy, void* scratch,
                                               uint64_t scratch_bytes, uint8_t* fmt_trace, void* stream) {
@@ -388,12 +500,7 @@ spccl_status_t spccl_vr_reduce_scatter_sliced(void* const* send, void* const* re
     const uint64_t m = n / (uint64_t)P, s = elem_bytes(dtype);
     if (dtype != SPCCL_F32 && dtype != SPCCL_BF16) return SPCCL_ERR_UNSUPPORTED;
     if (m >= (1ull << 32)) return SPCCL_ERR_UNSUPPORTED;
-    if (!send || !recv || !scratch || (reinterpret_cast<uintptr_t>(scratch) & 15u)) return SPCCL_ERR_INVALID_ARG;
-    const uintptr_t amask = (uintptr_t)s - 1;
-    for (int r = 0; r < P; r++)
-        if (!send[r] || !recv[r] || (reinterpret_cast<uintptr_t>(send[r]) & amask) ||
-            (reinterpret_cast<uintptr_t>(recv[r]) & amask))
-            return SPCCL_ERR_INVALID_ARG;
+    SPCCL_TRY(check_sliced_ranks(send, n, recv, m, P, dtype, scratch));
     const spccl_policy_t pol = policy ? *policy : kDefaultPolicy;
     if (!policy_ok(pol)) return SPCCL_ERR_INVALID_ARG;
     if (pol.sparse_fmt != SPCCL_FMT_PICI) return SPCCL_ERR_UNSUPPORTED;      // slices are Pici or dense
@@ -403,70 +510,88 @@ spccl_status_t spccl_vr_reduce_scatter_sliced(void* const* send, void* const* re
         if (m && hipMemcpyAsync(recv[0], send[0], m * s, hipMemcpyDeviceToDevice, st) != hipSuccess) return SPCCL_ERR_HIP;
         return hipStreamSynchronize(st) == hipSuccess ? SPCCL_OK : SPCCL_ERR_HIP;
     }
-    // the ranks' buffers are read and written by the same launches: no
-    // receive buffer may overlap another receive buffer or any send buffer
-    for (int r = 0; r < P; r++)
-        for (int q = 0; q < P; q++)
-            if (overlaps(recv[r], m * s, send[q], n * s) || (q != r && overlaps(recv[r], m * s, recv[q], m * s)))
-                return SPCCL_ERR_INVALID_ARG;
     SlicedLayout L;
     sliced_need(P, m, dtype, &L, scratch);
     SPCCL_TRY(spccl_workspace_init(L.ws, kWsFlagsOffset, stream));
     if (m == 0) return spccl_read_status(L.ws, 1, st);
-    auto chunk = [&](int r, int c) { return static_cast<const uint8_t*>(send[r]) + (uint64_t)c * m * s; };
-    auto fmt_at = [&](int step, int r) { return L.fmt + ((uint64_t)step * P + r) * L.S; };
-    // Every step runs all ranks in one launch per kernel (up to
-    // kMaxBatchRanks ranks each, grid y = rank): the P reductions of a ring
-    // step are independent, and nothing returns to the host until the end.
-    auto batch = [&](int r0, uint8_t* out0, const uint8_t* b0, double* track0, int32_t track_step, uint8_t* fmt0) {
-        SlicedBatch b{};
-        b.base = SlicedArgs{nullptr, b0, out0, m, slice_slot_bytes(dtype), 0.0, reinterpret_cast<WsCtrl*>(L.ws),
-                            track0, track_step, fmt0};
-        b.b_stride = L.sbytes;
-        b.out_stride = L.sbytes;
-        b.track_stride = 2 * L.S;
-        b.fmt_stride = L.S;
-        (void)r0;
-        return b;
-    };
-    for (int step = 0; step <= P - 1; step++) {
-        for (int r0 = 0; r0 < P; r0 += kMaxBatchRanks) {
-            const int cnt = P - r0 < kMaxBatchRanks ? P - r0 : kMaxBatchRanks;
-            if (step == 0) {
-                // every rank compresses its first chunk and initialises its slices' trackers
-                SlicedBatch b = batch(r0, L.stream(0, r0, P), nullptr, L.track + 2 * L.S * r0, 0, fmt_at(0, r0));
-                for (int j = 0; j < cnt; j++) {
-                    b.a[j] = chunk(r0 + j, (r0 + j - 1 + P) % P);
-                    b.thresh[j] = sliced_tau(pol, r0 + j, P);
-                }
-                SPCCL_TRY(launch_sliced_batch_dt(dtype, b, (uint32_t)cnt, kSlicedCompress, st));
-                continue;
-            }
-            // the sends: rank r receives rank r-1's stream
-            SlicedBatch c = batch(r0, L.stream(1, r0, P), nullptr, nullptr, 0, nullptr);
-            for (int j = 0; j < cnt; j++) c.a[j] = L.stream(0, (r0 + j - 1 + P) % P, P);
-            SPCCL_TRY(launch_copy_sliced_batch(c, (uint32_t)cnt, st));
-        }
-        if (step == 0) continue;
-        for (int r0 = 0; r0 < P; r0 += kMaxBatchRanks) {
-            const int cnt = P - r0 < kMaxBatchRanks ? P - r0 : kMaxBatchRanks;
-            const bool last = step == P - 1;
-            SlicedBatch b = last ? batch(r0, nullptr, L.stream(1, r0, P), nullptr, 0, nullptr)
-                                 : batch(r0, L.stream(0, r0, P), L.stream(1, r0, P), L.track + 2 * L.S * r0, 1,
-                                         fmt_at(step, r0));
-            for (int j = 0; j < cnt; j++) {
-                const int r = r0 + j;
-                b.a[j] = chunk(r, (r - step - 1 + 2 * P) % P);
-                b.thresh[j] = last ? 0.0 : sliced_tau(pol, r, P);
-                if (last) b.out_dense[j] = static_cast<uint8_t*>(recv[r]);
-            }
-            SPCCL_TRY(launch_sliced_batch_dt(dtype, b, (uint32_t)cnt, last ? kSlicedReduceToDense : kSlicedReduceToSliced,
-                                             st));
-        }
+    SPCCL_TRY(sliced_rs_steps(send, reinterpret_cast<uint8_t* const*>(recv), P, m, dtype, pol, L, st));
+    SPCCL_TRY(copy_to_host(fmt_trace, L.fmt, (uint64_t)(P - 1) * P * L.S, st));
+    return spccl_read_status(L.ws, 1, st);
+}
+
+spccl_status_t spccl_vr_all_gather_sliced(void* const* send, void* const* recv, int32_t P, uint64_t n, int32_t dtype,
+                                          void* scratch, uint64_t scratch_bytes, uint8_t* fmt_trace, void* stream) {
+    if (P < 1) return SPCCL_ERR_INVALID_ARG;
+    if (dtype != SPCCL_F32 && dtype != SPCCL_BF16) return SPCCL_ERR_UNSUPPORTED;
+    if (n >= (1ull << 32)) return SPCCL_ERR_UNSUPPORTED;
+    const uint64_t s = elem_bytes(dtype);
+    SPCCL_TRY(check_sliced_ranks(send, n, recv, (uint64_t)P * n, P, dtype, scratch));
+    if (scratch_bytes < sliced_need(P, n, dtype, nullptr, nullptr)) return SPCCL_ERR_WORKSPACE;
+    hipStream_t st = as_stream(stream);
+    if (P == 1) {
+        if (n && hipMemcpyAsync(recv[0], send[0], n * s, hipMemcpyDeviceToDevice, st) != hipSuccess) return SPCCL_ERR_HIP;
+        return hipStreamSynchronize(st) == hipSuccess ? SPCCL_OK : SPCCL_ERR_HIP;
     }
-    if (fmt_trace && hipMemcpyAsync(fmt_trace, L.fmt, (uint64_t)(P - 1) * P * L.S, hipMemcpyDeviceToHost, st) !=
-                         hipSuccess)
-        return SPCCL_ERR_HIP;
+    SlicedLayout L;
+    sliced_need(P, n, dtype, &L, scratch);
+    SPCCL_TRY(spccl_workspace_init(L.ws, kWsFlagsOffset, stream));
+    if (n == 0) return spccl_read_status(L.ws, 1, st);
+    // every rank encodes its part once, every slice Pici (a standalone
+    // all-gather does not densify)
+    for (int r0 = 0; r0 < P; r0 += kMaxBatchRanks) {
+        SlicedBatch b = make_batch(L, n, dtype, L.stream(0, r0, P), nullptr, nullptr, 0, L.fmt + (uint64_t)r0 * L.S);
+        for (int j = 0; j < batch_count(P, r0); j++) {
+            b.a[j] = static_cast<const uint8_t*>(send[r0 + j]);
+            b.thresh[j] = -1.0;
+        }
+        SPCCL_TRY(launch_sliced_batch_dt(dtype, b, (uint32_t)batch_count(P, r0), kSlicedCompress, st));
+    }
+    SPCCL_TRY(sliced_ag_hops(recv, P, n, dtype, L, false, st));
+    SPCCL_TRY(copy_to_host(fmt_trace, L.fmt, (uint64_t)P * L.S, st));
+    return spccl_read_status(L.ws, 1, st);
+}
+
+spccl_status_t spccl_vr_all_reduce_sliced(void* const* send, void* const* recv, int32_t P, uint64_t n, int32_t dtype,
+                                          const spccl_policy_t* policy, void* scratch, uint64_t scratch_bytes,
+                                          uint8_t* fmt_rs, uint8_t* fmt_ag, void* stream) {
+    if (P < 1 || n % (uint64_t)P) return SPCCL_ERR_INVALID_ARG;
+    const uint64_t m = n / (uint64_t)P, s = elem_bytes(dtype);
+    if (dtype != SPCCL_F32 && dtype != SPCCL_BF16) return SPCCL_ERR_UNSUPPORTED;
+    if (m >= (1ull << 32)) return SPCCL_ERR_UNSUPPORTED;
+    SPCCL_TRY(check_sliced_ranks(send, n, recv, n, P, dtype, scratch));
+    const spccl_policy_t pol = policy ? *policy : kDefaultPolicy;
+    if (!policy_ok(pol)) return SPCCL_ERR_INVALID_ARG;
+    if (pol.sparse_fmt != SPCCL_FMT_PICI) return SPCCL_ERR_UNSUPPORTED;
+    if (scratch_bytes < sliced_need(P, m, dtype, nullptr, nullptr)) return SPCCL_ERR_WORKSPACE;
+    hipStream_t st = as_stream(stream);
+    if (P == 1) {
+        if (n && hipMemcpyAsync(recv[0], send[0], n * s, hipMemcpyDeviceToDevice, st) != hipSuccess) return SPCCL_ERR_HIP;
+        return hipStreamSynchronize(st) == hipSuccess ? SPCCL_OK : SPCCL_ERR_HIP;
+    }
+    SlicedLayout L;
+    sliced_need(P, m, dtype, &L, scratch);
+    SPCCL_TRY(spccl_workspace_init(L.ws, kWsFlagsOffset, stream));
+    if (m == 0) return spccl_read_status(L.ws, 1, st);
+    // reduce-scatter: rank r's reduced chunk lands in its own place in recv[r]
+    std::vector<uint8_t*> own(P);
+    for (int r = 0; r < P; r++) own[r] = static_cast<uint8_t*>(recv[r]) + (uint64_t)r * m * s;
+    SPCCL_TRY(sliced_rs_steps(send, own.data(), P, m, dtype, pol, L, st));
+    // transition (Sec. IV-C per slice): est = sigma_prev * sigma0 from the
+    // slice's tracker; the slice is gathered densely iff est <= ag_thresh
+    const double ag_tau = pol.adaptive == 0 ? -1.0 : (pol.adaptive == 2 ? 2.0 : pol.ag_thresh);
+    uint8_t* fmt_ag_dev = L.fmt + (uint64_t)(P - 1) * P * L.S;
+    for (int r0 = 0; r0 < P; r0 += kMaxBatchRanks) {
+        SlicedBatch b = make_batch(L, m, dtype, L.stream(0, r0, P), nullptr, L.track + 2 * L.S * r0, 1,
+                                   fmt_ag_dev + (uint64_t)r0 * L.S);
+        for (int j = 0; j < batch_count(P, r0); j++) {
+            b.a[j] = own[r0 + j];
+            b.thresh[j] = ag_tau;
+        }
+        SPCCL_TRY(launch_sliced_batch_dt(dtype, b, (uint32_t)batch_count(P, r0), kSlicedCompress, st));
+    }
+    SPCCL_TRY(sliced_ag_hops(recv, P, m, dtype, L, true, st));
+    SPCCL_TRY(copy_to_host(fmt_rs, L.fmt, (uint64_t)(P - 1) * P * L.S, st));
+    SPCCL_TRY(copy_to_host(fmt_ag, fmt_ag_dev, (uint64_t)P * L.S, st));
     return spccl_read_status(L.ws, 1, st);
 }
 

@@ -152,6 +152,65 @@ def test_config4_all_gather(S):
         assert np.array_equal(to_host_bits(outs[r]), bits(exp[r])), f"rank {r}"
 
 
+def test_config4_all_gather_sliced(S):
+    """The all-gather workload over sliced streams (every slice Pici)."""
+    P, n = W.CFG4_P, W.CFG4_N
+    log("cfg4 sliced generate")
+    parts = [W.cfg4_rank(r) for r in range(P)]
+    ts = [to_dev(x) for x in parts]
+    outs = [torch.empty(P * n, dtype=torch.bfloat16, device="cuda") for _ in range(P)]
+    scratch = torch.empty(S.spccl_vr_sliced_scratch_bytes(P, n, O.BF16), dtype=torch.uint8, device="cuda")
+    log("cfg4 sliced gpu all-gather")
+    gfm = S.spccl_vr_all_gather_sliced(ts, outs, scratch)
+    log("cfg4 sliced oracle all-gather")
+    exp, efm = O.ring_all_gather_sliced(parts)
+    assert np.array_equal(gfm, efm)
+    for r in range(P):
+        assert np.array_equal(to_host_bits(outs[r]), bits(exp[r])), f"rank {r}"
+
+
+@pytest.mark.timeout(900)
+def test_config5_all_reduce_sliced(S):
+    """The all-reduce workload over sliced streams: per-slice decisions in
+    both phases on the device, checked slice by slice against the oracle."""
+    P = W.CFG5_P
+    log("cfg5 sliced plan")
+    plan = W.cfg5_plan()
+    n = plan.n
+    m = n // P
+    sends = []
+    for r in range(P):
+        log(f"cfg5 sliced generate rank {r}")
+        sends.append(W.cfg5_rank(plan, r))
+    result = {}
+
+    def run_oracle():
+        result["oracle"] = O.ring_all_reduce_sliced(sends)
+
+    th = threading.Thread(target=run_oracle)     # the C oracle releases the GIL
+    th.start()
+    ts = [to_dev(x) for x in sends]
+    outs = [torch.empty(n, dtype=torch.float32, device="cuda") for _ in range(P)]
+    scratch = torch.empty(S.spccl_vr_sliced_scratch_bytes(P, m, O.F32), dtype=torch.uint8, device="cuda")
+    log("cfg5 sliced gpu all-reduce")
+    grs, gag = S.spccl_vr_all_reduce_sliced(ts, outs, scratch)
+    torch.cuda.synchronize()
+    del ts
+    log("cfg5 sliced waiting for the oracle")
+    while th.is_alive():
+        th.join(timeout=20)
+        log("cfg5 sliced oracle still running")
+    exp, ers, eag = result["oracle"]
+    log(f"cfg5 sliced formats: dense slices {int((grs == 0).sum())} of {grs.size} sent in the reduce-scatter, "
+        f"{int((gag == 0).sum())} of {gag.size} in the all-gather")
+    assert np.array_equal(grs, ers)
+    assert np.array_equal(gag, eag)
+    for r in range(P):
+        got = to_host_bits(outs[r])
+        assert np.array_equal(got, bits(exp[r])), f"rank {r}: {first_diff(got, bits(exp[r]))}"
+        outs[r] = None
+
+
 @pytest.mark.timeout(900)
 def test_config5_all_reduce(S):
     P = W.CFG5_P

@@ -270,3 +270,81 @@ def test_vr_reduce_scatter_sliced_rejects_overlapping_buffers(S_):
         with pytest.raises(S_.SpcclError) as e:
             S_.spccl_vr_reduce_scatter_sliced(ts, bad, scratch)
         assert S_.STATUS_NAMES[e.value.status] == "ERR_INVALID_ARG"
+
+
+def run_sliced_ag(lib, parts):
+    P, n = len(parts), parts[0].size
+    dt = O.dtype_code(parts[0])
+    ts = [to_dev(x) for x in parts]
+    outs = [torch.empty(P * n, dtype=torch.bfloat16 if dt else torch.float32, device="cuda") for _ in range(P)]
+    scratch = torch.empty(max(16, lib.spccl_vr_sliced_scratch_bytes(P, n, dt)), dtype=torch.uint8, device="cuda")
+    fm = lib.spccl_vr_all_gather_sliced(ts, outs, scratch)
+    return [to_host_bits(o) for o in outs], fm
+
+
+def run_sliced_ar(lib, sends, policy):
+    P, n = len(sends), sends[0].size
+    dt = O.dtype_code(sends[0])
+    ts = [to_dev(x) for x in sends]
+    outs = [torch.empty(n, dtype=torch.bfloat16 if dt else torch.float32, device="cuda") for _ in range(P)]
+    scratch = torch.empty(max(16, lib.spccl_vr_sliced_scratch_bytes(P, n // P, dt)), dtype=torch.uint8,
+                          device="cuda")
+    frs, fag = lib.spccl_vr_all_reduce_sliced(ts, outs, scratch, policy)
+    return [to_host_bits(o) for o in outs], frs, fag
+
+
+@pytest.mark.parametrize("dtype", [W.F32, W.BF16])
+@pytest.mark.parametrize("P", [1, 2, 3, 8, 40])
+def test_vr_all_gather_sliced_matches_oracle(S_, dtype, P):
+    n = S + 999 if P == 40 else 2 * S + 555
+    parts = [W.sparse_array(n, [40, 3000, n // 3][r % 3], [93, P, r], dtype) for r in range(P)]
+    log(f"sliced ag P={P} dtype={dtype}")
+    got, gfm = run_sliced_ag(S_, parts)
+    exp, efm = O.ring_all_gather_sliced(parts)
+    for r in range(P):
+        assert np.array_equal(got[r], bits(exp[r])), f"rank {r}"
+    if P > 1:
+        assert np.array_equal(gfm, efm)
+
+
+@pytest.mark.parametrize("dtype", [W.F32, W.BF16])
+@pytest.mark.parametrize("P", [1, 2, 3, 8, 40])
+@pytest.mark.parametrize("pol", list(POLICIES))
+def test_vr_all_reduce_sliced_matches_oracle(S_, dtype, P, pol):
+    if P == 40 and (dtype == W.BF16 or pol != "default"):
+        pytest.skip("the 40-rank case runs once, fp32 with the default policy")
+    m = S + 123 if P == 40 else 2 * S + 777
+    frac = [0.5, 0.02, 0.15][P % 3]
+    sends = [W.sparse_array(P * m, int(frac * P * m), [94, P, r], dtype) for r in range(P)]
+    log(f"sliced ar P={P} dtype={dtype} policy={pol}")
+    got, grs, gag = run_sliced_ar(S_, sends, POLICIES[pol])
+    exp, ers, eag = O.ring_all_reduce_sliced(sends, POLICIES[pol])
+    for r in range(P):
+        assert np.array_equal(got[r], bits(exp[r])), f"rank {r}"
+    if P > 1:
+        assert np.array_equal(grs, ers)
+        assert np.array_equal(gag, eag)
+
+
+def test_vr_all_reduce_sliced_transition_per_slice(S_):
+    """The oracle's hand-computed two-slice construction: slice 0 Pici
+    throughout, slice 1 dense from step 1 and gathered densely."""
+    P, L0, L1 = 8, S, 10000
+    m = L0 + L1
+    idx0, idx1 = np.arange(L0), np.arange(L1)
+    sends = []
+    for r in range(P):
+        x = np.zeros(P * m, dtype=np.float32)
+        for c in range(P):
+            j = (r - c) % P or P
+            x[c * m:c * m + L0][idx0 % 100 == (j - 1)] = 1.0
+            x[c * m + L0:(c + 1) * m][(idx1 + 7 * j) % 10 < 3] = 1.0
+        sends.append(x)
+    got, grs, gag = run_sliced_ar(S_, sends, O.Policy())
+    assert (grs[:, :, 0] == O.FMT_PICI).all()
+    for r in range(P):
+        assert grs[:, r, 1].tolist() == [1, 0, 0, 0, 0, 0, 0]
+    assert gag[:, 0].tolist() == [O.FMT_PICI] * P and gag[:, 1].tolist() == [O.FMT_DENSE] * P
+    exp, _, _ = O.ring_all_reduce_sliced(sends, O.Policy())
+    for r in range(P):
+        assert np.array_equal(got[r], bits(exp[r]))
