@@ -450,8 +450,9 @@ def time_collectives(S, torch, reps=3):
     """The emulated reduce-scatter of the P = 8 x 33,554,432 fp32 workload at
     99%: the canonical ring (one global message per step, the host reads the
     step's headers to decide) and the sliced ring (per-slice decisions on
-    the device, one synchronisation at the end).  Wall time per collective,
-    each call synchronizing the stream itself."""
+    the device, one synchronisation at the end); and the all-gather of the
+    P = 8 x 16,777,216 bf16 workload at 99.9% in both forms.  Wall time per
+    collective, each call synchronizing the stream itself."""
     import workloads as W
     P, m = W.CFG3_P, W.CFG3_N // W.CFG3_P
     F = S.SPCCL_F32
@@ -464,17 +465,33 @@ def time_collectives(S, torch, reps=3):
         "sliced_ring_device_decisions_ms": (torch.empty(S.spccl_vr_sliced_scratch_bytes(P, m, F), dtype=torch.uint8,
                                                         device="cuda"), S.spccl_vr_reduce_scatter_sliced),
     }
-    for nm, (scratch, f) in runs.items():
-        f(sends, outs, scratch)
+    def timed(f, *args):
+        f(*args)
         torch.cuda.synchronize()
         t0 = time.perf_counter()
         for _ in range(reps):
-            f(sends, outs, scratch)
+            f(*args)
         torch.cuda.synchronize()
-        res[nm] = round((time.perf_counter() - t0) / reps * 1e3, 3)
+        return round((time.perf_counter() - t0) / reps * 1e3, 3)
+
+    for nm, (scratch, f) in runs.items():
+        res[nm] = timed(f, sends, outs, scratch)
         del scratch
     del sends, outs
     torch.cuda.empty_cache()
+    # the all-gather workload: P = 8 x 16,777,216 bf16 at 99.9%
+    P4, n4, B = W.CFG4_P, W.CFG4_N, S.SPCCL_BF16
+    parts = [torch.from_numpy(W.cfg4_rank(r).view(np.int16)).cuda().view(torch.bfloat16) for r in range(P4)]
+    outs = [torch.empty(P4 * n4, dtype=torch.bfloat16, device="cuda") for _ in range(P4)]
+    ag = {"workload": f"all-gather, P = {P4} x {n4:,} bf16, sigma = 0.999"}
+    scratch = torch.empty(S.spccl_vr_scratch_bytes(P4, n4, B), dtype=torch.uint8, device="cuda")
+    ag["canonical_ring_ms"] = timed(S.spccl_vr_all_gather, parts, outs, scratch)
+    del scratch
+    scratch = torch.empty(S.spccl_vr_sliced_scratch_bytes(P4, n4, B), dtype=torch.uint8, device="cuda")
+    ag["sliced_ring_ms"] = timed(S.spccl_vr_all_gather_sliced, parts, outs, scratch)
+    del scratch, parts, outs
+    torch.cuda.empty_cache()
+    res["all_gather"] = ag
     return res
 
 
