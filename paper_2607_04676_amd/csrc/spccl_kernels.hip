@@ -1891,34 +1891,35 @@ __device__ __forceinline__ void sliced_slice(const SlicedArgs& g, uint64_t q) {
         // header and column words first (both lie inside the slot whatever
         // the header says), then half of a's rows; by then the header is in,
         // and a Pici slice's values are read early, before the other half
-        // These reads stay inside the slot (sized for a full slice) or the
-        // slice's rows (a buffer resource that ends there) whether or not the
-        // wave has a tile, so no branch guards them: one would make the wave
-        // wait for the first reads before issuing the rest.
+        // The slice's header decides the path before any other read: a
+        // dense slice is a dense (+) dense pair, a Pici slice reads half of
+        // a's rows, its values early (once its offsets are in), then the
+        // other half.  The reads stay inside the slot (sized for a full
+        // slice) or the slice's rows (a buffer resource that ends there)
+        // whether or not the wave has a tile, so no branch guards them.
         const uint8_t* bm = g.b + q * g.slot;
-        const HeaderWords hw = load_header_words(bm);
-        const PiciMeta m = load_pici_meta<E>(bm, t, ns);
-        asm volatile("" ::: "memory");
-        fetch_dense<E, true, 0, kEarlySplit>(a, t, ns, v);
-        asm volatile("" ::: "memory");
-        const HeaderView h = check_header(hw, g.slot, ns, E::dtype, -1);
-        const bool pici = h.ok && h.fmt == (uint32_t)kFmtPici;
-        EarlyVals ev = fetch_early<E>(bm, pici ? g.slot : 0ull, ns, m);
-        asm volatile("" ::: "memory");
-        fetch_dense<E, true, kEarlySplit, 64>(a, t, ns, v);
+        const HeaderView h = check_header(load_header_words(bm), g.slot, ns, E::dtype, -1);
         if (!h.ok || h.fmt == (uint32_t)kFmtCoo) {       // the same in every wave of the block
             if (threadIdx.x == 0) set_status(g.ctrl, SPCCL_ERR_CORRUPT_STREAM);
             return;
         }
-        if (has_tile) {
-            if (h.fmt == (uint32_t)kFmtPici) {
+        if (h.fmt != (uint32_t)kFmtPici) {
+            fetch_dense<E, true>(a, t, ns, v);
+            fetch_dense<E, false>(bm + kHeaderBytes, t, ns, v);
+        } else {
+            const PiciMeta m = load_pici_meta<E>(bm, t, ns);
+            asm volatile("" ::: "memory");
+            fetch_dense<E, true, 0, kEarlySplit>(a, t, ns, v);
+            asm volatile("" ::: "memory");
+            const EarlyVals ev = fetch_early<E>(bm, g.slot, ns, m);
+            asm volatile("" ::: "memory");
+            fetch_dense<E, true, kEarlySplit, 64>(a, t, ns, v);
+            if (has_tile) {
                 // a dense output tile that is full takes its rows as they are finished
                 raw* col = (!OutSliced && ns - t * kTileElems >= kTileElems)
                                ? reinterpret_cast<raw*>(g.out) + base + t * kTileElems + l : nullptr;
                 if (expand_pici_early<E, false>(pici_columns(m, h.nnz, t, ns, g.ctrl), ev, bm, ns, stage, v, col))
                     return;
-            } else {
-                fetch_dense<E, false>(bm + kHeaderBytes, t, ns, v);
             }
         }
     } else {
