@@ -571,6 +571,8 @@ def main():
     ap.add_argument("--cpu-budget", type=float, default=10.0)
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--calib", action="store_true", help="also run one large plain copy (counter calibration)")
+    ap.add_argument("--iso-reps", type=int, default=50,
+                    help="repetitions of each op timed on its own; 0 skips them (profiling runs)")
     ap.add_argument("--no-collectives", dest="collectives", action="store_false",
                     help="skip timing the emulated reduce-scatter collectives")
     args = ap.parse_args()
@@ -607,7 +609,7 @@ def main():
             "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(dgbs / HBM_PEAK_GBS, 4),
             "traffic": traffic_for(dom),
             "algorithmic_bytes_per_launch": alg[dom], "avg_launch_ms": round(dom_ms, 5)}
-    isolated = time_isolated(R)
+    isolated = time_isolated(R, args.iso_reps) if args.iso_reps > 0 else None
     # the in-collective (sliced) form of the codec and reduce ops, per op
     SR = SlicedRunner(R)
     for w in range(2):
@@ -616,7 +618,7 @@ def main():
     _, _, per_s, _ = run_steps(SR, max(5, args.steps // 3), args.copies, [op[0] for op in SR.ops(0)])
     alg_s = SR.algorithmic_bytes()
     sliced = {"slice_elems": 16384, "dense_thresh": SR.thresh, "parity_compress_vs_oracle": SR.check_parity(),
-              "kernels": {}, "isolated": time_isolated(SR)}
+              "kernels": {}, "isolated": time_isolated(SR, args.iso_reps) if args.iso_reps > 0 else None}
     for nm, ms in per_s.items():
         gbs = alg_s[nm] / (ms / 1e3) / 1e9
         sliced["kernels"][nm] = {"ms": round(ms, 5), "algorithmic_bytes": alg_s[nm], "achieved_GBs": round(gbs, 1),
@@ -649,7 +651,7 @@ def main():
                              "frac_of_hbm_peak": round(a_s[nm] / (ms / 1e3) / 1e9 / HBM_PEAK_GBS, 4)}
                         for nm, ms in p_s.items()},
             "parity_compress": Rs.check_parity(),
-            "isolated": time_isolated(Rs),
+            "isolated": time_isolated(Rs, args.iso_reps) if args.iso_reps > 0 else None,
         }
         del Rs
         torch.cuda.empty_cache()
