@@ -24,6 +24,8 @@ spccl_status_t launch_fill_zero(void* p, uint64_t bytes, hipStream_t st);
 spccl_status_t launch_encode_dense_dt(int dtype, const uint8_t* src, uint8_t* out, uint64_t n, hipStream_t st);
 spccl_status_t launch_sliced_dt(int dtype, const SlicedArgs& g, int op, hipStream_t st);
 spccl_status_t launch_copy_sliced(const SlicedArgs& g, hipStream_t st);
+spccl_status_t launch_coo_index(const uint8_t* msg, uint64_t cap, uint64_t n, int dtype, uint32_t* idx,
+                                WsCtrl* ctrl, hipStream_t st);
 }  // namespace spccl
 
 using namespace spccl;
@@ -31,9 +33,14 @@ using namespace spccl;
 namespace {
 
 inline bool dtype_ok(int32_t dt) { return dt == kF32 || dt == kBF16; }
-inline uint64_t slots_offset(uint64_t n) { return (kWsFlagsOffset + 8ull * num_parts(n) + 255ull) & ~255ull; }
-// Workspace regions: control block, look-back words, value slots (the
-// two-pass Pici sink and the COO sink), index slots (the COO sink).
+inline uint64_t align256(uint64_t x) { return (x + 255ull) & ~255ull; }
+// Workspace regions: control block, look-back words, the tile indexes of two
+// COO operands, value slots (the two-pass Pici sink and the COO sink), index
+// slots (the COO sink).
+inline uint64_t coo_index_offset(uint64_t n, int which) {
+    return align256(kWsFlagsOffset + 8ull * num_parts(n)) + (uint64_t)which * align256(4ull * (num_tiles(n) + 1));
+}
+inline uint64_t slots_offset(uint64_t n) { return coo_index_offset(n, 2); }
 inline uint64_t value_slots_end(uint64_t n, int32_t dt) {
     return slots_offset(n) + num_parts(n) * kPartElems * elem_bytes(dt);
 }
@@ -116,7 +123,7 @@ uint64_t spccl_stream_bound(uint64_t n, int32_t dtype) {
 
 uint64_t spccl_workspace_min_bytes(uint64_t n, int32_t dtype) {
     (void)dtype;
-    return kWsFlagsOffset + 8ull * num_parts(n);
+    return slots_offset(n);
 }
 
 uint64_t spccl_workspace_bytes(uint64_t n, int32_t dtype) {
@@ -165,10 +172,22 @@ spccl_status_t spccl_compress(const void* dense, uint64_t n, int32_t dtype, void
 
 namespace {
 // The COO sink (three passes; needs the full workspace with its slots).
-spccl_status_t run_coo_sink(const Src& sa, const Src& sb, uint8_t* out, uint64_t n, int32_t dtype, void* ws,
+// A COO operand gets a tile index (k_coo_index) in the workspace when the
+// workspace has room for it (spccl_workspace_min_bytes); otherwise its tiles
+// search J for their entries.  The workspace has been checked.
+spccl_status_t index_coo(Src& s, int which, uint64_t n, int32_t dtype, void* ws, uint64_t ws_bytes, hipStream_t hs) {
+    if (s.kind != SRC_COO || n == 0 || ws_bytes < slots_offset(n)) return SPCCL_OK;
+    uint32_t* idx = reinterpret_cast<uint32_t*>(static_cast<uint8_t*>(ws) + coo_index_offset(n, which));
+    s.dev.idx = idx;
+    return launch_coo_index(s.dev.data, s.dev.cap, n, dtype, idx, static_cast<WsCtrl*>(ws), hs);
+}
+
+spccl_status_t run_coo_sink(Src sa, Src sb, uint8_t* out, uint64_t n, int32_t dtype, void* ws,
                             uint64_t ws_bytes, hipStream_t hs) {
     spccl_status_t st = check_ws(ws, ws_bytes, spccl_workspace_bytes(n, dtype));
     if (st != SPCCL_OK) return st;
+    if ((st = index_coo(sa, 0, n, dtype, ws, ws_bytes, hs)) != SPCCL_OK) return st;
+    if ((st = index_coo(sb, 1, n, dtype, ws, ws_bytes, hs)) != SPCCL_OK) return st;
     PiciSinkArgs g{};
     g.slots = static_cast<uint8_t*>(ws) + slots_offset(n);
     g.idx_slots = reinterpret_cast<uint32_t*>(static_cast<uint8_t*>(ws) + value_slots_end(n, dtype));
@@ -322,6 +341,8 @@ spccl_status_t spccl_reduce(spccl_operand_t a, spccl_operand_t b, spccl_operand_
         return launch_dense_dense_dt(dtype, sa.dev.hdr, sa.dev.data, sa.dev.cap, sb.dev.hdr, sb.dev.data,
                                      sb.dev.cap, out_hdr, out_data, n, ctrl, hs);
     if (n == 0 && !out_hdr) return SPCCL_OK;
+    if ((st = index_coo(sa, 0, n, dtype, ws, ws_bytes, hs)) != SPCCL_OK) return st;
+    if ((st = index_coo(sb, 1, n, dtype, ws, ws_bytes, hs)) != SPCCL_OK) return st;
     DenseSinkArgs g{};
     g.a = sa.dev;
     g.b = sb.dev;

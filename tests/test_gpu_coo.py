@@ -135,16 +135,20 @@ def test_reduce_coo_operand_kinds(S, n, dtype, ka, kb):
         keep = []
         ga, gb = _gpu_operand(S, a, ka, keep), _gpu_operand(S, b, kb, keep)
         oa, ob = _oracle_operand(a, ka), _oracle_operand(b, kb)
-        for out_kind in ("array", "coo", "dense_msg"):
+        for out_kind in ("array", "array_search", "coo", "dense_msg"):
             log(f"coo reduce n={n} {dtype} {ka}+{kb}->{out_kind} fill=({fa},{fb})")
-            if out_kind == "array":
+            if out_kind.startswith("array"):
+                # a full workspace builds a tile index of each COO operand; one
+                # of only the control block makes the tiles search J instead
+                wsk = ws if out_kind == "array" else torch.zeros(256, dtype=torch.uint8, device="cuda")
                 out = torch.empty(n, dtype=tdt(dtype), device="cuda")
                 out.fill_(9.0)
-                S.spccl_reduce(ga, gb, S.operand(out), n, dt, ws)
+                S.spccl_reduce(ga, gb, S.operand(out), n, dt, wsk)
                 torch.cuda.synchronize()
                 exp = O.reduce(oa, ob, n, dt)
                 got = to_host_bits(out)
                 assert np.array_equal(got, bits(exp)), first_diff(got, bits(exp))
+                assert S.spccl_read_status(wsk) == 0
             else:
                 fmt = S.SPCCL_FMT_COO if out_kind == "coo" else S.SPCCL_FMT_DENSE
                 out = S.alloc_stream(n, dt, fmt=S.SPCCL_FMT_COO)
@@ -224,6 +228,7 @@ def test_corrupt_coo_flagged(S):
     msg, nnz = O.compress_coo(a)
     J = msg[48:48 + 4 * nnz].view(np.uint32).copy()
     ws = S.alloc_workspace(n, O.F32)
+    small = torch.zeros(256, dtype=torch.uint8, device="cuda")       # the control block only: no tile index
     out = torch.empty(n, dtype=torch.float32, device="cuda")
     dense_out = torch.empty(n, dtype=torch.float32, device="cuda")
     coo_out = S.alloc_stream(n, O.F32, fmt=S.SPCCL_FMT_COO)
@@ -241,10 +246,11 @@ def test_corrupt_coo_flagged(S):
         log(f"corrupt coo {name}: decompress")
         S.spccl_decompress(tb, out, ws)
         assert S.spccl_read_status(ws, clear=True) == 4, name
-        log(f"corrupt coo {name}: dense + coo -> dense")
-        S.spccl_reduce(S.operand(to_dev(a)), S.operand(tb, S.SPCCL_STREAM, S.SPCCL_FMT_COO), S.operand(dense_out),
-                       n, O.F32, ws)
-        assert S.spccl_read_status(ws, clear=True) == 4, name
+        log(f"corrupt coo {name}: dense + coo -> dense (tile index, then search)")
+        for wsk in (ws, small):
+            S.spccl_reduce(S.operand(to_dev(a)), S.operand(tb, S.SPCCL_STREAM, S.SPCCL_FMT_COO),
+                           S.operand(dense_out), n, O.F32, wsk)
+            assert S.spccl_read_status(wsk, clear=True) == 4, name
         log(f"corrupt coo {name}: coo + dense -> coo")
         S.spccl_reduce(S.operand(tb, S.SPCCL_STREAM, S.SPCCL_FMT_COO), S.operand(to_dev(a)),
                        S.operand(coo_out, S.SPCCL_STREAM, S.SPCCL_FMT_COO), n, O.F32, ws)
