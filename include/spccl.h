@@ -114,14 +114,15 @@ uint64_t spccl_stream_bound(uint64_t n, int32_t dtype);
 
 /* Workspace for messages of up to n elements: a 256-byte control block
  * (the sticky device status), one 64-bit look-back word per partition of
- * 16384 elements, two tile indexes of COO operands (one 32-bit word per
+ * 16384 elements, two tile indexes of COO operands (one 64-bit word per
  * 4096-element tile plus one, each), one worst-case slot of compacted values
  * per partition (n elements' worth) and one of 32-bit indices (COO outputs).
  * spccl_workspace_min_bytes covers the first three regions.  A reduce whose
  * workspace holds them gives each COO operand a tile index (the first entry
- * of every tile, built from J by one extra pass) so its tiles find their
- * entries without searching J; a smaller workspace (at least the control
- * block, for a reduce into a dense result) makes them search.  With the
+ * of every tile, tagged with the call, built from J by one extra pass) so its
+ * tiles find their entries without searching J; tiles the index leaves out
+ * (long runs of empty tiles) and every tile of a reduce with a smaller
+ * workspace (at least the control block, for a dense result) search.  With the
  * value slots, Pici-producing calls run as two passes that never wait while
  * holding input data (count and park values, then resolve offsets by
  * look-back and move); a workspace of only spccl_workspace_min_bytes selects

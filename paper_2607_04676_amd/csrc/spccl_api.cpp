@@ -24,8 +24,8 @@ spccl_status_t launch_fill_zero(void* p, uint64_t bytes, hipStream_t st);
 spccl_status_t launch_encode_dense_dt(int dtype, const uint8_t* src, uint8_t* out, uint64_t n, hipStream_t st);
 spccl_status_t launch_sliced_dt(int dtype, const SlicedArgs& g, int op, hipStream_t st);
 spccl_status_t launch_copy_sliced(const SlicedArgs& g, hipStream_t st);
-spccl_status_t launch_coo_index(const uint8_t* msg, uint64_t cap, uint64_t n, int dtype, uint32_t* idx,
-                                WsCtrl* ctrl, hipStream_t st);
+spccl_status_t launch_coo_index(const uint8_t* msg, uint64_t cap, uint64_t n, int dtype, uint64_t* idx,
+                                uint32_t epoch, WsCtrl* ctrl, hipStream_t st);
 }  // namespace spccl
 
 using namespace spccl;
@@ -38,7 +38,7 @@ inline uint64_t align256(uint64_t x) { return (x + 255ull) & ~255ull; }
 // COO operands, value slots (the two-pass Pici sink and the COO sink), index
 // slots (the COO sink).
 inline uint64_t coo_index_offset(uint64_t n, int which) {
-    return align256(kWsFlagsOffset + 8ull * num_parts(n)) + (uint64_t)which * align256(4ull * (num_tiles(n) + 1));
+    return align256(kWsFlagsOffset + 8ull * num_parts(n)) + (uint64_t)which * align256(8ull * (num_tiles(n) + 1));
 }
 inline uint64_t slots_offset(uint64_t n) { return coo_index_offset(n, 2); }
 inline uint64_t value_slots_end(uint64_t n, int32_t dt) {
@@ -177,9 +177,12 @@ namespace {
 // search J for their entries.  The workspace has been checked.
 spccl_status_t index_coo(Src& s, int which, uint64_t n, int32_t dtype, void* ws, uint64_t ws_bytes, hipStream_t hs) {
     if (s.kind != SRC_COO || n == 0 || ws_bytes < slots_offset(n)) return SPCCL_OK;
-    uint32_t* idx = reinterpret_cast<uint32_t*>(static_cast<uint8_t*>(ws) + coo_index_offset(n, which));
+    uint64_t* idx = reinterpret_cast<uint64_t*>(static_cast<uint8_t*>(ws) + coo_index_offset(n, which));
+    uint32_t epoch = next_epoch();
+    if (epoch == 0) epoch = next_epoch();      // a zeroed workspace holds epoch-0 words
     s.dev.idx = idx;
-    return launch_coo_index(s.dev.data, s.dev.cap, n, dtype, idx, static_cast<WsCtrl*>(ws), hs);
+    s.dev.idx_epoch = epoch;
+    return launch_coo_index(s.dev.data, s.dev.cap, n, dtype, idx, epoch, static_cast<WsCtrl*>(ws), hs);
 }
 
 spccl_status_t run_coo_sink(Src sa, Src sb, uint8_t* out, uint64_t n, int32_t dtype, void* ws,

@@ -62,7 +62,9 @@ struct DevOperand {
     const uint8_t* hdr;    // message header, or nullptr for a raw array
     const uint8_t* data;   // raw array base, or the message base for Pici / COO
     uint64_t cap;          // capacity of the message buffer in bytes
-    const uint32_t* idx;   // COO: idx[t] = first entry of tile t (T + 1 words, k_coo_index), or nullptr: search J
+    const uint64_t* idx;   // COO: idx[t] = epoch << 32 | first entry of tile t (T + 1 words, k_coo_index),
+                           // or nullptr: search J
+    uint32_t idx_epoch;    // the epoch of this call's index words; a tile whose words carry another searches J
 };
 
 struct PiciSinkArgs {

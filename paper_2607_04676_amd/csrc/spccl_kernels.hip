@@ -662,25 +662,32 @@ __device__ bool coo_range_ok(const uint32_t* J, uint32_t lo, uint32_t hi, uint64
 }
 
 // Tile t of a checked COO message (nnz entries) added into v.  Its entry
-// range comes from the message's tile index when the call built one (idx,
-// see k_coo_index), else it is searched for; a range that fits one chunk is
-// checked as it is loaded, a larger one is checked in a pass of its own before
-// any entry is used; then the entries are applied a chunk at a time (a row
-// split between chunks gets its columns from both).  A tile that fails the
-// checks is flagged and adds nothing.
+// range comes from the message's tile index when the call built one and both
+// of the tile's index words carry the call's epoch (see k_coo_index), else it
+// is searched for; a range that fits one chunk is checked as it is loaded, a
+// larger one is checked in a pass of its own before any entry is used; then
+// the entries are applied a chunk at a time (a row split between chunks gets
+// its columns from both).  A tile that fails the checks is flagged and adds
+// nothing.
 template <class E>
-__device__ void coo_tile(const uint8_t* msg, uint64_t nnz, const uint32_t* idx, uint64_t t, uint64_t n,
-                         typename E::raw* stage, CooLds* cl, WsCtrl* ctrl, uint32_t (&v)[64]) {
+__device__ void coo_tile(const uint8_t* msg, uint64_t nnz, const uint64_t* idx, uint32_t epoch, uint64_t t,
+                         uint64_t n, typename E::raw* stage, CooLds* cl, WsCtrl* ctrl, uint32_t (&v)[64]) {
     using raw = typename E::raw;
     const uint32_t* J = reinterpret_cast<const uint32_t*>(msg + kHeaderBytes);
     const raw* V = reinterpret_cast<const raw*>(msg + coo_off_V(nnz));
     const uint64_t T = num_tiles(n);
     const uint64_t t0 = t * kTileElems, tlim = t0 + kTileElems < n ? t0 + kTileElems : n;
-    uint32_t lo, hi;
+    uint32_t lo = 0, hi = 0;
+    bool indexed = false;
     if (idx) {
-        lo = __builtin_amdgcn_readfirstlane(idx[t]);
-        hi = __builtin_amdgcn_readfirstlane(idx[t + 1]);
-    } else {
+        const uint64_t wl = idx[t], wh = idx[t + 1];
+        const uint32_t el = __builtin_amdgcn_readfirstlane((uint32_t)(wl >> 32));
+        const uint32_t eh = __builtin_amdgcn_readfirstlane((uint32_t)(wh >> 32));
+        indexed = el == epoch && eh == epoch;
+        lo = __builtin_amdgcn_readfirstlane((uint32_t)wl);
+        hi = __builtin_amdgcn_readfirstlane((uint32_t)wh);
+    }
+    if (!indexed) {
         const uint64_t key = (lane_id() < 32 ? t : t + 1) * kTileElems;
         const uint32_t b = coo_lower_bound<2>(J, 0u, (uint32_t)nnz, key);
         lo = lane_bcast(b, 0);
@@ -784,7 +791,7 @@ __device__ __forceinline__ bool load_tile_pair(const DevOperand& a, const DevOpe
 #pragma unroll
                 for (int r = 0; r < 64; r++) v[r] = 0;
             }
-            coo_tile<E>(a.data, nnza, a.idx, t, n, stage, cl, ctrl, v);
+            coo_tile<E>(a.data, nnza, a.idx, a.idx_epoch, t, n, stage, cl, ctrl, v);
         }
         if constexpr (early_b) {
             const bool st = expand_pici_early<E, false>(pici_columns(mb, nnzb, t, n, ctrl), ev, b.data, n, stage, v,
@@ -798,7 +805,7 @@ __device__ __forceinline__ bool load_tile_pair(const DevOperand& a, const DevOpe
 #pragma unroll
                 for (int r = 0; r < 64; r++) v[r] = 0;
             }
-            coo_tile<E>(b.data, nnzb, b.idx, t, n, stage, cl, ctrl, v);
+            coo_tile<E>(b.data, nnzb, b.idx, b.idx_epoch, t, n, stage, cl, ctrl, v);
         }
     }
     return true;
@@ -1400,21 +1407,27 @@ __global__ void __launch_bounds__(kBlockThreads) k_place(PiciSinkArgs g) {
 }
 
 // ---------------------------------------------------------------------------
-// Tile index of a COO message: idx[t] = the first entry whose index is
-// >= 4096 t, for t = 0 .. T (idx[T] = nnz).  One thread per entry i (and one
-// for the end, i = nnz) writes the tiles between its predecessor's tile and
-// its own, so every tile is written exactly once by a valid message and the
-// index is read in one pass over J.  Entries that are not strictly increasing
-// or not below n are flagged (the tiles that use the index check their
-// entries again, so a bad index can only drop work that is flagged anyway).
+// Tile index of a COO message: idx[t] = epoch << 32 | the first entry whose
+// index is >= 4096 t, for t = 0 .. T (idx[T] = nnz).  One thread per entry i
+// (and one for the end, i = nnz) writes the tiles between its predecessor's
+// tile and its own -- at most the last kIdxSpan of them, so a corrupt J that
+// jumps back and forth cannot make a thread write the whole index -- and the
+// index is read in one pass over J.  Tiles left unwritten keep words of an
+// earlier epoch (or none) and search J instead, so the index only ever saves
+// work: in a valid message every written word is exact.  Entries that are not
+// strictly increasing or not below n are flagged (the tiles check their
+// entries again as they use them).
+constexpr uint64_t kIdxSpan = 64;
+
 __global__ void __launch_bounds__(256) k_coo_index(const uint8_t* msg, uint64_t cap, uint64_t n, int dtype,
-                                                  uint32_t* idx, WsCtrl* ctrl) {
+                                                  uint64_t* idx, uint32_t epoch, WsCtrl* ctrl) {
     const HeaderView h = read_header(msg, cap, n, dtype, kFmtCoo);
     if (!h.ok) {
         if (blockIdx.x == 0 && threadIdx.x == 0) set_status(ctrl, SPCCL_ERR_CORRUPT_STREAM);
         return;
     }
     const uint64_t T = num_tiles(n), nnz = h.nnz;
+    const uint64_t tag = (uint64_t)epoch << 32;
     const uint32_t* J = reinterpret_cast<const uint32_t*>(msg + kHeaderBytes);
     for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i <= nnz;
          i += (uint64_t)gridDim.x * blockDim.x) {
@@ -1422,10 +1435,11 @@ __global__ void __launch_bounds__(256) k_coo_index(const uint8_t* msg, uint64_t 
         const uint64_t prev = i > 0 ? J[i - 1] : 0;
         if (i < nnz && (cur >= n || (i > 0 && cur <= prev))) set_status(ctrl, SPCCL_ERR_CORRUPT_STREAM);
         // tiles (tile(prev), tile(cur)] start at entry i (all of [0, tile(cur)] for the first)
-        const uint64_t first = i > 0 ? prev / kTileElems + 1 : 0;
+        uint64_t first = i > 0 ? prev / kTileElems + 1 : 0;
         uint64_t last = i < nnz ? cur / kTileElems : T;
         if (last > T) last = T;
-        for (uint64_t t = first; t <= last; t++) idx[t] = (uint32_t)i;
+        if (last >= kIdxSpan && first < last - kIdxSpan + 1) first = last - kIdxSpan + 1;
+        for (uint64_t t = first; t <= last; t++) idx[t] = tag | i;
     }
 }
 
@@ -2431,10 +2445,10 @@ spccl_status_t launch_copy_sliced_batch(const SlicedBatch& b, uint32_t ranks, hi
 }
 
 // nnz <= n, and the kernel strides over the grid
-spccl_status_t launch_coo_index(const uint8_t* msg, uint64_t cap, uint64_t n, int dtype, uint32_t* idx,
-                                WsCtrl* ctrl, hipStream_t st) {
+spccl_status_t launch_coo_index(const uint8_t* msg, uint64_t cap, uint64_t n, int dtype, uint64_t* idx,
+                                uint32_t epoch, WsCtrl* ctrl, hipStream_t st) {
     const dim3 grid(stream_grid(n + 1, 256, 4096)), block(256);
-    hipLaunchKernelGGL(k_coo_index, grid, block, 0, st, msg, cap, n, dtype, idx, ctrl);
+    hipLaunchKernelGGL(k_coo_index, grid, block, 0, st, msg, cap, n, dtype, idx, epoch, ctrl);
     return launch_status();
 }
 

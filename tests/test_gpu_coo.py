@@ -267,6 +267,38 @@ def test_corrupt_coo_flagged(S):
     assert_bytes_equal(got, msg, "after errors")
 
 
+def test_coo_tile_index_gaps_and_zigzag(S):
+    """The tile index leaves runs of more than 64 empty tiles to the search
+    of J, and a corrupt J that jumps back and forth costs a bounded pass."""
+    n = 300 * 4096 + 123
+    ws = S.alloc_workspace(n, O.F32)
+    out = torch.empty(n, dtype=torch.float32, device="cuda")
+    a = make(n, 2000, [70], W.F32)
+    for name, keep in (("first and last tiles", lambda i: (i < 3 * 4096) | (i >= 290 * 4096)),
+                       ("one entry in the middle", lambda i: i == 150 * 4096 + 7),
+                       ("no entries", lambda i: i < 0)):
+        b = make(n, 5000, [71], W.F32)
+        b[~keep(np.arange(n))] = 0
+        msg, _ = O.compress_coo(b)
+        log(f"coo index gaps: {name}")
+        S.spccl_reduce(S.operand(to_dev(a)), S.operand(torch.from_numpy(msg).cuda(), S.SPCCL_STREAM,
+                       S.SPCCL_FMT_COO), S.operand(out), n, O.F32, ws)
+        torch.cuda.synchronize()
+        assert S.spccl_read_status(ws, clear=True) == 0, name
+        exp = O.reduce(O.Operand.array(a), O.Operand.stream(msg), n, O.F32)
+        assert np.array_equal(to_host_bits(out), bits(exp)), name
+    b = make(n, 4096, [72], W.F32)
+    msg, nnz = O.compress_coo(b)
+    J = msg[48:48 + 4 * nnz].view(np.uint32).copy()
+    J[1::2] = n - 1 - np.arange(J[1::2].size, dtype=np.uint32)      # every other entry jumps to the end
+    bad = _coo_with(msg, J)
+    assert O.validate(bad, n, O.F32) == O.ERR_CORRUPT_STREAM
+    log("coo index zigzag")
+    S.spccl_reduce(S.operand(to_dev(a)), S.operand(torch.from_numpy(bad).cuda(), S.SPCCL_STREAM, S.SPCCL_FMT_COO),
+                   S.operand(out), n, O.F32, ws)
+    assert S.spccl_read_status(ws, clear=True) == 4
+
+
 def test_coo_host_errors(S):
     n = 4096
     a = to_dev(make(n, 10, [68], W.F32))
