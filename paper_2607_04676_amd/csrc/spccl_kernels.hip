@@ -557,16 +557,15 @@ __device__ __forceinline__ bool coo_load(const uint32_t* J, const typename E::ra
 // stage position; then lane c reads row r's value at rf[r] + (set bits of
 // rw[r] below c).  (An all-zero v takes the entries exactly: zero is the
 // identity of the reduction.)
-template <class E>
-__device__ __forceinline__ void coo_apply(const uint32_t (&x)[kCooSlots], const uint32_t (&y)[kCooSlots],
-                                          uint32_t m, uint64_t t, const typename E::raw* stage, CooLds* cl,
-                                          uint32_t (&v)[64]) {
+template <class E, int S>
+__device__ __forceinline__ void coo_apply(const uint32_t (&x)[S], const uint32_t (&y)[S], uint32_t m, uint64_t t,
+                                          const typename E::raw* stage, CooLds* cl, uint32_t (&v)[64]) {
     const uint32_t l = lane_id();
     const uint64_t t0 = t * kTileElems;
     cl->rw[l] = 0ull;
     wave_lds_sync();
 #pragma unroll
-    for (int q = 0; q < kCooSlots; q++) {
+    for (int q = 0; q < S; q++) {
         const uint32_t i = l + 64 * q;
         if (i < m && x[q] >= t0 && x[q] < t0 + kTileElems) {
             const uint32_t loc = (uint32_t)(x[q] - t0), r = loc >> 6;
@@ -710,6 +709,101 @@ __device__ void coo_tile(const uint8_t* msg, uint64_t nnz, const uint64_t* idx, 
     if (!ok && lane_id() == 0) set_status(ctrl, SPCCL_ERR_CORRUPT_STREAM);
 }
 
+// Early entries of a COO tile combined with dense rows.  The tile's entry
+// range comes from the call's tile index, which lives in the workspace and
+// needs no header, so when the range holds at most kCooEarly entries they are
+// read into registers while the dense rows are in flight.  The header that
+// places V is checked only afterwards, so these reads go through buffer
+// resources that end at the message's capacity (and the index's through one
+// that is empty without an index); the entries are used only once the header
+// and both index words have checked out.
+constexpr int kCooEarlySlots = 2;
+constexpr uint32_t kCooEarly = 64 * kCooEarlySlots;
+
+struct CooEarly {
+    uint32_t x[kCooEarlySlots];     // index l + 64 q of the range
+    uint32_t val[kCooEarlySlots];   // its value's bits
+    uint32_t lo, hi;                // the range, from the index
+    bool ok;                        // both index words carry the call's epoch and the range fits
+};
+
+// The tile's index words (issue first: the range is needed mid-way).
+__device__ __forceinline__ void coo_index_words(const DevOperand& c, uint64_t t, uint64_t T, uint32_t (&w)[4]) {
+    const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint64_t*>(c.idx), (short)0, c.idx ? (int)(8 * (T + 1)) : 0, kBufferWord3);
+    const uint32_t o = (uint32_t)(8 * t);
+#pragma unroll
+    for (int k = 0; k < 4; k++) w[k] = __builtin_amdgcn_raw_buffer_load_b32(rs, o + 4 * k, 0, 0);
+}
+
+template <class E>
+__device__ __forceinline__ CooEarly fetch_coo_early(const DevOperand& c, const HeaderWords& hw,
+                                                    const uint32_t (&w)[4]) {
+    using raw = typename E::raw;
+    CooEarly e;
+    const uint32_t lo = __builtin_amdgcn_readfirstlane(w[0]), el = __builtin_amdgcn_readfirstlane(w[1]);
+    const uint32_t hi = __builtin_amdgcn_readfirstlane(w[2]), eh = __builtin_amdgcn_readfirstlane(w[3]);
+    e.lo = lo;
+    e.hi = hi;
+    e.ok = c.idx != nullptr && el == c.idx_epoch && eh == c.idx_epoch && hi >= lo && hi - lo <= kCooEarly;
+    const uint64_t m = e.ok ? hi - lo : 0u;
+    const uint64_t js = kHeaderBytes + 4ull * lo, vs = hw.w[4] + (uint64_t)lo * sizeof(raw);
+    const uint64_t ja = c.cap > js ? c.cap - js : 0ull, va = c.cap > vs ? c.cap - vs : 0ull;
+    const uint32_t jb = (uint32_t)(4 * m < ja ? 4 * m : ja), vb = (uint32_t)(m * sizeof(raw) < va ? m * sizeof(raw) : va);
+    const __amdgpu_buffer_rsrc_t rj = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint8_t*>(c.data) + (jb ? js : 0ull), (short)0, (int)jb, kBufferWord3);
+    const __amdgpu_buffer_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint8_t*>(c.data) + (vb ? vs : 0ull), (short)0, (int)vb, kBufferWord3);
+    uint32_t lj = lane_id() * 4u, lv = lane_id() * (uint32_t)sizeof(raw);
+    asm volatile("" : "+v"(lj), "+v"(lv));
+#pragma unroll
+    for (int q = 0; q < kCooEarlySlots; q++) {
+        e.x[q] = __builtin_amdgcn_raw_buffer_load_b32(rj, lj + 256 * q, 0, kStreamLoad);
+        if constexpr (sizeof(raw) == 4)
+            e.val[q] = __builtin_amdgcn_raw_buffer_load_b32(rv, lv + 64 * sizeof(raw) * q, 0, kStreamLoad);
+        else
+            e.val[q] = __builtin_amdgcn_raw_buffer_load_b16(rv, lv + 64 * sizeof(raw) * q, 0, kStreamLoad);
+    }
+    return e;
+}
+
+// v (+)= tile t of a checked COO message from its early entries when they
+// cover the tile, else as coo_tile does.  The early range gets coo_tile's
+// checks: its place in the message, and every entry inside the tile and
+// above its predecessor.
+template <class E>
+__device__ void coo_tile_early(const DevOperand& c, uint64_t nnz, const CooEarly& e, uint64_t t, uint64_t n,
+                               typename E::raw* stage, CooLds* cl, WsCtrl* ctrl, uint32_t (&v)[64]) {
+    if (!e.ok) {
+        coo_tile<E>(c.data, nnz, c.idx, c.idx_epoch, t, n, stage, cl, ctrl, v);
+        return;
+    }
+    const uint32_t l = lane_id();
+    const uint64_t T = num_tiles(n);
+    const uint64_t t0 = t * kTileElems, tlim = t0 + kTileElems < n ? t0 + kTileElems : n;
+    const uint32_t lo = e.lo, hi = e.hi, m = hi - lo;
+    const bool ok = hi <= nnz && (t > 0 || lo == 0) && (t + 1 < T || hi == nnz);
+    uint32_t y[kCooEarlySlots];
+    bool bad = false;
+#pragma unroll
+    for (int q = 0; q < kCooEarlySlots; q++) {
+        // the predecessor of entry l + 64 q: lane l - 1's, or lane 63's of the slot before
+        const uint32_t up = __shfl_up(e.x[q], 1);
+        const uint32_t wrap = q > 0 ? __shfl(e.x[q > 0 ? q - 1 : 0], 63) : 0u;
+        y[q] = l > 0 ? up : wrap;
+        const uint32_t i = l + 64 * q;
+        if (i < m) {
+            stage[i] = (typename E::raw)e.val[q];
+            bad = bad || e.x[q] < t0 || e.x[q] >= tlim || (i > 0 && e.x[q] <= y[q]);
+        }
+    }
+    if (!ok || __any(bad)) {
+        if (l == 0) set_status(ctrl, SPCCL_ERR_CORRUPT_STREAM);
+        return;
+    }
+    coo_apply<E>(e.x, y, m, t, stage, cl, v);
+}
+
 // Tile t of a (+) b into v[64] (sources: dense rows or Pici tiles; b may be
 // absent).  Every read that needs no header -- the headers themselves, dense
 // rows, Pici column words and offsets -- is issued first; the headers are
@@ -737,7 +831,11 @@ __device__ __forceinline__ bool load_tile_pair(const DevOperand& a, const DevOpe
     // between the two halves of the dense rows
     constexpr bool early_a = SA == SRC_PICI && SB == SRC_DENSE;
     constexpr bool early_b = SA == SRC_DENSE && SB == SRC_PICI;
+    // one dense and one COO operand: the COO tile's entries likewise
+    constexpr bool coo_early_a = SA == SRC_COO && SB == SRC_DENSE;
+    constexpr bool coo_early_b = SA == SRC_DENSE && SB == SRC_COO;
     EarlyVals ev{{0u}, kNotEarly};
+    CooEarly ce{};
     if (has_tile) {
         if constexpr (SA == SRC_PICI) ma = load_pici_meta<E>(a.data, t, n);
         if constexpr (SB == SRC_PICI) mb = load_pici_meta<E>(b.data, t, n);
@@ -749,6 +847,16 @@ __device__ __forceinline__ bool load_tile_pair(const DevOperand& a, const DevOpe
             ev = early_b ? fetch_early<E>(b.data, b.cap, n, mb) : fetch_early<E>(a.data, a.cap, n, ma);
             asm volatile("" ::: "memory");
             fetch_dense<E, true, kEarlySplit, 64>(d, t, n, v);
+        } else if constexpr (coo_early_a || coo_early_b) {
+            const DevOperand& c = coo_early_b ? b : a;
+            uint32_t iw[4];
+            coo_index_words(c, t, num_tiles(n), iw);
+            asm volatile("" ::: "memory");
+            fetch_dense<E, true, 0, kEarlySplit>(coo_early_b ? a.data : b.data, t, n, v);
+            asm volatile("" ::: "memory");
+            ce = fetch_coo_early<E>(c, coo_early_b ? hwb : hwa, iw);
+            asm volatile("" ::: "memory");
+            fetch_dense<E, true, kEarlySplit, 64>(coo_early_b ? a.data : b.data, t, n, v);
         } else {
             if constexpr (SA == SRC_DENSE && SB == SRC_NONE) {
                 fetch_dense_paced<E>(a.data, t, n, v);
@@ -791,7 +899,10 @@ __device__ __forceinline__ bool load_tile_pair(const DevOperand& a, const DevOpe
 #pragma unroll
                 for (int r = 0; r < 64; r++) v[r] = 0;
             }
-            coo_tile<E>(a.data, nnza, a.idx, a.idx_epoch, t, n, stage, cl, ctrl, v);
+            if constexpr (coo_early_a)
+                coo_tile_early<E>(a, nnza, ce, t, n, stage, cl, ctrl, v);
+            else
+                coo_tile<E>(a.data, nnza, a.idx, a.idx_epoch, t, n, stage, cl, ctrl, v);
         }
         if constexpr (early_b) {
             const bool st = expand_pici_early<E, false>(pici_columns(mb, nnzb, t, n, ctrl), ev, b.data, n, stage, v,
@@ -805,7 +916,10 @@ __device__ __forceinline__ bool load_tile_pair(const DevOperand& a, const DevOpe
 #pragma unroll
                 for (int r = 0; r < 64; r++) v[r] = 0;
             }
-            coo_tile<E>(b.data, nnzb, b.idx, b.idx_epoch, t, n, stage, cl, ctrl, v);
+            if constexpr (coo_early_b)
+                coo_tile_early<E>(b, nnzb, ce, t, n, stage, cl, ctrl, v);
+            else
+                coo_tile<E>(b.data, nnzb, b.idx, b.idx_epoch, t, n, stage, cl, ctrl, v);
         }
     }
     return true;
