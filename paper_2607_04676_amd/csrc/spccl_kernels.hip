@@ -556,10 +556,13 @@ __device__ __forceinline__ bool coo_load(const uint32_t* J, const typename E::ra
 // and, for the first entry of a row among the loaded ones, records the row's
 // stage position; then lane c reads row r's value at rf[r] + (set bits of
 // rw[r] below c).  (An all-zero v takes the entries exactly: zero is the
-// identity of the reduction.)
+// identity of the reduction.)  With col (this lane's column of a full dense
+// output tile, when these are the tile's last entries) each row is also
+// stored as soon as it is final.
 template <class E, int S>
 __device__ __forceinline__ void coo_apply(const uint32_t (&x)[S], const uint32_t (&y)[S], uint32_t m, uint64_t t,
-                                          const typename E::raw* stage, CooLds* cl, uint32_t (&v)[64]) {
+                                          const typename E::raw* stage, CooLds* cl, uint32_t (&v)[64],
+                                          typename E::raw* col = nullptr) {
     const uint32_t l = lane_id();
     const uint64_t t0 = t * kTileElems;
     cl->rw[l] = 0ull;
@@ -577,12 +580,14 @@ __device__ __forceinline__ void coo_apply(const uint32_t (&x)[S], const uint32_t
     const uint64_t myrw = cl->rw[l];
     const uint32_t myrf = cl->rf[l];
     wave_lds_sync();
+    const uint64_t rows = __ballot(myrw != 0ull);          // rows holding entries: one scalar test per row
 #pragma unroll
     for (int r = 0; r < 64; r++) {
-        const uint64_t w = ((uint64_t)lane_bcast((uint32_t)(myrw >> 32), r) << 32) | lane_bcast((uint32_t)myrw, r);
-        if (w != 0ull) {
+        if ((rows >> r) & 1ull) {
+            const uint64_t w = ((uint64_t)lane_bcast((uint32_t)(myrw >> 32), r) << 32) | lane_bcast((uint32_t)myrw, r);
             if ((w >> l) & 1ull) v[r] = oplus(E{}, v[r], (uint32_t)stage[lane_bcast(myrf, r) + bits_below_lane(w)]);
         }
+        if (col) col[64 * r] = (typename E::raw)v[r];
     }
     wave_lds_sync();
 }
@@ -770,13 +775,15 @@ __device__ __forceinline__ CooEarly fetch_coo_early(const DevOperand& c, const H
 // v (+)= tile t of a checked COO message from its early entries when they
 // cover the tile, else as coo_tile does.  The early range gets coo_tile's
 // checks: its place in the message, and every entry inside the tile and
-// above its predecessor.
+// above its predecessor.  With col (see coo_apply) the rows of an early tile
+// are also stored; returns whether they were.
 template <class E>
-__device__ void coo_tile_early(const DevOperand& c, uint64_t nnz, const CooEarly& e, uint64_t t, uint64_t n,
-                               typename E::raw* stage, CooLds* cl, WsCtrl* ctrl, uint32_t (&v)[64]) {
+__device__ bool coo_tile_early(const DevOperand& c, uint64_t nnz, const CooEarly& e, uint64_t t, uint64_t n,
+                               typename E::raw* stage, CooLds* cl, WsCtrl* ctrl, uint32_t (&v)[64],
+                               typename E::raw* col = nullptr) {
     if (!e.ok) {
         coo_tile<E>(c.data, nnz, c.idx, c.idx_epoch, t, n, stage, cl, ctrl, v);
-        return;
+        return false;
     }
     const uint32_t l = lane_id();
     const uint64_t T = num_tiles(n);
@@ -799,9 +806,10 @@ __device__ void coo_tile_early(const DevOperand& c, uint64_t nnz, const CooEarly
     }
     if (!ok || __any(bad)) {
         if (l == 0) set_status(ctrl, SPCCL_ERR_CORRUPT_STREAM);
-        return;
+        return false;
     }
-    coo_apply<E>(e.x, y, m, t, stage, cl, v);
+    coo_apply<E>(e.x, y, m, t, stage, cl, v, col);
+    return col != nullptr;
 }
 
 // Tile t of a (+) b into v[64] (sources: dense rows or Pici tiles; b may be
@@ -899,9 +907,10 @@ __device__ __forceinline__ bool load_tile_pair(const DevOperand& a, const DevOpe
 #pragma unroll
                 for (int r = 0; r < 64; r++) v[r] = 0;
             }
-            if constexpr (coo_early_a)
-                coo_tile_early<E>(a, nnza, ce, t, n, stage, cl, ctrl, v);
-            else
+            if constexpr (coo_early_a) {
+                const bool st = coo_tile_early<E>(a, nnza, ce, t, n, stage, cl, ctrl, v, col);
+                if (stored) *stored = st;
+            } else
                 coo_tile<E>(a.data, nnza, a.idx, a.idx_epoch, t, n, stage, cl, ctrl, v);
         }
         if constexpr (early_b) {
@@ -916,9 +925,10 @@ __device__ __forceinline__ bool load_tile_pair(const DevOperand& a, const DevOpe
 #pragma unroll
                 for (int r = 0; r < 64; r++) v[r] = 0;
             }
-            if constexpr (coo_early_b)
-                coo_tile_early<E>(b, nnzb, ce, t, n, stage, cl, ctrl, v);
-            else
+            if constexpr (coo_early_b) {
+                const bool st = coo_tile_early<E>(b, nnzb, ce, t, n, stage, cl, ctrl, v, col);
+                if (stored) *stored = st;
+            } else
                 coo_tile<E>(b.data, nnzb, b.idx, b.idx_epoch, t, n, stage, cl, ctrl, v);
         }
     }
