@@ -2194,26 +2194,32 @@ __global__ void __launch_bounds__(kBlockThreads) k_sliced_batch(SlicedBatch b) {
     sliced_slice<E, HasB, OutSliced>(batch_rank(b, blockIdx.y), blockIdx.x);
 }
 
-// Expansion of a sliced stream: one wave per slice (its up to 4 tiles, all
-// reads before the first store).  A slice whose header fails its check is
-// flagged and not written.
+// Expansion of a sliced stream: two waves per slice, each expanding two of
+// its up to 4 tiles with all reads before the first store (as the gather
+// does; one wave for all four was slower).  A slice whose header fails its
+// check is flagged and not written.
+constexpr uint32_t kExpandWavesPerSlice = 2;
+
 template <class E>
 __device__ __forceinline__ void expand_slice(const SlicedArgs& g) {
     using raw = typename E::raw;
+    constexpr uint32_t K = kTilesPerPart / kExpandWavesPerSlice;
     __shared__ raw stage_all[kWavesPerBlock][kChunkVals];
     const uint32_t wave = threadIdx.x >> 6;
-    const uint64_t q = (uint64_t)blockIdx.x * kWavesPerBlock + wave;
+    const uint64_t wq = (uint64_t)blockIdx.x * kWavesPerBlock + wave;
+    const uint64_t q = wq / kExpandWavesPerSlice, t0 = K * (wq % kExpandWavesPerSlice);
     if (q >= num_slices(g.n)) return;
     const uint64_t base = q * kSliceElems;
     const uint64_t ns = g.n - base < kSliceElems ? g.n - base : kSliceElems;
+    if (t0 >= num_tiles(ns)) return;                      // a short last slice
     const uint8_t* bm = g.a + q * g.slot;
     const HeaderView h = check_header(load_header_words(bm), g.slot, ns, E::dtype, -1);
     if (!h.ok || h.fmt == (uint32_t)kFmtCoo) {           // slices are Pici or dense
         if (lane_id() == 0) set_status(g.ctrl, SPCCL_ERR_CORRUPT_STREAM);
         return;
     }
-    expand_tiles<E, kTilesPerPart>(bm, bm + kHeaderBytes, h.fmt, h.nnz, ns, num_tiles(ns), 0,
-                                   reinterpret_cast<raw*>(g.out) + base, stage_all[wave], g.ctrl);
+    expand_tiles<E, K>(bm, bm + kHeaderBytes, h.fmt, h.nnz, ns, num_tiles(ns), t0,
+                       reinterpret_cast<raw*>(g.out) + base, stage_all[wave], g.ctrl);
 }
 
 template <class E>
@@ -2532,7 +2538,8 @@ void launch_sliced_t(const SlicedArgs& g, int op, hipStream_t st) {
     if (op == kSlicedCompress) hipLaunchKernelGGL((k_sliced<E, false, true>), dim3(S), block, 0, st, g);
     else if (op == kSlicedReduceToSliced) hipLaunchKernelGGL((k_sliced<E, true, true>), dim3(S), block, 0, st, g);
     else if (op == kSlicedReduceToDense) hipLaunchKernelGGL((k_sliced<E, true, false>), dim3(S), block, 0, st, g);
-    else hipLaunchKernelGGL(k_expand_sliced<E>, dim3((S + kWavesPerBlock - 1) / kWavesPerBlock), block, 0, st, g);
+    else hipLaunchKernelGGL(k_expand_sliced<E>,
+                            dim3((S * kExpandWavesPerSlice + kWavesPerBlock - 1) / kWavesPerBlock), block, 0, st, g);
 }
 
 spccl_status_t launch_sliced_dt(int dtype, const SlicedArgs& g, int op, hipStream_t st) {
@@ -2546,7 +2553,8 @@ void launch_sliced_batch_t(const SlicedBatch& b, uint32_t ranks, int op, hipStre
     const uint64_t S = num_slices(b.base.n);
     const dim3 grid((unsigned)S, ranks), block(kBlockThreads);
     if (op == kSlicedExpand)
-        hipLaunchKernelGGL(k_expand_sliced_batch<E>, dim3((unsigned)((S + kWavesPerBlock - 1) / kWavesPerBlock), ranks),
+        hipLaunchKernelGGL(k_expand_sliced_batch<E>,
+                           dim3((unsigned)((S * kExpandWavesPerSlice + kWavesPerBlock - 1) / kWavesPerBlock), ranks),
                            block, 0, st, b);
     else if (op == kSlicedCompress) hipLaunchKernelGGL((k_sliced_batch<E, false, true>), grid, block, 0, st, b);
     else if (op == kSlicedReduceToSliced) hipLaunchKernelGGL((k_sliced_batch<E, true, true>), grid, block, 0, st, b);
