@@ -47,7 +47,8 @@ def make(n, frac, seed, dtype):
     return raw.view(x.dtype)
 
 
-SIZES = [1, 4097, S, S + 1, 3 * S + 777, 37 * 4096 + 123]
+# last slices of 1, 2, 3 and 4 tiles, full and partial (an expansion covers a slice with two waves of two tiles)
+SIZES = [1, 4097, S, S + 1, 3 * S + 777, 37 * 4096 + 123, 2 * S + 2 * 4096 + 5, 2 * S + 3 * 4096]
 
 
 @pytest.mark.parametrize("n", SIZES)
