@@ -153,7 +153,12 @@ def _nbytes(t: torch.Tensor) -> int:
 
 
 def operand(t: torch.Tensor, kind: int = SPCCL_ARRAY, fmt: int = SPCCL_FMT_DENSE) -> spccl_operand_t:
-    return spccl_operand_t(kind, fmt, t.data_ptr(), _nbytes(t))
+    """The C operand of a device tensor.  It holds a reference to the tensor,
+    so an operand made from a temporary keeps that memory alive as long as
+    the operand itself."""
+    o = spccl_operand_t(kind, fmt, t.data_ptr(), _nbytes(t))
+    o._tensor = t
+    return o
 
 
 # ---- sizes --------------------------------------------------------------------------

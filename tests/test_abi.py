@@ -97,3 +97,22 @@ def test_vr_argument_checks_on_host(S):
     assert lib.spccl_vr_reduce_scatter(ptrs, outs, P, 4096, 0, ctypes.byref(pol), 1 << 30, 16, None, None) == 5
     need = S.spccl_vr_scratch_bytes(P, 1024, 0)
     assert need >= 3 * P * O.stream_bound(1024, O.F32)
+
+
+def test_operand_keeps_its_tensor_alive(S):
+    """An operand built from a temporary tensor holds it: the memory behind the
+    operand's pointer is not released (and reused by the next allocation)
+    while the operand is still in use."""
+    import gc
+    import weakref
+    torch = pytest.importorskip("torch")
+    t = torch.arange(8, dtype=torch.float32)
+    ref = weakref.ref(t)
+    op = S.operand(t)
+    ptr = t.data_ptr()
+    del t
+    gc.collect()
+    assert ref() is not None and op.ptr == ptr
+    del op
+    gc.collect()
+    assert ref() is None

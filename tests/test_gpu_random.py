@@ -1,0 +1,92 @@
+"""Seeded random parity cases: sizes from one element to several hundred
+thousand (partial tiles and slices), densities from empty to full, both
+dtypes, exact cancellations, and every producer and reduce form -- canonical
+Pici, COO and sliced -- against the oracle, bit for bit."""
+import numpy as np
+import pytest
+
+import oracle as O
+import workloads as W
+from helpers import bits, first_diff, log, to_dev, to_host_bits
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+DENSITIES = [0.0, 0.001, 0.01, 0.1, 0.5, 1.0]
+
+
+@pytest.fixture(scope="module")
+def S():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2607_04676_amd as S
+    return S
+
+
+def case(i):
+    rng = np.random.default_rng([91, i])
+    dtype = [W.F32, W.BF16][int(rng.integers(2))]
+    n = int([rng.integers(1, 5000), rng.integers(1, 70000), rng.integers(1, 400000)][int(rng.integers(3))])
+    fa, fb = float(rng.choice(DENSITIES)), float(rng.choice(DENSITIES))
+    a = W.sparse_array(n, int(round(fa * n)), [91, i, 0], dtype)
+    b = W.sparse_array(n, int(round(fb * n)), [91, i, 1], dtype)
+    if rng.integers(3) == 0:                       # b holds -a at a quarter of a's places: exact cancellations
+        ia = np.flatnonzero(bits(a) != 0)
+        if ia.size:
+            pick = rng.choice(ia, size=max(1, ia.size // 4), replace=False)
+            bits(b)[pick] = bits(a)[pick] ^ (0x8000 if dtype == W.BF16 else 0x80000000)
+    return dtype, n, fa, fb, a, b
+
+
+@pytest.mark.parametrize("i", range(24))
+def test_random_case(S, i):
+    dtype, n, fa, fb, a, b = case(i)
+    dt = O.F32 if dtype == W.F32 else O.BF16
+    log(f"random case {i}: n={n} {dtype} densities {fa} {fb}")
+    ws = S.alloc_workspace(n, dt)
+    tdt = torch.float32 if dt == O.F32 else torch.bfloat16
+    P = lambda t: S.operand(t, S.SPCCL_STREAM, S.SPCCL_FMT_PICI)
+    C = lambda t: S.operand(t, S.SPCCL_STREAM, S.SPCCL_FMT_COO)
+    exp = O.reduce(O.Operand.array(a), O.Operand.array(b), n, dt)
+    da, db = to_dev(a), to_dev(b)
+    out = torch.empty(n, dtype=tdt, device="cuda")
+
+    ma, mb, mo = S.alloc_stream(n, dt), S.alloc_stream(n, dt), S.alloc_stream(n, dt)
+    S.spccl_compress(da, ma, ws)
+    S.spccl_compress(db, mb, ws)
+    for x, m in ((a, ma), (b, mb)):
+        e = O.compress(x)[0]
+        assert np.array_equal(m[:e.size].cpu().numpy(), e), "compress"
+    e_sum = O.compress(exp)[0]
+    for name, oa, ob in (("Pici+Pici", P(ma), P(mb)), ("dense+Pici", S.operand(da), P(mb)),
+                         ("Pici+dense", P(ma), S.operand(db))):
+        S.spccl_reduce(oa, ob, P(mo), n, dt, ws)
+        assert np.array_equal(mo[:e_sum.size].cpu().numpy(), e_sum), name + " -> Pici"
+        S.spccl_reduce(oa, ob, S.operand(out), n, dt, ws)
+        got = to_host_bits(out)
+        assert np.array_equal(got, bits(exp)), name + " -> dense: " + first_diff(got, bits(exp))
+
+    ca, cb, co = (S.alloc_stream(n, dt, fmt=S.SPCCL_FMT_COO) for _ in range(3))
+    S.spccl_compress_coo(da, ca, ws)
+    S.spccl_compress_coo(db, cb, ws)
+    e = O.compress_coo(a)[0]
+    assert np.array_equal(ca[:e.size].cpu().numpy(), e), "compress_coo"
+    e_sum = O.compress_coo(exp)[0]
+    for name, oa, ob in (("COO+COO", C(ca), C(cb)), ("dense+COO", S.operand(da), C(cb)),
+                         ("COO+dense", C(ca), S.operand(db))):
+        S.spccl_reduce(oa, ob, C(co), n, dt, ws)
+        assert np.array_equal(co[:e_sum.size].cpu().numpy(), e_sum), name + " -> COO"
+        S.spccl_reduce(oa, ob, S.operand(out), n, dt, ws)
+        got = to_host_bits(out)
+        assert np.array_equal(got, bits(exp)), name + " -> dense: " + first_diff(got, bits(exp))
+
+    sa, sb, so = S.alloc_sliced(n, dt), S.alloc_sliced(n, dt), S.alloc_sliced(n, dt)
+    S.spccl_compress_sliced(da, sa, ws, 0.6)
+    S.spccl_compress_sliced(db, sb, ws, 0.6)
+    S.spccl_decompress_sliced(sa, out, ws)
+    assert np.array_equal(to_host_bits(out), bits(a)), "sliced round trip"
+    S.spccl_reduce_sliced(da, sb, so, ws, True, 0.6)
+    S.spccl_decompress_sliced(so, out, ws)
+    got = to_host_bits(out)
+    assert np.array_equal(got, bits(exp)), "sliced reduce: " + first_diff(got, bits(exp))
+    assert S.spccl_read_status(ws) == 0
