@@ -541,7 +541,10 @@ done:
  * entries (step = trace_step). */
 static int ring_all_gather_fmt(const void* const* part, const int* fmt, void* const* out, int P, uint64_t n,
                                int dtype, orc_trace_t* trace, int trace_step, const double* sig_track) {
-    const uint64_t s = elem_size(dtype), cap = orc_message_bound(n, dtype, ORC_FMT_COO);
+    /* a part goes out dense, Pici or COO: room for the largest of the three
+     * (COO's bound is the larger one except for short parts) */
+    const uint64_t s = elem_size(dtype), cp = orc_message_bound(n, dtype, ORC_FMT_PICI),
+                   cc = orc_message_bound(n, dtype, ORC_FMT_COO), cap = cp > cc ? cp : cc;
     int st = ORC_OK;
     uint8_t** msg = (uint8_t**)calloc((size_t)P, sizeof(uint8_t*));
     uint8_t* hop = (uint8_t*)malloc(cap);

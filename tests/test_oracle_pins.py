@@ -326,6 +326,22 @@ def test_formats_never_change_values():
         assert np.array_equal(outs[0][r], outs[0][0])     # every rank's result is identical
 
 
+@pytest.mark.parametrize("dtype", [W.F32, W.BF16])
+@pytest.mark.parametrize("m", [1, 80, 102, 700])
+def test_formats_never_change_values_short_chunks(dtype, m):
+    """Short chunks, where a Pici message is larger than a COO one: every
+    policy and send format gives the same all-reduce."""
+    P = 5
+    sends = [W.sparse_array(P * m, [0, P * m, P * m // 3, 1, P * m // 10][r], [10, r, m], dtype) for r in range(P)]
+    pols = [O.Policy(adaptive=a) for a in (0, 1, 2)] + [O.Policy.coo(), O.Policy.coo(adaptive=0)]
+    outs = [O.ring_all_reduce(sends, p)[0] for p in pols]
+    for o in outs[1:]:
+        for r in range(P):
+            assert np.array_equal(o[r], outs[0][r])
+    red, _ = O.ring_reduce_scatter(sends, O.Policy(adaptive=2))
+    assert np.array_equal(outs[0][0], np.concatenate(red))
+
+
 def test_all_gather_is_concatenation():
     P, n = 5, 4096 + 7
     parts = [W.sparse_array(n, n // 4, [10, r], W.BF16) for r in range(P)]
