@@ -334,9 +334,10 @@ typedef struct {
 
 /* Scratch bytes the collectives need: P ranks exchanging messages of up to
  * msg_elems elements (n / P for reduce-scatter and all-reduce, n for
- * all-gather).  Holds one workspace and 3*P message buffers of
- * spccl_message_bound(msg_elems, dtype, SPCCL_FMT_COO) bytes (any format
- * fits). */
+ * all-gather).  Holds one workspace and 3*P message buffers of the larger
+ * of spccl_message_bound(msg_elems, dtype, SPCCL_FMT_COO) and
+ * spccl_stream_bound(msg_elems, dtype) bytes (any format fits; for short
+ * messages the Pici bound is the larger). */
 uint64_t spccl_vr_scratch_bytes(int32_t P, uint64_t msg_elems, int32_t dtype);
 
 /* Ring reduce-scatter (Sec. IV-B).  send: host array of P device pointers to

@@ -53,9 +53,11 @@ struct Layout {
     uint8_t* slot(int which, int r, int P) const { return slots + ((uint64_t)which * P + r) * slot_bytes; }
 };
 
-// every message buffer holds the worst case of any format (COO's is the largest)
+// every message buffer holds the worst case of any format: COO's for long
+// messages, Pici's (the column words and offsets of a whole tile) for short ones
 uint64_t slot_need(uint64_t msg_elems, int32_t dtype) {
-    return round_up(spccl_message_bound(msg_elems, dtype, SPCCL_FMT_COO));
+    const uint64_t c = spccl_message_bound(msg_elems, dtype, SPCCL_FMT_COO), p = spccl_stream_bound(msg_elems, dtype);
+    return round_up(c > p ? c : p);
 }
 
 uint64_t scratch_need(int32_t P, uint64_t msg_elems, int32_t dtype) {

@@ -144,3 +144,26 @@ def test_all_reduce_phase_aware_both_formats(S):
     assert {g[2] for g in gtr[P * (P - 1):]} == {0, 1}
     for r in range(P):
         assert np.array_equal(got[r], bits(exp[r]))
+
+
+@pytest.mark.parametrize("dtype", [W.F32, W.BF16])
+@pytest.mark.parametrize("m", [1, 80, 102, 700])
+@pytest.mark.parametrize("pol", ["never_dense", "default", "coo"])
+def test_short_chunks(S, dtype, m, pol):
+    """Chunks of a few hundred elements and less, where a Pici message (the
+    column words and offsets of a whole tile) is larger than a COO one: the
+    message buffers hold either, and results and traces match the oracle."""
+    P = 5
+    policy = O.Policy.coo(adaptive=0) if pol == "coo" else POLICIES[pol]
+    sends = [W.sparse_array(P * m, [0, P * m, P * m // 3, 1, P * m // 10][r], [41, r, m], dtype) for r in range(P)]
+    log(f"short chunks m={m} dtype={dtype} policy={pol}")
+    got, gtr = run_rs(S, sends, policy)
+    exp, otr = O.ring_reduce_scatter(sends, policy)
+    for r in range(P):
+        assert np.array_equal(got[r], bits(exp[r])), f"rs rank {r}: {first_diff(got[r], bits(exp[r]))}"
+    check_trace(gtr, otr)
+    got, gtr = run_ar(S, sends, policy)
+    exp, otr = O.ring_all_reduce(sends, policy)
+    for r in range(P):
+        assert np.array_equal(got[r], bits(exp[r])), f"ar rank {r}: {first_diff(got[r], bits(exp[r]))}"
+    check_trace(gtr, otr)
