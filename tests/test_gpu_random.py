@@ -90,3 +90,49 @@ def test_random_case(S, i):
     got = to_host_bits(out)
     assert np.array_equal(got, bits(exp)), "sliced reduce: " + first_diff(got, bits(exp))
     assert S.spccl_read_status(ws) == 0
+
+
+@pytest.mark.parametrize("i", range(12))
+def test_random_collectives(S, i):
+    """Seeded random ring collectives: P from 1 to 8 (and 33, past the
+    32-rank launch batching of the sliced ring), chunks from one element,
+    mixed densities, random thresholds, node sizes and send formats; the
+    canonical reduce-scatter, all-gather and all-reduce, and for Pici with the
+    threshold rule the sliced ones, against the oracle's rings."""
+    rng = np.random.default_rng([95, i])
+    dtype = [W.F32, W.BF16][int(rng.integers(2))]
+    dt = O.F32 if dtype == W.F32 else O.BF16
+    P = 33 if i == 11 else int(rng.integers(1, 9))
+    m = int([rng.integers(1, 300), rng.integers(1, 20000)][int(rng.integers(2))])
+    n = P * m
+    if rng.integers(4) == 0 and P <= 8:
+        pol = O.Policy.coo(ranks_per_node=int(rng.integers(0, P + 1)))
+    else:
+        pol = O.Policy(intra_thresh=float(rng.choice([0.0, 0.6, 0.9])), inter_thresh=float(rng.choice([0.0, 0.5, 1.0])),
+                       ag_thresh=float(rng.choice([0.0, 0.1, 0.9])), ranks_per_node=int(rng.integers(0, P + 1)),
+                       adaptive=1 if P > 8 else int(rng.integers(0, 3)))
+    fr = [float(rng.choice([0.0, 0.001, 0.01, 0.1, 0.3, 1.0])) for _ in range(P)]
+    sends = [W.sparse_array(n, int(round(f * n)), [95, i, r], dtype) for r, f in enumerate(fr)]
+    log(f"random collectives {i}: P={P} m={m} {dtype} {pol}")
+    ds = [to_dev(x) for x in sends]
+    tdt = torch.float32 if dt == O.F32 else torch.bfloat16
+    same = lambda got, exp: all(np.array_equal(to_host_bits(g), bits(e)) for g, e in zip(got, exp))
+    scr = torch.empty(S.spccl_vr_scratch_bytes(P, m, dt), dtype=torch.uint8, device="cuda")
+    rv = [torch.empty(m, dtype=tdt, device="cuda") for _ in range(P)]
+    av = [torch.empty(n, dtype=tdt, device="cuda") for _ in range(P)]
+    S.spccl_vr_reduce_scatter(ds, rv, scr, pol)
+    assert same(rv, O.ring_reduce_scatter(sends, pol)[0]), "reduce-scatter"
+    S.spccl_vr_all_reduce(ds, av, scr, pol)
+    assert same(av, O.ring_all_reduce(sends, pol)[0]), "all-reduce"
+    parts = [d[:m] for d in ds]
+    S.spccl_vr_all_gather(parts, av, scr, pol)
+    assert same(av, O.ring_all_gather([x[:m] for x in sends], pol.sparse_fmt)[0]), "all-gather"
+    if pol.sparse_fmt == O.FMT_PICI and pol.adaptive == 1:
+        ssc = torch.empty(S.spccl_vr_sliced_scratch_bytes(P, n, dt), dtype=torch.uint8, device="cuda")
+        S.spccl_vr_reduce_scatter_sliced(ds, rv, ssc, pol)
+        assert same(rv, O.ring_reduce_scatter_sliced(sends, pol)[0]), "sliced reduce-scatter"
+        S.spccl_vr_all_reduce_sliced(ds, av, ssc, pol)
+        assert same(av, O.ring_all_reduce_sliced(sends, pol)[0]), "sliced all-reduce"
+        ssg = torch.empty(S.spccl_vr_sliced_scratch_bytes(P, m, dt), dtype=torch.uint8, device="cuda")
+        S.spccl_vr_all_gather_sliced(parts, av, ssg)
+        assert same(av, O.ring_all_gather_sliced([x[:m] for x in sends])[0]), "sliced all-gather"
