@@ -7,16 +7,17 @@ import time
 import numpy as np
 
 
-_PROGRESS = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "gpurun_out")
+# a folder for a progress log (SPCCL_PROGRESS_DIR; none by default)
+_PROGRESS = os.environ.get("SPCCL_PROGRESS_DIR", "")
 
 
 def log(msg: str) -> None:
     """Name the case before a GPU step (flushed, so it survives a crash); the
-    line also goes to gpurun_out/progress.log when that folder exists, so a
+    line also goes to progress.log in SPCCL_PROGRESS_DIR when that is set, so a
     long test shows progress while pytest captures its output."""
     line = f"[gpu-case] {time.strftime('%H:%M:%S')} {msg}"
     print(line, file=sys.stderr, flush=True)
-    if os.path.isdir(_PROGRESS):
+    if _PROGRESS and os.path.isdir(_PROGRESS):
         with open(os.path.join(_PROGRESS, "progress.log"), "a") as f:
             f.write(line + "\n")
 
