@@ -211,7 +211,10 @@ spccl_status_t spccl_reduce(spccl_operand_t a, spccl_operand_t b, spccl_operand_
 
 /* dense_out[q*n_per_part .. (q+1)*n_per_part) = expand(parts[q]) for q < P.
  * parts (host array of P operands) are ARRAYs or STREAMs of any format
- * (a STREAM's format is read from its header; its fmt field is ignored). */
+ * (a STREAM's format is read from its header; its fmt field is ignored).
+ * Any P: parts are expanded 64 per launch, and every part is checked (kind,
+ * alignment, capacity, no overlap with dense_out) before the first launch,
+ * so a host-detectable error in any part leaves dense_out untouched. */
 spccl_status_t spccl_gather_expand(const spccl_operand_t* parts, int32_t P,
                                    uint64_t n_per_part, int32_t dtype,
                                    void* dense_out, uint64_t out_bytes,
@@ -346,7 +349,12 @@ uint64_t spccl_vr_scratch_bytes(int32_t P, uint64_t msg_elems, int32_t dtype);
  * At step s rank r sends chunk (r-s-1) mod P to rank r+1; step 0 compresses
  * and measures sigma0; later steps extrapolate sigma_prev * sigma0 (Eq. 7)
  * and send dense iff the estimate <= the link's threshold.  trace (host,
- * optional) gets P*(P-1) entries, step-major.  n % P == 0. */
+ * optional) gets P*(P-1) entries, step-major.  n % P == 0.  Buffers: no
+ * recv[r] may overlap another rank's recv, any other rank's send or the
+ * scratch, and recv[r] may lie in send[r] only as its own chunk r (in place,
+ * recv[r] == send[r] + r * n/P elements); no send may overlap the scratch.
+ * Any other overlap returns SPCCL_ERR_INVALID_ARG before anything is
+ * launched. */
 spccl_status_t spccl_vr_reduce_scatter(void* const* send, void* const* recv, int32_t P, uint64_t n,
                                        int32_t dtype, const spccl_policy_t* policy,
                                        void* scratch, uint64_t scratch_bytes,
@@ -355,7 +363,11 @@ spccl_status_t spccl_vr_reduce_scatter(void* const* send, void* const* recv, int
 /* Ring all-gather (Sec. IV-B): each rank compresses its n-element part once
  * (in policy->sparse_fmt; NULL policy = Pici), the message travels the ring
  * unchanged, and every rank expands all P parts into recv[r] (P*n
- * elements).  Never switches to dense.  trace gets P entries. */
+ * elements).  Never switches to dense.  trace gets P entries.  Buffers: no
+ * recv[r] may overlap another rank's recv, any other rank's send or the
+ * scratch, and send[r] may lie in recv[r] only at its own place (send[r] ==
+ * recv[r] + r * n elements); otherwise SPCCL_ERR_INVALID_ARG, before any
+ * launch. */
 spccl_status_t spccl_vr_all_gather(void* const* send, void* const* recv, int32_t P, uint64_t n,
                                    int32_t dtype, const spccl_policy_t* policy,
                                    void* scratch, uint64_t scratch_bytes,
@@ -364,7 +376,8 @@ spccl_status_t spccl_vr_all_gather(void* const* send, void* const* recv, int32_t
 /* Ring all-reduce = reduce-scatter, then all-gather of the reduced chunks;
  * at the transition each rank gathers densely iff sigma_prev * sigma0 <=
  * ag_thresh (phase-aware switch, Sec. IV-C).  recv[r] gets n elements.
- * trace gets P*(P-1) + P entries. */
+ * trace gets P*(P-1) + P entries.  No recv[r] may overlap any send, another
+ * recv or the scratch (SPCCL_ERR_INVALID_ARG, before any launch). */
 spccl_status_t spccl_vr_all_reduce(void* const* send, void* const* recv, int32_t P, uint64_t n,
                                    int32_t dtype, const spccl_policy_t* policy,
                                    void* scratch, uint64_t scratch_bytes,
@@ -377,7 +390,7 @@ spccl_status_t spccl_vr_all_reduce(void* const* send, void* const* recv, int32_t
  * receive reduces into recv[r] (n/P elements, the same values as
  * spccl_vr_reduce_scatter).  The P ranks' kernels of one ring step are one
  * launch (up to 32 ranks each), so no recv[r] may overlap another rank's
- * recv or any send buffer (SPCCL_ERR_INVALID_ARG).  tau per link as in
+ * recv, any send buffer or the scratch (SPCCL_ERR_INVALID_ARG).  tau per link as in
  * spccl_policy_t (adaptive 0: never dense, 2: always); sparse_fmt must be
  * SPCCL_FMT_PICI.  The stream is synchronised once, at the end.  fmt_trace
  * (host, optional) gets the format of every slice sent: (P-1) * P * S bytes,

@@ -243,6 +243,22 @@ spccl_status_t spccl_gather_expand(const spccl_operand_t* parts, int32_t P, uint
     spccl_status_t st = check_ws(ws, ws_bytes, kWsFlagsOffset);
     if (st != SPCCL_OK) return st;
     if (n_per_part == 0) return SPCCL_OK;
+    // every part is checked before the first launch: a bad part anywhere
+    // returns its error with nothing launched, however many launches the
+    // parts take
+    for (int32_t q = 0; q < P; q++) {
+        const spccl_operand_t& o = parts[q];
+        if (!o.ptr || (o.kind == SPCCL_ARRAY ? !aligned_elem(o.ptr, dtype) : !aligned16(o.ptr)))
+            return SPCCL_ERR_INVALID_ARG;
+        if (o.kind == SPCCL_ARRAY) {
+            if (o.bytes < n_per_part * s) return SPCCL_ERR_CAPACITY;
+        } else if (o.kind == SPCCL_STREAM) {
+            if (o.bytes < kHeaderBytes) return SPCCL_ERR_CAPACITY;
+        } else {
+            return SPCCL_ERR_INVALID_ARG;
+        }
+        if (overlaps(o.ptr, o.bytes, dense_out, out_bytes)) return SPCCL_ERR_INVALID_ARG;
+    }
     GatherArgs g{};
     g.n = n_per_part;
     g.T = num_tiles(n_per_part);
@@ -251,19 +267,8 @@ spccl_status_t spccl_gather_expand(const spccl_operand_t* parts, int32_t P, uint
         const int cnt = (P - q0) < kMaxGatherParts ? (P - q0) : kMaxGatherParts;
         for (int k = 0; k < cnt; k++) {
             const spccl_operand_t& o = parts[q0 + k];
-            if (!o.ptr || (o.kind == SPCCL_ARRAY ? !aligned_elem(o.ptr, dtype) : !aligned16(o.ptr)))
-                return SPCCL_ERR_INVALID_ARG;
             const uint8_t* p = static_cast<const uint8_t*>(o.ptr);
-            if (o.kind == SPCCL_ARRAY) {
-                if (o.bytes < n_per_part * s) return SPCCL_ERR_CAPACITY;
-                g.part[k] = DevOperand{nullptr, p, o.bytes};
-            } else if (o.kind == SPCCL_STREAM) {
-                if (o.bytes < kHeaderBytes) return SPCCL_ERR_CAPACITY;
-                g.part[k] = DevOperand{p, p, o.bytes};
-            } else {
-                return SPCCL_ERR_INVALID_ARG;
-            }
-            if (overlaps(o.ptr, o.bytes, dense_out, out_bytes)) return SPCCL_ERR_INVALID_ARG;
+            g.part[k] = o.kind == SPCCL_ARRAY ? DevOperand{nullptr, p, o.bytes} : DevOperand{p, p, o.bytes};
         }
         g.out = static_cast<uint8_t*>(dense_out) + (uint64_t)q0 * n_per_part * s;
         st = launch_gather_dt(dtype, g, cnt, as_stream(stream));

@@ -249,6 +249,38 @@ spccl_status_t check_common(void* const* send, void* const* recv, int32_t P, int
     return SPCCL_OK;
 }
 
+// Which layout of a rank's receive buffer inside its own send buffer (or the
+// reverse) a collective handles: the reduce-scatter writes chunk r of rank r
+// last, after reading it, so recv[r] may be that chunk of send[r]; the
+// all-gather reads every part before writing, so send[r] may sit at part r of
+// recv[r]; the all-reduce reduces into recv while chunks are still read.
+enum InPlace { kInPlaceNone, kInPlaceRsChunk, kInPlaceAgPart };
+
+// Every overlap among the P send buffers (send_bytes each), the P receive
+// buffers (recv_bytes each) and the scratch the collective uses, other than
+// the one in-place layout, is rejected before anything is launched: a receive
+// buffer written by one rank while another still reads it would change
+// results silently.  Send buffers may overlap each other (they are only
+// read).
+spccl_status_t check_disjoint(void* const* send, uint64_t send_bytes, void* const* recv, uint64_t recv_bytes,
+                              int32_t P, InPlace ip, uint64_t part_bytes, const void* scratch,
+                              uint64_t scratch_used) {
+    for (int r = 0; r < P; r++) {
+        if (overlaps(recv[r], recv_bytes, scratch, scratch_used) || overlaps(send[r], send_bytes, scratch, scratch_used))
+            return SPCCL_ERR_INVALID_ARG;
+        for (int q = 0; q < P; q++) {
+            if (q != r && overlaps(recv[r], recv_bytes, recv[q], recv_bytes)) return SPCCL_ERR_INVALID_ARG;
+            if (!overlaps(recv[r], recv_bytes, send[q], send_bytes)) continue;
+            const uint8_t* rb = static_cast<const uint8_t*>(recv[r]);
+            const uint8_t* sb = static_cast<const uint8_t*>(send[q]);
+            const bool allowed = q == r && ((ip == kInPlaceRsChunk && rb == sb + (uint64_t)r * part_bytes) ||
+                                            (ip == kInPlaceAgPart && sb == rb + (uint64_t)r * part_bytes));
+            if (!allowed) return SPCCL_ERR_INVALID_ARG;
+        }
+    }
+    return SPCCL_OK;
+}
+
 spccl_status_t finish(const Layout& L, hipStream_t st) {
     return spccl_read_status(L.ws, 1, st);
 }
@@ -266,8 +298,9 @@ spccl_status_t spccl_vr_reduce_scatter(void* const* send, void* const* recv, int
                                        const spccl_policy_t* policy, void* scratch, uint64_t scratch_bytes,
                                        spccl_trace_t* trace, void* stream) {
     if (P < 1 || n % (uint64_t)P) return SPCCL_ERR_INVALID_ARG;
-    const uint64_t m = n / (uint64_t)P;
+    const uint64_t m = n / (uint64_t)P, s = elem_bytes(dtype);
     SPCCL_TRY(check_common(send, recv, P, dtype, scratch, scratch_bytes, m));
+    SPCCL_TRY(check_disjoint(send, n * s, recv, m * s, P, kInPlaceRsChunk, m * s, scratch, scratch_need(P, m, dtype)));
     const spccl_policy_t pol = policy ? *policy : kDefaultPolicy;
     if (!policy_ok(pol)) return SPCCL_ERR_INVALID_ARG;
     hipStream_t st = as_stream(stream);
@@ -282,6 +315,9 @@ spccl_status_t spccl_vr_all_gather(void* const* send, void* const* recv, int32_t
                                    const spccl_policy_t* policy, void* scratch, uint64_t scratch_bytes,
                                    spccl_trace_t* trace, void* stream) {
     SPCCL_TRY(check_common(send, recv, P, dtype, scratch, scratch_bytes, n));
+    const uint64_t s = elem_bytes(dtype);
+    SPCCL_TRY(check_disjoint(send, n * s, recv, (uint64_t)P * n * s, P, kInPlaceAgPart, n * s, scratch,
+                             scratch_need(P, n, dtype)));
     const spccl_policy_t pol = policy ? *policy : kDefaultPolicy;
     if (!policy_ok(pol)) return SPCCL_ERR_INVALID_ARG;
     hipStream_t st = as_stream(stream);
@@ -302,11 +338,8 @@ spccl_status_t spccl_vr_all_reduce(void* const* send, void* const* recv, int32_t
     if (P < 1 || n % (uint64_t)P) return SPCCL_ERR_INVALID_ARG;
     const uint64_t m = n / (uint64_t)P, s = elem_bytes(dtype);
     SPCCL_TRY(check_common(send, recv, P, dtype, scratch, scratch_bytes, m));
-    for (int r = 0; r < P; r++)   // outputs must not overlap the inputs (chunks are reduced into them)
-        for (int q = 0; q < P; q++) {
-            const uintptr_t a = reinterpret_cast<uintptr_t>(recv[r]), b = reinterpret_cast<uintptr_t>(send[q]);
-            if (n && a < b + n * s && b < a + n * s) return SPCCL_ERR_INVALID_ARG;
-        }
+    // outputs must not overlap the inputs (chunks are reduced into them), each other or the scratch
+    SPCCL_TRY(check_disjoint(send, n * s, recv, n * s, P, kInPlaceNone, 0, scratch, scratch_need(P, m, dtype)));
     const spccl_policy_t pol = policy ? *policy : kDefaultPolicy;
     if (!policy_ok(pol)) return SPCCL_ERR_INVALID_ARG;
     hipStream_t st = as_stream(stream);
@@ -390,7 +423,7 @@ namespace {
 // buffer may overlap another or any send buffer, because the ranks of a step
 // share one launch.
 spccl_status_t check_sliced_ranks(void* const* send, uint64_t send_elems, void* const* recv, uint64_t recv_elems,
-                                  int32_t P, int32_t dtype, const void* scratch) {
+                                  int32_t P, int32_t dtype, const void* scratch, uint64_t scratch_used) {
     const uint64_t s = elem_bytes(dtype);
     if (!send || !recv || !scratch || (reinterpret_cast<uintptr_t>(scratch) & 15u)) return SPCCL_ERR_INVALID_ARG;
     const uintptr_t amask = (uintptr_t)s - 1;
@@ -398,11 +431,15 @@ spccl_status_t check_sliced_ranks(void* const* send, uint64_t send_elems, void* 
         if (!send[r] || !recv[r] || (reinterpret_cast<uintptr_t>(send[r]) & amask) ||
             (reinterpret_cast<uintptr_t>(recv[r]) & amask))
             return SPCCL_ERR_INVALID_ARG;
-    for (int r = 0; r < P; r++)
+    for (int r = 0; r < P; r++) {
+        if (overlaps(recv[r], recv_elems * s, scratch, scratch_used) ||
+            overlaps(send[r], send_elems * s, scratch, scratch_used))
+            return SPCCL_ERR_INVALID_ARG;
         for (int q = 0; q < P; q++)
             if (overlaps(recv[r], recv_elems * s, send[q], send_elems * s) ||
                 (q != r && overlaps(recv[r], recv_elems * s, recv[q], recv_elems * s)))
                 return SPCCL_ERR_INVALID_ARG;
+    }
     return SPCCL_OK;
 }
 
@@ -502,7 +539,7 @@ spccl_status_t spccl_vr_reduce_scatter_sliced(void* const* send, void* const* re
     const uint64_t m = n / (uint64_t)P, s = elem_bytes(dtype);
     if (dtype != SPCCL_F32 && dtype != SPCCL_BF16) return SPCCL_ERR_UNSUPPORTED;
     if (m >= (1ull << 32)) return SPCCL_ERR_UNSUPPORTED;
-    SPCCL_TRY(check_sliced_ranks(send, n, recv, m, P, dtype, scratch));
+    SPCCL_TRY(check_sliced_ranks(send, n, recv, m, P, dtype, scratch, sliced_need(P, m, dtype, nullptr, nullptr)));
     const spccl_policy_t pol = policy ? *policy : kDefaultPolicy;
     if (!policy_ok(pol)) return SPCCL_ERR_INVALID_ARG;
     if (pol.sparse_fmt != SPCCL_FMT_PICI) return SPCCL_ERR_UNSUPPORTED;      // slices are Pici or dense
@@ -527,7 +564,8 @@ spccl_status_t spccl_vr_all_gather_sliced(void* const* send, void* const* recv, 
     if (dtype != SPCCL_F32 && dtype != SPCCL_BF16) return SPCCL_ERR_UNSUPPORTED;
     if (n >= (1ull << 32)) return SPCCL_ERR_UNSUPPORTED;
     const uint64_t s = elem_bytes(dtype);
-    SPCCL_TRY(check_sliced_ranks(send, n, recv, (uint64_t)P * n, P, dtype, scratch));
+    SPCCL_TRY(check_sliced_ranks(send, n, recv, (uint64_t)P * n, P, dtype, scratch,
+                                 sliced_need(P, n, dtype, nullptr, nullptr)));
     if (scratch_bytes < sliced_need(P, n, dtype, nullptr, nullptr)) return SPCCL_ERR_WORKSPACE;
     hipStream_t st = as_stream(stream);
     if (P == 1) {
@@ -560,7 +598,7 @@ spccl_status_t spccl_vr_all_reduce_sliced(void* const* send, void* const* recv, 
     const uint64_t m = n / (uint64_t)P, s = elem_bytes(dtype);
     if (dtype != SPCCL_F32 && dtype != SPCCL_BF16) return SPCCL_ERR_UNSUPPORTED;
     if (m >= (1ull << 32)) return SPCCL_ERR_UNSUPPORTED;
-    SPCCL_TRY(check_sliced_ranks(send, n, recv, n, P, dtype, scratch));
+    SPCCL_TRY(check_sliced_ranks(send, n, recv, n, P, dtype, scratch, sliced_need(P, m, dtype, nullptr, nullptr)));
     const spccl_policy_t pol = policy ? *policy : kDefaultPolicy;
     if (!policy_ok(pol)) return SPCCL_ERR_INVALID_ARG;
     if (pol.sparse_fmt != SPCCL_FMT_PICI) return SPCCL_ERR_UNSUPPORTED;

@@ -116,3 +116,112 @@ def test_operand_keeps_its_tensor_alive(S):
     del op
     gc.collect()
     assert ref() is None
+
+
+def _parts(S, P, n, bad=None, kind=None):
+    """P fake device operands (dense arrays of n fp32 at distinct aligned
+    addresses); part `bad` is made invalid in the way `kind` says."""
+    op = S.spccl_operand_t
+    ps = []
+    for q in range(P):
+        ptr, k, nbytes = (q + 1) << 24, S.SPCCL_ARRAY, 4 * n
+        if q == bad:
+            if kind == "misaligned":
+                ptr += 2
+            elif kind == "small":
+                nbytes -= 4
+            elif kind == "kind":
+                k = 7
+            elif kind == "overlap":
+                ptr = 1 << 34                 # inside the output below
+        ps.append(op(k, 0, ptr, nbytes))
+    return (op * P)(*ps)
+
+
+@pytest.mark.parametrize("kind,status", [("misaligned", 1), ("small", 2), ("kind", 1), ("overlap", 1)])
+@pytest.mark.parametrize("bad", [0, 64, 100, 129])
+def test_gather_expand_checks_every_part_before_any_launch(S, kind, status, bad):
+    """A bad part in any 64-part launch chunk is reported before the first
+    chunk is launched: without a GPU a launch would fail with ERR_HIP, so the
+    part's own error code shows that nothing was launched."""
+    P, n = 130, 4096
+    parts = _parts(S, P, n, bad, kind)
+    out = 1 << 34
+    st = S._lib.spccl_gather_expand(parts, P, n, 0, out, P * n * 4, 1 << 40, 1 << 20, None)
+    assert st == status
+
+
+def _vr_call(S, which, send, recv, P, n, scratch, scratch_bytes):
+    lib = S._lib
+    pol = S.spccl_policy_t(0.6, 0.5, 0.1, 0, 1, 1)
+    sp = (ctypes.c_void_p * P)(*send)
+    rp = (ctypes.c_void_p * P)(*recv)
+    if which == "rs":
+        return lib.spccl_vr_reduce_scatter(sp, rp, P, n, 0, ctypes.byref(pol), scratch, scratch_bytes, None, None)
+    if which == "ag":
+        return lib.spccl_vr_all_gather(sp, rp, P, n, 0, ctypes.byref(pol), scratch, scratch_bytes, None, None)
+    if which == "ar":
+        return lib.spccl_vr_all_reduce(sp, rp, P, n, 0, ctypes.byref(pol), scratch, scratch_bytes, None, None)
+    if which == "rs_sliced":
+        return lib.spccl_vr_reduce_scatter_sliced(sp, rp, P, n, 0, ctypes.byref(pol), scratch, scratch_bytes, None,
+                                                  None)
+    if which == "ag_sliced":
+        return lib.spccl_vr_all_gather_sliced(sp, rp, P, n, 0, scratch, scratch_bytes, None, None)
+    return lib.spccl_vr_all_reduce_sliced(sp, rp, P, n, 0, ctypes.byref(pol), scratch, scratch_bytes, None, None,
+                                          None)
+
+
+def _scratch_bytes(S, which, P, n):
+    m = n if which.startswith("ag") else n // P
+    if which.endswith("sliced"):
+        return S.spccl_vr_sliced_scratch_bytes(P, m, 0)
+    return S.spccl_vr_scratch_bytes(P, m, 0)
+
+
+GB = 1 << 30
+
+
+@pytest.mark.parametrize("which", ["rs", "ag", "ar", "rs_sliced", "ag_sliced", "ar_sliced"])
+def test_collectives_reject_overlapping_buffers_before_launch(S, which):
+    """Overlaps between a rank's receive buffer and another rank's send or
+    receive buffer, or between any buffer and the scratch, are rejected on the
+    host (INVALID_ARG, where a launch without a GPU would give ERR_HIP)."""
+    P, n = 4, 4 * 4096
+    s = 4
+    rb = n * s if which.startswith(("ag", "ar")) else n // P * s
+    if which.startswith("ag"):
+        rb = P * n * s
+    send = [(1 + r) * GB for r in range(P)]
+    recv = [(10 + r) * GB for r in range(P)]
+    scratch, sb = 40 * GB, _scratch_bytes(S, which, P, n)
+    cases = {
+        "recv_in_other_send": (send, [send[1] + 256] + recv[1:], scratch),
+        "recv_overlaps_recv": (send, [recv[0], recv[0] + rb // 2] + recv[2:], scratch),
+        "recv_in_scratch": (send, recv[:3] + [scratch + 512], scratch),
+        "send_in_scratch": ([scratch + 1024] + send[1:], recv, scratch),
+    }
+    for name, (sd, rv, sc) in cases.items():
+        assert _vr_call(S, which, sd, rv, P, n, sc, sb) == 1, name
+
+
+def test_collectives_in_place_layouts_pass_the_host_checks(S):
+    """The in-place layouts the canonical rings handle -- recv[r] as chunk r
+    of send[r] (reduce-scatter), send[r] at part r of recv[r] (all-gather) --
+    pass the overlap checks; without a GPU the call then fails at its first
+    launch (ERR_HIP), which shows the checks let it through.  Any other
+    position inside the own buffer is rejected."""
+    P, n, s = 4, 4 * 4096, 4
+    m = n // P
+    send = [(1 + r) * GB for r in range(P)]
+    scratch = 40 * GB
+    sb = _scratch_bytes(S, "rs", P, n)
+    rs_in_place = [send[r] + r * m * s for r in range(P)]
+    assert _vr_call(S, "rs", send, rs_in_place, P, n, scratch, sb) == 6
+    shifted = [send[r] + ((r + 1) % P) * m * s for r in range(P)]
+    assert _vr_call(S, "rs", send, shifted, P, n, scratch, sb) == 1
+    recv = [(10 + 2 * r) * GB for r in range(P)]
+    sb = _scratch_bytes(S, "ag", P, n)
+    ag_in_place = [recv[r] + r * n * s for r in range(P)]
+    assert _vr_call(S, "ag", ag_in_place, recv, P, n, scratch, sb) == 6
+    shifted = [recv[r] + ((r + 1) % P) * n * s for r in range(P)]
+    assert _vr_call(S, "ag", shifted, recv, P, n, scratch, sb) == 1

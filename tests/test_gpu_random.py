@@ -117,22 +117,38 @@ def test_random_collectives(S, i):
     ds = [to_dev(x) for x in sends]
     tdt = torch.float32 if dt == O.F32 else torch.bfloat16
     same = lambda got, exp: all(np.array_equal(to_host_bits(g), bits(e)) for g, e in zip(got, exp))
+    # format decisions never change values (Sec. IV-C), so the traces --
+    # format, bytes, nonzeros and tracked sparsity of every send -- are
+    # compared as well: a wrong decision, threshold or link rule shows there
+    tup = lambda e: (e.step, e.rank, e.fmt, e.measured, e.bytes, e.nnz, e.sigma)
     scr = torch.empty(S.spccl_vr_scratch_bytes(P, m, dt), dtype=torch.uint8, device="cuda")
     rv = [torch.empty(m, dtype=tdt, device="cuda") for _ in range(P)]
     av = [torch.empty(n, dtype=tdt, device="cuda") for _ in range(P)]
-    S.spccl_vr_reduce_scatter(ds, rv, scr, pol)
-    assert same(rv, O.ring_reduce_scatter(sends, pol)[0]), "reduce-scatter"
-    S.spccl_vr_all_reduce(ds, av, scr, pol)
-    assert same(av, O.ring_all_reduce(sends, pol)[0]), "all-reduce"
+    gtr = S.spccl_vr_reduce_scatter(ds, rv, scr, pol)
+    exp, otr = O.ring_reduce_scatter(sends, pol)
+    assert same(rv, exp), "reduce-scatter"
+    assert gtr == [tup(e) for e in otr], "reduce-scatter trace"
+    gtr = S.spccl_vr_all_reduce(ds, av, scr, pol)
+    exp, otr = O.ring_all_reduce(sends, pol)
+    assert same(av, exp), "all-reduce"
+    assert gtr == [tup(e) for e in otr], "all-reduce trace"
     parts = [d[:m] for d in ds]
-    S.spccl_vr_all_gather(parts, av, scr, pol)
-    assert same(av, O.ring_all_gather([x[:m] for x in sends], pol.sparse_fmt)[0]), "all-gather"
+    gtr = S.spccl_vr_all_gather(parts, av, scr, pol)
+    exp, otr = O.ring_all_gather([x[:m] for x in sends], pol.sparse_fmt)
+    assert same(av, exp), "all-gather"
+    assert gtr == [tup(e) for e in otr], "all-gather trace"
     if pol.sparse_fmt == O.FMT_PICI and pol.adaptive == 1:
         ssc = torch.empty(S.spccl_vr_sliced_scratch_bytes(P, n, dt), dtype=torch.uint8, device="cuda")
-        S.spccl_vr_reduce_scatter_sliced(ds, rv, ssc, pol)
-        assert same(rv, O.ring_reduce_scatter_sliced(sends, pol)[0]), "sliced reduce-scatter"
-        S.spccl_vr_all_reduce_sliced(ds, av, ssc, pol)
-        assert same(av, O.ring_all_reduce_sliced(sends, pol)[0]), "sliced all-reduce"
+        gfm = S.spccl_vr_reduce_scatter_sliced(ds, rv, ssc, pol)
+        exp, ofm = O.ring_reduce_scatter_sliced(sends, pol)
+        assert same(rv, exp), "sliced reduce-scatter"
+        assert np.array_equal(gfm, ofm), "sliced reduce-scatter formats"
+        grs, gag = S.spccl_vr_all_reduce_sliced(ds, av, ssc, pol)
+        exp, ors, oag = O.ring_all_reduce_sliced(sends, pol)
+        assert same(av, exp), "sliced all-reduce"
+        assert np.array_equal(grs, ors) and np.array_equal(gag, oag), "sliced all-reduce formats"
         ssg = torch.empty(S.spccl_vr_sliced_scratch_bytes(P, m, dt), dtype=torch.uint8, device="cuda")
-        S.spccl_vr_all_gather_sliced(parts, av, ssg)
-        assert same(av, O.ring_all_gather_sliced([x[:m] for x in sends])[0]), "sliced all-gather"
+        gfm = S.spccl_vr_all_gather_sliced(parts, av, ssg)
+        exp, ofm = O.ring_all_gather_sliced([x[:m] for x in sends])
+        assert same(av, exp), "sliced all-gather"
+        assert np.array_equal(gfm, ofm), "sliced all-gather formats"
