@@ -290,6 +290,24 @@ spccl_status_t spccl_reduce_sliced_tracked(const void* a, const void* b, uint64_
                                            uint64_t tracker_bytes, uint8_t* fmt_out, uint64_t n,
                                            int32_t dtype, void* ws, uint64_t ws_bytes, void* stream);
 
+/* ---- compression without a caller workspace --------------------------------
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the same
+ * message as spccl_compress, made by the single-pass kernels, whose scratch
+ * (a status word and one look-back word per 16384-element partition) lives in
+ * a static device array of the library -- 128 KiB plus a 256-byte control
+ * block, one copy per GPU, held until the process ends.  The call allocates
+ * nothing.  n <= SPCCL_STATIC_MAX_ELEMS, else SPCCL_ERR_UNSUPPORTED; other
+ * argument errors as spccl_compress (out_bytes >= spccl_stream_bound).  Every
+ * call on a GPU shares that GPU's array, so calls that overlap on one GPU
+ * (two streams at once) race and must not be issued; calls in order on
+ * streams are fine.  A device-side wait that exceeds its spin limit clears
+ * the output header's magic, so the message is rejected as corrupt by every
+ * reader. */
+#define SPCCL_STATIC_MAX_ELEMS (1ull << 28)
+spccl_status_t spccl_compress_static(const void* dense, uint64_t n, int32_t dtype, void* out, uint64_t out_bytes,
+                                     void* stream);
+
 /* ---- message transport and inspection ------------------------------------ */
 
 /* The virtual-rank "send": copy header.total_bytes bytes of the message at

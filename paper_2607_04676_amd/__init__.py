@@ -42,7 +42,7 @@ EXPORTS = ("spccl_num_tiles", "spccl_pici_bytes", "spccl_stream_bound", "spccl_w
            "spccl_reduce_sliced", "spccl_copy_sliced", "spccl_coo_bytes", "spccl_message_bound",
            "spccl_compress_coo", "spccl_slice_tracker_bytes", "spccl_compress_sliced_tracked",
            "spccl_reduce_sliced_tracked", "spccl_vr_sliced_scratch_bytes", "spccl_vr_reduce_scatter_sliced",
-           "spccl_vr_all_gather_sliced", "spccl_vr_all_reduce_sliced")
+           "spccl_vr_all_gather_sliced", "spccl_vr_all_reduce_sliced", "spccl_compress_static")
 
 
 class spccl_operand_t(ctypes.Structure):
@@ -78,6 +78,7 @@ _sigs = {
     "spccl_workspace_init": (_i32, [_vp, _u64, _vp]),
     "spccl_compress": (_i32, [_vp, _u64, _i32, _vp, _u64, _vp, _u64, _vp]),
     "spccl_compress_coo": (_i32, [_vp, _u64, _i32, _vp, _u64, _vp, _u64, _vp]),
+    "spccl_compress_static": (_i32, [_vp, _u64, _i32, _vp, _u64, _vp]),
     "spccl_coo_bytes": (_u64, [_i32, _u64]),
     "spccl_message_bound": (_u64, [_u64, _i32, _i32]),
     "spccl_decompress": (_i32, [_vp, _u64, _vp, _u64, _i32, _vp, _u64, _vp]),
@@ -204,6 +205,16 @@ def spccl_workspace_init(ws: torch.Tensor, stream=None) -> None:
 def spccl_compress(dense: torch.Tensor, out: torch.Tensor, ws: torch.Tensor, stream=None) -> None:
     _check(_lib.spccl_compress(dense.data_ptr(), dense.numel(), _dt(dense), out.data_ptr(), _nbytes(out),
                                ws.data_ptr(), _nbytes(ws), _stream(stream)), "spccl_compress")
+
+
+def spccl_compress_static(dense: torch.Tensor, out: torch.Tensor, stream=None) -> None:
+    """spccl_compress without a workspace (its scratch is the library's own
+    static device array; n <= SPCCL_STATIC_MAX_ELEMS)."""
+    _check(_lib.spccl_compress_static(dense.data_ptr(), dense.numel(), _dt(dense), out.data_ptr(), _nbytes(out),
+                                      _stream(stream)), "spccl_compress_static")
+
+
+SPCCL_STATIC_MAX_ELEMS = 1 << 28
 
 
 def spccl_compress_coo(dense: torch.Tensor, out: torch.Tensor, ws: torch.Tensor, stream=None) -> None:

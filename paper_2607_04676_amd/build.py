@@ -15,7 +15,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libspccl.so")
-SOURCES = ["spccl_kernels.hip", "spccl_api.cpp", "spccl_vr.cpp"]
+SOURCES = ["spccl_kernels.hip", "spccl_api.cpp", "spccl_vr.cpp", "spccl_static.hip"]
 ARCH = os.environ.get("SPCCL_OFFLOAD_ARCH", "gfx950")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
