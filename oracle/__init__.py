@@ -119,6 +119,9 @@ def lib():
                                           ctypes.POINTER(_Policy), ctypes.POINTER(_Trace)]
         L.orc_ring_all_gather_sliced.restype = i32
         L.orc_ring_all_gather_sliced.argtypes = [ctypes.POINTER(vp), ctypes.POINTER(vp), i32, u64, i32, vp]
+        L.orc_time_step.restype = i32
+        L.orc_time_step.argtypes = [vp, vp, u64, u64, i32, vp, vp, vp, u64, vp, vp, i32,
+                                    ctypes.POINTER(ctypes.c_double)]
         L.orc_ring_all_reduce_sliced.restype = i32
         L.orc_ring_all_reduce_sliced.argtypes = [ctypes.POINTER(vp), ctypes.POINTER(vp), i32, u64, i32,
                                                  ctypes.POINTER(_Policy), vp, vp]
@@ -508,3 +511,20 @@ def ring_reduce_scatter_sliced(sends: list, policy: Policy | None = None):
                                                 ctypes.byref(pol), _ptr(fm)), "ring_reduce_scatter_sliced")
     return recvs, fm[:(P - 1) * P * S].reshape(max(P - 1, 0), P, S)
 
+
+def time_step(a: np.ndarray, b_msg: np.ndarray, reps: int = 3) -> list:
+    """The benchmark step's op sequence on the oracle, timed inside the C
+    library (monotonic clock), reps times: compress, decompress, the three
+    reductions (dense + Pici -> Pici, Pici + Pici -> Pici, dense + Pici ->
+    dense) and a two-part expansion.  Returns each repetition's seconds."""
+    a = np.ascontiguousarray(a)
+    n, dt = a.size, dtype_code(a)
+    cap = stream_bound(n, dt)
+    s1, s2, s3 = (np.zeros(cap, dtype=np.uint8) for _ in range(3))
+    d1, d2 = np.empty_like(a), np.empty_like(a)
+    secs = (ctypes.c_double * reps)()
+    _check(lib().orc_time_step(_ptr(a), _ptr(b_msg), b_msg.size, n, dt, _ptr(s1), _ptr(s2), _ptr(s3), cap,
+                               _ptr(d1), _ptr(d2), reps, secs), "time_step")
+    if not np.array_equal(d1.view(np.uint8), a.view(np.uint8)):
+        raise OracleError(4, "time_step: round trip differs")
+    return [secs[i] for i in range(reps)]

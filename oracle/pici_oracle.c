@@ -28,10 +28,12 @@
  * Build: gcc -O2 -std=c99 -fPIC -shared (no fast-math: IEEE round-to-nearest,
  * denormals kept).
  */
+#define _POSIX_C_SOURCE 199309L     /* clock_gettime, for the timing helper at the end */
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
 #include <math.h>
+#include <time.h>
 
 /* ---- constants of the format (Sec. III-B) ---------------------------- */
 #define ORC_TILE_ROWS 64u           /* a tile is 64 x 64 elements, row-major */
@@ -887,3 +889,37 @@ done:
     return st;
 }
 
+/* ---- timing helper of the benchmark's CPU-baseline leg ------------------ */
+/* Not a definition of the method: the benchmark's step, run on the functions
+ * above as they stand -- compress(a) into s1, decompress s1 into d1,
+ * a (+) Pici(b) -> Pici s2, Pici(s1) (+) Pici(b) -> Pici s3,
+ * a (+) Pici(b) -> dense d2, and the expansion of s1 and s2 (the all-gather
+ * receive side) -- reps times on caller-owned buffers (cap bytes each for s1,
+ * s2, s3; n elements each for d1, d2).  secs[r] is repetition r's time in
+ * seconds (monotonic clock).  Returns the first failing status, else 0. */
+static double now_s(void) {
+    struct timespec ts;
+    clock_gettime(CLOCK_MONOTONIC, &ts);
+    return (double)ts.tv_sec + 1e-9 * (double)ts.tv_nsec;
+}
+
+int orc_time_step(const void* a, const uint8_t* b, uint64_t b_cap, uint64_t n, int dtype, uint8_t* s1,
+                  uint8_t* s2, uint8_t* s3, uint64_t cap, void* d1, void* d2, int reps, double* secs) {
+    for (int r = 0; r < reps; r++) {
+        uint64_t nnz = 0;
+        const double t0 = now_s();
+        int st = orc_compress(a, n, dtype, s1, cap, &nnz);
+        if (!st) st = orc_decompress(s1, cap, d1, n, dtype);
+        if (!st) st = orc_reduce(ORC_ARRAY, a, n * elem_size(dtype), ORC_STREAM, b, b_cap, ORC_STREAM, ORC_FMT_PICI,
+                                 s2, cap, n, dtype, &nnz);
+        if (!st) st = orc_reduce(ORC_STREAM, s1, cap, ORC_STREAM, b, b_cap, ORC_STREAM, ORC_FMT_PICI, s3, cap, n,
+                                 dtype, &nnz);
+        if (!st) st = orc_reduce(ORC_ARRAY, a, n * elem_size(dtype), ORC_STREAM, b, b_cap, ORC_ARRAY, ORC_FMT_DENSE,
+                                 d2, n * elem_size(dtype), n, dtype, &nnz);
+        if (!st) st = orc_decompress(s1, cap, d1, n, dtype);
+        if (!st) st = orc_decompress(s2, cap, d2, n, dtype);
+        secs[r] = now_s() - t0;
+        if (st) return st;
+    }
+    return ORC_OK;
+}
