@@ -1277,9 +1277,10 @@ __device__ __forceinline__ void pp_merge(uint64_t wa, uint64_t wb, uint64_t wo, 
 // value ranges in its LDS buffer (one load round when together they fit
 // kChunkVals, else per column group), finds exact cancellations among the
 // rows both operands hold, and merges each column's two runs in row order
-// into the destination: its slot (two-pass mode) or its place once the
-// partition's offset is known by look-back (single pass).
-template <class E, bool Deferred>
+// into its place once the partition's offset is known by decoupled
+// look-back (the single-pass mode of a minimal workspace; with a full one,
+// k_pp_part and k_place run instead).
+template <class E>
 __global__ void __launch_bounds__(kBlockThreads) k_pp_tile(PiciSinkArgs g) {
     using raw = typename E::raw;
     __shared__ raw lds_in[kWavesPerBlock][kChunkVals];
@@ -1347,24 +1348,17 @@ __global__ void __launch_bounds__(kBlockThreads) k_pp_tile(PiciSinkArgs g) {
         tile_excl += k < wave ? ck : 0u;
         agg += ck;
     }
-    if (threadIdx.x == 0)
-        publish(g.flags, p, epoch30, (p == 0 && !Deferred) ? kFlagPrefix : kFlagAggregate, agg);
-    raw* dst;
-    uint32_t prefix = 0;
-    if constexpr (Deferred) {
-        dst = reinterpret_cast<raw*>(g.slots) + (uint64_t)p * kPartElems + tile_excl;
-    } else {
-        if (wave == 0) {
-            const uint32_t pre = p == 0 ? 0u : lookback(g.flags, p, epoch30, g.ctrl);
-            if (l == 0) {
-                if (p != 0) publish(g.flags, p, epoch30, kFlagPrefix, pre + agg);
-                s_prefix = pre;
-            }
+    if (threadIdx.x == 0) publish(g.flags, p, epoch30, p == 0 ? kFlagPrefix : kFlagAggregate, agg);
+    if (wave == 0) {
+        const uint32_t pre = p == 0 ? 0u : lookback(g.flags, p, epoch30, g.ctrl);
+        if (l == 0) {
+            if (p != 0) publish(g.flags, p, epoch30, kFlagPrefix, pre + agg);
+            s_prefix = pre;
         }
-        __syncthreads();
-        prefix = s_prefix;
-        dst = reinterpret_cast<raw*>(g.out + oA) + prefix + tile_excl;
     }
+    __syncthreads();
+    const uint32_t prefix = s_prefix;
+    raw* dst = reinterpret_cast<raw*>(g.out + oA) + prefix + tile_excl;
     if (has_tile) {
         if (one) {
             pp_merge<E>(ca.w, cb.w, wo, in, ca.colpref, la + cb.colpref, dst, cpo, true);
@@ -1379,17 +1373,187 @@ __global__ void __launch_bounds__(kBlockThreads) k_pp_tile(PiciSinkArgs g) {
                 wave_lds_sync();
             }
         }
-        if (l == 0) reinterpret_cast<uint32_t*>(g.out + oI)[t] = Deferred ? tile_excl : prefix + tile_excl;
+        if (l == 0) reinterpret_cast<uint32_t*>(g.out + oI)[t] = prefix + tile_excl;
     }
-    if constexpr (!Deferred) {
-        if (p == g.nparts - 1 && threadIdx.x == 0) {
-            const uint64_t nnz = (uint64_t)prefix + agg;
-            uint32_t* I = reinterpret_cast<uint32_t*>(g.out + oI);
-            I[g.T] = (uint32_t)nnz;
-            for (uint64_t b = oI + 4 * (g.T + 1); b < oA; b += 4) *reinterpret_cast<uint32_t*>(g.out + b) = 0u;
-            write_header(g.out, kFmtPici, E::dtype, g.n, nnz, oI, oA, oA + nnz * sizeof(raw));
+    if (p == g.nparts - 1 && threadIdx.x == 0) {
+        const uint64_t nnz = (uint64_t)prefix + agg;
+        uint32_t* I = reinterpret_cast<uint32_t*>(g.out + oI);
+        I[g.T] = (uint32_t)nnz;
+        for (uint64_t b = oI + 4 * (g.T + 1); b < oA; b += 4) *reinterpret_cast<uint32_t*>(g.out + b) = 0u;
+        write_header(g.out, kFmtPici, E::dtype, g.n, nnz, oI, oA, oA + nnz * sizeof(raw));
+    }
+}
+
+// Pici (+) Pici -> Pici, first of the two passes, one partition (four tiles)
+// per wave.  The wave reads the column words of its four tiles and their
+// offsets in one round trip; when the partition's values (a contiguous range
+// of each operand) fit the stage together, they arrive in one more; each
+// tile's merged results go into an LDS output buffer in partition order,
+// which is written to the partition's slot with contiguous stores whenever
+// the next tile might not fit, and at the end.  A wave needs no other wave,
+// so the 4096 waves of a 256 MiB array fit the device at once.  Tiles whose
+// values do not fit the stage take it one tile (or one column group) at a
+// time.  Slot layout, offsets and counts are those k_place expects.
+template <class E>
+__global__ void __launch_bounds__(kBlockThreads) k_pp_part(PiciSinkArgs g) {
+    using raw = typename E::raw;
+    constexpr int K = (int)kTilesPerPart;
+    __shared__ raw lds_in[kWavesPerBlock][kChunkVals];
+    __shared__ raw lds_out[kWavesPerBlock][kChunkVals];
+    const uint32_t wave = threadIdx.x >> 6, l = lane_id();
+    raw* in = lds_in[wave];
+    raw* ob = lds_out[wave];
+    const uint32_t p = blockIdx.x * kWavesPerBlock + wave;
+    const uint32_t epoch30 = g.epoch & 0x3FFFFFFFu;
+    const uint64_t oI = off_I(g.n), oA = off_A(g.n);
+    const uint64_t t0 = (uint64_t)p * kTilesPerPart;
+
+    // headers, the tiles' column words and offsets I[t0 .. t0 + 4] of both
+    // messages, through buffer resources that end at the index arrays (the
+    // host guarantees both capacities cover them; past them the hardware
+    // returns zeros), so every wave issues them before any check
+    const HeaderWords hwa = load_header_words(g.a.hdr);
+    const HeaderWords hwb = load_header_words(g.b.hdr);
+    uint64_t wa[K], wb[K];
+    uint32_t Ia, Ib;                              // lane j <= 4: I[t0 + j]
+    {
+        const uint64_t ea = oA < g.a.cap ? oA : g.a.cap, eb = oA < g.b.cap ? oA : g.b.cap;
+        const __amdgpu_buffer_rsrc_t ra = __builtin_amdgcn_make_buffer_rsrc(
+            const_cast<uint8_t*>(g.a.data), (short)0, (int)(uint32_t)ea, kBufferWord3);
+        const __amdgpu_buffer_rsrc_t rb = __builtin_amdgcn_make_buffer_rsrc(
+            const_cast<uint8_t*>(g.b.data), (short)0, (int)(uint32_t)eb, kBufferWord3);
+        const uint32_t tlo = __builtin_amdgcn_readfirstlane((uint32_t)t0);
+#pragma unroll
+        for (int k = 0; k < K; k++) {
+            const uint32_t ob8 = (uint32_t)(kHeaderBytes + 512ull * (tlo + k)) + l * 8u;
+            const auto x = __builtin_amdgcn_raw_buffer_load_b64(ra, ob8, 0, kStreamLoad);
+            const auto y = __builtin_amdgcn_raw_buffer_load_b64(rb, ob8, 0, kStreamLoad);
+            wa[k] = (uint64_t)x[0] | ((uint64_t)x[1] << 32);
+            wb[k] = (uint64_t)y[0] | ((uint64_t)y[1] << 32);
+        }
+        const uint32_t oi = (uint32_t)(oI + 4ull * tlo) + (l <= (uint32_t)K ? 4u * l : 0u);
+        Ia = __builtin_amdgcn_raw_buffer_load_b32(ra, oi, 0, kStreamLoad);
+        Ib = __builtin_amdgcn_raw_buffer_load_b32(rb, oi, 0, kStreamLoad);
+    }
+    const HeaderView ha = check_header(hwa, g.a.cap, g.n, E::dtype, kFmtPici);
+    const HeaderView hb = check_header(hwb, g.b.cap, g.n, E::dtype, kFmtPici);
+    if (!(ha.ok && hb.ok)) {          // the same in every wave: no partition publishes
+        if (blockIdx.x == 0 && threadIdx.x == 0) set_status(g.ctrl, SPCCL_ERR_CORRUPT_STREAM);
+        return;
+    }
+    if (p >= g.nparts) return;
+    const uint32_t ntile = g.T - t0 < (uint64_t)K ? (uint32_t)(g.T - t0) : (uint32_t)K;
+    const raw* Aa = reinterpret_cast<const raw*>(g.a.data + oA);
+    const raw* Ab = reinterpret_cast<const raw*>(g.b.data + oA);
+    raw* slot = reinterpret_cast<raw*>(g.slots) + (uint64_t)p * kPartElems;
+    uint64_t* Bo = reinterpret_cast<uint64_t*>(g.out + kHeaderBytes);
+
+    PiciCols ca[K], cb[K];
+    bool all_ok = true;
+#pragma unroll
+    for (int k = 0; k < K; k++) {
+        if ((uint32_t)k < ntile) {
+            ca[k] = pici_columns(PiciMeta{wa[k], lane_bcast(Ia, k), lane_bcast(Ia, k + 1)}, ha.nnz, t0 + k, g.n, g.ctrl);
+            cb[k] = pici_columns(PiciMeta{wb[k], lane_bcast(Ib, k), lane_bcast(Ib, k + 1)}, hb.nnz, t0 + k, g.n, g.ctrl);
+            all_ok = all_ok && ca[k].ok && cb[k].ok;
+        } else {
+            ca[k] = PiciCols{0, 0, 0, 0, true};
+            cb[k] = PiciCols{0, 0, 0, 0, true};
         }
     }
+    // the partition's values in one staging round when they fit together
+    const uint32_t a_lo = lane_bcast(Ia, 0), b_lo = lane_bcast(Ib, 0);
+    const uint32_t la = all_ok ? lane_bcast(Ia, ntile) - a_lo : 0u;
+    const uint32_t lb = all_ok ? lane_bcast(Ib, ntile) - b_lo : 0u;
+    const bool whole = all_ok && la + lb <= kChunkVals;
+    bool zero_all = false;
+    if (whole) {
+        raw x[kChunkSlots];
+#pragma unroll
+        for (int j = 0; j < kChunkSlots; j++) {
+            const uint32_t i = l + 64 * j;
+            x[j] = i < la ? Aa[a_lo + i] : (i < la + lb ? Ab[b_lo + (i - la)] : (raw)1);
+        }
+        bool z = false;
+#pragma unroll
+        for (int j = 0; j < kChunkSlots; j++) {
+            const uint32_t i = l + 64 * j;
+            z |= x[j] == 0;
+            if (i < la + lb) in[i] = x[j];
+        }
+        zero_all = __any(z);
+        wave_lds_sync();
+    }
+
+    uint32_t fill = 0, flushed = 0, excl = 0;     // values in the output buffer / written to the slot / before the tile
+    uint32_t tile_rel = 0;                         // lane k < ntile: tile k's offset in the partition
+    auto flush = [&]() {
+        wave_lds_sync();
+        for (uint32_t i = l; i < fill; i += 64) slot[flushed + i] = ob[i];
+        wave_lds_sync();
+        flushed += fill;
+        fill = 0;
+    };
+#pragma unroll
+    for (int k = 0; k < K; k++) {
+        if ((uint32_t)k >= ntile) break;
+        const PiciCols& A = ca[k];
+        const PiciCols& B = cb[k];
+        const uint64_t t = t0 + k;
+        if (l == (uint32_t)k) tile_rel = excl;
+        uint64_t cancel = 0;
+        const bool one = whole || A.cnt + B.cnt <= kChunkVals;
+        uint32_t ia = 0, ib = 0;
+        bool zero = zero_all;
+        if (whole) {
+            ia = (A.base - a_lo) + A.colpref;
+            ib = la + (B.base - b_lo) + B.colpref;
+            cancel = pp_cancel<E>(A.w, B.w, in, ia, ib, zero, true);
+        } else if (one) {
+            wave_lds_sync();
+            const uint32_t sa = pp_stage<E>(A, B, Aa + A.base, Ab + B.base, 0, 64, in, zero);
+            ia = A.colpref;
+            ib = sa + B.colpref;
+            cancel = pp_cancel<E>(A.w, B.w, in, ia, ib, zero, true);
+        } else {
+#pragma unroll 1
+            for (int h = 0; h < PPGroup::count; h++) {
+                const uint32_t c0 = PPGroup::cols * h, c1 = c0 + PPGroup::cols;
+                bool zg;
+                wave_lds_sync();
+                const uint32_t lg = pp_stage<E>(A, B, Aa + A.base, Ab + B.base, c0, c1, in, zg);
+                cancel |= pp_cancel<E>(A.w, B.w, in, A.colpref - lane_bcast(A.colpref, c0),
+                                       lg + B.colpref - lane_bcast(B.colpref, c0), zg, l >= c0 && l < c1);
+            }
+        }
+        const uint64_t wo = (A.w | B.w) & ~cancel;
+        Bo[t * 64 + l] = wo;
+        const uint32_t c = (uint32_t)__popcll(wo);
+        const uint32_t cpo = wave_excl_scan(c);
+        const uint32_t tilecnt = lane_bcast(cpo + c, 63);
+        if (one) {
+            if (fill + tilecnt > kChunkVals) flush();
+            pp_merge<E>(A.w, B.w, wo, in, ia, ib, ob, fill + cpo, true);
+            fill += tilecnt;
+        } else {
+#pragma unroll 1
+            for (int h = 0; h < PPGroup::count; h++) {
+                const uint32_t c0 = PPGroup::cols * h, c1 = c0 + PPGroup::cols;
+                const uint32_t go0 = lane_bcast(cpo, c0), go1 = c1 == 64 ? tilecnt : lane_bcast(cpo, c1);
+                if (fill + (go1 - go0) > kChunkVals) flush();
+                bool zg;
+                wave_lds_sync();
+                const uint32_t lg = pp_stage<E>(A, B, Aa + A.base, Ab + B.base, c0, c1, in, zg);
+                pp_merge<E>(A.w, B.w, wo, in, A.colpref - lane_bcast(A.colpref, c0),
+                            lg + B.colpref - lane_bcast(B.colpref, c0), ob, fill + cpo - go0, l >= c0 && l < c1);
+                fill += go1 - go0;
+            }
+        }
+        excl += tilecnt;
+    }
+    flush();
+    if (l < ntile) reinterpret_cast<uint32_t*>(g.out + oI)[t0 + l] = tile_rel;   // k_place adds the prefix
+    if (l == 0) publish(g.flags, p, epoch30, kFlagAggregate, flushed);
 }
 
 // Second pass of the two-pass Pici sink.  Every aggregate is final when this
@@ -2398,13 +2562,14 @@ spccl_status_t launch_to_pici(int sa, int sb, const PiciSinkArgs& g, hipStream_t
     dim3 grid(g.nparts), block(kBlockThreads);
     if (sa == SRC_PICI && sb == SRC_PICI) {
         if (g.slots) {
-            hipLaunchKernelGGL((k_pp_tile<E, true>), grid, block, 0, st, g);
+            dim3 wgrid((g.nparts + kWavesPerBlock - 1) / kWavesPerBlock);
+            hipLaunchKernelGGL(k_pp_part<E>, wgrid, block, 0, st, g);
             spccl_status_t st1 = launch_status();
             if (st1 != SPCCL_OK) return st1;
             dim3 pgrid((g.nparts + kPlacePer - 1) / kPlacePer);
             hipLaunchKernelGGL(k_place<E>, pgrid, block, 0, st, g);
         } else {
-            hipLaunchKernelGGL((k_pp_tile<E, false>), grid, block, 0, st, g);
+            hipLaunchKernelGGL(k_pp_tile<E>, grid, block, 0, st, g);
         }
         return launch_status();
     }
