@@ -28,6 +28,15 @@ spccl_status_t launch_coo_index(const uint8_t* msg, uint64_t cap, uint64_t n, in
                                 uint32_t epoch, WsCtrl* ctrl, hipStream_t st);
 }  // namespace spccl
 
+namespace spccl {
+// Every launch that publishes look-back words tags them with a fresh epoch,
+// so a workspace never needs clearing between calls: words left by earlier
+// calls carry other epochs (30 bits; a word would have to go unwritten for
+// 2^30 launches to be mistaken).
+static std::atomic<uint32_t> g_epoch{1};
+uint32_t next_epoch() { return g_epoch.fetch_add(1, std::memory_order_relaxed) & 0x3FFFFFFFu; }
+}  // namespace spccl
+
 using namespace spccl;
 
 namespace {
@@ -45,12 +54,6 @@ inline uint64_t value_slots_end(uint64_t n, int32_t dt) {
     return slots_offset(n) + num_parts(n) * kPartElems * elem_bytes(dt);
 }
 
-// Every single-pass launch tags its look-back words with a fresh epoch, so a
-// workspace never needs clearing between calls: words left by earlier calls
-// carry other epochs (30 bits; a word would have to go unwritten for 2^30
-// launches to be mistaken).
-std::atomic<uint32_t> g_epoch{1};
-inline uint32_t next_epoch() { return g_epoch.fetch_add(1, std::memory_order_relaxed) & 0x3FFFFFFFu; }
 inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 // dense arrays need only element alignment (chunks of a rank's buffer start anywhere)
 inline bool aligned_elem(const void* p, int32_t dt) {

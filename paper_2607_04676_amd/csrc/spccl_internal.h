@@ -54,6 +54,9 @@ __host__ __device__ inline uint64_t num_parts(uint64_t n) {
     return p ? p : 1;
 }
 
+// A fresh 30-bit epoch for the look-back words of one launch (host).
+uint32_t next_epoch();
+
 // Source kinds of the tile pipeline.
 enum SrcKind { SRC_NONE = 0, SRC_DENSE = 1, SRC_PICI = 2, SRC_COO = 3 };
 
@@ -138,6 +141,51 @@ struct SlicedBatch {
     uint64_t track_stride;           // doubles between ranks
     uint64_t fmt_stride;             // bytes between ranks
 };
+
+// One step of the canonical ring for a batch of virtual ranks in a single
+// launch (grid y = the rank's place in the batch): each rank's operands,
+// output, look-back words and value slots; sizes, the epoch, capacities and
+// the status word are the launch's base arguments, shared.  An operand
+// pointer replaces the base operand's (a message keeps its header-to-data
+// offset); a null b leaves the base's b.
+struct RankBatch {
+    const uint8_t* a[kMaxBatchRanks];
+    const uint8_t* b[kMaxBatchRanks];
+    uint8_t* out[kMaxBatchRanks];
+    uint8_t* flags[kMaxBatchRanks];     // the rank's look-back words (zeroed once per collective)
+    uint8_t* slots[kMaxBatchRanks];     // the rank's value slots (two-pass Pici sink)
+};
+
+__host__ __device__ inline DevOperand rebase(DevOperand o, const uint8_t* p) {
+    if (o.hdr) {
+        o.data = p + (o.data - o.hdr);
+        o.hdr = p;
+    } else {
+        o.data = p;
+    }
+    return o;
+}
+
+__host__ __device__ inline PiciSinkArgs rank_sink(PiciSinkArgs g, const RankBatch& rb, uint32_t r) {
+    g.a = rebase(g.a, rb.a[r]);
+    if (rb.b[r]) g.b = rebase(g.b, rb.b[r]);
+    g.out = rb.out[r];
+    g.flags = reinterpret_cast<uint64_t*>(rb.flags[r]);
+    g.slots = rb.slots[r];
+    return g;
+}
+
+__host__ __device__ inline DenseSinkArgs rank_dense(DenseSinkArgs g, const RankBatch& rb, uint32_t r) {
+    g.a = rebase(g.a, rb.a[r]);
+    if (rb.b[r]) g.b = rebase(g.b, rb.b[r]);
+    if (g.out_hdr) {
+        g.out_hdr = rb.out[r];
+        g.out = rb.out[r] + kHeaderBytes;
+    } else {
+        g.out = rb.out[r];
+    }
+    return g;
+}
 
 __host__ __device__ inline SlicedArgs batch_rank(const SlicedBatch& b, uint32_t r) {
     SlicedArgs g = b.base;

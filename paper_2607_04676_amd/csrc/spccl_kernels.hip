@@ -1055,7 +1055,7 @@ __device__ __forceinline__ uint32_t lookback(const uint64_t* flags, uint32_t p, 
 // parks its compacted values in its own worst-case slot of the workspace,
 // never waiting on another block; k_place then moves each slot into place.
 template <class E, int SA, int SB, bool Deferred>
-__global__ void __launch_bounds__(kBlockThreads) k_to_pici(PiciSinkArgs g) {
+__device__ __forceinline__ void to_pici_body(const PiciSinkArgs& g) {
     using raw = typename E::raw;
     __shared__ raw stage_all[kWavesPerBlock][E::cap];
     __shared__ uint32_t s_cnt[kWavesPerBlock];
@@ -1177,6 +1177,17 @@ __global__ void __launch_bounds__(kBlockThreads) k_to_pici(PiciSinkArgs g) {
         for (uint64_t b = oI + 4 * (g.T + 1); b < oA; b += 4) *reinterpret_cast<uint32_t*>(g.out + b) = 0u;
         write_header(g.out, kFmtPici, E::dtype, g.n, nnz, oI, oA, oA + nnz * sizeof(raw));
     }
+}
+
+template <class E, int SA, int SB, bool Deferred>
+__global__ void __launch_bounds__(kBlockThreads) k_to_pici(PiciSinkArgs g) {
+    to_pici_body<E, SA, SB, Deferred>(g);
+}
+
+// The count pass of one ring step for a batch of ranks (grid y).
+template <class E, int SA, int SB>
+__global__ void __launch_bounds__(kBlockThreads) k_to_pici_rb(PiciSinkArgs g, RankBatch rb) {
+    to_pici_body<E, SA, SB, true>(rank_sink(g, rb, blockIdx.y));
 }
 
 
@@ -1574,7 +1585,7 @@ constexpr uint32_t kPlacePer = kWavesPerBlock;   // partitions placed by one blo
 // combines the predecessor sum; then every store.  Reads waited for after a
 // store would also wait for that store, hence all reads first.
 template <class E>
-__global__ void __launch_bounds__(kBlockThreads) k_place(PiciSinkArgs g) {
+__device__ __forceinline__ void place_body(const PiciSinkArgs& g) {
     using raw = typename E::raw;
     constexpr int J = 8;
     constexpr uint32_t kEarly = 4;          // slot values per lane read before the aggregate is known
@@ -1692,6 +1703,16 @@ __global__ void __launch_bounds__(kBlockThreads) k_place(PiciSinkArgs g) {
         for (uint64_t b = oI + 4 * (g.T + 1); b < oA; b += 4) *reinterpret_cast<uint32_t*>(g.out + b) = 0u;
         write_header(g.out, kFmtPici, E::dtype, g.n, nnz, oI, oA, oA + nnz * sizeof(raw));
     }
+}
+
+template <class E>
+__global__ void __launch_bounds__(kBlockThreads) k_place(PiciSinkArgs g) {
+    place_body<E>(g);
+}
+
+template <class E>
+__global__ void __launch_bounds__(kBlockThreads) k_place_rb(PiciSinkArgs g, RankBatch rb) {
+    place_body<E>(rank_sink(g, rb, blockIdx.y));
 }
 
 // ---------------------------------------------------------------------------
@@ -1942,7 +1963,7 @@ __device__ __forceinline__ void store_tile(uint8_t* out, uint64_t t, uint64_t n,
 }
 
 template <class E, int SA, int SB>
-__global__ void __launch_bounds__(kBlockThreads) k_to_dense(DenseSinkArgs g) {
+__device__ __forceinline__ void to_dense_body(const DenseSinkArgs& g) {
     using raw = typename E::raw;
     constexpr bool coo = SA == SRC_COO || SB == SRC_COO;
     __shared__ raw stage_all[kWavesPerBlock][E::cap];
@@ -1961,6 +1982,16 @@ __global__ void __launch_bounds__(kBlockThreads) k_to_dense(DenseSinkArgs g) {
         write_header(g.out_hdr, kFmtDense, E::dtype, g.n, kNnzUnknown, 0, kHeaderBytes, dense_msg_bytes(g.n, E::dtype));
     if (!has_tile || stored) return;
     store_tile<E>(g.out, t, g.n, v);
+}
+
+template <class E, int SA, int SB>
+__global__ void __launch_bounds__(kBlockThreads) k_to_dense(DenseSinkArgs g) {
+    to_dense_body<E, SA, SB>(g);
+}
+
+template <class E, int SA, int SB>
+__global__ void __launch_bounds__(kBlockThreads) k_to_dense_rb(DenseSinkArgs g, RankBatch rb) {
+    to_dense_body<E, SA, SB>(rank_dense(g, rb, blockIdx.y));
 }
 
 // Expansion of P parts (all-gather receive side and decompress): the format
@@ -2171,18 +2202,18 @@ __device__ __forceinline__ void expand_tiles(const uint8_t* msg, const uint8_t* 
 }
 
 template <class E, int K>
-__global__ void __launch_bounds__(kBlockThreads) k_gather(GatherArgs g) {
+__device__ __forceinline__ void gather_body(const DevOperand& op, uint8_t* out_part, uint64_t n, uint64_t T,
+                                            WsCtrl* ctrl) {
     using raw = typename E::raw;
     __shared__ raw stage_all[kWavesPerBlock][kChunkVals];
     __shared__ uint32_t s_ok, s_fmt;
     __shared__ uint64_t s_nnz;
     const uint32_t wave = threadIdx.x >> 6;
-    const DevOperand op = g.part[blockIdx.y];
     if (threadIdx.x == 0) {
         if (op.hdr) {
-            HeaderView h = read_header(op.hdr, op.cap, g.n, E::dtype, -1);
+            HeaderView h = read_header(op.hdr, op.cap, n, E::dtype, -1);
             s_ok = h.ok; s_fmt = h.fmt; s_nnz = h.nnz;
-            if (!h.ok && blockIdx.x == 0) set_status(g.ctrl, SPCCL_ERR_CORRUPT_STREAM);
+            if (!h.ok && blockIdx.x == 0) set_status(ctrl, SPCCL_ERR_CORRUPT_STREAM);
         } else {
             s_ok = 1; s_fmt = kFmtDense; s_nnz = 0;
         }
@@ -2190,10 +2221,23 @@ __global__ void __launch_bounds__(kBlockThreads) k_gather(GatherArgs g) {
     __syncthreads();
     if (!s_ok) return;
     const uint64_t t0 = ((uint64_t)blockIdx.x * kWavesPerBlock + wave) * K;
-    if (t0 >= g.T) return;
-    raw* out = reinterpret_cast<raw*>(g.out + (uint64_t)blockIdx.y * g.n * sizeof(raw));
+    if (t0 >= T) return;
+    raw* out = reinterpret_cast<raw*>(out_part);
     const uint8_t* d = op.hdr ? op.hdr + kHeaderBytes : op.data;
-    expand_tiles<E, K>(op.data, d, s_fmt, s_nnz, g.n, g.T, t0, out, stage_all[wave], g.ctrl);
+    expand_tiles<E, K>(op.data, d, s_fmt, s_nnz, n, T, t0, out, stage_all[wave], ctrl);
+}
+
+template <class E, int K>
+__global__ void __launch_bounds__(kBlockThreads) k_gather(GatherArgs g) {
+    gather_body<E, K>(g.part[blockIdx.y], g.out + (uint64_t)blockIdx.y * g.n * sizeof(typename E::raw), g.n, g.T,
+                      g.ctrl);
+}
+
+// One all-gather hop for a batch of ranks (grid y): each rank expands its
+// received message (part rebased to rb.a) into rb.out.
+template <class E, int K>
+__global__ void __launch_bounds__(kBlockThreads) k_gather_rb(DevOperand part, uint64_t n, WsCtrl* ctrl, RankBatch rb) {
+    gather_body<E, K>(rebase(part, rb.a[blockIdx.y]), rb.out[blockIdx.y], n, num_tiles(n), ctrl);
 }
 
 // ---------------------------------------------------------------------------
@@ -2441,9 +2485,9 @@ __global__ void __launch_bounds__(kBlockThreads) k_copy_sliced_batch(SlicedBatch
 // dense (+) dense -> dense, 16 bytes per lane per step (the dense ring step)
 
 template <class E>
-__global__ void __launch_bounds__(256) k_dense_dense(const uint8_t* a_hdr, const uint8_t* a, uint64_t a_cap,
-                                                     const uint8_t* b_hdr, const uint8_t* b, uint64_t b_cap,
-                                                     uint8_t* out_hdr, uint8_t* out, uint64_t n, WsCtrl* ctrl) {
+__device__ __forceinline__ void dense_dense_body(const uint8_t* a_hdr, const uint8_t* a, uint64_t a_cap,
+                                                 const uint8_t* b_hdr, const uint8_t* b, uint64_t b_cap,
+                                                 uint8_t* out_hdr, uint8_t* out, uint64_t n, WsCtrl* ctrl) {
     using raw = typename E::raw;
     __shared__ uint32_t s_ok;
     if (threadIdx.x == 0) {
@@ -2486,11 +2530,24 @@ __global__ void __launch_bounds__(256) k_dense_dense(const uint8_t* a_hdr, const
         oe[i] = (raw)oplus(E{}, ae[i], be[i]);
 }
 
+template <class E>
+__global__ void __launch_bounds__(256) k_dense_dense(const uint8_t* a_hdr, const uint8_t* a, uint64_t a_cap,
+                                                     const uint8_t* b_hdr, const uint8_t* b, uint64_t b_cap,
+                                                     uint8_t* out_hdr, uint8_t* out, uint64_t n, WsCtrl* ctrl) {
+    dense_dense_body<E>(a_hdr, a, a_cap, b_hdr, b, b_cap, out_hdr, out, n, ctrl);
+}
+
+template <class E>
+__global__ void __launch_bounds__(256) k_dense_dense_rb(DenseSinkArgs g, RankBatch rb) {
+    const DenseSinkArgs r = rank_dense(g, rb, blockIdx.y);
+    dense_dense_body<E>(r.a.hdr, r.a.data, r.a.cap, r.b.hdr, r.b.data, r.b.cap, r.out_hdr, r.out, g.n, g.ctrl);
+}
+
 // ---------------------------------------------------------------------------
 // message copy sized on the device (the virtual-rank send)
 
-__global__ void __launch_bounds__(256) k_copy_message(const uint8_t* src, uint64_t src_cap, uint8_t* dst,
-                                                      uint64_t dst_cap, WsCtrl* ctrl) {
+__device__ __forceinline__ void copy_message_body(const uint8_t* src, uint64_t src_cap, uint8_t* dst,
+                                                  uint64_t dst_cap, WsCtrl* ctrl) {
     __shared__ uint64_t s_total;
     if (threadIdx.x == 0) {
         uint64_t total = 0;
@@ -2515,8 +2572,19 @@ __global__ void __launch_bounds__(256) k_copy_message(const uint8_t* src, uint64
         for (uint64_t b = nvec * 16 + threadIdx.x; b < total; b += blockDim.x) dst[b] = src[b];
 }
 
+__global__ void __launch_bounds__(256) k_copy_message(const uint8_t* src, uint64_t src_cap, uint8_t* dst,
+                                                      uint64_t dst_cap, WsCtrl* ctrl) {
+    copy_message_body(src, src_cap, dst, dst_cap, ctrl);
+}
+
+// The sends of one ring step for a batch of ranks (grid y): rb.a -> rb.out.
+__global__ void __launch_bounds__(256) k_copy_message_rb(uint64_t src_cap, uint64_t dst_cap, WsCtrl* ctrl,
+                                                         RankBatch rb) {
+    copy_message_body(rb.a[blockIdx.y], src_cap, rb.out[blockIdx.y], dst_cap, ctrl);
+}
+
 template <class E>
-__global__ void __launch_bounds__(256) k_encode_dense(const uint8_t* src, uint8_t* out, uint64_t n) {
+__device__ __forceinline__ void encode_dense_body(const uint8_t* src, uint8_t* out, uint64_t n) {
     if (blockIdx.x == 0 && threadIdx.x == 0)
         write_header(out, kFmtDense, E::dtype, n, kNnzUnknown, 0, kHeaderBytes, dense_msg_bytes(n, E::dtype));
     using raw = typename E::raw;
@@ -2532,6 +2600,17 @@ __global__ void __launch_bounds__(256) k_encode_dense(const uint8_t* src, uint8_
     raw* de = reinterpret_cast<raw*>(out + kHeaderBytes);
     for (uint64_t i = nvec * 16 / sizeof(raw) + (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride)
         de[i] = se[i];
+}
+
+template <class E>
+__global__ void __launch_bounds__(256) k_encode_dense(const uint8_t* src, uint8_t* out, uint64_t n) {
+    encode_dense_body<E>(src, out, n);
+}
+
+// Dense sends of one ring step for a batch of ranks (grid y): rb.a -> rb.out.
+template <class E>
+__global__ void __launch_bounds__(256) k_encode_dense_rb(uint64_t n, RankBatch rb) {
+    encode_dense_body<E>(rb.a[blockIdx.y], rb.out[blockIdx.y], n);
 }
 
 __global__ void __launch_bounds__(256) k_fill_zero(uint4* p, uint64_t nvec, uint8_t* tail, uint64_t ntail) {
@@ -2738,6 +2817,89 @@ spccl_status_t launch_copy_sliced_batch(const SlicedBatch& b, uint32_t ranks, hi
     const uint64_t S = num_slices(b.base.n);
     hipLaunchKernelGGL(k_copy_sliced_batch, dim3((unsigned)((S + kWavesPerBlock - 1) / kWavesPerBlock), ranks),
                        dim3(kBlockThreads), 0, st, b, S);
+    return launch_status();
+}
+
+// ---- batched launches of one canonical ring step (grid y = rank) ----------
+// Grid-stride kernels give each rank a share of about 4096 blocks.
+inline uint32_t per_rank_cap(uint32_t ranks) { return ranks >= 64 ? 64u : 4096u / ranks; }
+
+template <class E>
+spccl_status_t launch_to_pici_rb(int sa, int sb, const PiciSinkArgs& g, const RankBatch& rb, uint32_t ranks,
+                                 hipStream_t st) {
+    const dim3 grid(g.nparts, ranks), block(kBlockThreads);
+    if (sa == SRC_DENSE && sb == SRC_NONE) hipLaunchKernelGGL((k_to_pici_rb<E, SRC_DENSE, SRC_NONE>), grid, block, 0, st, g, rb);
+    else if (sa == SRC_PICI && sb == SRC_DENSE) hipLaunchKernelGGL((k_to_pici_rb<E, SRC_PICI, SRC_DENSE>), grid, block, 0, st, g, rb);
+    else if (sa == SRC_DENSE && sb == SRC_DENSE) hipLaunchKernelGGL((k_to_pici_rb<E, SRC_DENSE, SRC_DENSE>), grid, block, 0, st, g, rb);
+    else return SPCCL_ERR_UNSUPPORTED;
+    spccl_status_t s1 = launch_status();
+    if (s1 != SPCCL_OK) return s1;
+    hipLaunchKernelGGL(k_place_rb<E>, dim3((g.nparts + kPlacePer - 1) / kPlacePer, ranks), block, 0, st, g, rb);
+    return launch_status();
+}
+
+template <class E>
+spccl_status_t launch_to_dense_rb(int sa, int sb, const DenseSinkArgs& g, const RankBatch& rb, uint32_t ranks,
+                                  hipStream_t st) {
+    if (sa == SRC_DENSE && sb == SRC_DENSE) {
+        const uint64_t vec = g.n / (16 / sizeof(typename E::raw));
+        hipLaunchKernelGGL(k_dense_dense_rb<E>, dim3(stream_grid(vec, 256 * 4, per_rank_cap(ranks)), ranks), dim3(256), 0,
+                           st, g, rb);
+    } else if (sa == SRC_PICI && sb == SRC_DENSE) {
+        hipLaunchKernelGGL((k_to_dense_rb<E, SRC_PICI, SRC_DENSE>),
+                           dim3(stream_grid(g.T, kWavesPerBlock, 0x7FFFFFFF), ranks), dim3(kBlockThreads), 0, st, g, rb);
+    } else {
+        return SPCCL_ERR_UNSUPPORTED;
+    }
+    return launch_status();
+}
+
+spccl_status_t launch_to_pici_rb_dt(int dtype, int sa, int sb, const PiciSinkArgs& g, const RankBatch& rb,
+                                    uint32_t ranks, hipStream_t st) {
+    if (ranks == 0 || ranks > (uint32_t)kMaxBatchRanks || !g.slots) return SPCCL_ERR_INVALID_ARG;
+    return dtype == kBF16 ? launch_to_pici_rb<BF16>(sa, sb, g, rb, ranks, st)
+                          : launch_to_pici_rb<F32>(sa, sb, g, rb, ranks, st);
+}
+
+spccl_status_t launch_to_dense_rb_dt(int dtype, int sa, int sb, const DenseSinkArgs& g, const RankBatch& rb,
+                                     uint32_t ranks, hipStream_t st) {
+    if (ranks == 0 || ranks > (uint32_t)kMaxBatchRanks) return SPCCL_ERR_INVALID_ARG;
+    return dtype == kBF16 ? launch_to_dense_rb<BF16>(sa, sb, g, rb, ranks, st)
+                          : launch_to_dense_rb<F32>(sa, sb, g, rb, ranks, st);
+}
+
+spccl_status_t launch_copy_message_rb(uint64_t src_cap, uint64_t dst_cap, WsCtrl* ctrl, const RankBatch& rb,
+                                      uint32_t ranks, hipStream_t st) {
+    if (ranks == 0 || ranks > (uint32_t)kMaxBatchRanks) return SPCCL_ERR_INVALID_ARG;
+    const uint64_t cap = src_cap < dst_cap ? src_cap : dst_cap;
+    hipLaunchKernelGGL(k_copy_message_rb, dim3(stream_grid(cap / 16, 256 * 4, per_rank_cap(ranks)), ranks), dim3(256),
+                       0, st, src_cap, dst_cap, ctrl, rb);
+    return launch_status();
+}
+
+spccl_status_t launch_encode_dense_rb_dt(int dtype, uint64_t n, const RankBatch& rb, uint32_t ranks, hipStream_t st) {
+    if (ranks == 0 || ranks > (uint32_t)kMaxBatchRanks) return SPCCL_ERR_INVALID_ARG;
+    const dim3 grid(stream_grid(n * elem_bytes(dtype) / 16, 256 * 4, per_rank_cap(ranks)), ranks), block(256);
+    if (dtype == kBF16) hipLaunchKernelGGL(k_encode_dense_rb<BF16>, grid, block, 0, st, n, rb);
+    else hipLaunchKernelGGL(k_encode_dense_rb<F32>, grid, block, 0, st, n, rb);
+    return launch_status();
+}
+
+// One expansion per rank: rb.a[r] (a message, any format, or an array) into
+// rb.out[r]; part gives the operand's kind (hdr null: an array) and capacity.
+spccl_status_t launch_gather_rb_dt(int dtype, const DevOperand& part, uint64_t n, WsCtrl* ctrl, const RankBatch& rb,
+                                   uint32_t ranks, hipStream_t st) {
+    if (ranks == 0 || ranks > (uint32_t)kMaxBatchRanks) return SPCCL_ERR_INVALID_ARG;
+    const uint64_t T = num_tiles(n);
+    const int K = T * ranks >= 2 * 8192 ? 2 : 1;
+    const dim3 grid(stream_grid(T, kWavesPerBlock * K, 0x7FFFFFFF), ranks), block(kBlockThreads);
+    if (dtype == kBF16) {
+        if (K == 2) hipLaunchKernelGGL((k_gather_rb<BF16, 2>), grid, block, 0, st, part, n, ctrl, rb);
+        else hipLaunchKernelGGL((k_gather_rb<BF16, 1>), grid, block, 0, st, part, n, ctrl, rb);
+    } else {
+        if (K == 2) hipLaunchKernelGGL((k_gather_rb<F32, 2>), grid, block, 0, st, part, n, ctrl, rb);
+        else hipLaunchKernelGGL((k_gather_rb<F32, 1>), grid, block, 0, st, part, n, ctrl, rb);
+    }
     return launch_status();
 }
 

@@ -33,6 +33,16 @@ using namespace spccl;
 namespace spccl {
 spccl_status_t launch_sliced_batch_dt(int dtype, const SlicedBatch& b, uint32_t ranks, int op, hipStream_t st);
 spccl_status_t launch_copy_sliced_batch(const SlicedBatch& b, uint32_t ranks, hipStream_t st);
+spccl_status_t launch_to_pici_rb_dt(int dtype, int sa, int sb, const PiciSinkArgs& g, const RankBatch& rb,
+                                    uint32_t ranks, hipStream_t st);
+spccl_status_t launch_to_dense_rb_dt(int dtype, int sa, int sb, const DenseSinkArgs& g, const RankBatch& rb,
+                                     uint32_t ranks, hipStream_t st);
+spccl_status_t launch_copy_message_rb(uint64_t src_cap, uint64_t dst_cap, WsCtrl* ctrl, const RankBatch& rb,
+                                      uint32_t ranks, hipStream_t st);
+spccl_status_t launch_encode_dense_rb_dt(int dtype, uint64_t n, const RankBatch& rb, uint32_t ranks, hipStream_t st);
+spccl_status_t launch_gather_rb_dt(int dtype, const DevOperand& part, uint64_t n, WsCtrl* ctrl, const RankBatch& rb,
+                                   uint32_t ranks, hipStream_t st);
+spccl_status_t launch_fill_zero(void* p, uint64_t bytes, hipStream_t st);
 }  // namespace spccl
 
 namespace {
@@ -45,12 +55,23 @@ inline bool overlaps(const void* a, uint64_t an, const void* b, uint64_t bn) {
 }
 inline hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s); }
 
+// Scratch of the canonical collectives: one full workspace (its control block
+// holds the status word every launch of the call reports to; the per-rank
+// calls of COO sends use the rest), then for the batched Pici launches one
+// region of look-back words and one of value slots per rank, then 3 * P
+// message buffers.
 struct Layout {
     uint8_t* ws;
     uint64_t ws_bytes;
+    uint8_t* flags;             // P regions of look-back words (zeroed at the start of a call)
+    uint64_t flag_bytes;        // per rank
+    uint8_t* vslots;            // P regions of value slots
+    uint64_t vslot_bytes;       // per rank
     uint64_t slot_bytes;        // capacity of one message buffer
     uint8_t* slots;             // 3 * P message buffers
     uint8_t* slot(int which, int r, int P) const { return slots + ((uint64_t)which * P + r) * slot_bytes; }
+    uint8_t* rank_flags(int r) const { return flags + (uint64_t)r * flag_bytes; }
+    uint8_t* rank_slots(int r) const { return vslots + (uint64_t)r * vslot_bytes; }
 };
 
 // every message buffer holds the worst case of any format: COO's for long
@@ -60,17 +81,32 @@ uint64_t slot_need(uint64_t msg_elems, int32_t dtype) {
     return round_up(c > p ? c : p);
 }
 
-uint64_t scratch_need(int32_t P, uint64_t msg_elems, int32_t dtype) {
-    return round_up(spccl_workspace_bytes(msg_elems, dtype)) + 3ull * (uint64_t)P * slot_need(msg_elems, dtype);
-}
-
 Layout carve(void* scratch, int32_t P, uint64_t msg_elems, int32_t dtype) {
     Layout L;
     L.ws = static_cast<uint8_t*>(scratch);
     L.ws_bytes = round_up(spccl_workspace_bytes(msg_elems, dtype));
+    L.flags = L.ws + L.ws_bytes;
+    L.flag_bytes = round_up(8ull * num_parts(msg_elems));
+    L.vslots = L.flags + (uint64_t)P * L.flag_bytes;
+    L.vslot_bytes = round_up(num_parts(msg_elems) * kPartElems * elem_bytes(dtype));
     L.slot_bytes = slot_need(msg_elems, dtype);
-    L.slots = L.ws + L.ws_bytes;
+    L.slots = L.vslots + (uint64_t)P * L.vslot_bytes;
     return L;
+}
+
+uint64_t scratch_need(int32_t P, uint64_t msg_elems, int32_t dtype) {
+    const Layout L = carve(nullptr, P, msg_elems, dtype);
+    return (uint64_t)(L.slots - L.ws) + 3ull * (uint64_t)P * L.slot_bytes;
+}
+
+// Zero the parts of the scratch that must start clear: the workspace's
+// control block, look-back words and tile indexes, and every rank's
+// look-back words (the value slots and message buffers are written before
+// they are read).
+spccl_status_t init_scratch(const Layout& L, int32_t P, uint64_t msg_elems, int32_t dtype, hipStream_t st) {
+    spccl_status_t s1 = launch_fill_zero(L.ws, spccl_workspace_min_bytes(msg_elems, dtype), st);
+    if (s1 != SPCCL_OK) return s1;
+    return launch_fill_zero(L.flags, (uint64_t)P * L.flag_bytes, st);
 }
 
 double link_tau(const spccl_policy_t& pol, int r, int P) {
@@ -125,6 +161,221 @@ bool policy_ok(const spccl_policy_t& pol) {
         spccl_status_t st_ = (x);                  \
         if (st_ != SPCCL_OK) return st_;           \
     } while (0)
+
+// ---- batched ring steps (Pici sends) -------------------------------------
+// Every ring step launches each kernel once for all ranks that take the same
+// path (grid y = rank, up to kMaxBatchRanks per launch): the P reductions,
+// sends and expansions of a step are independent of each other.  Decisions
+// stay on the host, from the headers read once per step.
+
+struct RankPtrs {
+    const uint8_t* a;
+    const uint8_t* b;
+    uint8_t* out;
+};
+
+// launch(rb, count) for the given ranks in batches of up to kMaxBatchRanks,
+// each rank's pointers from ptrs(rank) and its own look-back words and slots.
+template <class Ptrs, class Launch>
+spccl_status_t batched(const Layout& L, const std::vector<int>& ranks, Ptrs ptrs, Launch launch) {
+    for (size_t i = 0; i < ranks.size(); i += kMaxBatchRanks) {
+        const uint32_t cnt = (uint32_t)(ranks.size() - i < (size_t)kMaxBatchRanks ? ranks.size() - i : kMaxBatchRanks);
+        RankBatch rb{};
+        for (uint32_t j = 0; j < cnt; j++) {
+            const int r = ranks[i + j];
+            const RankPtrs q = ptrs(r);
+            rb.a[j] = q.a;
+            rb.b[j] = q.b;
+            rb.out[j] = q.out;
+            rb.flags[j] = L.rank_flags(r);
+            rb.slots[j] = L.rank_slots(r);
+        }
+        SPCCL_TRY(launch(rb, cnt));
+    }
+    return SPCCL_OK;
+}
+
+// an operand whose pointer comes from the batch: an array, a Pici (or any)
+// message, a dense message
+DevOperand arr_op(uint64_t bytes) { return DevOperand{nullptr, nullptr, bytes}; }
+DevOperand msg_op(const Layout& L) { return DevOperand{L.slots, L.slots, L.slot_bytes}; }
+DevOperand dense_msg_op(const Layout& L) { return DevOperand{L.slots, L.slots + kHeaderBytes, L.slot_bytes}; }
+
+PiciSinkArgs sink_args(const Layout& L, uint64_t m, DevOperand a, DevOperand b) {
+    PiciSinkArgs g{};
+    g.a = a;
+    g.b = b;
+    g.n = m;
+    g.T = num_tiles(m);
+    g.nparts = (uint32_t)num_parts(m);
+    g.epoch = next_epoch();
+    g.ctrl = reinterpret_cast<WsCtrl*>(L.ws);
+    g.slots = L.vslots;           // each rank's own, from the batch
+    g.flags = reinterpret_cast<uint64_t*>(L.flags);
+    return g;
+}
+
+DenseSinkArgs dense_args(const Layout& L, uint64_t m, DevOperand a, DevOperand b, bool out_msg) {
+    DenseSinkArgs g{};
+    g.a = a;
+    g.b = b;
+    g.out_hdr = out_msg ? L.slots : nullptr;
+    g.out = out_msg ? L.slots + kHeaderBytes : L.slots;
+    g.n = m;
+    g.T = num_tiles(m);
+    g.ctrl = reinterpret_cast<WsCtrl*>(L.ws);
+    return g;
+}
+
+// Compress src(r) (m elements) into out(r) for the given ranks: Pici, or a
+// dense message for the ranks in `dense`.
+template <class Src, class Out>
+spccl_status_t batched_encode(const Layout& L, const std::vector<int>& ranks, const std::vector<char>& dense,
+                              uint64_t m, int32_t dtype, Src src, Out out, hipStream_t st) {
+    std::vector<int> sp, dn;
+    for (int r : ranks) (dense[r] ? dn : sp).push_back(r);
+    const uint64_t s = elem_bytes(dtype);
+    if (!sp.empty()) {
+        const PiciSinkArgs g = sink_args(L, m, arr_op(m * s), DevOperand{});
+        SPCCL_TRY(batched(L, sp, [&](int r) { return RankPtrs{src(r), nullptr, out(r)}; },
+                          [&](const RankBatch& rb, uint32_t c) {
+                              return launch_to_pici_rb_dt(dtype, SRC_DENSE, SRC_NONE, g, rb, c, st);
+                          }));
+    }
+    if (!dn.empty())
+        SPCCL_TRY(batched(L, dn, [&](int r) { return RankPtrs{src(r), nullptr, out(r)}; },
+                          [&](const RankBatch& rb, uint32_t c) { return launch_encode_dense_rb_dt(dtype, m, rb, c, st); }));
+    return SPCCL_OK;
+}
+
+// The batched reduce-scatter (Pici sends); the same decisions, messages and
+// trace as ring_rs.
+spccl_status_t ring_rs_batched(void* const* send, void* const* out, int P, uint64_t n, int dtype,
+                               const spccl_policy_t& pol, const Layout& L, spccl_trace_t* trace,
+                               std::vector<double>& sig0, std::vector<double>& sigp, hipStream_t st) {
+    const uint64_t m = n / (uint64_t)P, s = elem_bytes(dtype);
+    auto chunk = [&](int r, int c) { return static_cast<const uint8_t*>(send[r]) + (uint64_t)c * m * s; };
+    std::vector<int> all(P), fmt(P, SPCCL_FMT_PICI);
+    for (int r = 0; r < P; r++) all[r] = r;
+    std::vector<spccl_header_t> h;
+    WsCtrl* ctrl = reinterpret_cast<WsCtrl*>(L.ws);
+    // step 0: compress every rank's first chunk into slot 0, measure sigma0
+    SPCCL_TRY(batched_encode(L, all, std::vector<char>(P, 0), m, dtype,
+                             [&](int r) { return chunk(r, (r - 1 + P) % P); },
+                             [&](int r) { return L.slot(0, r, P); }, st));
+    SPCCL_TRY(read_headers(L, 0, P, h, st));
+    std::vector<char> dense(P, 0);
+    for (int r = 0; r < P; r++) {
+        sig0[r] = sigp[r] = sparsity(m, h[r].nnz);
+        dense[r] = send_dense(pol, sig0[r], link_tau(pol, r, P));
+        fmt[r] = dense[r] ? SPCCL_FMT_DENSE : SPCCL_FMT_PICI;
+        put_trace(trace, r, 0, r, fmt[r], 1, dense[r] ? dense_msg_bytes(m, dtype) : h[r].total_bytes, h[r].nnz,
+                  sigp[r]);
+    }
+    std::vector<int> dn;
+    for (int r = 0; r < P; r++)
+        if (dense[r]) dn.push_back(r);
+    if (!dn.empty())
+        SPCCL_TRY(batched(L, dn, [&](int r) { return RankPtrs{chunk(r, (r - 1 + P) % P), nullptr, L.slot(0, r, P)}; },
+                          [&](const RankBatch& rb, uint32_t c) { return launch_encode_dense_rb_dt(dtype, m, rb, c, st); }));
+    for (int step = 1; step <= P - 1; step++) {
+        // every send of the previous step arrives: rank r receives rank r-1's message
+        SPCCL_TRY(batched(L, all, [&](int r) { return RankPtrs{L.slot(0, (r - 1 + P) % P, P), nullptr, L.slot(1, r, P)}; },
+                          [&](const RankBatch& rb, uint32_t c) {
+                              return launch_copy_message_rb(L.slot_bytes, L.slot_bytes, ctrl, rb, c, st);
+                          }));
+        std::vector<int> in_fmt(P);
+        for (int r = 0; r < P; r++) in_fmt[r] = fmt[(r - 1 + P) % P];
+        auto own = [&](int r) { return chunk(r, (r - step - 1 + 2 * P) % P); };
+        const bool last = step == P - 1;
+        // per rank: the send format of this step (the last one reduces into out[r])
+        std::vector<char> to_dense(P, 0);
+        if (!last)
+            for (int r = 0; r < P; r++) {
+                const double est = sigp[r] * sig0[r];   // Eq. 7
+                to_dense[r] = send_dense(pol, est, link_tau(pol, r, P));
+                if (to_dense[r]) {
+                    fmt[r] = SPCCL_FMT_DENSE;
+                    sigp[r] = est;
+                    put_trace(trace, step * P + r, step, r, SPCCL_FMT_DENSE, 0, dense_msg_bytes(m, dtype),
+                              SPCCL_NNZ_UNKNOWN, est);
+                } else {
+                    fmt[r] = SPCCL_FMT_PICI;
+                }
+            }
+        bool any_measured = false;
+        for (int in_pici = 0; in_pici <= 1; in_pici++) {
+            const DevOperand a_op = in_pici ? msg_op(L) : dense_msg_op(L);
+            const int sa = in_pici ? SRC_PICI : SRC_DENSE;
+            std::vector<int> to_p, to_d;
+            for (int r = 0; r < P; r++) {
+                if ((in_fmt[r] == SPCCL_FMT_PICI) != (bool)in_pici) continue;
+                (last || to_dense[r] ? to_d : to_p).push_back(r);
+            }
+            auto ptrs = [&](int r) {
+                return RankPtrs{L.slot(1, r, P), own(r), last ? static_cast<uint8_t*>(out[r]) : L.slot(0, r, P)};
+            };
+            if (!to_p.empty()) {
+                any_measured = true;
+                const PiciSinkArgs g = sink_args(L, m, a_op, arr_op(m * s));
+                SPCCL_TRY(batched(L, to_p, ptrs, [&](const RankBatch& rb, uint32_t c) {
+                    return launch_to_pici_rb_dt(dtype, sa, SRC_DENSE, g, rb, c, st);
+                }));
+            }
+            if (!to_d.empty()) {
+                const DenseSinkArgs g = dense_args(L, m, a_op, arr_op(m * s), !last);
+                SPCCL_TRY(batched(L, to_d, ptrs, [&](const RankBatch& rb, uint32_t c) {
+                    return launch_to_dense_rb_dt(dtype, sa, SRC_DENSE, g, rb, c, st);
+                }));
+            }
+        }
+        if (any_measured && !last) {
+            SPCCL_TRY(read_headers(L, 0, P, h, st));
+            for (int r = 0; r < P; r++) {
+                if (fmt[r] != SPCCL_FMT_PICI) continue;
+                sigp[r] = sparsity(m, h[r].nnz);
+                put_trace(trace, step * P + r, step, r, SPCCL_FMT_PICI, 1, h[r].total_bytes, h[r].nnz, sigp[r]);
+            }
+        }
+    }
+    return SPCCL_OK;
+}
+
+// All-gather of P parts of `len` elements: part q is encoded once by rank q
+// (slot 0 holds those messages, of any format), travels the ring unchanged,
+// and is expanded into out[r] + q*len by every rank r != q; each rank's own
+// part is copied from own[r] unless it already sits in place.  One copy
+// launch and one expansion launch per hop.
+spccl_status_t ring_ag_batched(void* const* own, void* const* out, int P, uint64_t len, int dtype, const Layout& L,
+                               hipStream_t st) {
+    const uint64_t s = elem_bytes(dtype);
+    for (int r = 0; r < P; r++) {
+        uint8_t* dst = static_cast<uint8_t*>(out[r]) + (uint64_t)r * len * s;
+        if (len && dst != own[r] && hipMemcpyAsync(dst, own[r], len * s, hipMemcpyDeviceToDevice, st) != hipSuccess)
+            return SPCCL_ERR_HIP;
+    }
+    std::vector<int> all(P);
+    for (int r = 0; r < P; r++) all[r] = r;
+    WsCtrl* ctrl = reinterpret_cast<WsCtrl*>(L.ws);
+    for (int k = 0; k < P - 1; k++) {
+        const int in_slot = 1 + (k % 2), prev_slot = k == 0 ? 0 : 1 + ((k - 1) % 2);
+        SPCCL_TRY(batched(L, all,
+                          [&](int r) { return RankPtrs{L.slot(prev_slot, (r - 1 + P) % P, P), nullptr, L.slot(in_slot, r, P)}; },
+                          [&](const RankBatch& rb, uint32_t c) {
+                              return launch_copy_message_rb(L.slot_bytes, L.slot_bytes, ctrl, rb, c, st);
+                          }));
+        SPCCL_TRY(batched(L, all,
+                          [&](int r) {
+                              const int q = ((r - 1 - k) % P + P) % P;
+                              return RankPtrs{L.slot(in_slot, r, P), nullptr,
+                                              static_cast<uint8_t*>(out[r]) + (uint64_t)q * len * s};
+                          },
+                          [&](const RankBatch& rb, uint32_t c) {
+                              return launch_gather_rb_dt(dtype, msg_op(L), len, ctrl, rb, c, st);
+                          }));
+    }
+    return SPCCL_OK;
+}
 
 // Reduce-scatter over the chunks; the reduced chunk r goes to out[r] (m
 // elements).  On return sig0 / sigp hold each rank's sigma0 and tracked
@@ -205,33 +456,16 @@ spccl_status_t ring_rs(void* const* send, void* const* out, int P, uint64_t n, i
     return SPCCL_OK;
 }
 
-// All-gather of P parts of `len` elements: part q is encoded once by rank q
-// (slot 0 holds those messages), travels the ring unchanged, and is expanded
-// into out[r] + q*len by every rank r != q; each rank's own part is copied
-// from `own[r]` unless it already sits in place.
-spccl_status_t ring_ag_forward(void* const* own, void* const* out, int P, uint64_t len, int dtype, const Layout& L,
-                               hipStream_t st) {
-    const uint64_t s = elem_bytes(dtype);
-    for (int r = 0; r < P; r++) {
-        uint8_t* dst = static_cast<uint8_t*>(out[r]) + (uint64_t)r * len * s;
-        if (len && dst != own[r] && hipMemcpyAsync(dst, own[r], len * s, hipMemcpyDeviceToDevice, st) != hipSuccess)
-            return SPCCL_ERR_HIP;
+// The reduce-scatter: batched launches for Pici sends, per-rank calls for COO.
+spccl_status_t reduce_scatter(void* const* send, void* const* out, int P, uint64_t n, int dtype,
+                              const spccl_policy_t& pol, const Layout& L, spccl_trace_t* trace, std::vector<double>& sig0,
+                              std::vector<double>& sigp, hipStream_t st) {
+    if (pol.sparse_fmt == SPCCL_FMT_PICI && P > 1) {
+        sig0.assign(P, 1.0);
+        sigp.assign(P, 1.0);
+        return ring_rs_batched(send, out, P, n, dtype, pol, L, trace, sig0, sigp, st);
     }
-    for (int k = 0; k < P - 1; k++) {
-        // step k: rank r receives from rank r-1 what r-1 received at step k-1
-        // (its own message at k = 0): the part of rank q = r-1-k.
-        const int in_slot = 1 + (k % 2), prev_slot = k == 0 ? 0 : 1 + ((k - 1) % 2);
-        for (int r = 0; r < P; r++)
-            SPCCL_TRY(spccl_copy_message(L.slot(prev_slot, (r - 1 + P) % P, P), L.slot_bytes, L.slot(in_slot, r, P),
-                                         L.slot_bytes, L.ws, L.ws_bytes, st));
-        for (int r = 0; r < P; r++) {
-            const int q = ((r - 1 - k) % P + P) % P;
-            const spccl_operand_t part = msg(L.slot(in_slot, r, P), SPCCL_FMT_PICI, L.slot_bytes);
-            uint8_t* dst = static_cast<uint8_t*>(out[r]) + (uint64_t)q * len * s;
-            SPCCL_TRY(spccl_gather_expand(&part, 1, len, dtype, dst, len * s, L.ws, L.ws_bytes, st));
-        }
-    }
-    return SPCCL_OK;
+    return ring_rs(send, out, P, n, dtype, pol, L, trace, sig0, sigp, st);
 }
 
 spccl_status_t check_common(void* const* send, void* const* recv, int32_t P, int32_t dtype, void* scratch,
@@ -305,9 +539,9 @@ spccl_status_t spccl_vr_reduce_scatter(void* const* send, void* const* recv, int
     if (!policy_ok(pol)) return SPCCL_ERR_INVALID_ARG;
     hipStream_t st = as_stream(stream);
     const Layout L = carve(scratch, P, m, dtype);
-    SPCCL_TRY(spccl_workspace_init(L.ws, L.ws_bytes, stream));
+    SPCCL_TRY(init_scratch(L, P, m, dtype, st));
     std::vector<double> sig0, sigp;
-    SPCCL_TRY(ring_rs(send, recv, P, n, dtype, pol, L, trace, sig0, sigp, st));
+    SPCCL_TRY(reduce_scatter(send, recv, P, n, dtype, pol, L, trace, sig0, sigp, st));
     return finish(L, st);
 }
 
@@ -322,13 +556,20 @@ spccl_status_t spccl_vr_all_gather(void* const* send, void* const* recv, int32_t
     if (!policy_ok(pol)) return SPCCL_ERR_INVALID_ARG;
     hipStream_t st = as_stream(stream);
     const Layout L = carve(scratch, P, n, dtype);
-    SPCCL_TRY(spccl_workspace_init(L.ws, L.ws_bytes, stream));
-    for (int q = 0; q < P; q++) SPCCL_TRY(compress_fmt(pol.sparse_fmt, send[q], n, dtype, L, L.slot(0, q, P), st));
+    SPCCL_TRY(init_scratch(L, P, n, dtype, st));
+    std::vector<int> all(P);
+    for (int q = 0; q < P; q++) all[q] = q;
+    if (pol.sparse_fmt == SPCCL_FMT_PICI)
+        SPCCL_TRY(batched_encode(L, all, std::vector<char>(P, 0), n, dtype,
+                                 [&](int q) { return static_cast<const uint8_t*>(send[q]); },
+                                 [&](int q) { return L.slot(0, q, P); }, st));
+    else
+        for (int q = 0; q < P; q++) SPCCL_TRY(compress_fmt(pol.sparse_fmt, send[q], n, dtype, L, L.slot(0, q, P), st));
     std::vector<spccl_header_t> h;
     SPCCL_TRY(read_headers(L, 0, P, h, st));
     for (int q = 0; q < P; q++)
         put_trace(trace, q, 0, q, pol.sparse_fmt, 1, h[q].total_bytes, h[q].nnz, sparsity(n, h[q].nnz));
-    SPCCL_TRY(ring_ag_forward(send, recv, P, n, dtype, L, st));
+    SPCCL_TRY(ring_ag_batched(send, recv, P, n, dtype, L, st));
     return finish(L, st);
 }
 
@@ -344,21 +585,32 @@ spccl_status_t spccl_vr_all_reduce(void* const* send, void* const* recv, int32_t
     if (!policy_ok(pol)) return SPCCL_ERR_INVALID_ARG;
     hipStream_t st = as_stream(stream);
     const Layout L = carve(scratch, P, m, dtype);
-    SPCCL_TRY(spccl_workspace_init(L.ws, L.ws_bytes, stream));
+    SPCCL_TRY(init_scratch(L, P, m, dtype, st));
     // reduce-scatter straight into each rank's own chunk of its output
     std::vector<void*> chunk_out(P);
     for (int r = 0; r < P; r++) chunk_out[r] = static_cast<uint8_t*>(recv[r]) + (uint64_t)r * m * s;
     std::vector<double> sig0, sigp;
-    SPCCL_TRY(ring_rs(send, chunk_out.data(), P, n, dtype, pol, L, trace, sig0, sigp, st));
+    SPCCL_TRY(reduce_scatter(send, chunk_out.data(), P, n, dtype, pol, L, trace, sig0, sigp, st));
     // phase-aware transition: one message per rank, encoded once
     std::vector<int> fmt(P);
     std::vector<double> est(P);
+    std::vector<char> dense(P, 0);
+    std::vector<int> all(P);
     for (int r = 0; r < P; r++) {
+        all[r] = r;
         est[r] = sigp[r] * sig0[r];
-        const bool dense = pol.adaptive == 2 ? true : (pol.adaptive == 0 ? false : est[r] <= pol.ag_thresh);
-        fmt[r] = dense ? SPCCL_FMT_DENSE : pol.sparse_fmt;
-        if (dense) SPCCL_TRY(spccl_encode_dense(chunk_out[r], m, dtype, L.slot(0, r, P), L.slot_bytes, stream));
-        else SPCCL_TRY(compress_fmt(pol.sparse_fmt, chunk_out[r], m, dtype, L, L.slot(0, r, P), st));
+        dense[r] = pol.adaptive == 2 ? true : (pol.adaptive == 0 ? false : est[r] <= pol.ag_thresh);
+        fmt[r] = dense[r] ? SPCCL_FMT_DENSE : pol.sparse_fmt;
+    }
+    if (pol.sparse_fmt == SPCCL_FMT_PICI) {
+        SPCCL_TRY(batched_encode(L, all, dense, m, dtype,
+                                 [&](int r) { return static_cast<const uint8_t*>(chunk_out[r]); },
+                                 [&](int r) { return L.slot(0, r, P); }, st));
+    } else {
+        for (int r = 0; r < P; r++) {
+            if (dense[r]) SPCCL_TRY(spccl_encode_dense(chunk_out[r], m, dtype, L.slot(0, r, P), L.slot_bytes, stream));
+            else SPCCL_TRY(compress_fmt(pol.sparse_fmt, chunk_out[r], m, dtype, L, L.slot(0, r, P), st));
+        }
     }
     std::vector<spccl_header_t> h;
     SPCCL_TRY(read_headers(L, 0, P, h, st));
@@ -368,7 +620,7 @@ spccl_status_t spccl_vr_all_reduce(void* const* send, void* const* recv, int32_t
         put_trace(ag_tr, r, P - 1, r, fmt[r], sparse ? 1 : 0, h[r].total_bytes,
                   sparse ? h[r].nnz : SPCCL_NNZ_UNKNOWN, est[r]);
     }
-    SPCCL_TRY(ring_ag_forward(chunk_out.data(), recv, P, m, dtype, L, st));
+    SPCCL_TRY(ring_ag_batched(chunk_out.data(), recv, P, m, dtype, L, st));
     return finish(L, st);
 }
 
