@@ -148,13 +148,53 @@ struct SlicedBatch {
 // the status word are the launch's base arguments, shared.  An operand
 // pointer replaces the base operand's (a message keeps its header-to-data
 // offset); a null b leaves the base's b.
+// Per rank of a ring whose formats are decided on the device: its sigma0 and
+// tracked sparsity (Sec. IV-C), and the formats of the message it receives
+// and of the one it sends at the current step.
+struct RingRank {
+    double sigma0, sigma_prev;
+    int32_t in_fmt, out_fmt;
+};
+
 struct RankBatch {
     const uint8_t* a[kMaxBatchRanks];
     const uint8_t* b[kMaxBatchRanks];
     uint8_t* out[kMaxBatchRanks];
     uint8_t* flags[kMaxBatchRanks];     // the rank's look-back words (zeroed once per collective)
     uint8_t* slots[kMaxBatchRanks];     // the rank's value slots (two-pass Pici sink)
+    // With gate set, a rank takes part only if its decided formats match
+    // gate_in / gate_out (-1: any); rank[j] indexes gate for batch entry j.
+    const RingRank* gate;
+    int32_t gate_in, gate_out;
+    int32_t rank[kMaxBatchRanks];
 };
+
+// The decisions of one canonical ring step on the device (k_ring_decide):
+// rank r's last send is the message at slots0 + r * slot_bytes.
+enum RingDecide {
+    kDecideFirst = 0,     // after the first compression: sigma0, the first send's format
+    kDecideStep = 1,      // before ring step `step`: the previous step's trace, this step's formats
+    kDecideGather = 2,    // all-reduce transition, before encoding: the gather's formats
+    kDecideGatherSizes = 3,  // after the transition's encoding: its sizes in the trace
+    kDecideAllGather = 4  // a standalone all-gather's sends (every part Pici): their trace
+};
+
+struct RingArgs {
+    RingRank* rr;             // P entries
+    void* trace;              // spccl_trace_t[P * (P - 1) + P] in device memory
+    const uint8_t* slots0;
+    uint64_t slot_bytes;
+    uint64_t m;               // elements per message
+    int32_t P, step, mode, dtype;
+    double intra, inter, ag;  // the policy's thresholds
+    int32_t ranks_per_node, adaptive;
+};
+
+__host__ __device__ inline bool rank_skipped(const RankBatch& rb, uint32_t j) {
+    if (!rb.gate) return false;
+    const RingRank& q = rb.gate[rb.rank[j]];
+    return (rb.gate_in >= 0 && q.in_fmt != rb.gate_in) || (rb.gate_out >= 0 && q.out_fmt != rb.gate_out);
+}
 
 __host__ __device__ inline DevOperand rebase(DevOperand o, const uint8_t* p) {
     if (o.hdr) {

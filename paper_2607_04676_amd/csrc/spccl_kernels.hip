@@ -1187,6 +1187,7 @@ __global__ void __launch_bounds__(kBlockThreads) k_to_pici(PiciSinkArgs g) {
 // The count pass of one ring step for a batch of ranks (grid y).
 template <class E, int SA, int SB>
 __global__ void __launch_bounds__(kBlockThreads) k_to_pici_rb(PiciSinkArgs g, RankBatch rb) {
+    if (rank_skipped(rb, blockIdx.y)) return;
     to_pici_body<E, SA, SB, true>(rank_sink(g, rb, blockIdx.y));
 }
 
@@ -1712,6 +1713,7 @@ __global__ void __launch_bounds__(kBlockThreads) k_place(PiciSinkArgs g) {
 
 template <class E>
 __global__ void __launch_bounds__(kBlockThreads) k_place_rb(PiciSinkArgs g, RankBatch rb) {
+    if (rank_skipped(rb, blockIdx.y)) return;
     place_body<E>(rank_sink(g, rb, blockIdx.y));
 }
 
@@ -1991,6 +1993,7 @@ __global__ void __launch_bounds__(kBlockThreads) k_to_dense(DenseSinkArgs g) {
 
 template <class E, int SA, int SB>
 __global__ void __launch_bounds__(kBlockThreads) k_to_dense_rb(DenseSinkArgs g, RankBatch rb) {
+    if (rank_skipped(rb, blockIdx.y)) return;
     to_dense_body<E, SA, SB>(rank_dense(g, rb, blockIdx.y));
 }
 
@@ -2482,6 +2485,90 @@ __global__ void __launch_bounds__(kBlockThreads) k_copy_sliced_batch(SlicedBatch
 }
 
 // ---------------------------------------------------------------------------
+// Format decisions of the canonical ring on the device (Sec. IV-C), one
+// thread per rank, between the launches of a ring step: the same rule, in
+// the same IEEE double arithmetic, as the host's.  Sparsity = (m - nnz) / m;
+// a send is dense iff its sparsity (first send) or the estimate sigma_prev *
+// sigma0 (Eq. 7, later sends) is <= the link's threshold; a dense send tracks
+// the estimate, a Pici one its measured sparsity.  Each rank's trace entry
+// is written once its values are known: a Pici send's size and count by the
+// next decision, when its header is in.
+
+__device__ __forceinline__ double ring_sparsity(uint64_t m, uint64_t nnz) {
+    return m == 0 ? 1.0 : (double)(m - nnz) / (double)m;
+}
+
+__device__ __forceinline__ bool ring_dense(const RingArgs& a, double sigma, double tau) {
+    if (a.adaptive == 0) return false;
+    if (a.adaptive == 2) return true;
+    return sigma <= tau;
+}
+
+__device__ __forceinline__ double ring_tau(const RingArgs& a, int r) {
+    const int rpn = a.ranks_per_node > 0 ? a.ranks_per_node : a.P;
+    return ((r + 1) % rpn == 0 && rpn < a.P) ? a.inter : a.intra;
+}
+
+__device__ __forceinline__ void put_entry(spccl_trace_t* e, int step, int rank, int fmt, int measured, uint64_t bytes,
+                                          uint64_t nnz, double sigma) {
+    e->step = step; e->rank = rank; e->fmt = fmt; e->measured = measured;
+    e->bytes = bytes; e->nnz = nnz; e->sigma = sigma;
+}
+
+__global__ void __launch_bounds__(256) k_ring_decide(RingArgs a) {
+    spccl_trace_t* tr = static_cast<spccl_trace_t*>(a.trace);
+    const int P = a.P;
+    const uint64_t dense_bytes = dense_msg_bytes(a.m, a.dtype);
+    for (int r = (int)(blockIdx.x * blockDim.x + threadIdx.x); r < P; r += (int)(gridDim.x * blockDim.x)) {
+        RingRank& q = a.rr[r];
+        const HeaderWords h = load_header_words(a.slots0 + (uint64_t)r * a.slot_bytes);
+        const uint32_t fmt = (uint32_t)(h.w[0] >> 32) & 0xFFFFu;
+        const uint64_t nnz = h.w[2], total = h.w[5];
+        if (a.mode == kDecideFirst) {
+            const double sg = ring_sparsity(a.m, nnz);
+            const bool dense = ring_dense(a, sg, ring_tau(a, r));
+            q.sigma0 = q.sigma_prev = sg;
+            q.in_fmt = -1;
+            q.out_fmt = dense ? kFmtDense : kFmtPici;
+            put_entry(&tr[r], 0, r, q.out_fmt, 1, dense ? dense_bytes : total, nnz, sg);
+        } else if (a.mode == kDecideStep) {
+            const int s = a.step;
+            if (s >= 2 && q.out_fmt == kFmtPici) {          // the previous send was measured
+                const double sg = ring_sparsity(a.m, nnz);
+                q.sigma_prev = sg;
+                put_entry(&tr[(s - 1) * P + r], s - 1, r, kFmtPici, 1, total, nnz, sg);
+            }
+            const HeaderWords hp = load_header_words(a.slots0 + (uint64_t)((r - 1 + P) % P) * a.slot_bytes);
+            q.in_fmt = (int32_t)((uint32_t)(hp.w[0] >> 32) & 0xFFFFu);   // what rank r receives now
+            if (s <= P - 2) {
+                const double est = q.sigma_prev * q.sigma0;
+                const bool dense = ring_dense(a, est, ring_tau(a, r));
+                q.out_fmt = dense ? kFmtDense : kFmtPici;
+                if (dense) {
+                    q.sigma_prev = est;
+                    put_entry(&tr[s * P + r], s, r, kFmtDense, 0, dense_bytes, kNnzUnknown, est);
+                }
+            } else {
+                q.out_fmt = -1;                              // the last step reduces into the output
+            }
+        } else if (a.mode == kDecideGather) {
+            const double est = q.sigma_prev * q.sigma0;
+            const bool dense = a.adaptive == 2 ? true : (a.adaptive == 0 ? false : est <= a.ag);
+            q.out_fmt = dense ? kFmtDense : kFmtPici;
+            put_entry(&tr[P * (P - 1) + r], P - 1, r, q.out_fmt, dense ? 0 : 1, dense_bytes, kNnzUnknown, est);
+        } else if (a.mode == kDecideGatherSizes) {
+            if (q.out_fmt == kFmtPici) {
+                tr[P * (P - 1) + r].bytes = total;
+                tr[P * (P - 1) + r].nnz = nnz;
+            }
+        } else {
+            (void)fmt;
+            put_entry(&tr[r], 0, r, kFmtPici, 1, total, nnz, ring_sparsity(a.m, nnz));
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
 // dense (+) dense -> dense, 16 bytes per lane per step (the dense ring step)
 
 template <class E>
@@ -2539,6 +2626,7 @@ __global__ void __launch_bounds__(256) k_dense_dense(const uint8_t* a_hdr, const
 
 template <class E>
 __global__ void __launch_bounds__(256) k_dense_dense_rb(DenseSinkArgs g, RankBatch rb) {
+    if (rank_skipped(rb, blockIdx.y)) return;
     const DenseSinkArgs r = rank_dense(g, rb, blockIdx.y);
     dense_dense_body<E>(r.a.hdr, r.a.data, r.a.cap, r.b.hdr, r.b.data, r.b.cap, r.out_hdr, r.out, g.n, g.ctrl);
 }
@@ -2610,6 +2698,7 @@ __global__ void __launch_bounds__(256) k_encode_dense(const uint8_t* src, uint8_
 // Dense sends of one ring step for a batch of ranks (grid y): rb.a -> rb.out.
 template <class E>
 __global__ void __launch_bounds__(256) k_encode_dense_rb(uint64_t n, RankBatch rb) {
+    if (rank_skipped(rb, blockIdx.y)) return;
     encode_dense_body<E>(rb.a[blockIdx.y], rb.out[blockIdx.y], n);
 }
 
@@ -2900,6 +2989,11 @@ spccl_status_t launch_gather_rb_dt(int dtype, const DevOperand& part, uint64_t n
         if (K == 2) hipLaunchKernelGGL((k_gather_rb<F32, 2>), grid, block, 0, st, part, n, ctrl, rb);
         else hipLaunchKernelGGL((k_gather_rb<F32, 1>), grid, block, 0, st, part, n, ctrl, rb);
     }
+    return launch_status();
+}
+
+spccl_status_t launch_ring_decide(const RingArgs& a, hipStream_t st) {
+    hipLaunchKernelGGL(k_ring_decide, dim3((a.P + 255) / 256), dim3(256), 0, st, a);
     return launch_status();
 }
 

@@ -43,6 +43,7 @@ spccl_status_t launch_encode_dense_rb_dt(int dtype, uint64_t n, const RankBatch&
 spccl_status_t launch_gather_rb_dt(int dtype, const DevOperand& part, uint64_t n, WsCtrl* ctrl, const RankBatch& rb,
                                    uint32_t ranks, hipStream_t st);
 spccl_status_t launch_fill_zero(void* p, uint64_t bytes, hipStream_t st);
+spccl_status_t launch_ring_decide(const RingArgs& a, hipStream_t st);
 }  // namespace spccl
 
 namespace {
@@ -69,6 +70,8 @@ struct Layout {
     uint64_t vslot_bytes;       // per rank
     uint64_t slot_bytes;        // capacity of one message buffer
     uint8_t* slots;             // 3 * P message buffers
+    RingRank* rr;               // per rank: the device-side decision state
+    spccl_trace_t* dtrace;      // the trace, written on the device
     uint8_t* slot(int which, int r, int P) const { return slots + ((uint64_t)which * P + r) * slot_bytes; }
     uint8_t* rank_flags(int r) const { return flags + (uint64_t)r * flag_bytes; }
     uint8_t* rank_slots(int r) const { return vslots + (uint64_t)r * vslot_bytes; }
@@ -91,12 +94,15 @@ Layout carve(void* scratch, int32_t P, uint64_t msg_elems, int32_t dtype) {
     L.vslot_bytes = round_up(num_parts(msg_elems) * kPartElems * elem_bytes(dtype));
     L.slot_bytes = slot_need(msg_elems, dtype);
     L.slots = L.vslots + (uint64_t)P * L.vslot_bytes;
+    L.rr = reinterpret_cast<RingRank*>(L.slots + 3ull * (uint64_t)P * L.slot_bytes);
+    L.dtrace = reinterpret_cast<spccl_trace_t*>(reinterpret_cast<uint8_t*>(L.rr) + round_up(sizeof(RingRank) * P));
     return L;
 }
 
 uint64_t scratch_need(int32_t P, uint64_t msg_elems, int32_t dtype) {
     const Layout L = carve(nullptr, P, msg_elems, dtype);
-    return (uint64_t)(L.slots - L.ws) + 3ull * (uint64_t)P * L.slot_bytes;
+    const uint64_t trace_entries = (uint64_t)P * (uint64_t)(P - 1) + (uint64_t)P;
+    return (uint64_t)(reinterpret_cast<uint8_t*>(L.dtrace) - L.ws) + round_up(sizeof(spccl_trace_t) * trace_entries);
 }
 
 // Zero the parts of the scratch that must start clear: the workspace's
@@ -162,11 +168,13 @@ bool policy_ok(const spccl_policy_t& pol) {
         if (st_ != SPCCL_OK) return st_;           \
     } while (0)
 
-// ---- batched ring steps (Pici sends) -------------------------------------
-// Every ring step launches each kernel once for all ranks that take the same
+// ---- batched ring steps, decided on the device (Pici sends) --------------
+// Every ring step launches each kernel once for all ranks that may take that
 // path (grid y = rank, up to kMaxBatchRanks per launch): the P reductions,
-// sends and expansions of a step are independent of each other.  Decisions
-// stay on the host, from the headers read once per step.
+// sends and expansions of a step are independent of each other.  The format
+// decisions are made on the device between the launches (k_ring_decide), and
+// each rank's blocks skip the paths its decision rules out, so the host
+// enqueues the whole collective and synchronizes once, at the end.
 
 struct RankPtrs {
     const uint8_t* a;
@@ -174,13 +182,23 @@ struct RankPtrs {
     uint8_t* out;
 };
 
+// The formats a batched launch is for (checked per rank on the device).
+struct Gate {
+    const RingRank* rr;       // null: every rank takes part
+    int in_fmt, out_fmt;      // -1: any
+};
+constexpr Gate kNoGate{nullptr, -1, -1};
+
 // launch(rb, count) for the given ranks in batches of up to kMaxBatchRanks,
 // each rank's pointers from ptrs(rank) and its own look-back words and slots.
 template <class Ptrs, class Launch>
-spccl_status_t batched(const Layout& L, const std::vector<int>& ranks, Ptrs ptrs, Launch launch) {
+spccl_status_t batched(const Layout& L, const std::vector<int>& ranks, Gate gate, Ptrs ptrs, Launch launch) {
     for (size_t i = 0; i < ranks.size(); i += kMaxBatchRanks) {
         const uint32_t cnt = (uint32_t)(ranks.size() - i < (size_t)kMaxBatchRanks ? ranks.size() - i : kMaxBatchRanks);
         RankBatch rb{};
+        rb.gate = gate.rr;
+        rb.gate_in = gate.in_fmt;
+        rb.gate_out = gate.out_fmt;
         for (uint32_t j = 0; j < cnt; j++) {
             const int r = ranks[i + j];
             const RankPtrs q = ptrs(r);
@@ -189,6 +207,7 @@ spccl_status_t batched(const Layout& L, const std::vector<int>& ranks, Ptrs ptrs
             rb.out[j] = q.out;
             rb.flags[j] = L.rank_flags(r);
             rb.slots[j] = L.rank_slots(r);
+            rb.rank[j] = r;
         }
         SPCCL_TRY(launch(rb, cnt));
     }
@@ -227,114 +246,100 @@ DenseSinkArgs dense_args(const Layout& L, uint64_t m, DevOperand a, DevOperand b
     return g;
 }
 
-// Compress src(r) (m elements) into out(r) for the given ranks: Pici, or a
-// dense message for the ranks in `dense`.
+RingArgs ring_args(const Layout& L, int P, uint64_t m, int dtype, const spccl_policy_t& pol, int mode, int step) {
+    RingArgs a{};
+    a.rr = L.rr;
+    a.trace = L.dtrace;
+    a.slots0 = L.slot(0, 0, P);
+    a.slot_bytes = L.slot_bytes;
+    a.m = m;
+    a.P = P;
+    a.step = step;
+    a.mode = mode;
+    a.dtype = dtype;
+    a.intra = pol.intra_thresh;
+    a.inter = pol.inter_thresh;
+    a.ag = pol.ag_thresh;
+    a.ranks_per_node = pol.ranks_per_node;
+    a.adaptive = pol.adaptive;
+    return a;
+}
+
+// src(r) (m elements) into out(r) for the ranks whose decision is Pici
+// (compressed) and dense (a dense message); gated on the device unless gate
+// is kNoGate, when every rank compresses.
 template <class Src, class Out>
-spccl_status_t batched_encode(const Layout& L, const std::vector<int>& ranks, const std::vector<char>& dense,
-                              uint64_t m, int32_t dtype, Src src, Out out, hipStream_t st) {
-    std::vector<int> sp, dn;
-    for (int r : ranks) (dense[r] ? dn : sp).push_back(r);
+spccl_status_t batched_encode(const Layout& L, const std::vector<int>& ranks, Gate gate, bool with_dense, uint64_t m,
+                              int32_t dtype, Src src, Out out, hipStream_t st) {
     const uint64_t s = elem_bytes(dtype);
-    if (!sp.empty()) {
-        const PiciSinkArgs g = sink_args(L, m, arr_op(m * s), DevOperand{});
-        SPCCL_TRY(batched(L, sp, [&](int r) { return RankPtrs{src(r), nullptr, out(r)}; },
-                          [&](const RankBatch& rb, uint32_t c) {
-                              return launch_to_pici_rb_dt(dtype, SRC_DENSE, SRC_NONE, g, rb, c, st);
-                          }));
+    auto ptrs = [&](int r) { return RankPtrs{src(r), nullptr, out(r)}; };
+    const PiciSinkArgs g = sink_args(L, m, arr_op(m * s), DevOperand{});
+    Gate gp = gate;
+    if (gp.rr) gp.out_fmt = SPCCL_FMT_PICI;
+    SPCCL_TRY(batched(L, ranks, gp, ptrs, [&](const RankBatch& rb, uint32_t c) {
+        return launch_to_pici_rb_dt(dtype, SRC_DENSE, SRC_NONE, g, rb, c, st);
+    }));
+    if (with_dense && gate.rr) {
+        Gate gd = gate;
+        gd.out_fmt = SPCCL_FMT_DENSE;
+        SPCCL_TRY(batched(L, ranks, gd, ptrs, [&](const RankBatch& rb, uint32_t c) {
+            return launch_encode_dense_rb_dt(dtype, m, rb, c, st);
+        }));
     }
-    if (!dn.empty())
-        SPCCL_TRY(batched(L, dn, [&](int r) { return RankPtrs{src(r), nullptr, out(r)}; },
-                          [&](const RankBatch& rb, uint32_t c) { return launch_encode_dense_rb_dt(dtype, m, rb, c, st); }));
     return SPCCL_OK;
 }
 
-// The batched reduce-scatter (Pici sends); the same decisions, messages and
-// trace as ring_rs.
-spccl_status_t ring_rs_batched(void* const* send, void* const* out, int P, uint64_t n, int dtype,
-                               const spccl_policy_t& pol, const Layout& L, spccl_trace_t* trace,
-                               std::vector<double>& sig0, std::vector<double>& sigp, hipStream_t st) {
+// The reduce-scatter with Pici sends and device-side decisions: the same
+// messages, results and trace (in L.dtrace) as ring_rs.
+spccl_status_t ring_rs_dev(void* const* send, void* const* out, int P, uint64_t n, int dtype,
+                           const spccl_policy_t& pol, const Layout& L, hipStream_t st) {
     const uint64_t m = n / (uint64_t)P, s = elem_bytes(dtype);
     auto chunk = [&](int r, int c) { return static_cast<const uint8_t*>(send[r]) + (uint64_t)c * m * s; };
-    std::vector<int> all(P), fmt(P, SPCCL_FMT_PICI);
+    std::vector<int> all(P);
     for (int r = 0; r < P; r++) all[r] = r;
-    std::vector<spccl_header_t> h;
     WsCtrl* ctrl = reinterpret_cast<WsCtrl*>(L.ws);
-    // step 0: compress every rank's first chunk into slot 0, measure sigma0
-    SPCCL_TRY(batched_encode(L, all, std::vector<char>(P, 0), m, dtype,
-                             [&](int r) { return chunk(r, (r - 1 + P) % P); },
+    // which paths the policy leaves open: never dense (0), always dense (2), or either
+    const bool can_dense = pol.adaptive != 0, can_pici = pol.adaptive != 2;
+    // step 0: compress every rank's first chunk into slot 0 and measure sigma0;
+    // ranks whose first send is dense encode it again
+    SPCCL_TRY(batched_encode(L, all, kNoGate, false, m, dtype, [&](int r) { return chunk(r, (r - 1 + P) % P); },
                              [&](int r) { return L.slot(0, r, P); }, st));
-    SPCCL_TRY(read_headers(L, 0, P, h, st));
-    std::vector<char> dense(P, 0);
-    for (int r = 0; r < P; r++) {
-        sig0[r] = sigp[r] = sparsity(m, h[r].nnz);
-        dense[r] = send_dense(pol, sig0[r], link_tau(pol, r, P));
-        fmt[r] = dense[r] ? SPCCL_FMT_DENSE : SPCCL_FMT_PICI;
-        put_trace(trace, r, 0, r, fmt[r], 1, dense[r] ? dense_msg_bytes(m, dtype) : h[r].total_bytes, h[r].nnz,
-                  sigp[r]);
-    }
-    std::vector<int> dn;
-    for (int r = 0; r < P; r++)
-        if (dense[r]) dn.push_back(r);
-    if (!dn.empty())
-        SPCCL_TRY(batched(L, dn, [&](int r) { return RankPtrs{chunk(r, (r - 1 + P) % P), nullptr, L.slot(0, r, P)}; },
+    SPCCL_TRY(launch_ring_decide(ring_args(L, P, m, dtype, pol, kDecideFirst, 0), st));
+    if (can_dense)
+        SPCCL_TRY(batched(L, all, Gate{L.rr, -1, SPCCL_FMT_DENSE},
+                          [&](int r) { return RankPtrs{chunk(r, (r - 1 + P) % P), nullptr, L.slot(0, r, P)}; },
                           [&](const RankBatch& rb, uint32_t c) { return launch_encode_dense_rb_dt(dtype, m, rb, c, st); }));
     for (int step = 1; step <= P - 1; step++) {
+        SPCCL_TRY(launch_ring_decide(ring_args(L, P, m, dtype, pol, kDecideStep, step), st));
         // every send of the previous step arrives: rank r receives rank r-1's message
-        SPCCL_TRY(batched(L, all, [&](int r) { return RankPtrs{L.slot(0, (r - 1 + P) % P, P), nullptr, L.slot(1, r, P)}; },
+        SPCCL_TRY(batched(L, all, kNoGate,
+                          [&](int r) { return RankPtrs{L.slot(0, (r - 1 + P) % P, P), nullptr, L.slot(1, r, P)}; },
                           [&](const RankBatch& rb, uint32_t c) {
                               return launch_copy_message_rb(L.slot_bytes, L.slot_bytes, ctrl, rb, c, st);
                           }));
-        std::vector<int> in_fmt(P);
-        for (int r = 0; r < P; r++) in_fmt[r] = fmt[(r - 1 + P) % P];
-        auto own = [&](int r) { return chunk(r, (r - step - 1 + 2 * P) % P); };
         const bool last = step == P - 1;
-        // per rank: the send format of this step (the last one reduces into out[r])
-        std::vector<char> to_dense(P, 0);
-        if (!last)
-            for (int r = 0; r < P; r++) {
-                const double est = sigp[r] * sig0[r];   // Eq. 7
-                to_dense[r] = send_dense(pol, est, link_tau(pol, r, P));
-                if (to_dense[r]) {
-                    fmt[r] = SPCCL_FMT_DENSE;
-                    sigp[r] = est;
-                    put_trace(trace, step * P + r, step, r, SPCCL_FMT_DENSE, 0, dense_msg_bytes(m, dtype),
-                              SPCCL_NNZ_UNKNOWN, est);
-                } else {
-                    fmt[r] = SPCCL_FMT_PICI;
-                }
-            }
-        bool any_measured = false;
-        for (int in_pici = 0; in_pici <= 1; in_pici++) {
+        auto ptrs = [&](int r) {
+            return RankPtrs{L.slot(1, r, P), chunk(r, (r - step - 1 + 2 * P) % P),
+                            last ? static_cast<uint8_t*>(out[r]) : L.slot(0, r, P)};
+        };
+        for (int in_pici = 1; in_pici >= 0; in_pici--) {
+            // a received message is dense only where a dense send can occur
+            if (in_pici ? !can_pici : !can_dense) continue;
+            const int in_fmt = in_pici ? SPCCL_FMT_PICI : SPCCL_FMT_DENSE;
             const DevOperand a_op = in_pici ? msg_op(L) : dense_msg_op(L);
             const int sa = in_pici ? SRC_PICI : SRC_DENSE;
-            std::vector<int> to_p, to_d;
-            for (int r = 0; r < P; r++) {
-                if ((in_fmt[r] == SPCCL_FMT_PICI) != (bool)in_pici) continue;
-                (last || to_dense[r] ? to_d : to_p).push_back(r);
-            }
-            auto ptrs = [&](int r) {
-                return RankPtrs{L.slot(1, r, P), own(r), last ? static_cast<uint8_t*>(out[r]) : L.slot(0, r, P)};
-            };
-            if (!to_p.empty()) {
-                any_measured = true;
+            if (!last && can_pici) {
                 const PiciSinkArgs g = sink_args(L, m, a_op, arr_op(m * s));
-                SPCCL_TRY(batched(L, to_p, ptrs, [&](const RankBatch& rb, uint32_t c) {
+                SPCCL_TRY(batched(L, all, Gate{L.rr, in_fmt, SPCCL_FMT_PICI}, ptrs, [&](const RankBatch& rb, uint32_t c) {
                     return launch_to_pici_rb_dt(dtype, sa, SRC_DENSE, g, rb, c, st);
                 }));
             }
-            if (!to_d.empty()) {
+            if (last || can_dense) {
                 const DenseSinkArgs g = dense_args(L, m, a_op, arr_op(m * s), !last);
-                SPCCL_TRY(batched(L, to_d, ptrs, [&](const RankBatch& rb, uint32_t c) {
+                const Gate gd{L.rr, in_fmt, last ? -1 : SPCCL_FMT_DENSE};
+                SPCCL_TRY(batched(L, all, gd, ptrs, [&](const RankBatch& rb, uint32_t c) {
                     return launch_to_dense_rb_dt(dtype, sa, SRC_DENSE, g, rb, c, st);
                 }));
-            }
-        }
-        if (any_measured && !last) {
-            SPCCL_TRY(read_headers(L, 0, P, h, st));
-            for (int r = 0; r < P; r++) {
-                if (fmt[r] != SPCCL_FMT_PICI) continue;
-                sigp[r] = sparsity(m, h[r].nnz);
-                put_trace(trace, step * P + r, step, r, SPCCL_FMT_PICI, 1, h[r].total_bytes, h[r].nnz, sigp[r]);
             }
         }
     }
@@ -359,12 +364,12 @@ spccl_status_t ring_ag_batched(void* const* own, void* const* out, int P, uint64
     WsCtrl* ctrl = reinterpret_cast<WsCtrl*>(L.ws);
     for (int k = 0; k < P - 1; k++) {
         const int in_slot = 1 + (k % 2), prev_slot = k == 0 ? 0 : 1 + ((k - 1) % 2);
-        SPCCL_TRY(batched(L, all,
+        SPCCL_TRY(batched(L, all, kNoGate,
                           [&](int r) { return RankPtrs{L.slot(prev_slot, (r - 1 + P) % P, P), nullptr, L.slot(in_slot, r, P)}; },
                           [&](const RankBatch& rb, uint32_t c) {
                               return launch_copy_message_rb(L.slot_bytes, L.slot_bytes, ctrl, rb, c, st);
                           }));
-        SPCCL_TRY(batched(L, all,
+        SPCCL_TRY(batched(L, all, kNoGate,
                           [&](int r) {
                               const int q = ((r - 1 - k) % P + P) % P;
                               return RankPtrs{L.slot(in_slot, r, P), nullptr,
@@ -375,6 +380,13 @@ spccl_status_t ring_ag_batched(void* const* own, void* const* out, int P, uint64
                           }));
     }
     return SPCCL_OK;
+}
+
+// The trace written on the device into the caller's array (entries [0, count)).
+spccl_status_t copy_trace(const Layout& L, spccl_trace_t* trace, uint64_t count, hipStream_t st) {
+    if (!trace || !count) return SPCCL_OK;
+    return hipMemcpyAsync(trace, L.dtrace, sizeof(spccl_trace_t) * count, hipMemcpyDeviceToHost, st) == hipSuccess
+               ? SPCCL_OK : SPCCL_ERR_HIP;
 }
 
 // Reduce-scatter over the chunks; the reduced chunk r goes to out[r] (m
@@ -456,17 +468,9 @@ spccl_status_t ring_rs(void* const* send, void* const* out, int P, uint64_t n, i
     return SPCCL_OK;
 }
 
-// The reduce-scatter: batched launches for Pici sends, per-rank calls for COO.
-spccl_status_t reduce_scatter(void* const* send, void* const* out, int P, uint64_t n, int dtype,
-                              const spccl_policy_t& pol, const Layout& L, spccl_trace_t* trace, std::vector<double>& sig0,
-                              std::vector<double>& sigp, hipStream_t st) {
-    if (pol.sparse_fmt == SPCCL_FMT_PICI && P > 1) {
-        sig0.assign(P, 1.0);
-        sigp.assign(P, 1.0);
-        return ring_rs_batched(send, out, P, n, dtype, pol, L, trace, sig0, sigp, st);
-    }
-    return ring_rs(send, out, P, n, dtype, pol, L, trace, sig0, sigp, st);
-}
+// Pici sends over more than one rank run batched, decided on the device;
+// COO sends (and a single rank) run per rank, decided on the host.
+bool device_ring(const spccl_policy_t& pol, int P) { return pol.sparse_fmt == SPCCL_FMT_PICI && P > 1; }
 
 spccl_status_t check_common(void* const* send, void* const* recv, int32_t P, int32_t dtype, void* scratch,
                             uint64_t scratch_bytes, uint64_t msg_elems) {
@@ -540,8 +544,13 @@ spccl_status_t spccl_vr_reduce_scatter(void* const* send, void* const* recv, int
     hipStream_t st = as_stream(stream);
     const Layout L = carve(scratch, P, m, dtype);
     SPCCL_TRY(init_scratch(L, P, m, dtype, st));
-    std::vector<double> sig0, sigp;
-    SPCCL_TRY(reduce_scatter(send, recv, P, n, dtype, pol, L, trace, sig0, sigp, st));
+    if (device_ring(pol, P)) {
+        SPCCL_TRY(ring_rs_dev(send, recv, P, n, dtype, pol, L, st));
+        SPCCL_TRY(copy_trace(L, trace, (uint64_t)P * (uint64_t)(P - 1), st));
+    } else {
+        std::vector<double> sig0, sigp;
+        SPCCL_TRY(ring_rs(send, recv, P, n, dtype, pol, L, trace, sig0, sigp, st));
+    }
     return finish(L, st);
 }
 
@@ -557,18 +566,21 @@ spccl_status_t spccl_vr_all_gather(void* const* send, void* const* recv, int32_t
     hipStream_t st = as_stream(stream);
     const Layout L = carve(scratch, P, n, dtype);
     SPCCL_TRY(init_scratch(L, P, n, dtype, st));
-    std::vector<int> all(P);
-    for (int q = 0; q < P; q++) all[q] = q;
-    if (pol.sparse_fmt == SPCCL_FMT_PICI)
-        SPCCL_TRY(batched_encode(L, all, std::vector<char>(P, 0), n, dtype,
+    if (pol.sparse_fmt == SPCCL_FMT_PICI) {
+        std::vector<int> all(P);
+        for (int q = 0; q < P; q++) all[q] = q;
+        SPCCL_TRY(batched_encode(L, all, kNoGate, false, n, dtype,
                                  [&](int q) { return static_cast<const uint8_t*>(send[q]); },
                                  [&](int q) { return L.slot(0, q, P); }, st));
-    else
+        SPCCL_TRY(launch_ring_decide(ring_args(L, P, n, dtype, pol, kDecideAllGather, 0), st));
+        SPCCL_TRY(copy_trace(L, trace, (uint64_t)P, st));
+    } else {
         for (int q = 0; q < P; q++) SPCCL_TRY(compress_fmt(pol.sparse_fmt, send[q], n, dtype, L, L.slot(0, q, P), st));
-    std::vector<spccl_header_t> h;
-    SPCCL_TRY(read_headers(L, 0, P, h, st));
-    for (int q = 0; q < P; q++)
-        put_trace(trace, q, 0, q, pol.sparse_fmt, 1, h[q].total_bytes, h[q].nnz, sparsity(n, h[q].nnz));
+        std::vector<spccl_header_t> h;
+        SPCCL_TRY(read_headers(L, 0, P, h, st));
+        for (int q = 0; q < P; q++)
+            put_trace(trace, q, 0, q, pol.sparse_fmt, 1, h[q].total_bytes, h[q].nnz, sparsity(n, h[q].nnz));
+    }
     SPCCL_TRY(ring_ag_batched(send, recv, P, n, dtype, L, st));
     return finish(L, st);
 }
@@ -589,36 +601,38 @@ spccl_status_t spccl_vr_all_reduce(void* const* send, void* const* recv, int32_t
     // reduce-scatter straight into each rank's own chunk of its output
     std::vector<void*> chunk_out(P);
     for (int r = 0; r < P; r++) chunk_out[r] = static_cast<uint8_t*>(recv[r]) + (uint64_t)r * m * s;
-    std::vector<double> sig0, sigp;
-    SPCCL_TRY(reduce_scatter(send, chunk_out.data(), P, n, dtype, pol, L, trace, sig0, sigp, st));
-    // phase-aware transition: one message per rank, encoded once
-    std::vector<int> fmt(P);
-    std::vector<double> est(P);
-    std::vector<char> dense(P, 0);
-    std::vector<int> all(P);
-    for (int r = 0; r < P; r++) {
-        all[r] = r;
-        est[r] = sigp[r] * sig0[r];
-        dense[r] = pol.adaptive == 2 ? true : (pol.adaptive == 0 ? false : est[r] <= pol.ag_thresh);
-        fmt[r] = dense[r] ? SPCCL_FMT_DENSE : pol.sparse_fmt;
-    }
-    if (pol.sparse_fmt == SPCCL_FMT_PICI) {
-        SPCCL_TRY(batched_encode(L, all, dense, m, dtype,
+    if (device_ring(pol, P)) {
+        // the transition decided on the device from each rank's tracked sparsity
+        std::vector<int> all(P);
+        for (int r = 0; r < P; r++) all[r] = r;
+        SPCCL_TRY(ring_rs_dev(send, chunk_out.data(), P, n, dtype, pol, L, st));
+        SPCCL_TRY(launch_ring_decide(ring_args(L, P, m, dtype, pol, kDecideGather, 0), st));
+        SPCCL_TRY(batched_encode(L, all, Gate{L.rr, -1, -1}, pol.adaptive != 0, m, dtype,
                                  [&](int r) { return static_cast<const uint8_t*>(chunk_out[r]); },
                                  [&](int r) { return L.slot(0, r, P); }, st));
+        SPCCL_TRY(launch_ring_decide(ring_args(L, P, m, dtype, pol, kDecideGatherSizes, 0), st));
+        SPCCL_TRY(copy_trace(L, trace, (uint64_t)P * (uint64_t)(P - 1) + (uint64_t)P, st));
     } else {
+        std::vector<double> sig0, sigp;
+        SPCCL_TRY(ring_rs(send, chunk_out.data(), P, n, dtype, pol, L, trace, sig0, sigp, st));
+        // phase-aware transition: one message per rank, encoded once
+        std::vector<int> fmt(P);
+        std::vector<double> est(P);
         for (int r = 0; r < P; r++) {
-            if (dense[r]) SPCCL_TRY(spccl_encode_dense(chunk_out[r], m, dtype, L.slot(0, r, P), L.slot_bytes, stream));
+            est[r] = sigp[r] * sig0[r];
+            const bool dense = pol.adaptive == 2 ? true : (pol.adaptive == 0 ? false : est[r] <= pol.ag_thresh);
+            fmt[r] = dense ? SPCCL_FMT_DENSE : pol.sparse_fmt;
+            if (dense) SPCCL_TRY(spccl_encode_dense(chunk_out[r], m, dtype, L.slot(0, r, P), L.slot_bytes, stream));
             else SPCCL_TRY(compress_fmt(pol.sparse_fmt, chunk_out[r], m, dtype, L, L.slot(0, r, P), st));
         }
-    }
-    std::vector<spccl_header_t> h;
-    SPCCL_TRY(read_headers(L, 0, P, h, st));
-    spccl_trace_t* ag_tr = trace ? trace + (uint64_t)P * (uint64_t)(P - 1) : nullptr;
-    for (int r = 0; r < P; r++) {
-        const bool sparse = fmt[r] != SPCCL_FMT_DENSE;
-        put_trace(ag_tr, r, P - 1, r, fmt[r], sparse ? 1 : 0, h[r].total_bytes,
-                  sparse ? h[r].nnz : SPCCL_NNZ_UNKNOWN, est[r]);
+        std::vector<spccl_header_t> h;
+        SPCCL_TRY(read_headers(L, 0, P, h, st));
+        spccl_trace_t* ag_tr = trace ? trace + (uint64_t)P * (uint64_t)(P - 1) : nullptr;
+        for (int r = 0; r < P; r++) {
+            const bool sparse = fmt[r] != SPCCL_FMT_DENSE;
+            put_trace(ag_tr, r, P - 1, r, fmt[r], sparse ? 1 : 0, h[r].total_bytes,
+                      sparse ? h[r].nnz : SPCCL_NNZ_UNKNOWN, est[r]);
+        }
     }
     SPCCL_TRY(ring_ag_batched(chunk_out.data(), recv, P, m, dtype, L, st));
     return finish(L, st);
