@@ -14,7 +14,7 @@ constexpr uint32_t kWave = 64;                  // CDNA wavefront
 constexpr uint32_t kWavesPerBlock = 4;          // one tile per wave
 constexpr uint32_t kBlockThreads = kWave * kWavesPerBlock;
 constexpr uint32_t kTilesPerPart = kWavesPerBlock;   // look-back partition = one block
-constexpr uint32_t kStageBytes = 8192;          // LDS staging per wave (an fp32 tile up to half full in one go)
+constexpr uint32_t kStageBytes = 7168;          // LDS staging per wave (an fp32 tile up to 7/16 full in one go)
 
 constexpr int kFmtDense = 0, kFmtPici = 1, kFmtCoo = 2;
 constexpr int kKindArray = 0, kKindStream = 1;

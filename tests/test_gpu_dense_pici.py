@@ -20,7 +20,7 @@ torch = pytest.importorskip("torch")
 
 TILE = 4096
 EARLY = 512          # Pici values of a tile read before its dense rows finish
-STAGE = {W.F32: 2048, W.BF16: 4096}     # output values one wave stages at once
+STAGE = {W.F32: 1792, W.BF16: 3584}     # output values one wave stages at once
 
 
 @pytest.fixture(scope="module")
