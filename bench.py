@@ -598,8 +598,9 @@ def time_collectives(S, torch, with_cfg5=True, reps=3):
     P = 8 x 16,777,216 bf16 all-gather at 0.999, and the all-reduce of the
     8 x 268,435,456 fp32 pruned-gradient-like buffers (64 segments, sparsity
     U[0.5, 0.99], 70% shared positions) -- each in its canonical form (one
-    global message per step, the host decides from the headers) and its
-    sliced form (per-slice decisions on the device)."""
+    global message per rank and step, decided on the device from the
+    headers) and its sliced form (per-slice decisions on the device); and
+    the canonical reduce-scatter on one tile per rank (its launch cost)."""
     import workloads as W
 
     def timed(f, *args, times=reps):
@@ -618,6 +619,15 @@ def time_collectives(S, torch, with_cfg5=True, reps=3):
     sc = torch.empty(S.spccl_vr_scratch_bytes(P, m, F), dtype=torch.uint8, device="cuda")
     res["rs_canonical_ms"] = timed(S.spccl_vr_reduce_scatter, sends, outs, sc)
     del sc
+    # the same ring on one tile per rank: its bytes are negligible, so its
+    # time per launch is the launch cost of this sequence (the tuner check)
+    mt = 4096
+    tiny = [torch.from_numpy(W.sparse_array(P * mt, W.nnz_for(P * mt, 990), [3, r, 1, 990])).cuda()
+            for r in range(P)]
+    touts = [torch.empty(mt, dtype=torch.float32, device="cuda") for _ in range(P)]
+    tsc = torch.empty(S.spccl_vr_scratch_bytes(P, mt, F), dtype=torch.uint8, device="cuda")
+    res["rs_one_tile_ms"] = timed(S.spccl_vr_reduce_scatter, tiny, touts, tsc, times=20)
+    del tiny, touts, tsc
     sc = torch.empty(S.spccl_vr_sliced_scratch_bytes(P, m, F), dtype=torch.uint8, device="cuda")
     res["rs_sliced_ms"] = timed(S.spccl_vr_reduce_scatter_sliced, sends, outs, sc)
     del sc, sends, outs
@@ -653,6 +663,25 @@ def time_collectives(S, torch, with_cfg5=True, reps=3):
         del sc, sends, outs
         torch.cuda.empty_cache()
     return res
+
+
+def tuner_check(ops_tab, dense_ops, copy_GBs, coll, tolerance=0.25):
+    """The threshold model's kernel-cost term against the measured ring: the
+    P = 8 x 33,554,432 fp32 reduce-scatter at 0.99 predicted on one GPU with
+    free links (algorithmic bytes of every rank at the isolated 256 MiB op
+    bandwidths, plus a per-launch cost calibrated on the same ring with one
+    tile per rank), next to its measured wall time."""
+    import workloads as W
+    from paper_2607_04676_amd import tuner
+    km = tuner.KernelModel.from_ops(ops_tab, dense_ops, copy_GBs)
+    P, m, pol = W.CFG3_P, W.CFG3_N // W.CFG3_P, tuner.Policy()
+    one = tuner.vr_rs_time_us(P, 4096, 4, 0.99, pol, km, 0.0)
+    launch_us = max(0.0, (coll["rs_one_tile_ms"] * 1e3 - one["bytes_us"]) / one["launches"])
+    pred = tuner.vr_rs_time_us(P, m, 4, 0.99, pol, km, launch_us)
+    ratio = pred["total_us"] / 1e3 / coll["rs_canonical_ms"]
+    return {"predicted_ms": round(pred["total_us"] / 1e3, 3), "measured_ms": coll["rs_canonical_ms"],
+            "ratio": round(ratio, 3), "bytes_ms": round(pred["bytes_us"] / 1e3, 3), "launches": pred["launches"],
+            "launch_us": round(launch_us, 2), "tolerance": tolerance, "within": abs(ratio - 1.0) <= tolerance}
 
 
 def time_dense_ops(S, torch, n, reps=10):
@@ -871,6 +900,9 @@ def main():
     if not args.no_cpu:
         _log("timing the CPU oracle")
         cpu = cpu_baseline(args.permille, args.n)
+    check = None
+    if iso and collectives:
+        check = tuner_check(ops_tab, dense_ops, ceiling["GBs"], collectives)
     if iso:
         roof["ops"] = ops_tab
         roof["ops_key"] = ("config.dtype.sparsity(permille).op -> [isolated median us, algorithmic bytes, "
@@ -886,6 +918,7 @@ def main():
                    "n": args.n, "sigma": args.permille / 1000, "parallelism": "1 GPU (virtual ranks)"},
         "roofline": roof, "cpu_baseline": cpu, "copy_ceiling_GBs": ceiling["GBs"], "collectives_ms": collectives,
         "parity_vs_oracle": parity, "wall_s_timed": round(wall, 3), "calibration_copy_bytes": calib,
+        "tuner_check": check,
     }
     full.update({"line": out, "copy_ceiling": ceiling, "dense_ops": dense_ops, "sweep": sweep, **extras,
                  "kernels": full["step_ops"]})

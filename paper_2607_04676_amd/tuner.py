@@ -36,6 +36,7 @@ from dataclasses import dataclass, field
 FMT_DENSE, FMT_PICI, FMT_COO = 0, 1, 2
 HEADER = 48
 GRID = [round(0.1 * k, 1) for k in range(11)]          # thresholds swept at steps of 0.1
+TIE = 0.005             # geomean slowdowns within 0.5% of the best count as ties
 
 
 def _align16(x: int) -> int:
@@ -109,6 +110,30 @@ class KernelModel:
     def constant(GBs: float, fixed_us: float = 0.0) -> "KernelModel":
         names = ("compress", "expand", "to_sparse", "to_dense", "dense_dense", "copy")
         return KernelModel({k: OpCurve([0.0], [GBs], fixed_us) for k in names})
+
+    @staticmethod
+    def from_ops(ops: dict, dense_ops: dict, copy_GBs: float, fixed_us: float = 0.0) -> "KernelModel":
+        """Curves from isolated per-op times on the 256 MiB fp32 array:
+        ops["c2.f32.<permille>.<op>"] = [median us, algorithmic bytes, ...]
+        (the bench record's roofline table)."""
+        names = {"compress": "compress", "expand": "decompress", "to_sparse": "reduce_dense_pici_to_pici",
+                 "to_dense": "reduce_dense_pici_to_dense"}
+        points = {k: [] for k in names}
+        for key, val in ops.items():
+            parts = key.split(".")
+            if len(parts) != 4 or parts[0] != "c2" or parts[1] != "f32":
+                continue
+            for k, op in names.items():
+                if parts[3] == op:
+                    points[k].append((int(parts[2]) / 1000.0, val[1] / (val[0] * 1e-6) / 1e9))
+        curves = {}
+        for k, pts in points.items():
+            pts.sort()
+            curves[k] = OpCurve([p[0] for p in pts], [p[1] for p in pts], fixed_us)
+        for k in ("dense_dense", "copy"):
+            g = dense_ops.get(k, {}).get("achieved_GBs") or copy_GBs
+            curves[k] = OpCurve([0.0], [g], fixed_us)
+        return KernelModel(curves)
 
     @staticmethod
     def from_bench(rec: dict, fmt: int = FMT_PICI, fixed_us: float = 4.0) -> "KernelModel":
@@ -243,6 +268,50 @@ def rs_time_us(P: int, m: int, s: int, sigma0: float, pol: Policy, km: KernelMod
     return total
 
 
+def vr_rs_time_us(P: int, m: int, s: int, sigma0: float, pol: Policy, km: KernelModel, launch_us: float) -> dict:
+    """The same reduce-scatter on one GPU with P virtual ranks and free
+    links, as the library runs it: every kernel of a ring step is one
+    launch for all ranks, with the format decisions made on the device
+    between launches, so a step costs the sum over ranks of its algorithmic
+    bytes at the op's bandwidth plus launch_us per launch.  Launches per
+    step: a decide and a copy of the received messages, then for each input
+    format that can occur a count and a place pass (a Pici send) and a dense
+    sink (a dense send, or the last step's output); step 0 compresses (count
+    and place), decides and, if the policy allows dense sends, encodes them.
+    Returns the total and its two terms (us) and the launch count."""
+    if P == 1:
+        return {"total_us": 0.0, "bytes_us": 0.0, "launch_us": 0.0, "launches": 0}
+    can_dense, can_sparse = pol.adaptive != 0, pol.adaptive != 2
+    bw = lambda op, sg: km.ops[op].bandwidth(sg) * 1e3        # bytes per us
+    fmts, _, true, _, _ = replay_rs(P, sigma0, pol)
+    dense_chunk = m * s
+    bytes_us = 0.0
+    launches = 3 + (1 if can_dense else 0)
+    for r in range(P):
+        bytes_us += (dense_chunk + message_bytes(m, s, pol.sparse_fmt, sigma0)) / bw("compress", sigma0)
+        if fmts[0][r] == FMT_DENSE:
+            bytes_us += (2 * dense_chunk) / bw("copy", sigma0)
+    for step in range(1, P):
+        last = step == P - 1
+        launches += 2
+        for fin_ok in (can_sparse, can_dense):
+            if fin_ok:
+                launches += (2 if (not last and can_sparse) else 0) + (1 if (last or can_dense) else 0)
+        sig_in, sig_out = true[step - 1], sigma0 ** (step + 1)
+        for r in range(P):
+            fin = fmts[step - 1][(r - 1) % P]
+            in_b = message_bytes(m, s, fin, sig_in)
+            bytes_us += 2 * in_b / bw("copy", sig_in)
+            fout = FMT_DENSE if last else fmts[step][r]
+            if fout == FMT_DENSE:
+                op = "dense_dense" if fin == FMT_DENSE else "to_dense"
+                bytes_us += (2 * dense_chunk + in_b) / bw(op, sig_in)
+            else:
+                bytes_us += (dense_chunk + in_b + message_bytes(m, s, fout, sig_out)) / bw("to_sparse", sig_out)
+    return {"total_us": bytes_us + launches * launch_us, "bytes_us": bytes_us, "launch_us": launches * launch_us,
+            "launches": launches}
+
+
 def ag_time_us(P: int, m: int, s: int, sigma: float, fmt: int, km: KernelModel,
                pol: Policy | None = None, intra: Link = XGMI, inter: Link = NIC) -> float:
     """Modelled ring all-gather of P parts of m elements at sparsity sigma
@@ -312,6 +381,9 @@ def recommend(km: KernelModel, workloads=None, sparse_fmt: int = FMT_PICI, intra
                     "dense_us": round(dense_rs_time_us(P, m, s, km, intra, inter, 8), 2),
                     "paper_us": round(tab[(0.6, 0.5) if sparse_fmt == FMT_PICI else (0.8, 0.7)], 2)})
     pair = min(logs, key=logs.get)
+    # pairs within TIE of the best geomean slowdown: the optimum is often a
+    # plateau, and the single pick is then a tie-break (lowest thresholds)
+    tied = sorted(q for q in logs if logs[q] <= logs[pair] + math.log1p(TIE))
     # ag threshold: best for the all-reduce at the chosen pair
     ag_logs = {g: 0.0 for g in GRID}
     for P, mib, sg in workloads:
@@ -323,7 +395,12 @@ def recommend(km: KernelModel, workloads=None, sparse_fmt: int = FMT_PICI, intra
             ag_logs[g] += math.log(t / best)
     ag = min(ag_logs, key=ag_logs.get)
     n = len(workloads)
+    ag_tied = sorted(g for g in ag_logs if ag_logs[g] <= ag_logs[ag] + math.log1p(TIE))
     return {"intra_thresh": pair[0], "inter_thresh": pair[1], "ag_thresh": ag,
+            "ties": {"within": TIE, "pairs": len(tied),
+                     "intra": [min(q[0] for q in tied), max(q[0] for q in tied)],
+                     "inter": [min(q[1] for q in tied), max(q[1] for q in tied)],
+                     "ag": [ag_tied[0], ag_tied[-1]]},
             "geomean_slowdown_vs_best": round(math.exp(logs[pair] / n), 4),
             "paper_pair_geomean_slowdown": round(math.exp(logs[(0.6, 0.5) if sparse_fmt == FMT_PICI
                                                            else (0.8, 0.7)] / n), 4),

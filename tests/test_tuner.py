@@ -84,3 +84,43 @@ def test_recommend_is_a_grid_point_and_reports_the_paper_pair():
     assert rec["paper_pair_geomean_slowdown"] >= rec["geomean_slowdown_vs_best"]
     for w in rec["workloads"]:
         assert w["best_us"] <= w["paper_us"] and w["best_us"] <= w["dense_us"] + 1e-9
+
+
+@pytest.mark.parametrize("adaptive,launches", [(1, 56), (0, 30), (2, 25)])
+def test_one_gpu_ring_launches_follow_the_policy(adaptive, launches):
+    """The one-GPU ring issues, per step, a decide and a copy, then for each
+    input format the policy allows a count and a place pass (a sparse send)
+    and a dense sink (a dense send or the last step); step 0 compresses,
+    decides and, if dense sends are allowed, encodes them."""
+    km = T.KernelModel.constant(4000.0)
+    got = T.vr_rs_time_us(8, 1 << 16, 4, 0.99, T.Policy(adaptive=adaptive), km, 3.0)
+    assert got["launches"] == launches
+    assert got["launch_us"] == pytest.approx(3.0 * launches)
+
+
+def test_one_gpu_ring_bytes_are_every_rank_summed():
+    """Never dense, every op at one bandwidth: the bytes term is the sum over
+    ranks and steps of compress (dense chunk + message), the copy of each
+    received message (read and write) and the reduction (dense chunk, the
+    received message, and the sent message or the dense output at the last
+    step), with the message at sigma0^(k+1) after k + 1 contributions."""
+    P, m, s, sg, GBs = 4, 3 * 4096 + 17, 4, 0.95, 2000.0
+    km = T.KernelModel.constant(GBs)
+    pici = lambda x: T.message_bytes(m, s, T.FMT_PICI, x)
+    total = P * (m * s + pici(sg))
+    for step in range(1, P):
+        inb = pici(sg ** step)
+        total += P * 2 * inb
+        total += P * ((2 * m * s + inb) if step == P - 1 else (m * s + inb + pici(sg ** (step + 1))))
+    got = T.vr_rs_time_us(P, m, s, sg, T.Policy(adaptive=0), km, 0.0)
+    assert got["bytes_us"] == pytest.approx(total / (GBs * 1e3), rel=1e-12)
+
+
+def test_recommend_reports_the_tied_region():
+    km = T.KernelModel.constant(4000.0, fixed_us=4.0)
+    rec = T.recommend(km, workloads=[(16, 512, 0.95), (32, 2048, 0.99)])
+    ties = rec["ties"]
+    assert ties["pairs"] >= 1
+    assert ties["intra"][0] <= rec["intra_thresh"] <= ties["intra"][1]
+    assert ties["inter"][0] <= rec["inter_thresh"] <= ties["inter"][1]
+    assert ties["ag"][0] <= rec["ag_thresh"] <= ties["ag"][1]
