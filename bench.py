@@ -787,6 +787,9 @@ def main():
                     help="skip the 8 x 1 GiB all-reduce (its inputs take about a minute to generate)")
     ap.add_argument("--extras", action="store_true", help="also time the sliced and COO forms and the sweep")
     ap.add_argument("--full-out", default="", help="write the complete record (JSON) to this file")
+    ap.add_argument("--profile-bf16", type=int, default=0, metavar="PERMILLE",
+                    help="profiling run: only the bf16 ops of the 256 MiB array at this sparsity, three "
+                         "calls each (for per-kernel counters), then the parity check; no timing")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -797,6 +800,19 @@ def main():
     _ensure_built()
     import torch
     import paper_2607_04676_amd as S
+
+    if args.profile_bf16:
+        Rb = Runner(S, torch, args.n * 2, args.profile_bf16, 1, bf16=True)
+        names = ("compress", "decompress", "reduce_dense_pici_to_pici", "reduce_dense_pici_to_dense")
+        alg = run_once(Rb)
+        for _ in range(3):
+            for nm, f in Rb.isolated_ops():
+                if nm in names:
+                    f()
+        torch.cuda.synchronize()
+        print(json.dumps({"profile": f"bf16 ops, {args.n * 2:,} elements, sigma={args.profile_bf16 / 1000}",
+                          "algorithmic_bytes": {k: alg[k] for k in names}, "parity": Rb.check_parity()}))
+        return
 
     torch.cuda.init()
     _log(f"device: {torch.cuda.get_device_name(0)}")
