@@ -765,19 +765,24 @@ __device__ __forceinline__ bool coo_load_pairs(const uint32_t* J, const typename
                                                bool check, uint64_t first, uint64_t limit,
                                                uint32_t (&x)[kCooSlots], typename E::raw (&val)[kCooSlots]) {
     const uint32_t l = lane_id();
-    uint32_t y[kCooSlots];
 #pragma unroll
     for (int q = 0; q < kCooSlots; q++) {
         const uint32_t i = l + 64 * q;
         x[q] = i < m ? J[lo + i] : 0u;
-        y[q] = (check && i > 0 && i < m) ? J[lo + i - 1] : 0u;
         val[q] = i < m ? V[lo + i] : (typename E::raw)0;
     }
     bool bad = false;
+    if (check) {
 #pragma unroll
-    for (int q = 0; q < kCooSlots; q++) {
-        const uint32_t i = l + 64 * q;
-        if (check && i < m) bad = bad || x[q] < first || x[q] >= limit || (i > 0 && x[q] <= y[q]);
+        for (int q = 0; q < kCooSlots; q++) {
+            // the predecessor of entry l + 64 q: lane l - 1's, or lane 63's of
+            // the slot before (shuffled, not read again)
+            const uint32_t up = __shfl_up(x[q], 1);
+            const uint32_t wrap = q > 0 ? __shfl(x[q > 0 ? q - 1 : 0], 63) : 0u;
+            const uint32_t y = l > 0 ? up : wrap;
+            const uint32_t i = l + 64 * q;
+            if (i < m) bad = bad || x[q] < first || x[q] >= limit || (i > 0 && x[q] <= y);
+        }
     }
     return !__any(bad);
 }
@@ -2241,6 +2246,70 @@ __device__ __forceinline__ void store_from_stage(typename E::raw* col, uint64_t 
     }
 }
 
+// Tiles [t0, tend) of a COO expansion, from entries lo .. lo + cnt of J and
+// V (checked, in index order), a quarter tile (16 rows, kChunkVals elements)
+// at a time: the quarter is zeroed in the wave's LDS buffer, the entries that
+// fall in it are written there, and it is stored with 16-byte stores (element
+// stores when out is not 16-byte aligned).  Entries are held in registers a
+// chunk (kCooChunk) at a time, the first chunk (m entries) already loaded; a
+// quarter takes entries from the next chunks until the held chunk reaches
+// past it.  Every element is written once: zeroing the output first and then
+// storing the values over it wrote the lines twice.  Elements at or past n are
+// not written.
+template <class E>
+__device__ __forceinline__ void coo_tiles_lds(const uint32_t* J, const typename E::raw* V, uint32_t lo, uint32_t cnt,
+                                              uint32_t m, uint32_t (&x)[kCooSlots], typename E::raw (&val)[kCooSlots],
+                                              uint64_t t0, uint64_t tend, uint64_t n, typename E::raw* out,
+                                              typename E::raw* buf) {
+    using raw = typename E::raw;
+    constexpr uint32_t per16 = 16 / sizeof(raw);
+    constexpr uint32_t chunks = kChunkVals / per16;           // 16-byte chunks of a quarter
+    static_assert(chunks % 64 == 0, "whole chunks per lane");
+    const uint32_t l = lane_id();
+    const bool vec = (reinterpret_cast<uintptr_t>(out) & 15u) == 0;
+    uint4* b4 = reinterpret_cast<uint4*>(buf);
+    uint32_t c0 = 0;                                          // entries before the held chunk
+#pragma unroll 1
+    for (uint64_t base = t0 * kTileElems; base < tend * kTileElems && base < n; base += kChunkVals) {
+        const uint64_t rem = n - base;
+        const uint32_t b32 = (uint32_t)base;                  // indices are below 2^32
+#pragma unroll
+        for (uint32_t k = 0; k < chunks / 64; k++) b4[l + 64 * k] = uint4{0, 0, 0, 0};
+        wave_lds_sync();
+#pragma unroll 1
+        while (true) {
+#pragma unroll
+            for (int q = 0; q < kCooSlots; q++) {
+                const uint32_t rel = x[q] - b32;
+                if (l + 64u * q < m && rel < kChunkVals) buf[rel] = val[q];
+            }
+            if (c0 + m >= cnt) break;                         // no entries beyond the held chunk
+            uint32_t xl = 0;                                  // index of the held chunk's last entry
+#pragma unroll
+            for (int q = 0; q < kCooSlots; q++)
+                if ((uint32_t)q == (m - 1) / 64) xl = x[q];
+            if (lane_bcast(xl, (m - 1) % 64) - b32 >= kChunkVals) break;   // it reaches past this quarter
+            c0 += m;
+            m = cnt - c0 < kCooChunk ? cnt - c0 : kCooChunk;
+            coo_load_pairs<E>(J, V, lo + c0, m, false, 0, 0, x, val);
+        }
+        wave_lds_sync();
+        raw* o = out + base;
+#pragma unroll
+        for (uint32_t k = 0; k < chunks / 64; k++) {
+            const uint32_t c = l + 64 * k;
+            const uint64_t e0 = (uint64_t)c * per16;
+            if (vec && e0 + per16 <= rem) {
+                st_stream(reinterpret_cast<uint4*>(o) + c, b4[c]);
+            } else if (e0 < rem) {
+                const uint32_t k1 = rem - e0 < per16 ? (uint32_t)(rem - e0) : per16;
+                for (uint32_t k = 0; k < k1; k++) st_stream(&o[e0 + k], buf[e0 + k]);
+            }
+        }
+        wave_lds_sync();
+    }
+}
+
 // Tiles [t0, t0 + K) of one checked message (format fmt, nnz nonzeros, n
 // elements, T tiles; d = its dense values for a dense message, msg = the
 // message for a Pici one) expanded into out[0 .. n).  One wave; all reads
@@ -2254,11 +2323,10 @@ __device__ __forceinline__ void expand_tiles(const uint8_t* msg, const uint8_t* 
     const uint64_t g_n = n, g_T = T;
     if (fmt == (uint32_t)kFmtCoo) {
         // The wave's entry range, searched over the whole index array (so
-        // neighbouring waves meet exactly).  Its entries are read (checked:
-        // inside the wave's tiles, below n, strictly increasing), the tiles
-        // are written with zeros, and after those stores have completed each
-        // lane stores its entries' values at their indices.  A range larger
-        // than one chunk is checked in a pass of its own first.
+        // neighbouring waves meet exactly), its entries checked (inside the
+        // wave's tiles, below n, strictly increasing: as they are loaded when
+        // they fit one chunk, else in a pass of their own first), then the
+        // tiles assembled in LDS a quarter at a time (coo_tiles_lds).
         const uint32_t* J = reinterpret_cast<const uint32_t*>(msg + kHeaderBytes);
         const raw* V = reinterpret_cast<const raw*>(msg + coo_off_V(nnz));
         const uint64_t tend = t0 + K < g_T ? t0 + K : g_T;
@@ -2271,27 +2339,13 @@ __device__ __forceinline__ void expand_tiles(const uint8_t* msg, const uint8_t* 
         uint32_t cnt = ok ? hi - lo : 0u;
         uint32_t x[kCooSlots];
         raw val[kCooSlots];
-        if (cnt) ok = coo_load_pairs<E>(J, V, lo, cnt < kCooChunk ? cnt : kCooChunk, one, first, limit, x, val);
+        uint32_t m = cnt < kCooChunk ? cnt : kCooChunk;
+        if (m) ok = coo_load_pairs<E>(J, V, lo, m, one, first, limit, x, val);
         if (!ok) {
-            cnt = 0;
+            cnt = m = 0;
             if (l == 0) set_status(ctrl, SPCCL_ERR_CORRUPT_STREAM);
         }
-        for (uint64_t t = t0; t < tend; t++) {
-            raw* col = out + t * kTileElems + l;
-            const uint64_t rem = g_n - t * kTileElems;
-#pragma unroll 8
-            for (int r = 0; r < 64; r++)
-                if ((uint64_t)(64 * r + l) < rem) col[64 * r] = (raw)0;
-        }
-        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");      // the zeros are written before any value
-#pragma unroll 1
-        for (uint32_t i0 = 0; i0 < cnt; i0 += kCooChunk) {
-            const uint32_t m = cnt - i0 < kCooChunk ? cnt - i0 : kCooChunk;
-            if (i0) coo_load_pairs<E>(J, V, lo + i0, m, false, 0, 0, x, val);
-#pragma unroll
-            for (int q = 0; q < kCooSlots; q++)
-                if (l + 64u * q < m) out[x[q]] = val[q];
-        }
+        coo_tiles_lds<E>(J, V, lo, cnt, m, x, val, t0, tend, g_n, out, stage);
         return;
     }
     if (fmt != (uint32_t)kFmtPici) {
@@ -2390,7 +2444,7 @@ template <class E, int K>
 __device__ __forceinline__ void gather_body(const DevOperand& op, uint8_t* out_part, uint64_t n, uint64_t T,
                                             WsCtrl* ctrl) {
     using raw = typename E::raw;
-    __shared__ raw stage_all[kWavesPerBlock][kChunkVals];
+    __shared__ __attribute__((aligned(16))) raw stage_all[kWavesPerBlock][kChunkVals];
     __shared__ uint32_t s_ok, s_fmt;
     __shared__ uint64_t s_nnz;
     const uint32_t wave = threadIdx.x >> 6;
