@@ -114,7 +114,7 @@ uint64_t spccl_stream_bound(uint64_t n, int32_t dtype);
 
 /* Workspace for messages of up to n elements: a 256-byte control block
  * (the sticky device status), one 64-bit look-back word per partition of
- * 16384 elements, two tile indexes of COO operands (one 64-bit word per
+ * 16384 elements and one per 256 partitions, two tile indexes of COO operands (one 64-bit word per
  * 4096-element tile plus one, each), one worst-case slot of compacted values
  * per partition (n elements' worth) and one of 32-bit indices (COO outputs).
  * spccl_workspace_min_bytes covers the first three regions.  A reduce whose
@@ -124,8 +124,8 @@ uint64_t spccl_stream_bound(uint64_t n, int32_t dtype);
  * (long runs of empty tiles) and every tile of a reduce with a smaller
  * workspace (at least the control block, for a dense result) search.  With the
  * value slots, Pici-producing calls run as two passes that never wait while
- * holding input data (count and park values, then resolve offsets by
- * look-back and move); a workspace of only spccl_workspace_min_bytes selects
+ * holding input data (count and park values, then add up the counts per
+ * chunk of partitions and move); a workspace of only spccl_workspace_min_bytes selects
  * the single-pass kernels, which resolve offsets by decoupled look-back
  * while holding their tiles.  Outputs are identical.  COO outputs always
  * take three passes and need the full workspace.  Zero-fill a workspace once before first use (or clear it with

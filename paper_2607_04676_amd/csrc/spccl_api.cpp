@@ -47,7 +47,7 @@ inline uint64_t align256(uint64_t x) { return (x + 255ull) & ~255ull; }
 // COO operands, value slots (the two-pass Pici sink and the COO sink), index
 // slots (the COO sink).
 inline uint64_t coo_index_offset(uint64_t n, int which) {
-    return align256(kWsFlagsOffset + 8ull * num_parts(n)) + (uint64_t)which * align256(8ull * (num_tiles(n) + 1));
+    return align256(kWsFlagsOffset + 8ull * flag_words(n)) + (uint64_t)which * align256(8ull * (num_tiles(n) + 1));
 }
 inline uint64_t slots_offset(uint64_t n) { return coo_index_offset(n, 2); }
 inline uint64_t value_slots_end(uint64_t n, int32_t dt) {

@@ -54,6 +54,19 @@ __host__ __device__ inline uint64_t num_parts(uint64_t n) {
     return p ? p : 1;
 }
 
+// The second pass of a two-pass Pici sink sums the partitions' aggregates per
+// chunk of kPlaceChunk partitions; each chunk's sum has a look-back word of its
+// own, after the partitions' words.
+constexpr uint32_t kPlaceChunk = 256;
+__host__ __device__ inline uint64_t num_place_chunks(uint64_t nparts) {
+    return (nparts + kPlaceChunk - 1) / kPlaceChunk;
+}
+// look-back words of a workspace for n elements: one per partition, one per chunk
+__host__ __device__ inline uint64_t flag_words(uint64_t n) {
+    const uint64_t p = num_parts(n);
+    return p + num_place_chunks(p);
+}
+
 // A fresh 30-bit epoch for the look-back words of one launch (host).
 uint32_t next_epoch();
 

@@ -1748,29 +1748,36 @@ __global__ void __launch_bounds__(kBlockThreads) k_pp_part(PiciSinkArgs g) {
 }
 
 // Second pass of the two-pass Pici sink.  Every aggregate is final when this
-// kernel starts (the first pass has completed), so a block can add up its
-// predecessors' aggregates itself with ordinary cached loads -- no waiting on
-// other blocks.  That costs p loads for partition p, so past
-// kPlaceDirectMax partitions the blocks fall back to decoupled look-back
-// (which only waits for inclusive prefixes published by this pass).
-constexpr uint32_t kPlaceDirectMax = 16384;
-
+// kernel starts (the first pass has completed), so a partition's offset is a
+// sum of final numbers, found in two levels instead of by adding up all p
+// predecessors (p loads for partition p, O(P^2) for the pass): the partitions
+// are grouped in chunks of kPlaceChunk, block c of the first
+// num_place_chunks(P) blocks adds up chunk c's aggregates and publishes the
+// sum in the look-back word that follows the partitions' (flags[P + c]), and
+// a block adds the sums of the chunks before its own to the aggregates of
+// its own chunk's partitions before it.  A block waits only for chunk sums
+// published by lower-numbered blocks, which publish before they wait for
+// anything, and work-groups start in index order, so every wait ends (a spin
+// limit bounds it regardless and turns a stall into SPCCL_ERR_TIMEOUT).
 constexpr uint32_t kNoAggregate = 0xFFFFFFFFu;   // a partition the first pass did not publish
 constexpr uint32_t kPlacePer = kWavesPerBlock;   // partitions placed by one block (one per wave)
+static_assert(kPlaceChunk == kBlockThreads, "one aggregate of a chunk per thread");
+static_assert(kPlaceChunk % kPlacePer == 0, "a block's partitions lie in one chunk");
 
 // Each wave moves one partition.  Its own aggregate, the first kEarly slot
-// values per lane, its tiles' relative offsets and the block's share of the
-// predecessor sum are read at once; once the aggregate is known the rest of
-// the partition's values (up to kMore per lane) are read while the block
-// combines the predecessor sum; then every store.  Reads waited for after a
-// store would also wait for that store, hence all reads first.
+// values per lane, its tiles' relative offsets and one aggregate per thread
+// (its chunk's predecessors and, for a summing block, the chunk it sums) are
+// read at once; once the aggregate is known the rest of the partition's values
+// (up to kMore per lane) are read while the block waits for the chunk sums;
+// then every store.  Reads waited for after a store would also wait for that
+// store, hence all reads first.
 template <class E>
 __device__ __forceinline__ void place_body(const PiciSinkArgs& g) {
     using raw = typename E::raw;
-    constexpr int J = 8;
     constexpr uint32_t kEarly = 4;          // slot values per lane read before the aggregate is known
     constexpr uint32_t kMore = 16;          // slot values per lane read once it is
-    __shared__ uint32_t s_base, s_part[kWavesPerBlock], s_agg[kPlacePer];
+    __shared__ uint32_t s_base, s_part[kWavesPerBlock], s_csum[kWavesPerBlock], s_agg[kPlacePer];
+    __shared__ bool s_ok;
     const uint32_t wave = threadIdx.x >> 6, l = lane_id();
     const uint32_t p0 = blockIdx.x * kPlacePer;
     const uint32_t p = p0 + wave;
@@ -1779,31 +1786,26 @@ __device__ __forceinline__ void place_body(const PiciSinkArgs& g) {
     const uint64_t oI = off_I(g.n), oA = off_A(g.n);
     uint32_t* I = reinterpret_cast<uint32_t*>(g.out + oI);
     const raw* slot = reinterpret_cast<const raw*>(g.slots) + (uint64_t)p * kPartElems;
+    uint64_t* csums = g.flags + g.nparts;
+    const uint32_t chunk = p0 / kPlaceChunk;
+    const bool summer = blockIdx.x < num_place_chunks(g.nparts);
 
     // independent of every offset: own aggregate word, first slot values
-    // (a slot always has kPartElems of room), the tiles' relative offsets
+    // (a slot always has kPartElems of room), the tiles' relative offsets,
+    // the aggregates this block adds up
     const uint64_t f = mine ? g.flags[p] : 0ull;
     raw early[kEarly];
 #pragma unroll
     for (uint32_t u = 0; u < kEarly; u++) early[u] = mine ? slot[l + 64 * u] : (raw)0;
     const uint64_t t = (uint64_t)p * kTilesPerPart + l;
     const uint32_t tile_rel = (mine && l < kTilesPerPart && t < g.T) ? I[t] : 0u;
-    // this block's share of the sum of all earlier aggregates: two words per
-    // 16-byte load, eight independent loads in flight per thread
-    uint32_t part = 0;
-    if (g.nparts <= kPlaceDirectMax) {
-        const uint4* f2 = reinterpret_cast<const uint4*>(g.flags);
-        const uint32_t pairs = p0 / 2;                          // p0 is even
-        for (uint32_t q0 = threadIdx.x; q0 < pairs; q0 += 8 * kBlockThreads) {
-            uint4 x[8];
-#pragma unroll
-            for (int u = 0; u < 8; u++) {
-                const uint32_t q = q0 + u * kBlockThreads;
-                x[u] = q < pairs ? f2[q] : uint4{0, 0, 0, 0};
-            }
-#pragma unroll
-            for (int u = 0; u < 8; u++) part += x[u].x + x[u].z;    // low words hold the aggregates
-        }
+    const uint32_t qp = chunk * kPlaceChunk + threadIdx.x;           // a predecessor in this chunk
+    uint32_t part = qp < p0 ? (uint32_t)g.flags[qp] : 0u;
+    const uint32_t qs = blockIdx.x * kPlaceChunk + threadIdx.x;      // a partition of the summed chunk
+    uint32_t csum = 0;
+    if (summer && qs < g.nparts) {
+        const uint64_t fs = g.flags[qs];
+        csum = (uint32_t)(fs >> 34) == epoch30 ? (uint32_t)fs : 0u;
     }
     uint32_t agg = (uint32_t)f;
     bool bad = mine && ((uint32_t)(f >> 34) != epoch30 || agg > kPartElems);   // the first pass did not run
@@ -1816,39 +1818,65 @@ __device__ __forceinline__ void place_body(const PiciSinkArgs& g) {
         more[u] = i < agg ? slot[i] : (raw)0;
     }
     part = wave_sum(part);
+    csum = wave_sum(csum);
     if (l == 0) {
         s_part[wave] = part;
+        s_csum[wave] = csum;
         s_agg[wave] = bad ? kNoAggregate : agg;
         if (bad) set_status(g.ctrl, SPCCL_ERR_WORKSPACE);
     }
     __syncthreads();
+    if (summer && threadIdx.x == 0) {
+        uint32_t sum = 0;
+#pragma unroll
+        for (uint32_t k = 0; k < kWavesPerBlock; k++) sum += s_csum[k];
+        publish(g.flags, g.nparts + blockIdx.x, epoch30, kFlagPrefix, sum);
+    }
     bool any_bad = false;
-    uint32_t prefix = 0, tot = 0;
+    uint32_t prefix = 0;
 #pragma unroll
     for (uint32_t k = 0; k < kPlacePer; k++) {
         const uint32_t ak = s_agg[k];
         any_bad = any_bad || ak == kNoAggregate;
         prefix += k < wave ? ak : 0u;
-        tot += ak;
     }
     if (any_bad) return;          // the first pass stopped at a bad header: write nothing
-    if (g.nparts <= kPlaceDirectMax) {
-        uint32_t base = 0;
 #pragma unroll
-        for (uint32_t k = 0; k < kWavesPerBlock; k++) base += s_part[k];
-        prefix += base;
-    } else {
+    for (uint32_t k = 0; k < kWavesPerBlock; k++) prefix += s_part[k];
+    if (chunk != 0) {
+        // the sums of chunks 0 .. chunk-1, 64 per round, each round until
+        // every one of them carries this call's epoch
         if (wave == 0) {
-            Window<J> win{};
-            if (p0 != 0) win = load_window<J>(g.flags, (int64_t)p0 - 1);
-            const uint32_t base = p0 == 0 ? 0u : lookback_from<J>(g.flags, p0, epoch30, g.ctrl, win);
+            uint32_t sum = 0;
+            bool ok = true;
+            for (uint32_t k0 = 0; k0 < chunk && ok; k0 += 64) {
+                const uint32_t k = k0 + l;
+                uint64_t fk = 0;
+                bool ready = k >= chunk;
+                uint32_t spins = 0;
+                while (true) {
+                    if (!ready) {
+                        fk = __hip_atomic_load(&csums[k], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                        ready = (uint32_t)(fk >> 34) == epoch30;
+                    }
+                    if (__all(ready)) break;
+                    if (++spins > kSpinLimit) {
+                        if (l == 0) set_status(g.ctrl, SPCCL_ERR_TIMEOUT);
+                        ok = false;
+                        break;
+                    }
+                    __builtin_amdgcn_s_sleep(1);
+                }
+                sum += k < chunk ? (uint32_t)fk : 0u;
+            }
+            sum = wave_sum(sum);
             if (l == 0) {
-                const uint32_t last = (g.nparts - p0 < kPlacePer ? g.nparts - p0 : kPlacePer) - 1;
-                publish(g.flags, p0 + last, epoch30, kFlagPrefix, base + tot);
-                s_base = base;
+                s_base = sum;
+                s_ok = ok;
             }
         }
         __syncthreads();
+        if (!s_ok) return;        // a chunk sum never came: write nothing
         prefix += s_base;
     }
     if (!mine) return;

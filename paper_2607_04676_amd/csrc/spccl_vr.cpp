@@ -89,7 +89,7 @@ Layout carve(void* scratch, int32_t P, uint64_t msg_elems, int32_t dtype) {
     L.ws = static_cast<uint8_t*>(scratch);
     L.ws_bytes = round_up(spccl_workspace_bytes(msg_elems, dtype));
     L.flags = L.ws + L.ws_bytes;
-    L.flag_bytes = round_up(8ull * num_parts(msg_elems));
+    L.flag_bytes = round_up(8ull * flag_words(msg_elems));
     L.vslots = L.flags + (uint64_t)P * L.flag_bytes;
     L.vslot_bytes = round_up(num_parts(msg_elems) * kPartElems * elem_bytes(dtype));
     L.slot_bytes = slot_need(msg_elems, dtype);
