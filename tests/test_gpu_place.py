@@ -1,0 +1,87 @@
+"""GPU parity of the two-pass Pici sink around the chunks its second pass
+sums (Sec. III-B, the global exclusive scan of the tile counts): message
+sizes that end just inside a chunk of 256 partitions, one partition into the
+next chunk, and several chunks with a ragged last one, at a low and a high
+density (small and large parked values per partition), for compression,
+dense (+) Pici -> Pici and Pici (+) Pici -> Pici, all on one workspace
+sized for the largest message (so each call meets the previous call's chunk
+sums), against the oracle byte for byte."""
+import numpy as np
+import pytest
+
+import oracle as O
+import workloads as W
+from helpers import assert_bytes_equal, log, to_dev
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+PART = 16384                 # elements per partition
+CHUNK = 256                  # partitions per summed chunk
+
+
+@pytest.fixture(scope="module")
+def S():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2607_04676_amd as S
+    return S
+
+
+# (partitions, elements short of or past a whole number of partitions)
+SIZES = [(CHUNK, -123), (CHUNK + 1, -(PART - 1)), (2 * CHUNK + 1, -(PART - 4097)), (4 * CHUNK + 3, -3000)]
+
+
+@pytest.fixture(scope="module")
+def ws_big(S):
+    n = max(p * PART + d for p, d in SIZES)
+    return {dt: S.alloc_workspace(n, dt) for dt in (O.F32, O.BF16)}
+
+
+# every size in fp32, the several-chunk one in bf16 as well
+CASES = [(W.F32, size) for size in SIZES] + [(W.BF16, SIZES[-1])]
+
+
+@pytest.mark.parametrize("permille", [990, 500])
+@pytest.mark.parametrize("dtype,size", CASES)
+def test_place_across_chunks(S, ws_big, dtype, size, permille):
+    parts, delta = size
+    n = parts * PART + delta
+    dt = O.BF16 if dtype == W.BF16 else O.F32
+    assert -(-O.num_tiles(n) // 4) == parts
+    seed = parts * 7 + permille
+    a = W.sparse_array(n, W.nnz_for(n, permille), [40, seed, 0, permille], dtype)
+    b = W.sparse_array(n, W.nnz_for(n, permille), [40, seed, 1, permille], dtype)
+    ws = ws_big[dt]
+    pici = lambda t: S.operand(t, S.SPCCL_STREAM, S.SPCCL_FMT_PICI)
+
+    exp_a, _ = O.compress(a)
+    exp_b, _ = O.compress(b)
+    ta = to_dev(a)
+    out = S.alloc_stream(n, dt)
+    out.fill_(0xA5)
+    log(f"place chunks: compress n={n} parts={parts} {dtype} permille={permille}")
+    S.spccl_compress(ta, out, ws)
+    torch.cuda.synchronize()
+    assert S.spccl_read_status(ws) == 0
+    assert_bytes_equal(out[:exp_a.size].cpu().numpy(), exp_a, f"compress parts={parts}")
+
+    mb = S.alloc_stream(n, dt)
+    mb[:exp_b.size].copy_(torch.from_numpy(exp_b))
+    red = S.alloc_stream(n, dt)
+    exp_r, _ = O.reduce(O.Operand.array(a), O.Operand.stream(exp_b), n, dt, O.STREAM, O.FMT_PICI)
+    red.fill_(0x5A)
+    log(f"place chunks: dense+pici n={n}")
+    S.spccl_reduce(S.operand(ta), pici(mb), pici(red), n, dt, ws)
+    torch.cuda.synchronize()
+    assert S.spccl_read_status(ws) == 0
+    assert_bytes_equal(red[:exp_r.size].cpu().numpy(), exp_r, f"dense+pici parts={parts}")
+
+    exp_pp, _ = O.reduce(O.Operand.stream(exp_a), O.Operand.stream(exp_b), n, dt, O.STREAM, O.FMT_PICI)
+    red.fill_(0x3C)
+    log(f"place chunks: pici+pici n={n}")
+    S.spccl_reduce(pici(out), pici(mb), pici(red), n, dt, ws)
+    torch.cuda.synchronize()
+    assert S.spccl_read_status(ws) == 0
+    assert_bytes_equal(red[:exp_pp.size].cpu().numpy(), exp_pp, f"pici+pici parts={parts}")
