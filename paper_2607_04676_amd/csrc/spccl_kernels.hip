@@ -387,6 +387,7 @@ __device__ __forceinline__ void apply_staged(uint64_t wm, uint32_t rank, const t
     for (int r = 0; r < 64; r++) {
         const bool bit = (wm >> r) & 1ull;
         if (((r < 32 ? ulo : uhi) >> (r & 31)) & 1u) {   // rows empty in every column cost one scalar branch
+            asm volatile("");       // keeps that branch apart from the lanes' (see merge_sparse)
             if (bit) {
                 const uint32_t x = stage[rank];
                 rank++;
@@ -501,20 +502,23 @@ __device__ __forceinline__ bool expand_pici_early(PiciCols pc, const EarlyVals& 
 // The values of the rows set in w (this lane's column) in row order to
 // stage[rank ...].  A row set in no lane's word costs one scalar test; the
 // others are written without branching: a lane whose word lacks the row
-// writes its own slot of `spare` (one per lane, so no bank conflicts).
+// writes its own slot of `spare` (one per lane, so no bank conflicts).  The
+// address is own + bit * (next - own), one 24-bit multiply-add, and the
+// distance grows by bit: three VALU operations a row (a select would take a
+// compare, a hazard wait and a move as well).
 template <class E>
 __device__ __forceinline__ void compact_rows(uint64_t w, uint32_t rank, const uint32_t (&v)[64],
                                              typename E::raw* stage, typename E::raw* spare) {
     using raw = typename E::raw;
     const uint32_t olo = wave_or((uint32_t)w), ohi = wave_or((uint32_t)(w >> 32));
-    raw* dst = stage + rank;
-    raw* own = spare + lane_id();
+    char* own = reinterpret_cast<char*>(spare + lane_id());
+    int dist = (int)(reinterpret_cast<char*>(stage + rank) - own);    // LDS bytes: |dist| < 2^23
 #pragma unroll
     for (int r = 0; r < 64; r++) {
         if (((r < 32 ? olo : ohi) >> (r & 31)) & 1u) {
-            const uint32_t bit = (uint32_t)(w >> r) & 1u;
-            *(bit ? dst : own) = (raw)v[r];
-            dst += bit;
+            const int bit = (int)((w >> r) & 1ull);
+            *reinterpret_cast<raw*>(own + __mul24(bit, dist)) = (raw)v[r];
+            dist += bit * (int)sizeof(raw);
         }
     }
 }
@@ -567,7 +571,11 @@ __device__ __forceinline__ bool merge_sparse(const EarlyPici& ep, typename E::ra
     for (int j = 0; j < kEarlySlots; j++)
         if (l + 64u * j < pc.cnt) bv[l + 64 * j] = (raw)ep.ev.x[j];
     wave_lds_sync();
-    // rows held by both operands: add (an exact cancellation leaves the row absent)
+    // rows held by both operands: add (an exact cancellation leaves the row
+    // absent).  Few rows hold any: a row no lane holds twice costs one scalar
+    // test (the empty asm keeps that test a scalar branch of its own; merged
+    // with the lanes' test it would cost every row vector work and a branch
+    // on the execution mask).
     const uint64_t ov = wa & pc.w;
     uint64_t cancelled = 0;
     const uint32_t olo = wave_or((uint32_t)ov), ohi = wave_or((uint32_t)(ov >> 32));
@@ -575,6 +583,7 @@ __device__ __forceinline__ bool merge_sparse(const EarlyPici& ep, typename E::ra
 #pragma unroll
         for (int r = 0; r < 64; r++) {
             if (((r < 32 ? olo : ohi) >> (r & 31)) & 1u) {
+                asm volatile("");
                 if ((ov >> r) & 1ull) {
                     const uint32_t j = (uint32_t)__popcll(pc.w & ((1ull << r) - 1ull));
                     v[r] = oplus(E{}, v[r], (uint32_t)bv[pc.colpref + j]);
