@@ -5,7 +5,8 @@ next chunk, and several chunks with a ragged last one, at a low and a high
 density (small and large parked values per partition), for compression,
 dense (+) Pici -> Pici and Pici (+) Pici -> Pici, all on one workspace
 sized for the largest message (so each call meets the previous call's chunk
-sums), against the oracle byte for byte."""
+sums), against the oracle byte for byte; and either side of the size where
+Pici (+) Pici's first pass changes its shape."""
 import numpy as np
 import pytest
 
@@ -31,16 +32,19 @@ def S():
 
 # (partitions, elements short of or past a whole number of partitions)
 SIZES = [(CHUNK, -123), (CHUNK + 1, -(PART - 1)), (2 * CHUNK + 1, -(PART - 4097)), (4 * CHUNK + 3, -3000)]
+# either side of the size where Pici (+) Pici's first pass changes from one
+# tile per wave to one partition per wave (2048 partitions)
+EDGE = [(2047, -7), (2048, -(PART - 1))]
 
 
 @pytest.fixture(scope="module")
 def ws_big(S):
-    n = max(p * PART + d for p, d in SIZES)
+    n = max(p * PART + d for p, d in SIZES + EDGE)
     return {dt: S.alloc_workspace(n, dt) for dt in (O.F32, O.BF16)}
 
 
 # every size in fp32, the several-chunk one in bf16 as well
-CASES = [(W.F32, size) for size in SIZES] + [(W.BF16, SIZES[-1])]
+CASES = [(W.F32, size) for size in SIZES + EDGE] + [(W.BF16, SIZES[-1])]
 
 
 @pytest.mark.parametrize("permille", [990, 500])
