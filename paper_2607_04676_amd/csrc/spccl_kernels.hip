@@ -1486,6 +1486,7 @@ template <class E, bool Deferred>
 __global__ void __launch_bounds__(kBlockThreads) k_pp_tile(PiciSinkArgs g) {
     using raw = typename E::raw;
     __shared__ raw lds_in[kWavesPerBlock][kChunkVals];
+    __shared__ raw lds_out[Deferred ? kWavesPerBlock : 1][Deferred ? kChunkVals : 1];
     __shared__ uint32_t s_cnt[kWavesPerBlock];
     __shared__ uint32_t s_prefix;
     const uint32_t wave = threadIdx.x >> 6, l = lane_id();
@@ -1554,7 +1555,13 @@ __global__ void __launch_bounds__(kBlockThreads) k_pp_tile(PiciSinkArgs g) {
     if constexpr (Deferred) {
         if (!has_tile) return;
         raw* slot = reinterpret_cast<raw*>(g.slots) + (uint64_t)p * kPartElems + tile_excl;
-        if (one) {
+        if (one && tilecnt <= kChunkVals) {
+            // merged in LDS, then to the slot with contiguous stores
+            raw* ob = lds_out[Deferred ? wave : 0];
+            pp_merge<E>(ca.w, cb.w, wo, in, ca.colpref, la + cb.colpref, ob, cpo, true);
+            wave_lds_sync();
+            for (uint32_t i = l; i < tilecnt; i += 64) slot[i] = ob[i];
+        } else if (one) {
             pp_merge<E>(ca.w, cb.w, wo, in, ca.colpref, la + cb.colpref, slot, cpo, true);
         } else {
 #pragma unroll 1
@@ -3043,11 +3050,11 @@ inline uint32_t stream_grid(uint64_t work_items, uint32_t per_block, uint32_t ca
 }
 
 // Pici (+) Pici -> Pici in two passes: below this many partitions the first
-// pass takes one tile per wave (k_pp_tile, four times the waves: 12.8 against
-// 20.1 us at 2^20 fp32 elements, sigma 0.99, 20.2 against 39.5 at 0.9, still
-// ahead at 2^24), from it one partition per wave (k_pp_part, whose values
-// leave through LDS in contiguous stores: 28.2 against 29.7 us at 2^26 and
-// sigma 0.99, 75 against 101 at 0.9; even at 2^25).
+// pass takes one tile per wave (k_pp_tile, four times the waves: 12.7 against
+// 20.1 us at 2^20 fp32 elements, sigma 0.99, 20.9 against 39.5 at 0.9, 32.8
+// against 46.1 at 2^24 and 0.9), from it one partition per wave (k_pp_part,
+// four tiles' values per LDS flush: 28.2 against 36.3 us at 2^26 and sigma
+// 0.99, 75.0 against 80.4 at 0.9; at 2^25 they are level).
 constexpr uint32_t kPPTileMaxParts = 2048;
 
 template <class E>
