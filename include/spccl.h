@@ -128,7 +128,7 @@ uint64_t spccl_stream_bound(uint64_t n, int32_t dtype);
  * chunk of partitions and move); a workspace of only spccl_workspace_min_bytes selects
  * the single-pass kernels, which resolve offsets by decoupled look-back
  * while holding their tiles.  Outputs are identical.  COO outputs always
- * take three passes and need the full workspace.  Zero-fill a workspace once before first use (or clear it with
+ * take two passes and need the full workspace.  Zero-fill a workspace once before first use (or clear it with
  * spccl_workspace_init); look-back words are tagged with a per-launch epoch,
  * so it needs no clearing between calls.  One workspace must not be used by
  * two calls in flight at once. */

@@ -174,7 +174,7 @@ spccl_status_t spccl_compress(const void* dense, uint64_t n, int32_t dtype, void
 }
 
 namespace {
-// The COO sink (three passes; needs the full workspace with its slots).
+// The COO sink (two passes; needs the full workspace with its slots).
 // A COO operand gets a tile index (k_coo_index) in the workspace when the
 // workspace has room for it (spccl_workspace_min_bytes); otherwise its tiles
 // search J for their entries.  The workspace has been checked.

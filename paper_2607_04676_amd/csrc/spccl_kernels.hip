@@ -1999,17 +1999,16 @@ __global__ void __launch_bounds__(256) k_coo_index(const uint8_t* msg, uint64_t 
 }
 
 // ---------------------------------------------------------------------------
-// COO sink: out = COO(srcA (+) srcB) (Sec. II-B format), in three passes.
+// COO sink: out = COO(srcA (+) srcB) (Sec. II-B format), in two passes.
 // The value array of a COO message starts after all nnz indices, so no entry
 // can be placed before the total is known:
 //   k_to_coo       each partition (one block, one tile per wave) computes its
 //                  tiles, counts, publishes its aggregate and parks its
 //                  (index, value) entries in its own worst-case slots; never
 //                  waits on another block;
-//   k_coo_total    one block turns the aggregates into exclusive prefixes
-//                  (written back into the look-back words) and writes the
-//                  header and the pad;
-//   k_place_coo    one wave per partition moves its entries into place.
+//   k_place_coo    the partitions' offsets and the total from per-chunk sums
+//                  of the aggregates, the header and the pad; one wave per
+//                  partition moves its entries into place.
 // Entries leave a tile in row-major order, i.e. by increasing flat index:
 // row r's present lanes are a ballot mask, and each takes the position of
 // the set bits below it.
@@ -2079,99 +2078,110 @@ __global__ void __launch_bounds__(kBlockThreads) k_to_coo(PiciSinkArgs g) {
     for (uint32_t i = l; i < rank; i += 64) { islot[done + i] = sidx[i]; vslot[done + i] = stage[i]; }
 }
 
-// One block: exclusive prefixes of the partitions' aggregates (each thread
-// sums a contiguous run of partitions, the block scans the run totals), the
-// header and the pad between J and V.  A partition that did not publish
-// (an input failed its header check) stops the call: nothing is written.
-// The words are read with device-scope loads (they were published by
-// device-scope stores from every XCD; this block's own XCD may still cache
-// the lines it wrote in an earlier call), kTotalRun at a time with every
-// load in flight.
-constexpr uint32_t kTotalThreads = 1024;
-constexpr uint32_t kTotalRun = 8;
-
-template <class E>
-__global__ void __launch_bounds__(kTotalThreads) k_coo_total(PiciSinkArgs g) {
-    __shared__ uint32_t s_wsum[kTotalThreads / 64];
-    __shared__ uint32_t s_bad;
-    const uint32_t tid = threadIdx.x, l = lane_id(), wave = tid >> 6;
-    const uint32_t epoch30 = g.epoch & 0x3FFFFFFFu;
-    const uint32_t per = (g.nparts + kTotalThreads - 1) / kTotalThreads;
-    const uint32_t p0 = tid * per, p1 = p0 + per < g.nparts ? p0 + per : g.nparts;
-    if (tid == 0) s_bad = 0;
-    __syncthreads();
-    uint32_t run = 0;
-    bool bad = false;
-    for (uint32_t q0 = p0; q0 < p1; q0 += kTotalRun) {
-        uint64_t f[kTotalRun];
-#pragma unroll
-        for (uint32_t u = 0; u < kTotalRun; u++)
-            f[u] = q0 + u < p1 ? __hip_atomic_load(&g.flags[q0 + u], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0ull;
-#pragma unroll
-        for (uint32_t u = 0; u < kTotalRun; u++) {
-            if (q0 + u < p1) {
-                bad = bad || (uint32_t)(f[u] >> 34) != epoch30 || (uint32_t)f[u] > kPartElems;
-                run += (uint32_t)f[u];
-            }
-        }
-    }
-    if (bad) s_bad = 1;
-    const uint32_t incl = wave_incl_scan(run);
-    if (l == 63) s_wsum[wave] = incl;
-    __syncthreads();
-    if (s_bad) {
-        if (tid == 0) set_status(g.ctrl, SPCCL_ERR_WORKSPACE);
-        return;
-    }
-    uint32_t wbase = 0, total = 0;
-    for (uint32_t k = 0; k < kTotalThreads / 64; k++) {
-        const uint32_t x = s_wsum[k];
-        wbase += k < wave ? x : 0u;
-        total += x;
-    }
-    uint32_t excl = wbase + incl - run;
-    for (uint32_t q0 = p0; q0 < p1; q0 += kTotalRun) {
-        uint64_t f[kTotalRun];
-#pragma unroll
-        for (uint32_t u = 0; u < kTotalRun; u++)
-            f[u] = q0 + u < p1 ? __hip_atomic_load(&g.flags[q0 + u], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0ull;
-#pragma unroll
-        for (uint32_t u = 0; u < kTotalRun; u++) {
-            if (q0 + u < p1) {
-                publish(g.flags, q0 + u, epoch30, kFlagPrefix, excl);
-                excl += (uint32_t)f[u];
-            }
-        }
-    }
-    const uint64_t nnz = total, oV = coo_off_V(nnz);
-    if (tid == 0) write_header(g.out, kFmtCoo, E::dtype, g.n, nnz, kHeaderBytes, oV, coo_bytes(E::dtype, nnz));
-    for (uint64_t b = kHeaderBytes + 4 * nnz + tid; b < oV; b += kTotalThreads) g.out[b] = 0;
-}
-
-// One wave per partition: its prefix and count from the scanned words, all
-// its slot reads before its stores.
+// Second pass of the COO sink, one wave per partition.  The values' offset
+// depends on the total count, so every block needs every partition's
+// aggregate: as in the Pici place pass, block c of the first
+// num_place_chunks(P) blocks adds up chunk c's aggregates and publishes the
+// sum (flags[P + c]; state kFlagAggregate instead of kFlagPrefix if a
+// partition of the chunk did not publish: an input failed its header check
+// and nothing is written), and every block adds the chunk sums up to its
+// prefix and to the total.  The summing blocks publish before they wait for
+// anything and are the lowest-numbered ones, which start first and all fit
+// the device at once (at most 1024 blocks for n < 2^32), so every wait ends;
+// a spin limit bounds it regardless and turns a stall into SPCCL_ERR_TIMEOUT.
+// Block 0 writes the header and the pad between J and V.
 template <class E>
 __global__ void __launch_bounds__(kBlockThreads) k_place_coo(PiciSinkArgs g) {
     using raw = typename E::raw;
     constexpr int U = 8;
+    __shared__ uint32_t s_part[kWavesPerBlock], s_csum[kWavesPerBlock], s_bad[kWavesPerBlock], s_agg[kWavesPerBlock];
+    __shared__ uint32_t s_base, s_total, s_ok;
     const uint32_t wave = threadIdx.x >> 6, l = lane_id();
-    const uint32_t p = blockIdx.x * kWavesPerBlock + wave;
-    if (p >= g.nparts) return;
+    const uint32_t p0 = blockIdx.x * kWavesPerBlock;
+    const uint32_t p = p0 + wave;
+    const bool mine = p < g.nparts;
     const uint32_t epoch30 = g.epoch & 0x3FFFFFFFu;
-    const uint64_t f = __hip_atomic_load(&g.flags[p], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    const uint64_t fn = p + 1 < g.nparts ? __hip_atomic_load(&g.flags[p + 1], __ATOMIC_RELAXED,
-                                                             __HIP_MEMORY_SCOPE_AGENT) : 0ull;
-    const HeaderWords hw = load_header_words(g.out);
-    const uint64_t nnz = hw.w[2];
-    if ((uint32_t)hw.w[0] != kMagic || (uint32_t)(f >> 34) != epoch30 || ((uint32_t)(f >> 32) & 3u) != kFlagPrefix)
-        return;                   // k_coo_total stopped the call
-    const uint32_t prefix = (uint32_t)f;
-    const uint32_t next = p + 1 < g.nparts ? (uint32_t)fn : (uint32_t)nnz;
-    const uint32_t cnt = next - prefix;
+    const uint32_t nchunks = (uint32_t)num_place_chunks(g.nparts);
+    const uint32_t chunk = p0 / kPlaceChunk;
+    const bool summer = blockIdx.x < nchunks;
+    uint64_t* csums = g.flags + g.nparts;
+
+    const uint64_t f = mine ? g.flags[p] : 0ull;
+    const uint32_t qp = chunk * kPlaceChunk + threadIdx.x;           // a predecessor in this chunk
+    uint32_t part = qp < p0 ? (uint32_t)g.flags[qp] : 0u;
+    const uint32_t qs = blockIdx.x * kPlaceChunk + threadIdx.x;      // a partition of the summed chunk
+    uint32_t csum = 0, bad = 0;
+    if (summer && qs < g.nparts) {
+        const uint64_t fs = g.flags[qs];
+        bad = (uint32_t)(fs >> 34) != epoch30 || (uint32_t)fs > kPartElems;
+        csum = bad ? 0u : (uint32_t)fs;
+    }
+    part = wave_sum(part);
+    csum = wave_sum(csum);
+    bad = wave_or(bad);
+    if (l == 0) {
+        s_part[wave] = part;
+        s_csum[wave] = csum;
+        s_bad[wave] = bad;
+        s_agg[wave] = mine ? (uint32_t)f : 0u;
+    }
+    __syncthreads();
+    if (summer && threadIdx.x == 0) {
+        uint32_t sum = 0, any = 0;
+#pragma unroll
+        for (uint32_t k = 0; k < kWavesPerBlock; k++) { sum += s_csum[k]; any |= s_bad[k]; }
+        if (any) set_status(g.ctrl, SPCCL_ERR_WORKSPACE);
+        publish(g.flags, g.nparts + blockIdx.x, epoch30, any ? kFlagAggregate : kFlagPrefix, sum);
+    }
+    // every chunk sum, 64 per round, each round until all carry this call's epoch
+    if (wave == 0) {
+        uint32_t before = 0, total = 0;
+        bool ok = true;
+        for (uint32_t k0 = 0; k0 < nchunks && ok; k0 += 64) {
+            const uint32_t k = k0 + l;
+            uint64_t fk = 0;
+            bool ready = k >= nchunks;
+            uint32_t spins = 0;
+            while (true) {
+                if (!ready) {
+                    fk = __hip_atomic_load(&csums[k], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    ready = (uint32_t)(fk >> 34) == epoch30;
+                }
+                if (__all(ready)) break;
+                if (++spins > kSpinLimit) {
+                    if (l == 0) set_status(g.ctrl, SPCCL_ERR_TIMEOUT);
+                    ok = false;
+                    break;
+                }
+                __builtin_amdgcn_s_sleep(1);
+            }
+            ok = ok && !__any(k < nchunks && ((uint32_t)(fk >> 32) & 3u) != kFlagPrefix);
+            const uint32_t v = k < nchunks ? (uint32_t)fk : 0u;
+            before += wave_sum(k < chunk ? v : 0u);
+            total += wave_sum(v);
+        }
+        if (l == 0) {
+            s_base = before;
+            s_total = total;
+            s_ok = ok;
+        }
+    }
+    __syncthreads();
+    if (!s_ok) return;            // a partition did not publish, or a chunk sum never came: write nothing
+    uint32_t prefix = s_base;
+#pragma unroll
+    for (uint32_t k = 0; k < kWavesPerBlock; k++) prefix += s_part[k] + (k < wave ? s_agg[k] : 0u);
+    const uint64_t nnz = s_total, oV = coo_off_V(nnz);
+    if (blockIdx.x == 0 && threadIdx.x == 0) {
+        write_header(g.out, kFmtCoo, E::dtype, g.n, nnz, kHeaderBytes, oV, coo_bytes(E::dtype, nnz));
+        for (uint64_t b = kHeaderBytes + 4 * nnz; b < oV; b++) g.out[b] = 0;
+    }
+    if (!mine) return;
+    const uint32_t cnt = (uint32_t)f;
     const uint32_t* islot = g.idx_slots + (uint64_t)p * kPartElems;
     const raw* vslot = reinterpret_cast<const raw*>(g.slots) + (uint64_t)p * kPartElems;
     uint32_t* J = reinterpret_cast<uint32_t*>(g.out + kHeaderBytes) + prefix;
-    raw* V = reinterpret_cast<raw*>(g.out + coo_off_V(nnz)) + prefix;
+    raw* V = reinterpret_cast<raw*>(g.out + oV) + prefix;
     for (uint32_t i0 = l; i0 < cnt; i0 += 64 * U) {
         uint32_t x[U];
         raw y[U];
@@ -3101,7 +3111,7 @@ spccl_status_t launch_to_pici(int sa, int sb, const PiciSinkArgs& g, hipStream_t
     return launch_status();
 }
 
-// COO sink: count pass, one-block scan of the partition totals, place pass.
+// COO sink: count pass, then the place pass (offsets and total from chunk sums).
 template <class E>
 spccl_status_t launch_to_coo(int sa, int sb, const PiciSinkArgs& g, hipStream_t st) {
     dim3 grid(g.nparts), block(kBlockThreads);
@@ -3114,9 +3124,6 @@ spccl_status_t launch_to_coo(int sa, int sb, const PiciSinkArgs& g, hipStream_t 
     else return SPCCL_ERR_UNSUPPORTED;
 #undef SPCCL_TO_COO
     spccl_status_t st1 = launch_status();
-    if (st1 != SPCCL_OK) return st1;
-    hipLaunchKernelGGL(k_coo_total<E>, dim3(1), dim3(kTotalThreads), 0, st, g);
-    st1 = launch_status();
     if (st1 != SPCCL_OK) return st1;
     hipLaunchKernelGGL(k_place_coo<E>, dim3((g.nparts + kWavesPerBlock - 1) / kWavesPerBlock), block, 0, st, g);
     return launch_status();
