@@ -114,21 +114,23 @@ uint64_t spccl_stream_bound(uint64_t n, int32_t dtype);
 
 /* Workspace for messages of up to n elements: a 256-byte control block
  * (the sticky device status), one 64-bit look-back word per partition of
- * 16384 elements and one per 256 partitions, two tile indexes of COO operands (one 64-bit word per
- * 4096-element tile plus one, each), one worst-case slot of compacted values
- * per partition (n elements' worth) and one of 32-bit indices (COO outputs).
- * spccl_workspace_min_bytes covers the first three regions.  A reduce whose
- * workspace holds them gives each COO operand a tile index (the first entry
- * of every tile, tagged with the call, built from J by one extra pass) so its
- * tiles find their entries without searching J; tiles the index leaves out
- * (long runs of empty tiles) and every tile of a reduce with a smaller
- * workspace (at least the control block, for a dense result) search.  With the
- * value slots, Pici-producing calls run as two passes that never wait while
- * holding input data (count and park values, then add up the counts per
- * chunk of partitions and move); a workspace of only spccl_workspace_min_bytes selects
- * the single-pass kernels, which resolve offsets by decoupled look-back
- * while holding their tiles.  Outputs are identical.  COO outputs always
- * take two passes and need the full workspace.  Zero-fill a workspace once before first use (or clear it with
+ * 16384 elements and one per 256 partitions, two tile indexes of COO operands
+ * (one 64-bit word per 4096-element tile plus one, each), one worst-case slot
+ * of compacted values per partition (n elements' worth) and one of 32-bit
+ * indices (COO outputs).  spccl_workspace_min_bytes covers the first three
+ * regions.  A reduce whose workspace holds them gives each COO operand a tile
+ * index (the first entry of every tile, tagged with the call, built from J by
+ * one extra pass) so its tiles find their entries without searching J; tiles
+ * the index leaves out (long runs of empty tiles) and every tile of a reduce
+ * with a smaller workspace (at least the control block, for a dense result)
+ * search.  With the value slots, Pici-producing calls above the single-pass
+ * limit (spccl_set_single_pass_limit) run as two passes that never wait while
+ * holding input data (count and park values, then add up the counts per chunk
+ * of partitions and move); smaller outputs, and every call on a workspace of
+ * only spccl_workspace_min_bytes, take the single-pass kernels, which resolve
+ * offsets by decoupled look-back while holding their tiles.  Outputs are
+ * identical.  COO outputs always take two passes and need the full workspace.
+ * Zero-fill a workspace once before first use (or clear it with
  * spccl_workspace_init); look-back words are tagged with a per-launch epoch,
  * so it needs no clearing between calls.  One workspace must not be used by
  * two calls in flight at once. */
@@ -137,6 +139,18 @@ uint64_t spccl_workspace_min_bytes(uint64_t n, int32_t dtype);
 
 /* Zero-fill a workspace with a fill kernel on `stream` (no memset nodes). */
 spccl_status_t spccl_workspace_init(void* ws, uint64_t ws_bytes, void* stream);
+
+/* Pici outputs of at most max_partitions partitions (of 16384 elements) are
+ * written in a single pass even when the workspace holds the value slots: on
+ * small arrays the two-pass sink's second launch costs more than the
+ * look-back (Sec. III-B phase 2, the global scan).  Pici (+) Pici -> Pici
+ * takes half the limit (its two-pass first launch is lighter).  Default 1024;
+ * 0 keeps every call with a full workspace on two passes.  COO outputs, and
+ * the ring steps that the collectives batch over all ranks in one launch,
+ * always take two passes.  Process-wide (every device and thread), takes
+ * effect for later calls; outputs are identical either way.
+ * Returns the previous limit. */
+uint32_t spccl_set_single_pass_limit(uint32_t max_partitions);
 
 /* Exact byte size of a COO message with nnz nonzeros (Sec. II-B sizes: a
  * 32-bit index and a value per nonzero; plus header and pad).  0 for an

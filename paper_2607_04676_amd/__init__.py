@@ -42,7 +42,8 @@ EXPORTS = ("spccl_num_tiles", "spccl_pici_bytes", "spccl_stream_bound", "spccl_w
            "spccl_reduce_sliced", "spccl_copy_sliced", "spccl_coo_bytes", "spccl_message_bound",
            "spccl_compress_coo", "spccl_slice_tracker_bytes", "spccl_compress_sliced_tracked",
            "spccl_reduce_sliced_tracked", "spccl_vr_sliced_scratch_bytes", "spccl_vr_reduce_scatter_sliced",
-           "spccl_vr_all_gather_sliced", "spccl_vr_all_reduce_sliced", "spccl_compress_static")
+           "spccl_vr_all_gather_sliced", "spccl_vr_all_reduce_sliced", "spccl_compress_static",
+           "spccl_set_single_pass_limit")
 
 
 class spccl_operand_t(ctypes.Structure):
@@ -76,6 +77,7 @@ _sigs = {
     "spccl_workspace_bytes": (_u64, [_u64, _i32]),
     "spccl_workspace_min_bytes": (_u64, [_u64, _i32]),
     "spccl_workspace_init": (_i32, [_vp, _u64, _vp]),
+    "spccl_set_single_pass_limit": (ctypes.c_uint32, [ctypes.c_uint32]),
     "spccl_compress": (_i32, [_vp, _u64, _i32, _vp, _u64, _vp, _u64, _vp]),
     "spccl_compress_coo": (_i32, [_vp, _u64, _i32, _vp, _u64, _vp, _u64, _vp]),
     "spccl_compress_static": (_i32, [_vp, _u64, _i32, _vp, _u64, _vp]),
@@ -182,6 +184,12 @@ def spccl_workspace_bytes(n: int, dtype: int) -> int:
 
 def spccl_workspace_min_bytes(n: int, dtype: int) -> int:
     return _lib.spccl_workspace_min_bytes(n, dtype)
+
+
+def spccl_set_single_pass_limit(max_partitions: int) -> int:
+    """Largest Pici output (in 16384-element partitions) written in one pass
+    even with a full workspace; returns the previous limit."""
+    return _lib.spccl_set_single_pass_limit(max_partitions)
 
 
 def spccl_coo_bytes(dtype: int, nnz: int) -> int:

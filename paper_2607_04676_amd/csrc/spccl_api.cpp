@@ -26,6 +26,7 @@ spccl_status_t launch_sliced_dt(int dtype, const SlicedArgs& g, int op, hipStrea
 spccl_status_t launch_copy_sliced(const SlicedArgs& g, hipStream_t st);
 spccl_status_t launch_coo_index(const uint8_t* msg, uint64_t cap, uint64_t n, int dtype, uint64_t* idx,
                                 uint32_t epoch, WsCtrl* ctrl, hipStream_t st);
+uint32_t set_single_pass_max_parts(uint32_t parts);
 }  // namespace spccl
 
 namespace spccl {
@@ -144,6 +145,10 @@ uint64_t spccl_message_bound(uint64_t n, int32_t dtype, int32_t fmt) {
     else if (fmt == SPCCL_FMT_COO) w = coo_bytes(dtype, n);
     else return 0;
     return w > d ? w : d;
+}
+
+uint32_t spccl_set_single_pass_limit(uint32_t max_partitions) {
+    return spccl::set_single_pass_max_parts(max_partitions);
 }
 
 spccl_status_t spccl_workspace_init(void* ws, uint64_t ws_bytes, void* stream) {

@@ -23,6 +23,7 @@
 // reduction adds in fp32 (bf16 operands widened exactly, the sum rounded once
 // to bf16, nearest-even); an absent operand is the identity.
 #include <hip/hip_runtime.h>
+#include <atomic>
 #include <stdint.h>
 
 
@@ -3067,11 +3068,31 @@ inline uint32_t stream_grid(uint64_t work_items, uint32_t per_block, uint32_t ca
 // 0.99, 75.0 against 80.4 at 0.9; at 2^25 they are level).
 constexpr uint32_t kPPTileMaxParts = 2048;
 
+}  // namespace
+
+// A Pici output of at most this many partitions is written in a single pass
+// (look-back) even when the workspace has the value slots: on small arrays
+// the second launch costs more than the look-back. Measured in fp32 at sigma
+// 0.99 (0.9), single against two passes: compression at 2^20 elements 9.6
+// against 12.2 us (10.4 against 15.6), at 2^24 = 1024 partitions 21.8 against
+// 22.5 (23.0 against 27.3), at 2^25 40.7 against 34.7 (level); dense (+) Pici
+// -> Pici the same within 1 us. Pici (+) Pici -> Pici, whose two-pass first
+// launch is lighter, takes half the limit: 14.9 against 14.8 us at 2^23 (23.5
+// against 25.9), 18.4 against 16.5 at 2^24 (35.0 against 31.9).
+// spccl_set_single_pass_limit changes it.
+std::atomic<uint32_t> g_single_pass_max_parts{1024};
+
+uint32_t set_single_pass_max_parts(uint32_t parts) { return g_single_pass_max_parts.exchange(parts); }
+
+namespace {
+
 template <class E>
 spccl_status_t launch_to_pici(int sa, int sb, const PiciSinkArgs& g, hipStream_t st) {
     dim3 grid(g.nparts), block(kBlockThreads);
+    const uint64_t limit = g_single_pass_max_parts.load(std::memory_order_relaxed);
+    const bool two_pass = g.slots && g.nparts > limit;
     if (sa == SRC_PICI && sb == SRC_PICI) {
-        if (g.slots) {
+        if (g.slots && 2ull * g.nparts > limit) {
             if (g.nparts < kPPTileMaxParts) {
                 hipLaunchKernelGGL((k_pp_tile<E, true>), grid, block, 0, st, g);
             } else {
@@ -3087,7 +3108,7 @@ spccl_status_t launch_to_pici(int sa, int sb, const PiciSinkArgs& g, hipStream_t
         }
         return launch_status();
     }
-    if (g.slots) {
+    if (two_pass) {
 #define SPCCL_TO_PICI2(A, B) hipLaunchKernelGGL((k_to_pici<E, A, B, true>), grid, block, 0, st, g)
         if (sa == SRC_DENSE && sb == SRC_NONE) SPCCL_TO_PICI2(SRC_DENSE, SRC_NONE);
         else if (sa == SRC_DENSE && sb == SRC_DENSE) SPCCL_TO_PICI2(SRC_DENSE, SRC_DENSE);

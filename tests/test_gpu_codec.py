@@ -38,9 +38,18 @@ def make(n, nnz, seed, dtype, specials=False):
 
 
 @pytest.fixture(params=["two_pass", "single_pass"])
-def ws_mode(request):
-    """Full workspace (count + place passes) or minimal (single-pass look-back)."""
-    return request.param
+def ws_mode(request, S):
+    """Full workspace with the count + place passes forced at every size (the
+    library otherwise writes small outputs in one pass), or a minimal workspace
+    (single-pass look-back)."""
+    if request.param != "two_pass":
+        yield request.param
+        return
+    prev = S.spccl_set_single_pass_limit(0)
+    try:
+        yield request.param
+    finally:
+        S.spccl_set_single_pass_limit(prev)
 
 
 def gpu_compress(S, a, ws=None, minimal=False):

@@ -100,8 +100,18 @@ def plant_zeros(msg, n, dt, k, seed):
 
 
 @pytest.fixture(params=["two_pass", "single_pass"])
-def ws_mode(request):
-    return request.param
+def ws_mode(request, S):
+    """Full workspace with the count + place passes forced at every size (the
+    library otherwise writes small outputs in one pass), or a minimal workspace
+    (single-pass look-back)."""
+    if request.param != "two_pass":
+        yield request.param
+        return
+    prev = S.spccl_set_single_pass_limit(0)
+    try:
+        yield request.param
+    finally:
+        S.spccl_set_single_pass_limit(prev)
 
 
 @pytest.mark.parametrize("dtype", [W.F32, W.BF16])

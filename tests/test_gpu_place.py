@@ -6,7 +6,10 @@ density (small and large parked values per partition), for compression,
 dense (+) Pici -> Pici and Pici (+) Pici -> Pici, all on one workspace
 sized for the largest message (so each call meets the previous call's chunk
 sums), against the oracle byte for byte; and either side of the size where
-Pici (+) Pici's first pass changes its shape."""
+Pici (+) Pici's first pass changes its shape. The library writes outputs of
+at most 1,024 partitions in a single pass by default; these tests lower that
+limit to zero so the two passes run at every size, and a second test checks
+the default on both sides of the limit with the same large workspace."""
 import numpy as np
 import pytest
 
@@ -47,9 +50,33 @@ def ws_big(S):
 CASES = [(W.F32, size) for size in SIZES + EDGE] + [(W.BF16, SIZES[-1])]
 
 
+@pytest.fixture
+def two_pass_always(S):
+    prev = S.spccl_set_single_pass_limit(0)
+    try:
+        yield
+    finally:
+        S.spccl_set_single_pass_limit(prev)
+
+
 @pytest.mark.parametrize("permille", [990, 500])
 @pytest.mark.parametrize("dtype,size", CASES)
-def test_place_across_chunks(S, ws_big, dtype, size, permille):
+def test_place_across_chunks(S, ws_big, two_pass_always, dtype, size, permille):
+    check_sinks(S, ws_big, dtype, size, permille)
+
+
+# the default single-pass limit (1,024 partitions) and one partition past it,
+# plus a small message, all on the large workspace
+DEFAULT = [(1, -(PART - 100)), (CHUNK + 1, -(PART - 1)), (1024, -5), (1025, -(PART - 1))]
+
+
+@pytest.mark.parametrize("size", DEFAULT)
+def test_default_single_pass_limit(S, ws_big, size):
+    assert S.spccl_set_single_pass_limit(1024) == 1024
+    check_sinks(S, ws_big, W.F32, size, 990)
+
+
+def check_sinks(S, ws_big, dtype, size, permille):
     parts, delta = size
     n = parts * PART + delta
     dt = O.BF16 if dtype == W.BF16 else O.F32
