@@ -128,8 +128,12 @@ uint64_t spccl_stream_bound(uint64_t n, int32_t dtype);
  * holding input data (count and park values, then add up the counts per chunk
  * of partitions and move); smaller outputs, and every call on a workspace of
  * only spccl_workspace_min_bytes, take the single-pass kernels, which resolve
- * offsets by decoupled look-back while holding their tiles.  Outputs are
- * identical.  COO outputs always take two passes and need the full workspace.
+ * offsets by decoupled look-back while holding their tiles.  Pici (+) Pici ->
+ * Pici of 2048 to 4096 partitions is one launch that parks what its buffer
+ * cannot hold, then finds its offset from the partitions' and chunks' counts
+ * and moves its values (all of its waves fit the device at once).  Outputs
+ * are identical.  COO outputs always take two passes and need the full
+ * workspace.
  * Zero-fill a workspace once before first use (or clear it with
  * spccl_workspace_init); look-back words are tagged with a per-launch epoch,
  * so it needs no clearing between calls.  One workspace must not be used by

@@ -1400,6 +1400,16 @@ struct PPGroup {
     static constexpr int count = 64 / cols;
 };
 
+// Whether staging round j (lanes' j-th values) holds any of `count` values.
+// 32-bit values skip empty rounds behind a uniform branch; 16-bit ones take
+// every round, since behind such branches their loads were each waited for
+// before the next was issued (measured: bf16 Pici (+) Pici at sigma 0.9,
+// 2^27 elements, 119 -> 155 us).
+template <class E>
+__device__ __forceinline__ bool stage_round(int j, uint32_t count) {
+    return sizeof(typename E::raw) != 4 || 64u * (uint32_t)j < count;
+}
+
 // The value ranges of columns [c0, c1) of both operands into in[]: a's at
 // [0, la), b's at [la, la + lb) (la + lb <= kChunkVals), every load issued
 // before the first is used.  Returns la; zero = some staged value has
@@ -1419,14 +1429,17 @@ __device__ __forceinline__ uint32_t pp_stage(const PiciCols& ca, const PiciCols&
 #pragma unroll
     for (int j = 0; j < kChunkSlots; j++) {
         const uint32_t i = l + 64 * j;
-        x[j] = i < la ? pa[a0 + i] : (i < la + lb ? pb[b0 + (i - la)] : (raw)1);
+        x[j] = (raw)1;
+        if (stage_round<E>(j, la + lb)) x[j] = i < la ? pa[a0 + i] : (i < la + lb ? pb[b0 + (i - la)] : (raw)1);
     }
     bool z = false;
 #pragma unroll
     for (int j = 0; j < kChunkSlots; j++) {
         const uint32_t i = l + 64 * j;
-        z |= x[j] == 0;
-        if (i < la + lb) in[i] = x[j];
+        if (stage_round<E>(j, la + lb)) {
+            z |= x[j] == 0;
+            if (i < la + lb) in[i] = x[j];
+        }
     }
     zero = __any(z);
     wave_lds_sync();
@@ -1435,39 +1448,48 @@ __device__ __forceinline__ uint32_t pp_stage(const PiciCols& ca, const PiciCols&
 
 // Cancellations (exact zero sums) among the rows of this lane's column held by
 // both operands -- or by either one when `zero` says a staged value is itself
-// zero -- with a's run at in[ra ...] and b's at in[rb ...].
+// zero -- with a's run at in[ra ...] and b's at in[rb ...].  Branch-free over
+// the lane's rows: each round takes the lowest row still to check (no row for
+// a lane that is done: it reads in[0] and changes nothing).
 template <class E>
 __device__ __forceinline__ uint64_t pp_cancel(uint64_t wa, uint64_t wb, const typename E::raw* in, uint32_t ra,
                                               uint32_t rb, bool zero, bool mine) {
     uint64_t chk = mine ? (zero ? (wa | wb) : (wa & wb)) : 0ull;
     uint64_t cancel = 0;
     while (__any(chk != 0ull)) {
-        if (chk) {
-            const uint32_t r = (uint32_t)__builtin_ctzll(chk);
-            chk &= chk - 1ull;
-            const uint64_t below = (1ull << r) - 1ull;
-            const uint32_t xa = ((wa >> r) & 1ull) ? (uint32_t)in[ra + (uint32_t)__popcll(wa & below)] : 0u;
-            const uint32_t xb = ((wb >> r) & 1ull) ? (uint32_t)in[rb + (uint32_t)__popcll(wb & below)] : 0u;
-            if (oplus(E{}, xa, xb) == 0u) cancel |= 1ull << r;
-        }
+        const uint64_t bit = chk & (0ull - chk);
+        chk ^= bit;
+        const uint64_t below = bit - 1ull;
+        const bool ha = (wa & bit) != 0ull, hb = (wb & bit) != 0ull;
+        const uint32_t va = (uint32_t)in[ha ? ra + (uint32_t)__popcll(wa & below) : 0u];
+        const uint32_t vb = (uint32_t)in[hb ? rb + (uint32_t)__popcll(wb & below) : 0u];
+        const uint32_t x = oplus(E{}, ha ? va : 0u, hb ? vb : 0u);
+        cancel |= x == 0u ? bit : 0ull;
     }
     return cancel;
 }
 
 // Row-order merge of this lane's two runs (a's at in[ia ...], b's at
-// in[ib ...]); results present in wo go to dst[k ...].
+// in[ib ...]); results present in wo go to dst[k ...].  Each round takes the
+// lane's lowest remaining row: the two reads and the run positions advance
+// without branches (a lane that is done reads in[0] and changes nothing),
+// only the store is predicated.
 template <class E>
 __device__ __forceinline__ void pp_merge(uint64_t wa, uint64_t wb, uint64_t wo, const typename E::raw* in,
                                          uint32_t ia, uint32_t ib, typename E::raw* dst, uint32_t k, bool mine) {
     uint64_t todo = mine ? (wa | wb) : 0ull;
     while (__any(todo != 0ull)) {
-        if (todo) {
-            const uint32_t r = (uint32_t)__builtin_ctzll(todo);
-            todo &= todo - 1ull;
-            uint32_t xa = 0, xb = 0;
-            if ((wa >> r) & 1ull) { xa = in[ia]; ia++; }
-            if ((wb >> r) & 1ull) { xb = in[ib]; ib++; }
-            if ((wo >> r) & 1ull) { dst[k] = (typename E::raw)oplus(E{}, xa, xb); k++; }
+        const uint64_t bit = todo & (0ull - todo);
+        todo ^= bit;
+        const bool ha = (wa & bit) != 0ull, hb = (wb & bit) != 0ull;
+        const uint32_t va = (uint32_t)in[ha ? ia : 0u];
+        const uint32_t vb = (uint32_t)in[hb ? ib : 0u];
+        ia += ha ? 1u : 0u;
+        ib += hb ? 1u : 0u;
+        const uint32_t x = oplus(E{}, ha ? va : 0u, hb ? vb : 0u);
+        if ((wo & bit) != 0ull) {
+            dst[k] = (typename E::raw)x;
+            k++;
         }
     }
 }
@@ -1479,10 +1501,10 @@ __device__ __forceinline__ void pp_merge(uint64_t wa, uint64_t wb, uint64_t wo, 
 // kChunkVals, else per column group), finds exact cancellations among the
 // rows both operands hold, and merges each column's two runs in row order
 // into its place once the partition's offset is known by decoupled
-// look-back (the single-pass mode of a minimal workspace; with a full one,
-// k_pp_part and k_place run instead).  Deferred: the first of two passes
-// instead -- each partition publishes its aggregate and parks its merged
-// values in its own slot, as k_to_pici's first pass does.
+// look-back (a minimal workspace, or a small output).  Deferred: the first
+// of two passes instead -- each partition publishes its aggregate and parks
+// its merged values in its own slot, as k_to_pici's first pass does (a full
+// workspace below 2048 partitions; from there k_pp_part runs).
 template <class E, bool Deferred>
 __global__ void __launch_bounds__(kBlockThreads) k_pp_tile(PiciSinkArgs g) {
     using raw = typename E::raw;
@@ -1613,17 +1635,28 @@ __global__ void __launch_bounds__(kBlockThreads) k_pp_tile(PiciSinkArgs g) {
     }
 }
 
-// Pici (+) Pici -> Pici, first of the two passes, one partition (four tiles)
-// per wave.  The wave reads the column words of its four tiles and their
-// offsets in one round trip; when the partition's values (a contiguous range
-// of each operand) fit the stage together, they arrive in one more; each
-// tile's merged results go into an LDS output buffer in partition order,
-// which is written to the partition's slot with contiguous stores whenever
-// the next tile might not fit, and at the end.  A wave needs no other wave,
-// so the 4096 waves of a 256 MiB array fit the device at once.  Tiles whose
-// values do not fit the stage take it one tile (or one column group) at a
-// time.  Slot layout, offsets and counts are those k_place expects.
-template <class E>
+// Pici (+) Pici -> Pici, one partition (four tiles) per wave.  The wave
+// reads the column words of its four tiles and their offsets in one round
+// trip; when the partition's values (a contiguous range of each operand) fit
+// the stage together, they arrive in one more; each tile's merged results go
+// into an LDS output buffer in partition order, which is written to the
+// partition's slot with contiguous stores whenever the next tile might not
+// fit.  Tiles whose values do not fit the stage take it one tile (or one
+// column group) at a time.
+// Single = false: the first of two passes; the buffer goes to the slot at the
+// end too, and k_place moves the slot into place (slot layout, offsets and
+// counts are those k_place expects).  A wave needs no other wave.
+// Single = true: the wave publishes its aggregate and finds its offset itself
+// in two levels, as k_place does: the aggregates of the partitions before it
+// in its chunk of kPlaceChunk, and the sum of each earlier chunk, which the
+// chunk's last partition publishes (flags[P + c]) as soon as it has read its
+// chunk's aggregates.  A wave waits only for lower-numbered partitions, which
+// publish their aggregates before they wait for anything (and the chunk sums
+// depend on nothing else), and work-groups start in index order, so every
+// wait ends (bounded by the spin limit regardless).  It then moves its parked
+// values and its buffer into place: no second launch, and at high sparsity
+// nothing parked.
+template <class E, bool Single>
 __global__ void __launch_bounds__(kBlockThreads) k_pp_part(PiciSinkArgs g) {
     using raw = typename E::raw;
     constexpr int K = (int)kTilesPerPart;
@@ -1701,14 +1734,17 @@ __global__ void __launch_bounds__(kBlockThreads) k_pp_part(PiciSinkArgs g) {
 #pragma unroll
         for (int j = 0; j < kChunkSlots; j++) {
             const uint32_t i = l + 64 * j;
-            x[j] = i < la ? Aa[a_lo + i] : (i < la + lb ? Ab[b_lo + (i - la)] : (raw)1);
+            x[j] = (raw)1;
+            if (stage_round<E>(j, la + lb)) x[j] = i < la ? Aa[a_lo + i] : (i < la + lb ? Ab[b_lo + (i - la)] : (raw)1);
         }
         bool z = false;
 #pragma unroll
         for (int j = 0; j < kChunkSlots; j++) {
             const uint32_t i = l + 64 * j;
-            z |= x[j] == 0;
-            if (i < la + lb) in[i] = x[j];
+            if (stage_round<E>(j, la + lb)) {
+                z |= x[j] == 0;
+                if (i < la + lb) in[i] = x[j];
+            }
         }
         zero_all = __any(z);
         wave_lds_sync();
@@ -1740,9 +1776,9 @@ __global__ void __launch_bounds__(kBlockThreads) k_pp_part(PiciSinkArgs g) {
             cancel = pp_cancel<E>(A.w, B.w, in, ia, ib, zero, true);
         } else if (one) {
             wave_lds_sync();
-            const uint32_t sa = pp_stage<E>(A, B, Aa + A.base, Ab + B.base, 0, 64, in, zero);
+            pp_stage<E>(A, B, Aa + A.base, Ab + B.base, 0, 64, in, zero);
             ia = A.colpref;
-            ib = sa + B.colpref;
+            ib = A.cnt + B.colpref;
             cancel = pp_cancel<E>(A.w, B.w, in, ia, ib, zero, true);
         } else {
 #pragma unroll 1
@@ -1780,9 +1816,108 @@ __global__ void __launch_bounds__(kBlockThreads) k_pp_part(PiciSinkArgs g) {
         }
         excl += tilecnt;
     }
-    flush();
-    if (l < ntile) reinterpret_cast<uint32_t*>(g.out + oI)[t0 + l] = tile_rel;   // k_place adds the prefix
-    if (l == 0) publish(g.flags, p, epoch30, kFlagAggregate, flushed);
+    uint32_t* I = reinterpret_cast<uint32_t*>(g.out + oI);
+    if constexpr (!Single) {
+        flush();
+        if (l < ntile) I[t0 + l] = tile_rel;       // k_place adds the prefix
+        if (l == 0) publish(g.flags, p, epoch30, kFlagAggregate, flushed);
+        return;
+    }
+    const uint32_t agg = flushed + fill;
+    if (l == 0) publish(g.flags, p, epoch30, kFlagAggregate, agg);
+    const uint32_t chunk = p / kPlaceChunk, first = chunk * kPlaceChunk;
+    bool ok = true;
+    // the aggregates of this chunk's partitions before p, four per lane,
+    // reloading those not yet published until all are
+    constexpr int J = (int)(kPlaceChunk / 64);
+    uint32_t local = 0;
+    {
+        uint64_t fq[J];
+        bool ready[J];
+#pragma unroll
+        for (int j = 0; j < J; j++) {
+            ready[j] = first + l + 64u * j >= p;
+            fq[j] = 0;
+        }
+        uint32_t spins = 0;
+        while (true) {
+            bool all = true;
+#pragma unroll
+            for (int j = 0; j < J; j++) {
+                if (!ready[j]) {
+                    fq[j] = __hip_atomic_load(&g.flags[first + l + 64u * j], __ATOMIC_RELAXED,
+                                              __HIP_MEMORY_SCOPE_AGENT);
+                    ready[j] = (uint32_t)(fq[j] >> 34) == epoch30;
+                }
+                all = all && ready[j];
+            }
+            if (__all(all)) break;
+            if (++spins > kSpinLimit) {
+                ok = false;
+                break;
+            }
+            __builtin_amdgcn_s_sleep(1);
+        }
+#pragma unroll
+        for (int j = 0; j < J; j++) local += first + l + 64u * j < p ? (uint32_t)fq[j] : 0u;
+        local = wave_sum(local);
+    }
+    // a chunk's last partition publishes the chunk's sum before it waits for
+    // anything else
+    const bool last_of_chunk = p % kPlaceChunk == kPlaceChunk - 1 || p == g.nparts - 1;
+    if (ok && last_of_chunk && l == 0) publish(g.flags, g.nparts + chunk, epoch30, kFlagAggregate, local + agg);
+    // the sums of chunks 0 .. chunk-1, 64 per round
+    uint32_t base = 0;
+    for (uint32_t k0 = 0; k0 < chunk && ok; k0 += 64) {
+        const uint32_t k = k0 + l;
+        uint64_t fk = 0;
+        bool ready = k >= chunk;
+        uint32_t spins = 0;
+        while (true) {
+            if (!ready) {
+                fk = __hip_atomic_load(&g.flags[g.nparts + k], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                ready = (uint32_t)(fk >> 34) == epoch30;
+            }
+            if (__all(ready)) break;
+            if (++spins > kSpinLimit) {
+                ok = false;
+                break;
+            }
+            __builtin_amdgcn_s_sleep(1);
+        }
+        base += k < chunk ? (uint32_t)fk : 0u;
+    }
+    if (!ok) {                        // a predecessor never published: write nothing more
+        if (l == 0) set_status(g.ctrl, SPCCL_ERR_TIMEOUT);
+        return;
+    }
+    const uint32_t prefix = wave_sum(base) + local;
+    raw* dst = reinterpret_cast<raw*>(g.out + oA) + prefix;
+    if (flushed != 0) {
+        __threadfence_block();        // this wave's parked values are read back below
+        for (uint32_t i0 = l; i0 < flushed; i0 += 64 * 16) {
+            raw x[16];
+#pragma unroll
+            for (int u = 0; u < 16; u++) {
+                const uint32_t i = i0 + 64 * u;
+                x[u] = i < flushed ? slot[i] : (raw)0;
+            }
+#pragma unroll
+            for (int u = 0; u < 16; u++) {
+                const uint32_t i = i0 + 64 * u;
+                if (i < flushed) st_stream(&dst[i], x[u]);
+            }
+        }
+    }
+    wave_lds_sync();
+    for (uint32_t i = l; i < fill; i += 64) st_stream(&dst[flushed + i], ob[i]);
+    if (l < ntile) I[t0 + l] = prefix + tile_rel;
+    if (p == g.nparts - 1 && l == 0) {
+        const uint64_t nnz = (uint64_t)prefix + agg;
+        I[g.T] = (uint32_t)nnz;
+        for (uint64_t b = oI + 4 * (g.T + 1); b < oA; b += 4) *reinterpret_cast<uint32_t*>(g.out + b) = 0u;
+        write_header(g.out, kFmtPici, E::dtype, g.n, nnz, oI, oA, oA + nnz * sizeof(raw));
+    }
 }
 
 // Second pass of the two-pass Pici sink.  Every aggregate is final when this
@@ -3067,6 +3202,14 @@ inline uint32_t stream_grid(uint64_t work_items, uint32_t per_block, uint32_t ca
 // four tiles' values per LDS flush: 28.2 against 36.3 us at 2^26 and sigma
 // 0.99, 75.0 against 80.4 at 0.9; at 2^25 they are level).
 constexpr uint32_t kPPTileMaxParts = 2048;
+// Up to this many partitions (one wave each: the waves the device holds at
+// once at k_pp_part's register use, 4 per SIMD) Pici (+) Pici -> Pici is one
+// launch of k_pp_part<E, true>: a wave that waits for its predecessors'
+// counts keeps no other wave from starting.  Measured at 2^26 fp32 against
+// k_pp_part + k_place: 26.6 against 28.2 us at sigma 0.99, 66.2 against 75.2
+// at 0.9; at 2^27 bf16 (8192 partitions, two rounds of waves) 45.9 against
+// 41.5 at 0.99, so larger outputs keep the two passes.
+constexpr uint32_t kPPSingleMaxParts = 4096;
 
 }  // namespace
 
@@ -3097,7 +3240,11 @@ spccl_status_t launch_to_pici(int sa, int sb, const PiciSinkArgs& g, hipStream_t
                 hipLaunchKernelGGL((k_pp_tile<E, true>), grid, block, 0, st, g);
             } else {
                 dim3 wgrid((g.nparts + kWavesPerBlock - 1) / kWavesPerBlock);
-                hipLaunchKernelGGL(k_pp_part<E>, wgrid, block, 0, st, g);
+                if (g.nparts <= kPPSingleMaxParts) {
+                    hipLaunchKernelGGL((k_pp_part<E, true>), wgrid, block, 0, st, g);
+                    return launch_status();
+                }
+                hipLaunchKernelGGL((k_pp_part<E, false>), wgrid, block, 0, st, g);
             }
             spccl_status_t st1 = launch_status();
             if (st1 != SPCCL_OK) return st1;

@@ -3,13 +3,14 @@ sums (Sec. III-B, the global exclusive scan of the tile counts): message
 sizes that end just inside a chunk of 256 partitions, one partition into the
 next chunk, and several chunks with a ragged last one, at a low and a high
 density (small and large parked values per partition), for compression,
-dense (+) Pici -> Pici and Pici (+) Pici -> Pici, all on one workspace
-sized for the largest message (so each call meets the previous call's chunk
-sums), against the oracle byte for byte; and either side of the size where
-Pici (+) Pici's first pass changes its shape. The library writes outputs of
-at most 1,024 partitions in a single pass by default; these tests lower that
-limit to zero so the two passes run at every size, and a second test checks
-the default on both sides of the limit with the same large workspace."""
+dense (+) Pici -> Pici and Pici (+) Pici -> Pici, all on one workspace sized
+for the largest message (so each call meets the previous call's chunk sums),
+against the oracle byte for byte.  Also either side of the sizes where
+Pici (+) Pici's first pass changes its shape (2048 partitions) and up to
+which it finds its offsets itself in one launch (4096).  The library writes
+outputs of at most 1,024 partitions in a single pass by default; these tests
+lower that limit to zero so the other paths run at every size, and a second
+test checks the default on both sides of the limit on the same workspace."""
 import numpy as np
 import pytest
 
@@ -36,8 +37,9 @@ def S():
 # (partitions, elements short of or past a whole number of partitions)
 SIZES = [(CHUNK, -123), (CHUNK + 1, -(PART - 1)), (2 * CHUNK + 1, -(PART - 4097)), (4 * CHUNK + 3, -3000)]
 # either side of the size where Pici (+) Pici's first pass changes from one
-# tile per wave to one partition per wave (2048 partitions)
-EDGE = [(2047, -7), (2048, -(PART - 1))]
+# tile per wave to one partition per wave (2048 partitions), and of the size
+# up to which that pass finds its own offsets in a single launch (4096)
+EDGE = [(2047, -7), (2048, -(PART - 1)), (4096, -3), (4097, -(PART - 1))]
 
 
 @pytest.fixture(scope="module")
@@ -46,8 +48,8 @@ def ws_big(S):
     return {dt: S.alloc_workspace(n, dt) for dt in (O.F32, O.BF16)}
 
 
-# every size in fp32, the several-chunk one in bf16 as well
-CASES = [(W.F32, size) for size in SIZES + EDGE] + [(W.BF16, SIZES[-1])]
+# every size in fp32; in bf16 the several-chunk one and the smallest single launch
+CASES = [(W.F32, size) for size in SIZES + EDGE] + [(W.BF16, SIZES[-1]), (W.BF16, EDGE[1])]
 
 
 @pytest.fixture
