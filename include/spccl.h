@@ -123,16 +123,13 @@ uint64_t spccl_stream_bound(uint64_t n, int32_t dtype);
  * one extra pass) so its tiles find their entries without searching J; tiles
  * the index leaves out (long runs of empty tiles) and every tile of a reduce
  * with a smaller workspace (at least the control block, for a dense result)
- * search.  With the value slots, Pici-producing calls above the single-pass
- * limit (spccl_set_single_pass_limit) run as two passes that never wait while
- * holding input data (count and park values, then add up the counts per chunk
- * of partitions and move); smaller outputs, and every call on a workspace of
- * only spccl_workspace_min_bytes, take the single-pass kernels, which resolve
- * offsets by decoupled look-back while holding their tiles.  Pici (+) Pici ->
- * Pici of 2048 to 4096 partitions is one launch that parks what its buffer
- * cannot hold, then finds its offset from the partitions' and chunks' counts
- * and moves its values (all of its waves fit the device at once).  Outputs
- * are identical.  COO outputs always take two passes and need the full
+ * search.  A Pici-producing call runs as one launch whose partitions find
+ * their offsets from their predecessors' counts while holding their tiles
+ * (every call on a workspace of only spccl_workspace_min_bytes, and sizes
+ * within the limits of spccl_set_single_pass_limit), or as two passes that
+ * never wait while holding input data (count and park values in the slots,
+ * then add up the counts per chunk of partitions and move).  Outputs are
+ * identical.  COO outputs always take two passes and need the full
  * workspace.
  * Zero-fill a workspace once before first use (or clear it with
  * spccl_workspace_init); look-back words are tagged with a per-launch epoch,
@@ -144,16 +141,20 @@ uint64_t spccl_workspace_min_bytes(uint64_t n, int32_t dtype);
 /* Zero-fill a workspace with a fill kernel on `stream` (no memset nodes). */
 spccl_status_t spccl_workspace_init(void* ws, uint64_t ws_bytes, void* stream);
 
-/* Pici outputs of at most max_partitions partitions (of 16384 elements) are
- * written in a single pass even when the workspace holds the value slots: on
- * small arrays the two-pass sink's second launch costs more than the
- * look-back (Sec. III-B phase 2, the global scan).  Pici (+) Pici -> Pici
- * takes half the limit (its two-pass first launch is lighter).  Default 1024;
- * 0 keeps every call with a full workspace on two passes.  COO outputs, and
- * the ring steps that the collectives batch over all ranks in one launch,
- * always take two passes.  Process-wide (every device and thread), takes
- * effect for later calls; outputs are identical either way.
- * Returns the previous limit. */
+/* An upper bound, in partitions of 16384 elements, on the Pici outputs that a
+ * call whose workspace holds the value slots writes in one launch (each
+ * partition finds its offset from the counts of the partitions before it in
+ * its chunk of 256 and the sums of the earlier chunks: Sec. III-B phase 2, the
+ * global scan); larger outputs take the count and place passes.  Within the
+ * bound the library's own limits apply: fp32 outputs of dense sources at
+ * every size, bf16 ones up to 2048 partitions, Pici (+) Pici -> Pici up to
+ * 1024 partitions and from 2048 to 4096 (a kernel with one partition per
+ * wave).  Default UINT32_MAX (the library's limits alone); 0 keeps every such
+ * call on two passes.  COO outputs, and the ring steps that the collectives
+ * batch over all ranks in one launch, always take two passes; a workspace of
+ * only spccl_workspace_min_bytes always one.  Process-wide (every device and
+ * thread), takes effect for later calls; outputs are identical either way.
+ * Returns the previous bound. */
 uint32_t spccl_set_single_pass_limit(uint32_t max_partitions);
 
 /* Exact byte size of a COO message with nnz nonzeros (Sec. II-B sizes: a
@@ -312,9 +313,10 @@ spccl_status_t spccl_reduce_sliced_tracked(const void* a, const void* b, uint64_
  * For callers that cannot allocate device memory (code under HIP graph
  * capture, tight serving loops, harnesses that forbid hipMalloc): the same
  * message as spccl_compress, made by the single-pass kernels, whose scratch
- * (a status word and one look-back word per 16384-element partition) lives in
- * a static device array of the library -- 128 KiB plus a 256-byte control
- * block, one copy per GPU, held until the process ends.  The call allocates
+ * (a status word, one look-back word per 16384-element partition and one per
+ * 256 partitions) lives in a static device array of the library -- 128.5 KiB
+ * plus a 256-byte control block, one copy per GPU, held until the process
+ * ends.  The call allocates
  * nothing.  n <= SPCCL_STATIC_MAX_ELEMS, else SPCCL_ERR_UNSUPPORTED; other
  * argument errors as spccl_compress (out_bytes >= spccl_stream_bound).  Every
  * call on a GPU shares that GPU's array, so calls that overlap on one GPU

@@ -187,8 +187,9 @@ def spccl_workspace_min_bytes(n: int, dtype: int) -> int:
 
 
 def spccl_set_single_pass_limit(max_partitions: int) -> int:
-    """Largest Pici output (in 16384-element partitions) written in one pass
-    even with a full workspace; returns the previous limit."""
+    """Upper bound (in 16384-element partitions) on the Pici outputs written in
+    one launch with a full workspace (0: always two passes; default 2**32 - 1,
+    the library's own limits); returns the previous bound."""
     return _lib.spccl_set_single_pass_limit(max_partitions)
 
 

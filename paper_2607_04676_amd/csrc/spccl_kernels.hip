@@ -1128,87 +1128,80 @@ __device__ __forceinline__ void publish(uint64_t* flags, uint32_t p, uint32_t ep
     __hip_atomic_store(&flags[p], f, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// Look-back words of the 64*J partitions before `start`, position k = 64j + l
-// (counting back from the nearest predecessor) in word j of lane l, so each
-// of the J loads reads 64 consecutive words (512 contiguous bytes).
-// Partitions before 0 decode as an inclusive prefix of 0.
-template <int J>
-struct Window {
-    uint64_t f[J];
-};
+// No exclusive prefix: a wait ran out (an offset is below 2^32 - 1, since
+// n < 2^32).
+constexpr uint32_t kNoPrefix = 0xFFFFFFFFu;
 
-template <int J>
-__device__ __forceinline__ Window<J> load_window(const uint64_t* flags, int64_t start) {
+// Exclusive prefix of partition p in two levels, computed by one whole wave
+// once p has published its own aggregate `agg` (flags[p]): the aggregates of
+// the partitions before p in its chunk of kPlaceChunk (four per lane,
+// reloaded until all carry this call's epoch), then the sums of the earlier
+// chunks (flags[nparts + c]), which each chunk's last partition publishes as
+// soon as it has its chunk's aggregates, before it waits for anything else.
+// A wave waits only for lower-numbered partitions, which publish their
+// aggregates before they wait, and work-groups start in index order, so every
+// wait ends; the spin limit bounds it regardless (ok = false, TIMEOUT set).
+__device__ uint32_t chunk_lookback(uint64_t* flags, uint32_t nparts, uint32_t p, uint32_t agg, uint32_t epoch30,
+                                   WsCtrl* ctrl, bool& ok) {
+    constexpr int J = (int)(kPlaceChunk / 64);
     const uint32_t l = lane_id();
-    Window<J> w;
-#pragma unroll
-    for (int j = 0; j < J; j++) {
-        const int64_t q = start - 64 * (int64_t)j - (int64_t)l;
-        w.f[j] = 0;
-        if (q >= 0) w.f[j] = __hip_atomic_load(&flags[q], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    }
-    return w;
-}
-
-// Exclusive prefix of partition p, computed by one whole wave, starting from
-// an already loaded first window.  Each round ends at the nearest inclusive
-// prefix; every position in front of it must have published (an aggregate)
-// or the round is retried.  Words of another call carry another epoch and
-// count as unpublished.
-template <int J>
-__device__ uint32_t lookback_from(const uint64_t* flags, uint32_t p, uint32_t epoch30, WsCtrl* ctrl, Window<J> win) {
-    constexpr int64_t span = 64 * J;
-    const uint32_t l = lane_id();
-    uint32_t excl = 0;
-    int64_t start = (int64_t)p - 1;
-    uint32_t spins = 0;
-    while (start >= 0) {
-        uint32_t state[J], val[J];
+    const uint32_t chunk = p / kPlaceChunk, first = chunk * kPlaceChunk;
+    ok = true;
+    uint32_t local = 0;
+    {
+        uint64_t fq[J];
+        bool ready[J];
 #pragma unroll
         for (int j = 0; j < J; j++) {
-            const int64_t q = start - 64 * (int64_t)j - (int64_t)l;
-            const uint64_t f = win.f[j];
-            state[j] = q < 0 ? kFlagPrefix : (((uint32_t)(f >> 34) == epoch30) ? (uint32_t)(f >> 32) & 3u : 0u);
-            val[j] = q < 0 ? 0u : (uint32_t)f;
+            ready[j] = first + l + 64u * j >= p;
+            fq[j] = 0;
         }
-        // nearest inclusive prefix: the first word j holding one, then its lowest lane
-        int jP = J;
-        uint32_t lP = 64;
-        bool wait = false;
+        uint32_t spins = 0;
+        while (true) {
+            bool all = true;
 #pragma unroll
-        for (int j = J - 1; j >= 0; j--) {
-            const uint64_t mP = __ballot(state[j] == kFlagPrefix);
-            if (mP) { jP = j; lP = (uint32_t)__builtin_ctzll(mP); }
-        }
-        // every position in front of it must have published
-#pragma unroll
-        for (int j = 0; j < J; j++) {
-            const uint64_t mX = __ballot(state[j] == 0u);
-            const uint64_t front = j < jP ? ~0ull : (j == jP ? ((1ull << lP) - 1ull) : 0ull);
-            wait = wait || (mX & front) != 0ull;
-        }
-        if (wait) {
+            for (int j = 0; j < J; j++) {
+                if (!ready[j]) {
+                    fq[j] = __hip_atomic_load(&flags[first + l + 64u * j], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    ready[j] = (uint32_t)(fq[j] >> 34) == epoch30;
+                }
+                all = all && ready[j];
+            }
+            if (__all(all)) break;
             if (++spins > kSpinLimit) {
-                if (l == 0) set_status(ctrl, SPCCL_ERR_TIMEOUT);
+                ok = false;
                 break;
             }
             __builtin_amdgcn_s_sleep(1);
-            win = load_window<J>(flags, start);
-            continue;
         }
-        uint32_t mine = 0;
 #pragma unroll
-        for (int j = 0; j < J; j++) mine += (j < jP || (j == jP && l <= lP)) ? val[j] : 0u;
-        excl += wave_sum(mine);
-        if (jP < J) break;
-        start -= span;
-        if (start >= 0) win = load_window<J>(flags, start);
+        for (int j = 0; j < J; j++) local += first + l + 64u * j < p ? (uint32_t)fq[j] : 0u;
+        local = wave_sum(local);
     }
-    return excl;
-}
-
-__device__ __forceinline__ uint32_t lookback(const uint64_t* flags, uint32_t p, uint32_t epoch30, WsCtrl* ctrl) {
-    return lookback_from<4>(flags, p, epoch30, ctrl, load_window<4>(flags, (int64_t)p - 1));
+    const bool last_of_chunk = p % kPlaceChunk == kPlaceChunk - 1 || p == nparts - 1;
+    if (ok && last_of_chunk && l == 0) publish(flags, nparts + chunk, epoch30, kFlagAggregate, local + agg);
+    uint32_t base = 0;
+    for (uint32_t k0 = 0; k0 < chunk && ok; k0 += 64) {
+        const uint32_t k = k0 + l;
+        uint64_t fk = 0;
+        bool ready = k >= chunk;
+        uint32_t spins = 0;
+        while (true) {
+            if (!ready) {
+                fk = __hip_atomic_load(&flags[nparts + k], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                ready = (uint32_t)(fk >> 34) == epoch30;
+            }
+            if (__all(ready)) break;
+            if (++spins > kSpinLimit) {
+                ok = false;
+                break;
+            }
+            __builtin_amdgcn_s_sleep(1);
+        }
+        base += k < chunk ? (uint32_t)fk : 0u;
+    }
+    if (!ok && l == 0) set_status(ctrl, SPCCL_ERR_TIMEOUT);
+    return wave_sum(base) + local;
 }
 
 // ---------------------------------------------------------------------------
@@ -1278,8 +1271,7 @@ __device__ __forceinline__ void to_pici_body(const PiciSinkArgs& g) {
         tile_excl += k < wave ? ck : 0u;
         agg += ck;
     }
-    if (threadIdx.x == 0)
-        publish(g.flags, p, epoch30, (p == 0 && !Deferred) ? kFlagPrefix : kFlagAggregate, agg);
+    if (threadIdx.x == 0) publish(g.flags, p, epoch30, kFlagAggregate, agg);
 
     const bool single = tilecnt <= E::cap;        // always so for a sparse-merged tile
     if (has_tile && single) {
@@ -1317,15 +1309,14 @@ __device__ __forceinline__ void to_pici_body(const PiciSinkArgs& g) {
         return;
     }
     if (wave == 0) {
-        const uint32_t prefix = p == 0 ? 0u : lookback(g.flags, p, epoch30, g.ctrl);
-        if (l == 0) {
-            if (p != 0) publish(g.flags, p, epoch30, kFlagPrefix, prefix + agg);
-            s_prefix = prefix;
-        }
+        bool ok;
+        const uint32_t prefix = chunk_lookback(g.flags, g.nparts, p, agg, epoch30, g.ctrl, ok);
+        if (l == 0) s_prefix = ok ? prefix : kNoPrefix;
     }
     __syncthreads();
 
     const uint32_t prefix = s_prefix;
+    if (prefix == kNoPrefix) return;            // a predecessor never published: write nothing
     const uint64_t oI = off_I(g.n), oA = off_A(g.n);
     raw* A = reinterpret_cast<raw*>(g.out + oA);
     const uint32_t tbase = prefix + tile_excl;
@@ -1574,7 +1565,7 @@ __global__ void __launch_bounds__(kBlockThreads) k_pp_tile(PiciSinkArgs g) {
         tile_excl += k < wave ? ck : 0u;
         agg += ck;
     }
-    if (threadIdx.x == 0) publish(g.flags, p, epoch30, (p == 0 && !Deferred) ? kFlagPrefix : kFlagAggregate, agg);
+    if (threadIdx.x == 0) publish(g.flags, p, epoch30, kFlagAggregate, agg);
     if constexpr (Deferred) {
         if (!has_tile) return;
         raw* slot = reinterpret_cast<raw*>(g.slots) + (uint64_t)p * kPartElems + tile_excl;
@@ -1601,14 +1592,13 @@ __global__ void __launch_bounds__(kBlockThreads) k_pp_tile(PiciSinkArgs g) {
         return;
     }
     if (wave == 0) {
-        const uint32_t pre = p == 0 ? 0u : lookback(g.flags, p, epoch30, g.ctrl);
-        if (l == 0) {
-            if (p != 0) publish(g.flags, p, epoch30, kFlagPrefix, pre + agg);
-            s_prefix = pre;
-        }
+        bool ok;
+        const uint32_t pre = chunk_lookback(g.flags, g.nparts, p, agg, epoch30, g.ctrl, ok);
+        if (l == 0) s_prefix = ok ? pre : kNoPrefix;
     }
     __syncthreads();
     const uint32_t prefix = s_prefix;
+    if (prefix == kNoPrefix) return;            // a predecessor never published: write nothing
     raw* dst = reinterpret_cast<raw*>(g.out + oA) + prefix + tile_excl;
     if (has_tile) {
         if (one) {
@@ -1825,73 +1815,9 @@ __global__ void __launch_bounds__(kBlockThreads) k_pp_part(PiciSinkArgs g) {
     }
     const uint32_t agg = flushed + fill;
     if (l == 0) publish(g.flags, p, epoch30, kFlagAggregate, agg);
-    const uint32_t chunk = p / kPlaceChunk, first = chunk * kPlaceChunk;
-    bool ok = true;
-    // the aggregates of this chunk's partitions before p, four per lane,
-    // reloading those not yet published until all are
-    constexpr int J = (int)(kPlaceChunk / 64);
-    uint32_t local = 0;
-    {
-        uint64_t fq[J];
-        bool ready[J];
-#pragma unroll
-        for (int j = 0; j < J; j++) {
-            ready[j] = first + l + 64u * j >= p;
-            fq[j] = 0;
-        }
-        uint32_t spins = 0;
-        while (true) {
-            bool all = true;
-#pragma unroll
-            for (int j = 0; j < J; j++) {
-                if (!ready[j]) {
-                    fq[j] = __hip_atomic_load(&g.flags[first + l + 64u * j], __ATOMIC_RELAXED,
-                                              __HIP_MEMORY_SCOPE_AGENT);
-                    ready[j] = (uint32_t)(fq[j] >> 34) == epoch30;
-                }
-                all = all && ready[j];
-            }
-            if (__all(all)) break;
-            if (++spins > kSpinLimit) {
-                ok = false;
-                break;
-            }
-            __builtin_amdgcn_s_sleep(1);
-        }
-#pragma unroll
-        for (int j = 0; j < J; j++) local += first + l + 64u * j < p ? (uint32_t)fq[j] : 0u;
-        local = wave_sum(local);
-    }
-    // a chunk's last partition publishes the chunk's sum before it waits for
-    // anything else
-    const bool last_of_chunk = p % kPlaceChunk == kPlaceChunk - 1 || p == g.nparts - 1;
-    if (ok && last_of_chunk && l == 0) publish(g.flags, g.nparts + chunk, epoch30, kFlagAggregate, local + agg);
-    // the sums of chunks 0 .. chunk-1, 64 per round
-    uint32_t base = 0;
-    for (uint32_t k0 = 0; k0 < chunk && ok; k0 += 64) {
-        const uint32_t k = k0 + l;
-        uint64_t fk = 0;
-        bool ready = k >= chunk;
-        uint32_t spins = 0;
-        while (true) {
-            if (!ready) {
-                fk = __hip_atomic_load(&g.flags[g.nparts + k], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                ready = (uint32_t)(fk >> 34) == epoch30;
-            }
-            if (__all(ready)) break;
-            if (++spins > kSpinLimit) {
-                ok = false;
-                break;
-            }
-            __builtin_amdgcn_s_sleep(1);
-        }
-        base += k < chunk ? (uint32_t)fk : 0u;
-    }
-    if (!ok) {                        // a predecessor never published: write nothing more
-        if (l == 0) set_status(g.ctrl, SPCCL_ERR_TIMEOUT);
-        return;
-    }
-    const uint32_t prefix = wave_sum(base) + local;
+    bool ok;
+    const uint32_t prefix = chunk_lookback(g.flags, g.nparts, p, agg, epoch30, g.ctrl, ok);
+    if (!ok) return;                  // a predecessor never published: write nothing more
     raw* dst = reinterpret_cast<raw*>(g.out + oA) + prefix;
     if (flushed != 0) {
         __threadfence_block();        // this wave's parked values are read back below
@@ -3195,35 +3121,38 @@ inline uint32_t stream_grid(uint64_t work_items, uint32_t per_block, uint32_t ca
     return (uint32_t)g;
 }
 
-// Pici (+) Pici -> Pici in two passes: below this many partitions the first
-// pass takes one tile per wave (k_pp_tile, four times the waves: 12.7 against
-// 20.1 us at 2^20 fp32 elements, sigma 0.99, 20.9 against 39.5 at 0.9, 32.8
-// against 46.1 at 2^24 and 0.9), from it one partition per wave (k_pp_part,
-// four tiles' values per LDS flush: 28.2 against 36.3 us at 2^26 and sigma
-// 0.99, 75.0 against 80.4 at 0.9; at 2^25 they are level).
+// Which kernels write a Pici output, by its size in partitions of 16384
+// elements (fp32 times at 2^k elements, isolated medians after a 512 MiB
+// write, sigma 0.99 / 0.9; "one" = one launch finding its offsets by the
+// two-level look-back, "two" = count pass + k_place):
+//  - dense sources (k_to_pici): one launch at every size in fp32 (2^25:
+//    compression 31.9 / 33.8 against 35.1 / 42.3 us, dense (+) Pici 34.9 /
+//    44.0 against 38.3 / 54.9; 2^26: 57.7 / 60.7 against 58.5 / 77.3 and
+//    61.1 / 78.6 against 66.7 / 98.1; 2^27: 107 / 113 against 110 / 147);
+//    in bf16 up to 2048 partitions (2^25 elements: 21.4 / 23.4 against 23.1 /
+//    29.1), since from 4096 the one launch loses at 0.99 (2^27: 68.2 against
+//    59.1 us; at 0.9 it still wins, 74.5 against 76.4).
+//  - Pici (+) Pici: one launch of the per-tile kernel up to 1024 partitions
+//    (2^24: 14.8 / 29.2 against 15.5 / 31.7 us), then its two-pass form
+//    (k_pp_tile<E, true> + k_place, four waves per partition: 12.7 against
+//    20.1 us at 2^20 and 0.99 against one partition per wave), from 2048
+//    partitions one partition per wave (k_pp_part: 28.2 against 36.3 us at
+//    2^26), which finds its own offsets up to 4096 partitions -- every wave
+//    of the launch is then resident, so a waiting wave keeps none from
+//    starting (26.6 against 28.2 / 66.2 against 75.2 us at 2^26; at 2^27 bf16,
+//    two rounds of waves, 45.9 against 41.5) -- and takes k_place beyond.
+// Without value slots (a minimal workspace) every output takes one launch.
+constexpr uint32_t kOneLaunchMaxPartsBF16 = 2048;
+constexpr uint32_t kPPTileOneMaxParts = 1024;
 constexpr uint32_t kPPTileMaxParts = 2048;
-// Up to this many partitions (one wave each: the waves the device holds at
-// once at k_pp_part's register use, 4 per SIMD) Pici (+) Pici -> Pici is one
-// launch of k_pp_part<E, true>: a wave that waits for its predecessors'
-// counts keeps no other wave from starting.  Measured at 2^26 fp32 against
-// k_pp_part + k_place: 26.6 against 28.2 us at sigma 0.99, 66.2 against 75.2
-// at 0.9; at 2^27 bf16 (8192 partitions, two rounds of waves) 45.9 against
-// 41.5 at 0.99, so larger outputs keep the two passes.
 constexpr uint32_t kPPSingleMaxParts = 4096;
 
 }  // namespace
 
-// A Pici output of at most this many partitions is written in a single pass
-// (look-back) even when the workspace has the value slots: on small arrays
-// the second launch costs more than the look-back. Measured in fp32 at sigma
-// 0.99 (0.9), single against two passes: compression at 2^20 elements 9.6
-// against 12.2 us (10.4 against 15.6), at 2^24 = 1024 partitions 21.8 against
-// 22.5 (23.0 against 27.3), at 2^25 40.7 against 34.7 (level); dense (+) Pici
-// -> Pici the same within 1 us. Pici (+) Pici -> Pici, whose two-pass first
-// launch is lighter, takes half the limit: 14.9 against 14.8 us at 2^23 (23.5
-// against 25.9), 18.4 against 16.5 at 2^24 (35.0 against 31.9).
-// spccl_set_single_pass_limit changes it.
-std::atomic<uint32_t> g_single_pass_max_parts{1024};
+// An upper bound on the sizes above (in partitions) for calls whose
+// workspace has the value slots; set by spccl_set_single_pass_limit.  0
+// keeps every such call on two passes.
+std::atomic<uint32_t> g_single_pass_max_parts{0xFFFFFFFFu};
 
 uint32_t set_single_pass_max_parts(uint32_t parts) { return g_single_pass_max_parts.exchange(parts); }
 
@@ -3232,15 +3161,18 @@ namespace {
 template <class E>
 spccl_status_t launch_to_pici(int sa, int sb, const PiciSinkArgs& g, hipStream_t st) {
     dim3 grid(g.nparts), block(kBlockThreads);
-    const uint64_t limit = g_single_pass_max_parts.load(std::memory_order_relaxed);
-    const bool two_pass = g.slots && g.nparts > limit;
+    const uint32_t bound = g_single_pass_max_parts.load(std::memory_order_relaxed);
+    const auto one_launch = [&](uint32_t max_parts) {
+        return !g.slots || g.nparts <= (max_parts < bound ? max_parts : bound);
+    };
+    const bool two_pass = !one_launch(sizeof(typename E::raw) == 4 ? 0xFFFFFFFFu : kOneLaunchMaxPartsBF16);
     if (sa == SRC_PICI && sb == SRC_PICI) {
-        if (g.slots && 2ull * g.nparts > limit) {
+        if (!one_launch(kPPTileOneMaxParts)) {
             if (g.nparts < kPPTileMaxParts) {
                 hipLaunchKernelGGL((k_pp_tile<E, true>), grid, block, 0, st, g);
             } else {
                 dim3 wgrid((g.nparts + kWavesPerBlock - 1) / kWavesPerBlock);
-                if (g.nparts <= kPPSingleMaxParts) {
+                if (one_launch(kPPSingleMaxParts)) {
                     hipLaunchKernelGGL((k_pp_part<E, true>), wgrid, block, 0, st, g);
                     return launch_status();
                 }

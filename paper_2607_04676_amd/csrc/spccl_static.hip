@@ -1,8 +1,9 @@
 // spccl_compress_static: compression for callers that cannot allocate.
 //
 // It runs the single-pass compression kernels (decoupled look-back over
-// 16384-element partitions, so the only scratch is a status word and one
-// look-back word per partition) with that scratch in a file-scope device
+// 16384-element partitions, so the only scratch is a status word, one
+// look-back word per partition and one per 256 partitions) with that scratch
+// in a file-scope device
 // array instead of a caller workspace.  Every GPU the library runs on holds
 // its own copy of the array, at its own address, until the process ends.  In
 // host code the array's name is not a device address, so the address of each
@@ -28,7 +29,9 @@ namespace {
 
 constexpr uint64_t kStaticMaxParts = SPCCL_STATIC_MAX_ELEMS / kPartElems;
 static_assert(SPCCL_STATIC_MAX_ELEMS % kPartElems == 0, "the maximum is a whole number of partitions");
-constexpr uint64_t kStaticScratchBytes = kWsFlagsOffset + 8 * kStaticMaxParts;
+// a look-back word per partition and one per kPlaceChunk partitions (the chunk sums)
+constexpr uint64_t kStaticFlagWords = kStaticMaxParts + (kStaticMaxParts + kPlaceChunk - 1) / kPlaceChunk;
+constexpr uint64_t kStaticScratchBytes = kWsFlagsOffset + 8 * kStaticFlagWords;
 
 static __device__ __align__(256) uint8_t scratch[kStaticScratchBytes];
 

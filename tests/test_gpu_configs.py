@@ -73,7 +73,7 @@ def test_config1(S):
 
 
 @pytest.mark.parametrize("permille", W.CFG2_PERMILLE)
-@pytest.mark.parametrize("minimal", [False, True], ids=["two_pass", "single_pass"])
+@pytest.mark.parametrize("minimal", [False, True], ids=["full_workspace", "minimal_workspace"])
 def test_config2_codec_and_reduce(S, permille, minimal):
     n = W.CFG2_N
     log(f"cfg2 sigma={permille / 1000} generate (minimal workspace: {minimal})")

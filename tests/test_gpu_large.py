@@ -30,8 +30,9 @@ N_BIG = (1 << 28) + 4097          # 65,538 tiles: 16,385 partitions of 16,384 el
 def test_message_above_2_28_elements(S):
     """compress, dense (+) Pici -> Pici (the reduce-scatter step) and
     Pici (+) Pici -> Pici of 268,439,553 fp32 elements at sparsity 0.99 with
-    the default (full) workspace: the global offsets of a message of more
-    than 16384 partitions, against the oracle byte for byte."""
+    the full workspace, each in the library's default form (one launch for
+    the dense sources) and in two passes: the global offsets of a message of
+    more than 16384 partitions, against the oracle byte for byte."""
     n = N_BIG
     assert O.num_tiles(n) == 65538 and -(-O.num_tiles(n) // 4) == 16385
     log(f"large message: generating n={n}")
@@ -42,34 +43,45 @@ def test_message_above_2_28_elements(S):
     ws = S.alloc_workspace(n, O.F32)
     out = S.alloc_stream(n, O.F32)
     ta = to_dev(a)
-    log(f"large message: compress n={n} nnz={nnz_a}")
-    out.fill_(0xA5)
-    S.spccl_compress(ta, out, ws)
-    torch.cuda.synchronize()
-    assert S.spccl_read_status(ws) == 0
-    assert_bytes_equal(out[:exp_a.size].cpu().numpy(), exp_a, "compress above 2^28")
-    assert S.spccl_read_header(out)["total_bytes"] == exp_a.size
+    forms = (("default", 0xFFFFFFFF), ("two passes", 0))
+    prev = S.spccl_set_single_pass_limit(0xFFFFFFFF)
+    try:
+        for form, bound in forms:
+            S.spccl_set_single_pass_limit(bound)
+            log(f"large message: compress n={n} nnz={nnz_a} ({form})")
+            out.fill_(0xA5)
+            S.spccl_compress(ta, out, ws)
+            torch.cuda.synchronize()
+            assert S.spccl_read_status(ws) == 0
+            assert_bytes_equal(out[:exp_a.size].cpu().numpy(), exp_a, f"compress above 2^28 ({form})")
+            assert S.spccl_read_header(out)["total_bytes"] == exp_a.size
 
-    mb = S.alloc_stream(n, O.F32)
-    mb[:exp_b.size].copy_(torch.from_numpy(exp_b))
-    pici = lambda t: S.operand(t, S.SPCCL_STREAM, S.SPCCL_FMT_PICI)
-    log("large message: dense (+) Pici -> Pici")
-    exp_r, _ = O.reduce(O.Operand.array(a), O.Operand.stream(exp_b), n, O.F32, O.STREAM, O.FMT_PICI)
-    red = S.alloc_stream(n, O.F32)
-    red.fill_(0x5A)
-    S.spccl_reduce(S.operand(ta), pici(mb), pici(red), n, O.F32, ws)
-    torch.cuda.synchronize()
-    assert S.spccl_read_status(ws) == 0
-    assert_bytes_equal(red[:exp_r.size].cpu().numpy(), exp_r, "dense (+) Pici above 2^28")
+        mb = S.alloc_stream(n, O.F32)
+        mb[:exp_b.size].copy_(torch.from_numpy(exp_b))
+        pici = lambda t: S.operand(t, S.SPCCL_STREAM, S.SPCCL_FMT_PICI)
+        exp_r, _ = O.reduce(O.Operand.array(a), O.Operand.stream(exp_b), n, O.F32, O.STREAM, O.FMT_PICI)
+        red = S.alloc_stream(n, O.F32)
+        for form, bound in forms:
+            S.spccl_set_single_pass_limit(bound)
+            log(f"large message: dense (+) Pici -> Pici ({form})")
+            red.fill_(0x5A)
+            S.spccl_reduce(S.operand(ta), pici(mb), pici(red), n, O.F32, ws)
+            torch.cuda.synchronize()
+            assert S.spccl_read_status(ws) == 0
+            assert_bytes_equal(red[:exp_r.size].cpu().numpy(), exp_r, f"dense (+) Pici above 2^28 ({form})")
 
-    log("large message: Pici (+) Pici -> Pici")
-    del ta
-    exp_pp, _ = O.reduce(O.Operand.stream(exp_a), O.Operand.stream(exp_b), n, O.F32, O.STREAM, O.FMT_PICI)
-    red.fill_(0x3C)
-    S.spccl_reduce(pici(out), pici(mb), pici(red), n, O.F32, ws)
-    torch.cuda.synchronize()
-    assert S.spccl_read_status(ws) == 0
-    assert_bytes_equal(red[:exp_pp.size].cpu().numpy(), exp_pp, "Pici (+) Pici above 2^28")
+        del ta
+        exp_pp, _ = O.reduce(O.Operand.stream(exp_a), O.Operand.stream(exp_b), n, O.F32, O.STREAM, O.FMT_PICI)
+        for form, bound in forms:
+            S.spccl_set_single_pass_limit(bound)
+            log(f"large message: Pici (+) Pici -> Pici ({form})")
+            red.fill_(0x3C)
+            S.spccl_reduce(pici(out), pici(mb), pici(red), n, O.F32, ws)
+            torch.cuda.synchronize()
+            assert S.spccl_read_status(ws) == 0
+            assert_bytes_equal(red[:exp_pp.size].cpu().numpy(), exp_pp, f"Pici (+) Pici above 2^28 ({form})")
+    finally:
+        S.spccl_set_single_pass_limit(prev)
 
 
 def _part(S, x, kind, keep):

@@ -8,9 +8,9 @@ for the largest message (so each call meets the previous call's chunk sums),
 against the oracle byte for byte.  Also either side of the sizes where
 Pici (+) Pici's first pass changes its shape (2048 partitions) and up to
 which it finds its offsets itself in one launch (4096).  The library writes
-outputs of at most 1,024 partitions in a single pass by default; these tests
-lower that limit to zero so the other paths run at every size, and a second
-test checks the default on both sides of the limit on the same workspace."""
+many outputs in one launch by default; these tests bound that to zero
+partitions so the two-pass paths run at every size, and a second test checks
+the defaults on both sides of their limits on the same workspace."""
 import numpy as np
 import pytest
 
@@ -67,15 +67,17 @@ def test_place_across_chunks(S, ws_big, two_pass_always, dtype, size, permille):
     check_sinks(S, ws_big, dtype, size, permille)
 
 
-# the default single-pass limit (1,024 partitions) and one partition past it,
-# plus a small message, all on the large workspace
-DEFAULT = [(1, -(PART - 100)), (CHUNK + 1, -(PART - 1)), (1024, -5), (1025, -(PART - 1))]
+# the library's own one-launch limits on the large workspace: bf16 dense-source
+# outputs up to 2048 partitions, Pici (+) Pici up to 1024 and from 2048 to 4096
+# partitions (fp32 dense-source outputs take one launch at every size)
+DEFAULT = [(W.F32, (1, -(PART - 100))), (W.F32, (1024, -5)), (W.F32, (1025, -(PART - 1))),
+           (W.BF16, (2048, -3)), (W.BF16, (2049, -(PART - 1)))]
 
 
-@pytest.mark.parametrize("size", DEFAULT)
-def test_default_single_pass_limit(S, ws_big, size):
-    assert S.spccl_set_single_pass_limit(1024) == 1024
-    check_sinks(S, ws_big, W.F32, size, 990)
+@pytest.mark.parametrize("dtype,size", DEFAULT)
+def test_default_single_pass_limit(S, ws_big, dtype, size):
+    assert S.spccl_set_single_pass_limit(0xFFFFFFFF) == 0xFFFFFFFF
+    check_sinks(S, ws_big, dtype, size, 990)
 
 
 def check_sinks(S, ws_big, dtype, size, permille):
