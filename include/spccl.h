@@ -150,9 +150,9 @@ spccl_status_t spccl_workspace_init(void* ws, uint64_t ws_bytes, void* stream);
  * every size, bf16 ones up to 2048 partitions, Pici (+) Pici -> Pici up to
  * 1024 partitions and from 2048 to 4096 (a kernel with one partition per
  * wave).  Default UINT32_MAX (the library's limits alone); 0 keeps every such
- * call on two passes.  COO outputs, and the ring steps that the collectives
- * batch over all ranks in one launch, always take two passes; a workspace of
- * only spccl_workspace_min_bytes always one.  Process-wide (every device and
+ * call on two passes.  The ring steps of the spccl_vr_* collectives follow the
+ * same limits per rank's message; COO outputs always take two passes, and a
+ * workspace of only spccl_workspace_min_bytes always one.  Process-wide (every device and
  * thread), takes effect for later calls; outputs are identical either way.
  * Returns the previous bound. */
 uint32_t spccl_set_single_pass_limit(uint32_t max_partitions);

@@ -1364,11 +1364,14 @@ __global__ void __launch_bounds__(kBlockThreads, sink_waves(SB, Deferred)) k_to_
     to_pici_body<E, SA, SB, Deferred>(g);
 }
 
-// The count pass of one ring step for a batch of ranks (grid y).
-template <class E, int SA, int SB>
-__global__ void __launch_bounds__(kBlockThreads, sink_waves(SB, true)) k_to_pici_rb(PiciSinkArgs g, RankBatch rb) {
+// One ring step's Pici outputs for a batch of ranks (grid y), in one launch
+// or as the count pass.  Work-groups start in order of the flattened block
+// index, so a rank's blocks start after those of lower ranks, and a block
+// waits only for lower partitions of its own rank.
+template <class E, int SA, int SB, bool Deferred>
+__global__ void __launch_bounds__(kBlockThreads, sink_waves(SB, Deferred)) k_to_pici_rb(PiciSinkArgs g, RankBatch rb) {
     if (rank_skipped(rb, blockIdx.y)) return;
-    to_pici_body<E, SA, SB, true>(rank_sink(g, rb, blockIdx.y));
+    to_pici_body<E, SA, SB, Deferred>(rank_sink(g, rb, blockIdx.y));
 }
 
 
@@ -3356,17 +3359,30 @@ spccl_status_t launch_copy_sliced_batch(const SlicedBatch& b, uint32_t ranks, hi
 // Grid-stride kernels give each rank a share of about 4096 blocks.
 inline uint32_t per_rank_cap(uint32_t ranks) { return ranks >= 64 ? 64u : 4096u / ranks; }
 
+template <class E, bool Deferred>
+spccl_status_t launch_to_pici_rb_k(int sa, int sb, const PiciSinkArgs& g, const RankBatch& rb, uint32_t ranks,
+                                   hipStream_t st) {
+    const dim3 grid(g.nparts, ranks), block(kBlockThreads);
+#define SPCCL_TO_PICI_RB(A, B) hipLaunchKernelGGL((k_to_pici_rb<E, A, B, Deferred>), grid, block, 0, st, g, rb)
+    if (sa == SRC_DENSE && sb == SRC_NONE) SPCCL_TO_PICI_RB(SRC_DENSE, SRC_NONE);
+    else if (sa == SRC_PICI && sb == SRC_DENSE) SPCCL_TO_PICI_RB(SRC_PICI, SRC_DENSE);
+    else if (sa == SRC_DENSE && sb == SRC_DENSE) SPCCL_TO_PICI_RB(SRC_DENSE, SRC_DENSE);
+    else return SPCCL_ERR_UNSUPPORTED;
+#undef SPCCL_TO_PICI_RB
+    return launch_status();
+}
+
+// The same choice as launch_to_pici, per rank's message.
 template <class E>
 spccl_status_t launch_to_pici_rb(int sa, int sb, const PiciSinkArgs& g, const RankBatch& rb, uint32_t ranks,
                                  hipStream_t st) {
-    const dim3 grid(g.nparts, ranks), block(kBlockThreads);
-    if (sa == SRC_DENSE && sb == SRC_NONE) hipLaunchKernelGGL((k_to_pici_rb<E, SRC_DENSE, SRC_NONE>), grid, block, 0, st, g, rb);
-    else if (sa == SRC_PICI && sb == SRC_DENSE) hipLaunchKernelGGL((k_to_pici_rb<E, SRC_PICI, SRC_DENSE>), grid, block, 0, st, g, rb);
-    else if (sa == SRC_DENSE && sb == SRC_DENSE) hipLaunchKernelGGL((k_to_pici_rb<E, SRC_DENSE, SRC_DENSE>), grid, block, 0, st, g, rb);
-    else return SPCCL_ERR_UNSUPPORTED;
-    spccl_status_t s1 = launch_status();
+    const uint32_t bound = g_single_pass_max_parts.load(std::memory_order_relaxed);
+    const uint32_t own = sizeof(typename E::raw) == 4 ? 0xFFFFFFFFu : kOneLaunchMaxPartsBF16;
+    if (g.nparts <= (own < bound ? own : bound)) return launch_to_pici_rb_k<E, false>(sa, sb, g, rb, ranks, st);
+    spccl_status_t s1 = launch_to_pici_rb_k<E, true>(sa, sb, g, rb, ranks, st);
     if (s1 != SPCCL_OK) return s1;
-    hipLaunchKernelGGL(k_place_rb<E>, dim3((g.nparts + kPlacePer - 1) / kPlacePer, ranks), block, 0, st, g, rb);
+    hipLaunchKernelGGL(k_place_rb<E>, dim3((g.nparts + kPlacePer - 1) / kPlacePer, ranks), dim3(kBlockThreads), 0, st,
+                       g, rb);
     return launch_status();
 }
 

@@ -268,6 +268,13 @@ def rs_time_us(P: int, m: int, s: int, sigma0: float, pol: Policy, km: KernelMod
     return total
 
 
+def pici_sink_launches(m: int, s: int) -> int:
+    """Launches of one batched Pici-producing ring step: one (offsets found in
+    the same launch) for fp32 messages and bf16 ones of up to 2048 partitions
+    of 16384 elements, else a count and a place pass."""
+    return 1 if s == 4 or -(-m // 16384) <= 2048 else 2
+
+
 def vr_rs_time_us(P: int, m: int, s: int, sigma0: float, pol: Policy, km: KernelModel, launch_us: float) -> dict:
     """The same reduce-scatter on one GPU with P virtual ranks and free
     links, as the library runs it: every kernel of a ring step is one
@@ -275,9 +282,9 @@ def vr_rs_time_us(P: int, m: int, s: int, sigma0: float, pol: Policy, km: Kernel
     between launches, so a step costs the sum over ranks of its algorithmic
     bytes at the op's bandwidth plus launch_us per launch.  Launches per
     step: a decide and a copy of the received messages, then for each input
-    format that can occur a count and a place pass (a Pici send) and a dense
-    sink (a dense send, or the last step's output); step 0 compresses (count
-    and place), decides and, if the policy allows dense sends, encodes them.
+    format that can occur a Pici sink (a Pici send: pici_sink_launches) and a
+    dense sink (a dense send, or the last step's output); step 0 compresses
+    (a Pici sink), decides and, if the policy allows dense sends, encodes them.
     Returns the total and its two terms (us) and the launch count."""
     if P == 1:
         return {"total_us": 0.0, "bytes_us": 0.0, "launch_us": 0.0, "launches": 0}
@@ -286,7 +293,8 @@ def vr_rs_time_us(P: int, m: int, s: int, sigma0: float, pol: Policy, km: Kernel
     fmts, _, true, _, _ = replay_rs(P, sigma0, pol)
     dense_chunk = m * s
     bytes_us = 0.0
-    launches = 3 + (1 if can_dense else 0)
+    sink = pici_sink_launches(m, s)
+    launches = sink + 1 + (1 if can_dense else 0)
     for r in range(P):
         bytes_us += (dense_chunk + message_bytes(m, s, pol.sparse_fmt, sigma0)) / bw("compress", sigma0)
         if fmts[0][r] == FMT_DENSE:
@@ -296,7 +304,7 @@ def vr_rs_time_us(P: int, m: int, s: int, sigma0: float, pol: Policy, km: Kernel
         launches += 2
         for fin_ok in (can_sparse, can_dense):
             if fin_ok:
-                launches += (2 if (not last and can_sparse) else 0) + (1 if (last or can_dense) else 0)
+                launches += (sink if (not last and can_sparse) else 0) + (1 if (last or can_dense) else 0)
         sig_in, sig_out = true[step - 1], sigma0 ** (step + 1)
         for r in range(P):
             fin = fmts[step - 1][(r - 1) % P]

@@ -21,6 +21,20 @@ def S():
     return S
 
 
+@pytest.fixture(params=["one_launch", "two_passes"])
+def passes(request, S):
+    """The ring steps' Pici outputs in the library's default form (one launch
+    with the two-level look-back) or forced onto the count and place passes."""
+    if request.param == "one_launch":
+        yield request.param
+        return
+    prev = S.spccl_set_single_pass_limit(0)
+    try:
+        yield request.param
+    finally:
+        S.spccl_set_single_pass_limit(prev)
+
+
 def tdt(x):
     return torch.bfloat16 if x.dtype == np.uint16 else torch.float32
 
@@ -67,11 +81,11 @@ POLICIES = {
 @pytest.mark.parametrize("dtype", [W.F32, W.BF16])
 @pytest.mark.parametrize("P", [1, 2, 3, 8])
 @pytest.mark.parametrize("pol", list(POLICIES))
-def test_reduce_scatter_matches_oracle(S, dtype, P, pol):
+def test_reduce_scatter_matches_oracle(S, dtype, P, pol, passes):
     m = 2 * 4096 + 123
     frac = [0.3, 0.02, 0.15][P % 3]
     sends = [W.sparse_array(P * m, int(frac * P * m), [40, P, r], dtype) for r in range(P)]
-    log(f"rs P={P} dtype={dtype} policy={pol}")
+    log(f"rs P={P} dtype={dtype} policy={pol} {passes}")
     got, gtr = run_rs(S, sends, POLICIES[pol])
     exp, otr = O.ring_reduce_scatter(sends, POLICIES[pol])
     for r in range(P):
@@ -95,11 +109,11 @@ def test_reduce_scatter_decision_trace_hand_computed(S):
 
 @pytest.mark.parametrize("dtype", [W.F32, W.BF16])
 @pytest.mark.parametrize("P", [1, 2, 5])
-def test_all_gather_matches_oracle(S, dtype, P):
+def test_all_gather_matches_oracle(S, dtype, P, passes):
     n = 3 * 4096 + 11
     parts = [W.sparse_array(n, (r + 1) * n // 40, [41, P, r], dtype) for r in range(P)]
     dt = O.dtype_code(parts[0])
-    log(f"ag P={P} dtype={dtype}")
+    log(f"ag P={P} dtype={dtype} {passes}")
     ts = [to_dev(x) for x in parts]
     outs = [torch.empty(P * n, dtype=tdt(parts[0]), device="cuda") for _ in range(P)]
     scratch = torch.empty(S.spccl_vr_scratch_bytes(P, n, dt), dtype=torch.uint8, device="cuda")
@@ -114,10 +128,10 @@ def test_all_gather_matches_oracle(S, dtype, P):
 @pytest.mark.parametrize("dtype", [W.F32, W.BF16])
 @pytest.mark.parametrize("P", [1, 4, 8])
 @pytest.mark.parametrize("pol", ["default", "never_dense", "always_dense"])
-def test_all_reduce_matches_oracle(S, dtype, P, pol):
+def test_all_reduce_matches_oracle(S, dtype, P, pol, passes):
     m = 4096 + 77
     sends = [W.sparse_array(P * m, P * m // 6, [42, P, r], dtype) for r in range(P)]
-    log(f"ar P={P} dtype={dtype} policy={pol}")
+    log(f"ar P={P} dtype={dtype} policy={pol} {passes}")
     got, gtr = run_ar(S, sends, POLICIES[pol])
     exp, otr = O.ring_all_reduce(sends, POLICIES[pol])
     for r in range(P):

@@ -86,14 +86,17 @@ def test_recommend_is_a_grid_point_and_reports_the_paper_pair():
         assert w["best_us"] <= w["paper_us"] and w["best_us"] <= w["dense_us"] + 1e-9
 
 
-@pytest.mark.parametrize("adaptive,launches", [(1, 56), (0, 30), (2, 25)])
-def test_one_gpu_ring_launches_follow_the_policy(adaptive, launches):
+@pytest.mark.parametrize("s,m,adaptive,launches", [(4, 1 << 16, 1, 43), (4, 1 << 16, 0, 23), (4, 1 << 16, 2, 24),
+                                                     (2, 1 << 16, 1, 43), (2, 2049 * 16384, 1, 56),
+                                                     (2, 2049 * 16384, 0, 30), (2, 2049 * 16384, 2, 25)])
+def test_one_gpu_ring_launches_follow_the_policy(s, m, adaptive, launches):
     """The one-GPU ring issues, per step, a decide and a copy, then for each
-    input format the policy allows a count and a place pass (a sparse send)
-    and a dense sink (a dense send or the last step); step 0 compresses,
-    decides and, if dense sends are allowed, encodes them."""
+    input format the policy allows a Pici sink (a sparse send: one launch, or
+    a count and a place pass for bf16 messages above 2048 partitions) and a
+    dense sink (a dense send or the last step); step 0 compresses, decides
+    and, if dense sends are allowed, encodes them."""
     km = T.KernelModel.constant(4000.0)
-    got = T.vr_rs_time_us(8, 1 << 16, 4, 0.99, T.Policy(adaptive=adaptive), km, 3.0)
+    got = T.vr_rs_time_us(8, m, s, 0.99, T.Policy(adaptive=adaptive), km, 3.0)
     assert got["launches"] == launches
     assert got["launch_us"] == pytest.approx(3.0 * launches)
 
