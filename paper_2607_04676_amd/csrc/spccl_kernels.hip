@@ -23,6 +23,7 @@
 // reduction adds in fp32 (bf16 operands widened exactly, the sum rounded once
 // to bf16, nearest-even); an absent operand is the identity.
 #include <hip/hip_runtime.h>
+#include <hip/hip_bf16.h>
 #include <atomic>
 #include <stdint.h>
 
@@ -59,9 +60,13 @@ __device__ __forceinline__ uint32_t oplus(F32, uint32_t a, uint32_t b) {
     s = (a == 0u) ? b : s;
     return (b == 0u) ? a : s;
 }
+// bf16: the fp32 sum (exact enough: fp32 keeps at least 2 * 8 + 2 significant
+// bits, so rounding it again to bf16 gives the correctly rounded bf16 sum)
+// rounded to nearest even by the hardware conversion (v_cvt_pk_bf16_f32; fp32
+// subnormals are kept, so bf16 subnormals round the same way).
 __device__ __forceinline__ uint32_t oplus(BF16, uint32_t a, uint32_t b) {
-    uint32_t u = __float_as_uint(__uint_as_float(a << 16) + __uint_as_float(b << 16));
-    uint32_t s = (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;     // nearest-even to bf16
+    const float f = __uint_as_float(a << 16) + __uint_as_float(b << 16);
+    uint32_t s = (uint32_t)__bfloat16_as_ushort(__float2bfloat16(f));
     s = (a == 0u) ? b : s;
     return (b == 0u) ? a : s;
 }

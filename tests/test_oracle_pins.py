@@ -467,3 +467,34 @@ def test_validate_rejects_corruption():
     assert O.validate(bad, n, O.F32) == O.ERR_CORRUPT_STREAM
     with pytest.raises(O.OracleError):
         O.decompress(bad, n, O.F32)
+
+
+# bf16 sums whose correctly rounded results were worked out by hand from the
+# bit patterns (8 significant bits; subnormal spacing 2^-133; overflow to
+# infinity), each a case a plausible rounding mistake gets wrong
+BF16_SUMS = [
+    (0x3F80, 0x3B80, 0x3F80),   # 1 + 2^-8, halfway: to even, 1
+    (0x3F81, 0x3B80, 0x3F82),   # (1 + 2^-7) + 2^-8, halfway: to even, 1 + 2^-6
+    (0xBF80, 0xBB80, 0xBF80),   # the negative tie
+    (0x4380, 0x3F80, 0x4380),   # 256 + 1, halfway: 256
+    (0x4381, 0x3F80, 0x4382),   # 258 + 1, halfway: 260
+    (0x4B80, 0x3F80, 0x4B80),   # 2^24 + 1: 2^24
+    (0x0001, 0x0001, 0x0002),   # subnormals add exactly
+    (0x007F, 0x0001, 0x0080),   # into the smallest normal
+    (0x0080, 0x8001, 0x007F),   # back into the subnormals
+    (0x0001, 0x8001, 0x0000),   # exact cancellation: absent
+    (0x7F7F, 0x7F7F, 0x7F80),   # overflow: +inf
+    (0x7F7F, 0x7B00, 0x7F80),   # largest + half its unit, halfway: to even, +inf
+    (0x7F7F, 0x7A80, 0x7F7F),   # largest + a quarter unit: unchanged
+    (0xFF7F, 0xFB00, 0xFF80),   # -inf
+    (0x8000, 0x8000, 0x8000),   # -0 + -0 = -0
+    (0x8000, 0x3F80, 0x3F80),   # -0 + 1 = 1
+    (0x8000, 0x0000, 0x8000),   # absent operand: -0 kept
+    (0x0000, 0x8000, 0x8000),
+]
+
+
+@pytest.mark.parametrize("a,b,want", BF16_SUMS)
+def test_oracle_bf16_sum_hand_values(a, b, want):
+    assert O.oplus(a, b, O.BF16) == want
+    assert O.oplus(b, a, O.BF16) == want
