@@ -173,9 +173,9 @@ uint64_t spccl_message_bound(uint64_t n, int32_t dtype, int32_t fmt);
 /* Compress dense[0..n) into a Pici message at `out` (capacity out_bytes >=
  * spccl_stream_bound(n, dtype)): bit vector B, tile prefix sums I and
  * compacted values A, ordered tile -> column -> row.  The input is read
- * once; partition offsets come from a count pass and a place pass (full
- * workspace) or from decoupled look-back (minimal workspace).  nnz is in the
- * written header. */
+ * once; partition offsets are found in the same launch (each partition adds
+ * up its predecessors' counts in two levels) or by a count and a place pass
+ * (see spccl_set_single_pass_limit).  nnz is in the written header. */
 spccl_status_t spccl_compress(const void* dense, uint64_t n, int32_t dtype,
                               void* out, uint64_t out_bytes,
                               void* ws, uint64_t ws_bytes, void* stream);
@@ -312,7 +312,7 @@ spccl_status_t spccl_reduce_sliced_tracked(const void* a, const void* b, uint64_
 /* ---- compression without a caller workspace --------------------------------
  * For callers that cannot allocate device memory (code under HIP graph
  * capture, tight serving loops, harnesses that forbid hipMalloc): the same
- * message as spccl_compress, made by the single-pass kernels, whose scratch
+ * message as spccl_compress, made by the one-launch kernels, whose scratch
  * (a status word, one look-back word per 16384-element partition and one per
  * 256 partitions) lives in a static device array of the library -- 128.5 KiB
  * plus a 256-byte control block, one copy per GPU, held until the process

@@ -442,7 +442,7 @@ def alloc_stream(n: int, dtype: int, device="cuda", fmt: int = SPCCL_FMT_PICI) -
 
 def alloc_workspace(n: int, dtype: int, device="cuda", stream=None, minimal: bool = False) -> torch.Tensor:
     """A zeroed workspace for messages of up to n elements.  minimal=True
-    sizes it for the single-pass kernels only (no per-partition slots)."""
+    sizes it for the one-launch kernels only (no per-partition slots)."""
     need = spccl_workspace_min_bytes(n, dtype) if minimal else spccl_workspace_bytes(n, dtype)
     ws = torch.empty(max(need, 256), dtype=torch.uint8, device=device)
     spccl_workspace_init(ws, stream)

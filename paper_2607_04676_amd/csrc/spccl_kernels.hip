@@ -11,12 +11,14 @@
 // 32-lane warps give each thread two columns, Alg. 1; that split is not
 // needed here.)
 //
-// Single pass.  Compression and the Pici-producing reductions read their
-// input once: each block (four waves, four tiles = one look-back partition)
-// builds B, counts, publishes its aggregate,
-// resolves its global offset by decoupled look-back over earlier partitions
-// (Merrill & Garland, "Single-pass Parallel Prefix Scan with Decoupled
-// Look-back", 2016), and writes I and A.  Values are compacted through an
+// One pass over the input.  Compression and the Pici-producing reductions
+// read their input once: each block (four waves, four tiles = one
+// partition) builds B, counts, publishes its aggregate, and either finds its
+// global offset in the same launch -- from the aggregates of the partitions
+// before it in its chunk of 256 and the sums of the earlier chunks, a
+// two-level form of the look-back of Merrill & Garland, "Single-pass Parallel
+// Prefix Scan with Decoupled Look-back", 2016 -- and writes I and A, or parks
+// its values for a second (place) pass.  Values are compacted through an
 // 8 KiB per-wave LDS stage and written out contiguously.
 //
 // Numerics.  Elements are raw bit patterns; "present" = nonzero bits.  The
@@ -1123,7 +1125,7 @@ __device__ __forceinline__ bool load_tile_pair(const DevOperand& a, const DevOpe
 }
 
 // ---------------------------------------------------------------------------
-// decoupled look-back
+// look-back words and the two-level offset search
 
 constexpr uint32_t kFlagAggregate = 1, kFlagPrefix = 2;
 constexpr uint32_t kSpinLimit = 1u << 20;
@@ -1210,10 +1212,10 @@ __device__ uint32_t chunk_lookback(uint64_t* flags, uint32_t nparts, uint32_t p,
 }
 
 // ---------------------------------------------------------------------------
-// Pici sink: out = Pici(srcA (+) srcB), single pass.
+// Pici sink: out = Pici(srcA (+) srcB).
 
-// Deferred = false: single pass; each partition resolves its global offset by
-// decoupled look-back and writes its values in place.
+// Deferred = false: one launch; each partition finds its global offset with
+// chunk_lookback and writes its values in place.
 // Deferred = true: first of two passes; each partition publishes its
 // aggregate, writes B and the tile offsets relative to the partition, and
 // parks its compacted values in its own worst-case slot of the workspace,

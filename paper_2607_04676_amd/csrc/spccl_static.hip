@@ -1,10 +1,10 @@
 // spccl_compress_static: compression for callers that cannot allocate.
 //
-// It runs the single-pass compression kernels (decoupled look-back over
-// 16384-element partitions, so the only scratch is a status word, one
-// look-back word per partition and one per 256 partitions) with that scratch
-// in a file-scope device
-// array instead of a caller workspace.  Every GPU the library runs on holds
+// It runs the one-launch compression kernels (each 16384-element partition
+// finds its offset from its predecessors' counts, so the only scratch is a
+// status word, one look-back word per partition and one per 256 partitions)
+// with that scratch in a file-scope device array instead of a caller
+// workspace.  Every GPU the library runs on holds
 // its own copy of the array, at its own address, until the process ends.  In
 // host code the array's name is not a device address, so the address of each
 // device's copy is taken once (hipGetSymbolAddress, with that device current)
