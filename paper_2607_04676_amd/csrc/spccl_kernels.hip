@@ -1141,71 +1141,80 @@ constexpr uint32_t kNoPrefix = 0xFFFFFFFFu;
 
 // Exclusive prefix of partition p in two levels, computed by one whole wave
 // once p has published its own aggregate `agg` (flags[p]): the aggregates of
-// the partitions before p in its chunk of kPlaceChunk (four per lane,
-// reloaded until all carry this call's epoch), then the sums of the earlier
-// chunks (flags[nparts + c]), which each chunk's last partition publishes as
-// soon as it has its chunk's aggregates, before it waits for anything else.
-// A wave waits only for lower-numbered partitions, which publish their
-// aggregates before they wait, and work-groups start in index order, so every
-// wait ends; the spin limit bounds it regardless (ok = false, TIMEOUT set).
+// the partitions before p in its chunk of kPlaceChunk (four per lane) and the
+// sums of the earlier chunks (flags[nparts + c]; the first 64 loaded in the
+// same round trip, one per lane), each reloaded until it carries this call's
+// epoch.  A chunk's last partition publishes its chunk's sum as soon as it has
+// the chunk's aggregates, before it waits for anything else.  A wave waits
+// only for lower-numbered partitions, which publish their aggregates before
+// they wait, and work-groups start in index order, so every wait ends; the
+// spin limit bounds it regardless (ok = false, TIMEOUT set).
 __device__ uint32_t chunk_lookback(uint64_t* flags, uint32_t nparts, uint32_t p, uint32_t agg, uint32_t epoch30,
                                    WsCtrl* ctrl, bool& ok) {
     constexpr int J = (int)(kPlaceChunk / 64);
     const uint32_t l = lane_id();
     const uint32_t chunk = p / kPlaceChunk, first = chunk * kPlaceChunk;
+    const bool last_of_chunk = p % kPlaceChunk == kPlaceChunk - 1 || p == nparts - 1;
     ok = true;
-    uint32_t local = 0;
-    {
-        uint64_t fq[J];
-        bool ready[J];
+    uint64_t fq[J];
+    bool ready[J];
+#pragma unroll
+    for (int j = 0; j < J; j++) {
+        ready[j] = first + l + 64u * j >= p;
+        fq[j] = 0;
+    }
+    uint64_t fk = 0;
+    bool kready = l >= chunk;                        // lane l: the sum of chunk l
+    bool local_done = false;
+    uint32_t local = 0, spins = 0;
+    while (true) {
+        bool all = true;
 #pragma unroll
         for (int j = 0; j < J; j++) {
-            ready[j] = first + l + 64u * j >= p;
-            fq[j] = 0;
-        }
-        uint32_t spins = 0;
-        while (true) {
-            bool all = true;
-#pragma unroll
-            for (int j = 0; j < J; j++) {
-                if (!ready[j]) {
-                    fq[j] = __hip_atomic_load(&flags[first + l + 64u * j], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                    ready[j] = (uint32_t)(fq[j] >> 34) == epoch30;
-                }
-                all = all && ready[j];
+            if (!ready[j]) {
+                fq[j] = __hip_atomic_load(&flags[first + l + 64u * j], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                ready[j] = (uint32_t)(fq[j] >> 34) == epoch30;
             }
-            if (__all(all)) break;
-            if (++spins > kSpinLimit) {
-                ok = false;
-                break;
-            }
-            __builtin_amdgcn_s_sleep(1);
+            all = all && ready[j];
         }
+        if (!kready) {
+            fk = __hip_atomic_load(&flags[nparts + l], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            kready = (uint32_t)(fk >> 34) == epoch30;
+        }
+        if (!local_done && __all(all)) {
+            local_done = true;
 #pragma unroll
-        for (int j = 0; j < J; j++) local += first + l + 64u * j < p ? (uint32_t)fq[j] : 0u;
-        local = wave_sum(local);
+            for (int j = 0; j < J; j++) local += first + l + 64u * j < p ? (uint32_t)fq[j] : 0u;
+            local = wave_sum(local);
+            if (last_of_chunk && l == 0) publish(flags, nparts + chunk, epoch30, kFlagAggregate, local + agg);
+        }
+        if (local_done && __all(kready)) break;
+        if (++spins > kSpinLimit) {
+            ok = false;
+            break;
+        }
+        __builtin_amdgcn_s_sleep(1);
     }
-    const bool last_of_chunk = p % kPlaceChunk == kPlaceChunk - 1 || p == nparts - 1;
-    if (ok && last_of_chunk && l == 0) publish(flags, nparts + chunk, epoch30, kFlagAggregate, local + agg);
-    uint32_t base = 0;
-    for (uint32_t k0 = 0; k0 < chunk && ok; k0 += 64) {
+    uint32_t base = l < chunk ? (uint32_t)fk : 0u;
+    // chunks 64 and beyond (outputs of more than 16384 partitions), 64 per round
+    for (uint32_t k0 = 64; k0 < chunk && ok; k0 += 64) {
         const uint32_t k = k0 + l;
-        uint64_t fk = 0;
-        bool ready = k >= chunk;
-        uint32_t spins = 0;
+        uint64_t fk2 = 0;
+        bool ready2 = k >= chunk;
+        uint32_t spins2 = 0;
         while (true) {
-            if (!ready) {
-                fk = __hip_atomic_load(&flags[nparts + k], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                ready = (uint32_t)(fk >> 34) == epoch30;
+            if (!ready2) {
+                fk2 = __hip_atomic_load(&flags[nparts + k], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                ready2 = (uint32_t)(fk2 >> 34) == epoch30;
             }
-            if (__all(ready)) break;
-            if (++spins > kSpinLimit) {
+            if (__all(ready2)) break;
+            if (++spins2 > kSpinLimit) {
                 ok = false;
                 break;
             }
             __builtin_amdgcn_s_sleep(1);
         }
-        base += k < chunk ? (uint32_t)fk : 0u;
+        base += k < chunk ? (uint32_t)fk2 : 0u;
     }
     if (!ok && l == 0) set_status(ctrl, SPCCL_ERR_TIMEOUT);
     return wave_sum(base) + local;
