@@ -1768,9 +1768,49 @@ __global__ void __launch_bounds__(kBlockThreads) k_pp_part(PiciSinkArgs g) {
         flushed += fill;
         fill = 0;
     };
+    // One launch, the partition's values staged together: the four tiles'
+    // counts first, published before the merges, so that the partitions after
+    // this one wait less; the merged output always fits the buffer then.
+    bool early = false;
+    if constexpr (Single) {
+        if (whole) {
+            early = true;
+            uint64_t wo_k[K];
+            uint32_t cpo_k[K], base_k[K];
+#pragma unroll
+            for (int k = 0; k < K; k++) {
+                wo_k[k] = 0;
+                cpo_k[k] = 0;
+                base_k[k] = fill;
+                if ((uint32_t)k < ntile) {
+                    const PiciCols& A = ca[k];
+                    const PiciCols& B = cb[k];
+                    const uint32_t ia = (A.base - a_lo) + A.colpref, ib = la + (B.base - b_lo) + B.colpref;
+                    const uint64_t wo = (A.w | B.w) & ~pp_cancel<E>(A.w, B.w, in, ia, ib, zero_all, true);
+                    Bo[(t0 + k) * 64 + l] = wo;
+                    const uint32_t c = (uint32_t)__popcll(wo);
+                    const uint32_t cpo = wave_excl_scan(c);
+                    if (l == (uint32_t)k) tile_rel = fill;
+                    fill += lane_bcast(cpo + c, 63);
+                    wo_k[k] = wo;
+                    cpo_k[k] = cpo;
+                }
+            }
+            if (l == 0) publish(g.flags, p, epoch30, kFlagAggregate, fill);
+#pragma unroll
+            for (int k = 0; k < K; k++) {
+                if ((uint32_t)k < ntile) {
+                    const PiciCols& A = ca[k];
+                    const PiciCols& B = cb[k];
+                    pp_merge<E>(A.w, B.w, wo_k[k], in, (A.base - a_lo) + A.colpref, la + (B.base - b_lo) + B.colpref,
+                                ob, base_k[k] + cpo_k[k], true);
+                }
+            }
+        }
+    }
 #pragma unroll
     for (int k = 0; k < K; k++) {
-        if ((uint32_t)k >= ntile) break;
+        if (early || (uint32_t)k >= ntile) break;
         const PiciCols& A = ca[k];
         const PiciCols& B = cb[k];
         const uint64_t t = t0 + k;
@@ -1833,7 +1873,7 @@ __global__ void __launch_bounds__(kBlockThreads) k_pp_part(PiciSinkArgs g) {
         return;
     }
     const uint32_t agg = flushed + fill;
-    if (l == 0) publish(g.flags, p, epoch30, kFlagAggregate, agg);
+    if (!early && l == 0) publish(g.flags, p, epoch30, kFlagAggregate, agg);
     bool ok;
     const uint32_t prefix = chunk_lookback(g.flags, g.nparts, p, agg, epoch30, g.ctrl, ok);
     if (!ok) return;                  // a predecessor never published: write nothing more
