@@ -148,8 +148,7 @@ spccl_status_t spccl_workspace_init(void* ws, uint64_t ws_bytes, void* stream);
  * global scan); larger outputs take the count and place passes.  Within the
  * bound the library's own limits apply: fp32 outputs of dense sources at
  * every size, bf16 ones up to 2048 partitions, Pici (+) Pici -> Pici up to
- * 1024 partitions and from 2048 to 4096 (a kernel with one partition per
- * wave).  Default UINT32_MAX (the library's limits alone); 0 keeps every such
+ * 1024 partitions and from 2048 on (a kernel with one partition per wave).  Default UINT32_MAX (the library's limits alone); 0 keeps every such
  * call on two passes.  The ring steps of the spccl_vr_* collectives follow the
  * same limits per rank's message; COO outputs always take two passes, and a
  * workspace of only spccl_workspace_min_bytes always one.  Process-wide (every device and

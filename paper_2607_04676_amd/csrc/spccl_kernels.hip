@@ -3196,15 +3196,14 @@ inline uint32_t stream_grid(uint64_t work_items, uint32_t per_block, uint32_t ca
 //    (k_pp_tile<E, true> + k_place, four waves per partition: 12.7 against
 //    20.1 us at 2^20 and 0.99 against one partition per wave), from 2048
 //    partitions one partition per wave (k_pp_part: 28.2 against 36.3 us at
-//    2^26), which finds its own offsets up to 4096 partitions -- every wave
-//    of the launch is then resident, so a waiting wave keeps none from
-//    starting (26.6 against 28.2 / 66.2 against 75.2 us at 2^26; at 2^27 bf16,
-//    two rounds of waves, 45.9 against 41.5) -- and takes k_place beyond.
+//    2^26), which finds its own offsets (with its count published before its
+//    merges: 21.1 / 65.6 us at 2^26 against 28.2 / 75.2 with k_place; 38.0 /
+//    126.6 against 40.9 / 144.5 at 2^27, 8192 partitions, two rounds of
+//    waves).
 // Without value slots (a minimal workspace) every output takes one launch.
 constexpr uint32_t kOneLaunchMaxPartsBF16 = 2048;
 constexpr uint32_t kPPTileOneMaxParts = 1024;
 constexpr uint32_t kPPTileMaxParts = 2048;
-constexpr uint32_t kPPSingleMaxParts = 4096;
 
 }  // namespace
 
@@ -3231,7 +3230,7 @@ spccl_status_t launch_to_pici(int sa, int sb, const PiciSinkArgs& g, hipStream_t
                 hipLaunchKernelGGL((k_pp_tile<E, true>), grid, block, 0, st, g);
             } else {
                 dim3 wgrid((g.nparts + kWavesPerBlock - 1) / kWavesPerBlock);
-                if (one_launch(kPPSingleMaxParts)) {
+                if (one_launch(0xFFFFFFFFu)) {
                     hipLaunchKernelGGL((k_pp_part<E, true>), wgrid, block, 0, st, g);
                     return launch_status();
                 }

@@ -6,8 +6,8 @@ density (small and large parked values per partition), for compression,
 dense (+) Pici -> Pici and Pici (+) Pici -> Pici, all on one workspace sized
 for the largest message (so each call meets the previous call's chunk sums),
 against the oracle byte for byte.  Also either side of the sizes where
-Pici (+) Pici's first pass changes its shape (2048 partitions) and up to
-which it finds its offsets itself in one launch (4096).  The library writes
+Pici (+) Pici's first pass changes its shape (2048 partitions) and where its
+waves stop fitting the device at once (4096).  The library writes
 many outputs in one launch by default; these tests bound that to zero
 partitions so the two-pass paths run at every size, and a second test checks
 the defaults on both sides of their limits on the same workspace."""
@@ -37,8 +37,9 @@ def S():
 # (partitions, elements short of or past a whole number of partitions)
 SIZES = [(CHUNK, -123), (CHUNK + 1, -(PART - 1)), (2 * CHUNK + 1, -(PART - 4097)), (4 * CHUNK + 3, -3000)]
 # either side of the size where Pici (+) Pici's first pass changes from one
-# tile per wave to one partition per wave (2048 partitions), and of the size
-# up to which that pass finds its own offsets in a single launch (4096)
+# tile per wave to one partition per wave (2048 partitions), and of 4096
+# partitions (every wave of a one-partition-per-wave launch resident at once
+# up to there)
 EDGE = [(2047, -7), (2048, -(PART - 1)), (4096, -3), (4097, -(PART - 1))]
 
 
@@ -68,7 +69,7 @@ def test_place_across_chunks(S, ws_big, two_pass_always, dtype, size, permille):
 
 
 # the library's own one-launch limits on the large workspace: bf16 dense-source
-# outputs up to 2048 partitions, Pici (+) Pici up to 1024 and from 2048 to 4096
+# outputs up to 2048 partitions, Pici (+) Pici up to 1024 and from 2048 on
 # partitions (fp32 dense-source outputs take one launch at every size)
 DEFAULT = [(W.F32, (1, -(PART - 100))), (W.F32, (1024, -5)), (W.F32, (1025, -(PART - 1))),
            (W.BF16, (2048, -3)), (W.BF16, (2049, -(PART - 1)))]
