@@ -225,3 +225,16 @@ def test_collectives_in_place_layouts_pass_the_host_checks(S):
     assert _vr_call(S, "ag", ag_in_place, recv, P, n, scratch, sb) == 6
     shifted = [recv[r] + ((r + 1) % P) * n * s for r in range(P)]
     assert _vr_call(S, "ag", shifted, recv, P, n, scratch, sb) == 1
+
+
+def test_single_pass_limit_is_a_process_wide_bound(S):
+    """spccl_set_single_pass_limit returns the previous bound; the default is
+    UINT32_MAX (the library's own one-launch limits); host-only, no launch."""
+    first = S.spccl_set_single_pass_limit(0)
+    try:
+        assert first == 0xFFFFFFFF
+        assert S.spccl_set_single_pass_limit(1024) == 0
+        assert S.spccl_set_single_pass_limit(1024) == 1024
+    finally:
+        S.spccl_set_single_pass_limit(first)
+    assert S.spccl_set_single_pass_limit(first) == first
